@@ -1,0 +1,173 @@
+"""Benchmark: one training step of the CosmoFlow conv hot path on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+
+A step is the whole hot path over one batch of synthetic cubes: forward
+(conv, bias + leaky ReLU, 2^3 average pool per layer) and backward (pool
+backward, leaky-ReLU backward + bias grad, weight grad, data grad) through
+the C ABI.  Inputs, weights and the upstream gradient are resident in HBM
+before timing starts.  Prints ONE JSON line.
+
+value = algorithmic conv FLOPs per step (fwd + wgrad + dgrad, padded taps
+included, layer-1 dgrad skipped) x steps / wall time of the timed steps.
+The roofline entry is for the op that takes the most time per step, timed
+with events on the launch stream over the same timed steps.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK = {"bf16": 2516.6, "f32": 157.3}  # dense MFMA TFLOP/s, MI355X
+HBM_PEAK_GBS = 8000.0
+METRIC = "fwd+bwd 3D-conv TFLOP/s & samples/s, 128^3 CosmoFlow stack; % MFMA peak"
+
+
+def describe(name, wl):
+    return (f"CosmoFlow conv stack, {wl['size']}^3 x {wl['c0']} input, batch {wl['batch']}, {wl['dtype']}, "
+            f"{len(wl['layers'])} conv layers (3 pooled), TF-SAME padding, fwd+bwd")
+
+
+def cpu_baseline(name, seconds_hint=True):
+    """Time the oracle (fp64 CPU) on one sample of the workload: forward and
+    backward of every layer (layer-1 dgrad skipped, like the GPU step)."""
+    import numpy as np
+
+    import oracle
+    from paper_1808_04728_amd import inputs
+
+    wl = dict(inputs.WORKLOADS[name])
+    x = inputs.make_input(name)[:1]
+    ws, bs = inputs.make_weights(name)
+    layers = [dict(k=L["k"], stride=L["stride"], pool=L["pool"]) for L in wl["layers"]]
+    oracle.build(force=False)
+    t0 = time.perf_counter()
+    acts = oracle.stack_forward(x, layers, ws, bs, inputs.ALPHA)
+    dout = inputs.normal(acts[-1]["out"].shape, 30000 + wl["cfg"])
+    oracle.stack_backward(acts, layers, ws, dout, inputs.ALPHA, skip_first_dgrad=True)
+    dt = time.perf_counter() - t0
+    flops = 0
+    size = wl["size"]
+    for i, L in enumerate(wl["layers"]):
+        out = -(-size // L["stride"])
+        macs = out ** 3 * L["cout"] * L["k"] ** 3 * L["cin"]
+        flops += 2 * macs * (2 if i == 0 else 3)
+        size = out // 2 if L["pool"] else out
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or os.cpu_count()
+    return dict(value=flops / dt / 1e12, unit="TFLOP/s", cores=threads, kind="oracle",
+                sample=f"1 of {wl['batch']} samples (batch 1), full {wl['size']}^3 stack fwd+bwd in fp64, "
+                       f"{dt:.1f} s, {1.0 / dt:.4f} samples/s")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="stack_128c_b8_bf16")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--op-breakdown", action="store_true", help="print per-op times to stderr")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (data-parallel sharding is "
+              "described in DESIGN.md, not implemented); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_1808_04728_amd import inputs
+    from paper_1808_04728_amd.stack import ConvStack
+
+    name = args.workload
+    wl = inputs.WORKLOADS[name]
+    torch.cuda.set_device(0)
+    st = ConvStack(wl["layers"], wl["size"], wl["batch"], wl["dtype"], inputs.ALPHA, "cuda:0")
+    ws, bs = inputs.make_weights(name)
+    st.set_params(ws, bs)
+    st.set_input(inputs.make_input(name))
+    dout = torch.as_tensor(inputs.normal((wl["batch"],) + st.out_dhw + (wl["layers"][-1]["cout"],),
+                                         30000 + wl["cfg"]), device="cuda:0").to(st.tdt)
+
+    def step():
+        st.forward()
+        st.backward(dout)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # per-op times (events around every call) to find the dominant op
+    st.timer = {}
+    for _ in range(3):
+        step()
+    torch.cuda.synchronize()
+    op_ms = {k: float(np.mean([a.elapsed_time(b) for a, b in v])) for k, v in st.timer.items()}
+    dominant = max(op_ms, key=op_ms.get)
+    if args.op_breakdown:
+        for k, v in sorted(op_ms.items(), key=lambda kv: -kv[1]):
+            fl = st.op_flops(k)
+            extra = f"{fl / v / 1e9:8.1f} TFLOP/s" if fl else f"{st.op_bytes(k) / v / 1e6:8.1f} GB/s"
+            print(f"  {k:24s} {v * 1e3:9.1f} us  {extra}", file=sys.stderr)
+
+    # timed region: events bracket only the dominant op
+    st.timer = {}
+    st.timed_ops = {dominant}
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    dom_ms = float(np.mean([a.elapsed_time(b) for a, b in st.timer[dominant]]))
+    st.timer = None
+
+    ms = wall * 1e3 / args.steps
+    flops = st.conv_flops()
+    tflops = flops / (ms * 1e-3) / 1e12
+    peak = PEAK[wl["dtype"]]
+    dom_flops = st.op_flops(dominant)
+    if dom_flops:
+        ach = dom_flops / (dom_ms * 1e-3) / 1e12
+        roof = dict(bound="mfma", achieved=round(ach, 2), peak=peak, unit="TFLOP/s", frac=round(ach / peak, 4),
+                    traffic=None, kernel=dominant, launch_ms=round(dom_ms, 4),
+                    per_launch=f"{dom_flops / 1e9:.2f} GFLOP")
+    else:
+        gbs = st.op_bytes(dominant) / (dom_ms * 1e-3) / 1e9
+        roof = dict(bound="hbm", achieved=round(gbs, 1), peak=HBM_PEAK_GBS, unit="GB/s",
+                    frac=round(gbs / HBM_PEAK_GBS, 4), traffic=None, kernel=dominant, launch_ms=round(dom_ms, 4),
+                    per_launch=f"{st.op_bytes(dominant) / 2**20:.1f} MiB")
+    res = {
+        "metric": METRIC,
+        "value": round(tflops, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl["dtype"],
+        "data": "synthetic",
+        "config": {"workload": describe(name, wl), "name": name, "edge": wl["size"], "batch": wl["batch"],
+                   "input_channels": wl["c0"], "conv_gflop_per_step": round(flops / 1e9, 3)},
+        "samples_per_s": round(wl["batch"] / (ms * 1e-3), 2),
+        "mfma_peak_frac": round(tflops / peak, 4),
+        "roofline": roof,
+        "op_ms": {k: round(v, 4) for k, v in sorted(op_ms.items(), key=lambda kv: -kv[1])},
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(name)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

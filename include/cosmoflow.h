@@ -1,0 +1,157 @@
+/*
+ * cosmoflow.h -- C ABI of the MI355X (gfx950) CosmoFlow convolution hot path.
+ *
+ * The operations are those of the CosmoFlow network (arXiv:1808.04728):
+ * 3D convolution forward, backward-data and backward-weights (Section III-C,
+ * Algorithm 1 and the paragraphs after it), bias + leaky ReLU (Section III-A:
+ * every convolution layer uses leaky ReLU), and 3D average pooling with
+ * stride (2,2,2) (Section III-A; Section III-C treats it as a per-channel
+ * convolution with constant weights 1/KS^3).
+ *
+ * Conventions shared by every entry point
+ *   - Activations are NDHWC (channels innermost), weights are DHWIO
+ *     W[kd][kh][kw][c_in][c_out]; all tensors are dense and contiguous.
+ *   - Convolution is a cross-correlation: output o reads input o*stride +
+ *     tap - pad_before (no kernel flip).  CF_PAD_SAME_TF uses TensorFlow's
+ *     SAME rule (out = ceil(in/stride), the odd padding element after the
+ *     data); CF_PAD_VALID has no padding (out = floor((in-k)/stride)+1).
+ *   - Every pointer is a DEVICE pointer owned by the caller, except where
+ *     stated.  The library never allocates or frees device memory, never
+ *     synchronises, and launches on the caller's `stream` (a hipStream_t,
+ *     may be NULL for the default stream).  Calls are asynchronous and
+ *     stream-ordered.
+ *   - CF_BF16 tensors hold IEEE bfloat16; every bf16 store rounds to nearest
+ *     even.  Accumulation is fp32 in every dtype.  bias, db and dW are
+ *     always fp32.
+ *   - Errors: arguments are validated on the host before any launch.  On a
+ *     validation error nothing is launched, outputs are untouched, the code
+ *     is returned and cf_last_error() describes it.  A batch of 0 (or any
+ *     empty extent) is a no-op returning CF_OK.  A failed launch returns
+ *     CF_ERR_LAUNCH.  Input and output buffers of a call must not overlap
+ *     unless stated (CF_ERR_ALIAS).  Pointers must be 16-byte aligned
+ *     (CF_ERR_ALIGNMENT).
+ *   - Results are deterministic: no floating-point atomics; every reduction
+ *     has a fixed order that depends only on the shapes.
+ */
+#ifndef COSMOFLOW_H
+#define COSMOFLOW_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum cf_status {
+  CF_OK = 0,
+  CF_ERR_INVALID_ARG = 1, /* null pointer, non-positive size, kernel larger than input ... */
+  CF_ERR_UNSUPPORTED = 2, /* valid but not implemented (e.g. pooling with k != s) */
+  CF_ERR_ALIGNMENT = 3,   /* a pointer is not 16-byte aligned */
+  CF_ERR_ALIAS = 4,       /* input and output buffers overlap where that is forbidden */
+  CF_ERR_WORKSPACE = 5,   /* workspace missing or smaller than the size query returns */
+  CF_ERR_LAUNCH = 6       /* the HIP runtime reported an error */
+} cf_status;
+
+typedef enum cf_dtype { CF_F32 = 0, CF_BF16 = 1 } cf_dtype;
+
+typedef enum cf_pad { CF_PAD_SAME_TF = 0, CF_PAD_VALID = 1 } cf_pad;
+
+/* Geometry of one 3D convolution layer.  n, d, h, w: batch and input
+ * extent; c_in, c_out: channels; kd, kh, kw: kernel; sd, sh, sw: strides;
+ * pad: a cf_pad; dtype: a cf_dtype (type of x, W, z, dz, dx). */
+typedef struct cf_conv3d_desc {
+  int32_t n, d, h, w;
+  int32_t c_in, c_out;
+  int32_t kd, kh, kw;
+  int32_t sd, sh, sw;
+  int32_t pad;
+  int32_t dtype;
+} cf_conv3d_desc;
+
+/* Library version string (static storage). */
+const char *cf_version(void);
+
+/* Message of the last error returned on the calling thread ("" if none). */
+const char *cf_last_error(void);
+
+/* Host-only.  Output extent out_dhw[3] of the convolution described by desc
+ * (SAME: ceil(in/s); VALID: floor((in-k)/s)+1). */
+cf_status cf_conv3d_out_shape(const cf_conv3d_desc *desc, int32_t out_dhw[3]);
+
+/* Forward convolution, Section III-C / Algorithm 1:
+ *   z[n,o,co] = sum_{t,ci} x[n, o*s + t - pad_before, ci] * W[t,ci,co]
+ * x: [n,d,h,w,c_in], W: [kd,kh,kw,c_in,c_out], z: [n,od,oh,ow,c_out], all in
+ * desc->dtype.  z must not overlap x or W. */
+cf_status cf_conv3d_fwd(const cf_conv3d_desc *desc, const void *x, const void *w,
+                        void *z, void *stream);
+
+/* Backward data, Section III-C (the operator that propagates the output
+ * difference signal to the input): the adjoint of cf_conv3d_fwd in x,
+ *   dx[n,i,ci] = sum over (o,t) with o*s + t - pad_before = i of
+ *                sum_co dz[n,o,co] * W[t,ci,co].
+ * dz: [n,od,oh,ow,c_out], W as above, dx: [n,d,h,w,c_in]; every element of
+ * dx is written (zero where no output reads it).  dx must not overlap dz/W. */
+cf_status cf_conv3d_bwd_data(const cf_conv3d_desc *desc, const void *dz, const void *w,
+                             void *dx, void *stream);
+
+/* Bytes of device workspace cf_conv3d_bwd_weight needs for desc (the
+ * per-slice fp32 partial sums of the split reduction); 0 on invalid desc. */
+size_t cf_conv3d_bwd_weight_workspace_size(const cf_conv3d_desc *desc);
+
+/* Backward weights, Section III-C (a forward-like convolution with a large
+ * reduction and a small output; voxel slices accumulate privately and are
+ * then combined): the adjoint of cf_conv3d_fwd in W,
+ *   dW[t,ci,co] = sum_{n,o} x[n, o*s + t - pad_before, ci] * dz[n,o,co].
+ * x and dz in desc->dtype, dW fp32 [kd,kh,kw,c_in,c_out] (overwritten, not
+ * accumulated).  ws: caller-owned device workspace of at least
+ * cf_conv3d_bwd_weight_workspace_size(desc) bytes (may be NULL if that is 0).
+ * The reduction over voxels is split into fixed slices whose partials are
+ * summed in slice order, so the result is bitwise reproducible. */
+cf_status cf_conv3d_bwd_weight(const cf_conv3d_desc *desc, const void *x, const void *dz,
+                               float *dw, void *ws, size_t ws_bytes, void *stream);
+
+/* Bias + leaky ReLU forward (Section III-A):
+ *   y[v,c] = u > 0 ? u : alpha*u,  u = z[v,c] + bias[c]   (u in fp32)
+ * nvox = number of voxels (n*d*h*w), c = channels; z, y in dtype; bias fp32
+ * [c].  y may alias z exactly (in place); partial overlap is CF_ERR_ALIAS.
+ * alpha must be finite. */
+cf_status cf_bias_lrelu_fwd(int64_t nvox, int32_t c, int32_t dtype, const void *z,
+                            const float *bias, float alpha, void *y, void *stream);
+
+/* Bytes of workspace cf_bias_lrelu_bwd needs (per-block bias partials). */
+size_t cf_bias_lrelu_bwd_workspace_size(int64_t nvox, int32_t c);
+
+/* Bias + leaky ReLU backward:
+ *   dz[v,c] = dy[v,c] * (y[v,c] > 0 ? 1 : alpha),   db[c] = sum_v dz[v,c].
+ * The slope is read from the SAVED OUTPUT y (for alpha > 0, y > 0 exactly
+ * when the pre-activation is > 0; at a pre-activation of exactly 0 the slope
+ * is alpha).  dy, y, dz in dtype; db fp32 [c] (overwritten); the sum runs in
+ * fp32 over the unrounded products in a fixed order.  dz may alias dy
+ * exactly.  db may be NULL (no bias gradient; ws then unused). */
+cf_status cf_bias_lrelu_bwd(int64_t nvox, int32_t c, int32_t dtype, const void *dy,
+                            const void *y, float alpha, void *dz, float *db, void *ws,
+                            size_t ws_bytes, void *stream);
+
+/* Average pooling forward (Section III-C: per-channel convolution with
+ * constant weights 1/k^3; Section III-A: stride (2,2,2)):
+ *   p[n,o,c] = (1/k^3) * sum_{a in [0,k)^3} y[n, o*s + a, c]
+ * y: [n,d,h,w,c], p: [n,(d-k)/s+1,(h-k)/s+1,(w-k)/s+1,c] (floor), dtype.
+ * Only non-overlapping windows (k == s) are implemented; other pairs return
+ * CF_ERR_UNSUPPORTED.  The sum is fp32, rounded once on store. */
+cf_status cf_avgpool3d_fwd(int32_t n, int32_t d, int32_t h, int32_t w, int32_t c,
+                           int32_t k, int32_t s, int32_t dtype, const void *y, void *p,
+                           void *stream);
+
+/* Average pooling backward: the adjoint of cf_avgpool3d_fwd,
+ *   dy[n,i,c] = dp[n, i/s, c] / k^3 where i is covered by a window, else 0.
+ * Dimensions as for the forward call (d,h,w = the forward INPUT extent). */
+cf_status cf_avgpool3d_bwd(int32_t n, int32_t d, int32_t h, int32_t w, int32_t c,
+                           int32_t k, int32_t s, int32_t dtype, const void *dp, void *dy,
+                           void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* COSMOFLOW_H */

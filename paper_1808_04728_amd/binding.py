@@ -1,0 +1,178 @@
+"""ctypes binding of the C ABI in include/cosmoflow.h.
+
+Argument marshalling only: every function here has the name of its C entry
+point, turns torch tensors into device pointers and the current torch stream
+into a hipStream_t, calls the library and raises ``CfError`` on a non-zero
+status.  All computation happens in the HIP kernels of libcosmoflow_hip.so;
+if the library is missing this module raises instead of computing anything
+another way.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libcosmoflow_hip.so")
+
+CF_OK, CF_ERR_INVALID_ARG, CF_ERR_UNSUPPORTED, CF_ERR_ALIGNMENT, CF_ERR_ALIAS, \
+    CF_ERR_WORKSPACE, CF_ERR_LAUNCH = range(7)
+CF_F32, CF_BF16 = 0, 1
+CF_PAD_SAME_TF, CF_PAD_VALID = 0, 1
+
+STATUS_NAMES = {0: "CF_OK", 1: "CF_ERR_INVALID_ARG", 2: "CF_ERR_UNSUPPORTED", 3: "CF_ERR_ALIGNMENT",
+                4: "CF_ERR_ALIAS", 5: "CF_ERR_WORKSPACE", 6: "CF_ERR_LAUNCH"}
+
+# every symbol the header declares
+EXPORTS = [
+    "cf_version", "cf_last_error", "cf_conv3d_out_shape", "cf_conv3d_fwd", "cf_conv3d_bwd_data",
+    "cf_conv3d_bwd_weight_workspace_size", "cf_conv3d_bwd_weight", "cf_bias_lrelu_fwd",
+    "cf_bias_lrelu_bwd_workspace_size", "cf_bias_lrelu_bwd", "cf_avgpool3d_fwd", "cf_avgpool3d_bwd",
+]
+
+
+class CfError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{STATUS_NAMES.get(status, status)}: {msg}")
+        self.status = status
+
+
+class cf_conv3d_desc(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("n", "d", "h", "w", "c_in", "c_out", "kd", "kh", "kw", "sd", "sh", "sw", "pad", "dtype")]
+
+
+_lib = None
+
+
+def lib():
+    """Load libcosmoflow_hip.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_1808_04728_amd.build` "
+                          "(there is no fallback implementation)")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i32, i64, f32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_size_t
+    D = ctypes.POINTER(cf_conv3d_desc)
+    sig = {
+        "cf_version": ([], ctypes.c_char_p),
+        "cf_last_error": ([], ctypes.c_char_p),
+        "cf_conv3d_out_shape": ([D, ctypes.POINTER(i32)], ctypes.c_int),
+        "cf_conv3d_fwd": ([D, vp, vp, vp, vp], ctypes.c_int),
+        "cf_conv3d_bwd_data": ([D, vp, vp, vp, vp], ctypes.c_int),
+        "cf_conv3d_bwd_weight_workspace_size": ([D], sz),
+        "cf_conv3d_bwd_weight": ([D, vp, vp, vp, vp, sz, vp], ctypes.c_int),
+        "cf_bias_lrelu_fwd": ([i64, i32, i32, vp, vp, f32, vp, vp], ctypes.c_int),
+        "cf_bias_lrelu_bwd_workspace_size": ([i64, i32], sz),
+        "cf_bias_lrelu_bwd": ([i64, i32, i32, vp, vp, f32, vp, vp, vp, sz, vp], ctypes.c_int),
+        "cf_avgpool3d_fwd": ([i32] * 8 + [vp, vp, vp], ctypes.c_int),
+        "cf_avgpool3d_bwd": ([i32] * 8 + [vp, vp, vp], ctypes.c_int),
+    }
+    for name, (args, res) in sig.items():
+        f = getattr(L, name)
+        f.argtypes = args
+        f.restype = res
+    _lib = L
+    return L
+
+
+def _check(status: int):
+    if status != CF_OK:
+        raise CfError(status, lib().cf_last_error().decode())
+
+
+def _ptr(t):
+    """Device pointer of a tensor, or an int/None passed through."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def dtype_code(dt) -> int:
+    if dt in (torch.float32, "f32", CF_F32):
+        return CF_F32
+    if dt in (torch.bfloat16, "bf16", CF_BF16):
+        return CF_BF16
+    raise ValueError(f"unsupported dtype {dt}")
+
+
+def make_desc(n, dhw, c_in, c_out, k, stride=1, pad="same", dtype=CF_F32) -> cf_conv3d_desc:
+    k3 = tuple(k) if isinstance(k, (tuple, list)) else (k,) * 3
+    s3 = tuple(stride) if isinstance(stride, (tuple, list)) else (stride,) * 3
+    return cf_conv3d_desc(n, *dhw, c_in, c_out, *k3, *s3,
+                          CF_PAD_SAME_TF if pad == "same" else CF_PAD_VALID, dtype_code(dtype))
+
+
+# ---------------------------------------------------------------------------
+# entry points (same names as the C ABI)
+# ---------------------------------------------------------------------------
+
+def cf_version() -> str:
+    return lib().cf_version().decode()
+
+
+def cf_last_error() -> str:
+    return lib().cf_last_error().decode()
+
+
+def cf_conv3d_out_shape(desc):
+    out = (ctypes.c_int32 * 3)()
+    _check(lib().cf_conv3d_out_shape(ctypes.byref(desc), out))
+    return tuple(out)
+
+
+def cf_conv3d_fwd(desc, x, w, z, stream=None):
+    _check(lib().cf_conv3d_fwd(ctypes.byref(desc), _ptr(x), _ptr(w), _ptr(z), _stream(stream)))
+
+
+def cf_conv3d_bwd_data(desc, dz, w, dx, stream=None):
+    _check(lib().cf_conv3d_bwd_data(ctypes.byref(desc), _ptr(dz), _ptr(w), _ptr(dx), _stream(stream)))
+
+
+def cf_conv3d_bwd_weight_workspace_size(desc) -> int:
+    return int(lib().cf_conv3d_bwd_weight_workspace_size(ctypes.byref(desc)))
+
+
+def cf_conv3d_bwd_weight(desc, x, dz, dw, ws, ws_bytes=None, stream=None):
+    if ws_bytes is None:
+        ws_bytes = 0 if ws is None or isinstance(ws, int) else ws.numel() * ws.element_size()
+    _check(lib().cf_conv3d_bwd_weight(ctypes.byref(desc), _ptr(x), _ptr(dz), _ptr(dw), _ptr(ws),
+                                      ws_bytes, _stream(stream)))
+
+
+def cf_bias_lrelu_fwd(nvox, c, dtype, z, bias, alpha, y, stream=None):
+    _check(lib().cf_bias_lrelu_fwd(nvox, c, dtype_code(dtype), _ptr(z), _ptr(bias), alpha, _ptr(y),
+                                   _stream(stream)))
+
+
+def cf_bias_lrelu_bwd_workspace_size(nvox, c) -> int:
+    return int(lib().cf_bias_lrelu_bwd_workspace_size(nvox, c))
+
+
+def cf_bias_lrelu_bwd(nvox, c, dtype, dy, y, alpha, dz, db, ws, ws_bytes=None, stream=None):
+    if ws_bytes is None:
+        ws_bytes = 0 if ws is None or isinstance(ws, int) else ws.numel() * ws.element_size()
+    _check(lib().cf_bias_lrelu_bwd(nvox, c, dtype_code(dtype), _ptr(dy), _ptr(y), alpha, _ptr(dz), _ptr(db),
+                                   _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def cf_avgpool3d_fwd(n, d, h, w, c, k, s, dtype, y, p, stream=None):
+    _check(lib().cf_avgpool3d_fwd(n, d, h, w, c, k, s, dtype_code(dtype), _ptr(y), _ptr(p), _stream(stream)))
+
+
+def cf_avgpool3d_bwd(n, d, h, w, c, k, s, dtype, dp, dy, stream=None):
+    _check(lib().cf_avgpool3d_bwd(n, d, h, w, c, k, s, dtype_code(dtype), _ptr(dp), _ptr(dy), _stream(stream)))

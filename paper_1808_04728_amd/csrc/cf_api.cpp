@@ -1,0 +1,310 @@
+// cf_api.cpp -- the C ABI (include/cosmoflow.h): host-side argument
+// validation, geometry, and dispatch to the gfx950 kernel launchers.
+//
+// Every check runs on the host before anything is launched, so a rejected
+// call touches neither the device nor the outputs.
+
+#include "../../include/cosmoflow.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <string>
+
+#include "cf_common.h"
+#include "cf_kernels.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+cf_status fail(cf_status code, const std::string &msg) {
+  g_last_error = msg;
+  return code;
+}
+
+cf_status ok() {
+  g_last_error.clear();
+  return CF_OK;
+}
+
+bool debug_sync() {
+  static int v = [] {
+    const char *e = std::getenv("CF_DEBUG_SYNC");
+    return (e && e[0] && e[0] != '0') ? 1 : 0;
+  }();
+  return v != 0;
+}
+
+cf_status finish(hipError_t e, hipStream_t st, const char *what) {
+  if (e == hipSuccess && debug_sync()) e = hipStreamSynchronize(st);
+  if (e != hipSuccess)
+    return fail(CF_ERR_LAUNCH, std::string(what) + ": " + hipGetErrorString(e));
+  return ok();
+}
+
+size_t elem_size(int dtype) { return dtype == CF_BF16 ? 2 : 4; }
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+bool overlap(const void *a, size_t na, const void *b, size_t nb) {
+  if (!a || !b || na == 0 || nb == 0) return false;
+  uintptr_t a0 = (uintptr_t)a, b0 = (uintptr_t)b;
+  return a0 < b0 + nb && b0 < a0 + na;
+}
+
+constexpr long long kMaxRows = (1LL << 31) - 1;
+
+// Validate a convolution descriptor and resolve its geometry.
+cf_status resolve(const cf_conv3d_desc *d, cf::ConvShape *s) {
+  if (!d) return fail(CF_ERR_INVALID_ARG, "desc is NULL");
+  if (d->n < 0) return fail(CF_ERR_INVALID_ARG, "batch n must be >= 0");
+  if (d->d <= 0 || d->h <= 0 || d->w <= 0)
+    return fail(CF_ERR_INVALID_ARG, "spatial extents d, h, w must be > 0");
+  if (d->c_in <= 0 || d->c_out <= 0) return fail(CF_ERR_INVALID_ARG, "channels must be > 0");
+  if (d->kd <= 0 || d->kh <= 0 || d->kw <= 0) return fail(CF_ERR_INVALID_ARG, "kernel extents must be > 0");
+  if (d->sd <= 0 || d->sh <= 0 || d->sw <= 0) return fail(CF_ERR_INVALID_ARG, "strides must be > 0");
+  if (d->pad != CF_PAD_SAME_TF && d->pad != CF_PAD_VALID) return fail(CF_ERR_INVALID_ARG, "unknown pad mode");
+  if (d->dtype != CF_F32 && d->dtype != CF_BF16) return fail(CF_ERR_INVALID_ARG, "unknown dtype");
+  const int in[3] = {d->d, d->h, d->w}, k[3] = {d->kd, d->kh, d->kw}, st[3] = {d->sd, d->sh, d->sw};
+  int out[3], pb[3];
+  for (int a = 0; a < 3; ++a) {
+    if (d->pad == CF_PAD_SAME_TF) {
+      out[a] = (in[a] + st[a] - 1) / st[a];
+      long long tot = (long long)(out[a] - 1) * st[a] + k[a] - in[a];
+      if (tot < 0) tot = 0;
+      pb[a] = (int)(tot / 2);
+    } else {
+      if (k[a] > in[a]) return fail(CF_ERR_INVALID_ARG, "VALID convolution: kernel larger than input");
+      out[a] = (in[a] - k[a]) / st[a] + 1;
+      pb[a] = 0;
+    }
+  }
+  const long long taps = (long long)k[0] * k[1] * k[2];
+  if (taps * d->c_in >= kMaxRows || taps * d->c_out >= kMaxRows)
+    return fail(CF_ERR_INVALID_ARG, "kernel volume x channels overflows 32 bits");
+  const long long vin = (long long)d->n * in[0] * in[1] * in[2];
+  const long long vout = (long long)d->n * out[0] * out[1] * out[2];
+  if (vin >= kMaxRows || vout >= kMaxRows) return fail(CF_ERR_INVALID_ARG, "too many voxels (>= 2^31)");
+  s->n = d->n; s->d = in[0]; s->h = in[1]; s->w = in[2];
+  s->ci = d->c_in; s->co = d->c_out;
+  s->kd = k[0]; s->kh = k[1]; s->kw = k[2];
+  s->sd = st[0]; s->sh = st[1]; s->sw = st[2];
+  s->pd = pb[0]; s->ph = pb[1]; s->pw = pb[2];
+  s->od = out[0]; s->oh = out[1]; s->ow = out[2];
+  s->dtype = d->dtype == CF_BF16 ? cf::DT_BF16 : cf::DT_F32;
+  return CF_OK;
+}
+
+struct Sizes {
+  size_t x, w, z;
+};
+
+Sizes conv_bytes(const cf::ConvShape &s) {
+  const size_t es = s.dtype == cf::DT_BF16 ? 2 : 4;
+  Sizes r;
+  r.x = (size_t)s.n * s.d * s.h * s.w * s.ci * es;
+  r.w = (size_t)s.kd * s.kh * s.kw * s.ci * s.co * es;
+  r.z = (size_t)s.n * s.od * s.oh * s.ow * s.co * es;
+  return r;
+}
+
+cf_status check_ptrs(std::initializer_list<const void *> ptrs) {
+  for (const void *p : ptrs) {
+    if (!p) return fail(CF_ERR_INVALID_ARG, "NULL tensor pointer");
+    if (!aligned16(p)) return fail(CF_ERR_ALIGNMENT, "tensor pointer not 16-byte aligned");
+  }
+  return CF_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *cf_version(void) { return "cosmoflow-gfx950 0.1.0"; }
+
+const char *cf_last_error(void) { return g_last_error.c_str(); }
+
+cf_status cf_conv3d_out_shape(const cf_conv3d_desc *desc, int32_t out_dhw[3]) {
+  cf::ConvShape s;
+  cf_status r = resolve(desc, &s);
+  if (r != CF_OK) return r;
+  if (!out_dhw) return fail(CF_ERR_INVALID_ARG, "out_dhw is NULL");
+  out_dhw[0] = s.od;
+  out_dhw[1] = s.oh;
+  out_dhw[2] = s.ow;
+  return ok();
+}
+
+cf_status cf_conv3d_fwd(const cf_conv3d_desc *desc, const void *x, const void *w, void *z,
+                        void *stream) {
+  cf::ConvShape s;
+  cf_status r = resolve(desc, &s);
+  if (r != CF_OK) return r;
+  if (s.n == 0) return ok();
+  if ((r = check_ptrs({x, w, z})) != CF_OK) return r;
+  Sizes b = conv_bytes(s);
+  if (overlap(z, b.z, x, b.x) || overlap(z, b.z, w, b.w))
+    return fail(CF_ERR_ALIAS, "conv3d_fwd: z overlaps x or W");
+  hipStream_t st = (hipStream_t)stream;
+  return finish(cf::launch_conv_fwd(s, x, w, z, st), st, "cf_conv3d_fwd");
+}
+
+cf_status cf_conv3d_bwd_data(const cf_conv3d_desc *desc, const void *dz, const void *w, void *dx,
+                             void *stream) {
+  cf::ConvShape s;
+  cf_status r = resolve(desc, &s);
+  if (r != CF_OK) return r;
+  if (s.n == 0) return ok();
+  if ((r = check_ptrs({dz, w, dx})) != CF_OK) return r;
+  Sizes b = conv_bytes(s);
+  if (overlap(dx, b.x, dz, b.z) || overlap(dx, b.x, w, b.w))
+    return fail(CF_ERR_ALIAS, "conv3d_bwd_data: dx overlaps dz or W");
+  hipStream_t st = (hipStream_t)stream;
+  return finish(cf::launch_conv_bwd_data(s, dz, w, dx, st), st, "cf_conv3d_bwd_data");
+}
+
+size_t cf_conv3d_bwd_weight_workspace_size(const cf_conv3d_desc *desc) {
+  cf::ConvShape s;
+  std::string keep = g_last_error;
+  if (resolve(desc, &s) != CF_OK) {
+    g_last_error = keep;
+    return 0;
+  }
+  if (s.n == 0) return 0;
+  return cf::conv_bwd_weight_workspace(s);
+}
+
+cf_status cf_conv3d_bwd_weight(const cf_conv3d_desc *desc, const void *x, const void *dz, float *dw,
+                               void *ws, size_t ws_bytes, void *stream) {
+  cf::ConvShape s;
+  cf_status r = resolve(desc, &s);
+  if (r != CF_OK) return r;
+  hipStream_t st = (hipStream_t)stream;
+  Sizes b = conv_bytes(s);
+  const size_t dw_bytes = (size_t)s.kd * s.kh * s.kw * s.ci * s.co * sizeof(float);
+  if (s.n == 0) {
+    if ((r = check_ptrs({dw})) != CF_OK) return r;
+    // the sum over an empty batch is zero
+    return finish(cf::launch_fill_zero(dw, (long long)(dw_bytes / sizeof(float)), st), st,
+                  "cf_conv3d_bwd_weight");
+  }
+  if ((r = check_ptrs({x, dz, dw})) != CF_OK) return r;
+  const size_t need = cf::conv_bwd_weight_workspace(s);
+  if (need > 0 && (!ws || ws_bytes < need))
+    return fail(CF_ERR_WORKSPACE, "conv3d_bwd_weight: workspace smaller than cf_conv3d_bwd_weight_workspace_size()");
+  if (ws && !aligned16(ws)) return fail(CF_ERR_ALIGNMENT, "workspace not 16-byte aligned");
+  if (overlap(dw, dw_bytes, x, b.x) || overlap(dw, dw_bytes, dz, b.z))
+    return fail(CF_ERR_ALIAS, "conv3d_bwd_weight: dW overlaps x or dz");
+  if (overlap(ws, need, x, b.x) || overlap(ws, need, dz, b.z) || overlap(ws, need, dw, dw_bytes))
+    return fail(CF_ERR_ALIAS, "conv3d_bwd_weight: workspace overlaps a tensor");
+  return finish(cf::launch_conv_bwd_weight(s, x, dz, dw, ws, st), st, "cf_conv3d_bwd_weight");
+}
+
+cf_status cf_bias_lrelu_fwd(int64_t nvox, int32_t c, int32_t dtype, const void *z, const float *bias,
+                            float alpha, void *y, void *stream) {
+  if (nvox < 0) return fail(CF_ERR_INVALID_ARG, "nvox must be >= 0");
+  if (c <= 0) return fail(CF_ERR_INVALID_ARG, "channels must be > 0");
+  if (dtype != CF_F32 && dtype != CF_BF16) return fail(CF_ERR_INVALID_ARG, "unknown dtype");
+  if (!std::isfinite(alpha)) return fail(CF_ERR_INVALID_ARG, "alpha must be finite");
+  if (nvox == 0) return ok();
+  cf_status r;
+  if ((r = check_ptrs({z, y})) != CF_OK) return r;
+  if (!bias) return fail(CF_ERR_INVALID_ARG, "bias is NULL");
+  const size_t bytes = (size_t)nvox * c * elem_size(dtype);
+  if (y != z && overlap(y, bytes, z, bytes))
+    return fail(CF_ERR_ALIAS, "bias_lrelu_fwd: y partially overlaps z");
+  if (overlap(y, bytes, bias, (size_t)c * 4)) return fail(CF_ERR_ALIAS, "bias_lrelu_fwd: y overlaps bias");
+  hipStream_t st = (hipStream_t)stream;
+  return finish(cf::launch_bias_lrelu_fwd(nvox, c, dtype == CF_BF16 ? cf::DT_BF16 : cf::DT_F32, z, bias,
+                                          alpha, y, st),
+                st, "cf_bias_lrelu_fwd");
+}
+
+size_t cf_bias_lrelu_bwd_workspace_size(int64_t nvox, int32_t c) {
+  if (nvox <= 0 || c <= 0) return 0;
+  return cf::bias_lrelu_bwd_workspace(nvox, c);
+}
+
+cf_status cf_bias_lrelu_bwd(int64_t nvox, int32_t c, int32_t dtype, const void *dy, const void *y,
+                            float alpha, void *dz, float *db, void *ws, size_t ws_bytes,
+                            void *stream) {
+  if (nvox < 0) return fail(CF_ERR_INVALID_ARG, "nvox must be >= 0");
+  if (c <= 0) return fail(CF_ERR_INVALID_ARG, "channels must be > 0");
+  if (c > 2048) return fail(CF_ERR_UNSUPPORTED, "bias_lrelu_bwd: more than 2048 channels");
+  if (dtype != CF_F32 && dtype != CF_BF16) return fail(CF_ERR_INVALID_ARG, "unknown dtype");
+  if (!std::isfinite(alpha)) return fail(CF_ERR_INVALID_ARG, "alpha must be finite");
+  hipStream_t st = (hipStream_t)stream;
+  const int dt = dtype == CF_BF16 ? cf::DT_BF16 : cf::DT_F32;
+  if (nvox == 0) {
+    if (!db) return ok();
+    if (!aligned16(db)) return fail(CF_ERR_ALIGNMENT, "db not 16-byte aligned");
+    return finish(cf::launch_bias_lrelu_bwd(0, c, dt, nullptr, nullptr, alpha, nullptr, db, nullptr, st),
+                  st, "cf_bias_lrelu_bwd");
+  }
+  cf_status r;
+  if ((r = check_ptrs({dy, y, dz})) != CF_OK) return r;
+  const size_t bytes = (size_t)nvox * c * elem_size(dtype);
+  if (dz != dy && overlap(dz, bytes, dy, bytes))
+    return fail(CF_ERR_ALIAS, "bias_lrelu_bwd: dz partially overlaps dy");
+  if (overlap(dz, bytes, y, bytes)) return fail(CF_ERR_ALIAS, "bias_lrelu_bwd: dz overlaps y");
+  if (db) {
+    if (!aligned16(db)) return fail(CF_ERR_ALIGNMENT, "db not 16-byte aligned");
+    const size_t need = cf::bias_lrelu_bwd_workspace(nvox, c);
+    if (!ws || ws_bytes < need)
+      return fail(CF_ERR_WORKSPACE, "bias_lrelu_bwd: workspace smaller than cf_bias_lrelu_bwd_workspace_size()");
+    if (!aligned16(ws)) return fail(CF_ERR_ALIGNMENT, "workspace not 16-byte aligned");
+    if (overlap(db, (size_t)c * 4, dz, bytes) || overlap(ws, need, dz, bytes) ||
+        overlap(ws, need, dy, bytes) || overlap(ws, need, y, bytes) || overlap(ws, need, db, (size_t)c * 4))
+      return fail(CF_ERR_ALIAS, "bias_lrelu_bwd: db or workspace overlaps a tensor");
+  }
+  return finish(cf::launch_bias_lrelu_bwd(nvox, c, dt, dy, y, alpha, dz, db, ws, st), st,
+                "cf_bias_lrelu_bwd");
+}
+
+static cf_status pool_check(int32_t n, int32_t d, int32_t h, int32_t w, int32_t c, int32_t k,
+                            int32_t s, int32_t dtype) {
+  if (n < 0) return fail(CF_ERR_INVALID_ARG, "batch n must be >= 0");
+  if (d <= 0 || h <= 0 || w <= 0 || c <= 0) return fail(CF_ERR_INVALID_ARG, "extents and channels must be > 0");
+  if (k <= 0 || s <= 0) return fail(CF_ERR_INVALID_ARG, "window and stride must be > 0");
+  if (dtype != CF_F32 && dtype != CF_BF16) return fail(CF_ERR_INVALID_ARG, "unknown dtype");
+  if (k != s) return fail(CF_ERR_UNSUPPORTED, "avgpool3d: only non-overlapping windows (k == s)");
+  if (d < k || h < k || w < k) return fail(CF_ERR_INVALID_ARG, "avgpool3d: window larger than input");
+  if ((long long)n * d * h * w >= kMaxRows) return fail(CF_ERR_INVALID_ARG, "too many voxels (>= 2^31)");
+  return CF_OK;
+}
+
+cf_status cf_avgpool3d_fwd(int32_t n, int32_t d, int32_t h, int32_t w, int32_t c, int32_t k, int32_t s,
+                           int32_t dtype, const void *y, void *p, void *stream) {
+  cf_status r = pool_check(n, d, h, w, c, k, s, dtype);
+  if (r != CF_OK) return r;
+  if (n == 0) return ok();
+  if ((r = check_ptrs({y, p})) != CF_OK) return r;
+  const size_t es = elem_size(dtype);
+  const size_t by = (size_t)n * d * h * w * c * es;
+  const size_t bp = (size_t)n * ((d - k) / s + 1) * ((h - k) / s + 1) * ((w - k) / s + 1) * c * es;
+  if (overlap(y, by, p, bp)) return fail(CF_ERR_ALIAS, "avgpool3d_fwd: p overlaps y");
+  hipStream_t st = (hipStream_t)stream;
+  return finish(cf::launch_avgpool_fwd(n, d, h, w, c, k, dtype == CF_BF16 ? cf::DT_BF16 : cf::DT_F32, y, p, st),
+                st, "cf_avgpool3d_fwd");
+}
+
+cf_status cf_avgpool3d_bwd(int32_t n, int32_t d, int32_t h, int32_t w, int32_t c, int32_t k, int32_t s,
+                           int32_t dtype, const void *dp, void *dy, void *stream) {
+  cf_status r = pool_check(n, d, h, w, c, k, s, dtype);
+  if (r != CF_OK) return r;
+  if (n == 0) return ok();
+  if ((r = check_ptrs({dp, dy})) != CF_OK) return r;
+  const size_t es = elem_size(dtype);
+  const size_t by = (size_t)n * d * h * w * c * es;
+  const size_t bp = (size_t)n * ((d - k) / s + 1) * ((h - k) / s + 1) * ((w - k) / s + 1) * c * es;
+  if (overlap(dy, by, dp, bp)) return fail(CF_ERR_ALIAS, "avgpool3d_bwd: dy overlaps dp");
+  hipStream_t st = (hipStream_t)stream;
+  return finish(cf::launch_avgpool_bwd(n, d, h, w, c, k, dtype == CF_BF16 ? cf::DT_BF16 : cf::DT_F32, dp, dy, st),
+                st, "cf_avgpool3d_bwd");
+}
+
+}  // extern "C"

@@ -1,0 +1,42 @@
+// cf_common.h -- device helpers shared by the gfx950 kernels of this library.
+//
+// Storage types: fp32 tensors are `float`, bf16 tensors are raw `uint16_t`
+// (IEEE bfloat16 bit patterns).  Arithmetic is always fp32; every bf16 store
+// rounds to nearest even.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace cf {
+
+enum : int { DT_F32 = 0, DT_BF16 = 1 };
+
+template <int DT> struct Store;
+template <> struct Store<DT_F32> { using T = float; static constexpr int VEC = 4; };
+template <> struct Store<DT_BF16> { using T = uint16_t; static constexpr int VEC = 8; };
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float bf2f(uint16_t u) { return __uint_as_float(((uint32_t)u) << 16); }
+__device__ __forceinline__ uint16_t f2bf(float f) {
+  __bf16 b = (__bf16)f;  // round to nearest even (v_cvt_pk_bf16_f32 on gfx950)
+  return __builtin_bit_cast(uint16_t, b);
+}
+
+template <int DT> __device__ __forceinline__ float to_f32(typename Store<DT>::T v);
+template <> __device__ __forceinline__ float to_f32<DT_F32>(float v) { return v; }
+template <> __device__ __forceinline__ float to_f32<DT_BF16>(uint16_t v) { return bf2f(v); }
+
+template <int DT> __device__ __forceinline__ typename Store<DT>::T from_f32(float v);
+template <> __device__ __forceinline__ float from_f32<DT_F32>(float v) { return v; }
+template <> __device__ __forceinline__ uint16_t from_f32<DT_BF16>(float v) { return f2bf(v); }
+
+// 16-byte vector of storage elements, viewed either as raw words or elements.
+template <int DT> union Vec16 {
+  uint4 u;
+  typename Store<DT>::T e[Store<DT>::VEC];
+};
+
+}  // namespace cf

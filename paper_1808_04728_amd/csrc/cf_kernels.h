@@ -1,0 +1,47 @@
+// cf_kernels.h -- host-side launchers of the gfx950 kernels (internal).
+//
+// The C ABI layer (cf_api.cpp) validates arguments, derives the geometry
+// below and calls these launchers; they only pick a kernel variant and
+// launch it on the given stream.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace cf {
+
+// Fully resolved geometry of one convolution layer.
+struct ConvShape {
+  int n, d, h, w;        // input extent
+  int ci, co;            // channels
+  int kd, kh, kw;        // kernel
+  int sd, sh, sw;        // strides
+  int pd, ph, pw;        // padding before (after = whatever SAME leaves)
+  int od, oh, ow;        // output extent
+  int dtype;             // DT_F32 / DT_BF16
+};
+
+hipError_t launch_conv_fwd(const ConvShape &s, const void *x, const void *w, void *z,
+                           hipStream_t st);
+hipError_t launch_conv_bwd_data(const ConvShape &s, const void *dz, const void *w, void *dx,
+                                hipStream_t st);
+size_t conv_bwd_weight_workspace(const ConvShape &s);
+hipError_t launch_conv_bwd_weight(const ConvShape &s, const void *x, const void *dz, float *dw,
+                                  void *ws, hipStream_t st);
+
+hipError_t launch_bias_lrelu_fwd(int64_t nvox, int c, int dtype, const void *z,
+                                 const float *bias, float alpha, void *y, hipStream_t st);
+size_t bias_lrelu_bwd_workspace(int64_t nvox, int c);
+hipError_t launch_bias_lrelu_bwd(int64_t nvox, int c, int dtype, const void *dy, const void *y,
+                                 float alpha, void *dz, float *db, void *ws, hipStream_t st);
+
+// out[0..n) = 0 (a fill kernel, never hipMemsetAsync).
+hipError_t launch_fill_zero(float *out, long long n, hipStream_t st);
+
+hipError_t launch_avgpool_fwd(int n, int d, int h, int w, int c, int k, int dtype,
+                              const void *y, void *p, hipStream_t st);
+hipError_t launch_avgpool_bwd(int n, int d, int h, int w, int c, int k, int dtype,
+                              const void *dp, void *dy, hipStream_t st);
+
+}  // namespace cf

@@ -1,0 +1,209 @@
+// eltwise.hip -- bias + leaky ReLU forward / backward for gfx950.
+//
+// Section III-A: every convolution layer is followed by a leaky ReLU; the
+// paper runs it as separate, OpenMP-threaded TensorFlow element-wise ops and
+// notes their load imbalance (Section V-B).  Here both directions are single
+// HBM-bound passes with 16-byte vector access:
+//   forward   y = lrelu(z + b)                               (read z, write y)
+//   backward  dz = dy * (y > 0 ? 1 : alpha), db = sum dz      (read dy, y; write dz)
+// The bias gradient is reduced without atomics: each workgroup owns a fixed
+// contiguous voxel range, threads own (voxel phase, channel group) pairs and
+// keep fp32 partial sums in registers, the workgroup combines its phases in
+// LDS in phase order and writes one partial row; a second kernel sums the
+// rows in workgroup order.
+
+#include "cf_common.h"
+#include "cf_kernels.h"
+
+#include <algorithm>
+
+namespace cf {
+namespace {
+
+__device__ __forceinline__ float lrelu(float u, float alpha) { return u > 0.f ? u : alpha * u; }
+
+template <int DT, bool VECTOR>
+__global__ __launch_bounds__(256) void bias_lrelu_fwd_kernel(const typename Store<DT>::T *z,
+                                                             const float *__restrict__ bias,
+                                                             float alpha,
+                                                             typename Store<DT>::T *y,
+                                                             long long nelem, int c) {
+  using T = typename Store<DT>::T;
+  constexpr int V = VECTOR ? Store<DT>::VEC : 1;
+  const long long nv = nelem / V;
+  const long long stride = (long long)gridDim.x * 256;
+  for (long long i = (long long)blockIdx.x * 256 + threadIdx.x; i < nv; i += stride) {
+    const int c0 = (int)((i * V) % c);
+    if constexpr (VECTOR) {
+      Vec16<DT> v;
+      v.u = reinterpret_cast<const uint4 *>(z)[i];
+#pragma unroll
+      for (int j = 0; j < V; ++j)
+        v.e[j] = from_f32<DT>(lrelu(to_f32<DT>(v.e[j]) + bias[c0 + j], alpha));
+      reinterpret_cast<uint4 *>(y)[i] = v.u;
+    } else {
+      y[i] = from_f32<DT>(lrelu(to_f32<DT>(z[i]) + bias[c0], alpha));
+    }
+  }
+}
+
+// Thread layout of the backward kernel: CG channel groups of V channels,
+// PH = max(1, 256 / CG) voxel phases.
+template <int DT, bool VECTOR, bool WITH_DB>
+__global__ __launch_bounds__(256) void bias_lrelu_bwd_kernel(const typename Store<DT>::T *dy,
+                                                             const typename Store<DT>::T *__restrict__ y,
+                                                             float alpha,
+                                                             typename Store<DT>::T *dz,
+                                                             float *__restrict__ part,
+                                                             long long nvox, int c, long long vpb) {
+  using T = typename Store<DT>::T;
+  constexpr int V = VECTOR ? Store<DT>::VEC : 1;
+  __shared__ float red[2048];  // phases * c <= 256 * V, and c <= 2048 (checked by the host)
+  const int cg_n = c / V;
+  const int ph_n = cg_n >= 256 ? 1 : 256 / cg_n;
+  const int tid = threadIdx.x;
+  const long long v0 = (long long)blockIdx.x * vpb;
+  const long long v1 = v0 + vpb < nvox ? v0 + vpb : nvox;
+  const int ph = tid / (cg_n >= 256 ? 256 : cg_n);
+  // every (phase, group) pair this thread owns
+  for (int cg = (cg_n >= 256 ? tid : tid % cg_n); ph < ph_n && cg < cg_n; cg += 256) {
+    float s[V];
+#pragma unroll
+    for (int j = 0; j < V; ++j) s[j] = 0.f;
+    for (long long v = v0 + ph; v < v1; v += ph_n) {
+      const long long e = v * c + (long long)cg * V;
+      if constexpr (VECTOR) {
+        Vec16<DT> g, o;
+        g.u = *reinterpret_cast<const uint4 *>(dy + e);
+        o.u = *reinterpret_cast<const uint4 *>(y + e);
+#pragma unroll
+        for (int j = 0; j < V; ++j) {
+          float d = to_f32<DT>(g.e[j]) * (to_f32<DT>(o.e[j]) > 0.f ? 1.f : alpha);
+          s[j] += d;
+          g.e[j] = from_f32<DT>(d);
+        }
+        *reinterpret_cast<uint4 *>(dz + e) = g.u;
+      } else {
+        float d = to_f32<DT>(dy[e]) * (to_f32<DT>(y[e]) > 0.f ? 1.f : alpha);
+        s[0] += d;
+        dz[e] = from_f32<DT>(d);
+      }
+    }
+    if constexpr (WITH_DB) {
+#pragma unroll
+      for (int j = 0; j < V; ++j) {
+        if (cg_n >= 256) red[cg * V + j] = s[j];  // a single phase
+        else red[ph * c + cg * V + j] = s[j];
+      }
+    }
+    if (cg_n < 256) break;
+  }
+  if constexpr (WITH_DB) {
+    __syncthreads();
+    for (int ch = tid; ch < c; ch += 256) {
+      float acc = 0.f;
+      for (int k = 0; k < ph_n; ++k) acc += red[k * c + ch];
+      part[(long long)blockIdx.x * c + ch] = acc;
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void column_sum_kernel(const float *__restrict__ part,
+                                                         float *__restrict__ out, int rows,
+                                                         int cols) {
+  int ch = blockIdx.x * 256 + threadIdx.x;
+  if (ch >= cols) return;
+  float acc = 0.f;
+  for (int r = 0; r < rows; ++r) acc += part[(long long)r * cols + ch];
+  out[ch] = acc;
+}
+
+__global__ __launch_bounds__(256) void fill_zero_kernel(float *out, long long n) {
+  long long i = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (i < n) out[i] = 0.f;
+}
+
+struct BwdPlan {
+  long long vpb;
+  int blocks;
+};
+
+BwdPlan plan_bwd(long long nvox, int c) {
+  BwdPlan p;
+  long long vpb = std::max<long long>(64, (nvox + 2047) / 2048);
+  p.vpb = vpb;
+  p.blocks = (int)((nvox + vpb - 1) / vpb);
+  return p;
+}
+
+template <int DT>
+hipError_t fwd_t(long long nvox, int c, const void *z, const float *bias, float alpha, void *y,
+                 hipStream_t st) {
+  using T = typename Store<DT>::T;
+  const long long nelem = nvox * c;
+  const bool vec = c % Store<DT>::VEC == 0;
+  const long long items = vec ? nelem / Store<DT>::VEC : nelem;
+  const int blocks = (int)std::min<long long>((items + 255) / 256, 256LL * 64);
+  if (vec)
+    hipLaunchKernelGGL((bias_lrelu_fwd_kernel<DT, true>), dim3(blocks), dim3(256), 0, st,
+                       (const T *)z, bias, alpha, (T *)y, nelem, c);
+  else
+    hipLaunchKernelGGL((bias_lrelu_fwd_kernel<DT, false>), dim3(blocks), dim3(256), 0, st,
+                       (const T *)z, bias, alpha, (T *)y, nelem, c);
+  return hipGetLastError();
+}
+
+template <int DT, bool WITH_DB>
+hipError_t bwd_t(long long nvox, int c, const void *dy, const void *y, float alpha, void *dz,
+                 float *db, void *ws, hipStream_t st) {
+  using T = typename Store<DT>::T;
+  BwdPlan pl = plan_bwd(nvox, c);
+  const bool vec = c % Store<DT>::VEC == 0;
+  float *part = (float *)ws;
+  if (vec)
+    hipLaunchKernelGGL((bias_lrelu_bwd_kernel<DT, true, WITH_DB>), dim3(pl.blocks), dim3(256), 0, st,
+                       (const T *)dy, (const T *)y, alpha, (T *)dz, part, nvox, c, pl.vpb);
+  else
+    hipLaunchKernelGGL((bias_lrelu_bwd_kernel<DT, false, WITH_DB>), dim3(pl.blocks), dim3(256), 0, st,
+                       (const T *)dy, (const T *)y, alpha, (T *)dz, part, nvox, c, pl.vpb);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || !WITH_DB) return e;
+  hipLaunchKernelGGL(column_sum_kernel, dim3((c + 255) / 256), dim3(256), 0, st, part, db,
+                     pl.blocks, c);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_bias_lrelu_fwd(int64_t nvox, int c, int dtype, const void *z, const float *bias,
+                                 float alpha, void *y, hipStream_t st) {
+  if (nvox == 0) return hipSuccess;
+  return dtype == DT_BF16 ? fwd_t<DT_BF16>(nvox, c, z, bias, alpha, y, st)
+                          : fwd_t<DT_F32>(nvox, c, z, bias, alpha, y, st);
+}
+
+size_t bias_lrelu_bwd_workspace(int64_t nvox, int c) {
+  if (nvox <= 0) return 0;
+  BwdPlan pl = plan_bwd(nvox, c);
+  return (size_t)pl.blocks * c * sizeof(float);
+}
+
+hipError_t launch_bias_lrelu_bwd(int64_t nvox, int c, int dtype, const void *dy, const void *y,
+                                 float alpha, void *dz, float *db, void *ws, hipStream_t st) {
+  if (nvox == 0) {
+    return db ? launch_fill_zero(db, c, st) : hipSuccess;
+  }
+  if (dtype == DT_BF16)
+    return db ? bwd_t<DT_BF16, true>(nvox, c, dy, y, alpha, dz, db, ws, st)
+              : bwd_t<DT_BF16, false>(nvox, c, dy, y, alpha, dz, db, ws, st);
+  return db ? bwd_t<DT_F32, true>(nvox, c, dy, y, alpha, dz, db, ws, st)
+            : bwd_t<DT_F32, false>(nvox, c, dy, y, alpha, dz, db, ws, st);
+}
+
+hipError_t launch_fill_zero(float *out, long long n, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, out, n);
+  return hipGetLastError();
+}
+
+}  // namespace cf

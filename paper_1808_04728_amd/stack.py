@@ -1,0 +1,180 @@
+"""The CosmoFlow-shaped conv stack driven through the C ABI.
+
+One training step of the hot path (the order of a TensorFlow forward and
+backward pass over the network's convolution part, Section III-A):
+
+  forward,  layer 1..L:  conv -> bias + leaky ReLU (in place) -> [2^3 avg-pool]
+  backward, layer L..1:  [pool backward] -> leaky-ReLU backward (+ bias grad)
+                         -> weight grad -> data grad (skipped for layer 1,
+                            whose input needs no gradient)
+
+PyTorch only allocates device memory and supplies the stream; every step is
+one call of ``binding`` (a HIP kernel).  Buffers are allocated once, so a
+step launches kernels and nothing else.
+"""
+from __future__ import annotations
+
+import torch
+
+from . import binding as B
+
+
+def _t(dtype):
+    return torch.bfloat16 if dtype == "bf16" else torch.float32
+
+
+class ConvStack:
+    def __init__(self, layers, size, batch, dtype="f32", alpha=0.01, device="cuda", skip_first_dgrad=True):
+        self.layers = layers
+        self.batch = batch
+        self.dtype = dtype
+        self.tdt = _t(dtype)
+        self.alpha = float(alpha)
+        self.device = device
+        self.skip_first_dgrad = skip_first_dgrad
+        self.timer = None  # optional: {op name: [(start event, end event), ...]}
+        self.timed_ops = None  # None = every op, else the set of op names to time
+        self.L = []
+        dhw = (size, size, size)
+        for i, spec in enumerate(layers):
+            desc = B.make_desc(batch, dhw, spec["cin"], spec["cout"], spec["k"], spec["stride"],
+                               spec.get("pad", "same"), dtype)
+            od = B.cf_conv3d_out_shape(desc)
+            pdhw = tuple(t // 2 for t in od) if spec["pool"] else od
+            self.L.append(dict(spec=spec, desc=desc, in_dhw=dhw, out_dhw=od, pool_dhw=pdhw,
+                               nvox=batch * od[0] * od[1] * od[2]))
+            dhw = pdhw
+        self.out_dhw = dhw
+        self._alloc()
+
+    # ------------------------------------------------------------------
+    def _alloc(self):
+        dev, tdt, n = self.device, self.tdt, self.batch
+        for i, l in enumerate(self.L):
+            s = l["spec"]
+            l["w"] = torch.zeros((s["k"],) * 3 + (s["cin"], s["cout"]), dtype=tdt, device=dev)
+            l["b"] = torch.zeros(s["cout"], dtype=torch.float32, device=dev)
+            l["z"] = torch.empty((n,) + l["out_dhw"] + (s["cout"],), dtype=tdt, device=dev)  # z, then y in place
+            l["p"] = torch.empty((n,) + l["pool_dhw"] + (s["cout"],), dtype=tdt, device=dev) if s["pool"] else None
+            l["gout"] = torch.empty((n,) + l["pool_dhw"] + (s["cout"],), dtype=tdt, device=dev)
+            l["dy"] = torch.empty_like(l["z"]) if s["pool"] else None
+            l["dz"] = torch.empty_like(l["z"])
+            l["dw"] = torch.empty(l["w"].shape, dtype=torch.float32, device=dev)
+            l["db"] = torch.empty(s["cout"], dtype=torch.float32, device=dev)
+            wsw = B.cf_conv3d_bwd_weight_workspace_size(l["desc"])
+            wsb = B.cf_bias_lrelu_bwd_workspace_size(l["nvox"], s["cout"])
+            l["ws_w"] = torch.empty(max(wsw, 16), dtype=torch.uint8, device=dev)
+            l["ws_b"] = torch.empty(max(wsb, 16), dtype=torch.uint8, device=dev)
+            l["dx"] = None
+        for i in range(1, len(self.L)):
+            self.L[i]["dx"] = self.L[i - 1]["gout"]
+        if not self.skip_first_dgrad:
+            s = self.L[0]["spec"]
+            self.L[0]["dx"] = torch.empty((n,) + self.L[0]["in_dhw"] + (s["cin"],), dtype=tdt, device=dev)
+        self.x = torch.empty((n,) + self.L[0]["in_dhw"] + (self.L[0]["spec"]["cin"],), dtype=tdt, device=dev)
+
+    def set_params(self, weights, biases):
+        for l, w, b in zip(self.L, weights, biases):
+            l["w"].copy_(torch.as_tensor(w).to(self.tdt))
+            l["b"].copy_(torch.as_tensor(b).float())
+
+    def set_input(self, x):
+        self.x.copy_(torch.as_tensor(x).to(self.tdt))
+
+    def output(self):
+        l = self.L[-1]
+        return l["p"] if l["spec"]["pool"] else l["z"]
+
+    def _call(self, name, fn, *args):
+        if self.timer is None or (self.timed_ops is not None and name not in self.timed_ops):
+            fn(*args)
+            return
+        import torch as _torch
+        e0 = _torch.cuda.Event(enable_timing=True)
+        e1 = _torch.cuda.Event(enable_timing=True)
+        e0.record()
+        fn(*args)
+        e1.record()
+        self.timer.setdefault(name, []).append((e0, e1))
+
+    # ------------------------------------------------------------------
+    def forward(self, stream=None):
+        h = self.x
+        for i, l in enumerate(self.L):
+            s = l["spec"]
+            c = self._call
+            c(f"L{i+1}.conv_fwd", B.cf_conv3d_fwd, l["desc"], h, l["w"], l["z"], stream)
+            c(f"L{i+1}.bias_lrelu_fwd", B.cf_bias_lrelu_fwd, l["nvox"], s["cout"], self.dtype, l["z"], l["b"],
+              self.alpha, l["z"], stream)
+            if s["pool"]:
+                d, hh, w = l["out_dhw"]
+                c(f"L{i+1}.avgpool_fwd", B.cf_avgpool3d_fwd, self.batch, d, hh, w, s["cout"], 2, 2, self.dtype,
+                  l["z"], l["p"], stream)
+                h = l["p"]
+            else:
+                h = l["z"]
+        return h
+
+    def backward(self, dout, stream=None):
+        """dout: gradient w.r.t. the last layer's output (not modified)."""
+        g = dout
+        for i in range(len(self.L) - 1, -1, -1):
+            l = self.L[i]
+            s = l["spec"]
+            c = self._call
+            if s["pool"]:
+                d, hh, w = l["out_dhw"]
+                c(f"L{i+1}.avgpool_bwd", B.cf_avgpool3d_bwd, self.batch, d, hh, w, s["cout"], 2, 2, self.dtype,
+                  g, l["dy"], stream)
+                dy = l["dy"]
+            else:
+                dy = g
+            c(f"L{i+1}.bias_lrelu_bwd", B.cf_bias_lrelu_bwd, l["nvox"], s["cout"], self.dtype, dy, l["z"],
+              self.alpha, l["dz"], l["db"], l["ws_b"], None, stream)
+            c(f"L{i+1}.conv_bwd_weight", B.cf_conv3d_bwd_weight, l["desc"], self.layer_input(i), l["dz"], l["dw"],
+              l["ws_w"], None, stream)
+            if l["dx"] is not None:
+                c(f"L{i+1}.conv_bwd_data", B.cf_conv3d_bwd_data, l["desc"], l["dz"], l["w"], l["dx"], stream)
+                g = l["dx"]
+
+    def layer_input(self, i):
+        if i == 0:
+            return self.x
+        p = self.L[i - 1]
+        return p["p"] if p["spec"]["pool"] else p["z"]
+
+    def op_flops(self, name):
+        """Algorithmic FLOPs of one call of a conv op (2 * MACs), else 0."""
+        i = int(name[1:name.index(".")]) - 1
+        if ".conv_" not in name:
+            return 0
+        l = self.L[i]
+        s = l["spec"]
+        return 2 * l["nvox"] * s["cout"] * s["k"] ** 3 * s["cin"]
+
+    def op_bytes(self, name):
+        """Algorithmic HBM bytes of one call (every tensor read once, written once)."""
+        i = int(name[1:name.index(".")]) - 1
+        l = self.L[i]
+        s = l["spec"]
+        es = 2 if self.dtype == "bf16" else 4
+        vin = self.batch * l["in_dhw"][0] * l["in_dhw"][1] * l["in_dhw"][2]
+        xb = vin * s["cin"] * es
+        zb = l["nvox"] * s["cout"] * es
+        wb = s["k"] ** 3 * s["cin"] * s["cout"] * es
+        pb = zb // 8
+        op = name.split(".")[1]
+        return {"conv_fwd": xb + wb + zb, "conv_bwd_data": zb + wb + xb,
+                "conv_bwd_weight": xb + zb + wb // es * 4, "bias_lrelu_fwd": 2 * zb,
+                "bias_lrelu_bwd": 3 * zb, "avgpool_fwd": zb + pb, "avgpool_bwd": zb + pb}[op]
+
+    # ------------------------------------------------------------------
+    def conv_flops(self):
+        """Algorithmic conv FLOPs of one step: 2 * MACs for fwd, wgrad and
+        (except a skipped first layer) dgrad; padded taps included."""
+        f = 0
+        for i, l in enumerate(self.L):
+            s = l["spec"]
+            macs = l["nvox"] * s["cout"] * s["k"] ** 3 * s["cin"]
+            f += 2 * macs * (2 if (i == 0 and self.skip_first_dgrad) else 3)
+        return f

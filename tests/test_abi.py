@@ -1,0 +1,119 @@
+"""Host-side checks of the C ABI: the library loads, exports every symbol the
+header declares, and rejects invalid arguments before touching a device.
+
+No call here launches a kernel: every call either fails validation or is a
+host-only query, so these tests run without a GPU.
+"""
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+from paper_1808_04728_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "cosmoflow.h")
+
+A = 0x7F0000000000  # fake, 16-byte aligned device addresses (never dereferenced)
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(B.LIB_PATH):
+        pytest.skip("libcosmoflow_hip.so not built")
+    return B.lib()
+
+
+def header_symbols():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*(cf_[a-z0-9_]+)\s*\(", text, re.M)))
+
+
+def test_header_lists_every_entry_point():
+    assert header_symbols() == sorted(B.EXPORTS)
+
+
+def test_library_exports_every_header_symbol(L):
+    for name in header_symbols():
+        assert hasattr(L, name), name
+
+
+def test_version_and_last_error(L):
+    assert B.cf_version().startswith("cosmoflow-gfx950")
+    assert isinstance(B.cf_last_error(), str)
+
+
+def test_out_shape_same_and_valid(L):
+    assert B.cf_conv3d_out_shape(B.make_desc(1, (32, 32, 32), 32, 64, 4, 2)) == (16, 16, 16)
+    assert B.cf_conv3d_out_shape(B.make_desc(1, (64, 64, 64), 16, 32, 4, 1)) == (64, 64, 64)
+    assert B.cf_conv3d_out_shape(B.make_desc(1, (128, 127, 126), 1, 16, 3, 1, "valid")) == (126, 125, 124)
+    assert B.cf_conv3d_out_shape(B.make_desc(1, (7, 7, 7), 1, 16, 4, 2)) == (4, 4, 4)
+
+
+def expect(status, fn, *args):
+    with pytest.raises(B.CfError) as e:
+        fn(*args)
+    assert e.value.status == status, str(e.value)
+    assert B.cf_last_error() != ""
+
+
+def test_conv_validation(L):
+    d = B.make_desc(1, (8, 8, 8), 16, 32, 3)
+    expect(B.CF_ERR_INVALID_ARG, B.cf_conv3d_fwd, d, None, A, A + 0x100000, 0)
+    expect(B.CF_ERR_ALIGNMENT, B.cf_conv3d_fwd, d, A + 8, A + 0x100000, A + 0x200000, 0)
+    expect(B.CF_ERR_ALIAS, B.cf_conv3d_fwd, d, A, A + 0x100000, A + 0x40, 0)  # z inside x
+    bad = B.make_desc(1, (3, 8, 8), 16, 32, 4, 1, "valid")
+    expect(B.CF_ERR_INVALID_ARG, B.cf_conv3d_fwd, bad, A, A + 0x100000, A + 0x200000, 0)
+    neg = B.make_desc(1, (8, 8, 8), 0, 32, 3)
+    expect(B.CF_ERR_INVALID_ARG, B.cf_conv3d_bwd_data, neg, A, A + 0x100000, A + 0x200000, 0)
+    huge = B.make_desc(1, (8, 8, 8), 1 << 26, 32, 4)
+    expect(B.CF_ERR_INVALID_ARG, B.cf_conv3d_fwd, huge, A, A + 0x100000, A + 0x200000, 0)
+    d2 = B.make_desc(1, (8, 8, 8), 16, 32, 3)
+    d2.dtype = 7
+    expect(B.CF_ERR_INVALID_ARG, B.cf_conv3d_fwd, d2, A, A + 0x100000, A + 0x200000, 0)
+    expect(B.CF_ERR_INVALID_ARG, lambda: B._check(L.cf_conv3d_fwd(None, A, A, A, 0)))
+
+
+def test_wgrad_workspace_validation(L):
+    d = B.make_desc(2, (16, 16, 16), 16, 32, 4)
+    need = B.cf_conv3d_bwd_weight_workspace_size(d)
+    assert need > 0 and need % 4 == 0
+    # deterministic plan: same size every time
+    assert need == B.cf_conv3d_bwd_weight_workspace_size(d)
+    expect(B.CF_ERR_WORKSPACE, B.cf_conv3d_bwd_weight, d, A, A + 0x1000000, A + 0x2000000, None, 0, 0)
+    expect(B.CF_ERR_WORKSPACE, B.cf_conv3d_bwd_weight, d, A, A + 0x1000000, A + 0x2000000,
+           A + 0x3000000, need - 16, 0)
+    expect(B.CF_ERR_ALIAS, B.cf_conv3d_bwd_weight, d, A, A + 0x1000000, A + 0x10, A + 0x3000000, need, 0)
+
+
+def test_eltwise_validation(L):
+    expect(B.CF_ERR_INVALID_ARG, B.cf_bias_lrelu_fwd, 10, 16, "f32", A, A + 0x10000, math.nan, A + 0x20000, 0)
+    expect(B.CF_ERR_INVALID_ARG, B.cf_bias_lrelu_fwd, 10, 0, "f32", A, A + 0x10000, 0.01, A + 0x20000, 0)
+    expect(B.CF_ERR_ALIAS, B.cf_bias_lrelu_fwd, 100, 16, "f32", A, A + 0x100000, 0.01, A + 0x40, 0)
+    expect(B.CF_ERR_INVALID_ARG, B.cf_bias_lrelu_fwd, 100, 16, "f32", A, None, 0.01, A + 0x20000, 0)
+    need = B.cf_bias_lrelu_bwd_workspace_size(1000, 16)
+    assert need > 0
+    expect(B.CF_ERR_WORKSPACE, B.cf_bias_lrelu_bwd, 1000, 16, "f32", A, A + 0x100000, 0.01,
+           A + 0x200000, A + 0x300000, A + 0x400000, need - 4, 0)
+    expect(B.CF_ERR_UNSUPPORTED, B.cf_bias_lrelu_bwd, 10, 4096, "f32", A, A + 0x100000, 0.01,
+           A + 0x200000, None, None, 0, 0)
+    expect(B.CF_ERR_ALIAS, B.cf_bias_lrelu_bwd, 1000, 16, "f32", A, A + 0x100000, 0.01,
+           A + 0x100040, None, None, 0, 0)
+
+
+def test_pool_validation(L):
+    expect(B.CF_ERR_UNSUPPORTED, B.cf_avgpool3d_fwd, 1, 8, 8, 8, 16, 3, 2, "f32", A, A + 0x100000, 0)
+    expect(B.CF_ERR_INVALID_ARG, B.cf_avgpool3d_fwd, 1, 1, 8, 8, 16, 2, 2, "f32", A, A + 0x100000, 0)
+    expect(B.CF_ERR_ALIAS, B.cf_avgpool3d_fwd, 1, 8, 8, 8, 16, 2, 2, "f32", A, A + 0x400, 0)
+    expect(B.CF_ERR_ALIGNMENT, B.cf_avgpool3d_bwd, 1, 8, 8, 8, 16, 2, 2, "f32", A + 4, A + 0x100000, 0)
+
+
+def test_zero_batch_forward_is_host_noop(L):
+    d = B.make_desc(0, (8, 8, 8), 16, 32, 3)
+    B.cf_conv3d_fwd(d, None, None, None, 0)  # no pointer is needed for an empty batch
+    B.cf_conv3d_bwd_data(d, None, None, None, 0)
+    B.cf_avgpool3d_fwd(0, 8, 8, 8, 16, 2, 2, "f32", None, None, 0)
+    B.cf_bias_lrelu_fwd(0, 16, "f32", None, None, 0.01, None, 0)
+    B.cf_bias_lrelu_bwd(0, 16, "f32", None, None, 0.01, None, None, None, 0, 0)
