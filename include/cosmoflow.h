@@ -150,6 +150,57 @@ cf_status cf_avgpool3d_bwd(int32_t n, int32_t d, int32_t h, int32_t w, int32_t c
                            int32_t k, int32_t s, int32_t dtype, const void *dp, void *dy,
                            void *stream);
 
+/* ------------------------------------------------------------------------
+ * Fused layer variants.  Same mathematics as the unfused composition
+ *   conv -> bias + leaky ReLU -> 2^3 stride-2 average pool     (forward)
+ *   pool backward -> leaky-ReLU backward (+ db) -> weight / data gradient
+ * but the full-resolution activation and its gradient never reach HBM: the
+ * forward epilogue writes the pooled output plus a 1-bit slope mask, and the
+ * backward kernels rebuild dz from the pooled-output gradient and the mask.
+ * Rounding differs from the unfused composition only in where values are
+ * rounded to bf16 (the fused path rounds once, at the pooled output).
+ * ------------------------------------------------------------------------ */
+
+/* flags */
+#define CF_FUSE_POOL2 1u /* a 2^3 stride-2 average pool follows the activation */
+
+/* Bitmask of the fused entry points that accept (desc, flags) on this build:
+ * 1 = cf_conv3d_fwd_fused, 2 = cf_conv3d_bwd_weight_fused.  Host-only; 0 on
+ * an invalid desc. */
+int32_t cf_conv3d_fused_supported(const cf_conv3d_desc *desc, uint32_t flags);
+
+/* Bytes of the slope mask of a layer: one bit per element of the conv output
+ * [n,od,oh,ow,c_out], bit e (NDHWC element index) = bit e%32 of 32-bit word
+ * e/32, i.e. ceil(n*od*oh*ow*c_out/32)*4 bytes.  0 on invalid desc. */
+size_t cf_conv3d_mask_bytes(const cf_conv3d_desc *desc);
+
+/* Fused forward: u = conv(x, W) + bias (fp32), y = u > 0 ? u : alpha*u.
+ * With CF_FUSE_POOL2: out = avgpool 2^3 stride 2 of y, [n,od/2,oh/2,ow/2,c_out]
+ * (floor), summed in fp32 and rounded once; mask (required, see
+ * cf_conv3d_mask_bytes) records u > 0 for every conv-output element.
+ * alpha must be finite and >= 0 (then u > 0 <=> y > 0, the slope rule of
+ * cf_bias_lrelu_bwd).  Unsupported shapes return CF_ERR_UNSUPPORTED (see
+ * cf_conv3d_fused_supported); the unfused calls cover every shape. */
+cf_status cf_conv3d_fwd_fused(const cf_conv3d_desc *desc, const void *x, const void *w,
+                              const float *bias, float alpha, uint32_t flags, void *out,
+                              void *mask, void *stream);
+
+/* Workspace bytes of cf_conv3d_bwd_weight_fused for (desc, flags). */
+size_t cf_conv3d_bwd_weight_fused_workspace_size(const cf_conv3d_desc *desc, uint32_t flags);
+
+/* Fused backward-weights.  With CF_FUSE_POOL2, g is the gradient of the
+ * pooled output [n,od/2,oh/2,ow/2,c_out] and mask the forward's slope mask:
+ *   dz[v,c] = g[pool(v),c] / 8 * (mask(v,c) ? 1 : alpha)  (0 where no window covers v)
+ *   dW[t,ci,co] = sum_{n,o} x[n, o*s + t - pad_before, ci] * dz[n,o,co]   (fp32)
+ *   db[c] = sum_v dz[v,c]                                                  (fp32)
+ * dz is formed in fp32 (bf16 path: rounded to bf16 before the product, as
+ * the unfused path stores it); db sums the unrounded values.  ws: caller
+ * workspace of cf_conv3d_bwd_weight_fused_workspace_size bytes.  Partial sums
+ * are combined in a fixed order (bitwise reproducible). */
+cf_status cf_conv3d_bwd_weight_fused(const cf_conv3d_desc *desc, const void *x, const void *g,
+                                     const void *mask, float alpha, uint32_t flags, float *dw,
+                                     float *db, void *ws, size_t ws_bytes, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

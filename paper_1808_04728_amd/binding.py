@@ -21,6 +21,8 @@ CF_OK, CF_ERR_INVALID_ARG, CF_ERR_UNSUPPORTED, CF_ERR_ALIGNMENT, CF_ERR_ALIAS, \
     CF_ERR_WORKSPACE, CF_ERR_LAUNCH = range(7)
 CF_F32, CF_BF16 = 0, 1
 CF_PAD_SAME_TF, CF_PAD_VALID = 0, 1
+CF_FUSE_POOL2 = 1
+FUSED_FWD, FUSED_BWD_WEIGHT = 1, 2
 
 STATUS_NAMES = {0: "CF_OK", 1: "CF_ERR_INVALID_ARG", 2: "CF_ERR_UNSUPPORTED", 3: "CF_ERR_ALIGNMENT",
                 4: "CF_ERR_ALIAS", 5: "CF_ERR_WORKSPACE", 6: "CF_ERR_LAUNCH"}
@@ -30,6 +32,8 @@ EXPORTS = [
     "cf_version", "cf_last_error", "cf_conv3d_out_shape", "cf_conv3d_fwd", "cf_conv3d_bwd_data",
     "cf_conv3d_bwd_weight_workspace_size", "cf_conv3d_bwd_weight", "cf_bias_lrelu_fwd",
     "cf_bias_lrelu_bwd_workspace_size", "cf_bias_lrelu_bwd", "cf_avgpool3d_fwd", "cf_avgpool3d_bwd",
+    "cf_conv3d_fused_supported", "cf_conv3d_mask_bytes", "cf_conv3d_fwd_fused",
+    "cf_conv3d_bwd_weight_fused_workspace_size", "cf_conv3d_bwd_weight_fused",
 ]
 
 
@@ -71,6 +75,11 @@ def lib():
         "cf_bias_lrelu_bwd": ([i64, i32, i32, vp, vp, f32, vp, vp, vp, sz, vp], ctypes.c_int),
         "cf_avgpool3d_fwd": ([i32] * 8 + [vp, vp, vp], ctypes.c_int),
         "cf_avgpool3d_bwd": ([i32] * 8 + [vp, vp, vp], ctypes.c_int),
+        "cf_conv3d_fused_supported": ([D, ctypes.c_uint32], i32),
+        "cf_conv3d_mask_bytes": ([D], sz),
+        "cf_conv3d_fwd_fused": ([D, vp, vp, vp, f32, ctypes.c_uint32, vp, vp, vp], ctypes.c_int),
+        "cf_conv3d_bwd_weight_fused_workspace_size": ([D, ctypes.c_uint32], sz),
+        "cf_conv3d_bwd_weight_fused": ([D, vp, vp, vp, f32, ctypes.c_uint32, vp, vp, vp, sz, vp], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         f = getattr(L, name)
@@ -176,3 +185,27 @@ def cf_avgpool3d_fwd(n, d, h, w, c, k, s, dtype, y, p, stream=None):
 
 def cf_avgpool3d_bwd(n, d, h, w, c, k, s, dtype, dp, dy, stream=None):
     _check(lib().cf_avgpool3d_bwd(n, d, h, w, c, k, s, dtype_code(dtype), _ptr(dp), _ptr(dy), _stream(stream)))
+
+
+def cf_conv3d_fused_supported(desc, flags=CF_FUSE_POOL2) -> int:
+    return int(lib().cf_conv3d_fused_supported(ctypes.byref(desc), flags))
+
+
+def cf_conv3d_mask_bytes(desc) -> int:
+    return int(lib().cf_conv3d_mask_bytes(ctypes.byref(desc)))
+
+
+def cf_conv3d_fwd_fused(desc, x, w, bias, alpha, flags, out, mask, stream=None):
+    _check(lib().cf_conv3d_fwd_fused(ctypes.byref(desc), _ptr(x), _ptr(w), _ptr(bias), alpha, flags, _ptr(out),
+                                     _ptr(mask), _stream(stream)))
+
+
+def cf_conv3d_bwd_weight_fused_workspace_size(desc, flags=CF_FUSE_POOL2) -> int:
+    return int(lib().cf_conv3d_bwd_weight_fused_workspace_size(ctypes.byref(desc), flags))
+
+
+def cf_conv3d_bwd_weight_fused(desc, x, g, mask, alpha, flags, dw, db, ws, ws_bytes=None, stream=None):
+    if ws_bytes is None:
+        ws_bytes = 0 if ws is None or isinstance(ws, int) else ws.numel() * ws.element_size()
+    _check(lib().cf_conv3d_bwd_weight_fused(ctypes.byref(desc), _ptr(x), _ptr(g), _ptr(mask), alpha, flags,
+                                            _ptr(dw), _ptr(db), _ptr(ws), ws_bytes, _stream(stream)))

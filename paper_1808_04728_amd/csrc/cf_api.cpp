@@ -307,4 +307,113 @@ cf_status cf_avgpool3d_bwd(int32_t n, int32_t d, int32_t h, int32_t w, int32_t c
                 st, "cf_avgpool3d_bwd");
 }
 
+// ---------------------------------------------------------------------------
+// Fused layer variants
+// ---------------------------------------------------------------------------
+
+static int32_t fused_mask(const cf::ConvShape &s, uint32_t flags) {
+  int32_t m = 0;
+  if (flags == CF_FUSE_POOL2) {
+    if (cf::smallc_supported(s, true)) m |= 1;
+    if (cf::smallc_wgrad_fused_supported(s)) m |= 2;
+  }
+  return m;
+}
+
+int32_t cf_conv3d_fused_supported(const cf_conv3d_desc *desc, uint32_t flags) {
+  cf::ConvShape s;
+  std::string keep = g_last_error;
+  if (resolve(desc, &s) != CF_OK) {
+    g_last_error = keep;
+    return 0;
+  }
+  return fused_mask(s, flags);
+}
+
+static size_t mask_bytes(const cf::ConvShape &s) {
+  const size_t bits = (size_t)s.n * s.od * s.oh * s.ow * s.co;
+  return (bits + 31) / 32 * 4;
+}
+
+size_t cf_conv3d_mask_bytes(const cf_conv3d_desc *desc) {
+  cf::ConvShape s;
+  std::string keep = g_last_error;
+  if (resolve(desc, &s) != CF_OK) {
+    g_last_error = keep;
+    return 0;
+  }
+  return mask_bytes(s);
+}
+
+cf_status cf_conv3d_fwd_fused(const cf_conv3d_desc *desc, const void *x, const void *w, const float *bias,
+                              float alpha, uint32_t flags, void *out, void *mask, void *stream) {
+  cf::ConvShape s;
+  cf_status r = resolve(desc, &s);
+  if (r != CF_OK) return r;
+  if (!std::isfinite(alpha) || alpha < 0.f) return fail(CF_ERR_INVALID_ARG, "alpha must be finite and >= 0");
+  if (flags & ~CF_FUSE_POOL2) return fail(CF_ERR_INVALID_ARG, "unknown flags");
+  if (!(fused_mask(s, flags) & 1))
+    return fail(CF_ERR_UNSUPPORTED, "conv3d_fwd_fused: no fused kernel for this layer shape / flags");
+  if (s.n == 0) return ok();
+  if ((r = check_ptrs({x, w, out, mask})) != CF_OK) return r;
+  if (!bias) return fail(CF_ERR_INVALID_ARG, "bias is NULL");
+  Sizes b = conv_bytes(s);
+  const size_t ob = b.z / 8;  // pooled output (floor extents are smaller still)
+  const size_t mb = mask_bytes(s);
+  if (overlap(out, ob, x, b.x) || overlap(out, ob, w, b.w) || overlap(mask, mb, x, b.x) ||
+      overlap(mask, mb, w, b.w) || overlap(mask, mb, out, ob) || overlap(bias, (size_t)s.co * 4, out, ob) ||
+      overlap(bias, (size_t)s.co * 4, mask, mb))
+    return fail(CF_ERR_ALIAS, "conv3d_fwd_fused: an output overlaps an input");
+  hipStream_t st = (hipStream_t)stream;
+  return finish(cf::launch_conv_fwd_smallc(s, x, w, bias, alpha, out, (uint16_t *)mask, true, st), st,
+                "cf_conv3d_fwd_fused");
+}
+
+size_t cf_conv3d_bwd_weight_fused_workspace_size(const cf_conv3d_desc *desc, uint32_t flags) {
+  cf::ConvShape s;
+  std::string keep = g_last_error;
+  if (resolve(desc, &s) != CF_OK || !(fused_mask(s, flags) & 2) || s.n == 0) {
+    g_last_error = keep;
+    return 0;
+  }
+  return cf::smallc_wgrad_fused_workspace(s);
+}
+
+cf_status cf_conv3d_bwd_weight_fused(const cf_conv3d_desc *desc, const void *x, const void *g, const void *mask,
+                                     float alpha, uint32_t flags, float *dw, float *db, void *ws, size_t ws_bytes,
+                                     void *stream) {
+  cf::ConvShape s;
+  cf_status r = resolve(desc, &s);
+  if (r != CF_OK) return r;
+  if (!std::isfinite(alpha) || alpha < 0.f) return fail(CF_ERR_INVALID_ARG, "alpha must be finite and >= 0");
+  if (flags & ~CF_FUSE_POOL2) return fail(CF_ERR_INVALID_ARG, "unknown flags");
+  if (!(fused_mask(s, flags) & 2))
+    return fail(CF_ERR_UNSUPPORTED, "conv3d_bwd_weight_fused: no fused kernel for this layer shape / flags");
+  hipStream_t st = (hipStream_t)stream;
+  const size_t dw_bytes = (size_t)s.kd * s.kh * s.kw * s.ci * s.co * sizeof(float);
+  if (s.n == 0) {
+    if ((r = check_ptrs({dw, db})) != CF_OK) return r;
+    hipError_t e = cf::launch_fill_zero(dw, (long long)(dw_bytes / 4), st);
+    if (e == hipSuccess) e = cf::launch_fill_zero(db, s.co, st);
+    return finish(e, st, "cf_conv3d_bwd_weight_fused");
+  }
+  if ((r = check_ptrs({x, g, mask, dw, db})) != CF_OK) return r;
+  const size_t need = cf::smallc_wgrad_fused_workspace(s);
+  if (!ws || ws_bytes < need)
+    return fail(CF_ERR_WORKSPACE, "conv3d_bwd_weight_fused: workspace smaller than the size query");
+  if (!aligned16(ws)) return fail(CF_ERR_ALIGNMENT, "workspace not 16-byte aligned");
+  Sizes b = conv_bytes(s);
+  const size_t gb = b.z / 8, mb = mask_bytes(s), dbb = (size_t)s.co * 4;
+  const void *ins[3] = {x, g, mask};
+  const size_t insz[3] = {b.x, gb, mb};
+  for (int i = 0; i < 3; ++i)
+    if (overlap(dw, dw_bytes, ins[i], insz[i]) || overlap(db, dbb, ins[i], insz[i]) ||
+        overlap(ws, need, ins[i], insz[i]))
+      return fail(CF_ERR_ALIAS, "conv3d_bwd_weight_fused: an output or the workspace overlaps an input");
+  if (overlap(dw, dw_bytes, db, dbb) || overlap(ws, need, dw, dw_bytes) || overlap(ws, need, db, dbb))
+    return fail(CF_ERR_ALIAS, "conv3d_bwd_weight_fused: outputs / workspace overlap");
+  return finish(cf::launch_smallc_wgrad_fused(s, x, g, (const uint16_t *)mask, alpha, dw, db, ws, st), st,
+                "cf_conv3d_bwd_weight_fused");
+}
+
 }  // extern "C"

@@ -22,6 +22,22 @@ struct ConvShape {
   int dtype;             // DT_F32 / DT_BF16
 };
 
+// First-layer (few input channels) kernels, conv_smallc.hip.
+struct SmallcParams {
+  int n, d, h, w, ci, co;
+  int kd, kh, kw, pd, ph, pw;
+  int od, oh, ow;
+  int pod, poh, pow_;   // pooled extents (floor(o/2))
+  int tiles_per_block;  // backward-weights: output tiles folded into one workgroup
+};
+bool smallc_supported(const ConvShape &s, bool fused);
+hipError_t launch_conv_fwd_smallc(const ConvShape &s, const void *x, const void *w, const float *bias,
+                                  float alpha, void *out, uint16_t *mask, bool fused, hipStream_t st);
+bool smallc_wgrad_fused_supported(const ConvShape &s);
+size_t smallc_wgrad_fused_workspace(const ConvShape &s);
+hipError_t launch_smallc_wgrad_fused(const ConvShape &s, const void *x, const void *dp, const uint16_t *mask,
+                                     float alpha, float *dw, float *db, void *ws, hipStream_t st);
+
 hipError_t launch_conv_fwd(const ConvShape &s, const void *x, const void *w, void *z,
                            hipStream_t st);
 hipError_t launch_conv_bwd_data(const ConvShape &s, const void *dz, const void *w, void *dx,

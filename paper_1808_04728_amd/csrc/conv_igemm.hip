@@ -536,6 +536,9 @@ hipError_t dispatch_wgrad(const WgradPlan &pl, const WgradParams &p, const void 
 
 hipError_t launch_conv_fwd(const ConvShape &s, const void *x, const void *w, void *z,
                            hipStream_t st) {
+  // few input channels: the direct halo kernel (one im2col gather per MFMA tile)
+  if (smallc_supported(s, false))
+    return launch_conv_fwd_smallc(s, x, w, nullptr, 0.f, z, nullptr, false, st);
   IgemmParams p{};
   p.nb = s.n;
   p.sd_ = s.d; p.sh_ = s.h; p.sw_ = s.w; p.sc = s.ci;

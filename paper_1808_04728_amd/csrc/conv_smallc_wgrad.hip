@@ -1,0 +1,322 @@
+// conv_smallc_wgrad.hip -- fused backward-weights of the first layer (gfx950).
+//
+// Backward weights (Section III-C) of a few-input-channel layer that was run
+// with the fused forward epilogue (bias + leaky ReLU + 2^3 pool + slope mask):
+// the full-resolution gradient dz is never stored.  Each workgroup rebuilds
+// it tile by tile in LDS from the pooled-output gradient dp and the mask,
+//     dz[v,c] = dp[pool(v),c] / 8 * (mask(v,c) ? 1 : alpha)   (0 off the pool grid)
+// and contracts it with the input halo on MFMA:
+//     dW[(t,ci),co] = sum_v x~[v + t, ci] * dz[v, co]          (K = voxels)
+// The bias gradient db[c] = sum_v dz[v,c] is accumulated in the same pass.
+//
+// MFMA operands need the voxel axis contiguous per lane, so the tile is
+// stored transposed: dz as [co][voxel] (each thread builds an 8-voxel x
+// 8-channel block in registers and writes eight 16-byte rows), and the input
+// halo once per kw shift as [kw][ci][d][h][32 w] so that every tap's 8-voxel
+// run is a 16-byte aligned LDS read.  Each workgroup folds several 4x8x32
+// output tiles into its accumulators and writes one fp32 partial; a second
+// kernel sums the partials in workgroup order (deterministic).
+
+#include "cf_common.h"
+#include "cf_kernels.h"
+
+#include <type_traits>
+
+namespace cf {
+namespace {
+
+constexpr int TD = 4, TH = 8, TW = 32;
+constexpr int TVOX = TD * TH * TW;  // 1024 voxels, 32 w-rows of 32
+constexpr int KMAXE = 3;  // kernel extent limit of the fused path (the first layer is 3^3)
+
+template <int DT, int CIN, int NF>
+struct WgLds {
+  using T = typename Store<DT>::T;
+  static constexpr int COUT = 16 * NF;
+  static constexpr int XS = KMAXE * CIN * (TD + KMAXE - 1) * (TH + KMAXE - 1) * TW;  // shifted halo copies
+  static constexpr int DZ = COUT * TVOX;
+};
+
+template <int DT, int CIN, int NF, int MF>
+__global__ __launch_bounds__(256) void smallc_wgrad_fused_kernel(
+    const typename Store<DT>::T *__restrict__ x, const typename Store<DT>::T *__restrict__ dp,
+    const uint16_t *__restrict__ mask16, float alpha, float *__restrict__ part_w,
+    float *__restrict__ part_b, SmallcParams p) {
+  using T = typename Store<DT>::T;
+  using L = WgLds<DT, CIN, NF>;
+  constexpr int COUT = L::COUT;
+  constexpr bool BF = DT == DT_BF16;
+  // the cross-wave reduction buffer reuses the halo / dz space after the last tile
+  constexpr int RED = 4 * MF * 16 * COUT > 2048 ? 4 * MF * 16 * COUT : 2048;
+  constexpr int STAGE_BYTES = (L::XS + L::DZ) * (int)sizeof(T);
+  constexpr int SMEM = STAGE_BYTES > RED * 4 ? STAGE_BYTES : RED * 4;
+  __shared__ __attribute__((aligned(16))) unsigned char smem[SMEM];
+  T *xs = reinterpret_cast<T *>(smem);
+  T *dzs = xs + L::XS;
+  float *red = reinterpret_cast<float *>(smem);
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r = lane & 15, q = lane >> 4;
+  const int HD = TD + p.kd - 1, HH = TH + p.kh - 1, HWD = TW + p.kw - 1;
+  const int M = p.kd * p.kh * p.kw * CIN;
+  const int tiles_w = (p.ow + TW - 1) / TW, tiles_h = (p.oh + TH - 1) / TH, tiles_d = (p.od + TD - 1) / TD;
+  const int tiles_per_n = tiles_w * tiles_h * tiles_d;
+  const long long total_tiles = (long long)p.n * tiles_per_n;
+
+  // per-lane A offsets (rows = (tap, ci), padded rows read row 0's data)
+  int aoff[MF];
+#pragma unroll
+  for (int mf = 0; mf < MF; ++mf) {
+    int row = mf * 16 + r;
+    if (row >= M) row = 0;
+    int tap = row / CIN, ci = row % CIN;
+    int kd_ = tap / (p.kh * p.kw), kh_ = (tap / p.kw) % p.kh, kw_ = tap % p.kw;
+    aoff[mf] = (((kw_ * CIN + ci) * HD + kd_) * HH + kh_) * TW;
+  }
+
+  f32x4_t acc[MF][NF];
+#pragma unroll
+  for (int i = 0; i < MF; ++i)
+#pragma unroll
+    for (int f = 0; f < NF; ++f) acc[i][f] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  // bias-gradient partials of this thread's dz block: 8 channels
+  float dbs[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) dbs[j] = 0.f;
+
+  // dz staging item of this thread: 8 consecutive voxels of one w-row x 8 channels
+  constexpr int CG = COUT / 8;
+  static_assert(TVOX / 8 * CG >= 256 && (TVOX / 8 * CG) % 256 == 0, "dz items");
+  constexpr int NITEM = TVOX / 8 * CG / 256;
+
+  for (int it = 0; it < p.tiles_per_block; ++it) {
+    const long long gt = (long long)blockIdx.x * p.tiles_per_block + it;
+    if (gt >= total_tiles) break;
+    int t = (int)(gt % tiles_per_n);
+    const int n = (int)(gt / tiles_per_n);
+    const int tw = t % tiles_w; t /= tiles_w;
+    const int th = t % tiles_h;
+    const int td = t / tiles_h;
+    const int od0 = td * TD, oh0 = th * TH, ow0 = tw * TW;
+
+    // ---- stage the input halo, once per kw shift --------------------------
+    const int helems = HD * HH * HWD * CIN;
+    for (int e = tid; e < helems; e += 256) {
+      int ci = e % CIN;
+      int v = e / CIN;
+      int a = v / (HH * HWD), b = (v / HWD) % HH, c = v % HWD;
+      int id = od0 - p.pd + a, ih = oh0 - p.ph + b, iw = ow0 - p.pw + c;
+      T val = from_f32<DT>(0.f);
+      if ((unsigned)id < (unsigned)p.d && (unsigned)ih < (unsigned)p.h && (unsigned)iw < (unsigned)p.w)
+        val = x[((((long long)n * p.d + id) * p.h + ih) * p.w + iw) * CIN + ci];
+      for (int s = 0; s < p.kw; ++s) {
+        int wl = c - s;
+        if (wl >= 0 && wl < TW) xs[(((s * CIN + ci) * HD + a) * HH + b) * TW + wl] = val;
+      }
+    }
+    // ---- rebuild dz = dp/8 * slope(mask) for the tile, transposed ----------
+#pragma unroll
+    for (int i = 0; i < NITEM; ++i) {
+      const int item = tid + 256 * i;
+      const int cg = item % CG;
+      const int vb = item / CG;           // 8-voxel block: row = vb / 4, w8 = vb % 4
+      const int row = vb >> 2, w8 = vb & 3;
+      const int ld = row / TH, lh = row % TH;
+      const int vd = od0 + ld, vh = oh0 + lh, vw0 = ow0 + 8 * w8;
+      float dz[8][8];  // [voxel][channel]
+#pragma unroll
+      for (int a = 0; a < 8; ++a)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) dz[a][j] = 0.f;
+      const int pd_ = vd >> 1, ph_ = vh >> 1;
+      if (vd < p.od && vh < p.oh && pd_ < p.pod && ph_ < p.poh) {
+        const long long vrow = (((long long)n * p.od + vd) * p.oh + vh) * p.ow;
+        const long long prow = (((long long)n * p.pod + pd_) * p.poh + ph_) * p.pow_;
+#pragma unroll
+        for (int pp = 0; pp < 4; ++pp) {  // 4 pooled voxels cover the 8 voxels
+          const int pw_ = (vw0 >> 1) + pp;
+          if (pw_ >= p.pow_) continue;
+          float g[8];
+          if constexpr (BF) {
+            Vec16<DT_BF16> v;
+            v.u = *reinterpret_cast<const uint4 *>(dp + (prow + pw_) * COUT + 8 * cg);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) g[j] = bf2f(v.e[j]) * 0.125f;
+          } else {
+            const float4 *src = reinterpret_cast<const float4 *>(dp + (prow + pw_) * COUT + 8 * cg);
+            float4 v0 = src[0], v1 = src[1];
+            g[0] = v0.x * 0.125f; g[1] = v0.y * 0.125f; g[2] = v0.z * 0.125f; g[3] = v0.w * 0.125f;
+            g[4] = v1.x * 0.125f; g[5] = v1.y * 0.125f; g[6] = v1.z * 0.125f; g[7] = v1.w * 0.125f;
+          }
+#pragma unroll
+          for (int hlf = 0; hlf < 2; ++hlf) {
+            const int a = 2 * pp + hlf;
+            const int vw = vw0 + a;
+            const uint32_t bits = (uint32_t)(mask16[(vrow + vw) * NF + (8 * cg) / 16] >> ((8 * cg) % 16));
+#pragma unroll
+            for (int j = 0; j < 8; ++j) dz[a][j] = g[j] * (((bits >> j) & 1u) ? 1.f : alpha);
+          }
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        Vec16<DT> o[BF ? 1 : 2];
+#pragma unroll
+        for (int a = 0; a < 8; ++a) {
+          dbs[j] += dz[a][j];
+          if constexpr (BF) o[0].e[a] = f2bf(dz[a][j]);
+          else o[a / 4].e[a % 4] = dz[a][j];
+        }
+        T *dst = dzs + (8 * cg + j) * TVOX + row * TW + 8 * w8;
+        if constexpr (BF) {
+          *reinterpret_cast<uint4 *>(dst) = o[0].u;
+        } else {
+          reinterpret_cast<uint4 *>(dst)[0] = o[0].u;
+          reinterpret_cast<uint4 *>(dst)[1] = o[1].u;
+        }
+      }
+    }
+    __syncthreads();
+
+    // ---- MFMA: each wave takes 8 of the tile's 32 w-rows ------------------
+    for (int row = wave; row < TD * TH; row += 4) {
+      const int ld = row / TH, lh = row % TH;
+      const int xrow = (ld * HH + lh) * TW;
+      if constexpr (BF) {
+        bf16x8_t b[NF];
+#pragma unroll
+        for (int f = 0; f < NF; ++f)
+          b[f] = *reinterpret_cast<const bf16x8_t *>(dzs + (16 * f + r) * TVOX + row * TW + 8 * q);
+#pragma unroll
+        for (int mf = 0; mf < MF; ++mf) {
+          bf16x8_t a = *reinterpret_cast<const bf16x8_t *>(xs + aoff[mf] + xrow + 8 * q);
+#pragma unroll
+          for (int f = 0; f < NF; ++f)
+            acc[mf][f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b[f], acc[mf][f], 0, 0, 0);
+        }
+      } else {
+#pragma unroll
+        for (int ks = 0; ks < 8; ++ks) {
+          float b[NF];
+#pragma unroll
+          for (int f = 0; f < NF; ++f) b[f] = dzs[(16 * f + r) * TVOX + row * TW + 4 * ks + q];
+#pragma unroll
+          for (int mf = 0; mf < MF; ++mf) {
+            float a = xs[aoff[mf] + xrow + 4 * ks + q];
+#pragma unroll
+            for (int f = 0; f < NF; ++f)
+              acc[mf][f] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b[f], acc[mf][f], 0, 0, 0);
+          }
+        }
+      }
+    }
+    __syncthreads();
+  }
+
+  // ---- combine the four waves and write this workgroup's partials ---------
+  __syncthreads();
+  // acc[mf][f][j] = dW[row = mf*16 + 4q + j][co = 16f + r]
+#pragma unroll
+  for (int mf = 0; mf < MF; ++mf)
+#pragma unroll
+    for (int f = 0; f < NF; ++f)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        red[((wave * MF + mf) * 16 + 4 * q + j) * COUT + 16 * f + r] = acc[mf][f][j];
+  __syncthreads();
+  const int wsz = MF * 16 * COUT;
+  for (int i = tid; i < M * COUT; i += 256) {
+    float s = red[i] + red[wsz + i] + red[2 * wsz + i] + red[3 * wsz + i];
+    part_w[(long long)blockIdx.x * M * COUT + i] = s;
+  }
+  __syncthreads();
+  // bias partials: thread item cg = tid % CG holds channels 8cg..8cg+7
+  {
+    const int cg = tid % CG;
+    const int slot = tid / CG;  // 256 / CG slots
+#pragma unroll
+    for (int j = 0; j < 8; ++j) red[slot * COUT + 8 * cg + j] = dbs[j];
+  }
+  __syncthreads();
+  if (tid < COUT) {
+    float s = 0.f;
+    for (int k = 0; k < 256 / CG; ++k) s += red[k * COUT + tid];
+    part_b[(long long)blockIdx.x * COUT + tid] = s;
+  }
+}
+
+__global__ __launch_bounds__(256) void sum_rows_kernel(const float *__restrict__ part, float *__restrict__ out,
+                                                       int rows, int cols) {
+  int c = blockIdx.x * 256 + threadIdx.x;
+  if (c >= cols) return;
+  float s = 0.f;
+  for (int k = 0; k < rows; ++k) s += part[(long long)k * cols + c];
+  out[c] = s;
+}
+
+struct WPlan {
+  int tpb;
+  int blocks;
+};
+
+WPlan plan(const ConvShape &s) {
+  const long long tiles = (long long)s.n * ((s.od + TD - 1) / TD) * ((s.oh + TH - 1) / TH) * ((s.ow + TW - 1) / TW);
+  WPlan w;
+  w.tpb = (int)std::max<long long>(1, (tiles + 2047) / 2048);
+  w.blocks = (int)((tiles + w.tpb - 1) / w.tpb);
+  return w;
+}
+
+template <int DT, int CIN, int NF, int MF>
+hipError_t launch_t(const ConvShape &s, const SmallcParams &p, const void *x, const void *dp,
+                    const uint16_t *mask, float alpha, float *dw, float *db, void *ws, int blocks,
+                    hipStream_t st) {
+  using T = typename Store<DT>::T;
+  const int M = s.kd * s.kh * s.kw * s.ci;
+  float *pw = (float *)ws;
+  float *pb = pw + (size_t)blocks * M * s.co;
+  hipLaunchKernelGGL((smallc_wgrad_fused_kernel<DT, CIN, NF, MF>), dim3(blocks), dim3(256), 0, st,
+                     (const T *)x, (const T *)dp, mask, alpha, pw, pb, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(sum_rows_kernel, dim3((M * s.co + 255) / 256), dim3(256), 0, st, pw, dw, blocks, M * s.co);
+  hipLaunchKernelGGL(sum_rows_kernel, dim3((s.co + 255) / 256), dim3(256), 0, st, pb, db, blocks, s.co);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+bool smallc_wgrad_fused_supported(const ConvShape &s) {
+  if (s.sd != 1 || s.sh != 1 || s.sw != 1) return false;
+  if (s.kd > KMAXE || s.kh > KMAXE || s.kw > KMAXE) return false;
+  const int M = s.kd * s.kh * s.kw * s.ci;
+  if (s.co != 16) return false;
+  if (s.dtype == DT_BF16) return (s.ci == 1 && M <= 32) || (s.ci == 4 && M <= 112);
+  return s.ci == 1 && M <= 32;
+}
+
+size_t smallc_wgrad_fused_workspace(const ConvShape &s) {
+  WPlan w = plan(s);
+  const int M = s.kd * s.kh * s.kw * s.ci;
+  return (size_t)w.blocks * (M + 1) * s.co * sizeof(float);
+}
+
+hipError_t launch_smallc_wgrad_fused(const ConvShape &s, const void *x, const void *dp, const uint16_t *mask,
+                                     float alpha, float *dw, float *db, void *ws, hipStream_t st) {
+  WPlan w = plan(s);
+  SmallcParams p{};
+  p.n = s.n; p.d = s.d; p.h = s.h; p.w = s.w; p.ci = s.ci; p.co = s.co;
+  p.kd = s.kd; p.kh = s.kh; p.kw = s.kw; p.pd = s.pd; p.ph = s.ph; p.pw = s.pw;
+  p.od = s.od; p.oh = s.oh; p.ow = s.ow;
+  p.pod = s.od / 2; p.poh = s.oh / 2; p.pow_ = s.ow / 2;
+  p.tiles_per_block = w.tpb;
+  const int M = s.kd * s.kh * s.kw * s.ci;
+  if (s.dtype == DT_BF16) {
+    if (s.ci == 1) return launch_t<DT_BF16, 1, 1, 2>(s, p, x, dp, mask, alpha, dw, db, ws, w.blocks, st);
+    if (M <= 112) return launch_t<DT_BF16, 4, 1, 7>(s, p, x, dp, mask, alpha, dw, db, ws, w.blocks, st);
+    return hipErrorInvalidValue;
+  }
+  return launch_t<DT_F32, 1, 1, 2>(s, p, x, dp, mask, alpha, dw, db, ws, w.blocks, st);
+}
+
+}  // namespace cf

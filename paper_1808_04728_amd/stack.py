@@ -24,7 +24,12 @@ def _t(dtype):
 
 
 class ConvStack:
-    def __init__(self, layers, size, batch, dtype="f32", alpha=0.01, device="cuda", skip_first_dgrad=True):
+    def __init__(self, layers, size, batch, dtype="f32", alpha=0.01, device="cuda", skip_first_dgrad=True,
+                 fused=True):
+        """fused: run a pooled layer through the fused entry points (forward
+        epilogue writes pooled output + slope mask; backward rebuilds dz from
+        them) wherever the library has fused kernels for the layer."""
+        self.fused = fused
         self.layers = layers
         self.batch = batch
         self.dtype = dtype
@@ -52,20 +57,31 @@ class ConvStack:
         dev, tdt, n = self.device, self.tdt, self.batch
         for i, l in enumerate(self.L):
             s = l["spec"]
+            needs_dgrad = i > 0 or not self.skip_first_dgrad
+            sup = B.cf_conv3d_fused_supported(l["desc"], B.CF_FUSE_POOL2) if s["pool"] else 0
+            # fused needs both fused kernels; a layer whose data gradient is needed keeps dz
+            l["fused"] = bool(self.fused and sup == (B.FUSED_FWD | B.FUSED_BWD_WEIGHT) and not needs_dgrad)
             l["w"] = torch.zeros((s["k"],) * 3 + (s["cin"], s["cout"]), dtype=tdt, device=dev)
             l["b"] = torch.zeros(s["cout"], dtype=torch.float32, device=dev)
-            l["z"] = torch.empty((n,) + l["out_dhw"] + (s["cout"],), dtype=tdt, device=dev)  # z, then y in place
             l["p"] = torch.empty((n,) + l["pool_dhw"] + (s["cout"],), dtype=tdt, device=dev) if s["pool"] else None
             l["gout"] = torch.empty((n,) + l["pool_dhw"] + (s["cout"],), dtype=tdt, device=dev)
-            l["dy"] = torch.empty_like(l["z"]) if s["pool"] else None
-            l["dz"] = torch.empty_like(l["z"])
             l["dw"] = torch.empty(l["w"].shape, dtype=torch.float32, device=dev)
             l["db"] = torch.empty(s["cout"], dtype=torch.float32, device=dev)
+            l["dx"] = None
+            if l["fused"]:
+                l["z"] = l["dy"] = l["dz"] = None
+                l["mask"] = torch.empty(max(16, B.cf_conv3d_mask_bytes(l["desc"])), dtype=torch.uint8, device=dev)
+                wsf = B.cf_conv3d_bwd_weight_fused_workspace_size(l["desc"], B.CF_FUSE_POOL2)
+                l["ws_w"] = torch.empty(max(wsf, 16), dtype=torch.uint8, device=dev)
+                l["ws_b"] = None
+                continue
+            l["z"] = torch.empty((n,) + l["out_dhw"] + (s["cout"],), dtype=tdt, device=dev)  # z, then y in place
+            l["dy"] = torch.empty_like(l["z"]) if s["pool"] else None
+            l["dz"] = torch.empty_like(l["z"])
             wsw = B.cf_conv3d_bwd_weight_workspace_size(l["desc"])
             wsb = B.cf_bias_lrelu_bwd_workspace_size(l["nvox"], s["cout"])
             l["ws_w"] = torch.empty(max(wsw, 16), dtype=torch.uint8, device=dev)
             l["ws_b"] = torch.empty(max(wsb, 16), dtype=torch.uint8, device=dev)
-            l["dx"] = None
         for i in range(1, len(self.L)):
             self.L[i]["dx"] = self.L[i - 1]["gout"]
         if not self.skip_first_dgrad:
@@ -103,6 +119,11 @@ class ConvStack:
         for i, l in enumerate(self.L):
             s = l["spec"]
             c = self._call
+            if l["fused"]:
+                c(f"L{i+1}.conv_fwd_fused", B.cf_conv3d_fwd_fused, l["desc"], h, l["w"], l["b"], self.alpha,
+                  B.CF_FUSE_POOL2, l["p"], l["mask"], stream)
+                h = l["p"]
+                continue
             c(f"L{i+1}.conv_fwd", B.cf_conv3d_fwd, l["desc"], h, l["w"], l["z"], stream)
             c(f"L{i+1}.bias_lrelu_fwd", B.cf_bias_lrelu_fwd, l["nvox"], s["cout"], self.dtype, l["z"], l["b"],
               self.alpha, l["z"], stream)
@@ -122,6 +143,10 @@ class ConvStack:
             l = self.L[i]
             s = l["spec"]
             c = self._call
+            if l["fused"]:
+                c(f"L{i+1}.conv_bwd_weight_fused", B.cf_conv3d_bwd_weight_fused, l["desc"], self.layer_input(i), g,
+                  l["mask"], self.alpha, B.CF_FUSE_POOL2, l["dw"], l["db"], l["ws_w"], None, stream)
+                continue
             if s["pool"]:
                 d, hh, w = l["out_dhw"]
                 c(f"L{i+1}.avgpool_bwd", B.cf_avgpool3d_bwd, self.batch, d, hh, w, s["cout"], 2, 2, self.dtype,
@@ -142,6 +167,11 @@ class ConvStack:
             return self.x
         p = self.L[i - 1]
         return p["p"] if p["spec"]["pool"] else p["z"]
+
+    def output_tensors(self, i):
+        """(pooled-or-activated output, y or None) of layer i, for checks."""
+        l = self.L[i]
+        return (l["p"] if l["spec"]["pool"] else l["z"]), l["z"]
 
     def op_flops(self, name):
         """Algorithmic FLOPs of one call of a conv op (2 * MACs), else 0."""
@@ -164,7 +194,9 @@ class ConvStack:
         wb = s["k"] ** 3 * s["cin"] * s["cout"] * es
         pb = zb // 8
         op = name.split(".")[1]
-        return {"conv_fwd": xb + wb + zb, "conv_bwd_data": zb + wb + xb,
+        mb = l["nvox"] * s["cout"] // 8
+        return {"conv_fwd_fused": xb + wb + pb + mb, "conv_bwd_weight_fused": xb + pb + mb + wb // es * 4,
+                "conv_fwd": xb + wb + zb, "conv_bwd_data": zb + wb + xb,
                 "conv_bwd_weight": xb + zb + wb // es * 4, "bias_lrelu_fwd": 2 * zb,
                 "bias_lrelu_bwd": 3 * zb, "avgpool_fwd": zb + pb, "avgpool_bwd": zb + pb}[op]
 
