@@ -335,6 +335,12 @@ static size_t mask_bytes(const cf::ConvShape &s) {
   return (bits + 31) / 32 * 4;
 }
 
+// bytes of the 2^3 stride-2 pooled conv output (floor extents)
+static size_t pooled_bytes(const cf::ConvShape &s) {
+  const size_t es = s.dtype == cf::DT_BF16 ? 2 : 4;
+  return (size_t)s.n * (s.od / 2) * (s.oh / 2) * (s.ow / 2) * s.co * es;
+}
+
 size_t cf_conv3d_mask_bytes(const cf_conv3d_desc *desc) {
   cf::ConvShape s;
   std::string keep = g_last_error;
@@ -358,7 +364,7 @@ cf_status cf_conv3d_fwd_fused(const cf_conv3d_desc *desc, const void *x, const v
   if ((r = check_ptrs({x, w, out, mask})) != CF_OK) return r;
   if (!bias) return fail(CF_ERR_INVALID_ARG, "bias is NULL");
   Sizes b = conv_bytes(s);
-  const size_t ob = b.z / 8;  // pooled output (floor extents are smaller still)
+  const size_t ob = pooled_bytes(s);
   const size_t mb = mask_bytes(s);
   if (overlap(out, ob, x, b.x) || overlap(out, ob, w, b.w) || overlap(mask, mb, x, b.x) ||
       overlap(mask, mb, w, b.w) || overlap(mask, mb, out, ob) || overlap(bias, (size_t)s.co * 4, out, ob) ||
@@ -403,7 +409,7 @@ cf_status cf_conv3d_bwd_weight_fused(const cf_conv3d_desc *desc, const void *x, 
     return fail(CF_ERR_WORKSPACE, "conv3d_bwd_weight_fused: workspace smaller than the size query");
   if (!aligned16(ws)) return fail(CF_ERR_ALIGNMENT, "workspace not 16-byte aligned");
   Sizes b = conv_bytes(s);
-  const size_t gb = b.z / 8, mb = mask_bytes(s), dbb = (size_t)s.co * 4;
+  const size_t gb = pooled_bytes(s), mb = mask_bytes(s), dbb = (size_t)s.co * 4;
   const void *ins[3] = {x, g, mask};
   const size_t insz[3] = {b.x, gb, mb};
   for (int i = 0; i < 3; ++i)

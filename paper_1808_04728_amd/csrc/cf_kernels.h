@@ -52,6 +52,9 @@ size_t bias_lrelu_bwd_workspace(int64_t nvox, int c);
 hipError_t launch_bias_lrelu_bwd(int64_t nvox, int c, int dtype, const void *dy, const void *y,
                                  float alpha, void *dz, float *db, void *ws, hipStream_t st);
 
+// out[c] = sum_{r < rows} part[r * cols + c], in an order fixed by (rows, cols).
+hipError_t launch_sum_rows(const float *part, float *out, int rows, int cols, hipStream_t st);
+
 // out[0..n) = 0 (a fill kernel, never hipMemsetAsync).
 hipError_t launch_fill_zero(float *out, long long n, hipStream_t st);
 

@@ -166,8 +166,11 @@ __global__ __launch_bounds__(256) void conv_igemm_kernel(const typename Store<DT
   // registers holding the next stage
   uint4 a_reg[VECA ? AROWS : 1];
   T a_sreg[VECA ? 1 : BM * BK / 256];
-  constexpr int BELEM = BK * BN / 256;
+  constexpr int BELEM = VECA ? 1 : BK * BN / 256;   // scalar weight path
   T b_reg[BELEM > 0 ? BELEM : 1];
+  constexpr int BSLOTS = BN * (BK / VEC);            // 16-byte weight vectors per stage
+  constexpr int NBV = VECA ? (BSLOTS + 255) / 256 : 1;
+  uint4 b_vreg[NBV];
 
   auto load_stage = [&](int k0) {
     if constexpr (VECA) {
@@ -211,9 +214,33 @@ __global__ __launch_bounds__(256) void conv_igemm_kernel(const typename Store<DT
         a_sreg[i] = v;
       }
     }
-    // weights: element e -> (k = e / BN, n = e % BN)
+    if constexpr (VECA) {
+      // weights, 16-byte vectors.  Forward: W[kk][n..n+VEC) (n contiguous).  Backward-data:
+      // W[tap][n][c..c+VEC) (the K axis, output channels, contiguous).
 #pragma unroll
-    for (int i = 0; i < BELEM; ++i) {
+      for (int i = 0; i < NBV; ++i) {
+        const int slot = tid + 256 * i;
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (slot < BSLOTS) {
+          if constexpr (DGRAD) {
+            const int kk0 = k0 + (slot & 7) * VEC, nn = n0 + (slot >> 3);
+            if (kk0 < p.ktot && nn < p.dc) {
+              int u = kk0 / p.sc, c0 = kk0 - u * p.sc;
+              int ud = u / uhw, uh = (u / p.uw) % p.uh, uw = u % p.uw;
+              int tap = ((p.t0d + p.tsd * ud) * p.kh + (p.t0h + p.tsh * uh)) * p.kw + (p.t0w + p.tsw * uw);
+              v = *reinterpret_cast<const uint4 *>(wt + ((long long)tap * p.wci + nn) * p.wco + c0);
+            }
+          } else {
+            const int kk = k0 + slot / (BN / VEC), nn0 = n0 + (slot % (BN / VEC)) * VEC;
+            if (kk < p.ktot && nn0 < p.dc) v = *reinterpret_cast<const uint4 *>(wt + (long long)kk * p.wco + nn0);
+          }
+        }
+        b_vreg[i] = v;
+      }
+    }
+    // weights, scalar path: element e -> (k = e / BN, n = e % BN)
+#pragma unroll
+    for (int i = 0; i < (VECA ? 0 : BELEM); ++i) {
       int e = tid + 256 * i;
       int kk = k0 + e / BN;
       int nn = n0 + e % BN;
@@ -242,10 +269,27 @@ __global__ __launch_bounds__(256) void conv_igemm_kernel(const typename Store<DT
         a_lds[buf][(e / BK) * LDK + e % BK] = a_sreg[i];
       }
     }
+    if constexpr (VECA) {
 #pragma unroll
-    for (int i = 0; i < BELEM; ++i) {
-      int e = tid + 256 * i;
-      b_lds[buf][(e % BN) * LDK + e / BN] = b_reg[i];
+      for (int i = 0; i < NBV; ++i) {
+        const int slot = tid + 256 * i;
+        if (slot >= BSLOTS) continue;
+        if constexpr (DGRAD) {
+          *reinterpret_cast<uint4 *>(&b_lds[buf][(slot >> 3) * LDK + (slot & 7) * VEC]) = b_vreg[i];
+        } else {
+          Vec16<DT> v;
+          v.u = b_vreg[i];
+          const int kb = slot / (BN / VEC), nb0 = (slot % (BN / VEC)) * VEC;
+#pragma unroll
+          for (int j = 0; j < VEC; ++j) b_lds[buf][(nb0 + j) * LDK + kb] = v.e[j];
+        }
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < BELEM; ++i) {
+        int e = tid + 256 * i;
+        b_lds[buf][(e % BN) * LDK + e / BN] = b_reg[i];
+      }
     }
   };
 
@@ -438,17 +482,6 @@ __global__ __launch_bounds__(256) void conv_wgrad_kernel(const typename Store<DT
     }
 }
 
-// dw[i] = sum_{s < nsplit} part[s][i], in slice order.
-__global__ __launch_bounds__(256) void wgrad_reduce_kernel(const float *__restrict__ part,
-                                                           float *__restrict__ dw, int count,
-                                                           int nsplit) {
-  int i = blockIdx.x * 256 + threadIdx.x;
-  if (i >= count) return;
-  float s = 0.f;
-  for (int k = 0; k < nsplit; ++k) s += part[(long long)k * count + i];
-  dw[i] = s;
-}
-
 // ---------------------------------------------------------------------------
 // Host-side variant selection
 // ---------------------------------------------------------------------------
@@ -458,7 +491,8 @@ hipError_t launch_igemm(const IgemmParams &p, const void *src, const void *w, vo
                         hipStream_t st) {
   using T = typename Store<DT>::T;
   dim3 grid((p.m + BM - 1) / BM, (p.dc + BN - 1) / BN, 1);
-  if (p.sc % Store<DT>::VEC == 0)
+  // vector path: gathered channels and (forward) output channels multiples of the 16-byte vector
+  if (p.sc % Store<DT>::VEC == 0 && (DGRAD || p.dc % Store<DT>::VEC == 0))
     hipLaunchKernelGGL((conv_igemm_kernel<DT, BM, BN, WM, WN, true, DGRAD>), grid, dim3(256), 0, st,
                        (const T *)src, (const T *)w, (T *)dst, p);
   else
@@ -622,10 +656,7 @@ hipError_t launch_conv_bwd_weight(const ConvShape &s, const void *x, const void 
   hipError_t e = s.dtype == DT_BF16 ? dispatch_wgrad<DT_BF16>(pl, p, x, dz, part, st)
                                     : dispatch_wgrad<DT_F32>(pl, p, x, dz, part, st);
   if (e != hipSuccess) return e;
-  const int count = p.m * p.co;
-  hipLaunchKernelGGL(wgrad_reduce_kernel, dim3((count + 255) / 256), dim3(256), 0, st, part, dw,
-                     count, pl.nsplit);
-  return hipGetLastError();
+  return launch_sum_rows(part, dw, pl.nsplit, p.m * p.co, st);
 }
 
 }  // namespace cf

@@ -30,7 +30,7 @@ constexpr int NBLK = (TD / 2) * (TH / 2) * (TW / 4);  // 64 MFMA bricks of 2x2x4
 constexpr int KMAXE = 4;                      // kernel extent limit per dimension
 constexpr int HALO_MAX = (TD + KMAXE - 1) * (TH + KMAXE - 1) * (TW + KMAXE - 1);
 
-template <int DT, int CIN, int NF, bool FUSED>
+template <int DT, int CIN, int NF, int KE, bool FUSED>
 __global__ __launch_bounds__(256) void conv_smallc_fwd_kernel(
     const typename Store<DT>::T *__restrict__ x, const typename Store<DT>::T *__restrict__ w,
     const float *__restrict__ bias, float alpha, typename Store<DT>::T *__restrict__ out,
@@ -49,12 +49,13 @@ __global__ __launch_bounds__(256) void conv_smallc_fwd_kernel(
   const int td = t;
   const int n = blockIdx.y;
   const int od0 = td * TD, oh0 = th * TH, ow0 = tw * TW;
-  const int HD = TD + p.kd - 1, HH = TH + p.kh - 1, HW = TW + p.kw - 1;
-  const int K = p.kd * p.kh * p.kw * CIN;
-  const int ksteps = (K + KPER - 1) / KPER;
+  // cubic kernel of extent KE: every halo / tap index below divides by constants
+  constexpr int HD = TD + KE - 1, HH = TH + KE - 1, HW = TW + KE - 1;
+  constexpr int K = KE * KE * KE * CIN;
+  constexpr int ksteps = (K + KPER - 1) / KPER;
 
   // ---- stage the zero-padded input halo ------------------------------------
-  const int helems = HD * HH * HW * CIN;
+  constexpr int helems = HD * HH * HW * CIN;
   for (int e = tid; e < helems; e += 256) {
     int c = e % CIN;
     int v = e / CIN;
@@ -70,7 +71,7 @@ __global__ __launch_bounds__(256) void conv_smallc_fwd_kernel(
   const int r = lane & 15, q = lane >> 4;
   // brick row r -> voxel (dd, hh, ww) inside the 2x2x4 brick
   const int m_off = (((r >> 3) * HH + ((r >> 2) & 1)) * HW + (r & 3)) * CIN;
-  constexpr int KS_MAX = BF ? 4 : 8;
+  constexpr int KS_MAX = ksteps;
   constexpr int JPER = BF ? 8 : 1;  // K-values per lane per MFMA
   int toff[KS_MAX][JPER];
 #pragma unroll
@@ -81,7 +82,7 @@ __global__ __launch_bounds__(256) void conv_smallc_fwd_kernel(
       int off = 0;
       if (kg < K) {
         int tap = kg / CIN, c = kg % CIN;
-        int a = tap / (p.kh * p.kw), b = (tap / p.kw) % p.kh, cc = tap % p.kw;
+        int a = tap / (KE * KE), b = (tap / KE) % KE, cc = tap % KE;
         off = ((a * HH + b) * HW + cc) * CIN + c;
       }
       toff[ks][j] = off;
@@ -180,24 +181,31 @@ __global__ __launch_bounds__(256) void conv_smallc_fwd_kernel(
   }
 }
 
-template <int DT, int CIN, int NF, bool FUSED>
+template <int DT, int CIN, int NF, int KE, bool FUSED>
 hipError_t launch_t(const SmallcParams &p, const void *x, const void *w, const float *bias, float alpha,
                     void *out, uint16_t *mask, hipStream_t st) {
   using T = typename Store<DT>::T;
+  if constexpr (KE * KE * KE * CIN > (DT == DT_BF16 ? 128 : 32)) {
+    return hipErrorInvalidValue;  // not instantiated: the reduction is too long for this kernel
+  } else {
   const int tiles = ((p.ow + TW - 1) / TW) * ((p.oh + TH - 1) / TH) * ((p.od + TD - 1) / TD);
-  hipLaunchKernelGGL((conv_smallc_fwd_kernel<DT, CIN, NF, FUSED>), dim3(tiles, p.n), dim3(256), 0, st,
+  hipLaunchKernelGGL((conv_smallc_fwd_kernel<DT, CIN, NF, KE, FUSED>), dim3(tiles, p.n), dim3(256), 0, st,
                      (const T *)x, (const T *)w, bias, alpha, (T *)out, mask, p);
   return hipGetLastError();
+  }
 }
 
 template <int DT, bool FUSED>
 hipError_t dispatch(const SmallcParams &p, const void *x, const void *w, const float *bias, float alpha,
                     void *out, uint16_t *mask, hipStream_t st) {
   const int nf = p.co / 16;
-#define CF_SMALLC_CASE(CI, NFV) \
-  if (p.ci == CI && nf == NFV) return launch_t<DT, CI, NFV, FUSED>(p, x, w, bias, alpha, out, mask, st);
-  CF_SMALLC_CASE(1, 1) CF_SMALLC_CASE(1, 2) CF_SMALLC_CASE(2, 1) CF_SMALLC_CASE(4, 1)
-  CF_SMALLC_CASE(4, 2)
+#define CF_SMALLC_CASE(CI, NFV, KEV) \
+  if (p.ci == CI && nf == NFV && p.kd == KEV) return launch_t<DT, CI, NFV, KEV, FUSED>(p, x, w, bias, alpha, out, mask, st);
+#define CF_SMALLC_KE(KEV) \
+  CF_SMALLC_CASE(1, 1, KEV) CF_SMALLC_CASE(1, 2, KEV) CF_SMALLC_CASE(2, 1, KEV) CF_SMALLC_CASE(4, 1, KEV) \
+  CF_SMALLC_CASE(4, 2, KEV)
+  CF_SMALLC_KE(2) CF_SMALLC_KE(3) CF_SMALLC_KE(4)
+#undef CF_SMALLC_KE
 #undef CF_SMALLC_CASE
   return hipErrorInvalidValue;
 }
@@ -206,7 +214,7 @@ hipError_t dispatch(const SmallcParams &p, const void *x, const void *w, const f
 
 bool smallc_supported(const ConvShape &s, bool fused) {
   if (s.sd != 1 || s.sh != 1 || s.sw != 1) return false;
-  if (s.kd > KMAXE || s.kh > KMAXE || s.kw > KMAXE) return false;
+  if (s.kd != s.kh || s.kd != s.kw || s.kd < 2 || s.kd > KMAXE) return false;  // cubic 2^3..4^3
   const int nf = s.co / 16;
   if (s.co % 16 != 0) return false;
   const bool shape_ok = (s.ci == 1 && (nf == 1 || nf == 2)) || (s.ci == 2 && nf == 1) ||

@@ -37,7 +37,7 @@ struct WgLds {
   static constexpr int DZ = COUT * TVOX;
 };
 
-template <int DT, int CIN, int NF, int MF>
+template <int DT, int CIN, int NF, int MF, int KE>
 __global__ __launch_bounds__(256) void smallc_wgrad_fused_kernel(
     const typename Store<DT>::T *__restrict__ x, const typename Store<DT>::T *__restrict__ dp,
     const uint16_t *__restrict__ mask16, float alpha, float *__restrict__ part_w,
@@ -57,8 +57,9 @@ __global__ __launch_bounds__(256) void smallc_wgrad_fused_kernel(
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r = lane & 15, q = lane >> 4;
-  const int HD = TD + p.kd - 1, HH = TH + p.kh - 1, HWD = TW + p.kw - 1;
-  const int M = p.kd * p.kh * p.kw * CIN;
+  // cubic kernel of extent KE: halo and tap indices divide by constants
+  constexpr int HD = TD + KE - 1, HH = TH + KE - 1, HWD = TW + KE - 1;
+  constexpr int M = KE * KE * KE * CIN;
   const int tiles_w = (p.ow + TW - 1) / TW, tiles_h = (p.oh + TH - 1) / TH, tiles_d = (p.od + TD - 1) / TD;
   const int tiles_per_n = tiles_w * tiles_h * tiles_d;
   const long long total_tiles = (long long)p.n * tiles_per_n;
@@ -70,7 +71,7 @@ __global__ __launch_bounds__(256) void smallc_wgrad_fused_kernel(
     int row = mf * 16 + r;
     if (row >= M) row = 0;
     int tap = row / CIN, ci = row % CIN;
-    int kd_ = tap / (p.kh * p.kw), kh_ = (tap / p.kw) % p.kh, kw_ = tap % p.kw;
+    int kd_ = tap / (KE * KE), kh_ = (tap / KE) % KE, kw_ = tap % KE;
     aoff[mf] = (((kw_ * CIN + ci) * HD + kd_) * HH + kh_) * TW;
   }
 
@@ -100,7 +101,7 @@ __global__ __launch_bounds__(256) void smallc_wgrad_fused_kernel(
     const int od0 = td * TD, oh0 = th * TH, ow0 = tw * TW;
 
     // ---- stage the input halo, once per kw shift --------------------------
-    const int helems = HD * HH * HWD * CIN;
+    constexpr int helems = HD * HH * HWD * CIN;
     for (int e = tid; e < helems; e += 256) {
       int ci = e % CIN;
       int v = e / CIN;
@@ -109,7 +110,8 @@ __global__ __launch_bounds__(256) void smallc_wgrad_fused_kernel(
       T val = from_f32<DT>(0.f);
       if ((unsigned)id < (unsigned)p.d && (unsigned)ih < (unsigned)p.h && (unsigned)iw < (unsigned)p.w)
         val = x[((((long long)n * p.d + id) * p.h + ih) * p.w + iw) * CIN + ci];
-      for (int s = 0; s < p.kw; ++s) {
+#pragma unroll
+      for (int s = 0; s < KE; ++s) {
         int wl = c - s;
         if (wl >= 0 && wl < TW) xs[(((s * CIN + ci) * HD + a) * HH + b) * TW + wl] = val;
       }
@@ -245,15 +247,6 @@ __global__ __launch_bounds__(256) void smallc_wgrad_fused_kernel(
   }
 }
 
-__global__ __launch_bounds__(256) void sum_rows_kernel(const float *__restrict__ part, float *__restrict__ out,
-                                                       int rows, int cols) {
-  int c = blockIdx.x * 256 + threadIdx.x;
-  if (c >= cols) return;
-  float s = 0.f;
-  for (int k = 0; k < rows; ++k) s += part[(long long)k * cols + c];
-  out[c] = s;
-}
-
 struct WPlan {
   int tpb;
   int blocks;
@@ -267,7 +260,7 @@ WPlan plan(const ConvShape &s) {
   return w;
 }
 
-template <int DT, int CIN, int NF, int MF>
+template <int DT, int CIN, int NF, int MF, int KE>
 hipError_t launch_t(const ConvShape &s, const SmallcParams &p, const void *x, const void *dp,
                     const uint16_t *mask, float alpha, float *dw, float *db, void *ws, int blocks,
                     hipStream_t st) {
@@ -275,24 +268,23 @@ hipError_t launch_t(const ConvShape &s, const SmallcParams &p, const void *x, co
   const int M = s.kd * s.kh * s.kw * s.ci;
   float *pw = (float *)ws;
   float *pb = pw + (size_t)blocks * M * s.co;
-  hipLaunchKernelGGL((smallc_wgrad_fused_kernel<DT, CIN, NF, MF>), dim3(blocks), dim3(256), 0, st,
+  hipLaunchKernelGGL((smallc_wgrad_fused_kernel<DT, CIN, NF, MF, KE>), dim3(blocks), dim3(256), 0, st,
                      (const T *)x, (const T *)dp, mask, alpha, pw, pb, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(sum_rows_kernel, dim3((M * s.co + 255) / 256), dim3(256), 0, st, pw, dw, blocks, M * s.co);
-  hipLaunchKernelGGL(sum_rows_kernel, dim3((s.co + 255) / 256), dim3(256), 0, st, pb, db, blocks, s.co);
-  return hipGetLastError();
+  e = launch_sum_rows(pw, dw, blocks, M * s.co, st);
+  if (e != hipSuccess) return e;
+  return launch_sum_rows(pb, db, blocks, s.co, st);
 }
 
 }  // namespace
 
 bool smallc_wgrad_fused_supported(const ConvShape &s) {
   if (s.sd != 1 || s.sh != 1 || s.sw != 1) return false;
-  if (s.kd > KMAXE || s.kh > KMAXE || s.kw > KMAXE) return false;
-  const int M = s.kd * s.kh * s.kw * s.ci;
+  if (s.kd != s.kh || s.kd != s.kw || s.kd < 2 || s.kd > KMAXE) return false;  // cubic 2^3 or 3^3
   if (s.co != 16) return false;
-  if (s.dtype == DT_BF16) return (s.ci == 1 && M <= 32) || (s.ci == 4 && M <= 112);
-  return s.ci == 1 && M <= 32;
+  if (s.dtype == DT_BF16) return s.ci == 1 || s.ci == 4;
+  return s.ci == 1;
 }
 
 size_t smallc_wgrad_fused_workspace(const ConvShape &s) {
@@ -311,12 +303,19 @@ hipError_t launch_smallc_wgrad_fused(const ConvShape &s, const void *x, const vo
   p.pod = s.od / 2; p.poh = s.oh / 2; p.pow_ = s.ow / 2;
   p.tiles_per_block = w.tpb;
   const int M = s.kd * s.kh * s.kw * s.ci;
-  if (s.dtype == DT_BF16) {
-    if (s.ci == 1) return launch_t<DT_BF16, 1, 1, 2>(s, p, x, dp, mask, alpha, dw, db, ws, w.blocks, st);
-    if (M <= 112) return launch_t<DT_BF16, 4, 1, 7>(s, p, x, dp, mask, alpha, dw, db, ws, w.blocks, st);
-    return hipErrorInvalidValue;
+  (void)M;
+  if (s.kd == 2) {
+    if (s.dtype == DT_BF16) {
+      if (s.ci == 1) return launch_t<DT_BF16, 1, 1, 1, 2>(s, p, x, dp, mask, alpha, dw, db, ws, w.blocks, st);
+      return launch_t<DT_BF16, 4, 1, 2, 2>(s, p, x, dp, mask, alpha, dw, db, ws, w.blocks, st);
+    }
+    return launch_t<DT_F32, 1, 1, 1, 2>(s, p, x, dp, mask, alpha, dw, db, ws, w.blocks, st);
   }
-  return launch_t<DT_F32, 1, 1, 2>(s, p, x, dp, mask, alpha, dw, db, ws, w.blocks, st);
+  if (s.dtype == DT_BF16) {
+    if (s.ci == 1) return launch_t<DT_BF16, 1, 1, 2, 3>(s, p, x, dp, mask, alpha, dw, db, ws, w.blocks, st);
+    return launch_t<DT_BF16, 4, 1, 7, 3>(s, p, x, dp, mask, alpha, dw, db, ws, w.blocks, st);
+  }
+  return launch_t<DT_F32, 1, 1, 2, 3>(s, p, x, dp, mask, alpha, dw, db, ws, w.blocks, st);
 }
 
 }  // namespace cf

@@ -108,16 +108,6 @@ __global__ __launch_bounds__(256) void bias_lrelu_bwd_kernel(const typename Stor
   }
 }
 
-__global__ __launch_bounds__(256) void column_sum_kernel(const float *__restrict__ part,
-                                                         float *__restrict__ out, int rows,
-                                                         int cols) {
-  int ch = blockIdx.x * 256 + threadIdx.x;
-  if (ch >= cols) return;
-  float acc = 0.f;
-  for (int r = 0; r < rows; ++r) acc += part[(long long)r * cols + ch];
-  out[ch] = acc;
-}
-
 __global__ __launch_bounds__(256) void fill_zero_kernel(float *out, long long n) {
   long long i = (long long)blockIdx.x * 256 + threadIdx.x;
   if (i < n) out[i] = 0.f;
@@ -168,9 +158,7 @@ hipError_t bwd_t(long long nvox, int c, const void *dy, const void *y, float alp
                        (const T *)dy, (const T *)y, alpha, (T *)dz, part, nvox, c, pl.vpb);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !WITH_DB) return e;
-  hipLaunchKernelGGL(column_sum_kernel, dim3((c + 255) / 256), dim3(256), 0, st, part, db,
-                     pl.blocks, c);
-  return hipGetLastError();
+  return launch_sum_rows(part, db, pl.blocks, c, st);
 }
 
 }  // namespace

@@ -145,7 +145,13 @@ def test_fused_matches_unfused_composition(dt):
     wsf = torch.empty(B.cf_conv3d_bwd_weight_fused_workspace_size(desc), dtype=torch.uint8, device="cuda")
     B.cf_conv3d_bwd_weight_fused(desc, x, g, mask, 0.01, B.CF_FUSE_POOL2, dwf, dbf, wsf)
     torch.cuda.synchronize()
-    e = maxabs_err(to_np(dwf), to_np(dw))
-    assert e <= TOL[dt], e
-    e = maxabs_err(to_np(dbf), to_np(db))
-    assert e <= TOL[dt], e
+    # Two valid roundings of the same layer: the unfused path decides the slope
+    # from the bf16-rounded y, the fused one from the fp32 pre-activation, so a
+    # pre-activation within rounding of 0 can take different slopes, moving
+    # single dW entries by ~1/sqrt(voxels) of max|dW|.  Compare normwise.
+    ref, got = to_np(dw), to_np(dwf)
+    e = np.linalg.norm(got - ref) / np.linalg.norm(ref)
+    assert e <= (TOL["f32"] if dt == "f32" else 1e-2), e
+    ref, got = to_np(db), to_np(dbf)
+    e = np.linalg.norm(got - ref) / np.linalg.norm(ref)
+    assert e <= (TOL["f32"] if dt == "f32" else 1e-2), e
