@@ -178,6 +178,7 @@ size_t cf_conv3d_mask_bytes(const cf_conv3d_desc *desc);
  * With CF_FUSE_POOL2: out = avgpool 2^3 stride 2 of y, [n,od/2,oh/2,ow/2,c_out]
  * (floor), summed in fp32 and rounded once; mask (required, see
  * cf_conv3d_mask_bytes) records u > 0 for every conv-output element.
+ * Without it: out = y [n,od,oh,ow,c_out] in dtype, and mask may be NULL.
  * alpha must be finite and >= 0 (then u > 0 <=> y > 0, the slope rule of
  * cf_bias_lrelu_bwd).  Unsupported shapes return CF_ERR_UNSUPPORTED (see
  * cf_conv3d_fused_supported); the unfused calls cover every shape. */

@@ -317,6 +317,7 @@ static int32_t fused_mask(const cf::ConvShape &s, uint32_t flags) {
     if (cf::smallc_supported(s, true)) m |= 1;
     if (cf::smallc_wgrad_fused_supported(s)) m |= 2;
   }
+  if (cf::c16_fwd_supported(s)) m |= 1;  // with or without the pool
   return m;
 }
 
@@ -361,18 +362,25 @@ cf_status cf_conv3d_fwd_fused(const cf_conv3d_desc *desc, const void *x, const v
   if (!(fused_mask(s, flags) & 1))
     return fail(CF_ERR_UNSUPPORTED, "conv3d_fwd_fused: no fused kernel for this layer shape / flags");
   if (s.n == 0) return ok();
-  if ((r = check_ptrs({x, w, out, mask})) != CF_OK) return r;
+  const bool pool = (flags & CF_FUSE_POOL2) != 0;
+  if ((r = check_ptrs({x, w, out})) != CF_OK) return r;
+  if (pool && !mask) return fail(CF_ERR_INVALID_ARG, "conv3d_fwd_fused: the pooled variant needs the mask");
+  if (mask && !aligned16(mask)) return fail(CF_ERR_ALIGNMENT, "mask not 16-byte aligned");
   if (!bias) return fail(CF_ERR_INVALID_ARG, "bias is NULL");
   Sizes b = conv_bytes(s);
-  const size_t ob = pooled_bytes(s);
+  const size_t ob = pool ? pooled_bytes(s) : b.z;
   const size_t mb = mask_bytes(s);
   if (overlap(out, ob, x, b.x) || overlap(out, ob, w, b.w) || overlap(mask, mb, x, b.x) ||
       overlap(mask, mb, w, b.w) || overlap(mask, mb, out, ob) || overlap(bias, (size_t)s.co * 4, out, ob) ||
       overlap(bias, (size_t)s.co * 4, mask, mb))
     return fail(CF_ERR_ALIAS, "conv3d_fwd_fused: an output overlaps an input");
   hipStream_t st = (hipStream_t)stream;
-  return finish(cf::launch_conv_fwd_smallc(s, x, w, bias, alpha, out, (uint16_t *)mask, true, st), st,
-                "cf_conv3d_fwd_fused");
+  hipError_t e;
+  if (pool && cf::smallc_supported(s, true))
+    e = cf::launch_conv_fwd_smallc(s, x, w, bias, alpha, out, (uint16_t *)mask, true, st);
+  else
+    e = cf::launch_conv_fwd_c16(s, x, w, bias, alpha, out, (uint32_t *)mask, pool ? 2 : 1, st);
+  return finish(e, st, "cf_conv3d_fwd_fused");
 }
 
 size_t cf_conv3d_bwd_weight_fused_workspace_size(const cf_conv3d_desc *desc, uint32_t flags) {

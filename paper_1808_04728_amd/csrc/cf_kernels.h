@@ -30,6 +30,18 @@ struct SmallcParams {
   int pod, poh, pow_;   // pooled extents (floor(o/2))
   int tiles_per_block;  // backward-weights: output tiles folded into one workgroup
 };
+// 16 -> 32 channel stride-1 forward (bf16), conv_c16.hip.  epi: 0 store z,
+// 1 bias + lReLU -> y (+ mask if non-null), 2 bias + lReLU + mask + 2^3 pool.
+struct C16Params {
+  int n, d, h, w;
+  int pd, ph, pw;
+  int od, oh, ow;
+  int pod, poh, pow_;
+};
+bool c16_fwd_supported(const ConvShape &s);
+hipError_t launch_conv_fwd_c16(const ConvShape &s, const void *x, const void *w, const float *bias, float alpha,
+                               void *out, uint32_t *mask, int epi, hipStream_t st);
+
 bool smallc_supported(const ConvShape &s, bool fused);
 hipError_t launch_conv_fwd_smallc(const ConvShape &s, const void *x, const void *w, const float *bias,
                                   float alpha, void *out, uint16_t *mask, bool fused, hipStream_t st);

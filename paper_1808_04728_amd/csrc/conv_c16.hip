@@ -1,0 +1,310 @@
+// conv_c16.hip -- 16 -> 32 channel stride-1 3D convolution forward (gfx950, bf16).
+//
+// The second CosmoFlow layer (4^3 taps, 16 -> 32 channels) carries most of
+// the network's convolution FLOPs.  Its forward pass is the direct
+// convolution of Section III-C (Algorithm 1: every output voxel is an inner
+// product over taps and input channels), mapped onto
+// v_mfma_f32_32x32x16_bf16:
+//   A (32 x 16)  = 32 consecutive output voxels along w, one tap, 16 input
+//                  channels -- exactly one voxel row of the input halo;
+//   B (16 x 32)  = the tap's 16 x 32 weight slice;
+//   D (32 x 32)  = those 32 voxels x all 32 output channels.
+// A persistent workgroup (4 waves, one per SIMD) packs the whole weight
+// tensor into LDS once, then loops over 8x4x32-voxel output tiles: it stages
+// the zero-padded input halo of the tile in LDS and each wave computes a
+// 2x4x32 brick (eight 32x32 accumulators).  One A fragment (input row h',
+// shift kw) serves every output row h = h' - kh of the brick, so each LDS
+// read feeds up to k MFMAs.
+//
+// LDS layouts keep every fragment read a contiguous 512-byte run per half
+// wave: halo [d][h][ci/8][w][8 ci], weights [tap][ci/8][co][8 ci].
+//
+// Epilogues: store z; or bias + leaky ReLU + slope mask (+ 2^3 pool).  The
+// 32x32 accumulator layout (lane = output channel, registers = voxels along
+// w in runs of four) puts a whole 2x2x2 pooling window of one channel in one
+// lane, so the pool is register arithmetic.
+//
+// Tiles are handed out XCD-major: workgroup b runs on XCD b % 8, and the
+// eight XCDs own contiguous tile ranges, so halos shared by neighbouring tiles
+// meet in the same L2.
+
+#include "cf_common.h"
+#include "cf_kernels.h"
+
+namespace cf {
+namespace {
+
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+constexpr int TD = 8, TH = 4, TW = 32;  // output tile (voxels); wave brick = 2 x 4 x 32
+
+template <int KE>
+struct C16 {
+  static constexpr int HD = TD + KE - 1, HH = TH + KE - 1, HW = TW + KE - 1;
+  static constexpr int HALO_VEC = HD * HH * 2 * HW;           // 16-byte vectors (8 channels)
+  static constexpr int TAPS = KE * KE * KE;
+  static constexpr int W_VEC = TAPS * 2 * 32;                 // [tap][ci/8][co] x 8 ci
+  static constexpr int LDS_BYTES = (HALO_VEC + W_VEC) * 16;
+};
+
+template <int KE, int EPI>
+__global__ __launch_bounds__(256, 1) void conv_c16_fwd_kernel(const uint16_t *__restrict__ x,
+                                                              const uint16_t *__restrict__ w,
+                                                              const float *__restrict__ bias, float alpha,
+                                                              uint16_t *__restrict__ out,
+                                                              uint32_t *__restrict__ mask, C16Params p) {
+  using G = C16<KE>;
+  extern __shared__ __attribute__((aligned(16))) uint4 smem[];
+  uint4 *halo = smem;                 // [HD][HH][2][HW]
+  uint4 *wp = smem + G::HALO_VEC;     // [TAPS][2][32]
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int col = lane & 31, half = lane >> 5;
+
+  // ---- pack W[tap][ci][co] into [tap][ci/8][co][8 ci] once ---------------
+  // item = (tap, ci, 8-channel group of co): one 16-byte load, eight 2-byte LDS stores
+  {
+    constexpr int ITEMS = G::TAPS * 16 * 4;
+    constexpr int PER = (ITEMS + 255) / 256;
+    uint4 wv[PER];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int e = tid + 256 * k;
+      wv[k] = e < ITEMS ? *reinterpret_cast<const uint4 *>(w + (long long)e * 8) : make_uint4(0, 0, 0, 0);
+    }
+    uint16_t *wp16 = reinterpret_cast<uint16_t *>(wp);
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int e = tid + 256 * k;
+      if (e >= ITEMS) continue;
+      const int cg = e & 3, ci = (e >> 2) & 15, tap = e >> 6;
+      Vec16<DT_BF16> v;
+      v.u = wv[k];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) wp16[(((tap * 2 + (ci >> 3)) * 32) + 8 * cg + j) * 8 + (ci & 7)] = v.e[j];
+    }
+  }
+
+  const int tiles_w = (p.ow + TW - 1) / TW, tiles_h = (p.oh + TH - 1) / TH, tiles_d = (p.od + TD - 1) / TD;
+  const int tiles = p.n * tiles_d * tiles_h * tiles_w;
+  // XCD-major tile order: XCD x owns tiles [x*per, (x+1)*per)
+  const int nblk = gridDim.x;
+  const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3, per_xcd_blocks = (nblk + 7) >> 3;
+  const int per = (tiles + 7) >> 3;
+  float bz = 0.f;
+  if constexpr (EPI != 0) bz = bias[col];
+
+  // The next tile's halo is fetched into registers while the current tile
+  // computes (global loads in flight across the MFMA loop).
+  constexpr int NPRE = (G::HALO_VEC + 255) / 256;
+  uint4 pre[NPRE];
+  auto fetch = [&](int t) {
+    int r = t;
+    const int tw = r % tiles_w; r /= tiles_w;
+    const int th = r % tiles_h; r /= tiles_h;
+    const int td = r % tiles_d;
+    const int n = r / tiles_d;
+    const int od0 = td * TD, oh0 = th * TH, ow0 = tw * TW;
+#pragma unroll
+    for (int k = 0; k < NPRE; ++k) {
+      const int e = tid + 256 * k;
+      const int hf = e & 1;
+      int v = e >> 1;
+      const int hw = v % G::HW; v /= G::HW;
+      const int hh = v % G::HH;
+      const int hd = v / G::HH;
+      const int id = od0 - p.pd + hd, ih = oh0 - p.ph + hh, iw = ow0 - p.pw + hw;
+      uint4 val = make_uint4(0, 0, 0, 0);
+      if (e < G::HALO_VEC && (unsigned)id < (unsigned)p.d && (unsigned)ih < (unsigned)p.h &&
+          (unsigned)iw < (unsigned)p.w)
+        val = *reinterpret_cast<const uint4 *>(x + ((((long long)n * p.d + id) * p.h + ih) * p.w + iw) * 16 + 8 * hf);
+      pre[k] = val;
+    }
+  };
+  auto tile_of = [&](int i) { return xcd * per + i; };
+  if (slot < per && tile_of(slot) < tiles) fetch(tile_of(slot));
+
+  for (int i = slot;; i += per_xcd_blocks) {
+    const int t = tile_of(i);
+    if (i >= per || t >= tiles) break;
+    int r = t;
+    const int tw = r % tiles_w; r /= tiles_w;
+    const int th = r % tiles_h; r /= tiles_h;
+    const int td = r % tiles_d;
+    const int n = r / tiles_d;
+    const int od0 = td * TD, oh0 = th * TH, ow0 = tw * TW;
+
+    __syncthreads();  // previous tile's fragment reads are done (and the packed weights visible)
+#pragma unroll
+    for (int k = 0; k < NPRE; ++k) {
+      const int e = tid + 256 * k;
+      if (e >= G::HALO_VEC) continue;
+      const int hf = e & 1;
+      int v = e >> 1;
+      const int hw = v % G::HW; v /= G::HW;
+      const int hh = v % G::HH;
+      const int hd = v / G::HH;
+      halo[((hd * G::HH + hh) * 2 + hf) * G::HW + hw] = pre[k];
+    }
+    __syncthreads();
+    {
+      const int inext = i + per_xcd_blocks;
+      if (inext < per && tile_of(inext) < tiles) fetch(tile_of(inext));
+    }
+
+    // ---- 2 x 4 x 32 brick of this wave ------------------------------------
+    f32x16_t acc[2][TH];
+#pragma unroll
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+      for (int b = 0; b < TH; ++b)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) acc[a][b][j] = 0.f;
+
+    for (int kd = 0; kd < KE; ++kd) {
+#pragma unroll
+      for (int kw = 0; kw < KE; ++kw) {
+        bf16x8_t bfr[KE];
+#pragma unroll
+        for (int kh = 0; kh < KE; ++kh)
+          bfr[kh] = __builtin_bit_cast(bf16x8_t, wp[(((kd * KE + kh) * KE + kw) * 2 + half) * 32 + col]);
+#pragma unroll
+        for (int dd = 0; dd < 2; ++dd) {
+#pragma unroll
+          for (int hi = 0; hi < TH + KE - 1; ++hi) {
+            const bf16x8_t a = __builtin_bit_cast(
+                bf16x8_t, halo[(((2 * wave + dd + kd) * G::HH + hi) * 2 + half) * G::HW + kw + col]);
+#pragma unroll
+            for (int kh = 0; kh < KE; ++kh) {
+              const int hrow = hi - kh;
+              if (hrow >= 0 && hrow < TH)
+                acc[dd][hrow] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bfr[kh], acc[dd][hrow], 0, 0, 0);
+            }
+          }
+        }
+      }
+    }
+
+    // ---- epilogue ----------------------------------------------------------
+    // acc[dd][h][j]: channel col, voxel w = ow0 + 8*(j/4) + 4*half + (j%4)
+    const int vd0 = od0 + 2 * wave;
+    if constexpr (EPI == 0) {
+#pragma unroll
+      for (int dd = 0; dd < 2; ++dd)
+#pragma unroll
+        for (int hh = 0; hh < TH; ++hh) {
+          const int vd = vd0 + dd, vh = oh0 + hh;
+          if (vd >= p.od || vh >= p.oh) continue;
+          const long long rowv = (((long long)n * p.od + vd) * p.oh + vh) * p.ow;
+#pragma unroll
+          for (int j = 0; j < 16; ++j) {
+            const int vw = ow0 + 8 * (j >> 2) + 4 * half + (j & 3);
+            if (vw < p.ow) out[(rowv + vw) * 32 + col] = f2bf(acc[dd][hh][j]);
+          }
+        }
+    } else {
+      // u = acc + b; mask word per voxel (32 channel bits); y = lrelu(u)
+#pragma unroll
+      for (int dd = 0; dd < 2; ++dd)
+#pragma unroll
+        for (int hh = 0; hh < TH; ++hh) {
+          const int vd = vd0 + dd, vh = oh0 + hh;
+          uint32_t word = 0;
+#pragma unroll
+          for (int j = 0; j < 16; ++j) {
+            const float u = acc[dd][hh][j] + bz;
+            const unsigned long long bal = __ballot(u > 0.f);
+            // lane j holds the voxel of half 0, lane 32 + j the voxel of half 1
+            if (lane == j) word = (uint32_t)bal;
+            if (lane == 32 + j) word = (uint32_t)(bal >> 32);
+            acc[dd][hh][j] = u > 0.f ? u : alpha * u;
+          }
+          if (mask != nullptr && col < 16 && vd < p.od && vh < p.oh) {
+            const int vw = ow0 + 8 * (col >> 2) + 4 * half + (col & 3);
+            if (vw < p.ow) mask[(((long long)n * p.od + vd) * p.oh + vh) * p.ow + vw] = word;
+          }
+        }
+      if constexpr (EPI == 1) {  // y, no pool
+#pragma unroll
+        for (int dd = 0; dd < 2; ++dd)
+#pragma unroll
+          for (int hh = 0; hh < TH; ++hh) {
+            const int vd = vd0 + dd, vh = oh0 + hh;
+            if (vd >= p.od || vh >= p.oh) continue;
+            const long long rowv = (((long long)n * p.od + vd) * p.oh + vh) * p.ow;
+#pragma unroll
+            for (int j = 0; j < 16; ++j) {
+              const int vw = ow0 + 8 * (j >> 2) + 4 * half + (j & 3);
+              if (vw < p.ow) out[(rowv + vw) * 32 + col] = f2bf(acc[dd][hh][j]);
+            }
+          }
+      } else {  // 2^3 average pool: window = (dd 0..1) x (h pair) x (w pair), all in this lane
+        const int pd_ = vd0 >> 1;
+#pragma unroll
+        for (int hp = 0; hp < TH / 2; ++hp) {
+          const int ph_ = (oh0 >> 1) + hp;
+          if (pd_ >= p.pod || ph_ >= p.poh) continue;
+          const long long prow = (((long long)n * p.pod + pd_) * p.poh + ph_) * p.pow_;
+#pragma unroll
+          for (int j = 0; j < 16; j += 2) {
+            float s = 0.f;
+#pragma unroll
+            for (int dd = 0; dd < 2; ++dd)
+#pragma unroll
+              for (int hh = 0; hh < 2; ++hh) s += acc[dd][2 * hp + hh][j] + acc[dd][2 * hp + hh][j + 1];
+            const int pw_ = (ow0 >> 1) + 4 * (j >> 2) + 2 * half + ((j & 3) >> 1);
+            if (pw_ < p.pow_) out[(prow + pw_) * 32 + col] = f2bf(s * 0.125f);
+          }
+        }
+      }
+    }
+  }
+}
+
+template <int KE, int EPI>
+hipError_t launch_t(const C16Params &p, const void *x, const void *w, const float *bias, float alpha, void *out,
+                    uint32_t *mask, hipStream_t st) {
+  using G = C16<KE>;
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute((const void *)conv_c16_fwd_kernel<KE, EPI>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, G::LDS_BYTES);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  int dev = 0, cus = 256;
+  if (hipGetDevice(&dev) == hipSuccess) hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  const long long tiles = (long long)p.n * ((p.od + TD - 1) / TD) * ((p.oh + TH - 1) / TH) * ((p.ow + TW - 1) / TW);
+  int blocks = (int)std::min<long long>(tiles, cus);
+  blocks = std::max(8, (blocks + 7) / 8 * 8);
+  hipLaunchKernelGGL((conv_c16_fwd_kernel<KE, EPI>), dim3(blocks), dim3(256), G::LDS_BYTES, st,
+                     (const uint16_t *)x, (const uint16_t *)w, bias, alpha, (uint16_t *)out, mask, p);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+bool c16_fwd_supported(const ConvShape &s) {
+  return s.dtype == DT_BF16 && s.ci == 16 && s.co == 32 && s.sd == 1 && s.sh == 1 && s.sw == 1 &&
+         s.kd == s.kh && s.kd == s.kw && s.kd >= 2 && s.kd <= 4;
+}
+
+hipError_t launch_conv_fwd_c16(const ConvShape &s, const void *x, const void *w, const float *bias, float alpha,
+                               void *out, uint32_t *mask, int epi, hipStream_t st) {
+  C16Params p{};
+  p.n = s.n; p.d = s.d; p.h = s.h; p.w = s.w;
+  p.pd = s.pd; p.ph = s.ph; p.pw = s.pw;
+  p.od = s.od; p.oh = s.oh; p.ow = s.ow;
+  p.pod = s.od / 2; p.poh = s.oh / 2; p.pow_ = s.ow / 2;
+#define CF_C16_CASE(KEV)                                                                      \
+  if (s.kd == KEV) {                                                                          \
+    if (epi == 0) return launch_t<KEV, 0>(p, x, w, bias, alpha, out, mask, st);               \
+    if (epi == 1) return launch_t<KEV, 1>(p, x, w, bias, alpha, out, mask, st);               \
+    return launch_t<KEV, 2>(p, x, w, bias, alpha, out, mask, st);                             \
+  }
+  CF_C16_CASE(2) CF_C16_CASE(3) CF_C16_CASE(4)
+#undef CF_C16_CASE
+  return hipErrorInvalidValue;
+}
+
+}  // namespace cf

@@ -573,6 +573,8 @@ hipError_t launch_conv_fwd(const ConvShape &s, const void *x, const void *w, voi
   // few input channels: the direct halo kernel (one im2col gather per MFMA tile)
   if (smallc_supported(s, false))
     return launch_conv_fwd_smallc(s, x, w, nullptr, 0.f, z, nullptr, false, st);
+  // 16 -> 32 channels, stride 1: halo-tiled MFMA kernel with weights resident in LDS
+  if (c16_fwd_supported(s)) return launch_conv_fwd_c16(s, x, w, nullptr, 0.f, z, nullptr, 0, st);
   IgemmParams p{};
   p.nb = s.n;
   p.sd_ = s.d; p.sh_ = s.h; p.sw_ = s.w; p.sc = s.ci;

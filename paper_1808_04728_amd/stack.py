@@ -61,6 +61,8 @@ class ConvStack:
             sup = B.cf_conv3d_fused_supported(l["desc"], B.CF_FUSE_POOL2) if s["pool"] else 0
             # fused needs both fused kernels; a layer whose data gradient is needed keeps dz
             l["fused"] = bool(self.fused and sup == (B.FUSED_FWD | B.FUSED_BWD_WEIGHT) and not needs_dgrad)
+            # otherwise conv + bias + leaky ReLU may still share one kernel (y written once)
+            l["fused_act"] = bool(self.fused and not l["fused"] and B.cf_conv3d_fused_supported(l["desc"], 0) & 1)
             l["w"] = torch.zeros((s["k"],) * 3 + (s["cin"], s["cout"]), dtype=tdt, device=dev)
             l["b"] = torch.zeros(s["cout"], dtype=torch.float32, device=dev)
             l["p"] = torch.empty((n,) + l["pool_dhw"] + (s["cout"],), dtype=tdt, device=dev) if s["pool"] else None
@@ -124,9 +126,13 @@ class ConvStack:
                   B.CF_FUSE_POOL2, l["p"], l["mask"], stream)
                 h = l["p"]
                 continue
-            c(f"L{i+1}.conv_fwd", B.cf_conv3d_fwd, l["desc"], h, l["w"], l["z"], stream)
-            c(f"L{i+1}.bias_lrelu_fwd", B.cf_bias_lrelu_fwd, l["nvox"], s["cout"], self.dtype, l["z"], l["b"],
-              self.alpha, l["z"], stream)
+            if l["fused_act"]:
+                c(f"L{i+1}.conv_bias_lrelu_fwd", B.cf_conv3d_fwd_fused, l["desc"], h, l["w"], l["b"], self.alpha, 0,
+                  l["z"], None, stream)
+            else:
+                c(f"L{i+1}.conv_fwd", B.cf_conv3d_fwd, l["desc"], h, l["w"], l["z"], stream)
+                c(f"L{i+1}.bias_lrelu_fwd", B.cf_bias_lrelu_fwd, l["nvox"], s["cout"], self.dtype, l["z"], l["b"],
+                  self.alpha, l["z"], stream)
             if s["pool"]:
                 d, hh, w = l["out_dhw"]
                 c(f"L{i+1}.avgpool_fwd", B.cf_avgpool3d_fwd, self.batch, d, hh, w, s["cout"], 2, 2, self.dtype,
@@ -196,6 +202,7 @@ class ConvStack:
         op = name.split(".")[1]
         mb = l["nvox"] * s["cout"] // 8
         return {"conv_fwd_fused": xb + wb + pb + mb, "conv_bwd_weight_fused": xb + pb + mb + wb // es * 4,
+                "conv_bias_lrelu_fwd": xb + wb + zb,
                 "conv_fwd": xb + wb + zb, "conv_bwd_data": zb + wb + xb,
                 "conv_bwd_weight": xb + zb + wb // es * 4, "bias_lrelu_fwd": 2 * zb,
                 "bias_lrelu_bwd": 3 * zb, "avgpool_fwd": zb + pb, "avgpool_bwd": zb + pb}[op]

@@ -28,7 +28,40 @@ FWD_CASES = [
     (1, (9, 8, 34), 1, 32, 3),       # 32 output channels
     (1, (8, 9, 10), 2, 16, 2),       # even kernel, asymmetric SAME
     (1, (8, 8, 36), 1, 16, 4),
+    (1, (16, 12, 64), 16, 32, 4),    # the second CosmoFlow layer: 16 -> 32, 4^3
+    (2, (9, 7, 33), 16, 32, 4),      # ragged tiles in every dimension
+    (1, (10, 10, 40), 16, 32, 3),
+    (1, (10, 10, 10), 16, 32, 2),
 ]
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("case", FWD_CASES, ids=lambda c: "n%d_%dx%dx%d_c%d-%d_k%d" % (c[0], *c[1], *c[2:]))
+def test_fused_fwd_no_pool(case, dt):
+    """conv + bias + leaky ReLU in one kernel (y written once, optional mask)."""
+    N, dhw, CI, CO, k = case
+    desc = B.make_desc(N, dhw, CI, CO, k, 1, "same", dt)
+    if not B.cf_conv3d_fused_supported(desc, 0) & B.FUSED_FWD:
+        pytest.skip("no fused forward kernel without pooling for this shape")
+    rng = np.random.default_rng(14)
+    x = dev(rng.standard_normal((N, *dhw, CI)), dt)
+    w = dev(rng.standard_normal((k, k, k, CI, CO)) * np.sqrt(2.0 / (k ** 3 * CI)), dt)
+    b = torch.as_tensor(rng.standard_normal(CO) * 0.1, dtype=torch.float32, device="cuda")
+    od = B.cf_conv3d_out_shape(desc)
+    y = torch.full((N, *od, CO), float("nan"), dtype=tdtype(dt), device="cuda")
+    mask = torch.zeros(B.cf_conv3d_mask_bytes(desc), dtype=torch.uint8, device="cuda")
+    B.cf_conv3d_fwd_fused(desc, x, w, b, 0.2, 0, y, mask)
+    y2 = torch.full_like(y, float("nan"))
+    B.cf_conv3d_fwd_fused(desc, x, w, b, 0.2, 0, y2, None)
+    torch.cuda.synchronize()
+    z = oracle.conv3d_fwd(to_np(x), to_np(w))
+    u = z + to_np(b)
+    e = maxabs_err(to_np(y), oracle.bias_lrelu_fwd(z, to_np(b), 0.2))
+    assert e <= TOL[dt], e
+    assert torch.equal(y, y2)
+    bits = unpack_mask(mask, u.size).reshape(u.shape)
+    decided = np.abs(u) > 1e-5 * np.abs(u).max()
+    assert np.array_equal(bits[decided], (u > 0)[decided])
 
 
 def unpack_mask(m, count):
