@@ -165,8 +165,8 @@ cf_status cf_avgpool3d_bwd(int32_t n, int32_t d, int32_t h, int32_t w, int32_t c
 #define CF_FUSE_POOL2 1u /* a 2^3 stride-2 average pool follows the activation */
 
 /* Bitmask of the fused entry points that accept (desc, flags) on this build:
- * 1 = cf_conv3d_fwd_fused, 2 = cf_conv3d_bwd_weight_fused.  Host-only; 0 on
- * an invalid desc. */
+ * 1 = cf_conv3d_fwd_fused, 2 = cf_conv3d_bwd_weight_fused,
+ * 4 = cf_conv3d_bwd_data_fused.  Host-only; 0 on an invalid desc. */
 int32_t cf_conv3d_fused_supported(const cf_conv3d_desc *desc, uint32_t flags);
 
 /* Bytes of the slope mask of a layer: one bit per element of the conv output
@@ -201,6 +201,15 @@ size_t cf_conv3d_bwd_weight_fused_workspace_size(const cf_conv3d_desc *desc, uin
 cf_status cf_conv3d_bwd_weight_fused(const cf_conv3d_desc *desc, const void *x, const void *g,
                                      const void *mask, float alpha, uint32_t flags, float *dw,
                                      float *db, void *ws, size_t ws_bytes, void *stream);
+
+/* Fused backward-data (CF_FUSE_POOL2 required): dz is rebuilt from the
+ * pooled-output gradient g and the slope mask exactly as in
+ * cf_conv3d_bwd_weight_fused (rounded to the path dtype), then
+ *   dx[n,i,ci] = sum over (o,t) with o*s + t - pad_before = i of sum_co dz[n,o,co] * W[t,ci,co].
+ * dx [n,d,h,w,c_in] in dtype; every element is written. */
+cf_status cf_conv3d_bwd_data_fused(const cf_conv3d_desc *desc, const void *g, const void *mask,
+                                   const void *w, float alpha, uint32_t flags, void *dx,
+                                   void *stream);
 
 #ifdef __cplusplus
 }

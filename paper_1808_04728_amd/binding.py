@@ -33,7 +33,7 @@ EXPORTS = [
     "cf_conv3d_bwd_weight_workspace_size", "cf_conv3d_bwd_weight", "cf_bias_lrelu_fwd",
     "cf_bias_lrelu_bwd_workspace_size", "cf_bias_lrelu_bwd", "cf_avgpool3d_fwd", "cf_avgpool3d_bwd",
     "cf_conv3d_fused_supported", "cf_conv3d_mask_bytes", "cf_conv3d_fwd_fused",
-    "cf_conv3d_bwd_weight_fused_workspace_size", "cf_conv3d_bwd_weight_fused",
+    "cf_conv3d_bwd_weight_fused_workspace_size", "cf_conv3d_bwd_weight_fused", "cf_conv3d_bwd_data_fused",
 ]
 
 
@@ -80,6 +80,7 @@ def lib():
         "cf_conv3d_fwd_fused": ([D, vp, vp, vp, f32, ctypes.c_uint32, vp, vp, vp], ctypes.c_int),
         "cf_conv3d_bwd_weight_fused_workspace_size": ([D, ctypes.c_uint32], sz),
         "cf_conv3d_bwd_weight_fused": ([D, vp, vp, vp, f32, ctypes.c_uint32, vp, vp, vp, sz, vp], ctypes.c_int),
+        "cf_conv3d_bwd_data_fused": ([D, vp, vp, vp, f32, ctypes.c_uint32, vp, vp], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         f = getattr(L, name)

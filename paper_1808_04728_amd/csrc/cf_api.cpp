@@ -318,6 +318,7 @@ static int32_t fused_mask(const cf::ConvShape &s, uint32_t flags) {
     if (cf::smallc_wgrad_fused_supported(s)) m |= 2;
   }
   if (cf::c16_fwd_supported(s)) m |= 1;  // with or without the pool
+  if (flags == CF_FUSE_POOL2 && cf::c16_bwd_supported(s)) m |= 4;
   return m;
 }
 
@@ -428,6 +429,25 @@ cf_status cf_conv3d_bwd_weight_fused(const cf_conv3d_desc *desc, const void *x, 
     return fail(CF_ERR_ALIAS, "conv3d_bwd_weight_fused: outputs / workspace overlap");
   return finish(cf::launch_smallc_wgrad_fused(s, x, g, (const uint16_t *)mask, alpha, dw, db, ws, st), st,
                 "cf_conv3d_bwd_weight_fused");
+}
+
+cf_status cf_conv3d_bwd_data_fused(const cf_conv3d_desc *desc, const void *g, const void *mask, const void *w,
+                                   float alpha, uint32_t flags, void *dx, void *stream) {
+  cf::ConvShape s;
+  cf_status r = resolve(desc, &s);
+  if (r != CF_OK) return r;
+  if (!std::isfinite(alpha) || alpha < 0.f) return fail(CF_ERR_INVALID_ARG, "alpha must be finite and >= 0");
+  if (flags & ~CF_FUSE_POOL2) return fail(CF_ERR_INVALID_ARG, "unknown flags");
+  if (!(fused_mask(s, flags) & 4))
+    return fail(CF_ERR_UNSUPPORTED, "conv3d_bwd_data_fused: no fused kernel for this layer shape / flags");
+  if (s.n == 0) return ok();
+  if ((r = check_ptrs({g, mask, w, dx})) != CF_OK) return r;
+  Sizes b = conv_bytes(s);
+  if (overlap(dx, b.x, g, pooled_bytes(s)) || overlap(dx, b.x, mask, mask_bytes(s)) || overlap(dx, b.x, w, b.w))
+    return fail(CF_ERR_ALIAS, "conv3d_bwd_data_fused: dx overlaps an input");
+  hipStream_t st = (hipStream_t)stream;
+  return finish(cf::launch_conv_bwd_data_c16(s, g, (const uint32_t *)mask, w, alpha, dx, true, st), st,
+                "cf_conv3d_bwd_data_fused");
 }
 
 }  // extern "C"

@@ -39,6 +39,11 @@ struct C16Params {
   int pod, poh, pow_;
 };
 bool c16_fwd_supported(const ConvShape &s);
+// backward data of the same layers (conv_c16_bwd.hip); fused: g is the pooled-output
+// gradient and mask the forward's slope mask, else g is dz
+bool c16_bwd_supported(const ConvShape &s);
+hipError_t launch_conv_bwd_data_c16(const ConvShape &s, const void *g, const uint32_t *mask, const void *w,
+                                    float alpha, void *dx, bool fused, hipStream_t st);
 hipError_t launch_conv_fwd_c16(const ConvShape &s, const void *x, const void *w, const float *bias, float alpha,
                                void *out, uint32_t *mask, int epi, hipStream_t st);
 

@@ -164,21 +164,28 @@ __global__ __launch_bounds__(256, 1) void conv_c16_fwd_kernel(const uint16_t *__
     for (int kd = 0; kd < KE; ++kd) {
 #pragma unroll
       for (int kw = 0; kw < KE; ++kw) {
+        // issue every fragment read of this (kd, kw) step first, so LDS latency
+        // overlaps the MFMA chain (one wave per SIMD: nothing else hides it)
         bf16x8_t bfr[KE];
+        bf16x8_t afr[2][TH + KE - 1];
 #pragma unroll
         for (int kh = 0; kh < KE; ++kh)
           bfr[kh] = __builtin_bit_cast(bf16x8_t, wp[(((kd * KE + kh) * KE + kw) * 2 + half) * 32 + col]);
 #pragma unroll
+        for (int dd = 0; dd < 2; ++dd)
+#pragma unroll
+          for (int hi = 0; hi < TH + KE - 1; ++hi)
+            afr[dd][hi] = __builtin_bit_cast(
+                bf16x8_t, halo[(((2 * wave + dd + kd) * G::HH + hi) * 2 + half) * G::HW + kw + col]);
+#pragma unroll
         for (int dd = 0; dd < 2; ++dd) {
 #pragma unroll
           for (int hi = 0; hi < TH + KE - 1; ++hi) {
-            const bf16x8_t a = __builtin_bit_cast(
-                bf16x8_t, halo[(((2 * wave + dd + kd) * G::HH + hi) * 2 + half) * G::HW + kw + col]);
 #pragma unroll
             for (int kh = 0; kh < KE; ++kh) {
               const int hrow = hi - kh;
               if (hrow >= 0 && hrow < TH)
-                acc[dd][hrow] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, bfr[kh], acc[dd][hrow], 0, 0, 0);
+                acc[dd][hrow] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(afr[dd][hi], bfr[kh], acc[dd][hrow], 0, 0, 0);
             }
           }
         }

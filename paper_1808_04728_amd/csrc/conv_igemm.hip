@@ -597,6 +597,7 @@ hipError_t launch_conv_fwd(const ConvShape &s, const void *x, const void *w, voi
 
 hipError_t launch_conv_bwd_data(const ConvShape &s, const void *dz, const void *w, void *dx,
                                 hipStream_t st) {
+  if (c16_bwd_supported(s)) return launch_conv_bwd_data_c16(s, dz, nullptr, w, 0.f, dx, false, st);
   // one launch per parity class (r_d, r_h, r_w) of input voxels
   for (int rd = 0; rd < s.sd; ++rd)
     for (int rh = 0; rh < s.sh; ++rh)
