@@ -22,7 +22,7 @@ CF_OK, CF_ERR_INVALID_ARG, CF_ERR_UNSUPPORTED, CF_ERR_ALIGNMENT, CF_ERR_ALIAS, \
 CF_F32, CF_BF16 = 0, 1
 CF_PAD_SAME_TF, CF_PAD_VALID = 0, 1
 CF_FUSE_POOL2 = 1
-FUSED_FWD, FUSED_BWD_WEIGHT = 1, 2
+FUSED_FWD, FUSED_BWD_WEIGHT, FUSED_BWD_DATA = 1, 2, 4
 
 STATUS_NAMES = {0: "CF_OK", 1: "CF_ERR_INVALID_ARG", 2: "CF_ERR_UNSUPPORTED", 3: "CF_ERR_ALIGNMENT",
                 4: "CF_ERR_ALIAS", 5: "CF_ERR_WORKSPACE", 6: "CF_ERR_LAUNCH"}
@@ -210,3 +210,8 @@ def cf_conv3d_bwd_weight_fused(desc, x, g, mask, alpha, flags, dw, db, ws, ws_by
         ws_bytes = 0 if ws is None or isinstance(ws, int) else ws.numel() * ws.element_size()
     _check(lib().cf_conv3d_bwd_weight_fused(ctypes.byref(desc), _ptr(x), _ptr(g), _ptr(mask), alpha, flags,
                                             _ptr(dw), _ptr(db), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def cf_conv3d_bwd_data_fused(desc, g, mask, w, alpha, flags, dx, stream=None):
+    _check(lib().cf_conv3d_bwd_data_fused(ctypes.byref(desc), _ptr(g), _ptr(mask), _ptr(w), alpha, flags, _ptr(dx),
+                                          _stream(stream)))

@@ -188,3 +188,31 @@ def test_fused_matches_unfused_composition(dt):
     ref, got = to_np(db), to_np(dbf)
     e = np.linalg.norm(got - ref) / np.linalg.norm(ref)
     assert e <= (TOL["f32"] if dt == "f32" else 1e-2), e
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("case", FWD_CASES, ids=lambda c: "n%d_%dx%dx%d_c%d-%d_k%d" % (c[0], *c[1], *c[2:]))
+def test_fused_bwd_data(case, dt):
+    """dx from the pooled-output gradient and the mask, teacher-forced."""
+    N, dhw, CI, CO, k = case
+    desc = B.make_desc(N, dhw, CI, CO, k, 1, "same", dt)
+    if not B.cf_conv3d_fused_supported(desc) & B.FUSED_BWD_DATA:
+        pytest.skip("no fused backward-data kernel for this shape")
+    rng = np.random.default_rng(15)
+    od = B.cf_conv3d_out_shape(desc)
+    pdhw = tuple(t // 2 for t in od)
+    g = dev(rng.standard_normal((N, *pdhw, CO)), dt)
+    w = dev(rng.standard_normal((k, k, k, CI, CO)) / np.sqrt(k ** 3 * CO), dt)
+    mbytes = B.cf_conv3d_mask_bytes(desc)
+    mask_np = rng.integers(0, 256, mbytes, dtype=np.uint8)
+    mask = torch.as_tensor(mask_np, device="cuda")
+    alpha = 0.2
+    dx = torch.full((N, *dhw, CI), float("nan"), dtype=tdtype(dt), device="cuda")
+    B.cf_conv3d_bwd_data_fused(desc, g, mask, w, alpha, B.CF_FUSE_POOL2, dx)
+    torch.cuda.synchronize()
+    nbits = N * od[0] * od[1] * od[2] * CO
+    bits = np.unpackbits(mask_np, bitorder="little")[:nbits].astype(bool).reshape((N, *od, CO))
+    dz = oracle.avgpool3d_bwd(to_np(g), od) * np.where(bits, 1.0, alpha)
+    ref = oracle.conv3d_bwd_data(dz, to_np(w), dhw)
+    e = maxabs_err(to_np(dx), ref)
+    assert e <= TOL[dt], e
