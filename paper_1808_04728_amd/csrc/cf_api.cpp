@@ -315,7 +315,7 @@ static int32_t fused_mask(const cf::ConvShape &s, uint32_t flags) {
   int32_t m = 0;
   if (flags == CF_FUSE_POOL2) {
     if (cf::smallc_supported(s, true)) m |= 1;
-    if (cf::smallc_wgrad_fused_supported(s)) m |= 2;
+    if (cf::smallc_wgrad_fused_supported(s) || cf::c16_wgrad_supported(s)) m |= 2;
   }
   if (cf::c16_fwd_supported(s)) m |= 1;  // with or without the pool
   if (flags == CF_FUSE_POOL2 && cf::c16_bwd_supported(s)) m |= 4;
@@ -335,6 +335,10 @@ int32_t cf_conv3d_fused_supported(const cf_conv3d_desc *desc, uint32_t flags) {
 static size_t mask_bytes(const cf::ConvShape &s) {
   const size_t bits = (size_t)s.n * s.od * s.oh * s.ow * s.co;
   return (bits + 31) / 32 * 4;
+}
+
+static size_t fused_wgrad_workspace(const cf::ConvShape &s) {
+  return cf::smallc_wgrad_fused_supported(s) ? cf::smallc_wgrad_fused_workspace(s) : cf::c16_wgrad_workspace(s);
 }
 
 // bytes of the 2^3 stride-2 pooled conv output (floor extents)
@@ -391,7 +395,7 @@ size_t cf_conv3d_bwd_weight_fused_workspace_size(const cf_conv3d_desc *desc, uin
     g_last_error = keep;
     return 0;
   }
-  return cf::smallc_wgrad_fused_workspace(s);
+  return fused_wgrad_workspace(s);
 }
 
 cf_status cf_conv3d_bwd_weight_fused(const cf_conv3d_desc *desc, const void *x, const void *g, const void *mask,
@@ -413,7 +417,7 @@ cf_status cf_conv3d_bwd_weight_fused(const cf_conv3d_desc *desc, const void *x, 
     return finish(e, st, "cf_conv3d_bwd_weight_fused");
   }
   if ((r = check_ptrs({x, g, mask, dw, db})) != CF_OK) return r;
-  const size_t need = cf::smallc_wgrad_fused_workspace(s);
+  const size_t need = fused_wgrad_workspace(s);
   if (!ws || ws_bytes < need)
     return fail(CF_ERR_WORKSPACE, "conv3d_bwd_weight_fused: workspace smaller than the size query");
   if (!aligned16(ws)) return fail(CF_ERR_ALIGNMENT, "workspace not 16-byte aligned");
@@ -427,7 +431,11 @@ cf_status cf_conv3d_bwd_weight_fused(const cf_conv3d_desc *desc, const void *x, 
       return fail(CF_ERR_ALIAS, "conv3d_bwd_weight_fused: an output or the workspace overlaps an input");
   if (overlap(dw, dw_bytes, db, dbb) || overlap(ws, need, dw, dw_bytes) || overlap(ws, need, db, dbb))
     return fail(CF_ERR_ALIAS, "conv3d_bwd_weight_fused: outputs / workspace overlap");
-  return finish(cf::launch_smallc_wgrad_fused(s, x, g, (const uint16_t *)mask, alpha, dw, db, ws, st), st,
+  const hipError_t e =
+      cf::smallc_wgrad_fused_supported(s)
+          ? cf::launch_smallc_wgrad_fused(s, x, g, (const uint16_t *)mask, alpha, dw, db, ws, st)
+          : cf::launch_conv_bwd_weight_c16(s, x, g, (const uint32_t *)mask, alpha, dw, db, ws, true, st);
+  return finish(e,  st,
                 "cf_conv3d_bwd_weight_fused");
 }
 

@@ -1,0 +1,304 @@
+// conv_c16_wgrad.hip -- backward weights of the 16 -> 32 channel 4^3 stride-1 layer (gfx950, bf16).
+//
+// Backward weights (Section III-C) is a convolution with a long reduction
+// over voxels and a small output: dW[t, ci, co] = sum_v x~[v + t, ci] dz[v, co].
+// On v_mfma_f32_16x16x32_bf16 one instruction is one tap:
+//   A (16 x 32) = 16 input channels x 32 consecutive voxels of the input halo
+//                 shifted by the tap,
+//   B (32 x 16) = the same 32 voxels of dz x 16 output channels,
+//   D (16 x 16) += dW[tap][ci][co-block].
+// Both operands need 8 consecutive voxels per lane while the tensors are
+// channels-innermost (NDHWC).  The tiles are therefore kept in LDS in their
+// natural layout and read with ds_read_b64_tr_b16, the gfx950 transposing
+// LDS load: inside each 16-lane group, lane 4a+b receives element b of the
+// 4-element rows addressed by lanes a, a+4, a+8, a+12.  Pointing lane r of
+// the group at (voxel r/4 + 4t, channels 4(r%4) .. +3) and issuing t = 0, 1
+// hands lane i channel i of 8 consecutive voxels -- any voxel offset, so the
+// tap shift along w costs nothing.
+//
+// Work split: wave w owns the 16 taps with kd = w (all kh, kw, both 16-wide
+// output-channel blocks: 32 accumulators); a persistent workgroup loops over
+// 2x4x32-voxel dz tiles, staging the tile and its input halo in LDS, and in
+// every (d-row, kw) step reuses one A fragment (input row h') for the k taps
+// kh that reach dz rows h = h' - kh.  Each workgroup writes its fp32 partial
+// dW once; a second kernel sums the partials in workgroup order.
+//
+// Fused variant: dz is rebuilt from the pooled-output gradient and the slope
+// mask while staging (rounded to bf16 as the unfused path stores it), and the
+// bias gradient is summed from the unrounded values in the same pass.
+
+#include "cf_common.h"
+#include "cf_kernels.h"
+
+namespace cf {
+namespace {
+
+typedef short v4i16_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16_t lds_v4i16_t;
+
+constexpr int KE = 4;
+constexpr int TD = 2, TH = 4, TW = 32;
+constexpr int HD = TD + KE - 1, HH = TH + KE - 1, HW = TW + KE - 1;
+constexpr int XH_VEC = HD * HH * HW * 2;    // 16-byte units of the input halo (16 ci = 2 units)
+constexpr int DZ_VEC = TD * TH * TW * 4;    // 16-byte units of the dz tile (32 co = 4 units)
+constexpr int DB_VEC = 256 * 2;             // fused: per-thread running bias sums (8 floats)
+constexpr int LDS_BYTES = (XH_VEC + DZ_VEC + DB_VEC) * 16;
+constexpr int NX = (XH_VEC + 255) / 256, NZ = DZ_VEC / 256;
+static_assert(DZ_VEC % 256 == 0, "dz staging");
+
+// two transposing reads -> 8 consecutive voxels of one channel per lane
+__device__ __forceinline__ bf16x8_t tr_frag(const uint16_t *lds, int e0, int e1) {
+  const v4i16_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t *)(lds + e0));
+  const v4i16_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t *)(lds + e1));
+  typedef short v8i16_t __attribute__((ext_vector_type(8)));
+  const v8i16_t v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  return __builtin_bit_cast(bf16x8_t, v);
+}
+
+template <bool FUSED>
+__global__ __launch_bounds__(256, 2) void c16_wgrad_kernel(const uint16_t *__restrict__ x,
+                                                           const uint16_t *__restrict__ g,
+                                                           const uint32_t *__restrict__ mask, float alpha,
+                                                           float *__restrict__ part_w, float *__restrict__ part_b,
+                                                           C16Params p) {
+  extern __shared__ __attribute__((aligned(16))) uint4 smem[];
+  uint4 *xh = smem;                 // [HD][HH][HW][2 x 8 ci]
+  uint4 *dzt = smem + XH_VEC;       // [TD][TH][TW][4 x 8 co]
+  const uint16_t *xh16 = reinterpret_cast<const uint16_t *>(xh);
+  const uint16_t *dz16 = reinterpret_cast<const uint16_t *>(dzt);
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r16 = lane & 15, q = lane >> 4;
+  // transposing-read row of this lane: voxel r16/4 (+4 for the second read), channel group r16%4
+  const int trv = r16 >> 2, trc = 4 * (r16 & 3);
+
+  const int tiles_w = (p.ow + TW - 1) / TW, tiles_h = (p.oh + TH - 1) / TH, tiles_d = (p.od + TD - 1) / TD;
+  const int tiles = p.n * tiles_d * tiles_h * tiles_w;
+  const int nblk = gridDim.x;
+  const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3, per_xcd_blocks = (nblk + 7) >> 3;
+  const int per = (tiles + 7) >> 3;
+
+  f32x4_t acc[KE][KE][2];  // [kh][kw][co block]
+#pragma unroll
+  for (int a = 0; a < KE; ++a)
+#pragma unroll
+    for (int b = 0; b < KE; ++b)
+#pragma unroll
+      for (int c = 0; c < 2; ++c) acc[a][b][c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  // fused: running bias-gradient sums of this thread's 8 staged channels live in
+  // LDS between tiles, so they hold no registers across the MFMA section
+  float4 *dbl = reinterpret_cast<float4 *>(smem + XH_VEC + DZ_VEC) + 2 * tid;
+  if constexpr (FUSED) {
+    dbl[0] = make_float4(0.f, 0.f, 0.f, 0.f);
+    dbl[1] = make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+
+  for (int i = slot;; i += per_xcd_blocks) {
+    const int t = xcd * per + i;
+    if (i >= per || t >= tiles) break;
+    int r = t;
+    const int tw = r % tiles_w; r /= tiles_w;
+    const int th = r % tiles_h; r /= tiles_h;
+    const int td = r % tiles_d;
+    const int n = r / tiles_d;
+    const int o0d = td * TD, o0h = th * TH, o0w = tw * TW;
+
+    __syncthreads();
+    // ---- stage the input halo and the dz tile (all loads in flight first) ----
+    uint4 xv[NX];
+#pragma unroll
+    for (int k = 0; k < NX; ++k) {
+      const int e = tid + 256 * k;
+      const int hf = e & 1;
+      int v = e >> 1;
+      const int hw = v % HW; v /= HW;
+      const int hh = v % HH;
+      const int hd = v / HH;
+      const int id = o0d - p.pd + hd, ih = o0h - p.ph + hh, iw = o0w - p.pw + hw;
+      uint4 val = make_uint4(0, 0, 0, 0);
+      if (e < XH_VEC && (unsigned)id < (unsigned)p.d && (unsigned)ih < (unsigned)p.h && (unsigned)iw < (unsigned)p.w)
+        val = *reinterpret_cast<const uint4 *>(x + ((((long long)n * p.d + id) * p.h + ih) * p.w + iw) * 16 + 8 * hf);
+      xv[k] = val;
+    }
+    if constexpr (FUSED) {  // the dz rebuild needs registers: retire the halo first
+#pragma unroll
+      for (int k = 0; k < NX; ++k) {
+        const int e = tid + 256 * k;
+        if (e < XH_VEC) xh[e] = xv[k];
+      }
+    }
+    float dbs[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) dbs[j] = 0.f;
+#pragma unroll
+    for (int k = 0; k < NZ; ++k) {
+      const int e = tid + 256 * k;  // e & 3: which 8 of the 32 channels (fixed per thread)
+      const int cq = e & 3;
+      int v = e >> 2;
+      const int lw = v % TW; v /= TW;
+      const int lh = v % TH;
+      const int ld = v / TH;
+      const int od = o0d + ld, oh = o0h + lh, ow = o0w + lw;
+      uint4 val = make_uint4(0, 0, 0, 0);
+      if (od < p.od && oh < p.oh && ow < p.ow) {
+        const long long vox = (((long long)n * p.od + od) * p.oh + oh) * p.ow + ow;
+        if constexpr (!FUSED) {
+          val = *reinterpret_cast<const uint4 *>(g + vox * 32 + 8 * cq);
+        } else {
+          const int pd_ = od >> 1, ph_ = oh >> 1, pw_ = ow >> 1;
+          if (pd_ < p.pod && ph_ < p.poh && pw_ < p.pow_) {
+            Vec16<DT_BF16> gv;
+            gv.u = *reinterpret_cast<const uint4 *>(
+                g + ((((long long)n * p.pod + pd_) * p.poh + ph_) * p.pow_ + pw_) * 32 + 8 * cq);
+            const uint32_t bits = mask[vox] >> (8 * cq);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+              const float d = bf2f(gv.e[j]) * 0.125f * (((bits >> j) & 1u) ? 1.f : alpha);
+              dbs[j] += d;
+              gv.e[j] = f2bf(d);
+            }
+            val = gv.u;
+          }
+        }
+      }
+      dzt[tid + 256 * k] = val;  // the tile region is free: every read of it ended at the barrier above
+    }
+    if constexpr (FUSED) {
+      float4 a = dbl[0], b = dbl[1];
+      a.x += dbs[0]; a.y += dbs[1]; a.z += dbs[2]; a.w += dbs[3];
+      b.x += dbs[4]; b.y += dbs[5]; b.z += dbs[6]; b.w += dbs[7];
+      dbl[0] = a;
+      dbl[1] = b;
+    }
+    if constexpr (!FUSED) {
+#pragma unroll
+      for (int k = 0; k < NX; ++k) {
+        const int e = tid + 256 * k;
+        if (e < XH_VEC) xh[e] = xv[k];  // unit e is already the [hd][hh][hw][half] layout
+      }
+    }
+    __syncthreads();
+
+    // ---- MFMA: taps kd = wave; reuse A (input row h') over kh ----------------
+    if (wave < KE) {
+#pragma unroll 1
+      for (int ld = 0; ld < TD; ++ld) {
+        bf16x8_t bfr[TH][2];
+#pragma unroll
+        for (int hh = 0; hh < TH; ++hh)
+#pragma unroll
+          for (int nf = 0; nf < 2; ++nf) {
+            const int e0 = (((ld * TH + hh) * TW + 8 * q + trv) * 32) + 16 * nf + trc;
+            bfr[hh][nf] = tr_frag(dz16, e0, e0 + 4 * 32);
+          }
+#pragma unroll
+        for (int kw = 0; kw < KE; ++kw) {
+          // input rows h' stream through a two-deep register pipeline: the next
+          // row's transposing reads are in flight while this row's MFMAs issue
+          auto arow = [&](int hi) {
+            const int e0 = ((((ld + wave) * HH + hi) * HW + 8 * q + trv + kw) * 16) + trc;
+            return tr_frag(xh16, e0, e0 + 4 * 16);
+          };
+          bf16x8_t a_cur = arow(0), a_nxt = a_cur;
+#pragma unroll
+          for (int hi = 0; hi < TH + KE - 1; ++hi) {
+            if (hi + 1 < TH + KE - 1) a_nxt = arow(hi + 1);
+#pragma unroll
+            for (int kh = 0; kh < KE; ++kh) {
+              const int hrow = hi - kh;
+              if (hrow >= 0 && hrow < TH) {
+                acc[kh][kw][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_cur, bfr[hrow][0], acc[kh][kw][0], 0, 0, 0);
+                acc[kh][kw][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a_cur, bfr[hrow][1], acc[kh][kw][1], 0, 0, 0);
+              }
+            }
+            a_cur = a_nxt;
+          }
+        }
+      }
+    }
+  }
+
+  // ---- this workgroup's partials: D lane = co (16 nf + r16), rows 4q + j = ci ----
+  if (wave < KE) {
+    float *pw = part_w + (long long)blockIdx.x * (KE * KE * KE * 16 * 32);
+#pragma unroll
+    for (int kh = 0; kh < KE; ++kh)
+#pragma unroll
+      for (int kw = 0; kw < KE; ++kw) {
+        const int tap = (wave * KE + kh) * KE + kw;
+#pragma unroll
+        for (int nf = 0; nf < 2; ++nf)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) pw[(tap * 16 + 4 * q + j) * 32 + 16 * nf + r16] = acc[kh][kw][nf][j];
+      }
+  }
+  if constexpr (FUSED) {
+    // thread's channels: 8 * ((tid) & 3) .. +7 (staging unit e & 3 == tid & 3)
+    // slot of thread u holds channels 8 (u & 3) .. +7: sum the 64 threads of each group in order
+    __syncthreads();
+    const float *red = reinterpret_cast<const float *>(smem + XH_VEC + DZ_VEC);
+    if (tid < 32) {
+      float s = 0.f;
+      for (int k = 0; k < 64; ++k) s += red[(4 * k + (tid >> 3)) * 8 + (tid & 7)];
+      part_b[(long long)blockIdx.x * 32 + tid] = s;
+    }
+  }
+}
+
+int wgrad_blocks(const C16Params &p) {
+  int dev = 0, cus = 256;
+  if (hipGetDevice(&dev) == hipSuccess) hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+  const long long tiles = (long long)p.n * ((p.od + TD - 1) / TD) * ((p.oh + TH - 1) / TH) * ((p.ow + TW - 1) / TW);
+  int blocks = (int)std::min<long long>(tiles, 2LL * cus);
+  return std::max(8, (blocks + 7) / 8 * 8);
+}
+
+template <bool FUSED>
+hipError_t launch_w(const C16Params &p, const void *x, const void *g, const uint32_t *mask, float alpha, float *pw,
+                    float *pb, int blocks, hipStream_t st) {
+  static bool attr_set = false;
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute((const void *)c16_wgrad_kernel<FUSED>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, LDS_BYTES);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  hipLaunchKernelGGL((c16_wgrad_kernel<FUSED>), dim3(blocks), dim3(256), LDS_BYTES, st, (const uint16_t *)x,
+                     (const uint16_t *)g, mask, alpha, pw, pb, p);
+  return hipGetLastError();
+}
+
+C16Params params_of(const ConvShape &s) {
+  C16Params p{};
+  p.n = s.n; p.d = s.d; p.h = s.h; p.w = s.w;
+  p.pd = s.pd; p.ph = s.ph; p.pw = s.pw;
+  p.od = s.od; p.oh = s.oh; p.ow = s.ow;
+  p.pod = s.od / 2; p.poh = s.oh / 2; p.pow_ = s.ow / 2;
+  return p;
+}
+
+}  // namespace
+
+bool c16_wgrad_supported(const ConvShape &s) { return c16_fwd_supported(s) && s.kd == KE; }
+
+size_t c16_wgrad_workspace(const ConvShape &s) {
+  const int blocks = wgrad_blocks(params_of(s));
+  return (size_t)blocks * (KE * KE * KE * 16 * 32 + 32) * sizeof(float);
+}
+
+hipError_t launch_conv_bwd_weight_c16(const ConvShape &s, const void *x, const void *g, const uint32_t *mask,
+                                      float alpha, float *dw, float *db, void *ws, bool fused, hipStream_t st) {
+  const C16Params p = params_of(s);
+  const int blocks = wgrad_blocks(p);
+  const int cols = KE * KE * KE * 16 * 32;
+  float *pw = (float *)ws;
+  float *pb = pw + (size_t)blocks * cols;
+  hipError_t e = fused ? launch_w<true>(p, x, g, mask, alpha, pw, pb, blocks, st)
+                       : launch_w<false>(p, x, g, mask, alpha, pw, pb, blocks, st);
+  if (e != hipSuccess) return e;
+  e = launch_sum_rows(pw, dw, blocks, cols, st);
+  if (e != hipSuccess || !fused) return e;
+  return launch_sum_rows(pb, db, blocks, 32, st);
+}
+
+}  // namespace cf

@@ -60,7 +60,8 @@ class ConvStack:
             needs_dgrad = i > 0 or not self.skip_first_dgrad
             sup = B.cf_conv3d_fused_supported(l["desc"], B.CF_FUSE_POOL2) if s["pool"] else 0
             # fused needs both fused kernels; a layer whose data gradient is needed keeps dz
-            l["fused"] = bool(self.fused and sup == (B.FUSED_FWD | B.FUSED_BWD_WEIGHT) and not needs_dgrad)
+            both = B.FUSED_FWD | B.FUSED_BWD_WEIGHT
+            l["fused"] = bool(self.fused and (sup & both) == both and (not needs_dgrad or sup & B.FUSED_BWD_DATA))
             # otherwise conv + bias + leaky ReLU may still share one kernel (y written once)
             l["fused_act"] = bool(self.fused and not l["fused"] and B.cf_conv3d_fused_supported(l["desc"], 0) & 1)
             l["w"] = torch.zeros((s["k"],) * 3 + (s["cin"], s["cout"]), dtype=tdt, device=dev)
@@ -152,6 +153,10 @@ class ConvStack:
             if l["fused"]:
                 c(f"L{i+1}.conv_bwd_weight_fused", B.cf_conv3d_bwd_weight_fused, l["desc"], self.layer_input(i), g,
                   l["mask"], self.alpha, B.CF_FUSE_POOL2, l["dw"], l["db"], l["ws_w"], None, stream)
+                if l["dx"] is not None:
+                    c(f"L{i+1}.conv_bwd_data_fused", B.cf_conv3d_bwd_data_fused, l["desc"], g, l["mask"], l["w"],
+                      self.alpha, B.CF_FUSE_POOL2, l["dx"], stream)
+                    g = l["dx"]
                 continue
             if s["pool"]:
                 d, hh, w = l["out_dhw"]
@@ -202,6 +207,7 @@ class ConvStack:
         op = name.split(".")[1]
         mb = l["nvox"] * s["cout"] // 8
         return {"conv_fwd_fused": xb + wb + pb + mb, "conv_bwd_weight_fused": xb + pb + mb + wb // es * 4,
+                "conv_bwd_data_fused": pb + mb + wb + xb,
                 "conv_bias_lrelu_fwd": xb + wb + zb,
                 "conv_fwd": xb + wb + zb, "conv_bwd_data": zb + wb + xb,
                 "conv_bwd_weight": xb + zb + wb // es * 4, "bias_lrelu_fwd": 2 * zb,
