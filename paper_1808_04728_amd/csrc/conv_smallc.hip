@@ -58,16 +58,25 @@ __global__ __launch_bounds__(256) void conv_smallc_fwd_kernel(
   const int n = blockIdx.y;
   const int od0 = td * TD, oh0 = th * TH, ow0 = tw * TW;
 
-  // ---- stage the zero-padded input halo ------------------------------------
-  for (int e = tid; e < HALO; e += 256) {
-    const int c = e % CIN;
-    const int v = e / CIN;
-    const int a = v / (HH * HW), b = (v / HW) % HH, cc = v % HW;
-    const int id = od0 - p.pd + a, ih = oh0 - p.ph + b, iw = ow0 - p.pw + cc;
-    T val = from_f32<DT>(0.f);
-    if ((unsigned)id < (unsigned)p.d && (unsigned)ih < (unsigned)p.h && (unsigned)iw < (unsigned)p.w)
-      val = x[((((long long)n * p.d + id) * p.h + ih) * p.w + iw) * CIN + c];
-    halo[e] = val;
+  // ---- stage the zero-padded input halo: every load in flight before any store
+  {
+    constexpr int NL = (HALO + 255) / 256;
+    T hv[NL];
+#pragma unroll
+    for (int k = 0; k < NL; ++k) {
+      const int e = tid + 256 * k;
+      const int c = e % CIN;
+      const int v = e / CIN;
+      const int a = v / (HH * HW), b = (v / HW) % HH, cc = v % HW;
+      const int id = od0 - p.pd + a, ih = oh0 - p.ph + b, iw = ow0 - p.pw + cc;
+      T val = from_f32<DT>(0.f);
+      if (e < HALO && (unsigned)id < (unsigned)p.d && (unsigned)ih < (unsigned)p.h && (unsigned)iw < (unsigned)p.w)
+        val = x[((((long long)n * p.d + id) * p.h + ih) * p.w + iw) * CIN + c];
+      hv[k] = val;
+    }
+#pragma unroll
+    for (int k = 0; k < NL; ++k)
+      if (tid + 256 * k < HALO) halo[tid + 256 * k] = hv[k];
   }
 
   // ---- per-lane constants: im2col tap offsets and the weight fragments ------

@@ -101,20 +101,22 @@ __global__ __launch_bounds__(256) void smallc_wgrad_fused_kernel(
     const int od0 = td * TD, oh0 = th * TH, ow0 = tw * TW;
 
     // ---- stage the input halo, once per kw shift --------------------------
+    // (all of the tile's global loads -- halo here, dz sources below -- are issued
+    // before the first LDS store, so their latencies overlap)
     constexpr int helems = HD * HH * HWD * CIN;
-    for (int e = tid; e < helems; e += 256) {
-      int ci = e % CIN;
-      int v = e / CIN;
-      int a = v / (HH * HWD), b = (v / HWD) % HH, c = v % HWD;
-      int id = od0 - p.pd + a, ih = oh0 - p.ph + b, iw = ow0 - p.pw + c;
-      T val = from_f32<DT>(0.f);
-      if ((unsigned)id < (unsigned)p.d && (unsigned)ih < (unsigned)p.h && (unsigned)iw < (unsigned)p.w)
-        val = x[((((long long)n * p.d + id) * p.h + ih) * p.w + iw) * CIN + ci];
+    constexpr int NL = (helems + 255) / 256;
+    T xv[NL];
 #pragma unroll
-      for (int s = 0; s < KE; ++s) {
-        int wl = c - s;
-        if (wl >= 0 && wl < TW) xs[(((s * CIN + ci) * HD + a) * HH + b) * TW + wl] = val;
-      }
+    for (int k = 0; k < NL; ++k) {
+      const int e = tid + 256 * k;
+      const int ci = e % CIN;
+      const int v = e / CIN;
+      const int a = v / (HH * HWD), b = (v / HWD) % HH, c = v % HWD;
+      const int id = od0 - p.pd + a, ih = oh0 - p.ph + b, iw = ow0 - p.pw + c;
+      T val = from_f32<DT>(0.f);
+      if (e < helems && (unsigned)id < (unsigned)p.d && (unsigned)ih < (unsigned)p.h && (unsigned)iw < (unsigned)p.w)
+        val = x[((((long long)n * p.d + id) * p.h + ih) * p.w + iw) * CIN + ci];
+      xv[k] = val;
     }
     // ---- rebuild dz = dp/8 * slope(mask) for the tile, transposed ----------
 #pragma unroll
@@ -176,6 +178,20 @@ __global__ __launch_bounds__(256) void smallc_wgrad_fused_kernel(
           reinterpret_cast<uint4 *>(dst)[0] = o[0].u;
           reinterpret_cast<uint4 *>(dst)[1] = o[1].u;
         }
+      }
+    }
+    // the halo, once per kw shift (xs[s][ci][a][b][w] = halo(a, b, w + s, ci))
+#pragma unroll
+    for (int k = 0; k < NL; ++k) {
+      const int e = tid + 256 * k;
+      if (e >= helems) continue;
+      const int ci = e % CIN;
+      const int v = e / CIN;
+      const int a = v / (HH * HWD), b = (v / HWD) % HH, c = v % HWD;
+#pragma unroll
+      for (int s = 0; s < KE; ++s) {
+        const int wl = c - s;
+        if (wl >= 0 && wl < TW) xs[(((s * CIN + ci) * HD + a) * HH + b) * TW + wl] = xv[k];
       }
     }
     __syncthreads();
