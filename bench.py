@@ -66,6 +66,44 @@ def cpu_baseline(name, seconds_hint=True):
                        f"{dt:.1f} s, {1.0 / dt:.4f} samples/s")
 
 
+def measured_traffic(workload, op):
+    """HBM bytes per launch of `op` from the committed rocprofv3 counter
+    summary (FETCH_SIZE + WRITE_SIZE, scaled by a plain copy), or None when
+    there is none for this op or a source it was measured on has changed."""
+    import hashlib
+
+    path = os.path.join(ROOT, "profiles", "hbm_traffic.md")
+    if not os.path.exists(path):
+        return None
+    for line in open(path):
+        if not line.startswith("traffic:"):
+            continue
+        kv = dict(t.split("=", 1) for t in line.split()[1:])
+        if kv.get("workload") != workload or kv.get("op") != op:
+            continue
+        for spec in kv["sources"].split(","):
+            f, h = spec.rsplit(":", 1)
+            fp = os.path.join(ROOT, f)
+            if not os.path.exists(fp) or hashlib.sha256(open(fp, "rb").read()).hexdigest()[:len(h)] != h:
+                return None
+        return int(kv["bytes"])
+    return None
+
+
+def copy_probe(mib):
+    """A plain copy of known size: what the FETCH_SIZE / WRITE_SIZE counters
+    read for it is the scale that turns their readings into HBM bytes."""
+    import torch
+
+    torch.cuda.set_device(0)
+    src = torch.ones(mib << 20, dtype=torch.uint8, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": mib << 20, "copies": 5}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -74,6 +112,8 @@ def main():
     ap.add_argument("--workload", default="stack_128c_b8_bf16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--op-breakdown", action="store_true", help="print per-op times to stderr")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="only run 5 plain device copies of MIB MiB (calibrates the HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (data-parallel sharding is "
@@ -82,6 +122,10 @@ def main():
 
     import numpy as np
     import torch
+
+    if args.copy_probe:
+        copy_probe(args.copy_probe)
+        return
 
     from paper_1808_04728_amd import inputs
     from paper_1808_04728_amd.stack import ConvStack
@@ -137,13 +181,14 @@ def main():
     if dom_flops:
         ach = dom_flops / (dom_ms * 1e-3) / 1e12
         roof = dict(bound="mfma", achieved=round(ach, 2), peak=peak, unit="TFLOP/s", frac=round(ach / peak, 4),
-                    traffic=None, kernel=dominant, launch_ms=round(dom_ms, 4),
-                    per_launch=f"{dom_flops / 1e9:.2f} GFLOP")
+                    traffic=measured_traffic(name, dominant), kernel=dominant, launch_ms=round(dom_ms, 4),
+                    per_launch=f"{dom_flops / 1e9:.2f} GFLOP", algorithmic_bytes=st.op_bytes(dominant))
     else:
         gbs = st.op_bytes(dominant) / (dom_ms * 1e-3) / 1e9
         roof = dict(bound="hbm", achieved=round(gbs, 1), peak=HBM_PEAK_GBS, unit="GB/s",
-                    frac=round(gbs / HBM_PEAK_GBS, 4), traffic=None, kernel=dominant, launch_ms=round(dom_ms, 4),
-                    per_launch=f"{st.op_bytes(dominant) / 2**20:.1f} MiB")
+                    frac=round(gbs / HBM_PEAK_GBS, 4), traffic=measured_traffic(name, dominant), kernel=dominant,
+                    launch_ms=round(dom_ms, 4), per_launch=f"{st.op_bytes(dominant) / 2**20:.1f} MiB",
+                    algorithmic_bytes=st.op_bytes(dominant))
     res = {
         "metric": METRIC,
         "value": round(tflops, 3),
