@@ -318,6 +318,7 @@ static int32_t fused_mask(const cf::ConvShape &s, uint32_t flags) {
     if (cf::smallc_wgrad_fused_supported(s) || cf::c16_wgrad_supported(s)) m |= 2;
   }
   if (cf::c16_fwd_supported(s)) m |= 1;  // with or without the pool
+  if (flags == 0 && cf::direct_supported(s, true)) m |= 1;
   if (flags == CF_FUSE_POOL2 && cf::c16_bwd_supported(s)) m |= 4;
   return m;
 }
@@ -383,6 +384,8 @@ cf_status cf_conv3d_fwd_fused(const cf_conv3d_desc *desc, const void *x, const v
   hipError_t e;
   if (pool && cf::smallc_supported(s, true))
     e = cf::launch_conv_fwd_smallc(s, x, w, bias, alpha, out, (uint16_t *)mask, true, st);
+  else if (!pool && !cf::c16_fwd_supported(s))
+    e = cf::launch_conv_fwd_direct(s, x, w, bias, alpha, out, mask, true, st);
   else
     e = cf::launch_conv_fwd_c16(s, x, w, bias, alpha, out, (uint32_t *)mask, pool ? 2 : 1, st);
   return finish(e, st, "cf_conv3d_fwd_fused");

@@ -60,6 +60,14 @@ size_t smallc_wgrad_fused_workspace(const ConvShape &s);
 hipError_t launch_smallc_wgrad_fused(const ConvShape &s, const void *x, const void *dp, const uint16_t *mask,
                                      float alpha, float *dw, float *db, void *ws, hipStream_t st);
 
+// Deep-layer implicit GEMM (>= 32 contracted channels, bf16), conv_direct.hip.
+// act: bias + leaky ReLU epilogue (out = y), optional 1-bit slope mask.
+bool direct_supported(const ConvShape &s, bool fwd);
+hipError_t launch_conv_fwd_direct(const ConvShape &s, const void *x, const void *w, const float *bias, float alpha,
+                                  void *out, void *mask, bool act, hipStream_t st);
+hipError_t launch_conv_bwd_data_direct(const ConvShape &s, const void *dz, const void *w, void *dx,
+                                       hipStream_t st);
+
 hipError_t launch_conv_fwd(const ConvShape &s, const void *x, const void *w, void *z,
                            hipStream_t st);
 hipError_t launch_conv_bwd_data(const ConvShape &s, const void *dz, const void *w, void *dx,

@@ -575,6 +575,8 @@ hipError_t launch_conv_fwd(const ConvShape &s, const void *x, const void *w, voi
     return launch_conv_fwd_smallc(s, x, w, nullptr, 0.f, z, nullptr, false, st);
   // 16 -> 32 channels, stride 1: halo-tiled MFMA kernel with weights resident in LDS
   if (c16_fwd_supported(s)) return launch_conv_fwd_c16(s, x, w, nullptr, 0.f, z, nullptr, 0, st);
+  // many channels, bf16: waves split the taps, fragments gathered straight into registers
+  if (direct_supported(s, true)) return launch_conv_fwd_direct(s, x, w, nullptr, 0.f, z, nullptr, false, st);
   IgemmParams p{};
   p.nb = s.n;
   p.sd_ = s.d; p.sh_ = s.h; p.sw_ = s.w; p.sc = s.ci;
@@ -598,6 +600,7 @@ hipError_t launch_conv_fwd(const ConvShape &s, const void *x, const void *w, voi
 hipError_t launch_conv_bwd_data(const ConvShape &s, const void *dz, const void *w, void *dx,
                                 hipStream_t st) {
   if (c16_bwd_supported(s)) return launch_conv_bwd_data_c16(s, dz, nullptr, w, 0.f, dx, false, st);
+  if (direct_supported(s, false)) return launch_conv_bwd_data_direct(s, dz, w, dx, st);
   // one launch per parity class (r_d, r_h, r_w) of input voxels
   for (int rd = 0; rd < s.sd; ++rd)
     for (int rh = 0; rh < s.sh; ++rh)
