@@ -12,21 +12,26 @@
 //
 // Why a second implicit-GEMM kernel: at a few thousand rows, a 128-row
 // output tile per workgroup leaves most of the 256 compute units idle and
-// every workgroup serialises dozens of load -> LDS -> MFMA stages, so the
-// contraction runs at memory latency.  Here:
+// every workgroup serialises dozens of load -> LDS -> MFMA stages.  Here:
 //  * a workgroup's four waves split the reduction over taps (a wave owns
-//    taps u = w, w+4, ... or w, w+2, ...) and, optionally, the rows, so a
-//    16- to 128-row tile still gives every wave its own independent stream
-//    of loads; partial sums meet once, in LDS, at the end;
+//    taps w, w+4, ... or w, w+2, ...) and, optionally, the rows, so a 16- to
+//    128-row tile still gives every wave its own stream of loads; partial
+//    sums meet once, in LDS, at the end;
 //  * the im2col operand is never staged: every lane loads its MFMA fragment
 //    (8 consecutive channels of one gathered voxel, 16 bytes of NDHWC)
-//    straight into registers, one k-step ahead of the MFMAs;
+//    straight into registers, PF k-steps ahead of the MFMAs;
 //  * forward weights W[t][ci][co] have the output channel contiguous, but the
 //    MFMA B operand wants 8 consecutive input channels per lane: each wave
 //    copies its 32 x 64 weight slice into a private LDS buffer (swizzled
 //    against bank conflicts) and reads it back with the gfx950 transposing
 //    read ds_read_b64_tr_b16; backward-data weights are already K-contiguous
 //    (co fastest) and are loaded straight into registers;
+//  * index arithmetic is kept off the critical path: the host tabulates every
+//    class (row counts, launch-time divisors for the row decode, coordinate
+//    bases) and every tap (source and weight offsets) in the kernel
+//    arguments; loads are 32-bit-offset buffer loads whose hardware range
+//    check returns zero for an offset beyond the buffer, which is how padding
+//    voxels read as zero without a branch or a select;
 //  * the epilogue sums the waves' partial tiles in LDS and writes whole
 //    16-byte vectors of the destination (optionally bias + leaky ReLU and
 //    the slope mask, the fused forward of an unpooled layer).
@@ -37,6 +42,7 @@
 
 #include "cf_common.h"
 #include "cf_kernels.h"
+#include "fastdiv.h"
 
 #include <algorithm>
 #include <cstdio>
@@ -51,41 +57,37 @@ typedef __attribute__((address_space(3))) v4i16_t lds_v4i16_t;
 // address spaces stay memcpys through private memory)
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
+constexpr int DIR_MAX_CLS = 8;
+constexpr int DIR_MAX_TAPS = 64;
+constexpr uint32_t DIR_OOB = 0x80000000u;  // a byte offset past every buffer: the load returns zeros
+
+struct DirClass {
+  int m;                // GEMM rows (destination voxels) of the class
+  int tile0;            // first row tile of the class in the grid
+  int ntap, tap0;       // the class's taps: entries tap0 .. tap0 + ntap - 1 of the tap table
+  FastDiv fw, fh, fd;   // row = ((n * Jd + jd) * Jh + jh) * Jw + jw: divisors Jw, Jh, Jd
+  int bq_d, bq_h, bq_w; // source base coordinate = j * bstr + bq
+  int or_d, or_h, or_w; // destination coordinate = j * ostr + or
+};
+
+struct DirTap {
+  int a_off;            // element offset of the tap's source voxel from the row's base voxel
+  int w_off;            // element offset of W[tap][0][0]
+  int dd, dh, dw;       // source coordinate offsets (bounds check)
+};
+
 struct DirParams {
-  int nb;
-  int sd_, sh_, sw_, sc;  // gathered tensor extent and channels (x forward, dz backward)
-  int dd, dh, dw, dc;     // destination extent and channels (z forward, dx backward; GEMM N)
-  int kd, kh, kw;         // kernel extent
-  int s_d, s_h, s_w;      // conv stride
-  int pd, ph, pw;         // padding before
-  int wci, wco;           // weight channels W[t][wci][wco]
-  int ncls;               // row classes: 1 forward, s_d*s_h*s_w backward-data
+  int sd_, sh_, sw_, sc;        // gathered tensor extent and channels (x forward, dz backward)
+  int dd, dh, dw, dc;           // destination extent and channels (z forward, dx backward; GEMM N)
+  int bstr_d, bstr_h, bstr_w;   // source base stride per row coordinate
+  int ostr_d, ostr_h, ostr_w;   // destination stride per row coordinate
+  int wco;                      // weight row pitch (output channels)
+  int src_bytes, w_bytes;       // extents of the range-checked buffers
+  int ncls;
   float alpha;
+  DirClass cls[DIR_MAX_CLS];
+  DirTap tap[DIR_MAX_TAPS];
 };
-
-// Row geometry of one class along one dimension.
-//   forward:        source = j*s + q + u (q = -p),  weight tap = u,          destination = j
-//   backward-data:  source = j + q - u,             weight tap = t0 + s*u,   destination = j*s + r
-struct DimGeom {
-  int j, u, t0, q;
-};
-
-template <bool FWD>
-__device__ __forceinline__ DimGeom dim_geom(int r, int dst_ext, int k, int s, int pad) {
-  DimGeom g;
-  if (FWD) {
-    g.j = dst_ext;
-    g.u = k;
-    g.t0 = 0;
-    g.q = -pad;
-  } else {
-    g.j = dst_ext > r ? (dst_ext - r + s - 1) / s : 0;
-    g.t0 = (r + pad) % s;
-    g.u = g.t0 < k ? (k - g.t0 + s - 1) / s : 0;
-    g.q = (r + pad - g.t0) / s;
-  }
-  return g;
-}
 
 // swizzled byte offset of (row, 32-byte chunk) in a wave's 32 x 64 bf16 weight
 // slice: rows are 128 B, the chunk index is XORed with bits 1 and 3 of the row
@@ -96,12 +98,16 @@ __device__ __forceinline__ int wslice_off(int row, int chunk) {
   return row * 128 + ((chunk ^ h) << 5);
 }
 
-template <bool FWD, int FM, int FN, int WM, int WK, bool ACT>
+__device__ __forceinline__ u32x4_t buf_load(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 0);
+}
+
+template <bool FWD, int FM, int FN, int WM, int WK, int PF, bool ACT>
 __global__ __launch_bounds__(256) void conv_direct_kernel(const uint16_t *__restrict__ src,
                                                           const uint16_t *__restrict__ wt,
                                                           const float *__restrict__ bias,
                                                           uint16_t *__restrict__ dst, uint8_t *__restrict__ mask,
-                                                          DirParams p) {
+                                                          const DirParams p) {
   constexpr int BM = 16 * FM * WM, BN = 16 * FN;
   static_assert(WM * WK == 4, "four waves");
   static_assert(!FWD || FN == 4, "forward weight slices are 64 output channels wide");
@@ -118,102 +124,75 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const uint16_t *__rest
   const int wm = wave % WM, wk = wave / WM;
   const int g4 = lane >> 4, r16 = lane & 15;
 
-  // ---- class and row tile of this workgroup --------------------------------
-  int b = blockIdx.x, cls = 0;
-  DimGeom gd, gh, gw;
-  int rd = 0, rh = 0, rw = 0, m = 0;
-  for (;;) {
-    rd = FWD ? 0 : cls / (p.s_h * p.s_w);
-    rh = FWD ? 0 : (cls / p.s_w) % p.s_h;
-    rw = FWD ? 0 : cls % p.s_w;
-    gd = dim_geom<FWD>(rd, p.dd, p.kd, p.s_d, p.pd);
-    gh = dim_geom<FWD>(rh, p.dh, p.kh, p.s_h, p.ph);
-    gw = dim_geom<FWD>(rw, p.dw, p.kw, p.s_w, p.pw);
-    m = p.nb * gd.j * gh.j * gw.j;
-    const int tiles = (m + BM - 1) / BM;
-    if (b < tiles || cls + 1 >= p.ncls) break;
-    b -= tiles;
-    ++cls;
-  }
-  const int m0 = b * BM;
-  if (m0 >= m) return;  // uniform: the whole workgroup leaves
+  // ---- class and row tile of this workgroup (uniform) -----------------------
+  int c = 0;
+  while (c + 1 < p.ncls && (int)blockIdx.x >= p.cls[c + 1].tile0) ++c;
+  const DirClass &C = p.cls[c];
+  const int m0 = ((int)blockIdx.x - C.tile0) * BM;
+  if (m0 >= C.m) return;  // uniform: the whole workgroup leaves
   const int n0 = blockIdx.y * BN;
-  const int bs_d = FWD ? p.s_d : 1, bs_h = FWD ? p.s_h : 1, bs_w = FWD ? p.s_w : 1;
 
-  // ---- per-row-fragment source base ----------------------------------------
-  int rbd[FM], rbh[FM], rbw[FM];
-  const uint16_t *rp[FM];  // row base pointers (never dereferenced for an out-of-range voxel)
+  const __amdgpu_buffer_rsrc_t srsrc = __builtin_amdgcn_make_buffer_rsrc((void *)src, (short)0, p.src_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t wrsrc = __builtin_amdgcn_make_buffer_rsrc((void *)wt, (short)0, p.w_bytes, 0x00020000);
+
+  // ---- rows of this lane's A fragments ---------------------------------------
+  int rbd[FM], rbh[FM], rbw[FM], roff[FM];
   bool rok[FM];
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
     const int row = m0 + wm * 16 * FM + 16 * i + r16;
-    rok[i] = row < m;
+    rok[i] = row < C.m;
     const int rr = rok[i] ? row : 0;
-    const int jw_ = rr % gw.j;
-    int t = rr / gw.j;
-    const int jh_ = t % gh.j;
-    t /= gh.j;
-    const int jd_ = t % gd.j;
-    const int n = t / gd.j;
-    rbd[i] = jd_ * bs_d + gd.q;
-    rbh[i] = jh_ * bs_h + gh.q;
-    rbw[i] = jw_ * bs_w + gw.q;
-    const int rvox = ((n * p.sd_ + rbd[i]) * p.sh_ + rbh[i]) * p.sw_ + rbw[i];
-    rp[i] = src + (long long)rvox * p.sc + 8 * g4;
+    const int t1 = fdiv(rr, C.fw), t2 = fdiv(t1, C.fh), n = fdiv(t2, C.fd);
+    rbw[i] = (rr - t1 * (int)C.fw.div) * p.bstr_w + C.bq_w;
+    rbh[i] = (t1 - t2 * (int)C.fh.div) * p.bstr_h + C.bq_h;
+    rbd[i] = (t2 - n * (int)C.fd.div) * p.bstr_d + C.bq_d;
+    roff[i] = (((n * p.sd_ + rbd[i]) * p.sh_ + rbh[i]) * p.sw_ + rbw[i]) * p.sc + 8 * g4;
   }
 
-  // ---- this wave's k-steps: taps u = wk, wk + WK, ...; 32 channels per step --
-  const int ntap = gd.u * gh.u * gw.u;
+  // ---- this wave's k-steps: taps wk, wk + WK, ... of the class; 32 channels each
   const int nch = p.sc >> 5;
-  const int mytaps = ntap > wk ? (ntap - wk + WK - 1) / WK : 0;
+  const int mytaps = C.ntap > wk ? (C.ntap - wk + WK - 1) / WK : 0;
   const int nsteps = mytaps * nch;
-  int cc = 0, ud = 0, uh = 0, uw = 0;
-  if (mytaps > 0) {
-    ud = wk / (gh.u * gw.u);
-    uh = (wk / gw.u) % gh.u;
-    uw = wk % gw.u;
-  }
-  auto advance = [&]() {
-    if (++cc == nch) {
-      cc = 0;
-      uw += WK;
-      while (uw >= gw.u) {
-        uw -= gw.u;
-        if (++uh == gh.u) {
-          uh = 0;
-          ++ud;
-        }
+  int ti = wk, cc = 0, ldstep = 0;  // load cursor: tap, channel chunk, step
+  auto next = [&]() {
+    if (ldstep + 1 < nsteps) {
+      ++ldstep;
+      if (++cc == nch) {
+        cc = 0;
+        ti += WK;
       }
     }
   };
 
-  u32x4_t a_nx[FM], w_nx[NW];
-  auto load = [&]() {
-    const int sgn_d = FWD ? ud : -ud, sgn_h = FWD ? uh : -uh, sgn_w = FWD ? uw : -uw;
-    const long long soff = (long long)((sgn_d * p.sh_ + sgn_h) * p.sw_ + sgn_w) * p.sc + cc * 32;
+  // lane parts of the weight byte offsets
+  int wl[NW];
+#pragma unroll
+  for (int v = 0; v < NW; ++v) {
+    if constexpr (FWD) {
+      const int q = lane + 64 * v;  // 16-byte vector q of the 32 x 64 slice: row q/8, columns 8 (q%8) ..
+      wl[v] = ((q >> 3) * p.wco + n0 + 8 * (q & 7)) * 2;
+    } else {
+      wl[v] = ((n0 + 16 * v + r16) * p.wco + 8 * g4) * 2;  // column ci, K = 8 output channels
+    }
+  }
+
+  // Register ring of NS = PF + 1 slots: the loads of step s + PF are issued
+  // (into the slot step s - 1 used) before the MFMAs of step s.
+  constexpr int NS = PF + 1;
+  u32x4_t a_r[NS][FM], w_r[NS][NW];
+  auto load = [&](u32x4_t(&a)[FM], u32x4_t(&wv)[NW]) {
+    const DirTap &T = p.tap[C.tap0 + ti];
+    const int cofs = cc * 32;
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
-      const bool ok = rok[i] && (unsigned)(rbd[i] + sgn_d) < (unsigned)p.sd_ &&
-                      (unsigned)(rbh[i] + sgn_h) < (unsigned)p.sh_ && (unsigned)(rbw[i] + sgn_w) < (unsigned)p.sw_;
-      a_nx[i] = ok ? *reinterpret_cast<const u32x4_t *>(rp[i] + soff) : u32x4_t{0u, 0u, 0u, 0u};
+      const bool ok = rok[i] && (unsigned)(rbd[i] + T.dd) < (unsigned)p.sd_ &&
+                      (unsigned)(rbh[i] + T.dh) < (unsigned)p.sh_ && (unsigned)(rbw[i] + T.dw) < (unsigned)p.sw_;
+      a[i] = buf_load(srsrc, ok ? (uint32_t)(roff[i] + T.a_off + cofs) * 2u : DIR_OOB);
     }
-    const int tap = ((gd.t0 + (FWD ? 1 : p.s_d) * ud) * p.kh + (gh.t0 + (FWD ? 1 : p.s_h) * uh)) * p.kw +
-                    (gw.t0 + (FWD ? 1 : p.s_w) * uw);
-    if constexpr (FWD) {
-      // slice W[tap][32 cc .. +32][n0 .. n0 + 64): 256 16-byte vectors, 4 per lane
+    const int wbase = (T.w_off + cofs * (FWD ? p.wco : 1)) * 2;
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int q = lane + 64 * v;
-        w_nx[v] = *reinterpret_cast<const u32x4_t *>(wt + ((long long)tap * p.wci + cc * 32 + (q >> 3)) * p.wco + n0 +
-                                                   8 * (q & 7));
-      }
-    } else {
-      // B fragment j: column ci = n0 + 16 j + l%16, K = 8 consecutive output channels
-#pragma unroll
-      for (int j = 0; j < FN; ++j)
-        w_nx[j] = *reinterpret_cast<const u32x4_t *>(wt + ((long long)tap * p.wci + n0 + 16 * j + r16) * p.wco +
-                                                   cc * 32 + 8 * g4);
-    }
+    for (int v = 0; v < NW; ++v) wv[v] = buf_load(wrsrc, (uint32_t)(wl[v] + wbase));
   };
 
   unsigned char *wbuf = smem + wave * 2 * WSLICE;
@@ -224,11 +203,10 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const uint16_t *__rest
     const int q = lane + 64 * v;
     wst[v] = wslice_off(q >> 3, (q & 7) >> 1) + (q & 1) * 16;
   }
-#define CF_STAGE_W(buf)                                                              \
-  do {                                                                               \
-    _Pragma("unroll") for (int v = 0; v < 4; ++v)                                    \
-        *reinterpret_cast<u32x4_t *>(wbuf + (buf) * WSLICE + wst[v]) = w_nx[v];      \
-  } while (0)
+  auto stage_w = [&](const u32x4_t(&wv)[NW], int buf) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) *reinterpret_cast<u32x4_t *>(wbuf + buf * WSLICE + wst[v]) = wv[v];
+  };
 
   f32x4_t acc[FM][FN];
 #pragma unroll
@@ -236,59 +214,54 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const uint16_t *__rest
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
+  // Branch-free steady state (a conditional load would make the compiler wait
+  // for every load in flight at the merge): the step count is padded to a
+  // multiple of the ring size, the load cursor stops at the last real step
+  // (re-loading valid addresses), and padded steps multiply a zero A fragment.
   if (nsteps > 0) {
-    load();
-    if constexpr (FWD) CF_STAGE_W(0);
-    u32x4_t a_cu[FM], b_cu[FWD ? 1 : NW];
+    const int niter = (nsteps + NS - 1) / NS * NS;
 #pragma unroll
-    for (int i = 0; i < FM; ++i) a_cu[i] = a_nx[i];
-    if constexpr (!FWD) {
-#pragma unroll
-      for (int j = 0; j < NW; ++j) b_cu[j] = w_nx[j];
+    for (int q = 0; q < PF; ++q) {
+      load(a_r[q], w_r[q]);
+      next();
     }
-    for (int s = 0; s < nsteps; ++s) {
-      const bool more = s + 1 < nsteps;
-      if (more) {
-        advance();
-        load();
-      }
-      bf16x8_t bf[FN];
-      if constexpr (FWD) {
-        const unsigned char *rb = wbuf + (s & 1) * WSLICE;
+    if constexpr (FWD) stage_w(w_r[0], 0);
+    for (int s0 = 0; s0 < niter; s0 += NS) {
 #pragma unroll
-        for (int j = 0; j < FN; ++j) {
-          const int row = 8 * g4 + (r16 >> 2);
-          const v4i16_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (lds_v4i16_t *)(rb + wslice_off(row, j) + (r16 & 3) * 8));
-          const v4i16_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (lds_v4i16_t *)(rb + wslice_off(row + 4, j) + (r16 & 3) * 8));
-          typedef short v8i16_t __attribute__((ext_vector_type(8)));
-          const v8i16_t v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-          bf[j] = __builtin_bit_cast(bf16x8_t, v);
+      for (int q = 0; q < NS; ++q) {
+        const int s = s0 + q;
+        load(a_r[(q + PF) % NS], w_r[(q + PF) % NS]);
+        next();
+        bf16x8_t bf[FN];
+        if constexpr (FWD) {
+          const unsigned char *rb = wbuf + (s & 1) * WSLICE;
+#pragma unroll
+          for (int j = 0; j < FN; ++j) {
+            const int row = 8 * g4 + (r16 >> 2);
+            const v4i16_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (lds_v4i16_t *)(rb + wslice_off(row, j) + (r16 & 3) * 8));
+            const v4i16_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                (lds_v4i16_t *)(rb + wslice_off(row + 4, j) + (r16 & 3) * 8));
+            typedef short v8i16_t __attribute__((ext_vector_type(8)));
+            const v8i16_t v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+            bf[j] = __builtin_bit_cast(bf16x8_t, v);
+          }
+        } else {
+#pragma unroll
+          for (int j = 0; j < FN; ++j) bf[j] = __builtin_bit_cast(bf16x8_t, w_r[q][j]);
         }
-      } else {
+        const bool real = s < nsteps;
 #pragma unroll
-        for (int j = 0; j < FN; ++j) bf[j] = __builtin_bit_cast(bf16x8_t, b_cu[j]);
-      }
+        for (int i = 0; i < FM; ++i) {
+          const bf16x8_t af = __builtin_bit_cast(bf16x8_t, real ? a_r[q][i] : u32x4_t{0u, 0u, 0u, 0u});
 #pragma unroll
-      for (int i = 0; i < FM; ++i) {
-        const bf16x8_t af = __builtin_bit_cast(bf16x8_t, a_cu[i]);
-#pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bf[j], acc[i][j], 0, 0, 0);
-      }
-      if (more) {
-        if constexpr (FWD) CF_STAGE_W((s + 1) & 1);
-#pragma unroll
-        for (int i = 0; i < FM; ++i) a_cu[i] = a_nx[i];
-        if constexpr (!FWD) {
-#pragma unroll
-          for (int j = 0; j < NW; ++j) b_cu[j] = w_nx[j];
+          for (int j = 0; j < FN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bf[j], acc[i][j], 0, 0, 0);
         }
+        if constexpr (FWD) stage_w(w_r[(q + 1) % NS], (s + 1) & 1);
       }
     }
   }
-
-#undef CF_STAGE_W
 
   // ---- partial tiles meet in LDS ---------------------------------------------
   __syncthreads();  // every wave is done with its weight slices
@@ -306,7 +279,7 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const uint16_t *__rest
   for (int v = threadIdx.x; v < BM * CV; v += 256) {
     const int row = v / CV, c8 = v % CV;
     const int grow = m0 + row;
-    if (grow >= m) continue;
+    if (grow >= C.m) continue;
     float o[8];
 #pragma unroll
     for (int e = 0; e < 8; ++e) o[e] = 0.f;
@@ -317,16 +290,11 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const uint16_t *__rest
       o[0] += x0.x; o[1] += x0.y; o[2] += x0.z; o[3] += x0.w;
       o[4] += x1.x; o[5] += x1.y; o[6] += x1.z; o[7] += x1.w;
     }
-    const int jw_ = grow % gw.j;
-    int t = grow / gw.j;
-    const int jh_ = t % gh.j;
-    t /= gh.j;
-    const int jd_ = t % gd.j;
-    const int n = t / gd.j;
-    const int od_ = FWD ? jd_ : jd_ * p.s_d + rd;
-    const int oh_ = FWD ? jh_ : jh_ * p.s_h + rh;
-    const int ow_ = FWD ? jw_ : jw_ * p.s_w + rw;
-    const long long e0 = ((((long long)n * p.dd + od_) * p.dh + oh_) * p.dw + ow_) * p.dc + n0 + 8 * c8;
+    const int t1 = fdiv(grow, C.fw), t2 = fdiv(t1, C.fh), n = fdiv(t2, C.fd);
+    const int ow_ = (grow - t1 * (int)C.fw.div) * p.ostr_w + C.or_w;
+    const int oh_ = (t1 - t2 * (int)C.fh.div) * p.ostr_h + C.or_h;
+    const int od_ = (t2 - n * (int)C.fd.div) * p.ostr_d + C.or_d;
+    const int e0 = (((n * p.dd + od_) * p.dh + oh_) * p.dw + ow_) * p.dc + n0 + 8 * c8;
     uint32_t bits = 0;
     if constexpr (ACT) {
 #pragma unroll
@@ -345,32 +313,19 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const uint16_t *__rest
 }
 
 struct DirCfg {
-  int fm, wm, wk;
+  int fm, wm, wk, pf;
 };
 
-template <bool FWD>
-long long dir_tiles(const DirParams &p, int bm) {
-  long long t = 0;
-  for (int c = 0; c < p.ncls; ++c) {
-    const int rd = FWD ? 0 : c / (p.s_h * p.s_w), rh = FWD ? 0 : (c / p.s_w) % p.s_h, rw = FWD ? 0 : c % p.s_w;
-    auto J = [&](int r, int ext, int s) { return FWD ? ext : (ext > r ? (ext - r + s - 1) / s : 0); };
-    const long long m = (long long)p.nb * J(rd, p.dd, p.s_d) * J(rh, p.dh, p.s_h) * J(rw, p.dw, p.s_w);
-    t += (m + bm - 1) / bm;
-  }
-  return t;
-}
-
-template <bool FWD, int FN, bool ACT>
-hipError_t launch_dir_t(const DirCfg &c, const DirParams &p, const void *src, const void *w, const float *bias,
-                        void *dst, void *mask, hipStream_t st) {
-  const int bm = 16 * c.fm * c.wm;
-  dim3 grid((unsigned)dir_tiles<FWD>(p, bm), p.dc / (16 * FN), 1);
+template <bool FWD, int FN, int PF, bool ACT>
+hipError_t launch_dir_t(const DirCfg &c, const DirParams &p, int tiles, const void *src, const void *w,
+                        const float *bias, void *dst, void *mask, hipStream_t st) {
+  dim3 grid((unsigned)tiles, p.dc / (16 * FN), 1);
   if (grid.x == 0 || grid.y == 0) return hipSuccess;  // no destination rows
   const uint16_t *s16 = (const uint16_t *)src, *w16 = (const uint16_t *)w;
   uint16_t *d16 = (uint16_t *)dst;
   uint8_t *m8 = (uint8_t *)mask;
-#define CF_DIR_LAUNCH(FM_, WM_, WK_)                                                                       \
-  hipLaunchKernelGGL((conv_direct_kernel<FWD, FM_, FN, WM_, WK_, ACT>), grid, dim3(256), 0, st, s16, w16, \
+#define CF_DIR_LAUNCH(FM_, WM_, WK_)                                                                           \
+  hipLaunchKernelGGL((conv_direct_kernel<FWD, FM_, FN, WM_, WK_, PF, ACT>), grid, dim3(256), 0, st, s16, w16, \
                      bias, d16, m8, p)
   if (c.fm == 4 && c.wm == 2) CF_DIR_LAUNCH(4, 2, 2);
   else if (c.fm == 4 && c.wm == 1) CF_DIR_LAUNCH(4, 1, 4);
@@ -381,24 +336,116 @@ hipError_t launch_dir_t(const DirCfg &c, const DirParams &p, const void *src, co
   return hipGetLastError();
 }
 
-// Tile choice: the largest row tile that still yields 512 workgroups (two
-// per compute unit); more rows per wave amortise the weight stream, waves
-// along K keep every wave busy when rows are few.  CF_DIRECT_TILE="fm,wm,wk"
-// forces one of the candidates (tests cover every variant this way).
-template <bool FWD>
-DirCfg choose_cfg(const DirParams &p) {
-  static const DirCfg cand[] = {{4, 2, 2}, {2, 2, 2}, {4, 1, 4}, {2, 1, 4}, {1, 1, 4}};
+template <bool FWD, int FN, bool ACT>
+hipError_t launch_dir_pf(const DirCfg &c, const DirParams &p, int tiles, const void *src, const void *w,
+                         const float *bias, void *dst, void *mask, hipStream_t st) {
+  switch (c.pf) {
+    case 1: return launch_dir_t<FWD, FN, 1, ACT>(c, p, tiles, src, w, bias, dst, mask, st);
+    case 2: return launch_dir_t<FWD, FN, 2, ACT>(c, p, tiles, src, w, bias, dst, mask, st);
+    default: return launch_dir_t<FWD, FN, 3, ACT>(c, p, tiles, src, w, bias, dst, mask, st);
+  }
+}
+
+// Class and tap tables.  Forward: one class, rows = output voxels, source
+// base = j*s - p, taps u with source offset +u and weight tap u.  Backward-
+// data: class r in [0, s)^3 per dimension: rows j with input coordinate
+// j*s + r, first reaching tap t0 = (r + p) mod s, taps t0 + s*u with source
+// offset -u from base j + (r + p - t0)/s.
+void build_tables(const ConvShape &s, bool fwd, DirParams &p) {
+  const int S[3] = {s.sd, s.sh, s.sw}, P[3] = {s.pd, s.ph, s.pw}, K[3] = {s.kd, s.kh, s.kw};
+  const int IN[3] = {s.d, s.h, s.w}, OUT[3] = {s.od, s.oh, s.ow};
+  const int *SRC = fwd ? IN : OUT;
+  const int *DST = fwd ? OUT : IN;
+  p.sd_ = SRC[0]; p.sh_ = SRC[1]; p.sw_ = SRC[2];
+  p.dd = DST[0]; p.dh = DST[1]; p.dw = DST[2];
+  p.sc = fwd ? s.ci : s.co;
+  p.dc = fwd ? s.co : s.ci;
+  p.bstr_d = fwd ? s.sd : 1; p.bstr_h = fwd ? s.sh : 1; p.bstr_w = fwd ? s.sw : 1;
+  p.ostr_d = fwd ? 1 : s.sd; p.ostr_h = fwd ? 1 : s.sh; p.ostr_w = fwd ? 1 : s.sw;
+  p.wco = s.co;
+  p.ncls = fwd ? 1 : s.sd * s.sh * s.sw;
+  int ntaps = 0;
+  for (int c = 0; c < p.ncls; ++c) {
+    const int r[3] = {fwd ? 0 : c / (s.sh * s.sw), fwd ? 0 : (c / s.sw) % s.sh, fwd ? 0 : c % s.sw};
+    int J[3], U[3], T0[3], Q[3];
+    for (int a = 0; a < 3; ++a) {
+      if (fwd) {
+        J[a] = OUT[a]; U[a] = K[a]; T0[a] = 0; Q[a] = -P[a];
+      } else {
+        J[a] = IN[a] > r[a] ? (IN[a] - r[a] + S[a] - 1) / S[a] : 0;
+        T0[a] = (r[a] + P[a]) % S[a];
+        U[a] = T0[a] < K[a] ? (K[a] - T0[a] + S[a] - 1) / S[a] : 0;
+        Q[a] = (r[a] + P[a] - T0[a]) / S[a];
+      }
+    }
+    DirClass &C = p.cls[c];
+    C.m = s.n * J[0] * J[1] * J[2];
+    C.fw = make_fastdiv(std::max(J[2], 1));
+    C.fh = make_fastdiv(std::max(J[1], 1));
+    C.fd = make_fastdiv(std::max(J[0], 1));
+    C.bq_d = Q[0]; C.bq_h = Q[1]; C.bq_w = Q[2];
+    C.or_d = r[0]; C.or_h = r[1]; C.or_w = r[2];
+    C.tap0 = ntaps;
+    C.ntap = U[0] * U[1] * U[2];
+    const int sg = fwd ? 1 : -1;
+    for (int ud = 0; ud < U[0]; ++ud)
+      for (int uh = 0; uh < U[1]; ++uh)
+        for (int uw = 0; uw < U[2]; ++uw) {
+          DirTap &T = p.tap[ntaps++];
+          T.dd = sg * ud; T.dh = sg * uh; T.dw = sg * uw;
+          T.a_off = ((T.dd * p.sh_ + T.dh) * p.sw_ + T.dw) * p.sc;
+          // weight tap step: 1 forward, the stride between the taps of a class backward
+          const int st_d = fwd ? 1 : S[0], st_h = fwd ? 1 : S[1], st_w = fwd ? 1 : S[2];
+          const int tap = ((T0[0] + st_d * ud) * s.kh + (T0[1] + st_h * uh)) * s.kw + (T0[2] + st_w * uw);
+          T.w_off = tap * s.ci * s.co;
+        }
+  }
+  p.src_bytes = (int)((long long)s.n * p.sd_ * p.sh_ * p.sw_ * p.sc * 2);
+  p.w_bytes = s.kd * s.kh * s.kw * s.ci * s.co * 2;
+}
+
+int assign_tiles(DirParams &p, int bm) {
+  int t = 0;
+  for (int c = 0; c < p.ncls; ++c) {
+    p.cls[c].tile0 = t;
+    t += (p.cls[c].m + bm - 1) / bm;
+  }
+  return t;
+}
+
+// Tile choice (measured on the deep layers of the stack): the largest row
+// tile that still yields 256 workgroups (one per compute unit); more rows per
+// wave amortise the weight stream, waves along K keep every wave busy when
+// rows are few.  The 128-row tile pays off only for backward-data, whose
+// weights come straight from global memory.  One k-step of prefetch: the
+// kernels are bound by L2 -> L1 traffic, not by load latency.
+// CF_DIRECT_TILE="fm,wm,wk" and CF_DIRECT_PF force a variant (tests cover
+// every one this way).
+DirCfg choose_cfg(DirParams &p, int fn, bool fwd) {
+  static const DirCfg cand[] = {{4, 2, 2, 1}, {2, 2, 2, 1}, {4, 1, 4, 1}, {2, 1, 4, 1}, {1, 1, 4, 1}};
+  int pf = 0;
+  if (const char *e = getenv("CF_DIRECT_PF")) pf = atoi(e);
+  DirCfg pick = cand[4];
+  bool forced = false;
   if (const char *e = getenv("CF_DIRECT_TILE")) {
     int fm = 0, wm = 0, wk = 0;
     if (sscanf(e, "%d,%d,%d", &fm, &wm, &wk) == 3)
       for (const DirCfg &c : cand)
-        if (c.fm == fm && c.wm == wm && c.wk == wk) return c;
+        if (c.fm == fm && c.wm == wm && c.wk == wk) {
+          pick = c;
+          forced = true;
+        }
   }
-  const int fn = FWD ? 4 : (p.dc % 64 == 0 ? 4 : 2);
-  const long long ny = p.dc / (16 * fn);
-  for (const DirCfg &c : cand)
-    if (dir_tiles<FWD>(p, 16 * c.fm * c.wm) * ny >= 512) return c;
-  return cand[4];
+  if (!forced) {
+    const int ny = p.dc / (16 * fn);
+    for (int i = fwd ? 1 : 0; i < 5; ++i)
+      if ((long long)assign_tiles(p, 16 * cand[i].fm * cand[i].wm) * ny >= 256) {
+        pick = cand[i];
+        break;
+      }
+  }
+  if (pf >= 1 && pf <= 3) pick.pf = pf;
+  return pick;
 }
 
 }  // namespace
@@ -409,45 +456,36 @@ bool direct_supported(const ConvShape &s, bool fwd) {
   const int nc = fwd ? s.co : s.ci;  // GEMM columns
   if (gc % 32 != 0 || nc % 32 != 0) return false;
   if (fwd && nc % 64 != 0) return false;
-  if (s.sd * s.sh * s.sw > 8) return false;
-  // 32-bit voxel indices
-  const long long vin = (long long)s.n * s.d * s.h * s.w, vout = (long long)s.n * s.od * s.oh * s.ow;
-  if (vin >= (1LL << 31) / 8 || vout >= (1LL << 31) / 8) return false;
+  if (s.sd * s.sh * s.sw > DIR_MAX_CLS) return false;
+  // every class's taps fit the table (k <= 4 per dimension gives at most 64)
+  if (s.kd * s.kh * s.kw > DIR_MAX_TAPS) return false;
+  // 32-bit element offsets and buffer extents
+  const long long xin = (long long)s.n * s.d * s.h * s.w * s.ci, zout = (long long)s.n * s.od * s.oh * s.ow * s.co;
+  const long long wn = (long long)s.kd * s.kh * s.kw * s.ci * s.co;
+  if (xin * 2 >= (1LL << 31) || zout * 2 >= (1LL << 31) || wn * 2 >= (1LL << 31)) return false;
   return true;
 }
 
 hipError_t launch_conv_fwd_direct(const ConvShape &s, const void *x, const void *w, const float *bias, float alpha,
                                   void *out, void *mask, bool act, hipStream_t st) {
   DirParams p{};
-  p.nb = s.n;
-  p.sd_ = s.d; p.sh_ = s.h; p.sw_ = s.w; p.sc = s.ci;
-  p.dd = s.od; p.dh = s.oh; p.dw = s.ow; p.dc = s.co;
-  p.kd = s.kd; p.kh = s.kh; p.kw = s.kw;
-  p.s_d = s.sd; p.s_h = s.sh; p.s_w = s.sw;
-  p.pd = s.pd; p.ph = s.ph; p.pw = s.pw;
-  p.wci = s.ci; p.wco = s.co;
-  p.ncls = 1;
+  build_tables(s, true, p);
   p.alpha = alpha;
-  const DirCfg c = choose_cfg<true>(p);
-  return act ? launch_dir_t<true, 4, true>(c, p, x, w, bias, out, mask, st)
-             : launch_dir_t<true, 4, false>(c, p, x, w, nullptr, out, nullptr, st);
+  const DirCfg c = choose_cfg(p, 4, true);
+  const int tiles = assign_tiles(p, 16 * c.fm * c.wm);
+  return act ? launch_dir_pf<true, 4, true>(c, p, tiles, x, w, bias, out, mask, st)
+             : launch_dir_pf<true, 4, false>(c, p, tiles, x, w, nullptr, out, nullptr, st);
 }
 
 hipError_t launch_conv_bwd_data_direct(const ConvShape &s, const void *dz, const void *w, void *dx,
                                        hipStream_t st) {
   DirParams p{};
-  p.nb = s.n;
-  p.sd_ = s.od; p.sh_ = s.oh; p.sw_ = s.ow; p.sc = s.co;
-  p.dd = s.d; p.dh = s.h; p.dw = s.w; p.dc = s.ci;
-  p.kd = s.kd; p.kh = s.kh; p.kw = s.kw;
-  p.s_d = s.sd; p.s_h = s.sh; p.s_w = s.sw;
-  p.pd = s.pd; p.ph = s.ph; p.pw = s.pw;
-  p.wci = s.ci; p.wco = s.co;
-  p.ncls = s.sd * s.sh * s.sw;
-  p.alpha = 0.f;
-  const DirCfg c = choose_cfg<false>(p);
-  return p.dc % 64 == 0 ? launch_dir_t<false, 4, false>(c, p, dz, w, nullptr, dx, nullptr, st)
-                        : launch_dir_t<false, 2, false>(c, p, dz, w, nullptr, dx, nullptr, st);
+  build_tables(s, false, p);
+  const int fn = p.dc % 64 == 0 ? 4 : 2;
+  const DirCfg c = choose_cfg(p, fn, false);
+  const int tiles = assign_tiles(p, 16 * c.fm * c.wm);
+  return fn == 4 ? launch_dir_pf<false, 4, false>(c, p, tiles, dz, w, nullptr, dx, nullptr, st)
+                 : launch_dir_pf<false, 2, false>(c, p, tiles, dz, w, nullptr, dx, nullptr, st);
 }
 
 }  // namespace cf

@@ -136,3 +136,28 @@ def test_direct_delta_kernel_is_identity():
     torch.cuda.synchronize()
     assert torch.equal(z, x)
     assert torch.equal(dx, x)
+
+
+@pytest.mark.parametrize("pf", ["1", "3"])
+@pytest.mark.parametrize("tile", ["4,2,2", "1,1,4"], indirect=True)
+@pytest.mark.parametrize("case", [CASES[0], CASES[1], CASES[4]], ids=ids)
+def test_direct_prefetch_depths(case, tile, pf, monkeypatch):
+    """The register ring at prefetch depths 1 and 3 (step counts that are not
+    multiples of the ring size)."""
+    monkeypatch.setenv("CF_DIRECT_PF", pf)
+    N, dhw, CI, CO, k, s = case
+    rng = np.random.default_rng(35)
+    desc = B.make_desc(N, dhw, CI, CO, k, s, "same", "bf16")
+    od = B.cf_conv3d_out_shape(desc)
+    x = dev(rng.standard_normal((N, *dhw, CI)), "bf16")
+    w = dev(rng.standard_normal((k, k, k, CI, CO)) / np.sqrt(k ** 3 * CI), "bf16")
+    dz = dev(rng.standard_normal((N, *od, CO)), "bf16")
+    z = torch.full((N, *od, CO), float("nan"), dtype=tdtype("bf16"), device="cuda")
+    dx = torch.full((N, *dhw, CI), float("nan"), dtype=tdtype("bf16"), device="cuda")
+    B.cf_conv3d_fwd(desc, x, w, z)
+    B.cf_conv3d_bwd_data(desc, dz, w, dx)
+    torch.cuda.synchronize()
+    e = maxabs_err(to_np(z), oracle.conv3d_fwd(to_np(x), to_np(w), stride=s, pad="same"))
+    assert e <= TOL["bf16"], e
+    e = maxabs_err(to_np(dx), oracle.conv3d_bwd_data(to_np(dz), to_np(w), dhw, stride=s, pad="same"))
+    assert e <= TOL["bf16"], e
