@@ -29,8 +29,20 @@ namespace cf {
 namespace {
 
 constexpr int TD = 4, TH = 8, TW = 64;                   // output tile (voxels)
-constexpr int NPAIR = (TD / 2) * (TH / 2) * (TW / 8);    // 64 tile pairs of 2 x (2x2x8) voxels
 constexpr int KMAXE = 4;                                  // kernel extent limit per dimension
+
+// Halo row staging: the staged w-window starts a whole 16-byte vector before
+// the tile (covering the left padding) so that every row is a run of aligned
+// 16-byte vectors, each entirely inside or entirely outside the input.
+template <int DT, int CIN, int KE> struct HaloGeom {
+  static constexpr int ES = DT == DT_BF16 ? 2 : 4;
+  static constexpr int VV = 16 / (CIN * ES) > 0 ? 16 / (CIN * ES) : 1;  // voxels per 16-byte vector
+  static constexpr int LEAD = (KE - 1 + VV - 1) / VV * VV;             // staged voxels left of the tile (>= pad)
+  static constexpr int HD = TD + KE - 1, HH = TH + KE - 1;
+  static constexpr int HWS = (LEAD + TW + KE - 1 + VV - 1) / VV * VV;  // staged row length (voxels)
+  static constexpr int NVR = HWS / VV;                                 // 16-byte vectors per row
+  static constexpr int ELEMS = HD * HH * HWS * CIN;
+};
 
 template <int DT, int CIN, int NF, int KE, bool FUSED>
 __global__ __launch_bounds__(256) void conv_smallc_fwd_kernel(
@@ -38,18 +50,27 @@ __global__ __launch_bounds__(256) void conv_smallc_fwd_kernel(
     const float *__restrict__ bias, float alpha, typename Store<DT>::T *__restrict__ out,
     uint16_t *__restrict__ mask16, SmallcParams p) {
   using T = typename Store<DT>::T;
+  using G = HaloGeom<DT, CIN, KE>;
   constexpr int COUT = 16 * NF;
   constexpr bool BF = DT == DT_BF16;
   constexpr int KPER = BF ? 32 : 4;  // K per MFMA
-  // cubic kernel of extent KE: every halo / tap index below divides by constants
-  constexpr int HD = TD + KE - 1, HH = TH + KE - 1, HW = TW + KE - 1;
+  constexpr int HH = G::HH, HWS = G::HWS;
   constexpr int K = KE * KE * KE * CIN;
   constexpr int KS = (K + KPER - 1) / KPER;
   constexpr int JPER = BF ? 8 : 1;  // K-values per lane per MFMA
-  constexpr int HALO = HD * HH * HW * CIN;
-  __shared__ __attribute__((aligned(16))) T halo[HALO];
+  // Bias through the MFMA: with two spare K slots, slot K carries bf16(b) and
+  // slot K + 1 the bf16 rounding of the remainder (b to ~16 significant bits),
+  // both against A = 1.0, read from ONES_PLANES extra halo planes of ones that
+  // sit HD planes after every voxel of the tile.
+  constexpr bool BIAS_MFMA = FUSED && BF && (KS * 32 - K >= 2);
+  constexpr int ONES = BIAS_MFMA ? TD * HH * HWS * CIN : 0;
+  constexpr int ONES_OFF = G::HD * HH * HWS * CIN;  // element offset voxel -> its 1.0 slot
+  __shared__ __attribute__((aligned(16))) T halo[G::ELEMS + ONES];
+  // fused, 16 channels: raw slope ballots of one row of eight tile pairs per wave
+  __shared__ __attribute__((aligned(16))) uint64_t bstage[4][(FUSED && NF == 1) ? 64 : 1];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int tiles_w = (p.ow + TW - 1) / TW, tiles_h = (p.oh + TH - 1) / TH;
   int t = blockIdx.x;
   const int tw = t % tiles_w; t /= tiles_w;
@@ -57,32 +78,60 @@ __global__ __launch_bounds__(256) void conv_smallc_fwd_kernel(
   const int td = t;
   const int n = blockIdx.y;
   const int od0 = td * TD, oh0 = th * TH, ow0 = tw * TW;
+  // staged slot c of a halo row holds input column iw = ow0 - LEAD + c
 
   // ---- stage the zero-padded input halo: every load in flight before any store
-  {
-    constexpr int NL = (HALO + 255) / 256;
+  if (p.w % G::VV == 0) {
+    constexpr int NV = G::HD * HH * G::NVR;
+    constexpr int NL = (NV + 255) / 256;
+    uint4 hv[NL];
+#pragma unroll
+    for (int k = 0; k < NL; ++k) {
+      const int e = tid + 256 * k;
+      const int v = e % G::NVR, rb = e / G::NVR;
+      const int a = rb / HH, b = rb % HH;
+      const int id = od0 - p.pd + a, ih = oh0 - p.ph + b;
+      const int iw0 = ow0 - G::LEAD + v * G::VV;  // a whole vector, inside or outside [0, w)
+      uint4 val = make_uint4(0, 0, 0, 0);
+      if (e < NV && (unsigned)id < (unsigned)p.d && (unsigned)ih < (unsigned)p.h && iw0 >= 0 && iw0 < p.w)
+        val = *reinterpret_cast<const uint4 *>(x + ((((long long)n * p.d + id) * p.h + ih) * p.w + iw0) * CIN);
+      hv[k] = val;
+    }
+#pragma unroll
+    for (int k = 0; k < NL; ++k) {
+      const int e = tid + 256 * k;
+      if (e < NV) *reinterpret_cast<uint4 *>(&halo[e * G::VV * CIN]) = hv[k];
+    }
+  } else {
+    constexpr int NL = (G::ELEMS + 255) / 256;
     T hv[NL];
 #pragma unroll
     for (int k = 0; k < NL; ++k) {
       const int e = tid + 256 * k;
-      const int c = e % CIN;
-      const int v = e / CIN;
-      const int a = v / (HH * HW), b = (v / HW) % HH, cc = v % HW;
-      const int id = od0 - p.pd + a, ih = oh0 - p.ph + b, iw = ow0 - p.pw + cc;
+      const int c = e % CIN, v = e / CIN;
+      const int cc = v % HWS, rb = v / HWS;
+      const int a = rb / HH, b = rb % HH;
+      const int id = od0 - p.pd + a, ih = oh0 - p.ph + b, iw = ow0 - G::LEAD + cc;
       T val = from_f32<DT>(0.f);
-      if (e < HALO && (unsigned)id < (unsigned)p.d && (unsigned)ih < (unsigned)p.h && (unsigned)iw < (unsigned)p.w)
+      if (e < G::ELEMS && (unsigned)id < (unsigned)p.d && (unsigned)ih < (unsigned)p.h && (unsigned)iw < (unsigned)p.w)
         val = x[((((long long)n * p.d + id) * p.h + ih) * p.w + iw) * CIN + c];
       hv[k] = val;
     }
 #pragma unroll
     for (int k = 0; k < NL; ++k)
-      if (tid + 256 * k < HALO) halo[tid + 256 * k] = hv[k];
+      if (tid + 256 * k < G::ELEMS) halo[tid + 256 * k] = hv[k];
+  }
+
+  if constexpr (BIAS_MFMA) {
+    static_assert(G::ELEMS % 8 == 0 && ONES % 8 == 0, "16-byte fill");
+    const uint4 one8 = make_uint4(0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u);
+    for (int e = tid; e < ONES / 8; e += 256) *reinterpret_cast<uint4 *>(&halo[G::ELEMS + 8 * e]) = one8;
   }
 
   // ---- per-lane constants: im2col tap offsets and the weight fragments ------
   const int r = lane & 15, q = lane >> 4;
-  // A row r -> voxel (hh = (r&3)>>1, ww = r&1, w = 2 (r>>2) + ww) of a tile
-  const int m_off = ((((r & 3) >> 1) * HW) + 2 * (r >> 2) + (r & 1)) * CIN;
+  // A row r -> voxel (hh = (r&3)>>1, w = 2 (r>>2) + (r&1)) of a tile
+  const int m_off = ((((r & 3) >> 1) * HWS) + 2 * (r >> 2) + (r & 1)) * CIN;
   int toff[KS][JPER];
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks)
@@ -93,7 +142,9 @@ __global__ __launch_bounds__(256) void conv_smallc_fwd_kernel(
       if (kg < K) {
         const int tap = kg / CIN, c = kg % CIN;
         const int a = tap / (KE * KE), b = (tap / KE) % KE, cc = tap % KE;
-        off = ((a * HH + b) * HW + cc) * CIN + c;
+        off = ((a * HH + b) * HWS + cc) * CIN + c;
+      } else if (BIAS_MFMA && kg < K + 2) {
+        off = ONES_OFF;
       }
       toff[ks][j] = off;
     }
@@ -108,7 +159,13 @@ __global__ __launch_bounds__(256) void conv_smallc_fwd_kernel(
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
           const int kg = ks * 32 + 8 * q + j;
-          v.e[j] = kg < K ? w[(long long)kg * COUT + 16 * f + r] : (uint16_t)0;
+          uint16_t e = kg < K ? w[(long long)kg * COUT + 16 * f + r] : (uint16_t)0;
+          if (BIAS_MFMA && kg >= K && kg < K + 2) {
+            const float b = bias[16 * f + r];
+            const uint16_t hi = f2bf(b);
+            e = kg == K ? hi : f2bf(b - bf2f(hi));
+          }
+          v.e[j] = e;
         }
         bw[ks][f] = __builtin_bit_cast(bf16x8_t, v.u);
       } else {
@@ -118,99 +175,150 @@ __global__ __launch_bounds__(256) void conv_smallc_fwd_kernel(
     }
   float bz[NF];
 #pragma unroll
-  for (int f = 0; f < NF; ++f) bz[f] = FUSED ? bias[16 * f + r] : 0.f;
+  for (int f = 0; f < NF; ++f) bz[f] = FUSED && !BIAS_MFMA ? bias[16 * f + r] : 0.f;
   __syncthreads();
 
-  // ---- tile pairs: pooled voxels (pd, ph, pw .. pw+3) of this workgroup -----
-  for (int pi = wave; pi < NPAIR; pi += 4) {
-    const int bd = pi / ((TH / 2) * (TW / 8)), bh = (pi / (TW / 8)) % (TH / 2), bw8 = pi % (TW / 8);
-    f32x4_t acc[2][NF];  // [dd][channel block]
+  // ---- rows (bd, bh) of eight tile pairs; pair bw8 = pooled voxels
+  // (pd, ph, 4 bw8 .. 4 bw8 + 3) of the workgroup.  The lane's gather
+  // addresses are formed once per row; every tile of the row reads the halo
+  // at a compile-time byte offset from them.
+  const unsigned char *hb = reinterpret_cast<const unsigned char *>(halo);
+  for (int ri = wave; ri < (TD / 2) * (TH / 2); ri += 4) {
+    const int bd = ri / (TH / 2), bh = ri % (TH / 2);
+    const int row_base = ((2 * bd * HH + 2 * bh) * HWS + G::LEAD - p.pw) * CIN + m_off;
+    int addr[KS][JPER];
 #pragma unroll
-    for (int dd = 0; dd < 2; ++dd) {
-      const int base = (((2 * bd + dd) * HH + 2 * bh) * HW + 8 * bw8) * CIN + m_off;
+    for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
-      for (int f = 0; f < NF; ++f) acc[dd][f] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      for (int j = 0; j < JPER; ++j) addr[ks][j] = (row_base + toff[ks][j]) * (int)sizeof(T);
+    const int vd0 = od0 + 2 * bd, vh0 = oh0 + 2 * bh;
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        AFrag a;
-        if constexpr (BF) {
-          Vec16<DT_BF16> v;
+    for (int bw8 = 0; bw8 < TW / 8; ++bw8) {
+      f32x4_t acc[2][NF];  // [dd][channel block]
 #pragma unroll
-          for (int j = 0; j < 8; ++j) v.e[j] = halo[base + toff[ks][j]];
-          a = __builtin_bit_cast(bf16x8_t, v.u);
-        } else {
-          a = halo[base + toff[ks][0]];
-        }
+      for (int dd = 0; dd < 2; ++dd) {
+        const int imm = ((dd * HH * HWS) + 8 * bw8) * CIN * (int)sizeof(T);
 #pragma unroll
-        for (int f = 0; f < NF; ++f) {
-          if constexpr (BF)
-            acc[dd][f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bw[ks][f], acc[dd][f], 0, 0, 0);
-          else
-            acc[dd][f] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bw[ks][f], acc[dd][f], 0, 0, 0);
+        for (int f = 0; f < NF; ++f) acc[dd][f] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          AFrag a;
+          if constexpr (BF) {
+            // built element by element so that the halves load straight into
+            // place (ds_read_u16_d16 / _d16_hi) instead of being packed afterwards
+            typedef short v8i16_t __attribute__((ext_vector_type(8)));
+            v8i16_t v;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) v[j] = *reinterpret_cast<const short *>(hb + addr[ks][j] + imm);
+            a = __builtin_bit_cast(bf16x8_t, v);
+          } else {
+            a = *reinterpret_cast<const float *>(hb + addr[ks][0] + imm);
+          }
+#pragma unroll
+          for (int f = 0; f < NF; ++f) {
+            if constexpr (BF)
+              acc[dd][f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bw[ks][f], acc[dd][f], 0, 0, 0);
+            else
+              acc[dd][f] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bw[ks][f], acc[dd][f], 0, 0, 0);
+          }
         }
       }
-    }
-    // this lane: channel 16f + r, rows 4q + j -> voxel (hh = j>>1, w = 8 bw8 + 2q + (j&1))
-    const int vd0 = od0 + 2 * bd, vh0 = oh0 + 2 * bh, vw0 = ow0 + 8 * bw8;
-    if constexpr (!FUSED) {
-#pragma unroll
-      for (int dd = 0; dd < 2; ++dd)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int vd = vd0 + dd, vh = vh0 + (j >> 1), vw = vw0 + 2 * q + (j & 1);
-          if (vd >= p.od || vh >= p.oh || vw >= p.ow) continue;
-          const long long vox = (((long long)n * p.od + vd) * p.oh + vh) * p.ow + vw;
-#pragma unroll
-          for (int f = 0; f < NF; ++f) out[vox * COUT + 16 * f + r] = from_f32<DT>(acc[dd][f][j]);
-        }
-    } else {
-#pragma unroll
-      for (int f = 0; f < NF; ++f) {
-        float s = 0.f;
-        unsigned long long bal[2][4];
+      // this lane: channel 16f + r, rows 4q + j -> voxel (hh = j>>1, w = 8 bw8 + 2q + (j&1))
+      const int vw0 = ow0 + 8 * bw8;
+      if constexpr (!FUSED) {
 #pragma unroll
         for (int dd = 0; dd < 2; ++dd)
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
-            const float u = acc[dd][f][j] + bz[f];
-            bal[dd][j] = __ballot(u > 0.f);
-            s += u > 0.f ? u : alpha * u;
+            const int vd = vd0 + dd, vh = vh0 + (j >> 1), vw = vw0 + 2 * q + (j & 1);
+            if (vd >= p.od || vh >= p.oh || vw >= p.ow) continue;
+            const long long vox = (((long long)n * p.od + vd) * p.oh + vh) * p.ow + vw;
+#pragma unroll
+            for (int f = 0; f < NF; ++f) out[vox * COUT + 16 * f + r] = from_f32<DT>(acc[dd][f][j]);
           }
-        // pooled voxel (pd, ph, pw + q): the whole window sits in this lane
+      } else {
         const int pd_ = vd0 >> 1, ph_ = vh0 >> 1, pw_ = (vw0 >> 1) + q;
-        if (pd_ < p.pod && ph_ < p.poh && pw_ < p.pow_)
-          out[((((long long)n * p.pod + pd_) * p.poh + ph_) * p.pow_ + pw_) * COUT + 16 * f + r] =
-              from_f32<DT>(s * 0.125f);
-        // slope mask: row (dd, hh) holds voxels w = vw0 .. vw0+7, 16 bits each;
-        // lane 2 dd + hh (of the first four) writes those eight half-words
-        if (lane < 4) {
-          const int dd = lane >> 1, hh = lane & 1;
-          const int vd = vd0 + dd, vh = vh0 + hh;
-          if (vd < p.od && vh < p.oh) {
-            const unsigned long long b0 = dd ? (hh ? bal[1][2] : bal[1][0]) : (hh ? bal[0][2] : bal[0][0]);
-            const unsigned long long b1 = dd ? (hh ? bal[1][3] : bal[1][1]) : (hh ? bal[0][3] : bal[0][1]);
-            uint16_t words[8];
+        const bool pin = pd_ < p.pod && ph_ < p.poh && pw_ < p.pow_;
+        const long long pbase = ((((long long)n * p.pod + pd_) * p.poh + ph_) * p.pow_ + pw_) * COUT;
 #pragma unroll
-            for (int qq = 0; qq < 4; ++qq) {
-              words[2 * qq] = (uint16_t)((b0 >> (16 * qq)) & 0xffffu);
-              words[2 * qq + 1] = (uint16_t)((b1 >> (16 * qq)) & 0xffffu);
+        for (int f = 0; f < NF; ++f) {
+          float s = 0.f;
+          uint64_t bal[2][4];
+#pragma unroll
+          for (int dd = 0; dd < 2; ++dd)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const float u = BIAS_MFMA ? acc[dd][f][j] : acc[dd][f][j] + bz[f];
+              const bool pos = u > 0.f;
+              bal[dd][j] = __ballot(pos);
+              s = fmaf(pos ? 1.f : alpha, u, s);
             }
-            const long long vrow = (((long long)n * p.od + vd) * p.oh + vh) * p.ow;
-            if (NF == 1 && vw0 + 8 <= p.ow && ((vrow + vw0) & 7) == 0) {
-              uint4 pk;
-              pk.x = words[0] | ((uint32_t)words[1] << 16);
-              pk.y = words[2] | ((uint32_t)words[3] << 16);
-              pk.z = words[4] | ((uint32_t)words[5] << 16);
-              pk.w = words[6] | ((uint32_t)words[7] << 16);
-              *reinterpret_cast<uint4 *>(mask16 + (vrow + vw0)) = pk;
-            } else {
+          // pooled voxel (pd, ph, pw + q): the whole window sits in this lane
+          if (pin) out[pbase + 16 * f + r] = from_f32<DT>(s * 0.125f);
+          if constexpr (NF == 1) {
+            // the eight ballots of the pair go to LDS as they are (one lane writes);
+            // the row's mask words are interleaved from them after the last pair
+            if (lane == 0) {
 #pragma unroll
-              for (int k = 0; k < 8; ++k)
-                if (vw0 + k < p.ow) mask16[(vrow + vw0 + k) * NF + f] = words[k];
+              for (int dd = 0; dd < 2; ++dd)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) bstage[wave][bw8 * 8 + dd * 4 + j] = bal[dd][j];
+            }
+          } else {
+            // general channel count: lanes 0..3 write mask row (dd, hh) as half-words
+            if (lane < 4) {
+              const int dd = lane >> 1, hh = lane & 1;
+              const int vd = vd0 + dd, vh = vh0 + hh;
+              if (vd < p.od && vh < p.oh) {
+                const uint64_t b0 = dd ? (hh ? bal[1][2] : bal[1][0]) : (hh ? bal[0][2] : bal[0][0]);
+                const uint64_t b1 = dd ? (hh ? bal[1][3] : bal[1][1]) : (hh ? bal[0][3] : bal[0][1]);
+                const long long vrow = (((long long)n * p.od + vd) * p.oh + vh) * p.ow;
+#pragma unroll
+                for (int k = 0; k < 8; ++k) {
+                  const uint64_t bb = (k & 1) ? b1 : b0;
+                  if (vw0 + k < p.ow) mask16[(vrow + vw0 + k) * NF + f] = (uint16_t)((bb >> (16 * (k >> 1))) & 0xffffu);
+                }
+              }
             }
           }
         }
       }
+    }
+    if constexpr (FUSED && NF == 1) {
+      // lanes 0..31: the 16 bytes of mask row k = (dd, hh) = (lane & 3) for
+      // voxels w = 8 b8 .. 8 b8 + 7, b8 = lane >> 2.  Ballot bit 16 q + c is
+      // channel c of voxel w = 2q + parity, parity = which of the two ballots:
+      // the row is the ballots' 16-bit words interleaved, even voxel first.
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      if (lane < 32) {
+        const int k = lane & 3, b8 = lane >> 2;
+        const uint64_t be = bstage[wave][b8 * 8 + (k >> 1) * 4 + 2 * (k & 1)];
+        const uint64_t bo = bstage[wave][b8 * 8 + (k >> 1) * 4 + 2 * (k & 1) + 1];
+        const uint32_t el = (uint32_t)be, eh = (uint32_t)(be >> 32), ol = (uint32_t)bo, oh = (uint32_t)(bo >> 32);
+        uint4 mw;
+        mw.x = __builtin_amdgcn_perm(ol, el, 0x05040100u);  // w0 | w1 << 16
+        mw.y = __builtin_amdgcn_perm(ol, el, 0x07060302u);  // w2 | w3 << 16
+        mw.z = __builtin_amdgcn_perm(oh, eh, 0x05040100u);
+        mw.w = __builtin_amdgcn_perm(oh, eh, 0x07060302u);
+        const int vd = vd0 + (k >> 1), vh = vh0 + (k & 1), vw = ow0 + 8 * b8;
+        if (vd < p.od && vh < p.oh) {
+          const long long vrow = (((long long)n * p.od + vd) * p.oh + vh) * p.ow;
+          if (vw + 8 <= p.ow && ((vrow + vw) & 7) == 0) {
+            *reinterpret_cast<uint4 *>(mask16 + (vrow + vw)) = mw;
+          } else {
+            const uint32_t words[4] = {mw.x, mw.y, mw.z, mw.w};
+#pragma unroll
+            for (int k2 = 0; k2 < 8; ++k2)
+              if (vw + k2 < p.ow) mask16[vrow + vw + k2] = (uint16_t)((words[k2 >> 1] >> (16 * (k2 & 1))) & 0xffffu);
+          }
+        }
+      }
+      // the next row's ballots overwrite the stage only after every lane has read it
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
   }
 }

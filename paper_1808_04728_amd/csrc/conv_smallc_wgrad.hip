@@ -263,6 +263,207 @@ __global__ __launch_bounds__(256) void smallc_wgrad_fused_kernel(
   }
 }
 
+// ---------------------------------------------------------------------------
+// One input channel, bf16: dz built straight in MFMA-operand registers.
+//
+// With s = alpha + (1 - alpha) * mask the weight gradient splits into
+//     dW = alpha/8 * sum_v x~[v+t] dp[pool(v)] + (1-alpha)/8 * sum_v x~[v+t] (dp[pool(v)] & mask(v))
+// (dp/8 * s(v) = dz exactly), so neither term needs per-element arithmetic
+// beyond a bit mask: the B operand of the first term is the pooled gradient
+// with every value twice (one per voxel of the w-pair), that of the second the
+// same with the masked-off halves cleared.  A transposing LDS read
+// (ds_read_b64_tr_b16) hands every lane the four pooled values of its channel
+// for its eight voxels; the lane's 16 mask bytes come straight from global
+// memory.  An extra A row of ones makes the bias gradient db = sum_v dz a row
+// of the same MFMA accumulators.  The input halo is staged once per kw shift
+// (16-byte rows of 8 voxels, built from aligned 16-byte loads with byte
+// alignment shifts), so every A fragment is one 16-byte LDS read.
+// ---------------------------------------------------------------------------
+
+typedef short v4i16_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16_t lds_v4i16_t;
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));  // a plain 16-byte vector
+
+template <int KE, int PW>
+__global__ __launch_bounds__(256) void l1_wgrad_kernel(const uint16_t *__restrict__ x,
+                                                       const uint16_t *__restrict__ dp,
+                                                       const uint16_t *__restrict__ mask16, float alpha,
+                                                       float *__restrict__ part_w, float *__restrict__ part_b,
+                                                       SmallcParams p) {
+  constexpr int HD = TD + KE - 1, HH = TH + KE - 1;
+  constexpr int M = KE * KE * KE;  // weight-gradient rows; row M carries the bias gradient
+  constexpr int MF = 2;
+  static_assert(M + 1 <= 16 * MF, "rows");
+  constexpr int PLANE = HD * HH;                 // 64-byte rows per shifted copy
+  constexpr int XROWS = (KE + 2) * PLANE;        // KE copies, a plane of ones, a plane of zeros
+  constexpr int NXI = PLANE * 4;                 // staging items: (row, 16-byte output vector)
+  static_assert(NXI <= 256, "one staging item per thread");
+  constexpr int XP = 5;  // 16-byte slots per staged row: 4 used, 1 of padding against bank conflicts
+  __shared__ __attribute__((aligned(16))) uint4 xs[XROWS * XP];
+  __shared__ __attribute__((aligned(16))) uint4 dps[2 * 4 * 16 * 2];  // pooled [pd][ph][pw][16 ch]
+  __shared__ __attribute__((aligned(16))) uint4 mks[TD * TH * 4];      // mask [w-row][8-voxel group]
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int r = lane & 15, q = lane >> 4;
+  const int tiles_w = (p.ow + TW - 1) / TW, tiles_h = (p.oh + TH - 1) / TH, tiles_d = (p.od + TD - 1) / TD;
+  const int tiles_per_n = tiles_w * tiles_h * tiles_d;
+  const long long total_tiles = (long long)p.n * tiles_per_n;
+
+  // the constant planes: ones (A row M) and zeros (A rows beyond M)
+  for (int e = tid; e < 2 * PLANE * XP; e += 256)
+    xs[KE * PLANE * XP + e] = e < PLANE * XP ? make_uint4(0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u)
+                                             : make_uint4(0, 0, 0, 0);
+
+  // per-lane A plane offsets (64-byte rows): tap (kd, kh, kw) -> copy kw, plane row (kd, kh)
+  int arow[MF];
+#pragma unroll
+  for (int mf = 0; mf < MF; ++mf) {
+    const int t = 16 * mf + r;
+    if (t < M) {
+      const int kd = t / (KE * KE), kh = (t / KE) % KE, kw = t % KE;
+      arow[mf] = (kw * HD + kd) * HH + kh;
+    } else {
+      arow[mf] = (t == M ? KE : KE + 1) * PLANE;
+    }
+  }
+  // per-lane part of the transposing dp read: pooled voxel 4q + r/4, channels 4 (r%4) ..
+  const int dpoff = (4 * q + (r >> 2)) * 32 + 8 * (r & 3);
+
+  f32x4_t acc_u[MF], acc_m[MF];
+#pragma unroll
+  for (int mf = 0; mf < MF; ++mf) acc_u[mf] = acc_m[mf] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  // Tile pipeline: the global loads of tile it+1 (into registers) are issued
+  // right after tile it's data reached LDS, so their latency overlaps tile
+  // it's MFMAs; LDS is single-buffered (written only between two barriers).
+  const int xa = tid / (HH * 4), xb = (tid / 4) % HH, xi = tid & 3;
+  u32x4_t xv[3], dv, mv;
+  int cur_n = 0, cur_od0 = 0, cur_oh0 = 0, cur_ow0 = 0;
+  auto tile_origin = [&](int it, int &n, int &od0, int &oh0, int &ow0) -> bool {
+    const long long gt = (long long)blockIdx.x * p.tiles_per_block + it;
+    if (it >= p.tiles_per_block || gt >= total_tiles) return false;
+    int t = (int)(gt % tiles_per_n);
+    n = (int)(gt / tiles_per_n);
+    const int tw = t % tiles_w; t /= tiles_w;
+    const int th = t % tiles_h;
+    const int td = t / tiles_h;
+    od0 = td * TD; oh0 = th * TH; ow0 = tw * TW;
+    return true;
+  };
+  auto load_tile = [&](int n, int od0, int oh0, int ow0) {
+    // input: item (row a,b; output vector i) needs window vectors i .. i+2 of
+    // the aligned window [ow0 - 8, ow0 + 40) of its row
+#pragma unroll
+    for (int j = 0; j < 3; ++j) xv[j] = u32x4_t{0u, 0u, 0u, 0u};
+    if (tid < NXI) {
+      const int id = od0 - p.pd + xa, ih = oh0 - p.ph + xb;
+      if ((unsigned)id < (unsigned)p.d && (unsigned)ih < (unsigned)p.h) {
+        const long long rowoff = (((long long)n * p.d + id) * p.h + ih) * p.w;
+#pragma unroll
+        for (int j = 0; j < 3; ++j) {
+          const int iw = ow0 - 8 + 8 * (xi + j);
+          if (iw >= 0 && iw < p.w) xv[j] = *reinterpret_cast<const u32x4_t *>(x + rowoff + iw);
+        }
+      }
+    }
+    // pooled gradient: pooled voxel (pd0 + tid>>7, ph0 + (tid>>5)&3, pw0 + (tid>>1)&15), 8 channels
+    dv = u32x4_t{0u, 0u, 0u, 0u};
+    {
+      const int pd_ = (od0 >> 1) + (tid >> 7), ph_ = (oh0 >> 1) + ((tid >> 5) & 3), pw_ = (ow0 >> 1) + ((tid >> 1) & 15);
+      if (pd_ < p.pod && ph_ < p.poh && pw_ < p.pow_)
+        dv = *reinterpret_cast<const u32x4_t *>(dp + ((((long long)n * p.pod + pd_) * p.poh + ph_) * p.pow_ + pw_) *
+                                                      16 + 8 * (tid & 1));
+    }
+    // slope mask: thread tid < 128 loads 8 voxels (16 bytes) of w-row tid / 4
+    mv = u32x4_t{0u, 0u, 0u, 0u};
+    if (tid < 128) {
+      const int row = tid >> 2;
+      const int vd = od0 + row / TH, vh = oh0 + row % TH, vw = ow0 + 8 * (tid & 3);
+      if (vd < p.od && vh < p.oh && vw < p.ow)
+        mv = *reinterpret_cast<const u32x4_t *>(mask16 + (((long long)n * p.od + vd) * p.oh + vh) * p.ow + vw);
+    }
+  };
+
+  bool have = tile_origin(0, cur_n, cur_od0, cur_oh0, cur_ow0);
+  if (have) load_tile(cur_n, cur_od0, cur_oh0, cur_ow0);
+  for (int it = 0; have; ++it) {
+    // ---- LDS: shifted input copies, the pooled-gradient tile, the mask tile
+    if (tid < NXI) {
+      const uint32_t dw[12] = {xv[0][0], xv[0][1], xv[0][2], xv[0][3], xv[1][0], xv[1][1],
+                               xv[1][2], xv[1][3], xv[2][0], xv[2][1], xv[2][2], xv[2][3]};
+#pragma unroll
+      for (int kw = 0; kw < KE; ++kw) {
+        // copy kw, element i of a row = window element 8 - PW + kw + i
+        const int s0 = 8 - PW + kw;
+        uint32_t o[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int L = (s0 >> 1) + k;
+          o[k] = (s0 & 1) ? __builtin_amdgcn_alignbyte(dw[L + 1], dw[L], 2) : dw[L];
+        }
+        xs[((kw * HD + xa) * HH + xb) * XP + xi] = make_uint4(o[0], o[1], o[2], o[3]);
+      }
+    }
+    dps[tid] = make_uint4(dv[0], dv[1], dv[2], dv[3]);
+    if (tid < 128) mks[tid] = make_uint4(mv[0], mv[1], mv[2], mv[3]);
+    __syncthreads();
+    int nn = 0, nd0 = 0, nh0 = 0, nw0 = 0;
+    have = tile_origin(it + 1, nn, nd0, nh0, nw0);
+    if (have) load_tile(nn, nd0, nh0, nw0);
+
+    // ---- MFMA over this wave's eight w-rows of 32 voxels ------------------
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int row = wave + 4 * k;
+      const int ld = row / TH, lh = row % TH;
+      const unsigned char *dpb = reinterpret_cast<const unsigned char *>(dps) + ((ld >> 1) * 4 + (lh >> 1)) * 512;
+      const v4i16_t g = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t *)(dpb + dpoff));
+      const uint32_t p0 = (uint32_t)(uint16_t)g[0] | ((uint32_t)(uint16_t)g[1] << 16);
+      const uint32_t p1 = (uint32_t)(uint16_t)g[2] | ((uint32_t)(uint16_t)g[3] << 16);
+      uint32_t bu[4], bm[4];
+      bu[0] = __builtin_amdgcn_perm(p0, p0, 0x01000100u);
+      bu[1] = __builtin_amdgcn_perm(p0, p0, 0x03020302u);
+      bu[2] = __builtin_amdgcn_perm(p1, p1, 0x01000100u);
+      bu[3] = __builtin_amdgcn_perm(p1, p1, 0x03020302u);
+      const uint4 mq = mks[row * 4 + q];
+      const uint32_t mk[4] = {mq.x, mq.y, mq.z, mq.w};
+      // mask dword d holds channel bits of voxels 2d (bits 0..15) and 2d+1 (16..31):
+      // move bit r and bit 16+r to the two sign positions, spread each over its half
+      typedef short v2i16_t __attribute__((ext_vector_type(2)));
+#pragma unroll
+      for (int d = 0; d < 4; ++d) {
+        const v2i16_t sg = __builtin_bit_cast(v2i16_t, mk[d] << (15 - r)) >> (v2i16_t){15, 15};
+        bm[d] = bu[d] & __builtin_bit_cast(uint32_t, sg);
+      }
+      const bf16x8_t Bu = __builtin_bit_cast(bf16x8_t, make_uint4(bu[0], bu[1], bu[2], bu[3]));
+      const bf16x8_t Bm = __builtin_bit_cast(bf16x8_t, make_uint4(bm[0], bm[1], bm[2], bm[3]));
+#pragma unroll
+      for (int mf = 0; mf < MF; ++mf) {
+        const bf16x8_t a = __builtin_bit_cast(bf16x8_t, xs[(arow[mf] + ld * HH + lh) * XP + q]);
+        acc_u[mf] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, Bu, acc_u[mf], 0, 0, 0);
+        acc_m[mf] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, Bm, acc_m[mf], 0, 0, 0);
+      }
+    }
+    __syncthreads();
+  }
+
+  // ---- combine the two terms and the four waves; write the partials ------
+  float *red = reinterpret_cast<float *>(xs);  // [wave][32 rows][16 channels]
+  const float cu = 0.125f * alpha, cm = 0.125f * (1.f - alpha);
+#pragma unroll
+  for (int mf = 0; mf < MF; ++mf)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      red[(wave * 32 + 16 * mf + 4 * q + j) * 16 + r] = cu * acc_u[mf][j] + cm * acc_m[mf][j];
+  __syncthreads();
+  for (int i = tid; i < (M + 1) * 16; i += 256) {
+    const float v = red[i] + red[512 + i] + red[1024 + i] + red[1536 + i];
+    if (i < M * 16) part_w[(long long)blockIdx.x * M * 16 + i] = v;
+    else part_b[(long long)blockIdx.x * 16 + (i - M * 16)] = v;
+  }
+}
+
 struct WPlan {
   int tpb;
   int blocks;
@@ -293,6 +494,14 @@ hipError_t launch_t(const ConvShape &s, const SmallcParams &p, const void *x, co
   return launch_sum_rows(pb, db, blocks, s.co, st);
 }
 
+// the register-built-dz kernel: one input channel, 16 output channels, bf16,
+// rows of whole 16-byte vectors, left padding of at most one voxel
+bool l1_supported(const ConvShape &s) {
+  return s.dtype == DT_BF16 && s.ci == 1 && s.co == 16 && s.sd == 1 && s.sh == 1 && s.sw == 1 && s.kd == s.kh &&
+         s.kd == s.kw && (s.kd == 2 || s.kd == 3) && s.pw <= 1 && (s.kd == 3 || s.pw == 0) && s.w % 8 == 0 &&
+         s.ow % 8 == 0;
+}
+
 }  // namespace
 
 bool smallc_wgrad_fused_supported(const ConvShape &s) {
@@ -319,7 +528,24 @@ hipError_t launch_smallc_wgrad_fused(const ConvShape &s, const void *x, const vo
   p.pod = s.od / 2; p.poh = s.oh / 2; p.pow_ = s.ow / 2;
   p.tiles_per_block = w.tpb;
   const int M = s.kd * s.kh * s.kw * s.ci;
-  (void)M;
+  if (l1_supported(s)) {
+    float *pw = (float *)ws;
+    float *pb = pw + (size_t)w.blocks * M * s.co;
+    if (s.kd == 2)
+      hipLaunchKernelGGL((l1_wgrad_kernel<2, 0>), dim3(w.blocks), dim3(256), 0, st, (const uint16_t *)x,
+                         (const uint16_t *)dp, mask, alpha, pw, pb, p);
+    else if (s.pw == 0)
+      hipLaunchKernelGGL((l1_wgrad_kernel<3, 0>), dim3(w.blocks), dim3(256), 0, st, (const uint16_t *)x,
+                         (const uint16_t *)dp, mask, alpha, pw, pb, p);
+    else
+      hipLaunchKernelGGL((l1_wgrad_kernel<3, 1>), dim3(w.blocks), dim3(256), 0, st, (const uint16_t *)x,
+                         (const uint16_t *)dp, mask, alpha, pw, pb, p);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    e = launch_sum_rows(pw, dw, w.blocks, M * s.co, st);
+    if (e != hipSuccess) return e;
+    return launch_sum_rows(pb, db, w.blocks, s.co, st);
+  }
   if (s.kd == 2) {
     if (s.dtype == DT_BF16) {
       if (s.ci == 1) return launch_t<DT_BF16, 1, 1, 1, 2>(s, p, x, dp, mask, alpha, dw, db, ws, w.blocks, st);

@@ -32,6 +32,10 @@ FWD_CASES = [
     (2, (9, 7, 33), 16, 32, 4),      # ragged tiles in every dimension
     (1, (10, 10, 40), 16, 32, 3),
     (1, (10, 10, 10), 16, 32, 2),
+    (2, (16, 12, 40), 1, 16, 3),     # several 32-wide tiles, overhang in w
+    (1, (9, 7, 16), 1, 16, 3),       # odd extents: floor pooling, ragged tiles in d and h
+    (3, (6, 10, 8), 1, 16, 3),       # rows of one 16-byte vector
+    (1, (10, 6, 24), 1, 16, 2),      # 2^3 kernel, asymmetric SAME
 ]
 
 
