@@ -44,7 +44,9 @@ struct C16 {
   static constexpr int HALO_VEC = HD * HH * 2 * HW;           // 16-byte vectors (8 channels)
   static constexpr int TAPS = KE * KE * KE;
   static constexpr int W_VEC = TAPS * 2 * 32;                 // [tap][ci/8][co] x 8 ci
-  static constexpr int LDS_BYTES = (HALO_VEC + W_VEC) * 16;
+  // per wave: the slope-ballot stage (16 x 8 bytes) and 64 junk slots (+ 15 x 8 of offsets)
+  static constexpr int MSTAGE_WAVE = 128 + 4 * 64 + 8 * 16;
+  static constexpr int LDS_BYTES = (HALO_VEC + W_VEC) * 16 + 4 * MSTAGE_WAVE;
 };
 
 template <int KE, int EPI>
@@ -210,25 +212,43 @@ __global__ __launch_bounds__(256, 1) void conv_c16_fwd_kernel(const uint16_t *__
           }
         }
     } else {
-      // u = acc + b; mask word per voxel (32 channel bits); y = lrelu(u)
+      // u = acc + b; y = lrelu(u); the slope mask word of a voxel (32 channel
+      // bits) is half of a wave ballot of one accumulator register.  Every lane
+      // stores ballot >> (32 * half) to LDS without a branch (a branch would
+      // have to keep the compare alive across it): lanes 0 and 32 into the
+      // wave's stage (dword 2 j + half), every other lane into a private junk
+      // slot.  After the 16 registers of an output row, 32 lanes write the
+      // row's 128 mask bytes at once.
+      unsigned char *mst = reinterpret_cast<unsigned char *>(wp + G::W_VEC) + wave * G::MSTAGE_WAVE;
+      const int mslot = (lane & 31) == 0 ? 4 * half : 128 + 4 * lane;
 #pragma unroll
       for (int dd = 0; dd < 2; ++dd)
 #pragma unroll
         for (int hh = 0; hh < TH; ++hh) {
           const int vd = vd0 + dd, vh = oh0 + hh;
-          uint32_t word = 0;
 #pragma unroll
           for (int j = 0; j < 16; ++j) {
             const float u = acc[dd][hh][j] + bz;
             const unsigned long long bal = __ballot(u > 0.f);
-            // lane j holds the voxel of half 0, lane 32 + j the voxel of half 1
-            if (lane == j) word = (uint32_t)bal;
-            if (lane == 32 + j) word = (uint32_t)(bal >> 32);
-            acc[dd][hh][j] = u > 0.f ? u : alpha * u;
+            *reinterpret_cast<uint32_t *>(mst + mslot + 8 * j) = (uint32_t)(bal >> (32 * half));
+            // leaky ReLU without a compare (a select would keep one lane mask per
+            // register alive until the pooling below)
+            acc[dd][hh][j] = fmaxf(u, 0.f) + alpha * fminf(u, 0.f);
           }
-          if (mask != nullptr && col < 16 && vd < p.od && vh < p.oh) {
-            const int vw = ow0 + 8 * (col >> 2) + 4 * half + (col & 3);
-            if (vw < p.ow) mask[(((long long)n * p.od + vd) * p.oh + vh) * p.ow + vw] = word;
+          if (mask != nullptr) {
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            // row voxel v = lane: register j = 4 (v / 8) + v % 4 of half (v / 4) % 2
+            const int v = lane;
+            if (v < 32 && vd < p.od && vh < p.oh && ow0 + v < p.ow) {
+              const uint32_t word =
+                  *reinterpret_cast<const uint32_t *>(mst + 4 * (2 * (4 * (v >> 3) + (v & 3)) + ((v >> 2) & 1)));
+              mask[(((long long)n * p.od + vd) * p.oh + vh) * p.ow + ow0 + v] = word;
+            }
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
           }
         }
       if constexpr (EPI == 1) {  // y, no pool
