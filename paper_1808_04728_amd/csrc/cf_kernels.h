@@ -37,6 +37,7 @@ struct C16Params {
   int pd, ph, pw;
   int od, oh, ow;
   int pod, poh, pow_;
+  int x_bytes;  // forward: extent of the range-checked input buffer
 };
 bool c16_fwd_supported(const ConvShape &s);
 // backward data of the same layers (conv_c16_bwd.hip); fused: g is the pooled-output

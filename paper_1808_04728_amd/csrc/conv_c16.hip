@@ -36,29 +36,32 @@ namespace {
 
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
-constexpr int TD = 8, TH = 4, TW = 32;  // output tile (voxels); wave brick = 2 x 4 x 32
+constexpr int TD = 8, TH = 4, TW = 32;  // output tile (voxels)
+constexpr int NWAVE = 8;                // wave (dp, hp) owns the 2 x 2 x 32 brick d = 2dp.., h = 2hp..
+constexpr int BH = 2;                   // brick rows per wave
 
 template <int KE>
 struct C16 {
   static constexpr int HD = TD + KE - 1, HH = TH + KE - 1, HW = TW + KE - 1;
   static constexpr int HALO_VEC = HD * HH * 2 * HW;           // 16-byte vectors (8 channels)
+  static constexpr int HALO_PAD = (HALO_VEC + 63) / 64 * 64;  // whole 64-slot DMA chunks
   static constexpr int TAPS = KE * KE * KE;
   static constexpr int W_VEC = TAPS * 2 * 32;                 // [tap][ci/8][co] x 8 ci
   // per wave: the slope-ballot stage (16 x 8 bytes) and 64 junk slots (+ 15 x 8 of offsets)
   static constexpr int MSTAGE_WAVE = 128 + 4 * 64 + 8 * 16;
-  static constexpr int LDS_BYTES = (HALO_VEC + W_VEC) * 16 + 4 * MSTAGE_WAVE;
+  static constexpr int LDS_BYTES = (HALO_PAD + W_VEC) * 16 + 8 * MSTAGE_WAVE;
 };
 
 template <int KE, int EPI>
-__global__ __launch_bounds__(256, 1) void conv_c16_fwd_kernel(const uint16_t *__restrict__ x,
+__global__ __launch_bounds__(512, 1) void conv_c16_fwd_kernel(const uint16_t *__restrict__ x,
                                                               const uint16_t *__restrict__ w,
                                                               const float *__restrict__ bias, float alpha,
                                                               uint16_t *__restrict__ out,
                                                               uint32_t *__restrict__ mask, C16Params p) {
   using G = C16<KE>;
   extern __shared__ __attribute__((aligned(16))) uint4 smem[];
-  uint4 *halo = smem;                 // [HD][HH][2][HW]
-  uint4 *wp = smem + G::HALO_VEC;     // [TAPS][2][32]
+  uint4 *halo = smem;                 // [HD][HH][2][HW] (+ padding to whole DMA chunks)
+  uint4 *wp = smem + G::HALO_PAD;     // [TAPS][2][32]
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int col = lane & 31, half = lane >> 5;
@@ -67,17 +70,17 @@ __global__ __launch_bounds__(256, 1) void conv_c16_fwd_kernel(const uint16_t *__
   // item = (tap, ci, 8-channel group of co): one 16-byte load, eight 2-byte LDS stores
   {
     constexpr int ITEMS = G::TAPS * 16 * 4;
-    constexpr int PER = (ITEMS + 255) / 256;
+    constexpr int PER = (ITEMS + 64 * NWAVE - 1) / (64 * NWAVE);
     uint4 wv[PER];
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
-      const int e = tid + 256 * k;
+      const int e = tid + 64 * NWAVE * k;
       wv[k] = e < ITEMS ? *reinterpret_cast<const uint4 *>(w + (long long)e * 8) : make_uint4(0, 0, 0, 0);
     }
     uint16_t *wp16 = reinterpret_cast<uint16_t *>(wp);
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
-      const int e = tid + 256 * k;
+      const int e = tid + 64 * NWAVE * k;
       if (e >= ITEMS) continue;
       const int cg = e & 3, ci = (e >> 2) & 15, tap = e >> 6;
       Vec16<DT_BF16> v;
@@ -96,35 +99,38 @@ __global__ __launch_bounds__(256, 1) void conv_c16_fwd_kernel(const uint16_t *__
   float bz = 0.f;
   if constexpr (EPI != 0) bz = bias[col];
 
-  // The next tile's halo is fetched into registers while the current tile
-  // computes (global loads in flight across the MFMA loop).
-  constexpr int NPRE = (G::HALO_VEC + 255) / 256;
-  uint4 pre[NPRE];
-  auto fetch = [&](int t) {
+  // Halo staging by buffer -> LDS DMA (buffer_load_dwordx4 ... lds): wave w
+  // fills 64-slot chunks w, w + 8, ... of the halo, lane l slot 64 c + l.  A
+  // padding voxel gets a byte offset past the input buffer, which the range
+  // check turns into zeros.  The next tile's DMA is issued once every wave has
+  // finished reading the halo and completes during the epilogue -- no
+  // registers hold it.
+  const __amdgpu_buffer_rsrc_t xrsrc =
+      __builtin_amdgcn_make_buffer_rsrc((void *)x, (short)0, p.x_bytes, 0x00020000);
+  constexpr int NCHUNK = G::HALO_PAD / 64;
+  auto issue_halo = [&](int t) {
     int r = t;
     const int tw = r % tiles_w; r /= tiles_w;
     const int th = r % tiles_h; r /= tiles_h;
     const int td = r % tiles_d;
     const int n = r / tiles_d;
     const int od0 = td * TD, oh0 = th * TH, ow0 = tw * TW;
-#pragma unroll
-    for (int k = 0; k < NPRE; ++k) {
-      const int e = tid + 256 * k;
-      const int hf = e & 1;
-      int v = e >> 1;
-      const int hw = v % G::HW; v /= G::HW;
-      const int hh = v % G::HH;
-      const int hd = v / G::HH;
+    for (int c = wave; c < NCHUNK; c += NWAVE) {
+      const int s = 64 * c + lane;
+      const int hw = s % G::HW;
+      const int t1 = s / G::HW;
+      const int hf = t1 & 1, t2 = t1 >> 1;
+      const int hh = t2 % G::HH, hd = t2 / G::HH;
       const int id = od0 - p.pd + hd, ih = oh0 - p.ph + hh, iw = ow0 - p.pw + hw;
-      uint4 val = make_uint4(0, 0, 0, 0);
-      if (e < G::HALO_VEC && (unsigned)id < (unsigned)p.d && (unsigned)ih < (unsigned)p.h &&
-          (unsigned)iw < (unsigned)p.w)
-        val = *reinterpret_cast<const uint4 *>(x + ((((long long)n * p.d + id) * p.h + ih) * p.w + iw) * 16 + 8 * hf);
-      pre[k] = val;
+      uint32_t off = 0x80000000u;
+      if (s < G::HALO_VEC && (unsigned)id < (unsigned)p.d && (unsigned)ih < (unsigned)p.h && (unsigned)iw < (unsigned)p.w)
+        off = (uint32_t)((((n * p.d + id) * p.h + ih) * p.w + iw) * 32 + 16 * hf);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(xrsrc, (__attribute__((address_space(3))) void *)(halo + 64 * c), 16,
+                                               off, 0, 0, 0);
     }
   };
   auto tile_of = [&](int i) { return xcd * per + i; };
-  if (slot < per && tile_of(slot) < tiles) fetch(tile_of(slot));
+  if (slot < per && tile_of(slot) < tiles) issue_halo(tile_of(slot));
 
   for (int i = slot;; i += per_xcd_blocks) {
     const int t = tile_of(i);
@@ -136,73 +142,73 @@ __global__ __launch_bounds__(256, 1) void conv_c16_fwd_kernel(const uint16_t *__
     const int n = r / tiles_d;
     const int od0 = td * TD, oh0 = th * TH, ow0 = tw * TW;
 
-    __syncthreads();  // previous tile's fragment reads are done (and the packed weights visible)
-#pragma unroll
-    for (int k = 0; k < NPRE; ++k) {
-      const int e = tid + 256 * k;
-      if (e >= G::HALO_VEC) continue;
-      const int hf = e & 1;
-      int v = e >> 1;
-      const int hw = v % G::HW; v /= G::HW;
-      const int hh = v % G::HH;
-      const int hd = v / G::HH;
-      halo[((hd * G::HH + hh) * 2 + hf) * G::HW + hw] = pre[k];
-    }
+    // this wave's halo DMA has landed; after the barrier every wave's has (and
+    // the packed weights are visible)
+    __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0)
     __syncthreads();
-    {
-      const int inext = i + per_xcd_blocks;
-      if (inext < per && tile_of(inext) < tiles) fetch(tile_of(inext));
-    }
 
-    // ---- 2 x 4 x 32 brick of this wave ------------------------------------
-    f32x16_t acc[2][TH];
+    // ---- 2 x 2 x 32 brick of this wave ------------------------------------
+    const int dp2 = wave >> 1, hp2 = wave & 1;  // brick planes 2 dp2 + dd, rows 2 hp2 + hh
+    f32x16_t acc[2][BH];
 #pragma unroll
     for (int a = 0; a < 2; ++a)
 #pragma unroll
-      for (int b = 0; b < TH; ++b)
+      for (int b = 0; b < BH; ++b)
 #pragma unroll
         for (int j = 0; j < 16; ++j) acc[a][b][j] = 0.f;
 
-    for (int kd = 0; kd < KE; ++kd) {
+    // (kd, kw) steps, software-pipelined: the fragment reads of step s + 1 go
+    // into the other register set before the MFMAs of step s are issued
+    bf16x8_t bfr[2][KE];
+    bf16x8_t afr[2][2][BH + KE - 1];
+    auto load_step = [&](int st, bf16x8_t(&b)[KE], bf16x8_t(&a)[2][BH + KE - 1]) {
+      const int kd = st / KE, kw = st % KE;
 #pragma unroll
-      for (int kw = 0; kw < KE; ++kw) {
-        // issue every fragment read of this (kd, kw) step first, so LDS latency
-        // overlaps the MFMA chain (one wave per SIMD: nothing else hides it)
-        bf16x8_t bfr[KE];
-        bf16x8_t afr[2][TH + KE - 1];
+      for (int kh = 0; kh < KE; ++kh)
+        b[kh] = __builtin_bit_cast(bf16x8_t, wp[(((kd * KE + kh) * KE + kw) * 2 + half) * 32 + col]);
 #pragma unroll
-        for (int kh = 0; kh < KE; ++kh)
-          bfr[kh] = __builtin_bit_cast(bf16x8_t, wp[(((kd * KE + kh) * KE + kw) * 2 + half) * 32 + col]);
+      for (int dd = 0; dd < 2; ++dd)
 #pragma unroll
-        for (int dd = 0; dd < 2; ++dd)
+        for (int hi = 0; hi < BH + KE - 1; ++hi)
+          a[dd][hi] = __builtin_bit_cast(
+              bf16x8_t, halo[(((2 * dp2 + dd + kd) * G::HH + 2 * hp2 + hi) * 2 + half) * G::HW + kw + col]);
+    };
+    auto mfma_step = [&](const bf16x8_t(&b)[KE], const bf16x8_t(&a)[2][BH + KE - 1]) {
 #pragma unroll
-          for (int hi = 0; hi < TH + KE - 1; ++hi)
-            afr[dd][hi] = __builtin_bit_cast(
-                bf16x8_t, halo[(((2 * wave + dd + kd) * G::HH + hi) * 2 + half) * G::HW + kw + col]);
+      for (int dd = 0; dd < 2; ++dd)
 #pragma unroll
-        for (int dd = 0; dd < 2; ++dd) {
+        for (int hi = 0; hi < BH + KE - 1; ++hi)
 #pragma unroll
-          for (int hi = 0; hi < TH + KE - 1; ++hi) {
-#pragma unroll
-            for (int kh = 0; kh < KE; ++kh) {
-              const int hrow = hi - kh;
-              if (hrow >= 0 && hrow < TH)
-                acc[dd][hrow] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(afr[dd][hi], bfr[kh], acc[dd][hrow], 0, 0, 0);
-            }
+          for (int kh = 0; kh < KE; ++kh) {
+            const int hrow = hi - kh;
+            if (hrow >= 0 && hrow < BH)
+              acc[dd][hrow] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[dd][hi], b[kh], acc[dd][hrow], 0, 0, 0);
           }
-        }
-      }
+    };
+    constexpr int NSTEP = KE * KE;
+    load_step(0, bfr[0], afr[0]);
+#pragma unroll
+    for (int st = 0; st < NSTEP; ++st) {
+      if (st + 1 < NSTEP) load_step(st + 1, bfr[(st + 1) & 1], afr[(st + 1) & 1]);
+      mfma_step(bfr[st & 1], afr[st & 1]);
+    }
+
+    // every wave is done with the halo: the next tile's DMA overlaps the epilogue
+    __syncthreads();
+    {
+      const int inext = i + per_xcd_blocks;
+      if (inext < per && tile_of(inext) < tiles) issue_halo(tile_of(inext));
     }
 
     // ---- epilogue ----------------------------------------------------------
     // acc[dd][h][j]: channel col, voxel w = ow0 + 8*(j/4) + 4*half + (j%4)
-    const int vd0 = od0 + 2 * wave;
+    const int vd0 = od0 + 2 * dp2, vh0 = oh0 + 2 * hp2;
     if constexpr (EPI == 0) {
 #pragma unroll
       for (int dd = 0; dd < 2; ++dd)
 #pragma unroll
-        for (int hh = 0; hh < TH; ++hh) {
-          const int vd = vd0 + dd, vh = oh0 + hh;
+        for (int hh = 0; hh < BH; ++hh) {
+          const int vd = vd0 + dd, vh = vh0 + hh;
           if (vd >= p.od || vh >= p.oh) continue;
           const long long rowv = (((long long)n * p.od + vd) * p.oh + vh) * p.ow;
 #pragma unroll
@@ -224,8 +230,8 @@ __global__ __launch_bounds__(256, 1) void conv_c16_fwd_kernel(const uint16_t *__
 #pragma unroll
       for (int dd = 0; dd < 2; ++dd)
 #pragma unroll
-        for (int hh = 0; hh < TH; ++hh) {
-          const int vd = vd0 + dd, vh = oh0 + hh;
+        for (int hh = 0; hh < BH; ++hh) {
+          const int vd = vd0 + dd, vh = vh0 + hh;
 #pragma unroll
           for (int j = 0; j < 16; ++j) {
             const float u = acc[dd][hh][j] + bz;
@@ -255,8 +261,8 @@ __global__ __launch_bounds__(256, 1) void conv_c16_fwd_kernel(const uint16_t *__
 #pragma unroll
         for (int dd = 0; dd < 2; ++dd)
 #pragma unroll
-          for (int hh = 0; hh < TH; ++hh) {
-            const int vd = vd0 + dd, vh = oh0 + hh;
+          for (int hh = 0; hh < BH; ++hh) {
+            const int vd = vd0 + dd, vh = vh0 + hh;
             if (vd >= p.od || vh >= p.oh) continue;
             const long long rowv = (((long long)n * p.od + vd) * p.oh + vh) * p.ow;
 #pragma unroll
@@ -268,8 +274,8 @@ __global__ __launch_bounds__(256, 1) void conv_c16_fwd_kernel(const uint16_t *__
       } else {  // 2^3 average pool: window = (dd 0..1) x (h pair) x (w pair), all in this lane
         const int pd_ = vd0 >> 1;
 #pragma unroll
-        for (int hp = 0; hp < TH / 2; ++hp) {
-          const int ph_ = (oh0 >> 1) + hp;
+        for (int hp = 0; hp < BH / 2; ++hp) {
+          const int ph_ = (vh0 >> 1) + hp;
           if (pd_ >= p.pod || ph_ >= p.poh) continue;
           const long long prow = (((long long)n * p.pod + pd_) * p.poh + ph_) * p.pow_;
 #pragma unroll
@@ -304,7 +310,7 @@ hipError_t launch_t(const C16Params &p, const void *x, const void *w, const floa
   const long long tiles = (long long)p.n * ((p.od + TD - 1) / TD) * ((p.oh + TH - 1) / TH) * ((p.ow + TW - 1) / TW);
   int blocks = (int)std::min<long long>(tiles, cus);
   blocks = std::max(8, (blocks + 7) / 8 * 8);
-  hipLaunchKernelGGL((conv_c16_fwd_kernel<KE, EPI>), dim3(blocks), dim3(256), G::LDS_BYTES, st,
+  hipLaunchKernelGGL((conv_c16_fwd_kernel<KE, EPI>), dim3(blocks), dim3(64 * NWAVE), G::LDS_BYTES, st,
                      (const uint16_t *)x, (const uint16_t *)w, bias, alpha, (uint16_t *)out, mask, p);
   return hipGetLastError();
 }
@@ -313,7 +319,8 @@ hipError_t launch_t(const C16Params &p, const void *x, const void *w, const floa
 
 bool c16_fwd_supported(const ConvShape &s) {
   return s.dtype == DT_BF16 && s.ci == 16 && s.co == 32 && s.sd == 1 && s.sh == 1 && s.sw == 1 &&
-         s.kd == s.kh && s.kd == s.kw && s.kd >= 2 && s.kd <= 4;
+         s.kd == s.kh && s.kd == s.kw && s.kd >= 2 && s.kd <= 4 &&
+         (long long)s.n * s.d * s.h * s.w * s.ci * 2 < (1LL << 31);  // 32-bit buffer offsets
 }
 
 hipError_t launch_conv_fwd_c16(const ConvShape &s, const void *x, const void *w, const float *bias, float alpha,
@@ -323,6 +330,7 @@ hipError_t launch_conv_fwd_c16(const ConvShape &s, const void *x, const void *w,
   p.pd = s.pd; p.ph = s.ph; p.pw = s.pw;
   p.od = s.od; p.oh = s.oh; p.ow = s.ow;
   p.pod = s.od / 2; p.poh = s.oh / 2; p.pow_ = s.ow / 2;
+  p.x_bytes = (int)((long long)s.n * s.d * s.h * s.w * s.ci * 2);
 #define CF_C16_CASE(KEV)                                                                      \
   if (s.kd == KEV) {                                                                          \
     if (epi == 0) return launch_t<KEV, 0>(p, x, w, bias, alpha, out, mask, st);               \
