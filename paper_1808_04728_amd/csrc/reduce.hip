@@ -49,6 +49,59 @@ __global__ __launch_bounds__(256) void sum_rows_kernel(const float *__restrict__
   if (ph == 0 && c < cols) out[c] = red[tid];
 }
 
+// 16-byte variant (cols % 4 == 0, 16-byte aligned rows): thread (phase, q)
+// owns four consecutive columns, CQ = 256 / PH quads per workgroup, so a wave
+// reads row segments of 16 * CQ bytes with float4 loads.
+template <int PH>
+__global__ __launch_bounds__(256) void sum_rows4_kernel(const float4 *__restrict__ part, float4 *__restrict__ out,
+                                                        int rows, int cols4) {
+  constexpr int CQ = 256 / PH;
+  __shared__ float4 red[256];
+  const int tid = threadIdx.x;
+  const int cq = tid % CQ, ph = tid / CQ;
+  const int c = blockIdx.x * CQ + cq;
+  float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (c < cols4) {
+    int r = ph;
+    for (; r + 3 * PH < rows; r += 4 * PH) {
+      const float4 a0 = part[(long long)r * cols4 + c];
+      const float4 a1 = part[(long long)(r + PH) * cols4 + c];
+      const float4 a2 = part[(long long)(r + 2 * PH) * cols4 + c];
+      const float4 a3 = part[(long long)(r + 3 * PH) * cols4 + c];
+      s.x += a0.x; s.y += a0.y; s.z += a0.z; s.w += a0.w;
+      s.x += a1.x; s.y += a1.y; s.z += a1.z; s.w += a1.w;
+      s.x += a2.x; s.y += a2.y; s.z += a2.z; s.w += a2.w;
+      s.x += a3.x; s.y += a3.y; s.z += a3.z; s.w += a3.w;
+    }
+    for (; r < rows; r += PH) {
+      const float4 a = part[(long long)r * cols4 + c];
+      s.x += a.x; s.y += a.y; s.z += a.z; s.w += a.w;
+    }
+  }
+  red[tid] = s;
+  __syncthreads();
+#pragma unroll
+  for (int st = PH / 2; st > 0; st /= 2) {
+    if (ph < st) {
+      const float4 o = red[tid + st * CQ];
+      float4 m = red[tid];
+      m.x += o.x; m.y += o.y; m.z += o.z; m.w += o.w;
+      red[tid] = m;
+    }
+    __syncthreads();
+  }
+  if (ph == 0 && c < cols4) out[c] = red[tid];
+}
+
+template <int PH>
+hipError_t launch_ph4(const float *part, float *out, int rows, int cols, hipStream_t st) {
+  constexpr int CQ = 256 / PH;
+  const int cols4 = cols / 4;
+  hipLaunchKernelGGL((sum_rows4_kernel<PH>), dim3((cols4 + CQ - 1) / CQ), dim3(256), 0, st,
+                     reinterpret_cast<const float4 *>(part), reinterpret_cast<float4 *>(out), rows, cols4);
+  return hipGetLastError();
+}
+
 template <int PH>
 hipError_t launch_ph(const float *part, float *out, int rows, int cols, hipStream_t st) {
   constexpr int CPB = 256 / PH;
@@ -60,9 +113,26 @@ hipError_t launch_ph(const float *part, float *out, int rows, int cols, hipStrea
 
 hipError_t launch_sum_rows(const float *part, float *out, int rows, int cols, hipStream_t st) {
   if (cols <= 0) return hipSuccess;
-  // enough phases that each thread sums at most ~16 rows
+  // wide, 16-byte aligned: float4 columns; phases so that a thread sums ~32 rows,
+  // at least 16 (256-byte row segments per wave) once rows are many
+  if (cols % 4 == 0 && ((uintptr_t)part & 15) == 0 && ((uintptr_t)out & 15) == 0 && cols >= 256) {
+    int ph = 1;
+    while (ph < 64 && (long long)ph * 32 < rows) ph *= 2;
+    switch (ph) {
+      case 1: return launch_ph4<1>(part, out, rows, cols, st);
+      case 2: return launch_ph4<2>(part, out, rows, cols, st);
+      case 4: return launch_ph4<4>(part, out, rows, cols, st);
+      case 8: return launch_ph4<8>(part, out, rows, cols, st);
+      case 16: return launch_ph4<16>(part, out, rows, cols, st);
+      case 32: return launch_ph4<32>(part, out, rows, cols, st);
+      default: return launch_ph4<64>(part, out, rows, cols, st);
+    }
+  }
+  // enough phases that each thread sums at most ~16 rows (~4 when the matrix is
+  // narrow: few workgroups, so the serial chain per thread is the latency)
+  const int per = cols < 256 ? 4 : 16;
   int ph = 1;
-  while (ph < 256 && (long long)ph * 16 < rows) ph *= 2;
+  while (ph < 256 && (long long)ph * per < rows) ph *= 2;
   switch (ph) {
     case 1: return launch_ph<1>(part, out, rows, cols, st);
     case 2: return launch_ph<2>(part, out, rows, cols, st);
