@@ -38,6 +38,8 @@ struct C16Params {
   int od, oh, ow;
   int pod, poh, pow_;
   int x_bytes;  // forward: extent of the range-checked input buffer
+  int g_bytes;  // backward-data: extent of dz (or of the pooled gradient, fused)
+  int m_bytes;  // backward-data, fused: extent of the slope mask
 };
 bool c16_fwd_supported(const ConvShape &s);
 // backward data of the same layers (conv_c16_bwd.hip); fused: g is the pooled-output
