@@ -112,6 +112,8 @@ def main():
     ap.add_argument("--workload", default="stack_128c_b8_bf16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--op-breakdown", action="store_true", help="print per-op times to stderr")
+    ap.add_argument("--unfused", action="store_true",
+                    help="run every layer through the unfused entry points (conv, bias + lReLU, pool separately)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run 5 plain device copies of MIB MiB (calibrates the HBM byte counters)")
     args = ap.parse_args()
@@ -133,7 +135,7 @@ def main():
     name = args.workload
     wl = inputs.WORKLOADS[name]
     torch.cuda.set_device(0)
-    st = ConvStack(wl["layers"], wl["size"], wl["batch"], wl["dtype"], inputs.ALPHA, "cuda:0")
+    st = ConvStack(wl["layers"], wl["size"], wl["batch"], wl["dtype"], inputs.ALPHA, "cuda:0", fused=not args.unfused)
     ws, bs = inputs.make_weights(name)
     st.set_params(ws, bs)
     st.set_input(inputs.make_input(name))
@@ -202,7 +204,8 @@ def main():
         "vs_baseline": None,
         "dtype": wl["dtype"],
         "data": "synthetic",
-        "config": {"workload": describe(name, wl), "name": name, "edge": wl["size"], "batch": wl["batch"],
+        "config": {"workload": describe(name, wl) + (", unfused entry points" if args.unfused else ""),
+                   "name": name, "edge": wl["size"], "batch": wl["batch"],
                    "input_channels": wl["c0"], "conv_gflop_per_step": round(flops / 1e9, 3)},
         "samples_per_s": round(wl["batch"] / (ms * 1e-3), 2),
         "mfma_peak_frac": round(tflops / peak, 4),
