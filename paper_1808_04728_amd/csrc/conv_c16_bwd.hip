@@ -293,14 +293,14 @@ __global__ __launch_bounds__(256, 2) void c16_dgrad_kernel(const uint16_t *__res
       for (int b = 0; b < TH; ++b) acc[a][b] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     const uint4 *abase = halo + q * G::PLANE + (slot * G::WD + grp * G::KD0) * G::HH * G::HW + r16;
     // A fragments stream through a ring PF reads ahead of their MFMAs; the
-    // scheduling groups pin the order (one LDS read, then the MFMAs of the
-    // fragment read PF steps earlier)
+    // interleaving strategy keeps several LDS reads in flight between MFMAs
     constexpr int NPL = G::WD + G::KD0 - 1, NR = TH + KE - 1, NA = KE * NPL * NR, PF = 3;
     auto aload = [&](int i) {
       const int kw = i / (NPL * NR), pl = (i / NR) % NPL, r = i % NR;
       return __builtin_bit_cast(bf16x8_t, abase[(pl * G::HH + r) * G::HW + kw]);
     };
     bf16x8_t ar[PF + 1];
+    __builtin_amdgcn_iglp_opt(1);
 #pragma unroll
     for (int i = 0; i < PF; ++i) ar[i] = aload(i);
 #pragma unroll
@@ -312,7 +312,6 @@ __global__ __launch_bounds__(256, 2) void c16_dgrad_kernel(const uint16_t *__res
           const int i = (kw * NPL + pl) * NR + r;
           if (i + PF < NA) {
             ar[(i + PF) % (PF + 1)] = aload(i + PF);
-            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
           }
 #pragma unroll
           for (int od = 0; od < G::WD; ++od) {
@@ -324,7 +323,6 @@ __global__ __launch_bounds__(256, 2) void c16_dgrad_kernel(const uint16_t *__res
               if (orow < 0 || orow >= TH) continue;
               acc[od][orow] =
                   __builtin_amdgcn_mfma_f32_16x16x32_bf16(ar[i % (PF + 1)], bw[kdl][kh][kw], acc[od][orow], 0, 0, 0);
-              __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // then this fragment's MFMAs
             }
           }
         }
