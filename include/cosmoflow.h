@@ -166,7 +166,8 @@ cf_status cf_avgpool3d_bwd(int32_t n, int32_t d, int32_t h, int32_t w, int32_t c
 
 /* Bitmask of the fused entry points that accept (desc, flags) on this build:
  * 1 = cf_conv3d_fwd_fused, 2 = cf_conv3d_bwd_weight_fused,
- * 4 = cf_conv3d_bwd_data_fused.  Host-only; 0 on an invalid desc. */
+ * 4 = cf_conv3d_bwd_data_fused, 8 = cf_conv3d_bwd_weight_fused_dz.
+ * Host-only; 0 on an invalid desc. */
 int32_t cf_conv3d_fused_supported(const cf_conv3d_desc *desc, uint32_t flags);
 
 /* Bytes of the slope mask of a layer: one bit per element of the conv output
@@ -201,6 +202,20 @@ size_t cf_conv3d_bwd_weight_fused_workspace_size(const cf_conv3d_desc *desc, uin
 cf_status cf_conv3d_bwd_weight_fused(const cf_conv3d_desc *desc, const void *x, const void *g,
                                      const void *mask, float alpha, uint32_t flags, float *dw,
                                      float *db, void *ws, size_t ws_bytes, void *stream);
+
+/* Fused backward-weights that also stores the rebuilt dz (bit 8 of
+ * cf_conv3d_fused_supported; CF_FUSE_POOL2 required).  dW, db and ws exactly
+ * as cf_conv3d_bwd_weight_fused (bitwise the same results); in addition dz
+ * [n,od,oh,ow,c_out] in dtype receives every element of the rebuilt
+ * gradient, rounded as described there -- the input a following
+ * cf_conv3d_bwd_data call needs, which then returns the same dx bits as
+ * cf_conv3d_bwd_data_fused.  The tiles of the weight-gradient pass partition
+ * dz, so each element is built and stored once; dz must not overlap any
+ * other argument (CF_ERR_ALIAS).  NULL dz is CF_ERR_INVALID_ARG. */
+cf_status cf_conv3d_bwd_weight_fused_dz(const cf_conv3d_desc *desc, const void *x, const void *g,
+                                        const void *mask, float alpha, uint32_t flags, float *dw,
+                                        float *db, void *dz, void *ws, size_t ws_bytes,
+                                        void *stream);
 
 /* Fused backward-data (CF_FUSE_POOL2 required): dz is rebuilt from the
  * pooled-output gradient g and the slope mask exactly as in

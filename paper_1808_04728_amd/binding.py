@@ -22,7 +22,7 @@ CF_OK, CF_ERR_INVALID_ARG, CF_ERR_UNSUPPORTED, CF_ERR_ALIGNMENT, CF_ERR_ALIAS, \
 CF_F32, CF_BF16 = 0, 1
 CF_PAD_SAME_TF, CF_PAD_VALID = 0, 1
 CF_FUSE_POOL2 = 1
-FUSED_FWD, FUSED_BWD_WEIGHT, FUSED_BWD_DATA = 1, 2, 4
+FUSED_FWD, FUSED_BWD_WEIGHT, FUSED_BWD_DATA, FUSED_BWD_WEIGHT_DZ = 1, 2, 4, 8
 
 STATUS_NAMES = {0: "CF_OK", 1: "CF_ERR_INVALID_ARG", 2: "CF_ERR_UNSUPPORTED", 3: "CF_ERR_ALIGNMENT",
                 4: "CF_ERR_ALIAS", 5: "CF_ERR_WORKSPACE", 6: "CF_ERR_LAUNCH"}
@@ -33,7 +33,8 @@ EXPORTS = [
     "cf_conv3d_bwd_weight_workspace_size", "cf_conv3d_bwd_weight", "cf_bias_lrelu_fwd",
     "cf_bias_lrelu_bwd_workspace_size", "cf_bias_lrelu_bwd", "cf_avgpool3d_fwd", "cf_avgpool3d_bwd",
     "cf_conv3d_fused_supported", "cf_conv3d_mask_bytes", "cf_conv3d_fwd_fused",
-    "cf_conv3d_bwd_weight_fused_workspace_size", "cf_conv3d_bwd_weight_fused", "cf_conv3d_bwd_data_fused",
+    "cf_conv3d_bwd_weight_fused_workspace_size", "cf_conv3d_bwd_weight_fused", "cf_conv3d_bwd_weight_fused_dz",
+    "cf_conv3d_bwd_data_fused",
 ]
 
 
@@ -80,6 +81,8 @@ def lib():
         "cf_conv3d_fwd_fused": ([D, vp, vp, vp, f32, ctypes.c_uint32, vp, vp, vp], ctypes.c_int),
         "cf_conv3d_bwd_weight_fused_workspace_size": ([D, ctypes.c_uint32], sz),
         "cf_conv3d_bwd_weight_fused": ([D, vp, vp, vp, f32, ctypes.c_uint32, vp, vp, vp, sz, vp], ctypes.c_int),
+        "cf_conv3d_bwd_weight_fused_dz": ([D, vp, vp, vp, f32, ctypes.c_uint32, vp, vp, vp, vp, sz, vp],
+                                          ctypes.c_int),
         "cf_conv3d_bwd_data_fused": ([D, vp, vp, vp, f32, ctypes.c_uint32, vp, vp], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
@@ -210,6 +213,13 @@ def cf_conv3d_bwd_weight_fused(desc, x, g, mask, alpha, flags, dw, db, ws, ws_by
         ws_bytes = 0 if ws is None or isinstance(ws, int) else ws.numel() * ws.element_size()
     _check(lib().cf_conv3d_bwd_weight_fused(ctypes.byref(desc), _ptr(x), _ptr(g), _ptr(mask), alpha, flags,
                                             _ptr(dw), _ptr(db), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def cf_conv3d_bwd_weight_fused_dz(desc, x, g, mask, alpha, flags, dw, db, dz, ws, ws_bytes=None, stream=None):
+    if ws_bytes is None:
+        ws_bytes = 0 if ws is None or isinstance(ws, int) else ws.numel() * ws.element_size()
+    _check(lib().cf_conv3d_bwd_weight_fused_dz(ctypes.byref(desc), _ptr(x), _ptr(g), _ptr(mask), alpha, flags,
+                                               _ptr(dw), _ptr(db), _ptr(dz), _ptr(ws), ws_bytes, _stream(stream)))
 
 
 def cf_conv3d_bwd_data_fused(desc, g, mask, w, alpha, flags, dx, stream=None):

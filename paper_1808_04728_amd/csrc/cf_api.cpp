@@ -320,6 +320,7 @@ static int32_t fused_mask(const cf::ConvShape &s, uint32_t flags) {
   if (cf::c16_fwd_supported(s)) m |= 1;  // with or without the pool
   if (flags == 0 && cf::direct_supported(s, true)) m |= 1;
   if (flags == CF_FUSE_POOL2 && cf::c16_bwd_supported(s)) m |= 4;
+  if (flags == CF_FUSE_POOL2 && cf::c16_wgrad_supported(s) && !cf::smallc_wgrad_fused_supported(s)) m |= 8;
   return m;
 }
 
@@ -401,28 +402,28 @@ size_t cf_conv3d_bwd_weight_fused_workspace_size(const cf_conv3d_desc *desc, uin
   return fused_wgrad_workspace(s);
 }
 
-cf_status cf_conv3d_bwd_weight_fused(const cf_conv3d_desc *desc, const void *x, const void *g, const void *mask,
-                                     float alpha, uint32_t flags, float *dw, float *db, void *ws, size_t ws_bytes,
-                                     void *stream) {
+static cf_status bwd_weight_fused(const char *name, const cf_conv3d_desc *desc, const void *x, const void *g,
+                                  const void *mask, float alpha, uint32_t flags, float *dw, float *db, void *dz,
+                                  void *ws, size_t ws_bytes, void *stream) {
   cf::ConvShape s;
   cf_status r = resolve(desc, &s);
   if (r != CF_OK) return r;
   if (!std::isfinite(alpha) || alpha < 0.f) return fail(CF_ERR_INVALID_ARG, "alpha must be finite and >= 0");
   if (flags & ~CF_FUSE_POOL2) return fail(CF_ERR_INVALID_ARG, "unknown flags");
-  if (!(fused_mask(s, flags) & 2))
-    return fail(CF_ERR_UNSUPPORTED, "conv3d_bwd_weight_fused: no fused kernel for this layer shape / flags");
+  if (!(fused_mask(s, flags) & (dz ? 8 : 2)))
+    return fail(CF_ERR_UNSUPPORTED, std::string(name) + ": no fused kernel for this layer shape / flags");
   hipStream_t st = (hipStream_t)stream;
   const size_t dw_bytes = (size_t)s.kd * s.kh * s.kw * s.ci * s.co * sizeof(float);
   if (s.n == 0) {
     if ((r = check_ptrs({dw, db})) != CF_OK) return r;
     hipError_t e = cf::launch_fill_zero(dw, (long long)(dw_bytes / 4), st);
     if (e == hipSuccess) e = cf::launch_fill_zero(db, s.co, st);
-    return finish(e, st, "cf_conv3d_bwd_weight_fused");
+    return finish(e, st, name);
   }
   if ((r = check_ptrs({x, g, mask, dw, db})) != CF_OK) return r;
+  if (dz && (r = check_ptrs({dz})) != CF_OK) return r;
   const size_t need = fused_wgrad_workspace(s);
-  if (!ws || ws_bytes < need)
-    return fail(CF_ERR_WORKSPACE, "conv3d_bwd_weight_fused: workspace smaller than the size query");
+  if (!ws || ws_bytes < need) return fail(CF_ERR_WORKSPACE, std::string(name) + ": workspace smaller than the size query");
   if (!aligned16(ws)) return fail(CF_ERR_ALIGNMENT, "workspace not 16-byte aligned");
   Sizes b = conv_bytes(s);
   const size_t gb = pooled_bytes(s), mb = mask_bytes(s), dbb = (size_t)s.co * 4;
@@ -430,16 +431,32 @@ cf_status cf_conv3d_bwd_weight_fused(const cf_conv3d_desc *desc, const void *x, 
   const size_t insz[3] = {b.x, gb, mb};
   for (int i = 0; i < 3; ++i)
     if (overlap(dw, dw_bytes, ins[i], insz[i]) || overlap(db, dbb, ins[i], insz[i]) ||
-        overlap(ws, need, ins[i], insz[i]))
-      return fail(CF_ERR_ALIAS, "conv3d_bwd_weight_fused: an output or the workspace overlaps an input");
+        overlap(ws, need, ins[i], insz[i]) || (dz && overlap(dz, b.z, ins[i], insz[i])))
+      return fail(CF_ERR_ALIAS, std::string(name) + ": an output or the workspace overlaps an input");
   if (overlap(dw, dw_bytes, db, dbb) || overlap(ws, need, dw, dw_bytes) || overlap(ws, need, db, dbb))
-    return fail(CF_ERR_ALIAS, "conv3d_bwd_weight_fused: outputs / workspace overlap");
+    return fail(CF_ERR_ALIAS, std::string(name) + ": outputs / workspace overlap");
+  if (dz && (overlap(dz, b.z, dw, dw_bytes) || overlap(dz, b.z, db, dbb) || overlap(dz, b.z, ws, need)))
+    return fail(CF_ERR_ALIAS, std::string(name) + ": dz overlaps another output or the workspace");
   const hipError_t e =
       cf::smallc_wgrad_fused_supported(s)
           ? cf::launch_smallc_wgrad_fused(s, x, g, (const uint16_t *)mask, alpha, dw, db, ws, st)
-          : cf::launch_conv_bwd_weight_c16(s, x, g, (const uint32_t *)mask, alpha, dw, db, ws, true, st);
-  return finish(e,  st,
-                "cf_conv3d_bwd_weight_fused");
+          : cf::launch_conv_bwd_weight_c16(s, x, g, (const uint32_t *)mask, alpha, dw, db, ws, true, dz, st);
+  return finish(e, st, name);
+}
+
+cf_status cf_conv3d_bwd_weight_fused(const cf_conv3d_desc *desc, const void *x, const void *g, const void *mask,
+                                     float alpha, uint32_t flags, float *dw, float *db, void *ws, size_t ws_bytes,
+                                     void *stream) {
+  return bwd_weight_fused("cf_conv3d_bwd_weight_fused", desc, x, g, mask, alpha, flags, dw, db, nullptr, ws,
+                          ws_bytes, stream);
+}
+
+cf_status cf_conv3d_bwd_weight_fused_dz(const cf_conv3d_desc *desc, const void *x, const void *g, const void *mask,
+                                        float alpha, uint32_t flags, float *dw, float *db, void *dz, void *ws,
+                                        size_t ws_bytes, void *stream) {
+  if (!dz && desc && desc->n > 0) return fail(CF_ERR_INVALID_ARG, "cf_conv3d_bwd_weight_fused_dz: dz is NULL");
+  return bwd_weight_fused("cf_conv3d_bwd_weight_fused_dz", desc, x, g, mask, alpha, flags, dw, db, dz, ws,
+                          ws_bytes, stream);
 }
 
 cf_status cf_conv3d_bwd_data_fused(const cf_conv3d_desc *desc, const void *g, const void *mask, const void *w,

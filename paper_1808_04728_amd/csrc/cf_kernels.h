@@ -45,11 +45,13 @@ bool c16_fwd_supported(const ConvShape &s);
 // backward data of the same layers (conv_c16_bwd.hip); fused: g is the pooled-output
 // gradient and mask the forward's slope mask, else g is dz
 bool c16_bwd_supported(const ConvShape &s);
-// backward weights of the 4^3 16 -> 32 layer (conv_c16_wgrad.hip); fused as above, db only when fused
+// backward weights of the 4^3 16 -> 32 layer (conv_c16_wgrad.hip); fused as above, db only when fused;
+// dz_out (fused only, may be null) receives the rebuilt dz [n,od,oh,ow,32] in bf16
 bool c16_wgrad_supported(const ConvShape &s);
 size_t c16_wgrad_workspace(const ConvShape &s);
 hipError_t launch_conv_bwd_weight_c16(const ConvShape &s, const void *x, const void *g, const uint32_t *mask,
-                                      float alpha, float *dw, float *db, void *ws, bool fused, hipStream_t st);
+                                      float alpha, float *dw, float *db, void *ws, bool fused, void *dz_out,
+                                      hipStream_t st);
 hipError_t launch_conv_bwd_data_c16(const ConvShape &s, const void *g, const uint32_t *mask, const void *w,
                                     float alpha, void *dx, bool fused, hipStream_t st);
 hipError_t launch_conv_fwd_c16(const ConvShape &s, const void *x, const void *w, const float *bias, float alpha,

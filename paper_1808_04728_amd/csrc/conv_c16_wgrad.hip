@@ -25,7 +25,10 @@
 //
 // Fused variant: dz is rebuilt from the pooled-output gradient and the slope
 // mask while staging (rounded to bf16 as the unfused path stores it), and the
-// bias gradient is summed from the unrounded values in the same pass.
+// bias gradient is summed from the unrounded values in the same pass.  The
+// tiles partition dz, so every element is built exactly once; when the caller
+// asks for it, the staged dz is also written out (one 16-byte store per staged
+// unit) for a following backward-data pass.
 
 #include "cf_common.h"
 #include "cf_kernels.h"
@@ -60,7 +63,7 @@ __global__ __launch_bounds__(256, 2) void c16_wgrad_kernel(const uint16_t *__res
                                                            const uint16_t *__restrict__ g,
                                                            const uint32_t *__restrict__ mask, float alpha,
                                                            float *__restrict__ part_w, float *__restrict__ part_b,
-                                                           C16Params p) {
+                                                           uint16_t *__restrict__ dz_out, C16Params p) {
   extern __shared__ __attribute__((aligned(16))) uint4 smem[];
   uint4 *xh = smem;                 // [HD][HH][HW][2 x 8 ci]
   uint4 *dzt = smem + XH_VEC;       // [TD][TH][TW][4 x 8 co]
@@ -162,6 +165,10 @@ __global__ __launch_bounds__(256, 2) void c16_wgrad_kernel(const uint16_t *__res
         }
       }
       dzt[tid + 256 * k] = val;  // the tile region is free: every read of it ended at the barrier above
+      if constexpr (FUSED) {
+        if (dz_out && od < p.od && oh < p.oh && ow < p.ow)
+          *reinterpret_cast<uint4 *>(dz_out + ((((long long)n * p.od + od) * p.oh + oh) * p.ow + ow) * 32 + 8 * cq) = val;
+      }
     }
     if constexpr (FUSED) {
       float4 a = dbl[0], b = dbl[1];
@@ -255,7 +262,7 @@ int wgrad_blocks(const C16Params &p) {
 
 template <bool FUSED>
 hipError_t launch_w(const C16Params &p, const void *x, const void *g, const uint32_t *mask, float alpha, float *pw,
-                    float *pb, int blocks, hipStream_t st) {
+                    float *pb, void *dz_out, int blocks, hipStream_t st) {
   static bool attr_set = false;
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute((const void *)c16_wgrad_kernel<FUSED>,
@@ -264,7 +271,7 @@ hipError_t launch_w(const C16Params &p, const void *x, const void *g, const uint
     attr_set = true;
   }
   hipLaunchKernelGGL((c16_wgrad_kernel<FUSED>), dim3(blocks), dim3(256), LDS_BYTES, st, (const uint16_t *)x,
-                     (const uint16_t *)g, mask, alpha, pw, pb, p);
+                     (const uint16_t *)g, mask, alpha, pw, pb, (uint16_t *)dz_out, p);
   return hipGetLastError();
 }
 
@@ -287,14 +294,15 @@ size_t c16_wgrad_workspace(const ConvShape &s) {
 }
 
 hipError_t launch_conv_bwd_weight_c16(const ConvShape &s, const void *x, const void *g, const uint32_t *mask,
-                                      float alpha, float *dw, float *db, void *ws, bool fused, hipStream_t st) {
+                                      float alpha, float *dw, float *db, void *ws, bool fused, void *dz_out,
+                                      hipStream_t st) {
   const C16Params p = params_of(s);
   const int blocks = wgrad_blocks(p);
   const int cols = KE * KE * KE * 16 * 32;
   float *pw = (float *)ws;
   float *pb = pw + (size_t)blocks * cols;
-  hipError_t e = fused ? launch_w<true>(p, x, g, mask, alpha, pw, pb, blocks, st)
-                       : launch_w<false>(p, x, g, mask, alpha, pw, pb, blocks, st);
+  hipError_t e = fused ? launch_w<true>(p, x, g, mask, alpha, pw, pb, dz_out, blocks, st)
+                       : launch_w<false>(p, x, g, mask, alpha, pw, pb, nullptr, blocks, st);
   if (e != hipSuccess) return e;
   e = launch_sum_rows(pw, dw, blocks, cols, st);
   if (e != hipSuccess || !fused) return e;

@@ -651,7 +651,7 @@ size_t conv_bwd_weight_workspace(const ConvShape &s) {
 hipError_t launch_conv_bwd_weight(const ConvShape &s, const void *x, const void *dz, float *dw,
                                   void *ws, hipStream_t st) {
   if (c16_wgrad_supported(s))
-    return launch_conv_bwd_weight_c16(s, x, dz, nullptr, 0.f, dw, nullptr, ws, false, st);
+    return launch_conv_bwd_weight_c16(s, x, dz, nullptr, 0.f, dw, nullptr, ws, false, nullptr, st);
   WgradPlan pl = plan_wgrad(s);
   WgradParams p{};
   p.nb = s.n; p.d = s.d; p.h = s.h; p.w = s.w; p.ci = s.ci;

@@ -73,6 +73,11 @@ class ConvStack:
             l["dx"] = None
             if l["fused"]:
                 l["z"] = l["dy"] = l["dz"] = None
+                # a layer whose data gradient is needed may take dz from its weight-gradient
+                # pass and run the unfused backward-data on it (same dx bits, faster there)
+                l["dz_emit"] = bool(needs_dgrad and sup & B.FUSED_BWD_WEIGHT_DZ)
+                if l["dz_emit"]:
+                    l["dz"] = torch.empty((n,) + l["out_dhw"] + (s["cout"],), dtype=tdt, device=dev)
                 l["mask"] = torch.empty(max(16, B.cf_conv3d_mask_bytes(l["desc"])), dtype=torch.uint8, device=dev)
                 wsf = B.cf_conv3d_bwd_weight_fused_workspace_size(l["desc"], B.CF_FUSE_POOL2)
                 l["ws_w"] = torch.empty(max(wsf, 16), dtype=torch.uint8, device=dev)
@@ -150,6 +155,13 @@ class ConvStack:
             l = self.L[i]
             s = l["spec"]
             c = self._call
+            if l["fused"] and l["dz_emit"]:
+                c(f"L{i+1}.conv_bwd_weight_fused_dz", B.cf_conv3d_bwd_weight_fused_dz, l["desc"],
+                  self.layer_input(i), g, l["mask"], self.alpha, B.CF_FUSE_POOL2, l["dw"], l["db"], l["dz"],
+                  l["ws_w"], None, stream)
+                c(f"L{i+1}.conv_bwd_data", B.cf_conv3d_bwd_data, l["desc"], l["dz"], l["w"], l["dx"], stream)
+                g = l["dx"]
+                continue
             if l["fused"]:
                 c(f"L{i+1}.conv_bwd_weight_fused", B.cf_conv3d_bwd_weight_fused, l["desc"], self.layer_input(i), g,
                   l["mask"], self.alpha, B.CF_FUSE_POOL2, l["dw"], l["db"], l["ws_w"], None, stream)
@@ -207,6 +219,7 @@ class ConvStack:
         op = name.split(".")[1]
         mb = l["nvox"] * s["cout"] // 8
         return {"conv_fwd_fused": xb + wb + pb + mb, "conv_bwd_weight_fused": xb + pb + mb + wb // es * 4,
+                "conv_bwd_weight_fused_dz": xb + pb + mb + wb // es * 4 + zb,
                 "conv_bwd_data_fused": pb + mb + wb + xb,
                 "conv_bias_lrelu_fwd": xb + wb + zb,
                 "conv_fwd": xb + wb + zb, "conv_bwd_data": zb + wb + xb,

@@ -220,3 +220,50 @@ def test_fused_bwd_data(case, dt):
     ref = oracle.conv3d_bwd_data(dz, to_np(w), dhw)
     e = maxabs_err(to_np(dx), ref)
     assert e <= TOL[dt], e
+
+
+@pytest.mark.parametrize("dt", ["bf16"])
+@pytest.mark.parametrize("case", FWD_CASES, ids=lambda c: "n%d_%dx%dx%d_c%d-%d_k%d" % (c[0], *c[1], *c[2:]))
+def test_fused_bwd_weight_dz(case, dt):
+    """Backward-weights that also stores the rebuilt dz: dW, db bitwise equal to
+    the plain fused call, every dz element written and equal to the oracle's
+    dz within the path tolerance, and the unfused backward-data of that dz
+    bitwise equal to the fused backward-data."""
+    N, dhw, CI, CO, k = case
+    desc = B.make_desc(N, dhw, CI, CO, k, 1, "same", dt)
+    if not B.cf_conv3d_fused_supported(desc) & B.FUSED_BWD_WEIGHT_DZ:
+        pytest.skip("no dz-emitting backward-weights kernel for this shape")
+    rng = np.random.default_rng(16)
+    od = B.cf_conv3d_out_shape(desc)
+    pdhw = tuple(t // 2 for t in od)
+    x = dev(rng.standard_normal((N, *dhw, CI)), dt)
+    g = dev(rng.standard_normal((N, *pdhw, CO)), dt)
+    w = dev(rng.standard_normal((k, k, k, CI, CO)) / np.sqrt(k ** 3 * CO), dt)
+    mbytes = B.cf_conv3d_mask_bytes(desc)
+    mask_np = rng.integers(0, 256, mbytes, dtype=np.uint8)
+    mask = torch.as_tensor(mask_np, device="cuda")
+    alpha = 0.2
+    ws = torch.empty(B.cf_conv3d_bwd_weight_fused_workspace_size(desc), dtype=torch.uint8, device="cuda")
+    dw = torch.empty((k, k, k, CI, CO), dtype=torch.float32, device="cuda")
+    db = torch.empty((CO,), dtype=torch.float32, device="cuda")
+    dw2, db2 = torch.empty_like(dw), torch.empty_like(db)
+    dz = torch.full((N, *od, CO), float("nan"), dtype=tdtype(dt), device="cuda")
+    B.cf_conv3d_bwd_weight_fused(desc, x, g, mask, alpha, B.CF_FUSE_POOL2, dw, db, ws)
+    B.cf_conv3d_bwd_weight_fused_dz(desc, x, g, mask, alpha, B.CF_FUSE_POOL2, dw2, db2, dz, ws)
+    dx_f = torch.empty((N, *dhw, CI), dtype=tdtype(dt), device="cuda")
+    dx_u = torch.full_like(dx_f, float("nan"))
+    B.cf_conv3d_bwd_data_fused(desc, g, mask, w, alpha, B.CF_FUSE_POOL2, dx_f)
+    B.cf_conv3d_bwd_data(desc, dz, w, dx_u)
+    torch.cuda.synchronize()
+    assert torch.equal(dw, dw2) and torch.equal(db, db2)
+    nbits = N * od[0] * od[1] * od[2] * CO
+    bits = np.unpackbits(mask_np, bitorder="little")[:nbits].astype(bool).reshape((N, *od, CO))
+    dz_ref = oracle.avgpool3d_bwd(to_np(g), od) * np.where(bits, 1.0, alpha)
+    dz_np = to_np(dz)
+    assert np.isfinite(dz_np).all()
+    e = maxabs_err(dz_np, dz_ref)
+    assert e <= TOL[dt], e
+    assert torch.equal(dx_f, dx_u)
+    ref = oracle.conv3d_bwd_data(dz_ref, to_np(w), dhw)
+    e = maxabs_err(to_np(dx_u), ref)
+    assert e <= TOL[dt], e
