@@ -45,8 +45,9 @@ constexpr int HD = TD + KE - 1, HH = TH + KE - 1, HW = TW + KE - 1;
 constexpr int XH_VEC = HD * HH * HW * 2;    // 16-byte units of the input halo (16 ci = 2 units)
 constexpr int DZ_VEC = TD * TH * TW * 4;    // 16-byte units of the dz tile (32 co = 4 units)
 constexpr int DB_VEC = 256 * 2;             // fused: per-thread running bias sums (8 floats)
-constexpr int LDS_BYTES = (XH_VEC + DZ_VEC + DB_VEC) * 16;
-constexpr int NX = (XH_VEC + 255) / 256, NZ = DZ_VEC / 256;
+constexpr int NXC = (XH_VEC + 255) / 256, NZ = DZ_VEC / 256;  // DMA instructions per wave
+constexpr int XH_PAD = NXC * 256;           // the last DMA instructions write padding slots
+constexpr int LDS_BYTES = (XH_PAD + DZ_VEC + DB_VEC) * 16;
 static_assert(DZ_VEC % 256 == 0, "dz staging");
 
 // two transposing reads -> 8 consecutive voxels of one channel per lane
@@ -66,7 +67,7 @@ __global__ __launch_bounds__(256, 2) void c16_wgrad_kernel(const uint16_t *__res
                                                            uint16_t *__restrict__ dz_out, C16Params p) {
   extern __shared__ __attribute__((aligned(16))) uint4 smem[];
   uint4 *xh = smem;                 // [HD][HH][HW][2 x 8 ci]
-  uint4 *dzt = smem + XH_VEC;       // [TD][TH][TW][4 x 8 co]
+  uint4 *dzt = smem + XH_PAD;       // [TD][TH][TW][4 x 8 co]
   const uint16_t *xh16 = reinterpret_cast<const uint16_t *>(xh);
   const uint16_t *dz16 = reinterpret_cast<const uint16_t *>(dzt);
 
@@ -90,10 +91,38 @@ __global__ __launch_bounds__(256, 2) void c16_wgrad_kernel(const uint16_t *__res
       for (int c = 0; c < 2; ++c) acc[a][b][c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   // fused: running bias-gradient sums of this thread's 8 staged channels live in
   // LDS between tiles, so they hold no registers across the MFMA section
-  float4 *dbl = reinterpret_cast<float4 *>(smem + XH_VEC + DZ_VEC) + 2 * tid;
+  float4 *dbl = reinterpret_cast<float4 *>(smem + XH_PAD + DZ_VEC) + 2 * tid;
   if constexpr (FUSED) {
     dbl[0] = make_float4(0.f, 0.f, 0.f, 0.f);
     dbl[1] = make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+
+  // Input halo by buffer -> LDS DMA: per DMA slot e = 64 * (wave + 4k) + lane
+  // (slot order = the [hd][hh][hw][half] layout), computed once: the byte
+  // offset relative to the halo origin and the packed coordinates
+  // hw | hh << 6 | hd << 9 (31 << 9 marks the padding slots past the halo).
+  const __amdgpu_buffer_rsrc_t xrsrc = __builtin_amdgcn_make_buffer_rsrc((void *)x, (short)0, p.x_bytes, 0x00020000);
+  typedef __attribute__((address_space(3))) void lds_void_t;
+  uint32_t xrel[NXC], xpk[NXC];
+#pragma unroll
+  for (int k = 0; k < NXC; ++k) {
+    const int e = 64 * (wave + 4 * k) + lane;
+    const int hf = e & 1, v = e >> 1;
+    const int hw = v % HW, hh = (v / HW) % HH, hd = v / (HW * HH);
+    xrel[k] = (uint32_t)((((hd * p.h + hh) * p.w + hw) * 16 + 8 * hf) * 2);
+    xpk[k] = e < XH_VEC ? (uint32_t)(hw | hh << 6 | hd << 9) : 31u << 9;
+  }
+  // unfused dz tile likewise: slot e = (voxel of the tile) * 4 + channel quarter
+  const __amdgpu_buffer_rsrc_t grsrc =
+      __builtin_amdgcn_make_buffer_rsrc((void *)g, (short)0, FUSED ? 0 : p.g_bytes, 0x00020000);
+  uint32_t zrel[NZ], zpk[NZ];
+#pragma unroll
+  for (int k = 0; k < NZ; ++k) {
+    const int e = 64 * (wave + 4 * k) + lane;
+    const int cq = e & 3, v = e >> 2;
+    const int lw = v % TW, lh = (v / TW) % TH, ld = v / (TW * TH);
+    zrel[k] = (uint32_t)((((ld * p.oh + lh) * p.ow + lw) * 32 + 8 * cq) * 2);
+    zpk[k] = (uint32_t)(lw | lh << 6 | ld << 9);
   }
 
   for (int i = slot;; i += per_xcd_blocks) {
@@ -106,48 +135,50 @@ __global__ __launch_bounds__(256, 2) void c16_wgrad_kernel(const uint16_t *__res
     const int n = r / tiles_d;
     const int o0d = td * TD, o0h = th * TH, o0w = tw * TW;
 
-    __syncthreads();
-    // ---- stage the input halo and the dz tile (all loads in flight first) ----
-    uint4 xv[NX];
+    __syncthreads();  // every wave is done with the previous tile's LDS
+    // ---- stage the input halo (DMA) and the dz tile ----------------------------
+    {
+      const int x0d = o0d - p.pd, x0h = o0h - p.ph, x0w = o0w - p.pw;  // halo origin (may be < 0)
+      const uint32_t base = (uint32_t)(((n * p.d + x0d) * p.h + x0h) * p.w + x0w) * 32u;
 #pragma unroll
-    for (int k = 0; k < NX; ++k) {
-      const int e = tid + 256 * k;
-      const int hf = e & 1;
-      int v = e >> 1;
-      const int hw = v % HW; v /= HW;
-      const int hh = v % HH;
-      const int hd = v / HH;
-      const int id = o0d - p.pd + hd, ih = o0h - p.ph + hh, iw = o0w - p.pw + hw;
-      uint4 val = make_uint4(0, 0, 0, 0);
-      if (e < XH_VEC && (unsigned)id < (unsigned)p.d && (unsigned)ih < (unsigned)p.h && (unsigned)iw < (unsigned)p.w)
-        val = *reinterpret_cast<const uint4 *>(x + ((((long long)n * p.d + id) * p.h + ih) * p.w + iw) * 16 + 8 * hf);
-      xv[k] = val;
-    }
-    if constexpr (FUSED) {  // the dz rebuild needs registers: retire the halo first
+      for (int k = 0; k < NXC; ++k) {
+        uint32_t pk = xpk[k];
+        asm volatile("" : "+v"(pk));  // keep the decoded fields out of the tile loop's registers
+        const int hw = pk & 63, hh = (pk >> 6) & 7, hd = pk >> 9;
+        const bool ok = pk < (uint32_t)(HD << 9) && (unsigned)(x0w + hw) < (unsigned)p.w &&
+                        (unsigned)(x0h + hh) < (unsigned)p.h && (unsigned)(x0d + hd) < (unsigned)p.d;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(xrsrc, (lds_void_t *)(xh + 64 * (wave + 4 * k)), 16,
+                                                 ok ? xrel[k] + base : 0x80000000u, 0, 0, 0);
+      }
+      if constexpr (!FUSED) {
+        const uint32_t zbase = (uint32_t)(((n * p.od + o0d) * p.oh + o0h) * p.ow + o0w) * 64u;
 #pragma unroll
-      for (int k = 0; k < NX; ++k) {
-        const int e = tid + 256 * k;
-        if (e < XH_VEC) xh[e] = xv[k];
+        for (int k = 0; k < NZ; ++k) {
+          uint32_t pk = zpk[k];
+          asm volatile("" : "+v"(pk));
+          const int lw = pk & 63, lh = (pk >> 6) & 7, ld = pk >> 9;
+          const bool ok = o0w + lw < p.ow && o0h + lh < p.oh && o0d + ld < p.od;
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(grsrc, (lds_void_t *)(dzt + 64 * (wave + 4 * k)), 16,
+                                                   ok ? zrel[k] + zbase : 0x80000000u, 0, 0, 0);
+        }
       }
     }
     float dbs[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) dbs[j] = 0.f;
+    if constexpr (FUSED) {
 #pragma unroll
-    for (int k = 0; k < NZ; ++k) {
-      const int e = tid + 256 * k;  // e & 3: which 8 of the 32 channels (fixed per thread)
-      const int cq = e & 3;
-      int v = e >> 2;
-      const int lw = v % TW; v /= TW;
-      const int lh = v % TH;
-      const int ld = v / TH;
-      const int od = o0d + ld, oh = o0h + lh, ow = o0w + lw;
-      uint4 val = make_uint4(0, 0, 0, 0);
-      if (od < p.od && oh < p.oh && ow < p.ow) {
-        const long long vox = (((long long)n * p.od + od) * p.oh + oh) * p.ow + ow;
-        if constexpr (!FUSED) {
-          val = *reinterpret_cast<const uint4 *>(g + vox * 32 + 8 * cq);
-        } else {
+      for (int k = 0; k < NZ; ++k) {
+        const int e = tid + 256 * k;  // e & 3: which 8 of the 32 channels (fixed per thread)
+        const int cq = e & 3;
+        int v = e >> 2;
+        const int lw = v % TW; v /= TW;
+        const int lh = v % TH;
+        const int ld = v / TH;
+        const int od = o0d + ld, oh = o0h + lh, ow = o0w + lw;
+        uint4 val = make_uint4(0, 0, 0, 0);
+        if (od < p.od && oh < p.oh && ow < p.ow) {
+          const long long vox = (((long long)n * p.od + od) * p.oh + oh) * p.ow + ow;
           const int pd_ = od >> 1, ph_ = oh >> 1, pw_ = ow >> 1;
           if (pd_ < p.pod && ph_ < p.poh && pw_ < p.pow_) {
             Vec16<DT_BF16> gv;
@@ -162,28 +193,17 @@ __global__ __launch_bounds__(256, 2) void c16_wgrad_kernel(const uint16_t *__res
             }
             val = gv.u;
           }
+          if (dz_out) *reinterpret_cast<uint4 *>(dz_out + vox * 32 + 8 * cq) = val;
         }
+        dzt[tid + 256 * k] = val;  // the tile region is free: every read of it ended at the barrier above
       }
-      dzt[tid + 256 * k] = val;  // the tile region is free: every read of it ended at the barrier above
-      if constexpr (FUSED) {
-        if (dz_out && od < p.od && oh < p.oh && ow < p.ow)
-          *reinterpret_cast<uint4 *>(dz_out + ((((long long)n * p.od + od) * p.oh + oh) * p.ow + ow) * 32 + 8 * cq) = val;
-      }
-    }
-    if constexpr (FUSED) {
       float4 a = dbl[0], b = dbl[1];
       a.x += dbs[0]; a.y += dbs[1]; a.z += dbs[2]; a.w += dbs[3];
       b.x += dbs[4]; b.y += dbs[5]; b.z += dbs[6]; b.w += dbs[7];
       dbl[0] = a;
       dbl[1] = b;
     }
-    if constexpr (!FUSED) {
-#pragma unroll
-      for (int k = 0; k < NX; ++k) {
-        const int e = tid + 256 * k;
-        if (e < XH_VEC) xh[e] = xv[k];  // unit e is already the [hd][hh][hw][half] layout
-      }
-    }
+    __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): this wave's DMA has landed
     __syncthreads();
 
     // ---- MFMA: taps kd = wave; reuse A (input row h') over kh ----------------
@@ -243,7 +263,7 @@ __global__ __launch_bounds__(256, 2) void c16_wgrad_kernel(const uint16_t *__res
     // thread's channels: 8 * ((tid) & 3) .. +7 (staging unit e & 3 == tid & 3)
     // slot of thread u holds channels 8 (u & 3) .. +7: sum the 64 threads of each group in order
     __syncthreads();
-    const float *red = reinterpret_cast<const float *>(smem + XH_VEC + DZ_VEC);
+    const float *red = reinterpret_cast<const float *>(smem + XH_PAD + DZ_VEC);
     if (tid < 32) {
       float s = 0.f;
       for (int k = 0; k < 64; ++k) s += red[(4 * k + (tid >> 3)) * 8 + (tid & 7)];
@@ -281,12 +301,17 @@ C16Params params_of(const ConvShape &s) {
   p.pd = s.pd; p.ph = s.ph; p.pw = s.pw;
   p.od = s.od; p.oh = s.oh; p.ow = s.ow;
   p.pod = s.od / 2; p.poh = s.oh / 2; p.pow_ = s.ow / 2;
+  p.x_bytes = (int)((long long)s.n * s.d * s.h * s.w * 16 * 2);
+  p.g_bytes = (int)((long long)s.n * s.od * s.oh * s.ow * 32 * 2);
   return p;
 }
 
 }  // namespace
 
-bool c16_wgrad_supported(const ConvShape &s) { return c16_fwd_supported(s) && s.kd == KE; }
+// 32-bit byte offsets into x and dz
+bool c16_wgrad_supported(const ConvShape &s) {
+  return c16_fwd_supported(s) && s.kd == KE && (long long)s.n * s.od * s.oh * s.ow * 32 * 2 < (1LL << 31);
+}
 
 size_t c16_wgrad_workspace(const ConvShape &s) {
   const int blocks = wgrad_blocks(params_of(s));
