@@ -226,6 +226,59 @@ cf_status cf_conv3d_bwd_data_fused(const cf_conv3d_desc *desc, const void *g, co
                                    const void *w, float alpha, uint32_t flags, void *dx,
                                    void *stream);
 
+/* ------------------------------------------------------------------------
+ * Deferred gradient sums.  Every weight- and bias-gradient entry point ends
+ * with fixed-order column sums of per-workgroup fp32 partials held in its
+ * workspace (dW[c] = sum_r part[r][c], r ascending in a fixed grouping: the
+ * bitwise-reproducible reduction).  Nothing in a backward pass reads dW or db,
+ * so a training step can run those sums for all layers in one launch: the
+ * _deferred variants below do everything their plain counterparts do except
+ * these sums, and describe them in `pending` instead.  Passing the collected
+ * descriptions to cf_reduce_partials (in stream order, before dW / db are
+ * read and before the workspaces are reused) writes exactly the bits the
+ * plain call would have written.
+ * ------------------------------------------------------------------------ */
+
+/* One pending sum: out[c] = sum over r of part[r * cols + c], c < cols. */
+typedef struct cf_reduction {
+  const float *part; /* [rows][cols] fp32 partials (device, in a caller workspace) */
+  float *out;        /* [cols] fp32 result (device) */
+  int32_t rows, cols;
+} cf_reduction;
+
+/* Most pending sums one deferred call records. */
+#define CF_MAX_PENDING 4
+
+/* Runs n pending sums (any mix of layers) in as few launches as possible;
+ * each job's result bits depend only on its partials and (rows, cols).
+ * Pointers 4-byte aligned (CF_ERR_ALIGNMENT); out must not overlap its own
+ * partials (CF_ERR_ALIAS). */
+cf_status cf_reduce_partials(int32_t n, const cf_reduction *jobs, void *stream);
+
+/* cf_conv3d_bwd_weight without the final sums: dW is written by
+ * cf_reduce_partials(*npending, pending).  pending: room for CF_MAX_PENDING
+ * entries (host memory); *npending receives the count (0 when nothing is
+ * pending, e.g. an empty batch, whose dW is written directly). */
+cf_status cf_conv3d_bwd_weight_deferred(const cf_conv3d_desc *desc, const void *x, const void *dz,
+                                        float *dw, void *ws, size_t ws_bytes,
+                                        cf_reduction *pending, int32_t *npending, void *stream);
+
+/* cf_bias_lrelu_bwd without the final bias-gradient sum (dz is written by
+ * this call; db by cf_reduce_partials).  pending / npending as above. */
+cf_status cf_bias_lrelu_bwd_deferred(int64_t nvox, int32_t c, int32_t dtype, const void *dy,
+                                     const void *y, float alpha, void *dz, float *db, void *ws,
+                                     size_t ws_bytes, cf_reduction *pending, int32_t *npending,
+                                     void *stream);
+
+/* cf_conv3d_bwd_weight_fused (dz == NULL) or cf_conv3d_bwd_weight_fused_dz
+ * (dz != NULL: dz is written by this call) without the final sums of dW and
+ * db.  pending / npending as above. */
+cf_status cf_conv3d_bwd_weight_fused_deferred(const cf_conv3d_desc *desc, const void *x,
+                                              const void *g, const void *mask, float alpha,
+                                              uint32_t flags, float *dw, float *db, void *dz,
+                                              void *ws, size_t ws_bytes, cf_reduction *pending,
+                                              int32_t *npending, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

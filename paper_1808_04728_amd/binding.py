@@ -34,7 +34,8 @@ EXPORTS = [
     "cf_bias_lrelu_bwd_workspace_size", "cf_bias_lrelu_bwd", "cf_avgpool3d_fwd", "cf_avgpool3d_bwd",
     "cf_conv3d_fused_supported", "cf_conv3d_mask_bytes", "cf_conv3d_fwd_fused",
     "cf_conv3d_bwd_weight_fused_workspace_size", "cf_conv3d_bwd_weight_fused", "cf_conv3d_bwd_weight_fused_dz",
-    "cf_conv3d_bwd_data_fused",
+    "cf_conv3d_bwd_data_fused", "cf_reduce_partials", "cf_conv3d_bwd_weight_deferred", "cf_bias_lrelu_bwd_deferred",
+    "cf_conv3d_bwd_weight_fused_deferred",
 ]
 
 
@@ -47,6 +48,14 @@ class CfError(RuntimeError):
 class cf_conv3d_desc(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in
                 ("n", "d", "h", "w", "c_in", "c_out", "kd", "kh", "kw", "sd", "sh", "sw", "pad", "dtype")]
+
+
+class cf_reduction(ctypes.Structure):
+    _fields_ = [("part", ctypes.c_void_p), ("out", ctypes.c_void_p), ("rows", ctypes.c_int32),
+                ("cols", ctypes.c_int32)]
+
+
+CF_MAX_PENDING = 4
 
 
 _lib = None
@@ -84,6 +93,14 @@ def lib():
         "cf_conv3d_bwd_weight_fused_dz": ([D, vp, vp, vp, f32, ctypes.c_uint32, vp, vp, vp, vp, sz, vp],
                                           ctypes.c_int),
         "cf_conv3d_bwd_data_fused": ([D, vp, vp, vp, f32, ctypes.c_uint32, vp, vp], ctypes.c_int),
+        "cf_reduce_partials": ([i32, ctypes.POINTER(cf_reduction), vp], ctypes.c_int),
+        "cf_conv3d_bwd_weight_deferred": ([D, vp, vp, vp, vp, sz, ctypes.POINTER(cf_reduction),
+                                           ctypes.POINTER(i32), vp], ctypes.c_int),
+        "cf_bias_lrelu_bwd_deferred": ([i64, i32, i32, vp, vp, f32, vp, vp, vp, sz, ctypes.POINTER(cf_reduction),
+                                        ctypes.POINTER(i32), vp], ctypes.c_int),
+        "cf_conv3d_bwd_weight_fused_deferred": ([D, vp, vp, vp, f32, ctypes.c_uint32, vp, vp, vp, vp, sz,
+                                                 ctypes.POINTER(cf_reduction), ctypes.POINTER(i32), vp],
+                                                ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         f = getattr(L, name)
@@ -225,3 +242,47 @@ def cf_conv3d_bwd_weight_fused_dz(desc, x, g, mask, alpha, flags, dw, db, dz, ws
 def cf_conv3d_bwd_data_fused(desc, g, mask, w, alpha, flags, dx, stream=None):
     _check(lib().cf_conv3d_bwd_data_fused(ctypes.byref(desc), _ptr(g), _ptr(mask), _ptr(w), alpha, flags, _ptr(dx),
                                           _stream(stream)))
+
+
+# ---- deferred gradient sums --------------------------------------------------
+# The _deferred calls return a list of pending cf_reduction jobs (host
+# structures holding device pointers); cf_reduce_partials runs any collection
+# of them.
+
+def _pending_list(arr, n):
+    return [cf_reduction(arr[i].part, arr[i].out, arr[i].rows, arr[i].cols) for i in range(n.value)]
+
+
+def cf_reduce_partials(jobs, stream=None):
+    n = len(jobs)
+    arr = (cf_reduction * max(n, 1))(*jobs)
+    _check(lib().cf_reduce_partials(n, arr, _stream(stream)))
+
+
+def cf_conv3d_bwd_weight_deferred(desc, x, dz, dw, ws, ws_bytes=None, stream=None):
+    if ws_bytes is None:
+        ws_bytes = 0 if ws is None or isinstance(ws, int) else ws.numel() * ws.element_size()
+    arr, n = (cf_reduction * CF_MAX_PENDING)(), ctypes.c_int32(0)
+    _check(lib().cf_conv3d_bwd_weight_deferred(ctypes.byref(desc), _ptr(x), _ptr(dz), _ptr(dw), _ptr(ws), ws_bytes,
+                                               arr, ctypes.byref(n), _stream(stream)))
+    return _pending_list(arr, n)
+
+
+def cf_bias_lrelu_bwd_deferred(nvox, c, dtype, dy, y, alpha, dz, db, ws, ws_bytes=None, stream=None):
+    if ws_bytes is None:
+        ws_bytes = 0 if ws is None or isinstance(ws, int) else ws.numel() * ws.element_size()
+    arr, n = (cf_reduction * CF_MAX_PENDING)(), ctypes.c_int32(0)
+    _check(lib().cf_bias_lrelu_bwd_deferred(nvox, c, dtype_code(dtype), _ptr(dy), _ptr(y), alpha, _ptr(dz), _ptr(db),
+                                            _ptr(ws), ws_bytes, arr, ctypes.byref(n), _stream(stream)))
+    return _pending_list(arr, n)
+
+
+def cf_conv3d_bwd_weight_fused_deferred(desc, x, g, mask, alpha, flags, dw, db, dz, ws, ws_bytes=None,
+                                        stream=None):
+    if ws_bytes is None:
+        ws_bytes = 0 if ws is None or isinstance(ws, int) else ws.numel() * ws.element_size()
+    arr, n = (cf_reduction * CF_MAX_PENDING)(), ctypes.c_int32(0)
+    _check(lib().cf_conv3d_bwd_weight_fused_deferred(ctypes.byref(desc), _ptr(x), _ptr(g), _ptr(mask), alpha, flags,
+                                                     _ptr(dw), _ptr(db), _ptr(dz), _ptr(ws), ws_bytes, arr,
+                                                     ctypes.byref(n), _stream(stream)))
+    return _pending_list(arr, n)

@@ -13,6 +13,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <string>
+#include <vector>
 
 #include "cf_common.h"
 #include "cf_kernels.h"
@@ -120,6 +121,24 @@ cf_status check_ptrs(std::initializer_list<const void *> ptrs) {
   return CF_OK;
 }
 
+}  // namespace
+
+namespace {
+// runs `call` with the fixed-order column sums recorded instead of launched
+template <class F>
+cf_status deferred(cf_reduction *pending, int32_t *npending, F call) {
+  if (!pending || !npending) return fail(CF_ERR_INVALID_ARG, "pending / npending is NULL");
+  *npending = 0;
+  cf::SumCollector col{};
+  cf::set_sum_collector(&col);
+  const cf_status r = call();
+  cf::set_sum_collector(nullptr);
+  if (r != CF_OK) return r;
+  for (int i = 0; i < col.n; ++i)
+    pending[i] = cf_reduction{col.job[i].part, col.job[i].out, col.job[i].rows, col.job[i].cols};
+  *npending = col.n;
+  return CF_OK;
+}
 }  // namespace
 
 extern "C" {
@@ -476,6 +495,56 @@ cf_status cf_conv3d_bwd_data_fused(const cf_conv3d_desc *desc, const void *g, co
   hipStream_t st = (hipStream_t)stream;
   return finish(cf::launch_conv_bwd_data_c16(s, g, (const uint32_t *)mask, w, alpha, dx, true, st), st,
                 "cf_conv3d_bwd_data_fused");
+}
+
+// ---------------------------------------------------------------------------
+// Deferred gradient sums
+// ---------------------------------------------------------------------------
+
+
+cf_status cf_reduce_partials(int32_t n, const cf_reduction *jobs, void *stream) {
+  if (n < 0) return fail(CF_ERR_INVALID_ARG, "n must be >= 0");
+  if (n == 0) return ok();
+  if (!jobs) return fail(CF_ERR_INVALID_ARG, "jobs is NULL");
+  std::vector<cf::SumJob> v;
+  v.reserve(n);
+  for (int32_t i = 0; i < n; ++i) {
+    const cf_reduction &j = jobs[i];
+    if (j.rows < 0 || j.cols < 0) return fail(CF_ERR_INVALID_ARG, "reduction with negative rows or cols");
+    if (j.cols == 0) continue;
+    if (!j.out || (j.rows > 0 && !j.part)) return fail(CF_ERR_INVALID_ARG, "reduction with a NULL pointer");
+    if (((uintptr_t)j.out & 3) || ((uintptr_t)j.part & 3))
+      return fail(CF_ERR_ALIGNMENT, "reduction pointers must be 4-byte aligned");
+    if (overlap(j.out, (size_t)j.cols * 4, j.part, (size_t)j.rows * j.cols * 4))
+      return fail(CF_ERR_ALIAS, "reduction output overlaps its partials");
+    v.push_back(cf::SumJob{j.part, j.out, j.rows, j.cols});
+  }
+  hipStream_t st = (hipStream_t)stream;
+  return finish(cf::launch_sum_batch(v.data(), (int)v.size(), st), st, "cf_reduce_partials");
+}
+
+cf_status cf_conv3d_bwd_weight_deferred(const cf_conv3d_desc *desc, const void *x, const void *dz, float *dw,
+                                        void *ws, size_t ws_bytes, cf_reduction *pending, int32_t *npending,
+                                        void *stream) {
+  return deferred(pending, npending, [&] { return cf_conv3d_bwd_weight(desc, x, dz, dw, ws, ws_bytes, stream); });
+}
+
+cf_status cf_bias_lrelu_bwd_deferred(int64_t nvox, int32_t c, int32_t dtype, const void *dy, const void *y,
+                                     float alpha, void *dz, float *db, void *ws, size_t ws_bytes,
+                                     cf_reduction *pending, int32_t *npending, void *stream) {
+  return deferred(pending, npending, [&] {
+    return cf_bias_lrelu_bwd(nvox, c, dtype, dy, y, alpha, dz, db, ws, ws_bytes, stream);
+  });
+}
+
+cf_status cf_conv3d_bwd_weight_fused_deferred(const cf_conv3d_desc *desc, const void *x, const void *g,
+                                              const void *mask, float alpha, uint32_t flags, float *dw, float *db,
+                                              void *dz, void *ws, size_t ws_bytes, cf_reduction *pending,
+                                              int32_t *npending, void *stream) {
+  return deferred(pending, npending, [&] {
+    return bwd_weight_fused(dz ? "cf_conv3d_bwd_weight_fused_dz" : "cf_conv3d_bwd_weight_fused", desc, x, g, mask,
+                            alpha, flags, dw, db, dz, ws, ws_bytes, stream);
+  });
 }
 
 }  // extern "C"

@@ -89,6 +89,22 @@ hipError_t launch_bias_lrelu_bwd(int64_t nvox, int c, int dtype, const void *dy,
 
 // out[c] = sum_{r < rows} part[r * cols + c], in an order fixed by (rows, cols).
 hipError_t launch_sum_rows(const float *part, float *out, int rows, int cols, hipStream_t st);
+// one pending column sum out[c] = sum_r part[r][c] of a [rows][cols] fp32 matrix
+struct SumJob {
+  const float *part;
+  float *out;
+  int rows, cols;
+};
+// While a collector is installed on the calling thread, launch_sum_rows records
+// its job there instead of launching it (the deferred entry points).
+struct SumCollector {
+  static constexpr int CAP = 4;
+  int n;
+  SumJob job[CAP];
+};
+void set_sum_collector(SumCollector *c);
+// all jobs in as few launches as possible (same bits as one launch per job)
+hipError_t launch_sum_batch(const SumJob *jobs, int n, hipStream_t st);
 
 // out[0..n) = 0 (a fill kernel, never hipMemsetAsync).
 hipError_t launch_fill_zero(float *out, long long n, hipStream_t st);

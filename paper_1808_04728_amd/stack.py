@@ -25,11 +25,15 @@ def _t(dtype):
 
 class ConvStack:
     def __init__(self, layers, size, batch, dtype="f32", alpha=0.01, device="cuda", skip_first_dgrad=True,
-                 fused=True):
+                 fused=True, defer_reductions=True):
         """fused: run a pooled layer through the fused entry points (forward
         epilogue writes pooled output + slope mask; backward rebuilds dz from
-        them) wherever the library has fused kernels for the layer."""
+        them) wherever the library has fused kernels for the layer.
+        defer_reductions: batch all gradient sums of a backward pass into one
+        cf_reduce_partials launch."""
         self.fused = fused
+        self.defer_reductions = defer_reductions
+        self.reduce_bytes = 0
         self.layers = layers
         self.batch = batch
         self.dtype = dtype
@@ -111,15 +115,15 @@ class ConvStack:
 
     def _call(self, name, fn, *args):
         if self.timer is None or (self.timed_ops is not None and name not in self.timed_ops):
-            fn(*args)
-            return
+            return fn(*args)
         import torch as _torch
         e0 = _torch.cuda.Event(enable_timing=True)
         e1 = _torch.cuda.Event(enable_timing=True)
         e0.record()
-        fn(*args)
+        r = fn(*args)
         e1.record()
         self.timer.setdefault(name, []).append((e0, e1))
+        return r
 
     # ------------------------------------------------------------------
     def forward(self, stream=None):
@@ -149,22 +153,39 @@ class ConvStack:
         return h
 
     def backward(self, dout, stream=None):
-        """dout: gradient w.r.t. the last layer's output (not modified)."""
+        """dout: gradient w.r.t. the last layer's output (not modified).
+
+        With defer_reductions (the default) every layer's weight- and
+        bias-gradient calls leave their fixed-order partial sums pending and
+        one cf_reduce_partials call at the end writes all dW and db (the same
+        bits as the plain calls)."""
         g = dout
+        pend = []
+        d = self.defer_reductions
         for i in range(len(self.L) - 1, -1, -1):
             l = self.L[i]
             s = l["spec"]
             c = self._call
             if l["fused"] and l["dz_emit"]:
-                c(f"L{i+1}.conv_bwd_weight_fused_dz", B.cf_conv3d_bwd_weight_fused_dz, l["desc"],
-                  self.layer_input(i), g, l["mask"], self.alpha, B.CF_FUSE_POOL2, l["dw"], l["db"], l["dz"],
-                  l["ws_w"], None, stream)
+                if d:
+                    pend += c(f"L{i+1}.conv_bwd_weight_fused_dz", B.cf_conv3d_bwd_weight_fused_deferred, l["desc"],
+                              self.layer_input(i), g, l["mask"], self.alpha, B.CF_FUSE_POOL2, l["dw"], l["db"],
+                              l["dz"], l["ws_w"], None, stream)
+                else:
+                    c(f"L{i+1}.conv_bwd_weight_fused_dz", B.cf_conv3d_bwd_weight_fused_dz, l["desc"],
+                      self.layer_input(i), g, l["mask"], self.alpha, B.CF_FUSE_POOL2, l["dw"], l["db"], l["dz"],
+                      l["ws_w"], None, stream)
                 c(f"L{i+1}.conv_bwd_data", B.cf_conv3d_bwd_data, l["desc"], l["dz"], l["w"], l["dx"], stream)
                 g = l["dx"]
                 continue
             if l["fused"]:
-                c(f"L{i+1}.conv_bwd_weight_fused", B.cf_conv3d_bwd_weight_fused, l["desc"], self.layer_input(i), g,
-                  l["mask"], self.alpha, B.CF_FUSE_POOL2, l["dw"], l["db"], l["ws_w"], None, stream)
+                if d:
+                    pend += c(f"L{i+1}.conv_bwd_weight_fused", B.cf_conv3d_bwd_weight_fused_deferred, l["desc"],
+                              self.layer_input(i), g, l["mask"], self.alpha, B.CF_FUSE_POOL2, l["dw"], l["db"],
+                              None, l["ws_w"], None, stream)
+                else:
+                    c(f"L{i+1}.conv_bwd_weight_fused", B.cf_conv3d_bwd_weight_fused, l["desc"], self.layer_input(i),
+                      g, l["mask"], self.alpha, B.CF_FUSE_POOL2, l["dw"], l["db"], l["ws_w"], None, stream)
                 if l["dx"] is not None:
                     c(f"L{i+1}.conv_bwd_data_fused", B.cf_conv3d_bwd_data_fused, l["desc"], g, l["mask"], l["w"],
                       self.alpha, B.CF_FUSE_POOL2, l["dx"], stream)
@@ -177,13 +198,22 @@ class ConvStack:
                 dy = l["dy"]
             else:
                 dy = g
-            c(f"L{i+1}.bias_lrelu_bwd", B.cf_bias_lrelu_bwd, l["nvox"], s["cout"], self.dtype, dy, l["z"],
-              self.alpha, l["dz"], l["db"], l["ws_b"], None, stream)
-            c(f"L{i+1}.conv_bwd_weight", B.cf_conv3d_bwd_weight, l["desc"], self.layer_input(i), l["dz"], l["dw"],
-              l["ws_w"], None, stream)
+            if d:
+                pend += c(f"L{i+1}.bias_lrelu_bwd", B.cf_bias_lrelu_bwd_deferred, l["nvox"], s["cout"], self.dtype,
+                          dy, l["z"], self.alpha, l["dz"], l["db"], l["ws_b"], None, stream)
+                pend += c(f"L{i+1}.conv_bwd_weight", B.cf_conv3d_bwd_weight_deferred, l["desc"],
+                          self.layer_input(i), l["dz"], l["dw"], l["ws_w"], None, stream)
+            else:
+                c(f"L{i+1}.bias_lrelu_bwd", B.cf_bias_lrelu_bwd, l["nvox"], s["cout"], self.dtype, dy, l["z"],
+                  self.alpha, l["dz"], l["db"], l["ws_b"], None, stream)
+                c(f"L{i+1}.conv_bwd_weight", B.cf_conv3d_bwd_weight, l["desc"], self.layer_input(i), l["dz"],
+                  l["dw"], l["ws_w"], None, stream)
             if l["dx"] is not None:
                 c(f"L{i+1}.conv_bwd_data", B.cf_conv3d_bwd_data, l["desc"], l["dz"], l["w"], l["dx"], stream)
                 g = l["dx"]
+        if pend:
+            self.reduce_bytes = sum(j.rows * j.cols * 4 + j.cols * 4 for j in pend)
+            self._call("L0.reduce_partials", B.cf_reduce_partials, pend, stream)
 
     def layer_input(self, i):
         if i == 0:
@@ -198,15 +228,17 @@ class ConvStack:
 
     def op_flops(self, name):
         """Algorithmic FLOPs of one call of a conv op (2 * MACs), else 0."""
-        i = int(name[1:name.index(".")]) - 1
         if ".conv_" not in name:
             return 0
+        i = int(name[1:name.index(".")]) - 1
         l = self.L[i]
         s = l["spec"]
         return 2 * l["nvox"] * s["cout"] * s["k"] ** 3 * s["cin"]
 
     def op_bytes(self, name):
         """Algorithmic HBM bytes of one call (every tensor read once, written once)."""
+        if name.endswith(".reduce_partials"):
+            return self.reduce_bytes
         i = int(name[1:name.index(".")]) - 1
         l = self.L[i]
         s = l["spec"]

@@ -117,3 +117,19 @@ def test_zero_batch_forward_is_host_noop(L):
     B.cf_avgpool3d_fwd(0, 8, 8, 8, 16, 2, 2, "f32", None, None, 0)
     B.cf_bias_lrelu_fwd(0, 16, "f32", None, None, 0.01, None, 0)
     B.cf_bias_lrelu_bwd(0, 16, "f32", None, None, 0.01, None, None, None, 0, 0)
+
+
+def test_reduce_partials_validation(L):
+    B.cf_reduce_partials([], 0)  # nothing to do: no GPU call
+    with pytest.raises(B.CfError) as e:
+        B.cf_reduce_partials([B.cf_reduction(16, 32, -1, 4)], 0)
+    assert e.value.status == B.CF_ERR_INVALID_ARG
+    with pytest.raises(B.CfError) as e:
+        B.cf_reduce_partials([B.cf_reduction(0, 32, 3, 4)], 0)
+    assert e.value.status == B.CF_ERR_INVALID_ARG
+    with pytest.raises(B.CfError) as e:
+        B.cf_reduce_partials([B.cf_reduction(18, 32, 3, 4)], 0)
+    assert e.value.status == B.CF_ERR_ALIGNMENT
+    with pytest.raises(B.CfError) as e:
+        B.cf_reduce_partials([B.cf_reduction(1024, 1024 + 16, 4, 8)], 0)  # out inside its partials
+    assert e.value.status == B.CF_ERR_ALIAS
