@@ -47,6 +47,7 @@
 #include <algorithm>
 #include <cstdio>
 #include <cstdlib>
+#include <cstring>
 
 namespace cf {
 namespace {
@@ -312,6 +313,264 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const uint16_t *__rest
   }
 }
 
+// ---------------------------------------------------------------------------
+// LDS-staged variant for launches with many row tiles (the stride-2 layer and
+// its backward-data classes at batch 8).  Same contraction, class and tap
+// tables as above, different data movement:
+//  * a workgroup's four waves split the rows (BM = 64 FM rows, 16 FM per
+//    wave) and share every k-step's operands, which arrive by buffer -> LDS
+//    DMA: the A tile (BM gathered voxels x 32 channels, padding voxels read as
+//    zero through the range check) and the B tile (32 x BN weights);
+//  * LNS = 4 stages, each its own LDS array, visited in an unrolled ring: the
+//    loads of step s + 3 are in flight while step s runs, one barrier per
+//    k-step.  Distinct arrays and a compile-time stage per unrolled step let
+//    the compiler see that a stage's reads do not alias the other stages'
+//    DMA, so the only wait is the explicit one on this step's loads; the
+//    barrier is a bare s_barrier because a release fence would wait for all
+//    of them;
+//  * the DMA writes each lane's 16 bytes at a fixed LDS slot, so the bank
+//    swizzles are applied on the global side: lane slot (row, chunk) fetches
+//    logical channel chunk chunk ^ ((row >> 2) & 3) (A, and backward-data's
+//    [ci][co] B tile), which makes the fragment reads (16 consecutive rows,
+//    one chunk) conflict-free; forward B tiles use the weight-slice swizzle
+//    and transposing reads of the kernel above;
+//  * the class's tap fields sit one tap per lane (at most 64 taps) and reach
+//    the scalar unit by readlane: no memory access or division per k-step;
+//  * no split over taps, so the epilogue needs no cross-wave sum: each wave
+//    passes its own fp32 rows through its own stage array to leave as whole
+//    16-byte vectors.
+constexpr int LNS = 4;  // pipeline stages
+
+template <int N>
+struct StageIx {
+  static constexpr int v = N;
+};
+
+template <bool FWD, int FM, int FN, bool ACT>
+__global__ __launch_bounds__(256) void conv_lds_kernel(const uint16_t *__restrict__ src,
+                                                       const uint16_t *__restrict__ wt,
+                                                       const float *__restrict__ bias,
+                                                       uint16_t *__restrict__ dst, uint8_t *__restrict__ mask,
+                                                       const DirParams p) {
+  constexpr int BM = 64 * FM, BN = 16 * FN;
+  constexpr int A_SLOTS = BM * 4;                     // 16-byte slots of the A tile
+  constexpr int B_SLOTS = 32 * BN / 8;                // 16-byte slots of the B tile
+  constexpr int A_BYTES = A_SLOTS * 16, B_BYTES = B_SLOTS * 16;
+  constexpr int STAGE = A_BYTES + B_BYTES;
+  constexpr int NA = A_SLOTS / 256;                   // A DMA instructions per wave and step
+  constexpr int NB = (B_SLOTS + 255) / 256;           // B DMA instructions per wave and step
+  constexpr int RED_LD = BN + 4;
+  static_assert(A_SLOTS % 256 == 0, "whole DMA instructions");
+  static_assert(!FWD || FN == 4, "forward weight tiles are 64 output channels wide");
+  static_assert(16 * FM * RED_LD * 4 <= STAGE, "a wave's fp32 rows fit its stage array");
+  __shared__ __attribute__((aligned(16))) unsigned char stg0[STAGE];
+  __shared__ __attribute__((aligned(16))) unsigned char stg1[STAGE];
+  __shared__ __attribute__((aligned(16))) unsigned char stg2[STAGE];
+  __shared__ __attribute__((aligned(16))) unsigned char stg3[STAGE];
+  typedef __attribute__((address_space(3))) void lds_void_t;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int g4 = lane >> 4, r16 = lane & 15;
+
+  int c = 0;
+  while (c + 1 < p.ncls && (int)blockIdx.x >= p.cls[c + 1].tile0) ++c;
+  const DirClass &C = p.cls[c];
+  const int m0 = ((int)blockIdx.x - C.tile0) * BM;
+  if (m0 >= C.m) return;
+  const int n0 = blockIdx.y * BN;
+
+  const __amdgpu_buffer_rsrc_t srsrc = __builtin_amdgcn_make_buffer_rsrc((void *)src, (short)0, p.src_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t wrsrc = __builtin_amdgcn_make_buffer_rsrc((void *)wt, (short)0, p.w_bytes, 0x00020000);
+
+  // ---- the class's taps, one per lane -----------------------------------------
+  const int ntap = C.ntap;
+  int v_aoff = 0, v_woff = 0, v_dd = 0, v_dh = 0, v_dw = 0;
+  if (lane < ntap) {
+    const DirTap &T = p.tap[C.tap0 + lane];
+    v_aoff = T.a_off; v_woff = T.w_off; v_dd = T.dd; v_dh = T.dh; v_dw = T.dw;
+  }
+
+  // ---- this lane's A slots: row, swizzled channel chunk, source base --------
+  int rbd[NA], rbh[NA], rbw[NA], roff[NA];
+#pragma unroll
+  for (int k = 0; k < NA; ++k) {
+    const int sl = 256 * k + tid, row = sl >> 2, lch = (sl & 3) ^ ((row >> 2) & 3);
+    const int grow = m0 + row;
+    const int rr = grow < C.m ? grow : 0;
+    const int t1 = fdiv(rr, C.fw), t2 = fdiv(t1, C.fh), n = fdiv(t2, C.fd);
+    rbw[k] = (rr - t1 * (int)C.fw.div) * p.bstr_w + C.bq_w;
+    rbh[k] = (t1 - t2 * (int)C.fh.div) * p.bstr_h + C.bq_h;
+    rbd[k] = (t2 - n * (int)C.fd.div) * p.bstr_d + C.bq_d;
+    roff[k] = (((n * p.sd_ + rbd[k]) * p.sh_ + rbh[k]) * p.sw_ + rbw[k]) * p.sc + 8 * lch;
+    if (grow >= C.m) rbd[k] = -(1 << 20);  // rows past the class fail every bounds check
+  }
+  // this lane's B slot(s): element offset inside a step's weight tile
+  int boff[NB];
+#pragma unroll
+  for (int k = 0; k < NB; ++k) {
+    const int sl = (256 * k + tid) % B_SLOTS;  // narrow tiles: the spare waves repeat a slot
+    if constexpr (FWD) {
+      // [32 ci rows][64 co]: 16-byte slot j of row ci sits in 32-byte chunk j/2, which
+      // holds logical chunk (j/2) ^ h(row) (the swizzle of wslice_off)
+      const int row = sl >> 3, j = sl & 7;
+      const int h = ((row >> 1) & 1) | (((row >> 3) & 1) << 1);
+      const int lc = (j >> 1) ^ h;
+      boff[k] = row * p.wco + n0 + 16 * lc + 8 * (j & 1);
+    } else {
+      // [BN ci rows][32 co], chunk swizzle as the A tile
+      const int row = sl >> 2, lch = (sl & 3) ^ ((row >> 2) & 3);
+      boff[k] = (n0 + row) * p.wco + 8 * lch;
+    }
+  }
+
+  auto stage = [&](auto ix) -> unsigned char * {
+    constexpr int S = decltype(ix)::v;
+    if constexpr (S == 0) return stg0;
+    else if constexpr (S == 1) return stg1;
+    else if constexpr (S == 2) return stg2;
+    else return stg3;
+  };
+
+  const int nch = p.sc >> 5;
+  const int nsteps = ntap * nch;
+  // issue state: tap and channel chunk of the next step to load, and the steps
+  // left.  The k-loop runs whole rounds of LNS steps (straight-line code, in
+  // which the compiler keeps track of which stage each DMA fills); the steps
+  // past the end stay on the last tap with every A slot out of range, so they
+  // load zeros and add nothing.
+  int iti = 0, icc = 0, ileft = 0;
+  auto issue = [&](auto ix) {
+    unsigned char *stg = stage(ix);
+    const int dd = __builtin_amdgcn_readlane(v_dd, iti), dh = __builtin_amdgcn_readlane(v_dh, iti);
+    const int dw = __builtin_amdgcn_readlane(v_dw, iti);
+    const int aoff = __builtin_amdgcn_readlane(v_aoff, iti) + 32 * icc;
+    const int wbase = __builtin_amdgcn_readlane(v_woff, iti) + 32 * icc * (FWD ? p.wco : 1);
+#pragma unroll
+    for (int k = 0; k < NA; ++k) {
+      const bool ok = ((unsigned)(rbd[k] + dd) < (unsigned)p.sd_) & ((unsigned)(rbh[k] + dh) < (unsigned)p.sh_) &
+                      ((unsigned)(rbw[k] + dw) < (unsigned)p.sw_) & (ileft > 0);
+      const uint32_t off = ok ? (uint32_t)(roff[k] + aoff) * 2u : DIR_OOB;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(srsrc, (lds_void_t *)(stg + (256 * k + 64 * wave) * 16), 16, off, 0, 0, 0);
+    }
+#pragma unroll
+    for (int k = 0; k < NB; ++k) {
+      const int sl0 = (256 * k + 64 * wave) % B_SLOTS;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(wrsrc, (lds_void_t *)(stg + A_BYTES + sl0 * 16), 16,
+                                               (uint32_t)(wbase + boff[k]) * 2u, 0, 0, 0);
+    }
+    --ileft;
+    if (icc + 1 < nch) {
+      ++icc;
+    } else if (iti + 1 < ntap) {
+      icc = 0;
+      ++iti;
+    }
+  };
+
+  f32x4_t acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  // one k-step on stage ix: wait for this wave's loads of the step (the loads
+  // of the next LNS - 2 steps may stay in flight) and for its fragment reads
+  // of the previous step, barrier (everyone's loads landed, nobody reads the
+  // previous step's stage any more), refill that stage with step s + LNS - 1,
+  // then the MFMAs of this step
+  auto kstep = [&](auto ix) {
+    constexpr int S = decltype(ix)::v;
+    constexpr int VMC = (LNS - 2) * (NA + NB);
+    __builtin_amdgcn_s_waitcnt(0x0070 | (VMC & 15) | ((VMC >> 4) << 14));  // vmcnt(VMC) lgkmcnt(0)
+    asm volatile("s_barrier" ::: "memory");
+    issue(StageIx<(S + LNS - 1) % LNS>{});
+    const unsigned char *stg = stage(ix);
+    bf16x8_t af[FM], bf[FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int row = wave * 16 * FM + 16 * i + r16;
+      af[i] = *reinterpret_cast<const bf16x8_t *>(stg + (row * 4 + (g4 ^ ((row >> 2) & 3))) * 16);
+    }
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      if constexpr (FWD) {
+        const unsigned char *rb = stg + A_BYTES;
+        const int row = 8 * g4 + (r16 >> 2);
+        const v4i16_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t *)(rb + wslice_off(row, j) + (r16 & 3) * 8));
+        const v4i16_t hi =
+            __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t *)(rb + wslice_off(row + 4, j) + (r16 & 3) * 8));
+        typedef short v8i16_t __attribute__((ext_vector_type(8)));
+        const v8i16_t v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        bf[j] = __builtin_bit_cast(bf16x8_t, v);
+      } else {
+        const int row = 16 * j + r16;
+        bf[j] = *reinterpret_cast<const bf16x8_t *>(stg + A_BYTES + (row * 4 + (g4 ^ ((row >> 2) & 3))) * 16);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
+  };
+
+  if (nsteps > 0) {  // a class without taps leaves zeros
+    ileft = nsteps;
+    issue(StageIx<0>{});
+    issue(StageIx<1>{});
+    issue(StageIx<2>{});
+    for (int s = 0; s < nsteps; s += LNS) {
+      kstep(StageIx<0>{});
+      kstep(StageIx<1>{});
+      kstep(StageIx<2>{});
+      kstep(StageIx<3>{});
+    }
+  }
+
+  // ---- each wave's fp32 rows leave through its stage array as 16-byte vectors
+  __builtin_amdgcn_s_waitcnt(0x0f70);  // vmcnt(0): the trailing loads have landed
+  __syncthreads();                      // and every wave is done with every stage
+  float *red = reinterpret_cast<float *>(wave == 0 ? stg0 : wave == 1 ? stg1 : wave == 2 ? stg2 : stg3);
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) red[(16 * i + 4 * g4 + e) * RED_LD + 16 * j + r16] = acc[i][j][e];
+  constexpr int CV = BN / 8;
+#pragma unroll
+  for (int v = lane; v < 16 * FM * CV; v += 64) {
+    const int row = v / CV, c8 = v % CV;
+    const int grow = m0 + wave * 16 * FM + row;
+    if (grow >= C.m) continue;
+    float o[8];
+    const float4 x0 = *reinterpret_cast<const float4 *>(&red[row * RED_LD + 8 * c8]);
+    const float4 x1 = *reinterpret_cast<const float4 *>(&red[row * RED_LD + 8 * c8 + 4]);
+    o[0] = x0.x; o[1] = x0.y; o[2] = x0.z; o[3] = x0.w;
+    o[4] = x1.x; o[5] = x1.y; o[6] = x1.z; o[7] = x1.w;
+    const int t1 = fdiv(grow, C.fw), t2 = fdiv(t1, C.fh), n = fdiv(t2, C.fd);
+    const int ow_ = (grow - t1 * (int)C.fw.div) * p.ostr_w + C.or_w;
+    const int oh_ = (t1 - t2 * (int)C.fh.div) * p.ostr_h + C.or_h;
+    const int od_ = (t2 - n * (int)C.fd.div) * p.ostr_d + C.or_d;
+    const int e0 = (((n * p.dd + od_) * p.dh + oh_) * p.dw + ow_) * p.dc + n0 + 8 * c8;
+    uint32_t bits = 0;
+    if constexpr (ACT) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float u = o[e] + bias[n0 + 8 * c8 + e];
+        bits |= (u > 0.f ? 1u : 0u) << e;
+        o[e] = u > 0.f ? u : p.alpha * u;
+      }
+    }
+    Vec16<DT_BF16> pk;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) pk.e[e] = f2bf(o[e]);
+    *reinterpret_cast<uint4 *>(dst + e0) = pk.u;
+    if (ACT && mask) mask[e0 >> 3] = (uint8_t)bits;
+  }
+}
+
 struct DirCfg {
   int fm, wm, wk, pf;
 };
@@ -417,8 +676,10 @@ int assign_tiles(DirParams &p, int bm) {
 // tile that still yields 256 workgroups (one per compute unit); more rows per
 // wave amortise the weight stream, waves along K keep every wave busy when
 // rows are few.  The 128-row tile pays off only for backward-data, whose
-// weights come straight from global memory.  One k-step of prefetch: the
-// kernels are bound by L2 -> L1 traffic, not by load latency.
+// weights come straight from global memory.  Prefetch: three k-steps for the
+// forward kernels (their per-step weight staging leaves load latency exposed
+// at these row counts), one for backward-data (bound by L2 -> L1 traffic,
+// where a deeper ring only adds registers) -- measured on the stack's layers.
 // CF_DIRECT_TILE="fm,wm,wk" and CF_DIRECT_PF force a variant (tests cover
 // every one this way).
 DirCfg choose_cfg(DirParams &p, int fn, bool fwd) {
@@ -444,6 +705,7 @@ DirCfg choose_cfg(DirParams &p, int fn, bool fwd) {
         break;
       }
   }
+  if (fwd) pick.pf = 3;
   if (pf >= 1 && pf <= 3) pick.pf = pf;
   return pick;
 }
@@ -466,11 +728,45 @@ bool direct_supported(const ConvShape &s, bool fwd) {
   return true;
 }
 
+// LDS-staged kernel when its row tiles alone fill the machine (>= 256
+// workgroups), with 128-row tiles if they do, else 64-row tiles; 0 = the
+// register-streaming kernel.  CF_DIRECT_KERNEL=reg / lds128 / lds64 forces a
+// choice (tests cover every kernel on small shapes this way).
+int choose_lds(DirParams &p, int ny) {
+  if (const char *e = getenv("CF_DIRECT_KERNEL")) {
+    if (!strcmp(e, "reg")) return 0;
+    if (!strcmp(e, "lds128")) return 2;
+    if (!strcmp(e, "lds64")) return 1;
+  }
+  if ((long long)assign_tiles(p, 128) * ny >= 256) return 2;
+  if ((long long)assign_tiles(p, 64) * ny >= 256) return 1;
+  return 0;
+}
+
+template <bool FWD, int FN, bool ACT>
+hipError_t launch_lds(int fm, DirParams &p, const void *src, const void *w, const float *bias, void *dst,
+                      void *mask, hipStream_t st) {
+  const int tiles = assign_tiles(p, 64 * fm);
+  dim3 grid((unsigned)tiles, p.dc / (16 * FN), 1);
+  if (grid.x == 0 || grid.y == 0) return hipSuccess;
+  const uint16_t *s16 = (const uint16_t *)src, *w16 = (const uint16_t *)w;
+  if (fm == 2)
+    hipLaunchKernelGGL((conv_lds_kernel<FWD, 2, FN, ACT>), grid, dim3(256), 0, st, s16, w16, bias, (uint16_t *)dst,
+                       (uint8_t *)mask, p);
+  else
+    hipLaunchKernelGGL((conv_lds_kernel<FWD, 1, FN, ACT>), grid, dim3(256), 0, st, s16, w16, bias, (uint16_t *)dst,
+                       (uint8_t *)mask, p);
+  return hipGetLastError();
+}
+
 hipError_t launch_conv_fwd_direct(const ConvShape &s, const void *x, const void *w, const float *bias, float alpha,
                                   void *out, void *mask, bool act, hipStream_t st) {
   DirParams p{};
   build_tables(s, true, p);
   p.alpha = alpha;
+  if (const int fm = choose_lds(p, p.dc / 64))
+    return act ? launch_lds<true, 4, true>(fm, p, x, w, bias, out, mask, st)
+               : launch_lds<true, 4, false>(fm, p, x, w, nullptr, out, nullptr, st);
   const DirCfg c = choose_cfg(p, 4, true);
   const int tiles = assign_tiles(p, 16 * c.fm * c.wm);
   return act ? launch_dir_pf<true, 4, true>(c, p, tiles, x, w, bias, out, mask, st)
@@ -482,6 +778,9 @@ hipError_t launch_conv_bwd_data_direct(const ConvShape &s, const void *dz, const
   DirParams p{};
   build_tables(s, false, p);
   const int fn = p.dc % 64 == 0 ? 4 : 2;
+  if (const int fm = choose_lds(p, p.dc / (16 * fn)))
+    return fn == 4 ? launch_lds<false, 4, false>(fm, p, dz, w, nullptr, dx, nullptr, st)
+                   : launch_lds<false, 2, false>(fm, p, dz, w, nullptr, dx, nullptr, st);
   const DirCfg c = choose_cfg(p, fn, false);
   const int tiles = assign_tiles(p, 16 * c.fm * c.wm);
   return fn == 4 ? launch_dir_pf<false, 4, false>(c, p, tiles, dz, w, nullptr, dx, nullptr, st)

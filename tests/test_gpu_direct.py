@@ -161,3 +161,74 @@ def test_direct_prefetch_depths(case, tile, pf, monkeypatch):
     assert e <= TOL["bf16"], e
     e = maxabs_err(to_np(dx), oracle.conv3d_bwd_data(to_np(dz), to_np(w), dhw, stride=s, pad="same"))
     assert e <= TOL["bf16"], e
+
+
+# the LDS-staged kernel: 4-stage DMA ring run in whole rounds of four k-steps,
+# so step counts below one round and not a multiple of four are covered
+LDS_CASES = CASES + [
+    (1, (5, 6, 7), 32, 64, 1, 1),      # a single k-step (three padding steps); backward-data N = 32
+    (2, (7, 9, 6), 64, 32, 3, 2),      # k = 3, stride 2: classes of 1, 2, 4 and 8 taps
+    (2, (1, 6, 5), 32, 64, 3, 2),      # extent 1 along D: the odd-D classes are empty
+]
+
+
+@pytest.mark.parametrize("kern", ["lds128", "lds64"])
+@pytest.mark.parametrize("case", LDS_CASES, ids=ids)
+def test_lds_kernel(case, kern, monkeypatch):
+    """Forward, forward with the fused bias + leaky-ReLU epilogue and its mask,
+    and backward-data through the LDS-staged kernel at both row tiles."""
+    monkeypatch.setenv("CF_DIRECT_KERNEL", kern)
+    N, dhw, CI, CO, k, s = case
+    rng = np.random.default_rng(36)
+    desc = B.make_desc(N, dhw, CI, CO, k, s, "same", "bf16")
+    od = B.cf_conv3d_out_shape(desc)
+    x = dev(rng.standard_normal((N, *dhw, CI)), "bf16")
+    w = dev(rng.standard_normal((k, k, k, CI, CO)) / np.sqrt(k ** 3 * CI), "bf16")
+    dz = dev(rng.standard_normal((N, *od, CO)), "bf16")
+    b = torch.as_tensor(rng.standard_normal(CO) * 0.1, dtype=torch.float32, device="cuda")
+    z = torch.full((N, *od, CO), float("nan"), dtype=tdtype("bf16"), device="cuda")
+    y = torch.full_like(z, float("nan"))
+    dx = torch.full((N, *dhw, CI), float("nan"), dtype=tdtype("bf16"), device="cuda")
+    B.cf_conv3d_fwd(desc, x, w, z)
+    B.cf_conv3d_bwd_data(desc, dz, w, dx)
+    fused = bool(B.cf_conv3d_fused_supported(desc, 0) & B.FUSED_FWD)
+    if fused:
+        mask = torch.zeros(B.cf_conv3d_mask_bytes(desc), dtype=torch.uint8, device="cuda")
+        B.cf_conv3d_fwd_fused(desc, x, w, b, 0.01, 0, y, mask)
+    torch.cuda.synchronize()
+    zr = oracle.conv3d_fwd(to_np(x), to_np(w), stride=s, pad="same")
+    e = maxabs_err(to_np(z), zr)
+    assert e <= TOL["bf16"], e
+    e = maxabs_err(to_np(dx), oracle.conv3d_bwd_data(to_np(dz), to_np(w), dhw, stride=s, pad="same"))
+    assert e <= TOL["bf16"], e
+    if fused:
+        e = maxabs_err(to_np(y), oracle.bias_lrelu_fwd(zr, to_np(b), 0.01))
+        assert e <= TOL["bf16"], e
+        u = zr + to_np(b)
+        bits = unpack_mask(mask, u.size).reshape(u.shape)
+        decided = np.abs(u) > 1e-5 * np.abs(u).max()
+        assert np.array_equal(bits[decided], (u > 0)[decided])
+
+
+@pytest.mark.parametrize("case", [CASES[1], CASES[4], LDS_CASES[-2]], ids=ids)
+def test_lds_tiles_agree_bitwise(case, monkeypatch):
+    """Both row tiles of the LDS-staged kernel accumulate each output over the
+    same k-steps in the same order with the same MFMA: identical bits."""
+    N, dhw, CI, CO, k, s = case
+    rng = np.random.default_rng(37)
+    desc = B.make_desc(N, dhw, CI, CO, k, s, "same", "bf16")
+    od = B.cf_conv3d_out_shape(desc)
+    x = dev(rng.standard_normal((N, *dhw, CI)), "bf16")
+    w = dev(rng.standard_normal((k, k, k, CI, CO)) / np.sqrt(k ** 3 * CI), "bf16")
+    dz = dev(rng.standard_normal((N, *od, CO)), "bf16")
+    outs = {}
+    for kk in ("lds128", "lds64"):
+        monkeypatch.setenv("CF_DIRECT_KERNEL", kk)
+        z = torch.empty((N, *od, CO), dtype=tdtype("bf16"), device="cuda")
+        dx = torch.empty((N, *dhw, CI), dtype=tdtype("bf16"), device="cuda")
+        B.cf_conv3d_fwd(desc, x, w, z)
+        B.cf_conv3d_bwd_data(desc, dz, w, dx)
+        outs[kk] = (z, dx)
+    torch.cuda.synchronize()
+    assert torch.equal(outs["lds128"][0], outs["lds64"][0])
+    assert torch.equal(outs["lds128"][1], outs["lds64"][1])
