@@ -72,6 +72,12 @@ hipError_t launch_conv_fwd_direct(const ConvShape &s, const void *x, const void 
                                   void *out, void *mask, bool act, hipStream_t st);
 hipError_t launch_conv_bwd_data_direct(const ConvShape &s, const void *dz, const void *w, void *dx,
                                        hipStream_t st);
+// their weight gradient (bf16, ci % 8 == 0, co % 64 == 0), conv_direct_wgrad.hip: K-split
+// partials in ws, summed into dw by launch_sum_rows
+bool direct_wgrad_supported(const ConvShape &s);
+size_t direct_wgrad_workspace(const ConvShape &s);
+hipError_t launch_conv_bwd_weight_direct(const ConvShape &s, const void *x, const void *dz, float *dw, void *ws,
+                                         hipStream_t st);
 
 hipError_t launch_conv_fwd(const ConvShape &s, const void *x, const void *w, void *z,
                            hipStream_t st);

@@ -33,6 +33,8 @@
 #include "cf_kernels.h"
 
 #include <algorithm>
+#include <cstdlib>
+#include <cstring>
 
 namespace cf {
 namespace {
@@ -642,8 +644,18 @@ hipError_t launch_conv_bwd_data(const ConvShape &s, const void *dz, const void *
   return hipSuccess;
 }
 
+// The generic tiled weight-gradient kernel serves what neither the 16 -> 32
+// kernel nor the deep-layer kernel covers; CF_WGRAD_KERNEL=igemm forces it
+// for the deep layers (tests compare the two).
+static bool use_direct_wgrad(const ConvShape &s) {
+  const char *e = getenv("CF_WGRAD_KERNEL");
+  if (e && !strcmp(e, "igemm")) return false;
+  return direct_wgrad_supported(s);
+}
+
 size_t conv_bwd_weight_workspace(const ConvShape &s) {
   if (c16_wgrad_supported(s)) return c16_wgrad_workspace(s);
+  if (use_direct_wgrad(s)) return direct_wgrad_workspace(s);
   WgradPlan pl = plan_wgrad(s);
   return (size_t)pl.nsplit * s.kd * s.kh * s.kw * s.ci * s.co * sizeof(float);
 }
@@ -652,6 +664,7 @@ hipError_t launch_conv_bwd_weight(const ConvShape &s, const void *x, const void 
                                   void *ws, hipStream_t st) {
   if (c16_wgrad_supported(s))
     return launch_conv_bwd_weight_c16(s, x, dz, nullptr, 0.f, dw, nullptr, ws, false, nullptr, st);
+  if (use_direct_wgrad(s)) return launch_conv_bwd_weight_direct(s, x, dz, dw, ws, st);
   WgradPlan pl = plan_wgrad(s);
   WgradParams p{};
   p.nb = s.n; p.d = s.d; p.h = s.h; p.w = s.w; p.ci = s.ci;

@@ -232,3 +232,69 @@ def test_lds_tiles_agree_bitwise(case, monkeypatch):
     torch.cuda.synchronize()
     assert torch.equal(outs["lds128"][0], outs["lds64"][0])
     assert torch.equal(outs["lds128"][1], outs["lds64"][1])
+
+
+# deep-layer weight gradient: N, (D, H, W), CI, CO, k, stride, pad
+WG_CASES = [
+    (2, (10, 9, 8), 32, 64, 4, 2, "same"),   # stride-2 layer shape: two taps per 64-row block
+    (1, (7, 6, 8), 64, 64, 3, 1, "same"),    # 27 taps: ragged last row block
+    (1, (6, 5, 7), 64, 128, 2, 1, "same"),   # 128-wide column blocks (two waves per dz tile)
+    (1, (5, 6, 7), 40, 192, 3, 1, "same"),   # 40 channels: row blocks straddle taps; three column blocks
+    (1, (3, 2, 4), 64, 64, 2, 1, "same"),    # 24 voxels: one partial k-step
+    (2, (9, 8, 7), 64, 64, 3, 2, "valid"),   # VALID, stride 2
+    (2, (12, 12, 12), 64, 64, 3, 1, "same"), # 3456 voxels: many K slices
+]
+
+
+def wg_ids(c):
+    return "n%d_%dx%dx%d_c%d-%d_k%d_s%d_%s" % (c[0], *c[1], *c[2:])
+
+
+@pytest.mark.parametrize("wgs", [None, "1", "100000"], ids=["auto", "one_slice", "max_slices"])
+@pytest.mark.parametrize("case", WG_CASES, ids=wg_ids)
+def test_direct_wgrad(case, wgs, monkeypatch):
+    """dW through the LDS-staged K-split kernel (slice counts from one to the
+    most the 8-step minimum allows) against the oracle; repeat calls are
+    bitwise identical."""
+    if wgs is not None:
+        monkeypatch.setenv("CF_DWGRAD_WGS", wgs)
+    N, dhw, CI, CO, k, s, pad = case
+    rng = np.random.default_rng(38)
+    desc = B.make_desc(N, dhw, CI, CO, k, s, pad, "bf16")
+    od = B.cf_conv3d_out_shape(desc)
+    x = dev(rng.standard_normal((N, *dhw, CI)), "bf16")
+    dz = dev(rng.standard_normal((N, *od, CO)), "bf16")
+    dw = torch.full((k, k, k, CI, CO), float("nan"), dtype=torch.float32, device="cuda")
+    ws = torch.empty(max(16, B.cf_conv3d_bwd_weight_workspace_size(desc)), dtype=torch.uint8, device="cuda")
+    B.cf_conv3d_bwd_weight(desc, x, dz, dw, ws)
+    dw2 = torch.full_like(dw, float("nan"))
+    B.cf_conv3d_bwd_weight(desc, x, dz, dw2, ws)
+    torch.cuda.synchronize()
+    ref = oracle.conv3d_bwd_weight(to_np(x), to_np(dz), k, stride=s, pad=pad)
+    # bf16 products are exact in fp32: only the fp32 accumulation order differs
+    e = maxabs_err(to_np(dw), ref)
+    assert e <= 1e-4, e
+    assert torch.equal(dw, dw2)
+
+
+@pytest.mark.parametrize("case", [WG_CASES[0], WG_CASES[3]], ids=wg_ids)
+def test_direct_wgrad_matches_generic(case, monkeypatch):
+    """The deep-layer kernel and the generic tiled kernel agree to fp32
+    rounding (different summation orders)."""
+    N, dhw, CI, CO, k, s, pad = case
+    rng = np.random.default_rng(39)
+    desc = B.make_desc(N, dhw, CI, CO, k, s, pad, "bf16")
+    od = B.cf_conv3d_out_shape(desc)
+    x = dev(rng.standard_normal((N, *dhw, CI)), "bf16")
+    dz = dev(rng.standard_normal((N, *od, CO)), "bf16")
+    out = []
+    for kern in (None, "igemm"):
+        if kern:
+            monkeypatch.setenv("CF_WGRAD_KERNEL", kern)
+        dw = torch.empty((k, k, k, CI, CO), dtype=torch.float32, device="cuda")
+        ws = torch.empty(max(16, B.cf_conv3d_bwd_weight_workspace_size(desc)), dtype=torch.uint8, device="cuda")
+        B.cf_conv3d_bwd_weight(desc, x, dz, dw, ws)
+        torch.cuda.synchronize()
+        out.append(to_np(dw))
+    scale = np.abs(out[1]).max()
+    assert np.abs(out[0] - out[1]).max() <= 1e-5 * scale
