@@ -64,7 +64,8 @@ constexpr uint32_t DIR_OOB = 0x80000000u;  // a byte offset past every buffer: t
 
 struct DirClass {
   int m;                // GEMM rows (destination voxels) of the class
-  int tile0;            // first row tile of the class in the grid
+  int slot0, per;       // XCD-major grid: the class's row tiles are split into 8 contiguous
+                        // runs of `per`, one per XCD, at per-XCD slots slot0 .. slot0 + per - 1
   int ntap, tap0;       // the class's taps: entries tap0 .. tap0 + ntap - 1 of the tap table
   FastDiv fw, fh, fd;   // row = ((n * Jd + jd) * Jh + jh) * Jw + jw: divisors Jw, Jh, Jd
   int bq_d, bq_h, bq_w; // source base coordinate = j * bstr + bq
@@ -126,10 +127,14 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const uint16_t *__rest
   const int g4 = lane >> 4, r16 = lane & 15;
 
   // ---- class and row tile of this workgroup (uniform) -----------------------
+  // workgroup b runs on XCD b % 8; XCD x takes run x of every class, so its
+  // tiles cover one contiguous range of voxels (a share of the batch) and
+  // their overlapping source reads meet in that XCD's L2
+  const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
   int c = 0;
-  while (c + 1 < p.ncls && (int)blockIdx.x >= p.cls[c + 1].tile0) ++c;
+  while (c + 1 < p.ncls && slot >= p.cls[c + 1].slot0) ++c;
   const DirClass &C = p.cls[c];
-  const int m0 = ((int)blockIdx.x - C.tile0) * BM;
+  const int m0 = (xcd * C.per + slot - C.slot0) * BM;
   if (m0 >= C.m) return;  // uniform: the whole workgroup leaves
   const int n0 = blockIdx.y * BN;
 
@@ -321,9 +326,10 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const uint16_t *__rest
 //    wave) and share every k-step's operands, which arrive by buffer -> LDS
 //    DMA: the A tile (BM gathered voxels x 32 channels, padding voxels read as
 //    zero through the range check) and the B tile (32 x BN weights);
-//  * LNS = 4 stages, each its own LDS array, visited in an unrolled ring: the
-//    loads of step s + 3 are in flight while step s runs, one barrier per
-//    k-step.  Distinct arrays and a compile-time stage per unrolled step let
+//  * NS stages (4 or 8), each its own LDS array, visited in an unrolled
+//    ring: the loads of steps s + 1 .. s + NS - 1 are in flight while step s
+//    runs, one barrier per k-step; the fragments of step s + 1 are read while
+//    the MFMAs of step s run.  Distinct arrays and a compile-time stage per unrolled step let
 //    the compiler see that a stage's reads do not alias the other stages'
 //    DMA, so the only wait is the explicit one on this step's loads; the
 //    barrier is a bare s_barrier because a release fence would wait for all
@@ -339,14 +345,21 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const uint16_t *__rest
 //  * no split over taps, so the epilogue needs no cross-wave sum: each wave
 //    passes its own fp32 rows through its own stage array to leave as whole
 //    16-byte vectors.
-constexpr int LNS = 4;  // pipeline stages
-
 template <int N>
 struct StageIx {
   static constexpr int v = N;
 };
 
-template <bool FWD, int FM, int FN, bool ACT>
+// f(StageIx<I>), ..., f(StageIx<N - 1>) in order, as straight-line code
+template <int I, int N, class F>
+__device__ __forceinline__ void for_stages(F &&f) {
+  if constexpr (I < N) {
+    f(StageIx<I>{});
+    for_stages<I + 1, N>(f);
+  }
+}
+
+template <bool FWD, int FM, int FN, bool ACT, int NS>
 __global__ __launch_bounds__(256) void conv_lds_kernel(const uint16_t *__restrict__ src,
                                                        const uint16_t *__restrict__ wt,
                                                        const float *__restrict__ bias,
@@ -363,20 +376,24 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(const uint16_t *__restric
   static_assert(A_SLOTS % 256 == 0, "whole DMA instructions");
   static_assert(!FWD || FN == 4, "forward weight tiles are 64 output channels wide");
   static_assert(16 * FM * RED_LD * 4 <= STAGE, "a wave's fp32 rows fit its stage array");
-  __shared__ __attribute__((aligned(16))) unsigned char stg0[STAGE];
-  __shared__ __attribute__((aligned(16))) unsigned char stg1[STAGE];
-  __shared__ __attribute__((aligned(16))) unsigned char stg2[STAGE];
-  __shared__ __attribute__((aligned(16))) unsigned char stg3[STAGE];
+  static_assert(NS == 4 || NS == 8, "four or eight stages");
+  __shared__ __attribute__((aligned(16))) unsigned char stg0[STAGE], stg1[STAGE], stg2[STAGE], stg3[STAGE];
+  __shared__ __attribute__((aligned(16))) unsigned char stg4[NS > 4 ? STAGE : 16], stg5[NS > 4 ? STAGE : 16];
+  __shared__ __attribute__((aligned(16))) unsigned char stg6[NS > 4 ? STAGE : 16], stg7[NS > 4 ? STAGE : 16];
   typedef __attribute__((address_space(3))) void lds_void_t;
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g4 = lane >> 4, r16 = lane & 15;
 
+  // workgroup b runs on XCD b % 8; XCD x takes run x of every class, so its
+  // tiles cover one contiguous range of voxels (a share of the batch) and
+  // their overlapping source reads meet in that XCD's L2
+  const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
   int c = 0;
-  while (c + 1 < p.ncls && (int)blockIdx.x >= p.cls[c + 1].tile0) ++c;
+  while (c + 1 < p.ncls && slot >= p.cls[c + 1].slot0) ++c;
   const DirClass &C = p.cls[c];
-  const int m0 = ((int)blockIdx.x - C.tile0) * BM;
+  const int m0 = (xcd * C.per + slot - C.slot0) * BM;
   if (m0 >= C.m) return;
   const int n0 = blockIdx.y * BN;
 
@@ -429,13 +446,17 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(const uint16_t *__restric
     if constexpr (S == 0) return stg0;
     else if constexpr (S == 1) return stg1;
     else if constexpr (S == 2) return stg2;
-    else return stg3;
+    else if constexpr (S == 3) return stg3;
+    else if constexpr (S == 4) return stg4;
+    else if constexpr (S == 5) return stg5;
+    else if constexpr (S == 6) return stg6;
+    else return stg7;
   };
 
   const int nch = p.sc >> 5;
   const int nsteps = ntap * nch;
   // issue state: tap and channel chunk of the next step to load, and the steps
-  // left.  The k-loop runs whole rounds of LNS steps (straight-line code, in
+  // left.  The k-loop runs whole rounds of NS steps (straight-line code, in
   // which the compiler keeps track of which stage each DMA fills); the steps
   // past the end stay on the last tap with every A slot out of range, so they
   // load zeros and add nothing.
@@ -474,19 +495,9 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(const uint16_t *__restric
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  // one k-step on stage ix: wait for this wave's loads of the step (the loads
-  // of the next LNS - 2 steps may stay in flight) and for its fragment reads
-  // of the previous step, barrier (everyone's loads landed, nobody reads the
-  // previous step's stage any more), refill that stage with step s + LNS - 1,
-  // then the MFMAs of this step
-  auto kstep = [&](auto ix) {
-    constexpr int S = decltype(ix)::v;
-    constexpr int VMC = (LNS - 2) * (NA + NB);
-    __builtin_amdgcn_s_waitcnt(0x0070 | (VMC & 15) | ((VMC >> 4) << 14));  // vmcnt(VMC) lgkmcnt(0)
-    asm volatile("s_barrier" ::: "memory");
-    issue(StageIx<(S + LNS - 1) % LNS>{});
+  // MFMA fragments of the step held in stage ix
+  auto read_frags = [&](auto ix, bf16x8_t (&af)[FM], bf16x8_t (&bf)[FN]) {
     const unsigned char *stg = stage(ix);
-    bf16x8_t af[FM], bf[FN];
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
       const int row = wave * 16 * FM + 16 * i + r16;
@@ -508,24 +519,45 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(const uint16_t *__restric
         bf[j] = *reinterpret_cast<const bf16x8_t *>(stg + A_BYTES + (row * 4 + (g4 ^ ((row >> 2) & 3))) * 16);
       }
     }
+  };
+
+  // fragments of the step about to run (read one step ahead)
+  bf16x8_t af[FM], bf[FN];
+
+  // k-step s on stage ix, its fragments already in af / bf: wait for this
+  // wave's loads of step s + 1 (the loads of the next NS - 3 steps may stay in
+  // flight) and for its fragment reads of step s, barrier (everyone's loads
+  // of step s + 1 landed; nobody reads the stage of step s - 1 any more),
+  // refill that stage with step s + NS - 1, read the fragments of step s + 1
+  // while the MFMAs of step s run
+  auto kstep = [&](auto ix) {
+    constexpr int S = decltype(ix)::v;
+    constexpr int VMC = (NS - 3) * (NA + NB);
+    __builtin_amdgcn_s_waitcnt(0x0070 | (VMC & 15) | ((VMC >> 4) << 14));  // vmcnt(VMC) lgkmcnt(0)
+    asm volatile("s_barrier" ::: "memory");
+    issue(StageIx<(S + NS - 1) % NS>{});
+    bf16x8_t an[FM], bn[FN];
+    read_frags(StageIx<(S + 1) % NS>{}, an, bn);
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
       for (int j = 0; j < FN; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
+#pragma unroll
+    for (int i = 0; i < FM; ++i) af[i] = an[i];
+#pragma unroll
+    for (int j = 0; j < FN; ++j) bf[j] = bn[j];
   };
 
   if (nsteps > 0) {  // a class without taps leaves zeros
     ileft = nsteps;
-    issue(StageIx<0>{});
-    issue(StageIx<1>{});
-    issue(StageIx<2>{});
-    for (int s = 0; s < nsteps; s += LNS) {
-      kstep(StageIx<0>{});
-      kstep(StageIx<1>{});
-      kstep(StageIx<2>{});
-      kstep(StageIx<3>{});
-    }
+    for_stages<0, NS - 1>([&](auto ix) { issue(ix); });
+    // step 0 landed everywhere, its fragments in registers
+    constexpr int VMC0 = (NS - 2) * (NA + NB);
+    __builtin_amdgcn_s_waitcnt(0x0f70 | (VMC0 & 15) | ((VMC0 >> 4) << 14));  // vmcnt(VMC0)
+    asm volatile("s_barrier" ::: "memory");
+    read_frags(StageIx<0>{}, af, bf);
+    for (int s = 0; s < nsteps; s += NS) for_stages<0, NS>([&](auto ix) { kstep(ix); });
   }
 
   // ---- each wave's fp32 rows leave through its stage array as 16-byte vectors
@@ -663,13 +695,17 @@ void build_tables(const ConvShape &s, bool fwd, DirParams &p) {
   p.w_bytes = s.kd * s.kh * s.kw * s.ci * s.co * 2;
 }
 
+// Lays out the XCD-major grid for row tiles of bm rows; returns its size (a
+// multiple of 8; workgroups past a class's last tile leave at once).
 int assign_tiles(DirParams &p, int bm) {
-  int t = 0;
+  int slots = 0;
   for (int c = 0; c < p.ncls; ++c) {
-    p.cls[c].tile0 = t;
-    t += (p.cls[c].m + bm - 1) / bm;
+    const int tiles = (p.cls[c].m + bm - 1) / bm;
+    p.cls[c].slot0 = slots;
+    p.cls[c].per = (tiles + 7) / 8;
+    slots += p.cls[c].per;
   }
-  return t;
+  return 8 * slots;
 }
 
 // Tile choice (measured on the deep layers of the stack): the largest row
@@ -750,12 +786,23 @@ hipError_t launch_lds(int fm, DirParams &p, const void *src, const void *w, cons
   dim3 grid((unsigned)tiles, p.dc / (16 * FN), 1);
   if (grid.x == 0 || grid.y == 0) return hipSuccess;
   const uint16_t *s16 = (const uint16_t *)src, *w16 = (const uint16_t *)w;
-  if (fm == 2)
-    hipLaunchKernelGGL((conv_lds_kernel<FWD, 2, FN, ACT>), grid, dim3(256), 0, st, s16, w16, bias, (uint16_t *)dst,
-                       (uint8_t *)mask, p);
-  else
-    hipLaunchKernelGGL((conv_lds_kernel<FWD, 1, FN, ACT>), grid, dim3(256), 0, st, s16, w16, bias, (uint16_t *)dst,
-                       (uint8_t *)mask, p);
+  // four stages (measured on the stack's stride-2 layer: an eight-stage ring
+  // gains nothing there, where the waves are issue-bound, and halves the
+  // backward-data workgroups per compute unit); CF_DIRECT_STAGES=8 selects
+  // the deeper ring (tests cover both)
+  const char *e = getenv("CF_DIRECT_STAGES");
+  const bool ns4 = !(e && atoi(e) == 8);
+#define CF_LDS_LAUNCH(FM_, NS_)                                                                                  \
+  hipLaunchKernelGGL((conv_lds_kernel<FWD, FM_, FN, ACT, NS_>), grid, dim3(256), 0, st, s16, w16, bias,         \
+                     (uint16_t *)dst, (uint8_t *)mask, p)
+  if (fm == 2) {
+    if (ns4) CF_LDS_LAUNCH(2, 4);
+    else CF_LDS_LAUNCH(2, 8);
+  } else {
+    if (ns4) CF_LDS_LAUNCH(1, 4);
+    else CF_LDS_LAUNCH(1, 8);
+  }
+#undef CF_LDS_LAUNCH
   return hipGetLastError();
 }
 

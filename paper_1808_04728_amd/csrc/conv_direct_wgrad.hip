@@ -57,6 +57,8 @@ struct DwParams {
   int m;                  // GEMM rows: kd kh kw ci
   int pvox;               // output voxels n od oh ow (the reduction)
   int chunk;              // voxels per K slice (a multiple of 32)
+  int mt, nt, jobs;       // row blocks, column blocks, mt nt slices
+  int per;                // jobs per XCD
   int x_bytes, dz_bytes;  // extents of the range-checked buffers
   FastDiv fow, foh, fod;  // output extent divisors
 };
@@ -91,8 +93,14 @@ __global__ __launch_bounds__(256, 2) void dw_lds_kernel(const uint16_t *__restri
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WN, wn = wave % WN;
   const int g4 = lane >> 4, r16 = lane & 15;
-  const int mrow0 = blockIdx.x * 64 * WM, n0 = blockIdx.y * 64 * WN;
-  const int vbeg = blockIdx.z * p.chunk;
+  // jobs in slice-major order, XCD x (workgroups b with b % 8 == x) taking
+  // the contiguous run [x per, (x + 1) per): consecutive slices, i.e. one
+  // contiguous range of voxels whose x and dz stay in that XCD's L2
+  const int job = (blockIdx.x & 7) * p.per + (blockIdx.x >> 3);
+  if (job >= p.jobs) return;
+  const int split = job / (p.mt * p.nt), tile = job - split * (p.mt * p.nt);
+  const int mrow0 = (tile % p.mt) * 64 * WM, n0 = (tile / p.mt) * 64 * WN;
+  const int vbeg = split * p.chunk;
   const int vend = min(p.pvox, vbeg + p.chunk);
   const int nsteps = vend > vbeg ? (vend - vbeg + 31) >> 5 : 0;
 
@@ -215,7 +223,7 @@ __global__ __launch_bounds__(256, 2) void dw_lds_kernel(const uint16_t *__restri
   }
 
   // every partial element of the block is written (zeros for an empty slice)
-  float *dst = part + (long long)blockIdx.z * p.m * p.co;
+  float *dst = part + (long long)split * p.m * p.co;
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -285,8 +293,12 @@ hipError_t launch_conv_bwd_weight_direct(const ConvShape &s, const void *x, cons
   p.fow = make_fastdiv(s.ow);
   p.foh = make_fastdiv(s.oh);
   p.fod = make_fastdiv(s.od);
+  p.mt = pl.mt;
+  p.nt = pl.nt;
+  p.jobs = pl.mt * pl.nt * pl.nsplit;
+  p.per = (p.jobs + 7) / 8;
   float *part = (float *)ws;
-  const dim3 grid((unsigned)pl.mt, (unsigned)pl.nt, (unsigned)pl.nsplit);
+  const dim3 grid((unsigned)(8 * p.per));
   if (pl.wn == 2)
     hipLaunchKernelGGL(dw_lds_kernel<2>, grid, dim3(256), 0, st, (const uint16_t *)x, (const uint16_t *)dz, part, p);
   else

@@ -163,8 +163,8 @@ def test_direct_prefetch_depths(case, tile, pf, monkeypatch):
     assert e <= TOL["bf16"], e
 
 
-# the LDS-staged kernel: 4-stage DMA ring run in whole rounds of four k-steps,
-# so step counts below one round and not a multiple of four are covered
+# the LDS-staged kernel: a 4- or 8-stage DMA ring run in whole rounds of
+# k-steps, so step counts below one round and not a multiple of it are covered
 LDS_CASES = CASES + [
     (1, (5, 6, 7), 32, 64, 1, 1),      # a single k-step (three padding steps); backward-data N = 32
     (2, (7, 9, 6), 64, 32, 3, 2),      # k = 3, stride 2: classes of 1, 2, 4 and 8 taps
@@ -172,12 +172,15 @@ LDS_CASES = CASES + [
 ]
 
 
+@pytest.mark.parametrize("stages", ["4", "8"])
 @pytest.mark.parametrize("kern", ["lds128", "lds64"])
 @pytest.mark.parametrize("case", LDS_CASES, ids=ids)
-def test_lds_kernel(case, kern, monkeypatch):
+def test_lds_kernel(case, kern, stages, monkeypatch):
     """Forward, forward with the fused bias + leaky-ReLU epilogue and its mask,
-    and backward-data through the LDS-staged kernel at both row tiles."""
+    and backward-data through the LDS-staged kernel at both row tiles and
+    both ring depths."""
     monkeypatch.setenv("CF_DIRECT_KERNEL", kern)
+    monkeypatch.setenv("CF_DIRECT_STAGES", stages)
     N, dhw, CI, CO, k, s = case
     rng = np.random.default_rng(36)
     desc = B.make_desc(N, dhw, CI, CO, k, s, "same", "bf16")
