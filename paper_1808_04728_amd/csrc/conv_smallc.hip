@@ -196,16 +196,20 @@ __global__ __launch_bounds__(256) void conv_smallc_fwd_kernel(
     for (int bw8 = 0; bw8 < TW / 8; ++bw8) {
       f32x4_t acc[2][NF];  // [dd][channel block]
 #pragma unroll
-      for (int dd = 0; dd < 2; ++dd) {
-        const int imm = ((dd * HH * HWS) + 8 * bw8) * CIN * (int)sizeof(T);
+      for (int dd = 0; dd < 2; ++dd)
 #pragma unroll
         for (int f = 0; f < NF; ++f) acc[dd][f] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int dd = 0; dd < 2; ++dd) {
+        const int imm = ((dd * HH * HWS) + 8 * bw8) * CIN * (int)sizeof(T);
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
           AFrag a;
           if constexpr (BF) {
-            // built element by element so that the halves load straight into
-            // place (ds_read_u16_d16 / _d16_hi) instead of being packed afterwards
+            // element by element (16-bit reads, packed in pairs by the compiler:
+            // with SRAM ECC on, as on this part, a 16-bit read into half a
+            // register does not keep the other half, so halves cannot be
+            // loaded in place)
             typedef short v8i16_t __attribute__((ext_vector_type(8)));
             v8i16_t v;
 #pragma unroll
@@ -239,7 +243,10 @@ __global__ __launch_bounds__(256) void conv_smallc_fwd_kernel(
       } else {
         const int pd_ = vd0 >> 1, ph_ = vh0 >> 1, pw_ = (vw0 >> 1) + q;
         const bool pin = pd_ < p.pod && ph_ < p.poh && pw_ < p.pow_;
-        const long long pbase = ((((long long)n * p.pod + pd_) * p.poh + ph_) * p.pow_ + pw_) * COUT;
+        // pooled row of this lane's first pair; pair bw8 sits 4 bw8 pooled voxels on
+        // (a compile-time offset from one row pointer)
+        T *const prow = out + ((((long long)n * p.pod + pd_) * p.poh + ph_) * p.pow_ + (ow0 >> 1) + q) * COUT +
+                        (long long)(4 * bw8 * COUT);
 #pragma unroll
         for (int f = 0; f < NF; ++f) {
           float s = 0.f;
@@ -254,15 +261,21 @@ __global__ __launch_bounds__(256) void conv_smallc_fwd_kernel(
               s = fmaf(pos ? 1.f : alpha, u, s);
             }
           // pooled voxel (pd, ph, pw + q): the whole window sits in this lane
-          if (pin) out[pbase + 16 * f + r] = from_f32<DT>(s * 0.125f);
+          if (pin) prow[16 * f + r] = from_f32<DT>(s * 0.125f);
           if constexpr (NF == 1) {
             // the eight ballots of the pair go to LDS as they are (one lane writes);
             // the row's mask words are interleaved from them after the last pair
+            // one 64-bit move per ballot (uniform values, every lane gets a copy)
+            uint64_t bv[2][4];
+#pragma unroll
+            for (int dd = 0; dd < 2; ++dd)
+#pragma unroll
+              for (int j = 0; j < 4; ++j) asm volatile("v_mov_b64 %0, %1" : "=v"(bv[dd][j]) : "s"(bal[dd][j]));
             if (lane == 0) {
 #pragma unroll
               for (int dd = 0; dd < 2; ++dd)
 #pragma unroll
-                for (int j = 0; j < 4; ++j) bstage[wave][bw8 * 8 + dd * 4 + j] = bal[dd][j];
+                for (int j = 0; j < 4; ++j) bstage[wave][bw8 * 8 + dd * 4 + j] = bv[dd][j];
             }
           } else {
             // general channel count: lanes 0..3 write mask row (dd, hh) as half-words
