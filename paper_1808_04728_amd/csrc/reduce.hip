@@ -123,8 +123,10 @@ hipError_t launch_sum_batch(const SumJob *jobs, int n, hipStream_t st) {
       J.rows = s.rows;
       J.cols = s.cols;
       // phases: each thread sums ~4 rows of a narrow matrix (few workgroups: the
-      // serial chain is the latency), ~16 of a wide one; at most 64
-      const int per = s.cols < 256 ? 4 : 16;
+      // serial chain is the latency), ~64 of a wide one (fewer, longer row
+      // segments per workgroup: measured fastest on the stack's partials); at
+      // most 64 phases
+      const int per = s.cols < 256 ? 4 : 64;
       int ph = 1;
       while (ph < 64 && (long long)ph * per < s.rows) ph *= 2;
       J.ph = ph;
