@@ -52,7 +52,9 @@ struct C16 {
   static constexpr int LDS_BYTES = (HALO_PAD + W_VEC) * 16 + 8 * MSTAGE_WAVE;
 };
 
-template <int KE, int EPI>
+// AMAX: alpha <= 1, where lrelu(u) = max(u, alpha u); else min(u, alpha u).
+// Either form equals u > 0 ? u : alpha u bit for bit, and needs no lane mask.
+template <int KE, int EPI, bool AMAX>
 __global__ __launch_bounds__(512, 1) void conv_c16_fwd_kernel(const uint16_t *__restrict__ x,
                                                               const uint16_t *__restrict__ w,
                                                               const float *__restrict__ bias, float alpha,
@@ -155,7 +157,7 @@ __global__ __launch_bounds__(512, 1) void conv_c16_fwd_kernel(const uint16_t *__
 #pragma unroll
       for (int b = 0; b < BH; ++b)
 #pragma unroll
-        for (int j = 0; j < 16; ++j) acc[a][b][j] = 0.f;
+        for (int j = 0; j < 16; ++j) acc[a][b][j] = bz;  // the bias enters as the accumulators' start
 
     // (kd, kw) steps, software-pipelined: the fragment reads of step s + 1 go
     // into the other register set before the MFMAs of step s are issued
@@ -218,13 +220,15 @@ __global__ __launch_bounds__(512, 1) void conv_c16_fwd_kernel(const uint16_t *__
           }
         }
     } else {
-      // u = acc + b; y = lrelu(u); the slope mask word of a voxel (32 channel
+      // u = acc (started at b); the slope mask word of a voxel (32 channel
       // bits) is half of a wave ballot of one accumulator register.  Every lane
       // stores ballot >> (32 * half) to LDS without a branch (a branch would
       // have to keep the compare alive across it): lanes 0 and 32 into the
       // wave's stage (dword 2 j + half), every other lane into a private junk
       // slot.  After the 16 registers of an output row, 32 lanes write the
-      // row's 128 mask bytes at once.
+      // row's 128 mask bytes at once.  The leaky ReLU is a multiply and a
+      // max (or min): a select on the compare would keep one lane mask per
+      // register alive until the pooling below.
       unsigned char *mst = reinterpret_cast<unsigned char *>(wp + G::W_VEC) + wave * G::MSTAGE_WAVE;
       const int mslot = (lane & 31) == 0 ? 4 * half : 128 + 4 * lane;
 #pragma unroll
@@ -234,12 +238,18 @@ __global__ __launch_bounds__(512, 1) void conv_c16_fwd_kernel(const uint16_t *__
           const int vd = vd0 + dd, vh = vh0 + hh;
 #pragma unroll
           for (int j = 0; j < 16; ++j) {
-            const float u = acc[dd][hh][j] + bz;
+            const float u = acc[dd][hh][j];
             const unsigned long long bal = __ballot(u > 0.f);
             *reinterpret_cast<uint32_t *>(mst + mslot + 8 * j) = (uint32_t)(bal >> (32 * half));
-            // leaky ReLU without a compare (a select would keep one lane mask per
-            // register alive until the pooling below)
-            acc[dd][hh][j] = fmaxf(u, 0.f) + alpha * fminf(u, 0.f);
+            // one max (min) instruction: fmaxf would first canonicalize u, which
+            // is a finite sum of products here
+            const float au = alpha * u;
+            float y;
+            if constexpr (AMAX)
+              asm("v_max_f32 %0, %1, %2" : "=v"(y) : "v"(u), "v"(au));
+            else
+              asm("v_min_f32 %0, %1, %2" : "=v"(y) : "v"(u), "v"(au));
+            acc[dd][hh][j] = y;
           }
           if (mask != nullptr) {
             __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -294,13 +304,13 @@ __global__ __launch_bounds__(512, 1) void conv_c16_fwd_kernel(const uint16_t *__
   }
 }
 
-template <int KE, int EPI>
+template <int KE, int EPI, bool AMAX>
 hipError_t launch_t(const C16Params &p, const void *x, const void *w, const float *bias, float alpha, void *out,
                     uint32_t *mask, hipStream_t st) {
   using G = C16<KE>;
   static bool attr_set = false;
   if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void *)conv_c16_fwd_kernel<KE, EPI>,
+    hipError_t e = hipFuncSetAttribute((const void *)conv_c16_fwd_kernel<KE, EPI, AMAX>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, G::LDS_BYTES);
     if (e != hipSuccess) return e;
     attr_set = true;
@@ -310,7 +320,7 @@ hipError_t launch_t(const C16Params &p, const void *x, const void *w, const floa
   const long long tiles = (long long)p.n * ((p.od + TD - 1) / TD) * ((p.oh + TH - 1) / TH) * ((p.ow + TW - 1) / TW);
   int blocks = (int)std::min<long long>(tiles, cus);
   blocks = std::max(8, (blocks + 7) / 8 * 8);
-  hipLaunchKernelGGL((conv_c16_fwd_kernel<KE, EPI>), dim3(blocks), dim3(64 * NWAVE), G::LDS_BYTES, st,
+  hipLaunchKernelGGL((conv_c16_fwd_kernel<KE, EPI, AMAX>), dim3(blocks), dim3(64 * NWAVE), G::LDS_BYTES, st,
                      (const uint16_t *)x, (const uint16_t *)w, bias, alpha, (uint16_t *)out, mask, p);
   return hipGetLastError();
 }
@@ -333,9 +343,12 @@ hipError_t launch_conv_fwd_c16(const ConvShape &s, const void *x, const void *w,
   p.x_bytes = (int)((long long)s.n * s.d * s.h * s.w * s.ci * 2);
 #define CF_C16_CASE(KEV)                                                                      \
   if (s.kd == KEV) {                                                                          \
-    if (epi == 0) return launch_t<KEV, 0>(p, x, w, bias, alpha, out, mask, st);               \
-    if (epi == 1) return launch_t<KEV, 1>(p, x, w, bias, alpha, out, mask, st);               \
-    return launch_t<KEV, 2>(p, x, w, bias, alpha, out, mask, st);                             \
+    if (epi == 0) return launch_t<KEV, 0, true>(p, x, w, bias, alpha, out, mask, st);         \
+    if (alpha <= 1.f)                                                                         \
+      return epi == 1 ? launch_t<KEV, 1, true>(p, x, w, bias, alpha, out, mask, st)           \
+                      : launch_t<KEV, 2, true>(p, x, w, bias, alpha, out, mask, st);          \
+    return epi == 1 ? launch_t<KEV, 1, false>(p, x, w, bias, alpha, out, mask, st)            \
+                    : launch_t<KEV, 2, false>(p, x, w, bias, alpha, out, mask, st);           \
   }
   CF_C16_CASE(2) CF_C16_CASE(3) CF_C16_CASE(4)
 #undef CF_C16_CASE
