@@ -25,6 +25,14 @@ __device__ __forceinline__ uint16_t f2bf(float f) {
   return __builtin_bit_cast(uint16_t, b);
 }
 
+// two floats -> two bf16 (round to nearest even) in one v_cvt_pk_bf16_f32, lo in bits 0..15
+__device__ __forceinline__ uint32_t f2bf2(float lo, float hi) {
+  typedef float f32x2_t __attribute__((ext_vector_type(2)));
+  typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+  const bf16x2_t b = __builtin_convertvector((f32x2_t{lo, hi}), bf16x2_t);
+  return __builtin_bit_cast(uint32_t, b);
+}
+
 template <int DT> __device__ __forceinline__ float to_f32(typename Store<DT>::T v);
 template <> __device__ __forceinline__ float to_f32<DT_F32>(float v) { return v; }
 template <> __device__ __forceinline__ float to_f32<DT_BF16>(uint16_t v) { return bf2f(v); }

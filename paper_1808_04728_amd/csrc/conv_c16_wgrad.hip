@@ -109,7 +109,9 @@ __global__ __launch_bounds__(256, 2) void c16_wgrad_kernel(const uint16_t *__res
     const int e = 64 * (wave + 4 * k) + lane;
     const int hf = e & 1, v = e >> 1;
     const int hw = v % HW, hh = (v / HW) % HH, hd = v / (HW * HH);
-    xrel[k] = (uint32_t)((((hd * p.h + hh) * p.w + hw) * 16 + 8 * hf) * 2);
+    // padding slots: an offset past every buffer (the range check, which does
+    // not include the scalar offset, returns zeros)
+    xrel[k] = e < XH_VEC ? (uint32_t)((((hd * p.h + hh) * p.w + hw) * 16 + 8 * hf) * 2) : 0x80000000u;
     xpk[k] = e < XH_VEC ? (uint32_t)(hw | hh << 6 | hd << 9) : 31u << 9;
   }
   // unfused dz tile likewise: slot e = (voxel of the tile) * 4 + channel quarter
@@ -140,15 +142,25 @@ __global__ __launch_bounds__(256, 2) void c16_wgrad_kernel(const uint16_t *__res
     {
       const int x0d = o0d - p.pd, x0h = o0h - p.ph, x0w = o0w - p.pw;  // halo origin (may be < 0)
       const uint32_t base = (uint32_t)(((n * p.d + x0d) * p.h + x0h) * p.w + x0w) * 32u;
+      const bool xin = x0d >= 0 && x0d + HD <= p.d && x0h >= 0 && x0h + HH <= p.h && x0w >= 0 && x0w + HW <= p.w;
+      if (xin) {
+        // the whole halo is inside x: per-slot offsets as computed once, the
+        // tile's base in the scalar offset
 #pragma unroll
-      for (int k = 0; k < NXC; ++k) {
-        uint32_t pk = xpk[k];
-        asm volatile("" : "+v"(pk));  // keep the decoded fields out of the tile loop's registers
-        const int hw = pk & 63, hh = (pk >> 6) & 7, hd = pk >> 9;
-        const bool ok = pk < (uint32_t)(HD << 9) && (unsigned)(x0w + hw) < (unsigned)p.w &&
-                        (unsigned)(x0h + hh) < (unsigned)p.h && (unsigned)(x0d + hd) < (unsigned)p.d;
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(xrsrc, (lds_void_t *)(xh + 64 * (wave + 4 * k)), 16,
-                                                 ok ? xrel[k] + base : 0x80000000u, 0, 0, 0);
+        for (int k = 0; k < NXC; ++k)
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(xrsrc, (lds_void_t *)(xh + 64 * (wave + 4 * k)), 16, xrel[k],
+                                                   (int)base, 0, 0);
+      } else {
+#pragma unroll
+        for (int k = 0; k < NXC; ++k) {
+          uint32_t pk = xpk[k];
+          asm volatile("" : "+v"(pk));  // keep the decoded fields out of the tile loop's registers
+          const int hw = pk & 63, hh = (pk >> 6) & 7, hd = pk >> 9;
+          const bool ok = pk < (uint32_t)(HD << 9) && (unsigned)(x0w + hw) < (unsigned)p.w &&
+                          (unsigned)(x0h + hh) < (unsigned)p.h && (unsigned)(x0d + hd) < (unsigned)p.d;
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(xrsrc, (lds_void_t *)(xh + 64 * (wave + 4 * k)), 16,
+                                                   ok ? xrel[k] + base : 0x80000000u, 0, 0, 0);
+        }
       }
       if constexpr (!FUSED) {
         const uint32_t zbase = (uint32_t)(((n * p.od + o0d) * p.oh + o0h) * p.ow + o0w) * 64u;
@@ -167,35 +179,65 @@ __global__ __launch_bounds__(256, 2) void c16_wgrad_kernel(const uint16_t *__res
 #pragma unroll
     for (int j = 0; j < 8; ++j) dbs[j] = 0.f;
     if constexpr (FUSED) {
+      // unit k of this thread: voxel (ld, lh, lw) of the tile (packed in zpk),
+      // channels 8 cq .. 8 cq + 7 with cq = tid & 3.  The tile origins are even
+      // in every dimension, so voxel and pooled-voxel indices are a per-tile
+      // base plus a per-unit offset; interior tiles skip the bounds tests.
+      const int cq = tid & 3;
+      const int vox0 = ((n * p.od + o0d) * p.oh + o0h) * p.ow + o0w;
+      const int pool0 = ((n * p.pod + (o0d >> 1)) * p.poh + (o0h >> 1)) * p.pow_ + (o0w >> 1);
+      // every voxel of the tile and its pooled voxel exist
+      const bool interior = o0d + TD <= 2 * p.pod && o0h + TH <= 2 * p.poh && o0w + TW <= 2 * p.pow_;
+      // dz = g / 8 * slope: the scale by 2^-3 is exact, so folding it into the
+      // slope gives the same bits as scaling first
+      const float s1 = 0.125f, sa = 0.125f * alpha;
+      // 8 channels of one voxel: dz (bf16 pairs) and the running bias sums
+      auto rebuild = [&](int pv, int vox) {
+        Vec16<DT_BF16> gv;
+        gv.u = *reinterpret_cast<const uint4 *>(g + (pv * 32 + 8 * cq));
+        const uint32_t bits = mask[vox] >> (8 * cq);
+        float d[8];
 #pragma unroll
-      for (int k = 0; k < NZ; ++k) {
-        const int e = tid + 256 * k;  // e & 3: which 8 of the 32 channels (fixed per thread)
-        const int cq = e & 3;
-        int v = e >> 2;
-        const int lw = v % TW; v /= TW;
-        const int lh = v % TH;
-        const int ld = v / TH;
-        const int od = o0d + ld, oh = o0h + lh, ow = o0w + lw;
-        uint4 val = make_uint4(0, 0, 0, 0);
-        if (od < p.od && oh < p.oh && ow < p.ow) {
-          const long long vox = (((long long)n * p.od + od) * p.oh + oh) * p.ow + ow;
-          const int pd_ = od >> 1, ph_ = oh >> 1, pw_ = ow >> 1;
-          if (pd_ < p.pod && ph_ < p.poh && pw_ < p.pow_) {
-            Vec16<DT_BF16> gv;
-            gv.u = *reinterpret_cast<const uint4 *>(
-                g + ((((long long)n * p.pod + pd_) * p.poh + ph_) * p.pow_ + pw_) * 32 + 8 * cq);
-            const uint32_t bits = mask[vox] >> (8 * cq);
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-              const float d = bf2f(gv.e[j]) * 0.125f * (((bits >> j) & 1u) ? 1.f : alpha);
-              dbs[j] += d;
-              gv.e[j] = f2bf(d);
-            }
-            val = gv.u;
-          }
-          if (dz_out) *reinterpret_cast<uint4 *>(dz_out + vox * 32 + 8 * cq) = val;
+        for (int j = 0; j < 8; ++j) {
+          // slope bits picked by the sign-extended mask bit (all ones or zero)
+          const uint32_t m = (uint32_t)__builtin_amdgcn_sbfe((int)bits, j, 1);
+          uint32_t sl;
+          asm("v_bfi_b32 %0, %1, %2, %3" : "=v"(sl) : "v"(m), "s"(__float_as_uint(s1)), "v"(__float_as_uint(sa)));
+          d[j] = bf2f(gv.e[j]) * __uint_as_float(sl);
+          dbs[j] += d[j];
         }
-        dzt[tid + 256 * k] = val;  // the tile region is free: every read of it ended at the barrier above
+        return make_uint4(f2bf2(d[0], d[1]), f2bf2(d[2], d[3]), f2bf2(d[4], d[5]), f2bf2(d[6], d[7]));
+      };
+      if (interior) {
+#pragma unroll
+        for (int k = 0; k < NZ; ++k) {
+          uint32_t pk = zpk[k];
+          asm volatile("" : "+v"(pk));  // keep the decoded fields out of the tile loop's registers
+          const int lw = pk & 63, lh = (pk >> 6) & 7, ld = pk >> 9;
+          const int vox = vox0 + (int)__umul24(__umul24(ld, p.oh) + lh, p.ow) + lw;
+          const int pv = pool0 + (int)__umul24(__umul24(ld >> 1, p.poh) + (lh >> 1), p.pow_) + (lw >> 1);
+          const uint4 val = rebuild(pv, vox);
+          if (dz_out) *reinterpret_cast<uint4 *>(dz_out + (vox * 32 + 8 * cq)) = val;
+          dzt[tid + 256 * k] = val;  // the tile region is free: every read of it ended at the barrier above
+        }
+      } else {
+#pragma unroll
+        for (int k = 0; k < NZ; ++k) {
+          uint32_t pk = zpk[k];
+          asm volatile("" : "+v"(pk));
+          const int lw = pk & 63, lh = (pk >> 6) & 7, ld = pk >> 9;
+          const int od = o0d + ld, oh = o0h + lh, ow = o0w + lw;
+          const bool in_dz = od < p.od && oh < p.oh && ow < p.ow;
+          const bool in_p = (od >> 1) < p.pod && (oh >> 1) < p.poh && (ow >> 1) < p.pow_;
+          const int vox = vox0 + (int)__umul24(__umul24(ld, p.oh) + lh, p.ow) + lw;
+          const int pv = pool0 + (int)__umul24(__umul24(ld >> 1, p.poh) + (lh >> 1), p.pow_) + (lw >> 1);
+          uint4 val = make_uint4(0, 0, 0, 0);
+          if (in_dz) {
+            if (in_p) val = rebuild(pv, vox);
+            if (dz_out) *reinterpret_cast<uint4 *>(dz_out + (vox * 32 + 8 * cq)) = val;
+          }
+          dzt[tid + 256 * k] = val;
+        }
       }
       float4 a = dbl[0], b = dbl[1];
       a.x += dbs[0]; a.y += dbs[1]; a.z += dbs[2]; a.w += dbs[3];
