@@ -308,7 +308,7 @@ __global__ __launch_bounds__(256) void l1_wgrad_kernel(const uint16_t *__restric
   const int r = lane & 15, q = lane >> 4;
   const int tiles_w = (p.ow + TW - 1) / TW, tiles_h = (p.oh + TH - 1) / TH, tiles_d = (p.od + TD - 1) / TD;
   const int tiles_per_n = tiles_w * tiles_h * tiles_d;
-  const long long total_tiles = (long long)p.n * tiles_per_n;
+  const int total_tiles = p.n * tiles_per_n;  // the launcher keeps every index below 2^24
 
   // the constant planes: ones (A row M) and zeros (A rows beyond M)
   for (int e = tid; e < 2 * PLANE * XP; e += 256)
@@ -341,10 +341,10 @@ __global__ __launch_bounds__(256) void l1_wgrad_kernel(const uint16_t *__restric
   u32x4_t xv[3], dv, mv;
   int cur_n = 0, cur_od0 = 0, cur_oh0 = 0, cur_ow0 = 0;
   auto tile_origin = [&](int it, int &n, int &od0, int &oh0, int &ow0) -> bool {
-    const long long gt = (long long)blockIdx.x * p.tiles_per_block + it;
+    const int gt = (int)blockIdx.x * p.tiles_per_block + it;
     if (it >= p.tiles_per_block || gt >= total_tiles) return false;
-    int t = (int)(gt % tiles_per_n);
-    n = (int)(gt / tiles_per_n);
+    int t = gt % tiles_per_n;
+    n = gt / tiles_per_n;
     const int tw = t % tiles_w; t /= tiles_w;
     const int th = t % tiles_h;
     const int td = t / tiles_h;
@@ -359,7 +359,8 @@ __global__ __launch_bounds__(256) void l1_wgrad_kernel(const uint16_t *__restric
     if (tid < NXI) {
       const int id = od0 - p.pd + xa, ih = oh0 - p.ph + xb;
       if ((unsigned)id < (unsigned)p.d && (unsigned)ih < (unsigned)p.h) {
-        const long long rowoff = (((long long)n * p.d + id) * p.h + ih) * p.w;
+        // 24-bit products: n d h, n od oh and the element counts are below 2^24 / 2^31
+        const int rowoff = (int)__umul24(__umul24(n * p.d + id, p.h) + ih, p.w);
 #pragma unroll
         for (int j = 0; j < 3; ++j) {
           const int iw = ow0 - 8 + 8 * (xi + j);
@@ -372,8 +373,8 @@ __global__ __launch_bounds__(256) void l1_wgrad_kernel(const uint16_t *__restric
     {
       const int pd_ = (od0 >> 1) + (tid >> 7), ph_ = (oh0 >> 1) + ((tid >> 5) & 3), pw_ = (ow0 >> 1) + ((tid >> 1) & 15);
       if (pd_ < p.pod && ph_ < p.poh && pw_ < p.pow_)
-        dv = *reinterpret_cast<const u32x4_t *>(dp + ((((long long)n * p.pod + pd_) * p.poh + ph_) * p.pow_ + pw_) *
-                                                      16 + 8 * (tid & 1));
+        dv = *reinterpret_cast<const u32x4_t *>(
+            dp + ((int)__umul24(__umul24(n * p.pod + pd_, p.poh) + ph_, p.pow_) + pw_) * 16 + 8 * (tid & 1));
     }
     // slope mask: thread tid < 128 loads 8 voxels (16 bytes) of w-row tid / 4
     mv = u32x4_t{0u, 0u, 0u, 0u};
@@ -381,7 +382,7 @@ __global__ __launch_bounds__(256) void l1_wgrad_kernel(const uint16_t *__restric
       const int row = tid >> 2;
       const int vd = od0 + row / TH, vh = oh0 + row % TH, vw = ow0 + 8 * (tid & 3);
       if (vd < p.od && vh < p.oh && vw < p.ow)
-        mv = *reinterpret_cast<const u32x4_t *>(mask16 + (((long long)n * p.od + vd) * p.oh + vh) * p.ow + vw);
+        mv = *reinterpret_cast<const u32x4_t *>(mask16 + (int)__umul24(__umul24(n * p.od + vd, p.oh) + vh, p.ow) + vw);
     }
   };
 
@@ -496,10 +497,15 @@ hipError_t launch_t(const ConvShape &s, const SmallcParams &p, const void *x, co
 
 // the register-built-dz kernel: one input channel, 16 output channels, bf16,
 // rows of whole 16-byte vectors, left padding of at most one voxel
+// and index arithmetic in 24-bit products: n d h and n od oh below 2^24 (the
+// 128^3 stack at batch 8 has 2^17), every element offset below 2^31
 bool l1_supported(const ConvShape &s) {
+  const long long ndh = (long long)s.n * s.d * s.h, nodoh = (long long)s.n * s.od * s.oh;
+  const long long xel = ndh * s.w, mel = nodoh * s.ow * 16;
   return s.dtype == DT_BF16 && s.ci == 1 && s.co == 16 && s.sd == 1 && s.sh == 1 && s.sw == 1 && s.kd == s.kh &&
          s.kd == s.kw && (s.kd == 2 || s.kd == 3) && s.pw <= 1 && (s.kd == 3 || s.pw == 0) && s.w % 8 == 0 &&
-         s.ow % 8 == 0;
+         s.ow % 8 == 0 && ndh < (1LL << 24) && nodoh < (1LL << 24) && s.w < (1 << 24) && s.ow < (1 << 24) &&
+         xel < (1LL << 31) && mel < (1LL << 31);
 }
 
 }  // namespace
