@@ -326,10 +326,11 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const uint16_t *__rest
 //    wave) and share every k-step's operands, which arrive by buffer -> LDS
 //    DMA: the A tile (BM gathered voxels x 32 channels, padding voxels read as
 //    zero through the range check) and the B tile (32 x BN weights);
-//  * NS stages (4 or 8), each its own LDS array, visited in an unrolled
-//    ring: the loads of steps s + 1 .. s + NS - 1 are in flight while step s
-//    runs, one barrier per k-step; the fragments of step s + 1 are read while
-//    the MFMAs of step s run.  Distinct arrays and a compile-time stage per unrolled step let
+//  * NS stages (4 or 8) of KS k-steps each (KS = 2: half the barriers and
+//    per-step overhead per MFMA), each stage its own LDS array, visited in an
+//    unrolled ring: the loads of stages s + 1 .. s + NS - 1 are in flight
+//    while stage s runs, one barrier per stage; the fragments of stage s + 1
+//    are read while the MFMAs of stage s run.  Distinct arrays and a compile-time stage per unrolled step let
 //    the compiler see that a stage's reads do not alias the other stages'
 //    DMA, so the only wait is the explicit one on this step's loads; the
 //    barrier is a bare s_barrier because a release fence would wait for all
@@ -359,7 +360,7 @@ __device__ __forceinline__ void for_stages(F &&f) {
   }
 }
 
-template <bool FWD, int FM, int FN, bool ACT, int NS>
+template <bool FWD, int FM, int FN, bool ACT, int NS, int KS>
 __global__ __launch_bounds__(256) void conv_lds_kernel(const uint16_t *__restrict__ src,
                                                        const uint16_t *__restrict__ wt,
                                                        const float *__restrict__ bias,
@@ -369,7 +370,7 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(const uint16_t *__restric
   constexpr int A_SLOTS = BM * 4;                     // 16-byte slots of the A tile
   constexpr int B_SLOTS = 32 * BN / 8;                // 16-byte slots of the B tile
   constexpr int A_BYTES = A_SLOTS * 16, B_BYTES = B_SLOTS * 16;
-  constexpr int STAGE = A_BYTES + B_BYTES;
+  constexpr int STAGE = A_BYTES + B_BYTES;            // one k-step's tiles; KS of them per stage
   constexpr int NA = A_SLOTS / 256;                   // A DMA instructions per wave and step
   constexpr int NB = (B_SLOTS + 255) / 256;           // B DMA instructions per wave and step
   constexpr int RED_LD = BN + 4;
@@ -377,9 +378,13 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(const uint16_t *__restric
   static_assert(!FWD || FN == 4, "forward weight tiles are 64 output channels wide");
   static_assert(16 * FM * RED_LD * 4 <= STAGE, "a wave's fp32 rows fit its stage array");
   static_assert(NS == 4 || NS == 8, "four or eight stages");
+  static_assert(KS == 1 || KS == 2, "one or two k-steps per stage");
+  static_assert(NS * KS <= 8, "at most eight k-step arrays");
+  // k-step u of stage S lives in array S + NS u: every array is written by
+  // one DMA pattern, so the compiler matches each fragment read to its DMA
   __shared__ __attribute__((aligned(16))) unsigned char stg0[STAGE], stg1[STAGE], stg2[STAGE], stg3[STAGE];
-  __shared__ __attribute__((aligned(16))) unsigned char stg4[NS > 4 ? STAGE : 16], stg5[NS > 4 ? STAGE : 16];
-  __shared__ __attribute__((aligned(16))) unsigned char stg6[NS > 4 ? STAGE : 16], stg7[NS > 4 ? STAGE : 16];
+  __shared__ __attribute__((aligned(16))) unsigned char stg4[NS * KS > 4 ? STAGE : 16], stg5[NS * KS > 4 ? STAGE : 16];
+  __shared__ __attribute__((aligned(16))) unsigned char stg6[NS * KS > 4 ? STAGE : 16], stg7[NS * KS > 4 ? STAGE : 16];
   typedef __attribute__((address_space(3))) void lds_void_t;
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -441,7 +446,7 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(const uint16_t *__restric
     }
   }
 
-  auto stage = [&](auto ix) -> unsigned char * {
+  auto arr = [&](auto ix) -> unsigned char * {
     constexpr int S = decltype(ix)::v;
     if constexpr (S == 0) return stg0;
     else if constexpr (S == 1) return stg1;
@@ -461,8 +466,7 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(const uint16_t *__restric
   // past the end stay on the last tap with every A slot out of range, so they
   // load zeros and add nothing.
   int iti = 0, icc = 0, ileft = 0;
-  auto issue = [&](auto ix) {
-    unsigned char *stg = stage(ix);
+  auto issue_one = [&](unsigned char *stg) {
     const int dd = __builtin_amdgcn_readlane(v_dd, iti), dh = __builtin_amdgcn_readlane(v_dh, iti);
     const int dw = __builtin_amdgcn_readlane(v_dw, iti);
     const int aoff = __builtin_amdgcn_readlane(v_aoff, iti) + 32 * icc;
@@ -488,6 +492,10 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(const uint16_t *__restric
       ++iti;
     }
   };
+  auto issue = [&](auto ix) {
+    constexpr int S = decltype(ix)::v;
+    for_stages<0, KS>([&](auto u) { issue_one(arr(StageIx<S + NS * decltype(u)::v>{})); });
+  };
 
   f32x4_t acc[FM][FN];
 #pragma unroll
@@ -495,9 +503,9 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(const uint16_t *__restric
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  // MFMA fragments of the step held in stage ix
-  auto read_frags = [&](auto ix, bf16x8_t (&af)[FM], bf16x8_t (&bf)[FN]) {
-    const unsigned char *stg = stage(ix);
+  // MFMA fragments of k-step u of stage ix
+  auto read_frags = [&](auto ix, auto u, bf16x8_t (&af)[FM], bf16x8_t (&bf)[FN]) {
+    const unsigned char *stg = arr(StageIx<decltype(ix)::v + NS * decltype(u)::v>{});
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
       const int row = wave * 16 * FM + 16 * i + r16;
@@ -521,43 +529,48 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(const uint16_t *__restric
     }
   };
 
-  // fragments of the step about to run (read one step ahead)
-  bf16x8_t af[FM], bf[FN];
+  // fragments of the stage about to run (read one stage ahead)
+  bf16x8_t af[KS][FM], bf[KS][FN];
 
-  // k-step s on stage ix, its fragments already in af / bf: wait for this
-  // wave's loads of step s + 1 (the loads of the next NS - 3 steps may stay in
-  // flight) and for its fragment reads of step s, barrier (everyone's loads
-  // of step s + 1 landed; nobody reads the stage of step s - 1 any more),
-  // refill that stage with step s + NS - 1, read the fragments of step s + 1
-  // while the MFMAs of step s run
+  // stage s (KS k-steps) on array ix, its fragments already in af / bf: wait
+  // for this wave's loads of stage s + 1 (those of the next NS - 3 stages may
+  // stay in flight) and for its fragment reads of stage s, barrier
+  // (everyone's loads of stage s + 1 landed; nobody reads the array of stage
+  // s - 1 any more), refill that array with stage s + NS - 1, read the
+  // fragments of stage s + 1 while the MFMAs of stage s run
   auto kstep = [&](auto ix) {
     constexpr int S = decltype(ix)::v;
-    constexpr int VMC = (NS - 3) * (NA + NB);
+    constexpr int VMC = (NS - 3) * (NA + NB) * KS;
     __builtin_amdgcn_s_waitcnt(0x0070 | (VMC & 15) | ((VMC >> 4) << 14));  // vmcnt(VMC) lgkmcnt(0)
     asm volatile("s_barrier" ::: "memory");
     issue(StageIx<(S + NS - 1) % NS>{});
-    bf16x8_t an[FM], bn[FN];
-    read_frags(StageIx<(S + 1) % NS>{}, an, bn);
+    bf16x8_t an[KS][FM], bn[KS][FN];
+    for_stages<0, KS>([&](auto u) { read_frags(StageIx<(S + 1) % NS>{}, u, an[decltype(u)::v], bn[decltype(u)::v]); });
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
+    for (int u = 0; u < KS; ++u)
 #pragma unroll
-      for (int j = 0; j < FN; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
+      for (int i = 0; i < FM; ++i)
 #pragma unroll
-    for (int i = 0; i < FM; ++i) af[i] = an[i];
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[u][i], bf[u][j], acc[i][j], 0, 0, 0);
 #pragma unroll
-    for (int j = 0; j < FN; ++j) bf[j] = bn[j];
+    for (int u = 0; u < KS; ++u) {
+#pragma unroll
+      for (int i = 0; i < FM; ++i) af[u][i] = an[u][i];
+#pragma unroll
+      for (int j = 0; j < FN; ++j) bf[u][j] = bn[u][j];
+    }
   };
 
   if (nsteps > 0) {  // a class without taps leaves zeros
     ileft = nsteps;
     for_stages<0, NS - 1>([&](auto ix) { issue(ix); });
-    // step 0 landed everywhere, its fragments in registers
-    constexpr int VMC0 = (NS - 2) * (NA + NB);
+    // stage 0 landed everywhere, its fragments in registers
+    constexpr int VMC0 = (NS - 2) * (NA + NB) * KS;
     __builtin_amdgcn_s_waitcnt(0x0f70 | (VMC0 & 15) | ((VMC0 >> 4) << 14));  // vmcnt(VMC0)
     asm volatile("s_barrier" ::: "memory");
-    read_frags(StageIx<0>{}, af, bf);
-    for (int s = 0; s < nsteps; s += NS) for_stages<0, NS>([&](auto ix) { kstep(ix); });
+    for_stages<0, KS>([&](auto u) { read_frags(StageIx<0>{}, u, af[decltype(u)::v], bf[decltype(u)::v]); });
+    for (int s = 0; s < nsteps; s += NS * KS) for_stages<0, NS>([&](auto ix) { kstep(ix); });
   }
 
   // ---- each wave's fp32 rows leave through its stage array as 16-byte vectors
@@ -792,15 +805,23 @@ hipError_t launch_lds(int fm, DirParams &p, const void *src, const void *w, cons
   // the deeper ring (tests cover both)
   const char *e = getenv("CF_DIRECT_STAGES");
   const bool ns4 = !(e && atoi(e) == 8);
-#define CF_LDS_LAUNCH(FM_, NS_)                                                                                  \
-  hipLaunchKernelGGL((conv_lds_kernel<FWD, FM_, FN, ACT, NS_>), grid, dim3(256), 0, st, s16, w16, bias,         \
+  // k-steps per stage (four-stage ring): two forward (measured on the
+  // stride-2 layer: 30 -> 26 us), one for backward-data (its classes have few
+  // k-steps, and the larger stage halves the workgroups per compute unit);
+  // CF_DIRECT_KSUB=1|2 forces either; the eight-stage ring takes one
+  int ks = FWD ? 2 : 1;
+  if (const char *k = getenv("CF_DIRECT_KSUB")) ks = atoi(k) == 1 ? 1 : 2;
+#define CF_LDS_LAUNCH(FM_, NS_, KS_)                                                                             \
+  hipLaunchKernelGGL((conv_lds_kernel<FWD, FM_, FN, ACT, NS_, KS_>), grid, dim3(256), 0, st, s16, w16, bias,    \
                      (uint16_t *)dst, (uint8_t *)mask, p)
   if (fm == 2) {
-    if (ns4) CF_LDS_LAUNCH(2, 4);
-    else CF_LDS_LAUNCH(2, 8);
+    if (!ns4) CF_LDS_LAUNCH(2, 8, 1);
+    else if (ks == 2) CF_LDS_LAUNCH(2, 4, 2);
+    else CF_LDS_LAUNCH(2, 4, 1);
   } else {
-    if (ns4) CF_LDS_LAUNCH(1, 4);
-    else CF_LDS_LAUNCH(1, 8);
+    if (!ns4) CF_LDS_LAUNCH(1, 8, 1);
+    else if (ks == 2) CF_LDS_LAUNCH(1, 4, 2);
+    else CF_LDS_LAUNCH(1, 4, 1);
   }
 #undef CF_LDS_LAUNCH
   return hipGetLastError();

@@ -172,15 +172,17 @@ LDS_CASES = CASES + [
 ]
 
 
-@pytest.mark.parametrize("stages", ["4", "8"])
+@pytest.mark.parametrize("ring", ["4x1", "4x2", "8x1"])
 @pytest.mark.parametrize("kern", ["lds128", "lds64"])
 @pytest.mark.parametrize("case", LDS_CASES, ids=ids)
-def test_lds_kernel(case, kern, stages, monkeypatch):
+def test_lds_kernel(case, kern, ring, monkeypatch):
     """Forward, forward with the fused bias + leaky-ReLU epilogue and its mask,
-    and backward-data through the LDS-staged kernel at both row tiles and
-    both ring depths."""
+    and backward-data through the LDS-staged kernel at both row tiles, both
+    ring depths and one or two k-steps per stage."""
+    stages, ksub = ring.split("x")
     monkeypatch.setenv("CF_DIRECT_KERNEL", kern)
     monkeypatch.setenv("CF_DIRECT_STAGES", stages)
+    monkeypatch.setenv("CF_DIRECT_KSUB", ksub)
     N, dhw, CI, CO, k, s = case
     rng = np.random.default_rng(36)
     desc = B.make_desc(N, dhw, CI, CO, k, s, "same", "bf16")
