@@ -31,8 +31,12 @@ METRIC = "fwd+bwd 3D-conv TFLOP/s & samples/s, 128^3 CosmoFlow stack; % MFMA pea
 
 
 def describe(name, wl):
-    return (f"CosmoFlow conv stack, {wl['size']}^3 x {wl['c0']} input, batch {wl['batch']}, {wl['dtype']}, "
-            f"{len(wl['layers'])} conv layers (3 pooled), TF-SAME padding, fwd+bwd")
+    pads = {L.get("pad", "same") for L in wl["layers"]}
+    pad = "TF-SAME padding" if pads == {"same"} else "VALID padding" if pads == {"valid"} else "mixed padding"
+    pooled = sum(1 for L in wl["layers"] if L["pool"])
+    what = "CosmoFlow conv stack" if name.startswith("stack") else "the paper's first three conv layers"
+    return (f"{what}, {wl['size']}^3 x {wl['c0']} input, batch {wl['batch']}, {wl['dtype']}, "
+            f"{len(wl['layers'])} conv layers ({pooled} pooled), {pad}, fwd+bwd")
 
 
 def cpu_baseline(name, seconds_hint=True):
@@ -46,7 +50,7 @@ def cpu_baseline(name, seconds_hint=True):
     wl = dict(inputs.WORKLOADS[name])
     x = inputs.make_input(name)[:1]
     ws, bs = inputs.make_weights(name)
-    layers = [dict(k=L["k"], stride=L["stride"], pool=L["pool"]) for L in wl["layers"]]
+    layers = [dict(k=L["k"], stride=L["stride"], pool=L["pool"], pad=L.get("pad", "same")) for L in wl["layers"]]
     oracle.build(force=False)
     t0 = time.perf_counter()
     acts = oracle.stack_forward(x, layers, ws, bs, inputs.ALPHA)
@@ -56,7 +60,7 @@ def cpu_baseline(name, seconds_hint=True):
     flops = 0
     size = wl["size"]
     for i, L in enumerate(wl["layers"]):
-        out = -(-size // L["stride"])
+        out = -(-size // L["stride"]) if L.get("pad", "same") == "same" else (size - L["k"]) // L["stride"] + 1
         macs = out ** 3 * L["cout"] * L["k"] ** 3 * L["cin"]
         flops += 2 * macs * (2 if i == 0 else 3)
         size = out // 2 if L["pool"] else out

@@ -44,6 +44,18 @@ def stack_layers(c0: int = 1, c5: int = 128):
     ]
 
 
+def paper_layers():
+    """The first three conv layers of the paper's own network, the ones whose
+    geometry the per-layer FLOP products of Table I pin (Section V-B): VALID
+    padding, stride 1, each followed by the 2^3 stride-2 pool;
+    128^3 -> 126^3 -> 63^3 -> 60^3 -> 30^3 -> 27^3 -> 13^3."""
+    return [
+        dict(k=3, stride=1, cin=1, cout=16, pool=True, pad="valid"),
+        dict(k=4, stride=1, cin=16, cout=32, pool=True, pad="valid"),
+        dict(k=4, stride=1, cin=32, cout=64, pool=True, pad="valid"),
+    ]
+
+
 WORKLOADS = {
     # single layer, forward only
     "layer1_32c": dict(size=32, batch=1, dtype="f32", c0=1, recipe="iid",
@@ -56,6 +68,13 @@ WORKLOADS = {
                                layers=stack_layers(), backward=True, cfg=3),
     "stack_256c4_b2_bf16": dict(size=256, batch=2, dtype="bf16", c0=4, recipe="grf",
                                 layers=stack_layers(c0=4, c5=256), backward=True, cfg=4),
+    # the paper's own geometry (VALID) for its first three conv layers
+    "paper_c1c3_64_b1_f32": dict(size=64, batch=1, dtype="f32", c0=1, recipe="iid",
+                                 layers=paper_layers(), backward=True, cfg=5),
+    "paper_c1c3_128_b1_f32": dict(size=128, batch=1, dtype="f32", c0=1, recipe="grf",
+                                  layers=paper_layers(), backward=True, cfg=6),
+    "paper_c1c3_128_b8_bf16": dict(size=128, batch=8, dtype="bf16", c0=1, recipe="grf",
+                                   layers=paper_layers(), backward=True, cfg=7),
 }
 
 ALPHA = 0.01

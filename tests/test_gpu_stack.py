@@ -45,14 +45,16 @@ def fused_dz(l, g, alpha):
     return dy * np.where(mask_bits(l), 1.0, alpha)
 
 
+@pytest.mark.parametrize("name", ["stack_64c_b1_f32", "paper_c1c3_64_b1_f32"])
 @pytest.mark.parametrize("fused", [True, False])
-def test_stack_64_f32_chain(fused):
-    wl, st, dout = build("stack_64c_b1_f32", fused)
+def test_stack_64_f32_chain(fused, name):
+    """The SAME-padded stack and the paper's VALID first three layers."""
+    wl, st, dout = build(name, fused)
     st.forward()
     st.backward(dout)
     torch.cuda.synchronize()
     a = inputs.ALPHA
-    layers = [dict(k=L["k"], stride=L["stride"], pool=L["pool"]) for L in wl["layers"]]
+    layers = [dict(k=L["k"], stride=L["stride"], pool=L["pool"], pad=L.get("pad", "same")) for L in wl["layers"]]
     ws = [to_np(l["w"]) for l in st.L]
     bs = [to_np(l["b"]) for l in st.L]
     acts = oracle.stack_forward(to_np(st.x), layers, ws, bs, a)
@@ -80,11 +82,12 @@ def test_stack_64_f32_chain(fused):
             dz = to_np(l["dz"])
         e = maxabs_err(to_np(l["db"]), dbr)
         assert e <= TOL["f32"], ("db", i, e)
-        dwr = oracle.conv3d_bwd_weight(xin, dz, s["k"], stride=s["stride"])
+        pad = s.get("pad", "same")
+        dwr = oracle.conv3d_bwd_weight(xin, dz, s["k"], stride=s["stride"], pad=pad)
         e = maxabs_err(to_np(l["dw"]), dwr)
         assert e <= TOL["f32"], ("wgrad", i, e)
         if l["dx"] is not None:
-            dxr = oracle.conv3d_bwd_data(dz, to_np(l["w"]), l["in_dhw"], stride=s["stride"])
+            dxr = oracle.conv3d_bwd_data(dz, to_np(l["w"]), l["in_dhw"], stride=s["stride"], pad=pad)
             e = maxabs_err(to_np(l["dx"]), dxr)
             assert e <= TOL["f32"], ("dgrad", i, e)
             g = l["dx"]
@@ -94,7 +97,7 @@ def sample_idx(rng, shape, n):
     return np.stack([rng.integers(0, t, n) for t in shape], 1)
 
 
-@pytest.mark.parametrize("name", ["stack_128c_b1_f32", "stack_128c_b8_bf16"])
+@pytest.mark.parametrize("name", ["stack_128c_b1_f32", "stack_128c_b8_bf16", "paper_c1c3_128_b8_bf16"])
 def test_full_size_sampled(name):
     wl, st, dout = build(name, fused=True)
     st.forward()
@@ -116,12 +119,12 @@ def test_full_size_sampled(name):
             ref = []
             for n, pd, ph, pw, c in pidx:
                 pts = [(n, 2 * pd + u, 2 * ph + v, 2 * pw + t, c) for u in (0, 1) for v in (0, 1) for t in (0, 1)]
-                zz = oracle.conv3d_fwd_points(xin, w, pts, stride=s["stride"]) + b[c]
+                zz = oracle.conv3d_fwd_points(xin, w, pts, stride=s["stride"], pad=s.get("pad", "same")) + b[c]
                 ref.append(np.mean(np.where(zz > 0, zz, a * zz)))
             got = to_np(l["p"])[tuple(pidx.T)]
         else:
             zidx = sample_idx(rng, l["z"].shape, ns)
-            zz = oracle.conv3d_fwd_points(xin, w, zidx, stride=s["stride"]) + b[zidx[:, 4]]
+            zz = oracle.conv3d_fwd_points(xin, w, zidx, stride=s["stride"], pad=s.get("pad", "same")) + b[zidx[:, 4]]
             ref = np.where(zz > 0, zz, a * zz)
             got = to_np(l["z"])[tuple(zidx.T)]
         e = maxabs_err(got, np.asarray(ref))
@@ -133,7 +136,7 @@ def test_full_size_sampled(name):
         xin = to_np(st.layer_input(i))
         dz = fused_dz(l, g, a) if l["fused"] else to_np(l["dz"])
         widx = sample_idx(rng, l["dw"].shape, 24)
-        ref = oracle.conv3d_bwd_weight_points(xin, dz, s["k"], widx, stride=s["stride"])
+        ref = oracle.conv3d_bwd_weight_points(xin, dz, s["k"], widx, stride=s["stride"], pad=s.get("pad", "same"))
         e = maxabs_err(to_np(l["dw"])[tuple(widx.T)], ref)
         # a sample of dW: normalise by the largest |dW| of the full GPU tensor
         scale = np.abs(to_np(l["dw"])).max()
@@ -143,7 +146,8 @@ def test_full_size_sampled(name):
         assert e <= TOL[dt], ("db", i, e)
         if l["dx"] is not None:
             xidx = sample_idx(rng, l["dx"].shape, ns)
-            ref = oracle.conv3d_bwd_data_points(dz, to_np(l["w"]), l["in_dhw"], xidx, stride=s["stride"])
+            ref = oracle.conv3d_bwd_data_points(dz, to_np(l["w"]), l["in_dhw"], xidx, stride=s["stride"],
+                                                pad=s.get("pad", "same"))
             got = to_np(l["dx"])[tuple(xidx.T)]
             scale = np.abs(to_np(l["dx"])).max()
             assert np.abs(got - ref).max() <= TOL[dt] * scale, ("dgrad", i)
