@@ -381,8 +381,20 @@ __global__ __launch_bounds__(256) void l1_wgrad_kernel(const uint16_t *__restric
     if (tid < 128) {
       const int row = tid >> 2;
       const int vd = od0 + row / TH, vh = oh0 + row % TH, vw = ow0 + 8 * (tid & 3);
-      if (vd < p.od && vh < p.oh && vw < p.ow)
-        mv = *reinterpret_cast<const u32x4_t *>(mask16 + (int)__umul24(__umul24(n * p.od + vd, p.oh) + vh, p.ow) + vw);
+      if (vd < p.od && vh < p.oh && vw < p.ow) {
+        const uint16_t *mrow = mask16 + (int)__umul24(__umul24(n * p.od + vd, p.oh) + vh, p.ow);
+        if (vw + 8 <= p.ow) {
+          mv = *reinterpret_cast<const u32x4_t *>(mrow + vw);
+        } else {
+          // ragged end of a row: the voxels past it pool into no pooled voxel
+          // (their B values are zero), so their bits may be anything; read only
+          // the row's own voxels (the last row ends at the end of the buffer)
+          uint32_t h[8];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) h[u] = vw + u < p.ow ? mrow[vw + u] : 0u;
+          mv = u32x4_t{h[0] | h[1] << 16, h[2] | h[3] << 16, h[4] | h[5] << 16, h[6] | h[7] << 16};
+        }
+      }
     }
   };
 
@@ -496,7 +508,9 @@ hipError_t launch_t(const ConvShape &s, const SmallcParams &p, const void *x, co
 }
 
 // the register-built-dz kernel: one input channel, 16 output channels, bf16,
-// rows of whole 16-byte vectors, left padding of at most one voxel
+// input rows of whole 16-byte vectors, an even output width (every output
+// voxel of a row lies in a pooling window, or the row's last one does not),
+// left padding of at most one voxel
 // and index arithmetic in 24-bit products: n d h and n od oh below 2^24 (the
 // 128^3 stack at batch 8 has 2^17), every element offset below 2^31
 bool l1_supported(const ConvShape &s) {
@@ -504,7 +518,7 @@ bool l1_supported(const ConvShape &s) {
   const long long xel = ndh * s.w, mel = nodoh * s.ow * 16;
   return s.dtype == DT_BF16 && s.ci == 1 && s.co == 16 && s.sd == 1 && s.sh == 1 && s.sw == 1 && s.kd == s.kh &&
          s.kd == s.kw && (s.kd == 2 || s.kd == 3) && s.pw <= 1 && (s.kd == 3 || s.pw == 0) && s.w % 8 == 0 &&
-         s.ow % 8 == 0 && ndh < (1LL << 24) && nodoh < (1LL << 24) && s.w < (1 << 24) && s.ow < (1 << 24) &&
+         s.ow % 2 == 0 && ndh < (1LL << 24) && nodoh < (1LL << 24) && s.w < (1 << 24) && s.ow < (1 << 24) &&
          xel < (1LL << 31) && mel < (1LL << 31);
 }
 

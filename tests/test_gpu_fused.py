@@ -267,3 +267,39 @@ def test_fused_bwd_weight_dz(case, dt):
     ref = oracle.conv3d_bwd_data(dz_ref, to_np(w), dhw)
     e = maxabs_err(to_np(dx_u), ref)
     assert e <= TOL[dt], e
+
+
+# first layer, VALID padding: output widths that are even but not a multiple
+# of 8 (the mask rows then end inside a 16-byte group), and an odd one
+VALID_L1_CASES = [
+    (2, (12, 10, 48), 3),    # out (10, 8, 46)
+    (1, (9, 12, 128), 3),    # out (7, 10, 126): the paper's first-layer width
+    (1, (10, 10, 40), 2),    # out (9, 9, 39): odd width
+]
+
+
+@pytest.mark.parametrize("case", VALID_L1_CASES, ids=lambda c: "n%d_%dx%dx%d_k%d" % (c[0], *c[1], c[2]))
+def test_fused_bwd_weight_first_layer_valid(case):
+    N, dhw, k = case
+    desc = B.make_desc(N, dhw, 1, 16, k, 1, "valid", "bf16")
+    assert B.cf_conv3d_fused_supported(desc) & B.FUSED_BWD_WEIGHT
+    rng = np.random.default_rng(16)
+    od = B.cf_conv3d_out_shape(desc)
+    pdhw = tuple(t // 2 for t in od)
+    x = dev(rng.standard_normal((N, *dhw, 1)), "bf16")
+    g = dev(rng.standard_normal((N, *pdhw, 16)), "bf16")
+    nbits = N * od[0] * od[1] * od[2] * 16
+    mbytes = B.cf_conv3d_mask_bytes(desc)
+    mask_np = rng.integers(0, 256, mbytes, dtype=np.uint8)
+    mask = torch.as_tensor(mask_np, device="cuda")
+    dw = torch.full((k, k, k, 1, 16), float("nan"), dtype=torch.float32, device="cuda")
+    db = torch.full((16,), float("nan"), dtype=torch.float32, device="cuda")
+    ws = torch.empty(B.cf_conv3d_bwd_weight_fused_workspace_size(desc), dtype=torch.uint8, device="cuda")
+    B.cf_conv3d_bwd_weight_fused(desc, x, g, mask, 0.2, B.CF_FUSE_POOL2, dw, db, ws)
+    torch.cuda.synchronize()
+    bits = np.unpackbits(mask_np, bitorder="little")[:nbits].astype(bool).reshape((N, *od, 16))
+    dz = oracle.avgpool3d_bwd(to_np(g), od) * np.where(bits, 1.0, 0.2)
+    e = maxabs_err(to_np(dw), oracle.conv3d_bwd_weight(to_np(x), dz, k, pad="valid"))
+    assert e <= TOL["bf16"], e
+    e = maxabs_err(to_np(db), dz.reshape(-1, 16).sum(0))
+    assert e <= TOL["f32"], e
