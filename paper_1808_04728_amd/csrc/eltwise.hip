@@ -14,6 +14,7 @@
 
 #include "cf_common.h"
 #include "cf_kernels.h"
+#include "fastdiv.h"
 
 #include <algorithm>
 
@@ -45,6 +46,24 @@ __global__ __launch_bounds__(256) void bias_lrelu_fwd_kernel(const typename Stor
       y[i] = from_f32<DT>(lrelu(to_f32<DT>(z[i]) + bias[c0], alpha));
     }
   }
+}
+
+// 32-bit form of the vector forward pass (every element offset below 2^31):
+// the channel group of item i is i mod c/V by a launch-time divisor instead of
+// a 64-bit remainder
+template <int DT>
+__global__ __launch_bounds__(256) void bias_lrelu_fwd32_kernel(const typename Store<DT>::T *z,
+                                                               const float *__restrict__ bias, float alpha,
+                                                               typename Store<DT>::T *y, int nv, FastDiv fcg) {
+  constexpr int V = Store<DT>::VEC;
+  const int i = (int)blockIdx.x * 256 + threadIdx.x;
+  if (i >= nv) return;
+  const int c0 = (i - fdiv(i, fcg) * (int)fcg.div) * V;
+  Vec16<DT> v;
+  v.u = reinterpret_cast<const uint4 *>(z)[i];
+#pragma unroll
+  for (int j = 0; j < V; ++j) v.e[j] = from_f32<DT>(lrelu(to_f32<DT>(v.e[j]) + bias[c0 + j], alpha));
+  reinterpret_cast<uint4 *>(y)[i] = v.u;
 }
 
 // Thread layout of the backward kernel: CG channel groups of V channels,
@@ -133,6 +152,11 @@ hipError_t fwd_t(long long nvox, int c, const void *z, const float *bias, float 
   const long long nelem = nvox * c;
   const bool vec = c % Store<DT>::VEC == 0;
   const long long items = vec ? nelem / Store<DT>::VEC : nelem;
+  if (vec && nelem < (1LL << 31)) {
+    hipLaunchKernelGGL(bias_lrelu_fwd32_kernel<DT>, dim3((unsigned)((items + 255) / 256)), dim3(256), 0, st,
+                       (const T *)z, bias, alpha, (T *)y, (int)items, make_fastdiv(c / Store<DT>::VEC));
+    return hipGetLastError();
+  }
   const int blocks = (int)std::min<long long>((items + 255) / 256, 256LL * 64);
   if (vec)
     hipLaunchKernelGGL((bias_lrelu_fwd_kernel<DT, true>), dim3(blocks), dim3(256), 0, st,

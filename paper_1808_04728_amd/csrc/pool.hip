@@ -8,9 +8,13 @@
 //             vector loads, fp32 sum, one rounding on store;
 //   backward  one thread per (input voxel, channel group): dy = dp / k^3 of
 //             the covering window, or 0 outside every window (odd tails).
+// The backward pass decodes its items with launch-time divisors in 32-bit
+// arithmetic when every index fits (a 64-bit division per input item made it
+// ALU-bound); larger tensors take the 64-bit kernel.
 
 #include "cf_common.h"
 #include "cf_kernels.h"
+#include "fastdiv.h"
 
 #include <algorithm>
 
@@ -99,6 +103,30 @@ __global__ __launch_bounds__(256) void avgpool_bwd_kernel(const typename Store<D
   }
 }
 
+// 32-bit backward: fc = c / V and fw, fh, fd = the input extents; every element
+// offset is below 2^31.  (A 32-bit forward measured no faster than the kernel
+// above: its decode is per pooled voxel, eight times fewer items.)
+template <int DT>
+__global__ __launch_bounds__(256) void avgpool2_bwd32_kernel(const uint16_t *__restrict__ dp, uint16_t *__restrict__ dy,
+                                                             int c, int od, int oh, int ow, FastDiv fc, FastDiv fw,
+                                                             FastDiv fh, FastDiv fd, int items) {
+  const int i = (int)blockIdx.x * 256 + threadIdx.x;
+  if (i >= items) return;
+  const int t1 = fdiv(i, fc), t2 = fdiv(t1, fw), t3 = fdiv(t2, fh), n = fdiv(t3, fd);
+  const int cg = i - t1 * (int)fc.div, x_ = t1 - t2 * (int)fw.div, y_ = t2 - t3 * (int)fh.div;
+  const int z_ = t3 - n * (int)fd.div;
+  const int pz = z_ >> 1, py = y_ >> 1, px = x_ >> 1;
+  Vec16<DT_BF16> v;
+  if (pz < od && py < oh && px < ow) {
+    v.u = *reinterpret_cast<const uint4 *>(dp + (((n * od + pz) * oh + py) * ow + px) * c + 8 * cg);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v.e[j] = f2bf(bf2f(v.e[j]) * 0.125f);
+  } else {
+    v.u = make_uint4(0, 0, 0, 0);
+  }
+  *reinterpret_cast<uint4 *>(dy + 8 * i) = v.u;
+}
+
 template <int DT, bool BWD>
 hipError_t pool_t(int n, int d, int h, int w, int c, int k, const void *src, void *dst,
                   hipStream_t st) {
@@ -109,6 +137,16 @@ hipError_t pool_t(int n, int d, int h, int w, int c, int k, const void *src, voi
   const long long vox = BWD ? (long long)n * d * h * w : (long long)n * od * oh * ow;
   const long long items = vox * (c / V);
   if (items == 0) return hipSuccess;
+  // bf16 backward, 2^3 windows, whole 16-byte channel groups, offsets below 2^31
+  const long long elems = (long long)n * d * h * w * c;
+  if constexpr (DT == DT_BF16 && BWD) {
+    if (k == 2 && vec && elems < (1LL << 31)) {
+      hipLaunchKernelGGL(avgpool2_bwd32_kernel<DT>, dim3((int)((items + 255) / 256)), dim3(256), 0, st,
+                         (const uint16_t *)src, (uint16_t *)dst, c, od, oh, ow, make_fastdiv(c / 8),
+                         make_fastdiv(w), make_fastdiv(h), make_fastdiv(d), (int)items);
+      return hipGetLastError();
+    }
+  }
   const int blocks = (int)std::min<long long>((items + 255) / 256, 256LL * 64);
   if (BWD) {
     if (vec)

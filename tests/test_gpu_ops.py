@@ -122,7 +122,7 @@ def test_delta_kernel_identity_bitwise(dt, k):
 
 
 @pytest.mark.parametrize("dt", DTYPES)
-@pytest.mark.parametrize("c", [16, 3, 64])
+@pytest.mark.parametrize("c", [16, 3, 64, 24])
 def test_bias_lrelu(dt, c):
     rng = np.random.default_rng(5)
     shape = (2, 7, 6, 5, c)
@@ -180,7 +180,7 @@ def test_bias_lrelu_in_place_and_large(dt):
 
 
 @pytest.mark.parametrize("dt", DTYPES)
-@pytest.mark.parametrize("shape", [(2, 8, 6, 10, 16), (1, 7, 5, 9, 3), (1, 12, 12, 12, 64)])
+@pytest.mark.parametrize("shape", [(2, 8, 6, 10, 16), (1, 7, 5, 9, 3), (1, 12, 12, 12, 64), (2, 7, 5, 9, 24)])
 def test_avgpool(dt, shape):
     rng = np.random.default_rng(7)
     n, d, h, w, c = shape
