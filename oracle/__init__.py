@@ -33,7 +33,7 @@ def build(force: bool = True) -> str:
     if force or not os.path.exists(_LIB_PATH):
         tmp = _LIB_PATH + ".tmp%d" % os.getpid()
         cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp",
-               "-fno-fast-math", "-ffp-contract=off", _SRC, "-o", tmp]
+               "-fno-fast-math", "-ffp-contract=off", _SRC, "-o", tmp, "-lm"]
         subprocess.run(cmd, check=True)
         os.replace(tmp, _LIB_PATH)
     return _LIB_PATH
@@ -70,6 +70,11 @@ def _load():
             f = getattr(lib, name)
             f.argtypes = [P, P] + [I] * 7
             f.restype = None
+        I64 = ctypes.c_int64
+        lib.ref_lr_schedule.argtypes = [I64, I64, ctypes.c_double, ctypes.c_double]
+        lib.ref_lr_schedule.restype = ctypes.c_double
+        lib.ref_adam_larc_step.argtypes = [I, ctypes.POINTER(I64), I64, I64, P, P, P, P, P, P]
+        lib.ref_adam_larc_step.restype = None
         _lib = lib
         return lib
 
@@ -275,3 +280,37 @@ def stack_backward(acts, layers, weights, dout, alpha, skip_first_dgrad=True):
         grads[i] = dict(dy=dy, dz=dz, db=db, dw=dw, dx=dx)
         g = dx
     return grads
+
+
+# ----------------------------------------------------------------------
+# Parameter update (Section III-B): Adam + LARC + linear learning-rate decay
+
+#: the paper's hyperparameters (Section III-B); t_decay is not given there
+PAPER_HPARAMS = dict(eta0=2e-3, eta_min=1e-4, beta1=0.9, beta2=0.999, eps_hat=1e-8,
+                     larc_coef=0.002, larc_fallback=6.25e-5, larc_clip=1.0)
+
+
+def lr_schedule(t, t_decay, eta0=2e-3, eta_min=1e-4):
+    """Global learning rate of step t (linear decay, clamped after t_decay)."""
+    return _load().ref_lr_schedule(int(t), int(t_decay), float(eta0), float(eta_min))
+
+
+def adam_larc_step(offsets, t, t_decay, v, g, m, s, **hp):
+    """One update of every group; returns (v, m, s, eta_dagger) as new float64
+    arrays.  offsets has ngroups + 1 entries; group l is [offsets[l],
+    offsets[l+1]).  hp overrides PAPER_HPARAMS."""
+    h = dict(PAPER_HPARAMS)
+    h.update(hp)
+    off = np.ascontiguousarray(offsets, dtype=np.int64)
+    ng = len(off) - 1
+    v = _f64(v).copy()
+    g = _f64(g)
+    m = _f64(m).copy()
+    s = _f64(s).copy()
+    assert v.shape == g.shape == m.shape == s.shape and v.ndim == 1 and off[-1] <= v.size
+    hpa = np.array([h["eta0"], h["eta_min"], h["beta1"], h["beta2"], h["eps_hat"],
+                    h["larc_coef"], h["larc_fallback"], h["larc_clip"]], np.float64)
+    dag = np.zeros(max(ng, 1), np.float64)
+    _load().ref_adam_larc_step(ng, off.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), int(t), int(t_decay),
+                               _ptr(hpa), _ptr(v), _ptr(g), _ptr(m), _ptr(s), _ptr(dag))
+    return v, m, s, dag[:ng]

@@ -37,7 +37,11 @@
  *     exactly zero is taken as alpha (the saved output y is <= 0 there).
  *   - bias: not described by the paper; y = lrelu(z + b[c]) with a
  *     per-output-channel bias, db[c] = sum over voxels of dz.
+ *   - parameter update: Section III-B ("SGD Optimizer"): Adam on a gradient
+ *     rescaled per layer by LARC's clipped local rate, with a global rate on
+ *     a linear (power 1) decay.  See ref_adam_larc_step for the readings.
  */
+#include <math.h>
 #include <stddef.h>
 #include <stdint.h>
 
@@ -363,6 +367,79 @@ void ref_avgpool3d_bwd(const double *dp, double *dy, int N, int D, int H, int W,
         }
       }
       dy[IDX5(n, id, ih, iw, c, D, H, W, C)] = acc;
+    }
+  }
+}
+
+/* ---------------------------------------------------------------------- */
+/* Parameter update (Section III-B, "SGD Optimizer")                        */
+/* ---------------------------------------------------------------------- */
+
+/*
+ * Global learning rate of step t: linear decay from eta0 at t = 0 to eta_min
+ * at t = t_decay (the schedule equation of Section III-B, power 1).  The
+ * paper does not say what follows t_decay; the rate stays at eta_min (t is
+ * clamped), as in TensorFlow's non-cycling polynomial decay.
+ */
+double ref_lr_schedule(int64_t t, int64_t t_decay, double eta0, double eta_min) {
+  const double tc = (double)(t < t_decay ? t : t_decay);
+  return (eta0 - eta_min) * (1.0 - tc / (double)t_decay) + eta_min;
+}
+
+/*
+ * One update of every parameter group (Section III-B equations, in order):
+ *   1. eta_t = ref_lr_schedule(t)                            global rate
+ *   2. vn = ||v_l||_2, gn = ||g_l||_2                        per group l
+ *   3. eta*  = coef * vn / gn if vn != 0 and gn != 0, else fallback
+ *   4. eta+  = min(eta*, clip)                               clipped local rate
+ *   5. g*    = eta+ * g_l
+ *   6. v_l   = Adam(v_l, g*, eta_t)
+ * The paper's constants are coef = 0.002, fallback = 6.25e-5, clip = 1,
+ * beta1 = 0.9, beta2 = 0.999, eps_hat = 1e-8, eta0 = 2e-3, eta_min = 1e-4.
+ *
+ * Adam is Kingma and Ba's method in the form the paper's epsilon-hat names
+ * (their Section 2, the reformulation at its end; TensorFlow's Adam, which
+ * the paper trains with, implements this form): the moments are updated
+ *   m = beta1 m + (1 - beta1) g*,   s = beta2 s + (1 - beta2) g*^2,
+ * and the step is v -= a_k m / (sqrt(s) + eps_hat) with
+ *   a_k = eta_t sqrt(1 - beta2^k) / (1 - beta1^k),
+ * where k = t + 1 counts updates from 1 (Adam's bias corrections), while the
+ * decay counts them from t = 0 (the first update uses eta0).
+ *
+ * A group is one parameter tensor (a layer's weights, or its biases): the
+ * paper speaks of the parameters "in a layer" without saying whether a
+ * layer's weights and biases share one norm; the caller chooses by how it
+ * lays out the groups.  Group l holds elements [off[l], off[l+1]) of
+ * v, g, m, s.  hp = {eta0, eta_min, beta1, beta2, eps_hat, coef, fallback,
+ * clip}.  eta_dag (may be NULL) receives eta+ of every group.
+ */
+void ref_adam_larc_step(int ngroups, const int64_t *off, int64_t t, int64_t t_decay,
+                        const double *hp, double *v, const double *g, double *m,
+                        double *s, double *eta_dag) {
+  const double eta0 = hp[0], eta_min = hp[1], beta1 = hp[2], beta2 = hp[3];
+  const double eps_hat = hp[4], coef = hp[5], fallback = hp[6], clip = hp[7];
+  /* 1. */
+  const double eta_t = ref_lr_schedule(t, t_decay, eta0, eta_min);
+  const double k = (double)(t + 1);
+  const double a_k = eta_t * sqrt(1.0 - pow(beta2, k)) / (1.0 - pow(beta1, k));
+  for (int l = 0; l < ngroups; ++l) {
+    /* 2. */
+    double vv = 0.0, gg = 0.0;
+    for (int64_t i = off[l]; i < off[l + 1]; ++i) {
+      vv += v[i] * v[i];
+      gg += g[i] * g[i];
+    }
+    const double vn = sqrt(vv), gn = sqrt(gg);
+    /* 3. and 4. */
+    const double star = (vn != 0.0 && gn != 0.0) ? coef * vn / gn : fallback;
+    const double dag = star < clip ? star : clip;
+    if (eta_dag) eta_dag[l] = dag;
+    /* 5. and 6. */
+    for (int64_t i = off[l]; i < off[l + 1]; ++i) {
+      const double gs = dag * g[i];
+      m[i] = beta1 * m[i] + (1.0 - beta1) * gs;
+      s[i] = beta2 * s[i] + (1.0 - beta2) * gs * gs;
+      v[i] = v[i] - a_k * m[i] / (sqrt(s[i]) + eps_hat);
     }
   }
 }
