@@ -12,6 +12,10 @@ value = algorithmic conv FLOPs per step (fwd + wgrad + dgrad, padded taps
 included, layer-1 dgrad skipped) x steps / wall time of the timed steps.
 The roofline entry is for the op that takes the most time per step, timed
 with events on the launch stream over the same timed steps.
+
+The parameter update that follows each step in training (Adam + LARC +
+linear decay, Section III-B) is timed on its own after the timed steps and
+reported under "update"; --with-update also runs it inside every step.
 """
 from __future__ import annotations
 
@@ -108,6 +112,42 @@ def copy_probe(mib):
     print(json.dumps({"copy_probe_bytes": mib << 20, "copies": 5}), flush=True)
 
 
+def update_at_paper_size(step, B, np, torch, bf16):
+    """The update over as many parameters as the paper's network holds
+    (28.15 MB of fp32, Section IV: about 7.04 M) in 20 groups of seeded sizes
+    (its layer widths are not recoverable), queued behind a step; there the
+    pass is bound by HBM bandwidth, not latency."""
+    total = 7_037_500
+    r = np.random.default_rng(11)
+    w = r.uniform(0.2, 1.0, 20)
+    sizes = np.floor(w / w.sum() * total).astype(np.int64) // 4 * 4
+    off = [0] + np.cumsum(sizes).tolist()
+    n = off[-1]
+    v = torch.randn(n, device="cuda:0") * 0.05
+    g = torch.randn(n, device="cuda:0")
+    m = torch.zeros(n, device="cuda:0")
+    s = torch.zeros(n, device="cuda:0")
+    v16 = torch.empty(n, dtype=torch.bfloat16, device="cuda:0") if bf16 else None
+    ws = torch.empty(max(B.cf_adam_larc_workspace_size(off), 16), dtype=torch.uint8, device="cuda:0")
+    offc = B.adam_offsets(off)
+    hp = B.make_hparams(100000)
+    times = []
+    for rep in range(3):
+        step()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for t in range(10):
+            B.cf_adam_larc_step(offc, 10 * rep + t, hp, v, g, m, s, v16, ws)
+        e1.record()
+        times.append((e0, e1))
+    torch.cuda.synchronize()
+    ms = float(np.mean([a.elapsed_time(b) for a, b in times])) / 10
+    nbytes = n * (28 + (2 if bf16 else 0))
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    return dict(params=n, groups=20, launch_ms=round(ms, 4), algorithmic_bytes=nbytes, achieved=round(gbs, 1),
+                frac=round(gbs / HBM_PEAK_GBS, 4))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -116,6 +156,8 @@ def main():
     ap.add_argument("--workload", default="stack_128c_b8_bf16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--op-breakdown", action="store_true", help="print per-op times to stderr")
+    ap.add_argument("--with-update", action="store_true",
+                    help="apply the Adam + LARC parameter update inside every timed step")
     ap.add_argument("--unfused", action="store_true",
                     help="run every layer through the unfused entry points (conv, bias + lReLU, pool separately)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -133,6 +175,7 @@ def main():
         copy_probe(args.copy_probe)
         return
 
+    from paper_1808_04728_amd import binding as B
     from paper_1808_04728_amd import inputs
     from paper_1808_04728_amd.stack import ConvStack
 
@@ -146,9 +189,13 @@ def main():
     dout = torch.as_tensor(inputs.normal((wl["batch"],) + st.out_dhw + (wl["layers"][-1]["cout"],),
                                          30000 + wl["cfg"]), device="cuda:0").to(st.tdt)
 
+    hp = B.make_hparams(100000)  # the paper's constants; its decay length is not given
+
     def step():
         st.forward()
         st.backward(dout)
+        if args.with_update:
+            st.update(hp)
 
     for _ in range(args.warmup):
         step()
@@ -179,6 +226,27 @@ def main():
     dom_ms = float(np.mean([a.elapsed_time(b) for a, b in st.timer[dominant]]))
     st.timer = None
 
+    # the parameter update alone, after the timed steps (it changes the weights):
+    # K updates queued behind a step, so that the device never waits for the host
+    # to submit the next one, bracketed by events
+    ups = []
+    for _ in range(3):
+        step()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(10):
+            st.update(hp)
+        e1.record()
+        ups.append((e0, e1))
+    torch.cuda.synchronize()
+    upd_ms = float(np.mean([a.elapsed_time(b) for a, b in ups])) / 10
+    upd_bytes = st.update_bytes()
+    upd_gbs = upd_bytes / (upd_ms * 1e-3) / 1e9
+    update = dict(kernel="adam_norms + adam_update", params=st.param_offsets[-1], groups=len(st.param_offsets) - 1,
+                  launch_ms=round(upd_ms, 4), algorithmic_bytes=upd_bytes, achieved=round(upd_gbs, 1),
+                  unit="GB/s", peak=HBM_PEAK_GBS, frac=round(upd_gbs / HBM_PEAK_GBS, 4), in_step=args.with_update)
+    update["paper_network_size"] = update_at_paper_size(step, B, np, torch, wl["dtype"] == "bf16")
+
     ms = wall * 1e3 / args.steps
     flops = st.conv_flops()
     tflops = flops / (ms * 1e-3) / 1e12
@@ -208,13 +276,15 @@ def main():
         "vs_baseline": None,
         "dtype": wl["dtype"],
         "data": "synthetic",
-        "config": {"workload": describe(name, wl) + (", unfused entry points" if args.unfused else ""),
+        "config": {"workload": describe(name, wl) + (", unfused entry points" if args.unfused else "")
+                   + (", Adam + LARC update in every step" if args.with_update else ""),
                    "name": name, "edge": wl["size"], "batch": wl["batch"],
                    "input_channels": wl["c0"], "conv_gflop_per_step": round(flops / 1e9, 3)},
         "samples_per_s": round(wl["batch"] / (ms * 1e-3), 2),
         "mfma_peak_frac": round(tflops / peak, 4),
         "roofline": roof,
         "op_ms": {k: round(v, 4) for k, v in sorted(op_ms.items(), key=lambda kv: -kv[1])},
+        "update": update,
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(name)

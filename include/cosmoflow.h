@@ -279,6 +279,63 @@ cf_status cf_conv3d_bwd_weight_fused_deferred(const cf_conv3d_desc *desc, const 
                                               void *ws, size_t ws_bytes, cf_reduction *pending,
                                               int32_t *npending, void *stream);
 
+/* ------------------------------------------------------------------------
+ * Parameter update (Section III-B, "SGD Optimizer").  Per parameter group l
+ * (a contiguous range of flat fp32 arrays) at step t:
+ *   eta_t  = (eta0 - eta_min) * (1 - min(t, t_decay) / t_decay) + eta_min
+ *   vn     = ||v_l||_2,  gn = ||g_l||_2
+ *   eta*   = coef * vn / gn if vn != 0 and gn != 0, else fallback
+ *   eta+   = min(eta*, clip)
+ *   g*     = eta+ * g_l
+ *   m      = beta1 m + (1 - beta1) g*,  s = beta2 s + (1 - beta2) g*^2
+ *   v_l   -= eta_t sqrt(1 - beta2^(t+1)) / (1 - beta1^(t+1)) * m / (sqrt(s) + eps_hat)
+ * i.e. Adam (Kingma and Ba, in the epsilon-hat form the paper's constant
+ * names) on the gradient rescaled by LARC's clipped local rate, with the
+ * global rate on a power-1 polynomial decay.  The paper's values: eta0 =
+ * 2e-3, eta_min = 1e-4, beta1 = 0.9, beta2 = 0.999, eps_hat = 1e-8, coef =
+ * 0.002, fallback = 6.25e-5, clip = 1; t_decay is not given there.
+ * t counts the updates already applied (0 for the first): the decay starts
+ * from eta0, Adam's bias corrections count from 1.  The clamp of t at
+ * t_decay is a reading (the paper leaves the rate after t_decay open).
+ * ------------------------------------------------------------------------ */
+typedef struct cf_adam_larc_hparams {
+  double eta0, eta_min; /* global rate at t = 0 and from t = t_decay on */
+  int64_t t_decay;      /* length of the linear decay, > 0 */
+  double beta1, beta2;  /* Adam's moment decays, in [0, 1) */
+  double eps_hat;       /* >= 0 */
+  double larc_coef;     /* eta* = coef * ||v|| / ||g|| */
+  double larc_fallback; /* eta* when either norm is zero */
+  double larc_clip;     /* eta+ = min(eta*, clip) */
+} cf_adam_larc_hparams;
+
+/* Most parameter groups one call takes. */
+#define CF_ADAM_MAX_GROUPS 128
+
+/* Bytes of device workspace cf_adam_larc_step needs for these groups (16
+ * per chunk; 0 when every group is empty or the arguments are invalid).
+ * offsets: host array of ngroups + 1 element offsets, as below. */
+size_t cf_adam_larc_workspace_size(int32_t ngroups, const int64_t *offsets);
+
+/* One update of every group.  offsets (HOST memory, ngroups + 1 entries,
+ * non-decreasing): group l is elements [offsets[l], offsets[l+1]) of the
+ * flat fp32 device arrays v (parameters, updated in place), g (gradient,
+ * read only), m and s (Adam's first and second moments, updated in place;
+ * zero before the first update).  Every group start offsets[l], l <
+ * ngroups, must be a multiple of 4 (CF_ERR_ALIGNMENT); group lengths are
+ * free.  v16: NULL, or a bf16 device array that receives RNE(v) after the
+ * update at the same offsets (the copy the convolutions of a bf16 step
+ * read).  ws: device workspace of cf_adam_larc_workspace_size() bytes; its
+ * contents need no initialisation.  All device pointers 16-byte aligned;
+ * v, g, m, s, v16 and ws must not overlap (CF_ERR_ALIAS).  Elements outside
+ * the groups are not touched.  The norms are summed in fp64 in a fixed
+ * order and the update is evaluated in fp64 with one rounding per fp32
+ * store: results are deterministic.  More than CF_ADAM_MAX_GROUPS groups:
+ * CF_ERR_UNSUPPORTED.  Invalid hyperparameters (non-finite values, beta
+ * outside [0, 1), eps_hat < 0, t < 0, t_decay <= 0): CF_ERR_INVALID_ARG. */
+cf_status cf_adam_larc_step(int32_t ngroups, const int64_t *offsets, int64_t t,
+                            const cf_adam_larc_hparams *hp, float *v, const float *g, float *m,
+                            float *s, void *v16, void *ws, size_t ws_bytes, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -35,7 +35,7 @@ EXPORTS = [
     "cf_conv3d_fused_supported", "cf_conv3d_mask_bytes", "cf_conv3d_fwd_fused",
     "cf_conv3d_bwd_weight_fused_workspace_size", "cf_conv3d_bwd_weight_fused", "cf_conv3d_bwd_weight_fused_dz",
     "cf_conv3d_bwd_data_fused", "cf_reduce_partials", "cf_conv3d_bwd_weight_deferred", "cf_bias_lrelu_bwd_deferred",
-    "cf_conv3d_bwd_weight_fused_deferred",
+    "cf_conv3d_bwd_weight_fused_deferred", "cf_adam_larc_workspace_size", "cf_adam_larc_step",
 ]
 
 
@@ -56,6 +56,25 @@ class cf_reduction(ctypes.Structure):
 
 
 CF_MAX_PENDING = 4
+
+
+class cf_adam_larc_hparams(ctypes.Structure):
+    _fields_ = [("eta0", ctypes.c_double), ("eta_min", ctypes.c_double), ("t_decay", ctypes.c_int64),
+                ("beta1", ctypes.c_double), ("beta2", ctypes.c_double), ("eps_hat", ctypes.c_double),
+                ("larc_coef", ctypes.c_double), ("larc_fallback", ctypes.c_double), ("larc_clip", ctypes.c_double)]
+
+
+CF_ADAM_MAX_GROUPS = 128
+#: the paper's hyperparameters (Section III-B); t_decay is the caller's choice
+PAPER_HPARAMS = dict(eta0=2e-3, eta_min=1e-4, beta1=0.9, beta2=0.999, eps_hat=1e-8,
+                     larc_coef=0.002, larc_fallback=6.25e-5, larc_clip=1.0)
+
+
+def make_hparams(t_decay, **kw) -> cf_adam_larc_hparams:
+    h = dict(PAPER_HPARAMS)
+    h.update(kw)
+    return cf_adam_larc_hparams(h["eta0"], h["eta_min"], int(t_decay), h["beta1"], h["beta2"], h["eps_hat"],
+                                h["larc_coef"], h["larc_fallback"], h["larc_clip"])
 
 
 _lib = None
@@ -101,6 +120,9 @@ def lib():
         "cf_conv3d_bwd_weight_fused_deferred": ([D, vp, vp, vp, f32, ctypes.c_uint32, vp, vp, vp, vp, sz,
                                                  ctypes.POINTER(cf_reduction), ctypes.POINTER(i32), vp],
                                                 ctypes.c_int),
+        "cf_adam_larc_workspace_size": ([i32, ctypes.POINTER(i64)], sz),
+        "cf_adam_larc_step": ([i32, ctypes.POINTER(i64), i64, ctypes.POINTER(cf_adam_larc_hparams), vp, vp, vp, vp,
+                               vp, vp, sz, vp], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         f = getattr(L, name)
@@ -286,3 +308,30 @@ def cf_conv3d_bwd_weight_fused_deferred(desc, x, g, mask, alpha, flags, dw, db, 
                                                      _ptr(dw), _ptr(db), _ptr(dz), _ptr(ws), ws_bytes, arr,
                                                      ctypes.byref(n), _stream(stream)))
     return _pending_list(arr, n)
+
+
+def _offsets(offsets):
+    """(ngroups, ctypes int64 array); an already built pair passes through."""
+    if isinstance(offsets, tuple) and len(offsets) == 2 and isinstance(offsets[1], ctypes.Array):
+        return offsets
+    arr = (ctypes.c_int64 * max(len(offsets), 1))(*[int(o) for o in offsets])
+    return len(offsets) - 1, arr
+
+
+def adam_offsets(offsets):
+    """Pre-marshalled offsets for repeated cf_adam_larc_step calls."""
+    return _offsets(offsets)
+
+
+def cf_adam_larc_workspace_size(offsets) -> int:
+    n, arr = _offsets(offsets)
+    return lib().cf_adam_larc_workspace_size(n, arr)
+
+
+def cf_adam_larc_step(offsets, t, hp, v, g, m, s, v16, ws, ws_bytes=None, stream=None):
+    """offsets: ngroups + 1 host integers; hp: a cf_adam_larc_hparams (see make_hparams)."""
+    if ws_bytes is None:
+        ws_bytes = 0 if ws is None or isinstance(ws, int) else ws.numel() * ws.element_size()
+    n, arr = _offsets(offsets)
+    _check(lib().cf_adam_larc_step(n, arr, int(t), ctypes.byref(hp), _ptr(v), _ptr(g), _ptr(m), _ptr(s), _ptr(v16),
+                                   _ptr(ws), ws_bytes, _stream(stream)))

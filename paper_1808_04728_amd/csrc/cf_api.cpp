@@ -141,6 +141,25 @@ cf_status deferred(cf_reduction *pending, int32_t *npending, F call) {
 }
 }  // namespace
 
+namespace {
+// validates the group table and fills the kernel's plan; chunks = 0 when every group is empty
+cf_status adam_plan(int32_t ngroups, const int64_t *offsets, cf::OptGroups *G, int *chunks) {
+  if (ngroups < 0) return fail(CF_ERR_INVALID_ARG, "adam_larc: ngroups must be >= 0");
+  if (ngroups > CF_ADAM_MAX_GROUPS) return fail(CF_ERR_UNSUPPORTED, "adam_larc: more than CF_ADAM_MAX_GROUPS groups");
+  if (!offsets) return fail(CF_ERR_INVALID_ARG, "adam_larc: offsets is NULL");
+  if (offsets[0] < 0) return fail(CF_ERR_INVALID_ARG, "adam_larc: negative offset");
+  for (int l = 0; l < ngroups; ++l) {
+    if (offsets[l + 1] < offsets[l]) return fail(CF_ERR_INVALID_ARG, "adam_larc: offsets must be non-decreasing");
+    if (offsets[l] % 4 != 0) return fail(CF_ERR_ALIGNMENT, "adam_larc: a group start is not a multiple of 4");
+  }
+  if (offsets[ngroups] >= (1LL << 40)) return fail(CF_ERR_INVALID_ARG, "adam_larc: too many elements");
+  static_assert(cf::kOptMaxGroups == CF_ADAM_MAX_GROUPS, "group table size");
+  std::vector<long long> off(offsets, offsets + ngroups + 1);
+  *chunks = cf::plan_opt_groups(ngroups, off.data(), G);
+  return CF_OK;
+}
+}  // namespace
+
 extern "C" {
 
 const char *cf_version(void) { return "cosmoflow-gfx950 0.1.0"; }
@@ -545,6 +564,56 @@ cf_status cf_conv3d_bwd_weight_fused_deferred(const cf_conv3d_desc *desc, const 
     return bwd_weight_fused(dz ? "cf_conv3d_bwd_weight_fused_dz" : "cf_conv3d_bwd_weight_fused", desc, x, g, mask,
                             alpha, flags, dw, db, dz, ws, ws_bytes, stream);
   });
+}
+
+
+size_t cf_adam_larc_workspace_size(int32_t ngroups, const int64_t *offsets) {
+  std::string keep = g_last_error;
+  cf::OptGroups G;
+  int chunks = 0;
+  if (adam_plan(ngroups, offsets, &G, &chunks) != CF_OK) {
+    g_last_error = keep;
+    return 0;
+  }
+  return (size_t)chunks * 2 * sizeof(double);
+}
+
+cf_status cf_adam_larc_step(int32_t ngroups, const int64_t *offsets, int64_t t, const cf_adam_larc_hparams *hp,
+                            float *v, const float *g, float *m, float *s, void *v16, void *ws, size_t ws_bytes,
+                            void *stream) {
+  cf::OptGroups G;
+  int chunks = 0;
+  cf_status r = adam_plan(ngroups, offsets, &G, &chunks);
+  if (r != CF_OK) return r;
+  if (!hp) return fail(CF_ERR_INVALID_ARG, "adam_larc: hp is NULL");
+  if (t < 0) return fail(CF_ERR_INVALID_ARG, "adam_larc: t must be >= 0");
+  if (hp->t_decay <= 0) return fail(CF_ERR_INVALID_ARG, "adam_larc: t_decay must be > 0");
+  const double vals[] = {hp->eta0, hp->eta_min, hp->beta1, hp->beta2, hp->eps_hat,
+                         hp->larc_coef, hp->larc_fallback, hp->larc_clip};
+  for (double x : vals)
+    if (!std::isfinite(x)) return fail(CF_ERR_INVALID_ARG, "adam_larc: hyperparameters must be finite");
+  if (hp->beta1 < 0.0 || hp->beta1 >= 1.0 || hp->beta2 < 0.0 || hp->beta2 >= 1.0)
+    return fail(CF_ERR_INVALID_ARG, "adam_larc: beta1 and beta2 must lie in [0, 1)");
+  if (hp->eps_hat < 0.0) return fail(CF_ERR_INVALID_ARG, "adam_larc: eps_hat must be >= 0");
+  if (chunks == 0) return ok();
+  if ((r = check_ptrs({v, g, m, s})) != CF_OK) return r;
+  if (v16 && !aligned16(v16)) return fail(CF_ERR_ALIGNMENT, "adam_larc: v16 not 16-byte aligned");
+  const size_t need = (size_t)chunks * 2 * sizeof(double);
+  if (!ws || ws_bytes < need)
+    return fail(CF_ERR_WORKSPACE, "adam_larc: workspace smaller than cf_adam_larc_workspace_size()");
+  if (!aligned16(ws)) return fail(CF_ERR_ALIGNMENT, "workspace not 16-byte aligned");
+  const size_t nb = (size_t)offsets[ngroups] * 4;
+  const void *bufs[] = {v, g, m, s, v16, ws};
+  const size_t lens[] = {nb, nb, nb, nb, nb / 2, need};
+  for (int a = 0; a < 6; ++a)
+    for (int b = a + 1; b < 6; ++b)
+      if (overlap(bufs[a], lens[a], bufs[b], lens[b]))
+        return fail(CF_ERR_ALIAS, "adam_larc: v, g, m, s, v16 and the workspace must not overlap");
+  cf::OptHparams h{hp->eta0,  hp->eta_min,   hp->t_decay,       hp->beta1,    hp->beta2,
+                   hp->eps_hat, hp->larc_coef, hp->larc_fallback, hp->larc_clip};
+  hipStream_t st = (hipStream_t)stream;
+  return finish(cf::launch_adam_larc(G, chunks, h, (long long)t, v, g, m, s, (uint16_t *)v16, (double *)ws, st),
+                st, "cf_adam_larc_step");
 }
 
 }  // extern "C"

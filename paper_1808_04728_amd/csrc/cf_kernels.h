@@ -120,4 +120,24 @@ hipError_t launch_avgpool_fwd(int n, int d, int h, int w, int c, int k, int dtyp
 hipError_t launch_avgpool_bwd(int n, int d, int h, int w, int c, int k, int dtype,
                               const void *dp, void *dy, hipStream_t st);
 
+// Parameter update (optim.hip): Adam + LARC + linear learning-rate decay over
+// parameter groups of flat fp32 arrays.  Passed by value as a kernel argument.
+constexpr int kOptMaxGroups = 128;
+struct OptGroups {
+  int n;                             // groups
+  int chunk0[kOptMaxGroups + 1];     // first chunk of each group; chunk0[n] = all chunks
+  int shift[kOptMaxGroups];          // a chunk of group l holds 1024 << shift[l] elements
+  long long off[kOptMaxGroups + 1];  // element offsets; group l is [off[l], off[l+1])
+};
+struct OptHparams {
+  double eta0, eta_min;
+  long long t_decay;
+  double beta1, beta2, eps_hat, coef, fallback, clip;
+};
+// fills G from n + 1 offsets (off[l] % 4 == 0 for l < n), returns the chunk count
+int plan_opt_groups(int n, const long long *off, OptGroups *G);
+// part: 2 doubles per chunk (caller workspace); v16 may be null
+hipError_t launch_adam_larc(const OptGroups &G, int chunks, const OptHparams &hp, long long t, float *v,
+                            const float *g, float *m, float *s, uint16_t *v16, double *part, hipStream_t st);
+
 }  // namespace cf

@@ -11,6 +11,13 @@ backward pass over the network's convolution part, Section III-A):
 PyTorch only allocates device memory and supplies the stream; every step is
 one call of ``binding`` (a HIP kernel).  Buffers are allocated once, so a
 step launches kernels and nothing else.
+
+Parameters live in flat buffers, one parameter group per tensor (layer l's
+weights, then its biases): fp32 master values ``flat_param`` (the weights of
+an fp32 stack and every bias are views of it), the bf16 copy ``flat_w16``
+the convolutions of a bf16 stack read, and the gradient ``flat_grad`` that
+the backward pass writes.  ``update`` applies the paper's Adam + LARC rule
+(Section III-B) to all groups in one call.
 """
 from __future__ import annotations
 
@@ -57,8 +64,45 @@ class ConvStack:
         self._alloc()
 
     # ------------------------------------------------------------------
+    def _alloc_params(self):
+        """Flat parameter / gradient buffers; every group starts on a multiple
+        of 16 elements (64 bytes), padding (zeros) belongs to the group before."""
+        dev = self.device
+        off, shapes = [0], []
+        for l in self.L:
+            s = l["spec"]
+            for shape in (((s["k"],) * 3 + (s["cin"], s["cout"])), (s["cout"],)):
+                n = 1
+                for t in shape:
+                    n *= t
+                shapes.append(shape)
+                off.append(off[-1] + (n + 15) // 16 * 16)
+        self.param_offsets = off
+        total = off[-1]
+        self.flat_param = torch.zeros(total, dtype=torch.float32, device=dev)
+        self.flat_grad = torch.zeros(total, dtype=torch.float32, device=dev)
+        self.flat_w16 = torch.zeros(total, dtype=torch.bfloat16, device=dev) if self.dtype == "bf16" else None
+        wsrc = self.flat_w16 if self.flat_w16 is not None else self.flat_param
+
+        def view(buf, g):
+            shape = shapes[g]
+            n = 1
+            for t in shape:
+                n *= t
+            return buf[off[g]:off[g] + n].view(shape)
+
+        for i, l in enumerate(self.L):
+            l["w"] = view(wsrc, 2 * i)
+            l["w32"] = view(self.flat_param, 2 * i)
+            l["b"] = view(self.flat_param, 2 * i + 1)
+            l["dw"] = view(self.flat_grad, 2 * i)
+            l["db"] = view(self.flat_grad, 2 * i + 1)
+        self.opt_m = self.opt_s = self.opt_ws = None
+        self.opt_t = 0
+
     def _alloc(self):
         dev, tdt, n = self.device, self.tdt, self.batch
+        self._alloc_params()
         for i, l in enumerate(self.L):
             s = l["spec"]
             needs_dgrad = i > 0 or not self.skip_first_dgrad
@@ -68,12 +112,8 @@ class ConvStack:
             l["fused"] = bool(self.fused and (sup & both) == both and (not needs_dgrad or sup & B.FUSED_BWD_DATA))
             # otherwise conv + bias + leaky ReLU may still share one kernel (y written once)
             l["fused_act"] = bool(self.fused and not l["fused"] and B.cf_conv3d_fused_supported(l["desc"], 0) & 1)
-            l["w"] = torch.zeros((s["k"],) * 3 + (s["cin"], s["cout"]), dtype=tdt, device=dev)
-            l["b"] = torch.zeros(s["cout"], dtype=torch.float32, device=dev)
             l["p"] = torch.empty((n,) + l["pool_dhw"] + (s["cout"],), dtype=tdt, device=dev) if s["pool"] else None
             l["gout"] = torch.empty((n,) + l["pool_dhw"] + (s["cout"],), dtype=tdt, device=dev)
-            l["dw"] = torch.empty(l["w"].shape, dtype=torch.float32, device=dev)
-            l["db"] = torch.empty(s["cout"], dtype=torch.float32, device=dev)
             l["dx"] = None
             if l["fused"]:
                 l["z"] = l["dy"] = l["dz"] = None
@@ -102,9 +142,41 @@ class ConvStack:
         self.x = torch.empty((n,) + self.L[0]["in_dhw"] + (self.L[0]["spec"]["cin"],), dtype=tdt, device=dev)
 
     def set_params(self, weights, biases):
+        """Weights are rounded to the stack's dtype; the fp32 master copy holds
+        exactly those values.  Resets the optimizer state."""
         for l, w, b in zip(self.L, weights, biases):
             l["w"].copy_(torch.as_tensor(w).to(self.tdt))
+            if l["w32"].data_ptr() != l["w"].data_ptr():
+                l["w32"].copy_(l["w"].float())
             l["b"].copy_(torch.as_tensor(b).float())
+        self.reset_optimizer()
+
+    def reset_optimizer(self):
+        self.opt_t = 0
+        if self.opt_m is not None:
+            self.opt_m.zero_()
+            self.opt_s.zero_()
+
+    def update(self, hp, stream=None):
+        """One parameter update from the gradient of the last backward pass
+        (Adam + LARC + linear decay, one group per tensor); hp is a
+        binding.cf_adam_larc_hparams.  Writes the master values and, for a
+        bf16 stack, the bf16 weights the next forward pass reads."""
+        if self.opt_m is None:
+            self.opt_m = torch.zeros_like(self.flat_param)
+            self.opt_s = torch.zeros_like(self.flat_param)
+            nws = B.cf_adam_larc_workspace_size(self.param_offsets)
+            self.opt_ws = torch.empty(max(nws, 16), dtype=torch.uint8, device=self.device)
+            self._opt_off = B.adam_offsets(self.param_offsets)
+        self._call("L0.adam_larc_update", B.cf_adam_larc_step, self._opt_off, self.opt_t, hp, self.flat_param,
+                   self.flat_grad, self.opt_m, self.opt_s, self.flat_w16, self.opt_ws, None, stream)
+        self.opt_t += 1
+
+    def update_bytes(self):
+        """Algorithmic HBM bytes of one update: v, g, m, s read, v, m, s (and
+        the bf16 copy) written."""
+        n = self.param_offsets[-1]
+        return n * (7 * 4 + (2 if self.flat_w16 is not None else 0))
 
     def set_input(self, x):
         self.x.copy_(torch.as_tensor(x).to(self.tdt))
@@ -239,6 +311,8 @@ class ConvStack:
         """Algorithmic HBM bytes of one call (every tensor read once, written once)."""
         if name.endswith(".reduce_partials"):
             return self.reduce_bytes
+        if name.endswith(".adam_larc_update"):
+            return self.update_bytes()
         i = int(name[1:name.index(".")]) - 1
         l = self.L[i]
         s = l["spec"]

@@ -133,3 +133,39 @@ def test_reduce_partials_validation(L):
     with pytest.raises(B.CfError) as e:
         B.cf_reduce_partials([B.cf_reduction(1024, 1024 + 16, 4, 8)], 0)  # out inside its partials
     assert e.value.status == B.CF_ERR_ALIAS
+
+
+def test_adam_larc_workspace_and_validation(L):
+    off = [0, 4096, 4096, 4100, 4103]  # groups of 4096, 0, 4 and 3 elements
+    # 4 + 0 + 1 + 1 chunks (of 1024 elements), 16 bytes each
+    assert B.cf_adam_larc_workspace_size(off) == 6 * 16
+    # at most 256 chunks per group: 2^20 + 1 elements take chunks of 8192, 129 of them
+    assert B.cf_adam_larc_workspace_size([0, (1 << 20) + 1]) == 129 * 16
+    assert B.cf_adam_larc_workspace_size([0, 1 << 18]) == 256 * 16
+    assert B.cf_adam_larc_workspace_size([0, 0, 0]) == 0
+    assert B.cf_adam_larc_workspace_size([8, 4]) == 0  # invalid: decreasing
+    hp = B.make_hparams(1000)
+    ws, nws = A + 0x400000, B.cf_adam_larc_workspace_size(off)
+    v, g, m, s = A, A + 0x10000, A + 0x20000, A + 0x30000
+    B.cf_adam_larc_step([0, 0, 0], 0, hp, None, None, None, None, None, None, 0, 0)  # empty: no GPU call
+    B.cf_adam_larc_step([0], 0, hp, None, None, None, None, None, None, 0, 0)  # no groups
+    expect(B.CF_ERR_INVALID_ARG, B.cf_adam_larc_step, [], 0, hp, v, g, m, s, None, ws, nws, 0)
+    expect(B.CF_ERR_ALIGNMENT, B.cf_adam_larc_step, [0, 6, 12], 0, hp, v, g, m, s, None, ws, nws, 0)
+    expect(B.CF_ERR_INVALID_ARG, B.cf_adam_larc_step, [8, 4], 0, hp, v, g, m, s, None, ws, nws, 0)
+    expect(B.CF_ERR_INVALID_ARG, B.cf_adam_larc_step, [-4, 4], 0, hp, v, g, m, s, None, ws, nws, 0)
+    expect(B.CF_ERR_UNSUPPORTED, B.cf_adam_larc_step, [4 * i for i in range(130)], 0, hp, v, g, m, s, None,
+           ws, nws, 0)
+    expect(B.CF_ERR_INVALID_ARG, B.cf_adam_larc_step, off, -1, hp, v, g, m, s, None, ws, nws, 0)
+    for bad in (dict(t_decay=0), dict(beta1=1.0), dict(beta2=-0.1), dict(eps_hat=-1e-8), dict(eta0=math.nan),
+                dict(larc_coef=math.inf)):
+        h = B.make_hparams(bad.pop("t_decay", 1000), **bad)
+        expect(B.CF_ERR_INVALID_ARG, B.cf_adam_larc_step, off, 0, h, v, g, m, s, None, ws, nws, 0)
+    expect(B.CF_ERR_WORKSPACE, B.cf_adam_larc_step, off, 0, hp, v, g, m, s, None, ws, nws - 16, 0)
+    expect(B.CF_ERR_WORKSPACE, B.cf_adam_larc_step, off, 0, hp, v, g, m, s, None, None, 0, 0)
+    expect(B.CF_ERR_INVALID_ARG, B.cf_adam_larc_step, off, 0, hp, v, None, m, s, None, ws, nws, 0)
+    expect(B.CF_ERR_ALIGNMENT, B.cf_adam_larc_step, off, 0, hp, v, g, m + 4, s, None, ws, nws, 0)
+    expect(B.CF_ERR_ALIGNMENT, B.cf_adam_larc_step, off, 0, hp, v, g, m, s, A + 0x50008, ws, nws, 0)
+    # 4103 floats span 16412 bytes: m at v + 16400 overlaps v
+    expect(B.CF_ERR_ALIAS, B.cf_adam_larc_step, off, 0, hp, v, g, v + 16400, s, None, ws, nws, 0)
+    expect(B.CF_ERR_ALIAS, B.cf_adam_larc_step, off, 0, hp, v, g, m, s, None, s + 16, nws, 0)
+    expect(B.CF_ERR_ALIAS, B.cf_adam_larc_step, off, 0, hp, v, g, m, s, g + 16, ws, nws, 0)
