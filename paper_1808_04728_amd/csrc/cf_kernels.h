@@ -62,6 +62,11 @@ hipError_t launch_conv_fwd_smallc(const ConvShape &s, const void *x, const void 
                                   float alpha, void *out, uint16_t *mask, bool fused, hipStream_t st);
 bool smallc_wgrad_fused_supported(const ConvShape &s);
 size_t smallc_wgrad_fused_workspace(const ConvShape &s);
+// the same layer unfused (dz given), bf16, one input channel, 16 outputs: partials in ws
+bool smallc_wgrad_dz_supported(const ConvShape &s);
+size_t smallc_wgrad_dz_workspace(const ConvShape &s);
+hipError_t launch_smallc_wgrad_dz(const ConvShape &s, const void *x, const void *dz, float *dw, void *ws,
+                                  hipStream_t st);
 hipError_t launch_smallc_wgrad_fused(const ConvShape &s, const void *x, const void *dp, const uint16_t *mask,
                                      float alpha, float *dw, float *db, void *ws, hipStream_t st);
 

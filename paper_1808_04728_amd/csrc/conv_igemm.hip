@@ -653,7 +653,15 @@ static bool use_direct_wgrad(const ConvShape &s) {
   return direct_wgrad_supported(s);
 }
 
+// the single-channel first layer (bf16): CF_WGRAD_KERNEL=igemm forces the generic kernel
+static bool use_l1_wgrad(const ConvShape &s) {
+  const char *e = getenv("CF_WGRAD_KERNEL");
+  if (e && !strcmp(e, "igemm")) return false;
+  return smallc_wgrad_dz_supported(s);
+}
+
 size_t conv_bwd_weight_workspace(const ConvShape &s) {
+  if (use_l1_wgrad(s)) return smallc_wgrad_dz_workspace(s);
   if (c16_wgrad_supported(s)) return c16_wgrad_workspace(s);
   if (use_direct_wgrad(s)) return direct_wgrad_workspace(s);
   WgradPlan pl = plan_wgrad(s);
@@ -662,6 +670,7 @@ size_t conv_bwd_weight_workspace(const ConvShape &s) {
 
 hipError_t launch_conv_bwd_weight(const ConvShape &s, const void *x, const void *dz, float *dw,
                                   void *ws, hipStream_t st) {
+  if (use_l1_wgrad(s)) return launch_smallc_wgrad_dz(s, x, dz, dw, ws, st);
   if (c16_wgrad_supported(s))
     return launch_conv_bwd_weight_c16(s, x, dz, nullptr, 0.f, dw, nullptr, ws, false, nullptr, st);
   if (use_direct_wgrad(s)) return launch_conv_bwd_weight_direct(s, x, dz, dw, ws, st);

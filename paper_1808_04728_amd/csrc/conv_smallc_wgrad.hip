@@ -284,6 +284,53 @@ typedef short v4i16_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4i16_t lds_v4i16_t;
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));  // a plain 16-byte vector
 
+// Input halo of one tile for the single-channel kernels: item (row a, b;
+// 16-byte output vector i) needs the vectors i .. i+2 of the aligned window
+// [ow0 - 8, ow0 + 40) of its input row (zeros outside the input).
+template <int KE>
+__device__ __forceinline__ void l1_load_x(const uint16_t *__restrict__ x, const SmallcParams &p, int tid, int n,
+                                          int od0, int oh0, int ow0, u32x4_t (&xv)[3]) {
+  constexpr int HD = TD + KE - 1, HH = TH + KE - 1;
+  const int xa = tid / (HH * 4), xb = (tid / 4) % HH, xi = tid & 3;
+#pragma unroll
+  for (int j = 0; j < 3; ++j) xv[j] = u32x4_t{0u, 0u, 0u, 0u};
+  if (tid < HD * HH * 4) {
+    const int id = od0 - p.pd + xa, ih = oh0 - p.ph + xb;
+    if ((unsigned)id < (unsigned)p.d && (unsigned)ih < (unsigned)p.h) {
+      // 24-bit products: n d h, n od oh and the element counts are below 2^24 / 2^31
+      const int rowoff = (int)__umul24(__umul24(n * p.d + id, p.h) + ih, p.w);
+#pragma unroll
+      for (int j = 0; j < 3; ++j) {
+        const int iw = ow0 - 8 + 8 * (xi + j);
+        if (iw >= 0 && iw < p.w) xv[j] = *reinterpret_cast<const u32x4_t *>(x + rowoff + iw);
+      }
+    }
+  }
+}
+
+// ... and its KE shifted copies in LDS: copy kw, element i of a row = window
+// element 8 - PW + kw + i (16-byte rows of 8 voxels, XP slots per row).
+template <int KE, int PW, int XP>
+__device__ __forceinline__ void l1_store_x(uint4 *xs, int tid, const u32x4_t (&xv)[3]) {
+  constexpr int HD = TD + KE - 1, HH = TH + KE - 1;
+  const int xa = tid / (HH * 4), xb = (tid / 4) % HH, xi = tid & 3;
+  if (tid < HD * HH * 4) {
+    const uint32_t dw[12] = {xv[0][0], xv[0][1], xv[0][2], xv[0][3], xv[1][0], xv[1][1],
+                             xv[1][2], xv[1][3], xv[2][0], xv[2][1], xv[2][2], xv[2][3]};
+#pragma unroll
+    for (int kw = 0; kw < KE; ++kw) {
+      const int s0 = 8 - PW + kw;
+      uint32_t o[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int L = (s0 >> 1) + k;
+        o[k] = (s0 & 1) ? __builtin_amdgcn_alignbyte(dw[L + 1], dw[L], 2) : dw[L];
+      }
+      xs[((kw * HD + xa) * HH + xb) * XP + xi] = make_uint4(o[0], o[1], o[2], o[3]);
+    }
+  }
+}
+
 template <int KE, int PW>
 __global__ __launch_bounds__(256) void l1_wgrad_kernel(const uint16_t *__restrict__ x,
                                                        const uint16_t *__restrict__ dp,
@@ -337,7 +384,6 @@ __global__ __launch_bounds__(256) void l1_wgrad_kernel(const uint16_t *__restric
   // Tile pipeline: the global loads of tile it+1 (into registers) are issued
   // right after tile it's data reached LDS, so their latency overlaps tile
   // it's MFMAs; LDS is single-buffered (written only between two barriers).
-  const int xa = tid / (HH * 4), xb = (tid / 4) % HH, xi = tid & 3;
   u32x4_t xv[3], dv, mv;
   int cur_n = 0, cur_od0 = 0, cur_oh0 = 0, cur_ow0 = 0;
   auto tile_origin = [&](int it, int &n, int &od0, int &oh0, int &ow0) -> bool {
@@ -352,22 +398,7 @@ __global__ __launch_bounds__(256) void l1_wgrad_kernel(const uint16_t *__restric
     return true;
   };
   auto load_tile = [&](int n, int od0, int oh0, int ow0) {
-    // input: item (row a,b; output vector i) needs window vectors i .. i+2 of
-    // the aligned window [ow0 - 8, ow0 + 40) of its row
-#pragma unroll
-    for (int j = 0; j < 3; ++j) xv[j] = u32x4_t{0u, 0u, 0u, 0u};
-    if (tid < NXI) {
-      const int id = od0 - p.pd + xa, ih = oh0 - p.ph + xb;
-      if ((unsigned)id < (unsigned)p.d && (unsigned)ih < (unsigned)p.h) {
-        // 24-bit products: n d h, n od oh and the element counts are below 2^24 / 2^31
-        const int rowoff = (int)__umul24(__umul24(n * p.d + id, p.h) + ih, p.w);
-#pragma unroll
-        for (int j = 0; j < 3; ++j) {
-          const int iw = ow0 - 8 + 8 * (xi + j);
-          if (iw >= 0 && iw < p.w) xv[j] = *reinterpret_cast<const u32x4_t *>(x + rowoff + iw);
-        }
-      }
-    }
+    l1_load_x<KE>(x, p, tid, n, od0, oh0, ow0, xv);
     // pooled gradient: pooled voxel (pd0 + tid>>7, ph0 + (tid>>5)&3, pw0 + (tid>>1)&15), 8 channels
     dv = u32x4_t{0u, 0u, 0u, 0u};
     {
@@ -402,22 +433,7 @@ __global__ __launch_bounds__(256) void l1_wgrad_kernel(const uint16_t *__restric
   if (have) load_tile(cur_n, cur_od0, cur_oh0, cur_ow0);
   for (int it = 0; have; ++it) {
     // ---- LDS: shifted input copies, the pooled-gradient tile, the mask tile
-    if (tid < NXI) {
-      const uint32_t dw[12] = {xv[0][0], xv[0][1], xv[0][2], xv[0][3], xv[1][0], xv[1][1],
-                               xv[1][2], xv[1][3], xv[2][0], xv[2][1], xv[2][2], xv[2][3]};
-#pragma unroll
-      for (int kw = 0; kw < KE; ++kw) {
-        // copy kw, element i of a row = window element 8 - PW + kw + i
-        const int s0 = 8 - PW + kw;
-        uint32_t o[4];
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          const int L = (s0 >> 1) + k;
-          o[k] = (s0 & 1) ? __builtin_amdgcn_alignbyte(dw[L + 1], dw[L], 2) : dw[L];
-        }
-        xs[((kw * HD + xa) * HH + xb) * XP + xi] = make_uint4(o[0], o[1], o[2], o[3]);
-      }
-    }
+    l1_store_x<KE, PW, XP>(xs, tid, xv);
     dps[tid] = make_uint4(dv[0], dv[1], dv[2], dv[3]);
     if (tid < 128) mks[tid] = make_uint4(mv[0], mv[1], mv[2], mv[3]);
     __syncthreads();
@@ -477,6 +493,135 @@ __global__ __launch_bounds__(256) void l1_wgrad_kernel(const uint16_t *__restric
   }
 }
 
+// ---------------------------------------------------------------------------
+// The same single-channel bf16 layer without the fused epilogue (the plain
+// backward-weights call): dz comes from HBM.  A tile's dz (32 w-rows x 32
+// voxels x 16 channels, 32 KiB) is staged in LDS voxel-major, the 16
+// channels of a voxel in 32 bytes, with 128 bytes of padding after every 8
+// voxels.  Lane (r, q)'s B fragment of a w-row (channel r of voxels
+// 8q .. 8q+7) is two transposing reads of four voxels each; with the padding
+// the 128-byte windows of the four 16-lane groups alternate between the two
+// halves of the 64 banks.  The A side (input halo, shifted copies) and the
+// tile pipeline are those of the fused kernel above.
+// ---------------------------------------------------------------------------
+template <int KE, int PW>
+__global__ __launch_bounds__(256) void l1_wgrad_dz_kernel(const uint16_t *__restrict__ x,
+                                                          const uint16_t *__restrict__ dz,
+                                                          float *__restrict__ part_w, SmallcParams p) {
+  constexpr int HD = TD + KE - 1, HH = TH + KE - 1;
+  constexpr int M = KE * KE * KE;
+  constexpr int MF = 2;
+  static_assert(M <= 16 * MF, "rows");
+  constexpr int PLANE = HD * HH;
+  constexpr int XROWS = (KE + 1) * PLANE;  // KE shifted copies, a plane of zeros (A rows >= M)
+  static_assert(PLANE * 4 <= 256, "one staging item per thread");
+  constexpr int XP = 5;
+  constexpr int ROWB = 32 * 32 + 4 * 128;  // bytes of one staged w-row of dz
+  constexpr int NDZ = TD * TH * 32 * 2 / 256;  // 16-byte dz vectors per thread and tile
+  __shared__ __attribute__((aligned(16))) uint4 xs[XROWS * XP];
+  __shared__ __attribute__((aligned(16))) unsigned char dzs[TD * TH * ROWB];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int r = lane & 15, q = lane >> 4;
+  const int tiles_w = (p.ow + TW - 1) / TW, tiles_h = (p.oh + TH - 1) / TH, tiles_d = (p.od + TD - 1) / TD;
+  const int tiles_per_n = tiles_w * tiles_h * tiles_d;
+  const int total_tiles = p.n * tiles_per_n;  // the launcher keeps every index below 2^24
+
+  for (int e = tid; e < PLANE * XP; e += 256) xs[KE * PLANE * XP + e] = make_uint4(0, 0, 0, 0);
+  int arow[MF];
+#pragma unroll
+  for (int mf = 0; mf < MF; ++mf) {
+    const int t = 16 * mf + r;
+    if (t < M) {
+      const int kd = t / (KE * KE), kh = (t / KE) % KE, kw = t % KE;
+      arow[mf] = (kw * HD + kd) * HH + kh;
+    } else {
+      arow[mf] = KE * PLANE;
+    }
+  }
+  // B reads: voxel 8q + r/4 (its pad is 128 q bytes), channels 4 (r%4) .. 4 (r%4) + 3
+  const int boff = (8 * q + (r >> 2)) * 32 + 128 * q + 8 * (r & 3);
+  // dz staging: vector j of this thread is w-row 4j + tid/64, voxel (tid%64)/2, channel half tid%2
+  const int sw = (tid & 63) >> 1, sc = tid & 1;
+  const int soff = sw * 32 + (sw >> 3) * 128 + 16 * sc;
+
+  f32x4_t acc[MF];
+#pragma unroll
+  for (int mf = 0; mf < MF; ++mf) acc[mf] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  u32x4_t xv[3], dv[NDZ];
+  auto tile_origin = [&](int it, int &n, int &od0, int &oh0, int &ow0) -> bool {
+    const int gt = (int)blockIdx.x * p.tiles_per_block + it;
+    if (it >= p.tiles_per_block || gt >= total_tiles) return false;
+    int t = gt % tiles_per_n;
+    n = gt / tiles_per_n;
+    const int tw = t % tiles_w; t /= tiles_w;
+    const int th = t % tiles_h;
+    const int td = t / tiles_h;
+    od0 = td * TD; oh0 = th * TH; ow0 = tw * TW;
+    return true;
+  };
+  auto load_tile = [&](int n, int od0, int oh0, int ow0) {
+    l1_load_x<KE>(x, p, tid, n, od0, oh0, ow0, xv);
+    const int vw = ow0 + sw;
+#pragma unroll
+    for (int j = 0; j < NDZ; ++j) {
+      const int row = 4 * j + (tid >> 6);
+      const int vd = od0 + row / TH, vh = oh0 + row % TH;
+      dv[j] = u32x4_t{0u, 0u, 0u, 0u};
+      if (vd < p.od && vh < p.oh && vw < p.ow)
+        dv[j] = *reinterpret_cast<const u32x4_t *>(
+            dz + ((int)__umul24(__umul24(n * p.od + vd, p.oh) + vh, p.ow) + vw) * 16 + 8 * sc);
+    }
+  };
+
+  int n0 = 0, d0 = 0, h0 = 0, w0 = 0;
+  bool have = tile_origin(0, n0, d0, h0, w0);
+  if (have) load_tile(n0, d0, h0, w0);
+  for (int it = 0; have; ++it) {
+    l1_store_x<KE, PW, XP>(xs, tid, xv);
+#pragma unroll
+    for (int j = 0; j < NDZ; ++j)
+      *reinterpret_cast<uint4 *>(dzs + (4 * j + (tid >> 6)) * ROWB + soff) =
+          make_uint4(dv[j][0], dv[j][1], dv[j][2], dv[j][3]);
+    __syncthreads();
+    int nn = 0, nd0 = 0, nh0 = 0, nw0 = 0;
+    have = tile_origin(it + 1, nn, nd0, nh0, nw0);
+    if (have) load_tile(nn, nd0, nh0, nw0);
+
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int row = wave + 4 * k;
+      const int ld = row / TH, lh = row % TH;
+      const unsigned char *rb = dzs + row * ROWB + boff;
+      const v4i16_t g0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t *)rb);
+      const v4i16_t g1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t *)(rb + 128));
+      const bf16x8_t b = __builtin_bit_cast(
+          bf16x8_t, make_uint4((uint32_t)(uint16_t)g0[0] | ((uint32_t)(uint16_t)g0[1] << 16),
+                               (uint32_t)(uint16_t)g0[2] | ((uint32_t)(uint16_t)g0[3] << 16),
+                               (uint32_t)(uint16_t)g1[0] | ((uint32_t)(uint16_t)g1[1] << 16),
+                               (uint32_t)(uint16_t)g1[2] | ((uint32_t)(uint16_t)g1[3] << 16)));
+#pragma unroll
+      for (int mf = 0; mf < MF; ++mf) {
+        const bf16x8_t a = __builtin_bit_cast(bf16x8_t, xs[(arow[mf] + ld * HH + lh) * XP + q]);
+        acc[mf] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc[mf], 0, 0, 0);
+      }
+    }
+    __syncthreads();
+  }
+
+  // ---- combine the four waves; write the partials -------------------------
+  float *red = reinterpret_cast<float *>(dzs);  // [wave][32 rows][16 channels]
+#pragma unroll
+  for (int mf = 0; mf < MF; ++mf)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) red[(wave * 32 + 16 * mf + 4 * q + j) * 16 + r] = acc[mf][j];
+  __syncthreads();
+  for (int i = tid; i < M * 16; i += 256)
+    part_w[(long long)blockIdx.x * M * 16 + i] = red[i] + red[512 + i] + red[1024 + i] + red[1536 + i];
+}
+
 struct WPlan {
   int tpb;
   int blocks;
@@ -522,7 +667,54 @@ bool l1_supported(const ConvShape &s) {
          xel < (1LL << 31) && mel < (1LL << 31);
 }
 
+// the unfused kernel: as l1_supported, with any output width and the dz
+// element count (16 per output voxel) below 2^31
+bool l1_dz_supported(const ConvShape &s) {
+  const long long ndh = (long long)s.n * s.d * s.h, nodoh = (long long)s.n * s.od * s.oh;
+  const long long xel = ndh * s.w, zel = nodoh * s.ow * 16;
+  return s.dtype == DT_BF16 && s.ci == 1 && s.co == 16 && s.sd == 1 && s.sh == 1 && s.sw == 1 && s.kd == s.kh &&
+         s.kd == s.kw && (s.kd == 2 || s.kd == 3) && s.pw <= 1 && (s.kd == 3 || s.pw == 0) && s.w % 8 == 0 &&
+         ndh < (1LL << 24) && nodoh < (1LL << 24) && s.w < (1 << 24) && s.ow < (1 << 24) && xel < (1LL << 31) &&
+         zel < (1LL << 31);
+}
+
+SmallcParams params(const ConvShape &s, const WPlan &w) {
+  SmallcParams p{};
+  p.n = s.n; p.d = s.d; p.h = s.h; p.w = s.w; p.ci = s.ci; p.co = s.co;
+  p.kd = s.kd; p.kh = s.kh; p.kw = s.kw; p.pd = s.pd; p.ph = s.ph; p.pw = s.pw;
+  p.od = s.od; p.oh = s.oh; p.ow = s.ow;
+  p.pod = s.od / 2; p.poh = s.oh / 2; p.pow_ = s.ow / 2;
+  p.tiles_per_block = w.tpb;
+  return p;
+}
+
 }  // namespace
+
+bool smallc_wgrad_dz_supported(const ConvShape &s) { return l1_dz_supported(s); }
+
+size_t smallc_wgrad_dz_workspace(const ConvShape &s) {
+  const WPlan w = plan(s);
+  return (size_t)w.blocks * s.kd * s.kh * s.kw * s.co * sizeof(float);
+}
+
+hipError_t launch_smallc_wgrad_dz(const ConvShape &s, const void *x, const void *dz, float *dw, void *ws,
+                                  hipStream_t st) {
+  const WPlan w = plan(s);
+  const SmallcParams p = params(s, w);
+  float *pw = (float *)ws;
+  if (s.kd == 2)
+    hipLaunchKernelGGL((l1_wgrad_dz_kernel<2, 0>), dim3(w.blocks), dim3(256), 0, st, (const uint16_t *)x,
+                       (const uint16_t *)dz, pw, p);
+  else if (s.pw == 0)
+    hipLaunchKernelGGL((l1_wgrad_dz_kernel<3, 0>), dim3(w.blocks), dim3(256), 0, st, (const uint16_t *)x,
+                       (const uint16_t *)dz, pw, p);
+  else
+    hipLaunchKernelGGL((l1_wgrad_dz_kernel<3, 1>), dim3(w.blocks), dim3(256), 0, st, (const uint16_t *)x,
+                       (const uint16_t *)dz, pw, p);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_sum_rows(pw, dw, w.blocks, s.kd * s.kh * s.kw * s.co, st);
+}
 
 bool smallc_wgrad_fused_supported(const ConvShape &s) {
   if (s.sd != 1 || s.sh != 1 || s.sw != 1) return false;
@@ -541,12 +733,7 @@ size_t smallc_wgrad_fused_workspace(const ConvShape &s) {
 hipError_t launch_smallc_wgrad_fused(const ConvShape &s, const void *x, const void *dp, const uint16_t *mask,
                                      float alpha, float *dw, float *db, void *ws, hipStream_t st) {
   WPlan w = plan(s);
-  SmallcParams p{};
-  p.n = s.n; p.d = s.d; p.h = s.h; p.w = s.w; p.ci = s.ci; p.co = s.co;
-  p.kd = s.kd; p.kh = s.kh; p.kw = s.kw; p.pd = s.pd; p.ph = s.ph; p.pw = s.pw;
-  p.od = s.od; p.oh = s.oh; p.ow = s.ow;
-  p.pod = s.od / 2; p.poh = s.oh / 2; p.pow_ = s.ow / 2;
-  p.tiles_per_block = w.tpb;
+  const SmallcParams p = params(s, w);
   const int M = s.kd * s.kh * s.kw * s.ci;
   if (l1_supported(s)) {
     float *pw = (float *)ws;

@@ -104,6 +104,41 @@ def test_conv_bwd_weight(case, dt):
     assert torch.equal(dw, dw2)
 
 
+# the single-input-channel bf16 first layer: N, (D,H,W), k, pad (output widths
+# 48 with a left pad, 126, 40 and 39, several tiles per row and ragged rows)
+L1_WGRAD_CASES = [
+    (2, (12, 10, 48), 3, "same"),
+    (1, (9, 12, 128), 3, "valid"),
+    (1, (10, 10, 40), 2, "same"),
+    (1, (10, 10, 40), 2, "valid"),
+    (3, (5, 17, 24), 3, "same"),
+]
+
+
+@pytest.mark.parametrize("case", L1_WGRAD_CASES, ids=lambda c: "n%d_%dx%dx%d_k%d_%s" % (c[0], *c[1], *c[2:]))
+def test_conv_bwd_weight_first_layer(case, monkeypatch):
+    """The unfused first-layer kernel (dz from HBM) against the oracle and
+    against the generic kernel (CF_WGRAD_KERNEL=igemm)."""
+    N, dhw, k, pad = case
+    rng = np.random.default_rng(17)
+    desc = B.make_desc(N, dhw, 1, 16, k, 1, pad, "bf16")
+    od = B.cf_conv3d_out_shape(desc)
+    x = dev(rng.standard_normal((N, *dhw, 1)), "bf16")
+    dz = dev(rng.standard_normal((N, *od, 16)), "bf16")
+    ref = oracle.conv3d_bwd_weight(to_np(x), to_np(dz), k, pad=pad)
+    out = []
+    for kern in ("", "igemm"):
+        monkeypatch.setenv("CF_WGRAD_KERNEL", kern)
+        dw = torch.full((k, k, k, 1, 16), float("nan"), dtype=torch.float32, device="cuda")
+        ws = torch.empty(max(16, B.cf_conv3d_bwd_weight_workspace_size(desc)), dtype=torch.uint8, device="cuda")
+        B.cf_conv3d_bwd_weight(desc, x, dz, dw, ws)
+        torch.cuda.synchronize()
+        e = maxabs_err(to_np(dw), ref)
+        assert e <= 1e-4, (kern, e)
+        out.append(to_np(dw))
+    assert maxabs_err(out[0], out[1]) <= 1e-4
+
+
 @pytest.mark.parametrize("dt", DTYPES)
 @pytest.mark.parametrize("k", [1, 2, 3, 4])
 def test_delta_kernel_identity_bitwise(dt, k):
