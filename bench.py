@@ -16,6 +16,8 @@ with events on the launch stream over the same timed steps.
 The parameter update that follows each step in training (Adam + LARC +
 linear decay, Section III-B) is timed on its own after the timed steps and
 reported under "update"; --with-update also runs it inside every step.
+"hbm_passes" times the unfused elementwise and pooling kernels alone at the
+first layer's activation shape.
 """
 from __future__ import annotations
 
@@ -148,6 +150,55 @@ def update_at_paper_size(step, B, np, torch, bf16):
                 frac=round(gbs / HBM_PEAK_GBS, 4))
 
 
+def hbm_passes(B, np, torch, wl):
+    """The unfused elementwise and pooling passes (bias + leaky ReLU forward and
+    backward, 2^3 average pool forward and backward) at the first layer's
+    activation shape of the workload, each timed alone: 10 launches back to
+    back on resident tensors, HIP events around them.  Inside the unfused step
+    the same kernels also absorb the write-back of the previous kernel's
+    output, so their in-sequence times (--unfused --op-breakdown) are longer."""
+    dt = wl["dtype"]
+    tdt = torch.bfloat16 if dt == "bf16" else torch.float32
+    n, s, c = wl["batch"], wl["size"], wl["layers"][0]["cout"]
+    nvox = n * s ** 3
+    dev = "cuda:0"
+    g = torch.Generator(device=dev)
+    g.manual_seed(5)
+    z = torch.randn((n, s, s, s, c), generator=g, device=dev).to(tdt)
+    y = torch.empty_like(z)
+    dy = torch.randn((n, s, s, s, c), generator=g, device=dev).to(tdt)
+    dz = torch.empty_like(z)
+    dp = torch.randn((n, s // 2, s // 2, s // 2, c), generator=g, device=dev).to(tdt)
+    pool = torch.empty_like(dp)
+    dy2 = torch.empty_like(z)
+    bias = torch.zeros(c, device=dev)
+    db = torch.empty(c, device=dev)
+    ws = torch.empty(max(B.cf_bias_lrelu_bwd_workspace_size(nvox, c), 16), dtype=torch.uint8, device=dev)
+    zb = z.numel() * z.element_size()
+    pb = pool.numel() * pool.element_size()
+    ops = {
+        "bias_lrelu_fwd": (lambda: B.cf_bias_lrelu_fwd(nvox, c, dt, z, bias, 0.01, y), 2 * zb),
+        "bias_lrelu_bwd": (lambda: B.cf_bias_lrelu_bwd(nvox, c, dt, dy, y, 0.01, dz, db, ws), 3 * zb),
+        "avgpool_fwd": (lambda: B.cf_avgpool3d_fwd(n, s, s, s, c, 2, 2, dt, y, pool), zb + pb),
+        "avgpool_bwd": (lambda: B.cf_avgpool3d_bwd(n, s, s, s, c, 2, 2, dt, dp, dy2), zb + pb),
+    }
+    out = {}
+    for name, (fn, nbytes) in ops.items():
+        for _ in range(2):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(10):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / 10
+        gbs = nbytes / (us * 1e-6) / 1e9
+        out[name] = dict(us=round(us, 1), algorithmic_bytes=nbytes, achieved=round(gbs, 1),
+                         frac=round(gbs / HBM_PEAK_GBS, 4))
+    return dict(shape=[n, s, s, s, c], dtype=dt, unit="GB/s", peak=HBM_PEAK_GBS, passes=out)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -246,6 +297,7 @@ def main():
                   launch_ms=round(upd_ms, 4), algorithmic_bytes=upd_bytes, achieved=round(upd_gbs, 1),
                   unit="GB/s", peak=HBM_PEAK_GBS, frac=round(upd_gbs / HBM_PEAK_GBS, 4), in_step=args.with_update)
     update["paper_network_size"] = update_at_paper_size(step, B, np, torch, wl["dtype"] == "bf16")
+    passes = hbm_passes(B, np, torch, wl)
 
     ms = wall * 1e3 / args.steps
     flops = st.conv_flops()
@@ -285,6 +337,7 @@ def main():
         "roofline": roof,
         "op_ms": {k: round(v, 4) for k, v in sorted(op_ms.items(), key=lambda kv: -kv[1])},
         "update": update,
+        "hbm_passes": passes,
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(name)

@@ -8,9 +8,9 @@
 //             vector loads, fp32 sum, one rounding on store;
 //   backward  one thread per (input voxel, channel group): dy = dp / k^3 of
 //             the covering window, or 0 outside every window (odd tails).
-// The backward pass decodes its items with launch-time divisors in 32-bit
-// arithmetic when every index fits (a 64-bit division per input item made it
-// ALU-bound); larger tensors take the 64-bit kernel.
+// 2^3 windows over whole 16-byte channel vectors take the vector kernels
+// below (32-bit indices with launch-time divisors: a 64-bit division per
+// item made the passes ALU-bound); anything else the general kernels.
 
 #include "cf_common.h"
 #include "cf_kernels.h"
@@ -103,28 +103,73 @@ __global__ __launch_bounds__(256) void avgpool_bwd_kernel(const typename Store<D
   }
 }
 
-// 32-bit backward: fc = c / V and fw, fh, fd = the input extents; every element
-// offset is below 2^31.  (A 32-bit forward measured no faster than the kernel
-// above: its decode is per pooled voxel, eight times fewer items.)
+// 2^3 windows with whole 16-byte vectors and every offset below 2^31 (the
+// bf16 and fp32 fast paths).  Forward: one thread per (pooled voxel, vector),
+// its eight loads issued together.  Backward: one thread per (batch, pooled
+// plane, pooled row, vector of an input row): it loads the covering pooled
+// vector once and stores it, scaled by 1/8, into the four input rows of the
+// window, so every store instruction of a wave writes a contiguous 1 KiB;
+// the planes, rows and columns that no window covers (odd extents) get
+// zeros.  Items are decoded with launch-time divisors.
 template <int DT>
-__global__ __launch_bounds__(256) void avgpool2_bwd32_kernel(const uint16_t *__restrict__ dp, uint16_t *__restrict__ dy,
-                                                             int c, int od, int oh, int ow, FastDiv fc, FastDiv fw,
-                                                             FastDiv fh, FastDiv fd, int items) {
+__global__ __launch_bounds__(256) void avgpool2_fwd_vec_kernel(const typename Store<DT>::T *__restrict__ y,
+                                                               typename Store<DT>::T *__restrict__ p, int d, int h,
+                                                               int w, int c, FastDiv fcg, FastDiv fow, FastDiv foh,
+                                                               FastDiv fod, int items) {
+  constexpr int V = Store<DT>::VEC;
   const int i = (int)blockIdx.x * 256 + threadIdx.x;
   if (i >= items) return;
-  const int t1 = fdiv(i, fc), t2 = fdiv(t1, fw), t3 = fdiv(t2, fh), n = fdiv(t3, fd);
-  const int cg = i - t1 * (int)fc.div, x_ = t1 - t2 * (int)fw.div, y_ = t2 - t3 * (int)fh.div;
-  const int z_ = t3 - n * (int)fd.div;
-  const int pz = z_ >> 1, py = y_ >> 1, px = x_ >> 1;
-  Vec16<DT_BF16> v;
-  if (pz < od && py < oh && px < ow) {
-    v.u = *reinterpret_cast<const uint4 *>(dp + (((n * od + pz) * oh + py) * ow + px) * c + 8 * cg);
+  const int t1 = fdiv(i, fcg), t2 = fdiv(t1, fow), t3 = fdiv(t2, foh), n = fdiv(t3, fod);
+  const int cg = i - t1 * (int)fcg.div, x_ = t1 - t2 * (int)fow.div, y_ = t2 - t3 * (int)foh.div;
+  const int z_ = t3 - n * (int)fod.div;
+  const int base = (((n * d + 2 * z_) * h + 2 * y_) * w + 2 * x_) * c + V * cg;
+  Vec16<DT> v[8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) v.e[j] = f2bf(bf2f(v.e[j]) * 0.125f);
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int e = 0; e < 2; ++e)
+        v[4 * a + 2 * b + e].u = *reinterpret_cast<const uint4 *>(y + base + ((a * h + b) * w + e) * c);
+  float sum[V];
+#pragma unroll
+  for (int j = 0; j < V; ++j) sum[j] = 0.f;
+#pragma unroll
+  for (int u = 0; u < 8; ++u)
+#pragma unroll
+    for (int j = 0; j < V; ++j) sum[j] += to_f32<DT>(v[u].e[j]);
+  Vec16<DT> o;
+#pragma unroll
+  for (int j = 0; j < V; ++j) o.e[j] = from_f32<DT>(sum[j] * 0.125f);
+  *reinterpret_cast<uint4 *>(p + V * i) = o.u;  // output is dense NDHWC in item order
+}
+
+template <int DT>
+__global__ __launch_bounds__(256) void avgpool2_bwd_vec_kernel(const typename Store<DT>::T *__restrict__ dp,
+                                                               typename Store<DT>::T *__restrict__ dy, int d, int h,
+                                                               int w, int c, int od, int oh, int ow, FastDiv frow,
+                                                               FastDiv fhc, FastDiv fdc, FastDiv fcg, int items) {
+  constexpr int V = Store<DT>::VEC;
+  const int i = (int)blockIdx.x * 256 + threadIdx.x;
+  if (i >= items) return;
+  // frow = vectors per input row, fhc / fdc = pooled rows / planes including an uncovered last one
+  const int t = fdiv(i, frow), t2 = fdiv(t, fhc), n = fdiv(t2, fdc);
+  const int j = i - t * (int)frow.div, py = t - t2 * (int)fhc.div, pz = t2 - n * (int)fdc.div;
+  const int xv = fdiv(j, fcg), cg = j - xv * (int)fcg.div, px = xv >> 1;
+  Vec16<DT> v;
+  if (pz < od && py < oh && px < ow) {
+    v.u = *reinterpret_cast<const uint4 *>(dp + (((n * od + pz) * oh + py) * ow + px) * c + V * cg);
+#pragma unroll
+    for (int k = 0; k < V; ++k) v.e[k] = from_f32<DT>(to_f32<DT>(v.e[k]) * 0.125f);
   } else {
     v.u = make_uint4(0, 0, 0, 0);
   }
-  *reinterpret_cast<uint4 *>(dy + 8 * i) = v.u;
+  const int base = ((n * d + 2 * pz) * h + 2 * py) * w * c + V * j;
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+      if (2 * pz + a < d && 2 * py + b < h) *reinterpret_cast<uint4 *>(dy + base + (a * h + b) * w * c) = v.u;
 }
 
 template <int DT, bool BWD>
@@ -137,15 +182,22 @@ hipError_t pool_t(int n, int d, int h, int w, int c, int k, const void *src, voi
   const long long vox = BWD ? (long long)n * d * h * w : (long long)n * od * oh * ow;
   const long long items = vox * (c / V);
   if (items == 0) return hipSuccess;
-  // bf16 backward, 2^3 windows, whole 16-byte channel groups, offsets below 2^31
+  // 2^3 windows, whole 16-byte vectors, offsets below 2^31: the vector kernels
   const long long elems = (long long)n * d * h * w * c;
-  if constexpr (DT == DT_BF16 && BWD) {
-    if (k == 2 && vec && elems < (1LL << 31)) {
-      hipLaunchKernelGGL(avgpool2_bwd32_kernel<DT>, dim3((int)((items + 255) / 256)), dim3(256), 0, st,
-                         (const uint16_t *)src, (uint16_t *)dst, c, od, oh, ow, make_fastdiv(c / 8),
-                         make_fastdiv(w), make_fastdiv(h), make_fastdiv(d), (int)items);
-      return hipGetLastError();
+  if (k == 2 && vec && elems < (1LL << 31)) {
+    const int cgn = c / V;
+    if (BWD) {
+      const int dc = (d + 1) / 2, hc = (h + 1) / 2;
+      const long long its = (long long)n * dc * hc * w * cgn;
+      hipLaunchKernelGGL(avgpool2_bwd_vec_kernel<DT>, dim3((int)((its + 255) / 256)), dim3(256), 0, st,
+                         (const T *)src, (T *)dst, d, h, w, c, od, oh, ow, make_fastdiv(w * cgn), make_fastdiv(hc),
+                         make_fastdiv(dc), make_fastdiv(cgn), (int)its);
+    } else {
+      hipLaunchKernelGGL(avgpool2_fwd_vec_kernel<DT>, dim3((int)((items + 255) / 256)), dim3(256), 0, st,
+                         (const T *)src, (T *)dst, d, h, w, c, make_fastdiv(cgn), make_fastdiv(ow), make_fastdiv(oh),
+                         make_fastdiv(od), (int)items);
     }
+    return hipGetLastError();
   }
   const int blocks = (int)std::min<long long>((items + 255) / 256, 256LL * 64);
   if (BWD) {

@@ -215,7 +215,8 @@ def test_bias_lrelu_in_place_and_large(dt):
 
 
 @pytest.mark.parametrize("dt", DTYPES)
-@pytest.mark.parametrize("shape", [(2, 8, 6, 10, 16), (1, 7, 5, 9, 3), (1, 12, 12, 12, 64), (2, 7, 5, 9, 24)])
+@pytest.mark.parametrize("shape", [(2, 8, 6, 10, 16), (1, 7, 5, 9, 3), (1, 12, 12, 12, 64), (2, 7, 5, 9, 24),
+                                   (3, 6, 7, 8, 16), (1, 9, 8, 6, 32)])
 def test_avgpool(dt, shape):
     rng = np.random.default_rng(7)
     n, d, h, w, c = shape
