@@ -47,4 +47,29 @@ template <int DT> union Vec16 {
   typename Store<DT>::T e[Store<DT>::VEC];
 };
 
+// 16-byte global load / store; NT = non-temporal (streaming) access for
+// tensors read or written once and larger than the last-level cache, so they
+// do not displace lines that other data still needs.
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+template <bool NT> __device__ __forceinline__ uint4 ld16(const void *p) {
+  if constexpr (NT) {
+    const u32x4_t a = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p));
+    return make_uint4(a.x, a.y, a.z, a.w);
+  } else {
+    return *reinterpret_cast<const uint4 *>(p);
+  }
+}
+template <bool NT> __device__ __forceinline__ void st16(void *p, uint4 v) {
+  if constexpr (NT) {
+    const u32x4_t a = {v.x, v.y, v.z, v.w};
+    __builtin_nontemporal_store(a, reinterpret_cast<u32x4_t *>(p));
+  } else {
+    *reinterpret_cast<uint4 *>(p) = v;
+  }
+}
+
+// tensors of at least this many bytes take the non-temporal forms in the
+// streaming elementwise and pooling passes (the last-level cache is 256 MiB)
+constexpr long long kStreamBytes = 1LL << 28;
+
 }  // namespace cf

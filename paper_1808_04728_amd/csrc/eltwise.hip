@@ -51,7 +51,7 @@ __global__ __launch_bounds__(256) void bias_lrelu_fwd_kernel(const typename Stor
 // 32-bit form of the vector forward pass (every element offset below 2^31):
 // the channel group of item i is i mod c/V by a launch-time divisor instead of
 // a 64-bit remainder
-template <int DT>
+template <int DT, bool NT>
 __global__ __launch_bounds__(256) void bias_lrelu_fwd32_kernel(const typename Store<DT>::T *z,
                                                                const float *__restrict__ bias, float alpha,
                                                                typename Store<DT>::T *y, int nv, FastDiv fcg) {
@@ -60,10 +60,10 @@ __global__ __launch_bounds__(256) void bias_lrelu_fwd32_kernel(const typename St
   if (i >= nv) return;
   const int c0 = (i - fdiv(i, fcg) * (int)fcg.div) * V;
   Vec16<DT> v;
-  v.u = reinterpret_cast<const uint4 *>(z)[i];
+  v.u = ld16<NT>(z + (long long)V * i);
 #pragma unroll
   for (int j = 0; j < V; ++j) v.e[j] = from_f32<DT>(lrelu(to_f32<DT>(v.e[j]) + bias[c0 + j], alpha));
-  reinterpret_cast<uint4 *>(y)[i] = v.u;
+  st16<NT>(y + (long long)V * i, v.u);
 }
 
 // Thread layout of the backward kernel: CG channel groups of V channels,
@@ -89,7 +89,31 @@ __global__ __launch_bounds__(256) void bias_lrelu_bwd_kernel(const typename Stor
     float s[V];
 #pragma unroll
     for (int j = 0; j < V; ++j) s[j] = 0.f;
-    for (long long v = v0 + ph; v < v1; v += ph_n) {
+    long long v = v0 + ph;
+    if constexpr (VECTOR) {
+      // four voxels per step (eight loads in flight), summed in voxel order as below
+      for (; v + 3LL * ph_n < v1; v += 4LL * ph_n) {
+        Vec16<DT> g[4], o[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const long long e = (v + (long long)u * ph_n) * c + (long long)cg * V;
+          g[u].u = *reinterpret_cast<const uint4 *>(dy + e);
+          o[u].u = *reinterpret_cast<const uint4 *>(y + e);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int j = 0; j < V; ++j) {
+            float d = to_f32<DT>(g[u].e[j]) * (to_f32<DT>(o[u].e[j]) > 0.f ? 1.f : alpha);
+            s[j] += d;
+            g[u].e[j] = from_f32<DT>(d);
+          }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          *reinterpret_cast<uint4 *>(dz + (v + (long long)u * ph_n) * c + (long long)cg * V) = g[u].u;
+      }
+    }
+    for (; v < v1; v += ph_n) {
       const long long e = v * c + (long long)cg * V;
       if constexpr (VECTOR) {
         Vec16<DT> g, o;
@@ -127,18 +151,78 @@ __global__ __launch_bounds__(256) void bias_lrelu_bwd_kernel(const typename Stor
   }
 }
 
+// One pass over whole 16-byte vectors with 32-bit offsets, for c / V a power
+// of two up to 64 and c <= 256: workgroup b takes the U * 256 consecutive
+// vectors from b * U * 256, thread t the ones at t, t + 256, ... (all of
+// channel group t % (c / V), since c / V divides 256).  The bias-gradient
+// partial of the workgroup: each thread sums its vectors in order, a fixed
+// butterfly over the lanes of a wave that share a channel group, then the
+// four waves as (w0 + w1) + (w2 + w3).
+template <int DT, bool WITH_DB, int U, bool NT>
+__global__ __launch_bounds__(256) void bias_lrelu_bwd_vec_kernel(const typename Store<DT>::T *__restrict__ dy,
+                                                                 const typename Store<DT>::T *__restrict__ y,
+                                                                 float alpha, typename Store<DT>::T *__restrict__ dz,
+                                                                 float *__restrict__ part, int nv, int cg_n, int c) {
+  constexpr int V = Store<DT>::VEC;
+  __shared__ float red[4 * 256];
+  const int tid = threadIdx.x;
+  const int k0 = (int)blockIdx.x * (256 * U) + tid;
+  Vec16<DT> g[U], o[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u)
+    if (k0 + 256 * u < nv) {
+      g[u].u = ld16<NT>(dy + V * (k0 + 256 * u));
+      o[u].u = ld16<NT>(y + V * (k0 + 256 * u));
+    }
+  float s[V];
+#pragma unroll
+  for (int j = 0; j < V; ++j) s[j] = 0.f;
+#pragma unroll
+  for (int u = 0; u < U; ++u)
+    if (k0 + 256 * u < nv) {
+#pragma unroll
+      for (int j = 0; j < V; ++j) {
+        const float d = to_f32<DT>(g[u].e[j]) * (to_f32<DT>(o[u].e[j]) > 0.f ? 1.f : alpha);
+        s[j] += d;
+        g[u].e[j] = from_f32<DT>(d);
+      }
+      st16<NT>(dz + V * (k0 + 256 * u), g[u].u);
+    }
+  if constexpr (WITH_DB) {
+    for (int off = cg_n; off < 64; off <<= 1)
+#pragma unroll
+      for (int j = 0; j < V; ++j) s[j] += __shfl_xor(s[j], off, 64);
+    const int lane = tid & 63, wave = tid >> 6;
+    if (lane < cg_n)
+#pragma unroll
+      for (int j = 0; j < V; ++j) red[wave * 256 + lane * V + j] = s[j];
+    __syncthreads();
+    if (tid < c)
+      part[(long long)blockIdx.x * c + tid] = (red[tid] + red[256 + tid]) + (red[512 + tid] + red[768 + tid]);
+  }
+}
+
 __global__ __launch_bounds__(256) void fill_zero_kernel(float *out, long long n) {
   long long i = (long long)blockIdx.x * 256 + threadIdx.x;
   if (i < n) out[i] = 0.f;
 }
 
 struct BwdPlan {
-  long long vpb;
+  long long vpb;  // general kernel: voxels per workgroup
   int blocks;
+  int unroll;     // vector kernel: vectors per thread (0: the general kernel)
 };
 
-BwdPlan plan_bwd(long long nvox, int c) {
-  BwdPlan p;
+// V = elements per 16-byte vector of the dtype
+BwdPlan plan_bwd(long long nvox, int c, int V) {
+  BwdPlan p{};
+  const int cg_n = c / V;
+  if (c % V == 0 && (cg_n & (cg_n - 1)) == 0 && cg_n <= 64 && c <= 256 && nvox * c < (1LL << 31)) {
+    const long long nv = nvox * cg_n;
+    p.unroll = nv >= (1LL << 22) ? 4 : 1;
+    p.blocks = (int)((nv + 256LL * p.unroll - 1) / (256LL * p.unroll));
+    return p;
+  }
   long long vpb = std::max<long long>(64, (nvox + 2047) / 2048);
   p.vpb = vpb;
   p.blocks = (int)((nvox + vpb - 1) / vpb);
@@ -153,8 +237,12 @@ hipError_t fwd_t(long long nvox, int c, const void *z, const float *bias, float 
   const bool vec = c % Store<DT>::VEC == 0;
   const long long items = vec ? nelem / Store<DT>::VEC : nelem;
   if (vec && nelem < (1LL << 31)) {
-    hipLaunchKernelGGL(bias_lrelu_fwd32_kernel<DT>, dim3((unsigned)((items + 255) / 256)), dim3(256), 0, st,
-                       (const T *)z, bias, alpha, (T *)y, (int)items, make_fastdiv(c / Store<DT>::VEC));
+    if (nelem * (long long)sizeof(T) >= kStreamBytes)
+      hipLaunchKernelGGL((bias_lrelu_fwd32_kernel<DT, true>), dim3((unsigned)((items + 255) / 256)), dim3(256), 0,
+                         st, (const T *)z, bias, alpha, (T *)y, (int)items, make_fastdiv(c / Store<DT>::VEC));
+    else
+      hipLaunchKernelGGL((bias_lrelu_fwd32_kernel<DT, false>), dim3((unsigned)((items + 255) / 256)), dim3(256), 0,
+                         st, (const T *)z, bias, alpha, (T *)y, (int)items, make_fastdiv(c / Store<DT>::VEC));
     return hipGetLastError();
   }
   const int blocks = (int)std::min<long long>((items + 255) / 256, 256LL * 64);
@@ -171,10 +259,21 @@ template <int DT, bool WITH_DB>
 hipError_t bwd_t(long long nvox, int c, const void *dy, const void *y, float alpha, void *dz,
                  float *db, void *ws, hipStream_t st) {
   using T = typename Store<DT>::T;
-  BwdPlan pl = plan_bwd(nvox, c);
+  const BwdPlan pl = plan_bwd(nvox, c, Store<DT>::VEC);
   const bool vec = c % Store<DT>::VEC == 0;
   float *part = (float *)ws;
-  if (vec)
+  if (pl.unroll) {
+    const int nv = (int)(nvox * c / Store<DT>::VEC), cg_n = c / Store<DT>::VEC;
+    if (nvox * c * (long long)sizeof(T) >= kStreamBytes)
+      hipLaunchKernelGGL((bias_lrelu_bwd_vec_kernel<DT, WITH_DB, 4, true>), dim3(pl.blocks), dim3(256), 0, st,
+                         (const T *)dy, (const T *)y, alpha, (T *)dz, part, nv, cg_n, c);
+    else if (pl.unroll == 4)
+      hipLaunchKernelGGL((bias_lrelu_bwd_vec_kernel<DT, WITH_DB, 4, false>), dim3(pl.blocks), dim3(256), 0, st,
+                         (const T *)dy, (const T *)y, alpha, (T *)dz, part, nv, cg_n, c);
+    else
+      hipLaunchKernelGGL((bias_lrelu_bwd_vec_kernel<DT, WITH_DB, 1, false>), dim3(pl.blocks), dim3(256), 0, st,
+                         (const T *)dy, (const T *)y, alpha, (T *)dz, part, nv, cg_n, c);
+  } else if (vec)
     hipLaunchKernelGGL((bias_lrelu_bwd_kernel<DT, true, WITH_DB>), dim3(pl.blocks), dim3(256), 0, st,
                        (const T *)dy, (const T *)y, alpha, (T *)dz, part, nvox, c, pl.vpb);
   else
@@ -196,8 +295,9 @@ hipError_t launch_bias_lrelu_fwd(int64_t nvox, int c, int dtype, const void *z, 
 
 size_t bias_lrelu_bwd_workspace(int64_t nvox, int c) {
   if (nvox <= 0) return 0;
-  BwdPlan pl = plan_bwd(nvox, c);
-  return (size_t)pl.blocks * c * sizeof(float);
+  // the larger of the two dtypes' plans (the workspace query takes no dtype)
+  const int blocks = std::max(plan_bwd(nvox, c, 8).blocks, plan_bwd(nvox, c, 4).blocks);
+  return (size_t)blocks * c * sizeof(float);
 }
 
 hipError_t launch_bias_lrelu_bwd(int64_t nvox, int c, int dtype, const void *dy, const void *y,

@@ -111,7 +111,7 @@ __global__ __launch_bounds__(256) void avgpool_bwd_kernel(const typename Store<D
 // window, so every store instruction of a wave writes a contiguous 1 KiB;
 // the planes, rows and columns that no window covers (odd extents) get
 // zeros.  Items are decoded with launch-time divisors.
-template <int DT>
+template <int DT, bool NT>
 __global__ __launch_bounds__(256) void avgpool2_fwd_vec_kernel(const typename Store<DT>::T *__restrict__ y,
                                                                typename Store<DT>::T *__restrict__ p, int d, int h,
                                                                int w, int c, FastDiv fcg, FastDiv fow, FastDiv foh,
@@ -130,7 +130,7 @@ __global__ __launch_bounds__(256) void avgpool2_fwd_vec_kernel(const typename St
     for (int b = 0; b < 2; ++b)
 #pragma unroll
       for (int e = 0; e < 2; ++e)
-        v[4 * a + 2 * b + e].u = *reinterpret_cast<const uint4 *>(y + base + ((a * h + b) * w + e) * c);
+        v[4 * a + 2 * b + e].u = ld16<NT>(y + base + ((a * h + b) * w + e) * c);
   float sum[V];
 #pragma unroll
   for (int j = 0; j < V; ++j) sum[j] = 0.f;
@@ -141,10 +141,10 @@ __global__ __launch_bounds__(256) void avgpool2_fwd_vec_kernel(const typename St
   Vec16<DT> o;
 #pragma unroll
   for (int j = 0; j < V; ++j) o.e[j] = from_f32<DT>(sum[j] * 0.125f);
-  *reinterpret_cast<uint4 *>(p + V * i) = o.u;  // output is dense NDHWC in item order
+  st16<NT>(p + V * i, o.u);  // output is dense NDHWC in item order
 }
 
-template <int DT>
+template <int DT, bool NT>
 __global__ __launch_bounds__(256) void avgpool2_bwd_vec_kernel(const typename Store<DT>::T *__restrict__ dp,
                                                                typename Store<DT>::T *__restrict__ dy, int d, int h,
                                                                int w, int c, int od, int oh, int ow, FastDiv frow,
@@ -158,7 +158,7 @@ __global__ __launch_bounds__(256) void avgpool2_bwd_vec_kernel(const typename St
   const int xv = fdiv(j, fcg), cg = j - xv * (int)fcg.div, px = xv >> 1;
   Vec16<DT> v;
   if (pz < od && py < oh && px < ow) {
-    v.u = *reinterpret_cast<const uint4 *>(dp + (((n * od + pz) * oh + py) * ow + px) * c + V * cg);
+    v.u = ld16<NT>(dp + (((n * od + pz) * oh + py) * ow + px) * c + V * cg);
 #pragma unroll
     for (int k = 0; k < V; ++k) v.e[k] = from_f32<DT>(to_f32<DT>(v.e[k]) * 0.125f);
   } else {
@@ -169,7 +169,7 @@ __global__ __launch_bounds__(256) void avgpool2_bwd_vec_kernel(const typename St
   for (int a = 0; a < 2; ++a)
 #pragma unroll
     for (int b = 0; b < 2; ++b)
-      if (2 * pz + a < d && 2 * py + b < h) *reinterpret_cast<uint4 *>(dy + base + (a * h + b) * w * c) = v.u;
+      if (2 * pz + a < d && 2 * py + b < h) st16<NT>(dy + base + (a * h + b) * w * c, v.u);
 }
 
 template <int DT, bool BWD>
@@ -186,14 +186,17 @@ hipError_t pool_t(int n, int d, int h, int w, int c, int k, const void *src, voi
   const long long elems = (long long)n * d * h * w * c;
   if (k == 2 && vec && elems < (1LL << 31)) {
     const int cgn = c / V;
+    const bool nt = elems * (long long)sizeof(T) >= kStreamBytes;
     if (BWD) {
       const int dc = (d + 1) / 2, hc = (h + 1) / 2;
       const long long its = (long long)n * dc * hc * w * cgn;
-      hipLaunchKernelGGL(avgpool2_bwd_vec_kernel<DT>, dim3((int)((its + 255) / 256)), dim3(256), 0, st,
+      hipLaunchKernelGGL((nt ? avgpool2_bwd_vec_kernel<DT, true> : avgpool2_bwd_vec_kernel<DT, false>),
+                         dim3((int)((its + 255) / 256)), dim3(256), 0, st,
                          (const T *)src, (T *)dst, d, h, w, c, od, oh, ow, make_fastdiv(w * cgn), make_fastdiv(hc),
                          make_fastdiv(dc), make_fastdiv(cgn), (int)its);
     } else {
-      hipLaunchKernelGGL(avgpool2_fwd_vec_kernel<DT>, dim3((int)((items + 255) / 256)), dim3(256), 0, st,
+      hipLaunchKernelGGL((nt ? avgpool2_fwd_vec_kernel<DT, true> : avgpool2_fwd_vec_kernel<DT, false>),
+                         dim3((int)((items + 255) / 256)), dim3(256), 0, st,
                          (const T *)src, (T *)dst, d, h, w, c, make_fastdiv(cgn), make_fastdiv(ow), make_fastdiv(oh),
                          make_fastdiv(od), (int)items);
     }

@@ -215,6 +215,30 @@ def test_bias_lrelu_in_place_and_large(dt):
 
 
 @pytest.mark.parametrize("dt", DTYPES)
+def test_bias_lrelu_bwd_large(dt):
+    """Over 2^22 16-byte vectors (four per thread) with a ragged last
+    workgroup, dz written in place over dy; the bias gradient against the
+    oracle and bitwise against a second call."""
+    rng = np.random.default_rng(8)
+    shape = (1, 129, 128, 129, 16)
+    nvox = int(np.prod(shape[:4]))
+    y = dev(rng.standard_normal(shape), dt)
+    dyn = rng.standard_normal(shape)
+    dzref, dbref = oracle.bias_lrelu_bwd(to_np(dev(dyn, dt)), to_np(y), 0.01)
+    ws = torch.empty(max(16, B.cf_bias_lrelu_bwd_workspace_size(nvox, 16)), dtype=torch.uint8, device="cuda")
+    dbs = []
+    for _ in range(2):
+        dy = dev(dyn, dt)
+        db = torch.empty(16, dtype=torch.float32, device="cuda")
+        B.cf_bias_lrelu_bwd(nvox, 16, dt, dy, y, 0.01, dy, db, ws)
+        torch.cuda.synchronize()
+        dbs.append(db.cpu())
+    assert maxabs_err(to_np(dy), dzref) <= TOL[dt]
+    assert maxabs_err(dbs[0].double().numpy(), dbref) <= 1e-5
+    assert torch.equal(dbs[0], dbs[1])
+
+
+@pytest.mark.parametrize("dt", DTYPES)
 @pytest.mark.parametrize("shape", [(2, 8, 6, 10, 16), (1, 7, 5, 9, 3), (1, 12, 12, 12, 64), (2, 7, 5, 9, 24),
                                    (3, 6, 7, 8, 16), (1, 9, 8, 6, 32)])
 def test_avgpool(dt, shape):
@@ -247,3 +271,40 @@ def test_empty_batch_is_noop_and_zero_grads():
     torch.cuda.synchronize()
     assert z.item() == 7.0
     assert torch.all(dw == 0) and torch.all(db == 0)
+
+
+@pytest.mark.parametrize("dt", DTYPES)
+def test_streaming_passes_at_256mib(dt):
+    """Tensors of 256 MiB, where the elementwise and pooling passes switch to
+    non-temporal loads and stores: bias + leaky ReLU forward and backward and
+    the 2^3 pool forward and backward against the oracle over every element."""
+    rng = np.random.default_rng(11)
+    shape = (2 if dt == "f32" else 4, 128, 128, 128, 16)
+    n, d, h, w, c = shape
+    nvox = n * d * h * w
+    z = dev(rng.standard_normal(shape, dtype=np.float32), dt)
+    assert z.numel() * z.element_size() == 1 << 28
+    bias = torch.from_numpy(rng.normal(0, 0.1, c).astype(np.float32)).cuda()
+    y = torch.empty_like(z)
+    B.cf_bias_lrelu_fwd(nvox, c, dt, z, bias, 0.01, y)
+    torch.cuda.synchronize()
+    assert maxabs_err(to_np(y), oracle.bias_lrelu_fwd(to_np(z), bias.cpu().double().numpy(), 0.01)) <= TOL[dt]
+    del z
+    dy = dev(rng.standard_normal(shape, dtype=np.float32), dt)
+    dzref, dbref = oracle.bias_lrelu_bwd(to_np(dy), to_np(y), 0.01)
+    dz = torch.empty_like(y)
+    db = torch.empty(c, dtype=torch.float32, device="cuda")
+    ws = torch.empty(max(16, B.cf_bias_lrelu_bwd_workspace_size(nvox, c)), dtype=torch.uint8, device="cuda")
+    B.cf_bias_lrelu_bwd(nvox, c, dt, dy, y, 0.01, dz, db, ws)
+    torch.cuda.synchronize()
+    assert maxabs_err(to_np(dz), dzref) <= TOL[dt]
+    assert maxabs_err(db.cpu().double().numpy(), dbref) <= 1e-5
+    del dz, dzref, dy
+    p = torch.empty((n, d // 2, h // 2, w // 2, c), dtype=tdtype(dt), device="cuda")
+    B.cf_avgpool3d_fwd(n, d, h, w, c, 2, 2, dt, y, p)
+    torch.cuda.synchronize()
+    assert maxabs_err(to_np(p), oracle.avgpool3d_fwd(to_np(y))) <= TOL[dt]
+    dx = torch.full(shape, float("nan"), dtype=tdtype(dt), device="cuda")
+    B.cf_avgpool3d_bwd(n, d, h, w, c, 2, 2, dt, p, dx)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_np(dx), oracle.avgpool3d_bwd(to_np(p), (d, h, w)))
