@@ -75,6 +75,12 @@ def _load():
         lib.ref_lr_schedule.restype = ctypes.c_double
         lib.ref_adam_larc_step.argtypes = [I, ctypes.POINTER(I64), I64, I64, P, P, P, P, P, P]
         lib.ref_adam_larc_step.restype = None
+        for name in ("ref_fc_fwd", "ref_fc_bwd_data", "ref_fc_bwd_weight"):
+            f = getattr(lib, name)
+            f.argtypes = [P, P, P, I, I, I]
+            f.restype = None
+        lib.ref_mse_loss.argtypes = [P, P, P, I, I]
+        lib.ref_mse_loss.restype = ctypes.c_double
         _lib = lib
         return lib
 
@@ -314,3 +320,86 @@ def adam_larc_step(offsets, t, t_decay, v, g, m, s, **hp):
     _load().ref_adam_larc_step(ng, off.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), int(t), int(t_decay),
                                _ptr(hpa), _ptr(v), _ptr(g), _ptr(m), _ptr(s), _ptr(dag))
     return v, m, s, dag[:ng]
+
+
+# ----------------------------------------------------------------------
+# Fully-connected head and loss (Section III-A: three FC layers, leaky ReLU
+# on every layer, three outputs).  x rows are [M][K], W is [K][N].
+
+def fc_fwd(x, w):
+    """z = x W for x [M][K] (a batch of flattened feature rows) and W [K][N]."""
+    x = _f64(x)
+    w = _f64(w)
+    M = x.shape[0]
+    x = x.reshape(M, -1)
+    K, N = w.shape
+    assert x.shape[1] == K
+    z = np.empty((M, N), np.float64)
+    _load().ref_fc_fwd(_ptr(x), _ptr(w), _ptr(z), M, K, N)
+    return z
+
+
+def fc_bwd_data(dz, w):
+    """dx = dz W^T, shape [M][K]."""
+    dz = _f64(dz)
+    w = _f64(w)
+    K, N = w.shape
+    M = dz.shape[0]
+    assert dz.shape == (M, N)
+    dx = np.empty((M, K), np.float64)
+    _load().ref_fc_bwd_data(_ptr(dz), _ptr(w), _ptr(dx), M, K, N)
+    return dx
+
+
+def fc_bwd_weight(x, dz):
+    """dW = x^T dz, shape [K][N]."""
+    x = _f64(x)
+    dz = _f64(dz)
+    M = x.shape[0]
+    x = x.reshape(M, -1)
+    K = x.shape[1]
+    N = dz.shape[1]
+    assert dz.shape == (M, N)
+    dw = np.empty((K, N), np.float64)
+    _load().ref_fc_bwd_weight(_ptr(x), _ptr(dz), _ptr(dw), M, K, N)
+    return dw
+
+
+def mse_loss(p, t):
+    """(loss, dL/dp) of the mean squared error over all M x N outputs."""
+    p = _f64(p)
+    t = _f64(t)
+    assert p.shape == t.shape and p.ndim == 2
+    dp = np.empty_like(p)
+    loss = _load().ref_mse_loss(_ptr(p), _ptr(t), _ptr(dp), p.shape[0], p.shape[1])
+    return loss, dp
+
+
+def head_forward(feat, weights, biases, alpha, target):
+    """FC layers (each fc -> bias + leaky ReLU) on feature rows feat [M][K0],
+    then the loss against target [M][N_last].  Returns (loss, dL/d(last
+    output), acts) with acts a per-layer list of dicts x, z, y."""
+    acts = []
+    h = _f64(feat).reshape(np.asarray(feat).shape[0], -1)
+    for w, b in zip(weights, biases):
+        z = fc_fwd(h, w)
+        y = bias_lrelu_fwd(z, b, alpha)
+        acts.append(dict(x=h, z=z, y=y))
+        h = y
+    loss, dp = mse_loss(h, target)
+    return loss, dp, acts
+
+
+def head_backward(acts, weights, dp, alpha):
+    """Backward through the FC layers from dL/d(last output).  Returns
+    (per-layer dicts dz, db, dw, dx; gradient of the feature rows)."""
+    grads = [None] * len(acts)
+    g = _f64(dp)
+    for i in range(len(acts) - 1, -1, -1):
+        a = acts[i]
+        dz, db = bias_lrelu_bwd(g, a["y"], alpha)
+        dw = fc_bwd_weight(a["x"], dz)
+        dx = fc_bwd_data(dz, weights[i])
+        grads[i] = dict(dz=dz, db=db, dw=dw, dx=dx)
+        g = dx
+    return grads, g

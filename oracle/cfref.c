@@ -40,6 +40,15 @@
  *   - parameter update: Section III-B ("SGD Optimizer"): Adam on a gradient
  *     rescaled per layer by LARC's clipped local rate, with a global rate on
  *     a linear (power 1) decay.  See ref_adam_larc_step for the readings.
+ *   - fully-connected layers: Section III-A (three FC layers after the
+ *     convolutions, leaky ReLU on every one, three outputs for the three
+ *     cosmological parameters).  A layer maps a row x[m][0..K) to
+ *     z[m][j] = sum_k x[m][k] W[k][j] (W stored [K][N], input index major);
+ *     its backward maps are the exact adjoints.  The widths of the first two
+ *     layers are in Fig. 2, which the text lacks: they are parameters here.
+ *   - loss: not named by the paper.  Read as the mean squared error of the
+ *     three regressed parameters over the batch,
+ *     L = (1 / (M N)) sum_{m,j} (p[m][j] - t[m][j])^2, dL/dp = 2 (p - t) / (M N).
  */
 #include <math.h>
 #include <stddef.h>
@@ -442,4 +451,55 @@ void ref_adam_larc_step(int ngroups, const int64_t *off, int64_t t, int64_t t_de
       v[i] = v[i] - a_k * m[i] / (sqrt(s[i]) + eps_hat);
     }
   }
+}
+
+/* ------------------------------------------------------------------------
+ * Fully-connected layers (Section III-A) and the loss.
+ * x: [M][K] rows (for the first layer, one sample's NDHWC output flattened
+ * in memory order), W: [K][N], z / dz: [M][N].
+ * ------------------------------------------------------------------------ */
+
+/* z[m][j] = sum over k = 0 .. K-1 (in order) of x[m][k] W[k][j] */
+void ref_fc_fwd(const double *x, const double *wt, double *z, int M, int K, int N) {
+#pragma omp parallel for collapse(2) schedule(static)
+  for (int m = 0; m < M; ++m)
+    for (int j = 0; j < N; ++j) {
+      double s = 0.0;
+      for (int k = 0; k < K; ++k) s += x[(int64_t)m * K + k] * wt[(int64_t)k * N + j];
+      z[(int64_t)m * N + j] = s;
+    }
+}
+
+/* dx[m][k] = sum over j (in order) of dz[m][j] W[k][j]  (adjoint in x) */
+void ref_fc_bwd_data(const double *dz, const double *wt, double *dx, int M, int K, int N) {
+#pragma omp parallel for collapse(2) schedule(static)
+  for (int m = 0; m < M; ++m)
+    for (int k = 0; k < K; ++k) {
+      double s = 0.0;
+      for (int j = 0; j < N; ++j) s += dz[(int64_t)m * N + j] * wt[(int64_t)k * N + j];
+      dx[(int64_t)m * K + k] = s;
+    }
+}
+
+/* dW[k][j] = sum over m (in order) of x[m][k] dz[m][j]  (adjoint in W) */
+void ref_fc_bwd_weight(const double *x, const double *dz, double *dw, int M, int K, int N) {
+#pragma omp parallel for collapse(2) schedule(static)
+  for (int k = 0; k < K; ++k)
+    for (int j = 0; j < N; ++j) {
+      double s = 0.0;
+      for (int m = 0; m < M; ++m) s += x[(int64_t)m * K + k] * dz[(int64_t)m * N + j];
+      dw[(int64_t)k * N + j] = s;
+    }
+}
+
+/* mean squared error over the M x N predictions; dp = dL/dp.  Returns L. */
+double ref_mse_loss(const double *p, const double *t, double *dp, int M, int N) {
+  const double inv = 1.0 / ((double)M * (double)N);
+  double s = 0.0;
+  for (int64_t i = 0; i < (int64_t)M * N; ++i) {
+    const double e = p[i] - t[i];
+    s += e * e;
+    dp[i] = 2.0 * e * inv;
+  }
+  return s * inv;
 }
