@@ -336,6 +336,52 @@ cf_status cf_adam_larc_step(int32_t ngroups, const int64_t *offsets, int64_t t,
                             const cf_adam_larc_hparams *hp, float *v, const float *g, float *m,
                             float *s, void *v16, void *ws, size_t ws_bytes, void *stream);
 
+/* ------------------------------------------------------------------------
+ * Fully-connected head and loss (Section III-A: three fully-connected layers
+ * follow the convolutions, each with leaky ReLU -- applied by
+ * cf_bias_lrelu_fwd / _bwd with nvox = m rows and c = n features -- the last
+ * with three outputs, one per regressed cosmological parameter).
+ *
+ * A layer maps the m rows of x [m][k] (for the first layer: each sample's
+ * NDHWC activation flattened in memory order, k = d*h*w*c) to
+ *   z[i][j] = sum_{l < k} x[i][l] W[l][j],    W stored [k][n] (row l = input l).
+ * x, W, z, dz, dx are in dtype; dW is fp32; products and sums are fp32.
+ * Sizes: m >= 0 (m == 0 is a no-op), 1 <= k < 2^31, 1 <= n <= 65536 and
+ * k * n < 2^40.  All device pointers 16-byte aligned; outputs must not
+ * overlap inputs (CF_ERR_ALIAS).  Every sum has an order fixed by the sizes:
+ * results are deterministic.  Bandwidth-bound: each call streams W (or dW)
+ * through HBM once per 8 rows of the batch.
+ * ------------------------------------------------------------------------ */
+
+/* Bytes of device workspace cf_fc_fwd needs (fp32 partial sums of the split
+ * over k; 0 for invalid sizes). */
+size_t cf_fc_fwd_workspace_size(int32_t m, int32_t k, int32_t n);
+
+/* z = x W (see above).  ws: cf_fc_fwd_workspace_size() bytes, contents
+ * need no initialisation, must not overlap x, W or z. */
+cf_status cf_fc_fwd(int32_t m, int32_t k, int32_t n, int32_t dtype, const void *x, const void *w,
+                    void *z, void *ws, size_t ws_bytes, void *stream);
+
+/* Backward data, the adjoint in x:  dx[i][l] = sum_j dz[i][j] W[l][j].
+ * dz [m][n], W [k][n], dx [m][k]. */
+cf_status cf_fc_bwd_data(int32_t m, int32_t k, int32_t n, int32_t dtype, const void *dz,
+                         const void *w, void *dx, void *stream);
+
+/* Backward weights, the adjoint in W:  dW[l][j] = sum_{i < m} x[i][l] dz[i][j]
+ * (summed over the batch rows in order), dW fp32 [k][n], overwritten.  m == 0
+ * writes dW = 0. */
+cf_status cf_fc_bwd_weight(int32_t m, int32_t k, int32_t n, int32_t dtype, const void *x,
+                           const void *dz, float *dw, void *stream);
+
+/* Loss.  The paper does not name it; it is read as the mean squared error
+ * of the regressed parameters over the batch:
+ *   loss = (1/(m n)) sum_{i,j} (p[i][j] - t[i][j])^2,
+ *   dp[i][j] = 2 (p[i][j] - t[i][j]) / (m n)      (dL/dp, rounded once to dtype).
+ * p, dp [m][n] in dtype; t [m][n] fp32; loss: one fp32 on the device.  dp may
+ * be NULL (loss only).  m, n >= 1 and m * n < 2^31.  One workgroup. */
+cf_status cf_mse_loss(int32_t m, int32_t n, int32_t dtype, const void *p, const float *t,
+                      float *loss, void *dp, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -36,6 +36,7 @@ EXPORTS = [
     "cf_conv3d_bwd_weight_fused_workspace_size", "cf_conv3d_bwd_weight_fused", "cf_conv3d_bwd_weight_fused_dz",
     "cf_conv3d_bwd_data_fused", "cf_reduce_partials", "cf_conv3d_bwd_weight_deferred", "cf_bias_lrelu_bwd_deferred",
     "cf_conv3d_bwd_weight_fused_deferred", "cf_adam_larc_workspace_size", "cf_adam_larc_step",
+    "cf_fc_fwd_workspace_size", "cf_fc_fwd", "cf_fc_bwd_data", "cf_fc_bwd_weight", "cf_mse_loss",
 ]
 
 
@@ -123,6 +124,11 @@ def lib():
         "cf_adam_larc_workspace_size": ([i32, ctypes.POINTER(i64)], sz),
         "cf_adam_larc_step": ([i32, ctypes.POINTER(i64), i64, ctypes.POINTER(cf_adam_larc_hparams), vp, vp, vp, vp,
                                vp, vp, sz, vp], ctypes.c_int),
+        "cf_fc_fwd_workspace_size": ([i32, i32, i32], sz),
+        "cf_fc_fwd": ([i32, i32, i32, i32, vp, vp, vp, vp, sz, vp], ctypes.c_int),
+        "cf_fc_bwd_data": ([i32, i32, i32, i32, vp, vp, vp, vp], ctypes.c_int),
+        "cf_fc_bwd_weight": ([i32, i32, i32, i32, vp, vp, vp, vp], ctypes.c_int),
+        "cf_mse_loss": ([i32, i32, i32, vp, vp, vp, vp, vp], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         f = getattr(L, name)
@@ -335,3 +341,28 @@ def cf_adam_larc_step(offsets, t, hp, v, g, m, s, v16, ws, ws_bytes=None, stream
     n, arr = _offsets(offsets)
     _check(lib().cf_adam_larc_step(n, arr, int(t), ctypes.byref(hp), _ptr(v), _ptr(g), _ptr(m), _ptr(s), _ptr(v16),
                                    _ptr(ws), ws_bytes, _stream(stream)))
+
+
+# ---- fully-connected head and loss ---------------------------------------------
+
+def cf_fc_fwd_workspace_size(m, k, n) -> int:
+    return int(lib().cf_fc_fwd_workspace_size(m, k, n))
+
+
+def cf_fc_fwd(m, k, n, dtype, x, w, z, ws, ws_bytes=None, stream=None):
+    if ws_bytes is None:
+        ws_bytes = 0 if ws is None or isinstance(ws, int) else ws.numel() * ws.element_size()
+    _check(lib().cf_fc_fwd(m, k, n, dtype_code(dtype), _ptr(x), _ptr(w), _ptr(z), _ptr(ws), ws_bytes,
+                           _stream(stream)))
+
+
+def cf_fc_bwd_data(m, k, n, dtype, dz, w, dx, stream=None):
+    _check(lib().cf_fc_bwd_data(m, k, n, dtype_code(dtype), _ptr(dz), _ptr(w), _ptr(dx), _stream(stream)))
+
+
+def cf_fc_bwd_weight(m, k, n, dtype, x, dz, dw, stream=None):
+    _check(lib().cf_fc_bwd_weight(m, k, n, dtype_code(dtype), _ptr(x), _ptr(dz), _ptr(dw), _stream(stream)))
+
+
+def cf_mse_loss(m, n, dtype, p, t, loss, dp, stream=None):
+    _check(lib().cf_mse_loss(m, n, dtype_code(dtype), _ptr(p), _ptr(t), _ptr(loss), _ptr(dp), _stream(stream)))

@@ -617,3 +617,88 @@ cf_status cf_adam_larc_step(int32_t ngroups, const int64_t *offsets, int64_t t, 
 }
 
 }  // extern "C"
+
+// ---- fully-connected head and loss -------------------------------------------
+
+namespace {
+cf_status fc_check(int32_t m, int32_t k, int32_t n, int32_t dtype, const char *who) {
+  if (m < 0) return fail(CF_ERR_INVALID_ARG, std::string(who) + ": m must be >= 0");
+  if (k <= 0 || n <= 0) return fail(CF_ERR_INVALID_ARG, std::string(who) + ": k and n must be > 0");
+  if (n > 65536) return fail(CF_ERR_UNSUPPORTED, std::string(who) + ": more than 65536 outputs");
+  if ((long long)k * n >= (1LL << 40)) return fail(CF_ERR_UNSUPPORTED, std::string(who) + ": k * n too large");
+  if (dtype != CF_F32 && dtype != CF_BF16) return fail(CF_ERR_INVALID_ARG, "unknown dtype");
+  return CF_OK;
+}
+int kdt(int32_t dtype) { return dtype == CF_BF16 ? cf::DT_BF16 : cf::DT_F32; }
+}  // namespace
+
+size_t cf_fc_fwd_workspace_size(int32_t m, int32_t k, int32_t n) {
+  if (m <= 0 || k <= 0 || n <= 0 || n > 65536 || (long long)k * n >= (1LL << 40)) return 0;
+  return cf::fc_fwd_workspace(m, k, n);
+}
+
+cf_status cf_fc_fwd(int32_t m, int32_t k, int32_t n, int32_t dtype, const void *x, const void *w, void *z,
+                    void *ws, size_t ws_bytes, void *stream) {
+  cf_status r = fc_check(m, k, n, dtype, "fc_fwd");
+  if (r != CF_OK) return r;
+  if (m == 0) return ok();
+  if ((r = check_ptrs({x, w, z})) != CF_OK) return r;
+  const size_t es = elem_size(dtype);
+  const size_t bx = (size_t)m * k * es, bw = (size_t)k * n * es, bz = (size_t)m * n * es;
+  const size_t need = cf::fc_fwd_workspace(m, k, n);
+  if (!ws || ws_bytes < need) return fail(CF_ERR_WORKSPACE, "fc_fwd: workspace smaller than cf_fc_fwd_workspace_size()");
+  if (!aligned16(ws)) return fail(CF_ERR_ALIGNMENT, "workspace not 16-byte aligned");
+  if (overlap(z, bz, x, bx) || overlap(z, bz, w, bw)) return fail(CF_ERR_ALIAS, "fc_fwd: z overlaps x or W");
+  if (overlap(ws, need, x, bx) || overlap(ws, need, w, bw) || overlap(ws, need, z, bz))
+    return fail(CF_ERR_ALIAS, "fc_fwd: workspace overlaps a tensor");
+  hipStream_t st = (hipStream_t)stream;
+  return finish(cf::launch_fc_fwd(m, k, n, kdt(dtype), x, w, z, ws, st), st, "cf_fc_fwd");
+}
+
+cf_status cf_fc_bwd_data(int32_t m, int32_t k, int32_t n, int32_t dtype, const void *dz, const void *w, void *dx,
+                         void *stream) {
+  cf_status r = fc_check(m, k, n, dtype, "fc_bwd_data");
+  if (r != CF_OK) return r;
+  if (m == 0) return ok();
+  if ((r = check_ptrs({dz, w, dx})) != CF_OK) return r;
+  const size_t es = elem_size(dtype);
+  const size_t bx = (size_t)m * k * es, bw = (size_t)k * n * es, bz = (size_t)m * n * es;
+  if (overlap(dx, bx, dz, bz) || overlap(dx, bx, w, bw)) return fail(CF_ERR_ALIAS, "fc_bwd_data: dx overlaps dz or W");
+  hipStream_t st = (hipStream_t)stream;
+  return finish(cf::launch_fc_bwd_data(m, k, n, kdt(dtype), dz, w, dx, st), st, "cf_fc_bwd_data");
+}
+
+cf_status cf_fc_bwd_weight(int32_t m, int32_t k, int32_t n, int32_t dtype, const void *x, const void *dz, float *dw,
+                           void *stream) {
+  cf_status r = fc_check(m, k, n, dtype, "fc_bwd_weight");
+  if (r != CF_OK) return r;
+  hipStream_t st = (hipStream_t)stream;
+  if (m == 0) {
+    if ((r = check_ptrs({dw})) != CF_OK) return r;
+    return finish(cf::launch_fill_zero(dw, (long long)k * n, st), st, "cf_fc_bwd_weight");
+  }
+  if ((r = check_ptrs({x, dz, dw})) != CF_OK) return r;
+  const size_t es = elem_size(dtype);
+  const size_t bx = (size_t)m * k * es, bz = (size_t)m * n * es, bw = (size_t)k * n * 4;
+  if (overlap(dw, bw, x, bx) || overlap(dw, bw, dz, bz)) return fail(CF_ERR_ALIAS, "fc_bwd_weight: dW overlaps x or dz");
+  return finish(cf::launch_fc_bwd_weight(m, k, n, kdt(dtype), x, dz, dw, st), st, "cf_fc_bwd_weight");
+}
+
+cf_status cf_mse_loss(int32_t m, int32_t n, int32_t dtype, const void *p, const float *t, float *loss, void *dp,
+                      void *stream) {
+  if (m <= 0 || n <= 0) return fail(CF_ERR_INVALID_ARG, "mse_loss: m and n must be > 0");
+  if ((long long)m * n >= (1LL << 31)) return fail(CF_ERR_UNSUPPORTED, "mse_loss: m * n too large");
+  if (dtype != CF_F32 && dtype != CF_BF16) return fail(CF_ERR_INVALID_ARG, "unknown dtype");
+  cf_status r;
+  if ((r = check_ptrs({p, t, loss})) != CF_OK) return r;
+  if (dp && !aligned16(dp)) return fail(CF_ERR_ALIGNMENT, "dp not 16-byte aligned");
+  const long long cnt = (long long)m * n;
+  const size_t es = elem_size(dtype);
+  if (overlap(loss, 4, p, cnt * es) || overlap(loss, 4, t, cnt * 4) || overlap(loss, 4, dp, dp ? cnt * es : 0))
+    return fail(CF_ERR_ALIAS, "mse_loss: loss overlaps a tensor");
+  if (dp && (overlap(dp, cnt * es, p, cnt * es) || overlap(dp, cnt * es, t, cnt * 4)))
+    return fail(CF_ERR_ALIAS, "mse_loss: dp overlaps p or t");
+  hipStream_t st = (hipStream_t)stream;
+  return finish(cf::launch_mse_loss(cnt, kdt(dtype), p, t, loss, dp, (float)(1.0 / (double)cnt), st), st,
+                "cf_mse_loss");
+}

@@ -145,4 +145,16 @@ int plan_opt_groups(int n, const long long *off, OptGroups *G);
 hipError_t launch_adam_larc(const OptGroups &G, int chunks, const OptHparams &hp, long long t, float *v,
                             const float *g, float *m, float *s, uint16_t *v16, double *part, hipStream_t st);
 
+// Fully-connected layers (fc.hip): rows x[M][K], W[K][N], z[M][N].
+size_t fc_fwd_workspace(int M, int K, int N);
+hipError_t launch_fc_fwd(int M, int K, int N, int dtype, const void *x, const void *w, void *y, void *ws,
+                         hipStream_t st);
+hipError_t launch_fc_bwd_data(int M, int K, int N, int dtype, const void *dz, const void *w, void *dx,
+                              hipStream_t st);
+hipError_t launch_fc_bwd_weight(int M, int K, int N, int dtype, const void *x, const void *dz, float *dw,
+                                hipStream_t st);
+// mean squared error over n predictions; inv = 1 / n; dp may be null
+hipError_t launch_mse_loss(long long n, int dtype, const void *p, const float *t, float *loss, void *dp,
+                           float inv, hipStream_t st);
+
 }  // namespace cf

@@ -1,0 +1,336 @@
+// fc.hip -- fully-connected layers and the loss for gfx950.
+//
+// Section III-A: after the convolutions the network has three
+// fully-connected layers, each followed by leaky ReLU (applied by the
+// bias + leaky ReLU kernels of eltwise.hip), the last with the three outputs
+// that regress the cosmological parameters.  A layer maps rows x[m][0..K)
+// to z[m][j] = sum_k x[m][k] W[k][j], W stored [K][N] (input index major).
+// With a batch of a few rows every pass is bound by reading W (or writing
+// dW) once from HBM, so the kernels below stream W with 16-byte loads over
+// the whole machine and keep the few batch rows in registers and LDS; no
+// pass is recast as a GEMM tile for the matrix cores.
+//   forward        split over K: workgroup b sums rows [b KC, (b+1) KC) of
+//                  W for all M x N outputs (its phases combined in LDS in
+//                  phase order), one partial row per workgroup, then the
+//                  fixed-order column sum of the partials;
+//   backward data  one group of G lanes per row k of W: each lane dots its
+//                  columns with dz, a lane butterfly completes the row;
+//   backward wts   one thread per (k, 4 columns) of dW: sum over the batch
+//                  rows in order (the reduction is only M long);
+//   loss           mean squared error, one workgroup, fixed-order tree.
+// Every sum has an order fixed by the shapes, so results are deterministic.
+
+#include "cf_common.h"
+#include "cf_kernels.h"
+
+#include <algorithm>
+
+namespace cf {
+namespace {
+
+constexpr int MB = 8;  // batch rows per pass (larger batches take several passes)
+
+// ---- forward ------------------------------------------------------------
+// Thread t: column group cg = t % cgw (+ cgw, 2 cgw, ... while < cg_n),
+// phase t / cgw of np phases; rows k0 + phase + np * u, u < U.
+template <int DT, bool VECTOR>
+__global__ __launch_bounds__(256) void fc_fwd_kernel(const typename Store<DT>::T *__restrict__ x,
+                                                     const typename Store<DT>::T *__restrict__ w,
+                                                     float *__restrict__ part, int m0, int mcnt, int K, int N,
+                                                     int cgw, int np, int kc) {
+  constexpr int V = VECTOR ? Store<DT>::VEC : 1;
+  __shared__ float xs[MB * 512];  // x[m0 + m][k0 + kk], kc <= 512
+  __shared__ float red[256 * V];  // [phase][column of the pass]
+  const int tid = threadIdx.x;
+  const int cg_n = N / V;
+  const long long k0 = (long long)blockIdx.x * kc;
+  const int krows = (int)std::min<long long>(kc, K - k0);
+  for (int i = tid; i < MB * kc; i += 256) {
+    const int m = i / kc, kk = i - m * kc;
+    xs[i] = (m < mcnt && kk < krows) ? to_f32<DT>(x[(long long)(m0 + m) * K + k0 + kk]) : 0.f;
+  }
+  __syncthreads();
+  const int ph = tid / cgw, c_in = tid - ph * cgw;
+  float *prow = part + (long long)blockIdx.x * mcnt * N;  // this workgroup's partial row [mcnt][N]
+  for (int cbase = 0; cbase < cg_n; cbase += cgw) {
+    const int cg = cbase + c_in;
+    const bool active = ph < np && cg < cg_n;
+    float acc[MB][V];
+#pragma unroll
+    for (int m = 0; m < MB; ++m)
+#pragma unroll
+      for (int j = 0; j < V; ++j) acc[m][j] = 0.f;
+    if (active) {
+#pragma unroll 4
+      for (int kk = ph; kk < krows; kk += np) {
+        const typename Store<DT>::T *wr = w + (k0 + kk) * N + (long long)cg * V;
+        float wv[V];
+        if constexpr (VECTOR) {
+          Vec16<DT> v;
+          v.u = ld16<false>(wr);
+#pragma unroll
+          for (int j = 0; j < V; ++j) wv[j] = to_f32<DT>(v.e[j]);
+        } else {
+          wv[0] = to_f32<DT>(wr[0]);
+        }
+#pragma unroll
+        for (int m = 0; m < MB; ++m) {
+          const float xv = xs[m * kc + kk];
+#pragma unroll
+          for (int j = 0; j < V; ++j) acc[m][j] = fmaf(xv, wv[j], acc[m][j]);
+        }
+      }
+    }
+    // combine the phases in phase order, one batch row at a time
+    const int ncols = std::min(cgw, cg_n - cbase) * V;
+#pragma unroll
+    for (int m = 0; m < MB; ++m) {
+      if (m >= mcnt) break;
+      __syncthreads();
+      if (active)
+#pragma unroll
+        for (int j = 0; j < V; ++j) red[ph * (cgw * V) + c_in * V + j] = acc[m][j];
+      __syncthreads();
+      for (int col = tid; col < ncols; col += 256) {
+        float s = 0.f;
+        for (int p = 0; p < np; ++p) s += red[p * (cgw * V) + col];
+        prow[m * N + cbase * V + col] = s;
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// y[m0 + m][j] = RNE(sum over workgroups), from the fp32 column sums
+template <int DT>
+__global__ __launch_bounds__(256) void fc_store_kernel(const float *__restrict__ s, typename Store<DT>::T *y, int m0,
+                                                       int mcnt, int N) {
+  const int i = (int)blockIdx.x * 256 + threadIdx.x;
+  if (i >= mcnt * N) return;
+  y[(long long)m0 * N + i] = from_f32<DT>(s[i]);
+}
+
+struct FwdPlan {
+  int cgw, np, kc, blocks;
+  bool vec;
+};
+
+FwdPlan plan_fwd(int K, int N, int V) {
+  FwdPlan p{};
+  p.vec = N % V == 0;
+  const int cg_n = p.vec ? N / V : N;
+  p.cgw = std::min(cg_n, 256);
+  p.np = 256 / p.cgw;
+  // about 512 workgroups, at most 512 rows each
+  const long long target = ((long long)K + 511) / 512;
+  long long u = std::max<long long>(1, (target + p.np - 1) / p.np);
+  long long kc = std::min<long long>(u * p.np, 512);
+  p.kc = (int)kc;
+  p.blocks = (int)(((long long)K + kc - 1) / kc);
+  return p;
+}
+
+template <int DT>
+hipError_t fc_fwd_t(int M, int K, int N, const void *x, const void *w, void *y, void *ws, hipStream_t st) {
+  using T = typename Store<DT>::T;
+  const FwdPlan pl = plan_fwd(K, N, Store<DT>::VEC);
+  float *part = (float *)ws;
+  float *sum = part + (size_t)pl.blocks * MB * N;
+  for (int m0 = 0; m0 < M; m0 += MB) {
+    const int mcnt = std::min(MB, M - m0);
+    if (pl.vec)
+      hipLaunchKernelGGL((fc_fwd_kernel<DT, true>), dim3(pl.blocks), dim3(256), 0, st, (const T *)x, (const T *)w,
+                         part, m0, mcnt, K, N, pl.cgw, pl.np, pl.kc);
+    else
+      hipLaunchKernelGGL((fc_fwd_kernel<DT, false>), dim3(pl.blocks), dim3(256), 0, st, (const T *)x, (const T *)w,
+                         part, m0, mcnt, K, N, pl.cgw, pl.np, pl.kc);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    e = launch_sum_rows(part, sum, pl.blocks, mcnt * N, st);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((fc_store_kernel<DT>), dim3((mcnt * N + 255) / 256), dim3(256), 0, st, sum, (T *)y, m0, mcnt,
+                       N);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+// ---- backward data --------------------------------------------------------
+// G lanes per row (a power of two, G >= the column groups when they fit one
+// wave); 256 / G rows per workgroup step.
+template <int DT, bool VECTOR>
+__global__ __launch_bounds__(256) void fc_bwd_data_kernel(const typename Store<DT>::T *__restrict__ dz,
+                                                          const typename Store<DT>::T *__restrict__ w,
+                                                          typename Store<DT>::T *__restrict__ dx, int m0, int mcnt,
+                                                          int K, int N, int G) {
+  constexpr int V = VECTOR ? Store<DT>::VEC : 1;
+  const int tid = threadIdx.x;
+  const int cg_n = N / V;
+  const int gl = tid & (G - 1), rows_per = 256 / G;
+  for (long long k = (long long)blockIdx.x * rows_per + tid / G; k < K; k += (long long)gridDim.x * rows_per) {
+    float acc[MB];
+#pragma unroll
+    for (int m = 0; m < MB; ++m) acc[m] = 0.f;
+    for (int cg = gl; cg < cg_n; cg += G) {
+      float wv[V];
+      if constexpr (VECTOR) {
+        Vec16<DT> v;
+        v.u = ld16<false>(w + k * N + (long long)cg * V);
+#pragma unroll
+        for (int j = 0; j < V; ++j) wv[j] = to_f32<DT>(v.e[j]);
+      } else {
+        wv[0] = to_f32<DT>(w[k * N + cg]);
+      }
+#pragma unroll
+      for (int m = 0; m < MB; ++m) {
+        if (m < mcnt) {
+          const typename Store<DT>::T *dr = dz + (long long)(m0 + m) * N + (long long)cg * V;
+          if constexpr (VECTOR) {
+            Vec16<DT> g;
+            g.u = ld16<false>(dr);
+#pragma unroll
+            for (int j = 0; j < V; ++j) acc[m] = fmaf(to_f32<DT>(g.e[j]), wv[j], acc[m]);
+          } else {
+            acc[m] = fmaf(to_f32<DT>(dr[0]), wv[0], acc[m]);
+          }
+        }
+      }
+    }
+    // butterfly over the G lanes of the row: every lane ends with the same sums
+    for (int off = G >> 1; off > 0; off >>= 1)
+#pragma unroll
+      for (int m = 0; m < MB; ++m) acc[m] += __shfl_xor(acc[m], off, 64);
+#pragma unroll
+    for (int m = 0; m < MB; ++m)
+      if (m < mcnt && gl == m % G) dx[(long long)(m0 + m) * K + k] = from_f32<DT>(acc[m]);
+  }
+}
+
+template <int DT>
+hipError_t fc_bwd_data_t(int M, int K, int N, const void *dz, const void *w, void *dx, hipStream_t st) {
+  using T = typename Store<DT>::T;
+  const bool vec = N % Store<DT>::VEC == 0;
+  const int cg_n = vec ? N / Store<DT>::VEC : N;
+  int G = 1;
+  while (G < cg_n && G < 64) G <<= 1;
+  const int rows_per = 256 / G;
+  const int blocks = (int)std::min<long long>(((long long)K + rows_per - 1) / rows_per, 4096);
+  for (int m0 = 0; m0 < M; m0 += MB) {
+    const int mcnt = std::min(MB, M - m0);
+    if (vec)
+      hipLaunchKernelGGL((fc_bwd_data_kernel<DT, true>), dim3(blocks), dim3(256), 0, st, (const T *)dz,
+                         (const T *)w, (T *)dx, m0, mcnt, K, N, G);
+    else
+      hipLaunchKernelGGL((fc_bwd_data_kernel<DT, false>), dim3(blocks), dim3(256), 0, st, (const T *)dz,
+                         (const T *)w, (T *)dx, m0, mcnt, K, N, G);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+// ---- backward weights ------------------------------------------------------
+// dW[k][4 c .. 4 c + 3] = sum over m = 0 .. M-1 of x[m][k] dz[m][4 c ..]
+template <int DT, bool VECTOR>
+__global__ __launch_bounds__(256) void fc_bwd_weight_kernel(const typename Store<DT>::T *__restrict__ x,
+                                                            const typename Store<DT>::T *__restrict__ dz,
+                                                            float *__restrict__ dw, int M, int K, int N,
+                                                            long long items) {
+  constexpr int V = VECTOR ? 4 : 1;
+  const int gq = N / V;
+  for (long long i = (long long)blockIdx.x * 256 + threadIdx.x; i < items; i += (long long)gridDim.x * 256) {
+    const long long k = i / gq;
+    const int c = (int)(i - k * gq) * V;
+    float acc[V];
+#pragma unroll
+    for (int j = 0; j < V; ++j) acc[j] = 0.f;
+    for (int m = 0; m < M; ++m) {
+      const float xv = to_f32<DT>(x[(long long)m * K + k]);
+#pragma unroll
+      for (int j = 0; j < V; ++j) acc[j] = fmaf(xv, to_f32<DT>(dz[(long long)m * N + c + j]), acc[j]);
+    }
+    if constexpr (VECTOR)
+      *reinterpret_cast<float4 *>(dw + k * N + c) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+    else
+      dw[k * N + c] = acc[0];
+  }
+}
+
+template <int DT>
+hipError_t fc_bwd_weight_t(int M, int K, int N, const void *x, const void *dz, float *dw, hipStream_t st) {
+  using T = typename Store<DT>::T;
+  const bool vec = N % 4 == 0;
+  const long long items = (long long)K * (vec ? N / 4 : N);
+  const int blocks = (int)std::min<long long>((items + 255) / 256, 256LL * 64);
+  if (vec)
+    hipLaunchKernelGGL((fc_bwd_weight_kernel<DT, true>), dim3(blocks), dim3(256), 0, st, (const T *)x,
+                       (const T *)dz, dw, M, K, N, items);
+  else
+    hipLaunchKernelGGL((fc_bwd_weight_kernel<DT, false>), dim3(blocks), dim3(256), 0, st, (const T *)x,
+                       (const T *)dz, dw, M, K, N, items);
+  return hipGetLastError();
+}
+
+// ---- loss ------------------------------------------------------------------
+template <int DT>
+__global__ __launch_bounds__(256) void mse_loss_kernel(const typename Store<DT>::T *__restrict__ p,
+                                                       const float *__restrict__ t, float *__restrict__ loss,
+                                                       typename Store<DT>::T *__restrict__ dp, long long n,
+                                                       float inv) {
+  __shared__ float red[256];
+  const int tid = threadIdx.x;
+  float s = 0.f;
+  for (long long i = tid; i < n; i += 256) {
+    const float e = to_f32<DT>(p[i]) - t[i];
+    s = fmaf(e, e, s);
+    if (dp) dp[i] = from_f32<DT>(2.f * e * inv);
+  }
+  red[tid] = s;
+  __syncthreads();
+  for (int h = 128; h > 0; h >>= 1) {
+    if (tid < h) red[tid] += red[tid + h];
+    __syncthreads();
+  }
+  if (tid == 0) loss[0] = red[0] * inv;
+}
+
+}  // namespace
+
+size_t fc_fwd_workspace(int M, int K, int N) {
+  if (M <= 0 || K <= 0 || N <= 0) return 0;
+  const FwdPlan a = plan_fwd(K, N, 8), b = plan_fwd(K, N, 4);
+  const int blocks = std::max(a.blocks, b.blocks);
+  return ((size_t)blocks * MB * N + (size_t)MB * N) * sizeof(float);
+}
+
+hipError_t launch_fc_fwd(int M, int K, int N, int dtype, const void *x, const void *w, void *y, void *ws,
+                         hipStream_t st) {
+  return dtype == DT_BF16 ? fc_fwd_t<DT_BF16>(M, K, N, x, w, y, ws, st)
+                          : fc_fwd_t<DT_F32>(M, K, N, x, w, y, ws, st);
+}
+
+hipError_t launch_fc_bwd_data(int M, int K, int N, int dtype, const void *dz, const void *w, void *dx,
+                              hipStream_t st) {
+  return dtype == DT_BF16 ? fc_bwd_data_t<DT_BF16>(M, K, N, dz, w, dx, st)
+                          : fc_bwd_data_t<DT_F32>(M, K, N, dz, w, dx, st);
+}
+
+hipError_t launch_fc_bwd_weight(int M, int K, int N, int dtype, const void *x, const void *dz, float *dw,
+                                hipStream_t st) {
+  return dtype == DT_BF16 ? fc_bwd_weight_t<DT_BF16>(M, K, N, x, dz, dw, st)
+                          : fc_bwd_weight_t<DT_F32>(M, K, N, x, dz, dw, st);
+}
+
+hipError_t launch_mse_loss(long long n, int dtype, const void *p, const float *t, float *loss, void *dp,
+                           float inv, hipStream_t st) {
+  if (dtype == DT_BF16)
+    hipLaunchKernelGGL(mse_loss_kernel<DT_BF16>, dim3(1), dim3(256), 0, st, (const uint16_t *)p, t, loss,
+                       (uint16_t *)dp, n, inv);
+  else
+    hipLaunchKernelGGL(mse_loss_kernel<DT_F32>, dim3(1), dim3(256), 0, st, (const float *)p, t, loss, (float *)dp,
+                       n, inv);
+  return hipGetLastError();
+}
+
+}  // namespace cf

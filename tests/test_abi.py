@@ -169,3 +169,28 @@ def test_adam_larc_workspace_and_validation(L):
     expect(B.CF_ERR_ALIAS, B.cf_adam_larc_step, off, 0, hp, v, g, v + 16400, s, None, ws, nws, 0)
     expect(B.CF_ERR_ALIAS, B.cf_adam_larc_step, off, 0, hp, v, g, m, s, None, s + 16, nws, 0)
     expect(B.CF_ERR_ALIAS, B.cf_adam_larc_step, off, 0, hp, v, g, m, s, g + 16, ws, nws, 0)
+
+
+def test_fc_and_loss_validation(L):
+    # workspace: 512-ish split of K, fp32 partial rows of 8 x n plus the column sums
+    need = B.cf_fc_fwd_workspace_size(8, 65536, 128)
+    assert need > 0 and need % 16 == 0
+    assert B.cf_fc_fwd_workspace_size(0, 10, 10) == 0
+    assert B.cf_fc_fwd_workspace_size(8, 10, 70000) == 0
+    x, w, z, ws = A, A + 0x1000000, A + 0x2000000, A + 0x3000000
+    B.cf_fc_fwd(0, 65536, 128, "bf16", None, None, None, None, 0, 0)  # empty batch: nothing to do
+    expect(B.CF_ERR_INVALID_ARG, B.cf_fc_fwd, -1, 10, 10, "f32", x, w, z, ws, need, 0)
+    expect(B.CF_ERR_INVALID_ARG, B.cf_fc_fwd, 8, 0, 10, "f32", x, w, z, ws, need, 0)
+    expect(B.CF_ERR_UNSUPPORTED, B.cf_fc_fwd, 8, 10, 70000, "f32", x, w, z, ws, need, 0)
+    expect(B.CF_ERR_WORKSPACE, B.cf_fc_fwd, 8, 65536, 128, "bf16", x, w, z, ws, need - 16, 0)
+    expect(B.CF_ERR_ALIGNMENT, B.cf_fc_fwd, 8, 65536, 128, "bf16", x + 2, w, z, ws, need, 0)
+    expect(B.CF_ERR_ALIAS, B.cf_fc_fwd, 8, 65536, 128, "bf16", x, w, w + 1024, ws, need, 0)
+    expect(B.CF_ERR_ALIAS, B.cf_fc_fwd, 8, 65536, 128, "bf16", x, w, z, x + 512, need, 0)
+    expect(B.CF_ERR_ALIAS, B.cf_fc_bwd_data, 8, 65536, 128, "bf16", z, w, w + 4096, 0)
+    expect(B.CF_ERR_INVALID_ARG, B.cf_fc_bwd_data, 8, 65536, 128, "bf16", z, None, x, 0)
+    expect(B.CF_ERR_ALIAS, B.cf_fc_bwd_weight, 8, 65536, 128, "bf16", x, z, x + 16, 0)
+    assert L.cf_fc_bwd_weight(8, 65536, 128, 7, x, z, ws, 0) == B.CF_ERR_INVALID_ARG  # unknown dtype
+    expect(B.CF_ERR_INVALID_ARG, B.cf_mse_loss, 0, 3, "f32", x, z, ws, None, 0)
+    expect(B.CF_ERR_ALIGNMENT, B.cf_mse_loss, 8, 3, "f32", x, z, ws, w + 8, 0)
+    expect(B.CF_ERR_ALIAS, B.cf_mse_loss, 8, 3, "f32", x, z, x + 16, None, 0)
+    expect(B.CF_ERR_ALIAS, B.cf_mse_loss, 8, 3, "f32", x, z, ws, z, 0)
