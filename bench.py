@@ -16,6 +16,11 @@ with events on the launch stream over the same timed steps.
 The parameter update that follows each step in training (Adam + LARC +
 linear decay, Section III-B) is timed on its own after the timed steps and
 reported under "update"; --with-update also runs it inside every step.
+The fully-connected head and loss on the stack's output (three FC layers
+with leaky ReLU, mean squared error) is likewise timed on its own and
+reported under "head"; --with-head runs it inside every step, the stack's
+upstream gradient then being the loss gradient instead of a fixed N(0,1)
+tensor.
 "hbm_passes" times the unfused elementwise and pooling kernels alone at the
 first layer's activation shape.
 """
@@ -209,6 +214,8 @@ def main():
     ap.add_argument("--op-breakdown", action="store_true", help="print per-op times to stderr")
     ap.add_argument("--with-update", action="store_true",
                     help="apply the Adam + LARC parameter update inside every timed step")
+    ap.add_argument("--with-head", action="store_true",
+                    help="run the FC head + loss inside every step (its input gradient drives the backward pass)")
     ap.add_argument("--unfused", action="store_true",
                     help="run every layer through the unfused entry points (conv, bias + lReLU, pool separately)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
@@ -242,9 +249,20 @@ def main():
 
     hp = B.make_hparams(100000)  # the paper's constants; its decay length is not given
 
+    from paper_1808_04728_amd.head import FCHead
+    feats = int(np.prod(st.out_dhw)) * wl["layers"][-1]["cout"]
+    head = FCHead(wl["batch"], feats, inputs.HEAD_WIDTHS, wl["dtype"], inputs.ALPHA, "cuda:0")
+    head.set_params(*inputs.make_head(name, feats))
+    head_dout = head.dx[0].view(dout.shape)
+
     def step():
         st.forward()
-        st.backward(dout)
+        if args.with_head:
+            head.forward(st.output())
+            head.backward()
+            st.backward(head_dout)
+        else:
+            st.backward(dout)
         if args.with_update:
             st.update(hp)
 
@@ -277,6 +295,28 @@ def main():
     dom_ms = float(np.mean([a.elapsed_time(b) for a, b in st.timer[dominant]]))
     st.timer = None
 
+    # the FC head + loss alone (before any parameter update): forward and
+    # backward twice, queued behind a step so that the device never waits for
+    # the host to submit its ~25 short launches
+    hts = []
+    for _ in range(5):
+        step()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(2):
+            head.forward(st.output())
+            head.backward()
+        e1.record()
+        hts.append((e0, e1))
+    torch.cuda.synchronize()
+    head_ms = float(np.mean([a.elapsed_time(b) for a, b in hts])) / 2
+    head_bytes = head.weight_bytes()
+    head_gbs = head_bytes / (head_ms * 1e-3) / 1e9
+    head_res = dict(widths=[feats, *inputs.HEAD_WIDTHS], ms=round(head_ms, 4),
+                    algorithmic_bytes=head_bytes, achieved=round(head_gbs, 1), unit="GB/s", peak=HBM_PEAK_GBS,
+                    frac=round(head_gbs / HBM_PEAK_GBS, 4), in_step=args.with_head,
+                    loss=round(float(head.loss[0].item()), 6))
+
     # the parameter update alone, after the timed steps (it changes the weights):
     # K updates queued behind a step, so that the device never waits for the host
     # to submit the next one, bracketed by events
@@ -297,6 +337,7 @@ def main():
                   launch_ms=round(upd_ms, 4), algorithmic_bytes=upd_bytes, achieved=round(upd_gbs, 1),
                   unit="GB/s", peak=HBM_PEAK_GBS, frac=round(upd_gbs / HBM_PEAK_GBS, 4), in_step=args.with_update)
     update["paper_network_size"] = update_at_paper_size(step, B, np, torch, wl["dtype"] == "bf16")
+
     passes = hbm_passes(B, np, torch, wl)
 
     ms = wall * 1e3 / args.steps
@@ -329,7 +370,8 @@ def main():
         "dtype": wl["dtype"],
         "data": "synthetic",
         "config": {"workload": describe(name, wl) + (", unfused entry points" if args.unfused else "")
-                   + (", Adam + LARC update in every step" if args.with_update else ""),
+                   + (", Adam + LARC update in every step" if args.with_update else "")
+                   + (", FC head + loss in every step" if args.with_head else ""),
                    "name": name, "edge": wl["size"], "batch": wl["batch"],
                    "input_channels": wl["c0"], "conv_gflop_per_step": round(flops / 1e9, 3)},
         "samples_per_s": round(wl["batch"] / (ms * 1e-3), 2),
@@ -337,6 +379,7 @@ def main():
         "roofline": roof,
         "op_ms": {k: round(v, 4) for k, v in sorted(op_ms.items(), key=lambda kv: -kv[1])},
         "update": update,
+        "head": head_res,
         "hbm_passes": passes,
     }
     if not args.no_cpu_baseline:

@@ -29,6 +29,7 @@ namespace cf {
 namespace {
 
 constexpr int MB = 8;  // batch rows per pass (larger batches take several passes)
+constexpr int MH = 4;  // batch rows per LDS round of the forward's phase combine
 
 // ---- forward ------------------------------------------------------------
 // Thread t: column group cg = t % cgw (+ cgw, 2 cgw, ... while < cg_n),
@@ -40,7 +41,7 @@ __global__ __launch_bounds__(256) void fc_fwd_kernel(const typename Store<DT>::T
                                                      int cgw, int np, int kc) {
   constexpr int V = VECTOR ? Store<DT>::VEC : 1;
   __shared__ float xs[MB * 512];  // x[m0 + m][k0 + kk], kc <= 512
-  __shared__ float red[256 * V];  // [phase][column of the pass]
+  __shared__ float red[256 * MH * V];  // [phase][batch row][column of the pass] (np * cgw <= 256)
   const int tid = threadIdx.x;
   const int cg_n = N / V;
   const long long k0 = (long long)blockIdx.x * kc;
@@ -81,23 +82,38 @@ __global__ __launch_bounds__(256) void fc_fwd_kernel(const typename Store<DT>::T
         }
       }
     }
-    // combine the phases in phase order, one batch row at a time
+    // combine the phases in phase order, MH batch rows at a time: every (row,
+    // column) sum reads its np partials with eight loads in flight and adds
+    // them in order
     const int ncols = std::min(cgw, cg_n - cbase) * V;
+    const int rs = cgw * V;  // LDS row stride
 #pragma unroll
-    for (int m = 0; m < MB; ++m) {
-      if (m >= mcnt) break;
-      __syncthreads();
+    for (int h0 = 0; h0 < MB; h0 += MH) {
+      if (h0 >= mcnt) break;
       if (active)
 #pragma unroll
-        for (int j = 0; j < V; ++j) red[ph * (cgw * V) + c_in * V + j] = acc[m][j];
+        for (int m = 0; m < MH; ++m)
+#pragma unroll
+          for (int j = 0; j < V; ++j) red[(ph * MH + m) * rs + c_in * V + j] = acc[h0 + m][j];
       __syncthreads();
-      for (int col = tid; col < ncols; col += 256) {
+      const int hc = std::min(MH, mcnt - h0);
+      for (int q = tid; q < hc * ncols; q += 256) {
+        const int m = q / ncols, col = q - m * ncols;
+        const float *r = red + m * rs + col;
         float s = 0.f;
-        for (int p = 0; p < np; ++p) s += red[p * (cgw * V) + col];
-        prow[m * N + cbase * V + col] = s;
+        int p = 0;
+        for (; p + 8 <= np; p += 8) {
+          float v[8];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) v[u] = r[(p + u) * MH * rs];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) s += v[u];
+        }
+        for (; p < np; ++p) s += r[p * MH * rs];
+        prow[(h0 + m) * N + cbase * V + col] = s;
       }
+      __syncthreads();
     }
-    __syncthreads();
   }
 }
 
@@ -121,8 +137,8 @@ FwdPlan plan_fwd(int K, int N, int V) {
   const int cg_n = p.vec ? N / V : N;
   p.cgw = std::min(cg_n, 256);
   p.np = 256 / p.cgw;
-  // about 512 workgroups, at most 512 rows each
-  const long long target = ((long long)K + 511) / 512;
+  // about 256 workgroups (fewer partial rows to sum), at most 512 rows each
+  const long long target = ((long long)K + 255) / 256;
   long long u = std::max<long long>(1, (target + p.np - 1) / p.np);
   long long kc = std::min<long long>(u * p.np, 512);
   p.kc = (int)kc;
@@ -158,8 +174,10 @@ hipError_t fc_fwd_t(int M, int K, int N, const void *x, const void *w, void *y, 
 
 // ---- backward data --------------------------------------------------------
 // G lanes per row (a power of two, G >= the column groups when they fit one
-// wave); 256 / G rows per workgroup step.
-template <int DT, bool VECTOR>
+// wave); 256 / G rows per workgroup step.  When every lane owns at most one
+// column group (RESIDENT), its dz values for all batch rows are loaded once
+// and stay in registers across the rows it visits.
+template <int DT, bool VECTOR, bool RESIDENT>
 __global__ __launch_bounds__(256) void fc_bwd_data_kernel(const typename Store<DT>::T *__restrict__ dz,
                                                           const typename Store<DT>::T *__restrict__ w,
                                                           typename Store<DT>::T *__restrict__ dx, int m0, int mcnt,
@@ -168,31 +186,92 @@ __global__ __launch_bounds__(256) void fc_bwd_data_kernel(const typename Store<D
   const int tid = threadIdx.x;
   const int cg_n = N / V;
   const int gl = tid & (G - 1), rows_per = 256 / G;
-  for (long long k = (long long)blockIdx.x * rows_per + tid / G; k < K; k += (long long)gridDim.x * rows_per) {
+  // one batch row's dz for this lane's column group
+  auto load_dz = [&](int m, int cg, float *d) {
+    const typename Store<DT>::T *dr = dz + (long long)(m0 + m) * N + (long long)cg * V;
+    if constexpr (VECTOR) {
+      Vec16<DT> g;
+      g.u = ld16<false>(dr);
+#pragma unroll
+      for (int j = 0; j < V; ++j) d[j] = to_f32<DT>(g.e[j]);
+    } else {
+      d[0] = to_f32<DT>(dr[0]);
+    }
+  };
+  auto load_w = [&](long long k, int cg, float *wv) {
+    if constexpr (VECTOR) {
+      Vec16<DT> v;
+      v.u = ld16<false>(w + k * N + (long long)cg * V);
+#pragma unroll
+      for (int j = 0; j < V; ++j) wv[j] = to_f32<DT>(v.e[j]);
+    } else {
+      wv[0] = to_f32<DT>(w[k * N + cg]);
+    }
+  };
+  float dzr[RESIDENT ? MB : 1][V];
+  if constexpr (RESIDENT) {
+#pragma unroll
+    for (int m = 0; m < MB; ++m) {
+      if (m < mcnt && gl < cg_n) {
+        load_dz(m, gl, dzr[m]);
+      } else {
+#pragma unroll
+        for (int j = 0; j < V; ++j) dzr[m][j] = 0.f;
+      }
+    }
+  }
+  const long long kstep = (long long)gridDim.x * rows_per;
+  long long k = (long long)blockIdx.x * rows_per + tid / G;
+  if constexpr (RESIDENT) {
+    // four rows per iteration, their W loads issued together
+    for (; k + 3 * kstep < K; k += 4 * kstep) {
+      float wv[4][V];
+      if (gl < cg_n)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) load_w(k + u * kstep, gl, wv[u]);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        float acc[MB];
+#pragma unroll
+        for (int m = 0; m < MB; ++m) acc[m] = 0.f;
+        if (gl < cg_n)
+#pragma unroll
+          for (int m = 0; m < MB; ++m)
+#pragma unroll
+            for (int j = 0; j < V; ++j) acc[m] = fmaf(dzr[m][j], wv[u][j], acc[m]);
+        for (int off = G >> 1; off > 0; off >>= 1)
+#pragma unroll
+          for (int m = 0; m < MB; ++m) acc[m] += __shfl_xor(acc[m], off, 64);
+#pragma unroll
+        for (int m = 0; m < MB; ++m)
+          if (m < mcnt && gl == m % G) dx[(long long)(m0 + m) * K + k + u * kstep] = from_f32<DT>(acc[m]);
+      }
+    }
+  }
+  for (; k < K; k += kstep) {
     float acc[MB];
 #pragma unroll
     for (int m = 0; m < MB; ++m) acc[m] = 0.f;
-    for (int cg = gl; cg < cg_n; cg += G) {
-      float wv[V];
-      if constexpr (VECTOR) {
-        Vec16<DT> v;
-        v.u = ld16<false>(w + k * N + (long long)cg * V);
+    if constexpr (RESIDENT) {
+      if (gl < cg_n) {
+        float wv[V];
+        load_w(k, gl, wv);
 #pragma unroll
-        for (int j = 0; j < V; ++j) wv[j] = to_f32<DT>(v.e[j]);
-      } else {
-        wv[0] = to_f32<DT>(w[k * N + cg]);
+        for (int m = 0; m < MB; ++m)
+#pragma unroll
+          for (int j = 0; j < V; ++j) acc[m] = fmaf(dzr[m][j], wv[j], acc[m]);
       }
+    } else {
+      for (int cg = gl; cg < cg_n; cg += G) {
+        float wv[V];
+        load_w(k, cg, wv);
 #pragma unroll
-      for (int m = 0; m < MB; ++m) {
-        if (m < mcnt) {
-          const typename Store<DT>::T *dr = dz + (long long)(m0 + m) * N + (long long)cg * V;
-          if constexpr (VECTOR) {
-            Vec16<DT> g;
-            g.u = ld16<false>(dr);
+        for (int m = 0; m < MB; ++m) {
+          if (m < mcnt) {
+            float d[V];
+            load_dz(m, cg, d);
 #pragma unroll
-            for (int j = 0; j < V; ++j) acc[m] = fmaf(to_f32<DT>(g.e[j]), wv[j], acc[m]);
-          } else {
-            acc[m] = fmaf(to_f32<DT>(dr[0]), wv[0], acc[m]);
+            for (int j = 0; j < V; ++j) acc[m] = fmaf(d[j], wv[j], acc[m]);
           }
         }
       }
@@ -214,16 +293,27 @@ hipError_t fc_bwd_data_t(int M, int K, int N, const void *dz, const void *w, voi
   const int cg_n = vec ? N / Store<DT>::VEC : N;
   int G = 1;
   while (G < cg_n && G < 64) G <<= 1;
+  const bool res = cg_n <= G;
   const int rows_per = 256 / G;
-  const int blocks = (int)std::min<long long>(((long long)K + rows_per - 1) / rows_per, 4096);
+  // one row per thread for short matrices; about four per thread for long
+  // ones when dz is register-resident
+  const long long want = ((long long)K + rows_per - 1) / rows_per;
+  const int blocks = (int)std::min<long long>(res ? std::max(std::min<long long>(want, 1024), (want + 3) / 4) : want,
+                                              4096);
   for (int m0 = 0; m0 < M; m0 += MB) {
     const int mcnt = std::min(MB, M - m0);
-    if (vec)
-      hipLaunchKernelGGL((fc_bwd_data_kernel<DT, true>), dim3(blocks), dim3(256), 0, st, (const T *)dz,
-                         (const T *)w, (T *)dx, m0, mcnt, K, N, G);
+#define CF_FC_BWD_DATA(VEC_, RES_)                                                                                \
+  hipLaunchKernelGGL((fc_bwd_data_kernel<DT, VEC_, RES_>), dim3(blocks), dim3(256), 0, st, (const T *)dz,            \
+                     (const T *)w, (T *)dx, m0, mcnt, K, N, G)
+    if (vec && res)
+      CF_FC_BWD_DATA(true, true);
+    else if (vec)
+      CF_FC_BWD_DATA(true, false);
+    else if (res)
+      CF_FC_BWD_DATA(false, true);
     else
-      hipLaunchKernelGGL((fc_bwd_data_kernel<DT, false>), dim3(blocks), dim3(256), 0, st, (const T *)dz,
-                         (const T *)w, (T *)dx, m0, mcnt, K, N, G);
+      CF_FC_BWD_DATA(false, false);
+#undef CF_FC_BWD_DATA
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -257,18 +347,86 @@ __global__ __launch_bounds__(256) void fc_bwd_weight_kernel(const typename Store
   }
 }
 
+// Blocked form for N % 4 == 0: thread = (8 consecutive rows kb .. kb+7,
+// column quad c .. c+3).  Per batch row one load of 4 dz values and one
+// 16-byte load of x[m][kb .. kb+7] (bf16; two for fp32) when K % 8 == 0,
+// else guarded element loads; 32 outputs summed over m in order.
+template <int DT, bool XVEC>
+__global__ __launch_bounds__(256) void fc_bwd_weight_blk_kernel(const typename Store<DT>::T *__restrict__ x,
+                                                                const typename Store<DT>::T *__restrict__ dz,
+                                                                float *__restrict__ dw, int M, int K, int N,
+                                                                long long items) {
+  const int gq = N / 4;
+  for (long long i = (long long)blockIdx.x * 256 + threadIdx.x; i < items; i += (long long)gridDim.x * 256) {
+    const long long kb = (i / gq) * 8;
+    const int c = (int)(i - (i / gq) * gq) * 4;
+    const int kn = (int)std::min<long long>(8, K - kb);
+    float acc[8][4];
+#pragma unroll
+    for (int r = 0; r < 8; ++r)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[r][j] = 0.f;
+    for (int m = 0; m < M; ++m) {
+      float d[4];
+      const typename Store<DT>::T *dr = dz + (long long)m * N + c;
+      if constexpr (DT == DT_BF16) {
+        const uint2 u = *reinterpret_cast<const uint2 *>(dr);
+        d[0] = __uint_as_float(u.x << 16); d[1] = __uint_as_float(u.x & 0xffff0000u);
+        d[2] = __uint_as_float(u.y << 16); d[3] = __uint_as_float(u.y & 0xffff0000u);
+      } else {
+        const float4 f = *reinterpret_cast<const float4 *>(dr);
+        d[0] = f.x; d[1] = f.y; d[2] = f.z; d[3] = f.w;
+      }
+      float xv[8];
+      const typename Store<DT>::T *xr = x + (long long)m * K + kb;
+      if constexpr (XVEC) {
+        if constexpr (DT == DT_BF16) {
+          Vec16<DT_BF16> v;
+          v.u = ld16<false>(xr);
+#pragma unroll
+          for (int r = 0; r < 8; ++r) xv[r] = bf2f(v.e[r]);
+        } else {
+          const float4 a = *reinterpret_cast<const float4 *>(xr);
+          const float4 b = *reinterpret_cast<const float4 *>(xr + 4);
+          xv[0] = a.x; xv[1] = a.y; xv[2] = a.z; xv[3] = a.w;
+          xv[4] = b.x; xv[5] = b.y; xv[6] = b.z; xv[7] = b.w;
+        }
+      } else {
+#pragma unroll
+        for (int r = 0; r < 8; ++r) {
+          xv[r] = 0.f;
+          if (r < kn) xv[r] = to_f32<DT>(xr[r]);
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < 8; ++r)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[r][j] = fmaf(xv[r], d[j], acc[r][j]);
+    }
+#pragma unroll
+    for (int r = 0; r < 8; ++r)
+      if (r < kn) *reinterpret_cast<float4 *>(dw + (kb + r) * N + c) = make_float4(acc[r][0], acc[r][1], acc[r][2], acc[r][3]);
+  }
+}
+
 template <int DT>
 hipError_t fc_bwd_weight_t(int M, int K, int N, const void *x, const void *dz, float *dw, hipStream_t st) {
   using T = typename Store<DT>::T;
-  const bool vec = N % 4 == 0;
-  const long long items = (long long)K * (vec ? N / 4 : N);
+  if (N % 4 == 0) {
+    const long long items = ((long long)K + 7) / 8 * (N / 4);
+    const int blocks = (int)std::min<long long>((items + 255) / 256, 256LL * 64);
+    if (K % 8 == 0)
+      hipLaunchKernelGGL((fc_bwd_weight_blk_kernel<DT, true>), dim3(blocks), dim3(256), 0, st, (const T *)x,
+                         (const T *)dz, dw, M, K, N, items);
+    else
+      hipLaunchKernelGGL((fc_bwd_weight_blk_kernel<DT, false>), dim3(blocks), dim3(256), 0, st, (const T *)x,
+                         (const T *)dz, dw, M, K, N, items);
+    return hipGetLastError();
+  }
+  const long long items = (long long)K * N;
   const int blocks = (int)std::min<long long>((items + 255) / 256, 256LL * 64);
-  if (vec)
-    hipLaunchKernelGGL((fc_bwd_weight_kernel<DT, true>), dim3(blocks), dim3(256), 0, st, (const T *)x,
-                       (const T *)dz, dw, M, K, N, items);
-  else
-    hipLaunchKernelGGL((fc_bwd_weight_kernel<DT, false>), dim3(blocks), dim3(256), 0, st, (const T *)x,
-                       (const T *)dz, dw, M, K, N, items);
+  hipLaunchKernelGGL((fc_bwd_weight_kernel<DT, false>), dim3(blocks), dim3(256), 0, st, (const T *)x, (const T *)dz,
+                     dw, M, K, N, items);
   return hipGetLastError();
 }
 

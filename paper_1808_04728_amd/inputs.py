@@ -137,6 +137,30 @@ def make_weights(name: str):
     return ws, bs
 
 
+#: widths of the fully-connected head (Section III-A: three FC layers, three
+#: outputs; the first two widths are in the paper's missing Fig. 2 -- a reading)
+HEAD_WIDTHS = (128, 64, 3)
+
+#: parameter ranges of the simulations (Section IV-C): Omega_M, sigma_8, n_s
+PARAM_RANGES = ((0.25, 0.35), (0.78, 0.95), (0.9, 1.0))
+
+
+def make_head(name: str, features: int, widths=HEAD_WIDTHS):
+    """He-normal FC weights [in][out] (seed 40000 + 100 cfg + layer), zero
+    biases, and per-sample targets drawn uniformly from the simulations'
+    parameter ranges (seed 50000 + cfg)."""
+    wl = WORKLOADS[name]
+    dims = [features, *widths]
+    ws, bs = [], []
+    for i in range(len(widths)):
+        rng = np.random.Generator(np.random.PCG64(40000 + 100 * wl["cfg"] + i))
+        ws.append((rng.standard_normal((dims[i], dims[i + 1])) * np.sqrt(2.0 / dims[i])).astype(np.float32))
+        bs.append(np.zeros(dims[i + 1], np.float32))
+    rng = np.random.Generator(np.random.PCG64(50000 + wl["cfg"]))
+    tgt = np.stack([rng.uniform(lo, hi, wl["batch"]) for lo, hi in PARAM_RANGES], 1).astype(np.float32)
+    return ws, bs, tgt
+
+
 def normal(shape, seed: int, scale: float = 1.0) -> np.ndarray:
     rng = np.random.Generator(np.random.PCG64(seed))
     return (rng.standard_normal(shape) * scale).astype(np.float32)

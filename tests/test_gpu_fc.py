@@ -21,8 +21,11 @@ from tests._util import TOL, dev, maxabs_err, tdtype, to_np
 pytestmark = pytest.mark.gpu
 
 DTYPES = ["f32", "bf16"]
+# (m, k, n): scalar columns (n = 1, 5, 3), vector columns with k a multiple of
+# 8 or not, more than 8 batch rows, more column groups than one row group of
+# 64 lanes (n = 1040) and than one forward pass of 256 threads (n = 2056)
 SHAPES = [(1, 1, 1), (3, 37, 5), (8, 1000, 128), (5, 2049, 64), (13, 300, 24), (8, 64, 3), (2, 70001, 16),
-          (8, 65536, 128)]
+          (3, 100, 1040), (2, 40, 2056), (4, 70001, 128), (8, 65536, 128)]
 
 
 def fwd(m, k, n, dt, x, w):
