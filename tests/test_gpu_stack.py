@@ -97,8 +97,9 @@ def sample_idx(rng, shape, n):
     return np.stack([rng.integers(0, t, n) for t in shape], 1)
 
 
-@pytest.mark.parametrize("name,fused", [("stack_128c_b1_f32", True), ("stack_128c_b8_bf16", True),
-                                        ("stack_128c_b8_bf16", False), ("paper_c1c3_128_b8_bf16", True)])
+@pytest.mark.parametrize("name,fused", [("layer1_32c", True), ("stack_128c_b1_f32", True), ("stack_128c_b8_bf16", True),
+                                        ("stack_128c_b8_bf16", False), ("paper_c1c3_128_b8_bf16", True),
+                                        ("stack_256c4_b2_bf16", True)])
 def test_full_size_sampled(name, fused):
     """At the workloads' full sizes, in the launch configuration the benchmark
     times (fused) and through the unfused entry points."""
