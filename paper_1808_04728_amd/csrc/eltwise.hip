@@ -152,12 +152,14 @@ __global__ __launch_bounds__(256) void bias_lrelu_bwd_kernel(const typename Stor
 }
 
 // One pass over whole 16-byte vectors with 32-bit offsets, for c / V a power
-// of two up to 64 and c <= 256: workgroup b takes the U * 256 consecutive
-// vectors from b * U * 256, thread t the ones at t, t + 256, ... (all of
-// channel group t % (c / V), since c / V divides 256).  The bias-gradient
-// partial of the workgroup: each thread sums its vectors in order, a fixed
-// butterfly over the lanes of a wave that share a channel group, then the
-// four waves as (w0 + w1) + (w2 + w3).
+// of two up to 64 and c <= 256: workgroup b takes the chunks of U * 256
+// consecutive vectors starting at (b + i * gridDim) * U * 256, thread t the
+// vectors t, t + 256, ... of each chunk (all of channel group t % (c / V),
+// since c / V divides 256), its U loads of a chunk issued together.  The
+// bias-gradient partial of the workgroup: each thread sums its vectors in
+// order, a fixed butterfly over the lanes of a wave that share a channel
+// group, then the four waves as (w0 + w1) + (w2 + w3).  Looping over chunks
+// keeps the number of workgroups, and so of partial rows to sum, small.
 template <int DT, bool WITH_DB, int U, bool NT>
 __global__ __launch_bounds__(256) void bias_lrelu_bwd_vec_kernel(const typename Store<DT>::T *__restrict__ dy,
                                                                  const typename Store<DT>::T *__restrict__ y,
@@ -166,28 +168,29 @@ __global__ __launch_bounds__(256) void bias_lrelu_bwd_vec_kernel(const typename 
   constexpr int V = Store<DT>::VEC;
   __shared__ float red[4 * 256];
   const int tid = threadIdx.x;
-  const int k0 = (int)blockIdx.x * (256 * U) + tid;
-  Vec16<DT> g[U], o[U];
-#pragma unroll
-  for (int u = 0; u < U; ++u)
-    if (k0 + 256 * u < nv) {
-      g[u].u = ld16<NT>(dy + V * (k0 + 256 * u));
-      o[u].u = ld16<NT>(y + V * (k0 + 256 * u));
-    }
   float s[V];
 #pragma unroll
   for (int j = 0; j < V; ++j) s[j] = 0.f;
+  for (int k0 = (int)blockIdx.x * (256 * U) + tid; k0 < nv; k0 += (int)gridDim.x * (256 * U)) {
+    Vec16<DT> g[U], o[U];
 #pragma unroll
-  for (int u = 0; u < U; ++u)
-    if (k0 + 256 * u < nv) {
-#pragma unroll
-      for (int j = 0; j < V; ++j) {
-        const float d = to_f32<DT>(g[u].e[j]) * (to_f32<DT>(o[u].e[j]) > 0.f ? 1.f : alpha);
-        s[j] += d;
-        g[u].e[j] = from_f32<DT>(d);
+    for (int u = 0; u < U; ++u)
+      if (k0 + 256 * u < nv) {
+        g[u].u = ld16<NT>(dy + V * (k0 + 256 * u));
+        o[u].u = ld16<NT>(y + V * (k0 + 256 * u));
       }
-      st16<NT>(dz + V * (k0 + 256 * u), g[u].u);
-    }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (k0 + 256 * u < nv) {
+#pragma unroll
+        for (int j = 0; j < V; ++j) {
+          const float d = to_f32<DT>(g[u].e[j]) * (to_f32<DT>(o[u].e[j]) > 0.f ? 1.f : alpha);
+          s[j] += d;
+          g[u].e[j] = from_f32<DT>(d);
+        }
+        st16<NT>(dz + V * (k0 + 256 * u), g[u].u);
+      }
+  }
   if constexpr (WITH_DB) {
     for (int off = cg_n; off < 64; off <<= 1)
 #pragma unroll
@@ -219,8 +222,10 @@ BwdPlan plan_bwd(long long nvox, int c, int V) {
   const int cg_n = c / V;
   if (c % V == 0 && (cg_n & (cg_n - 1)) == 0 && cg_n <= 64 && c <= 256 && nvox * c < (1LL << 31)) {
     const long long nv = nvox * cg_n;
-    p.unroll = nv >= (1LL << 22) ? 4 : 1;
+    // large tensors: four vectors per thread and chunk, at most 1024 workgroups
+    p.unroll = nv >= (1LL << 20) ? 4 : 1;
     p.blocks = (int)((nv + 256LL * p.unroll - 1) / (256LL * p.unroll));
+    if (p.unroll == 4) p.blocks = std::min(p.blocks, 1024);
     return p;
   }
   long long vpb = std::max<long long>(64, (nvox + 2047) / 2048);
