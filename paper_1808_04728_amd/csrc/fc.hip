@@ -11,8 +11,8 @@
 // pass is recast as a GEMM tile for the matrix cores.
 //   forward        split over K: workgroup b sums rows [b KC, (b+1) KC) of
 //                  W for all M x N outputs (its phases combined in LDS in
-//                  phase order), one partial row per workgroup, then the
-//                  fixed-order column sum of the partials;
+//                  phase order), one partial row per workgroup, then a
+//                  fixed-order column sum of the partials rounded once;
 //   backward data  one group of G lanes per row k of W: each lane dots its
 //                  columns with dz, a lane butterfly completes the row;
 //   backward wts   one thread per (k, 4 columns) of dW: sum over the batch
@@ -62,7 +62,7 @@ __global__ __launch_bounds__(256) void fc_fwd_kernel(const typename Store<DT>::T
 #pragma unroll
       for (int j = 0; j < V; ++j) acc[m][j] = 0.f;
     if (active) {
-#pragma unroll 4
+#pragma unroll 8
       for (int kk = ph; kk < krows; kk += np) {
         const typename Store<DT>::T *wr = w + (k0 + kk) * N + (long long)cg * V;
         float wv[V];
@@ -117,13 +117,35 @@ __global__ __launch_bounds__(256) void fc_fwd_kernel(const typename Store<DT>::T
   }
 }
 
-// y[m0 + m][j] = RNE(sum over workgroups), from the fp32 column sums
+// y[m0 + i] = RNE(sum over the rows of the partial matrix [rows][cols]):
+// 16 columns per workgroup, 16 row phases per column (phase p sums rows p,
+// p + 16, ... in order, eight loads in flight), phases combined in order.
 template <int DT>
-__global__ __launch_bounds__(256) void fc_store_kernel(const float *__restrict__ s, typename Store<DT>::T *y, int m0,
-                                                       int mcnt, int N) {
-  const int i = (int)blockIdx.x * 256 + threadIdx.x;
-  if (i >= mcnt * N) return;
-  y[(long long)m0 * N + i] = from_f32<DT>(s[i]);
+__global__ __launch_bounds__(256) void fc_finalize_kernel(const float *__restrict__ part, int rows, int cols,
+                                                          typename Store<DT>::T *y) {
+  __shared__ float red[16][16];
+  const int tid = threadIdx.x, cl = tid & 15, ph = tid >> 4;
+  const int col = (int)blockIdx.x * 16 + cl;
+  float s = 0.f;
+  if (col < cols) {
+    int r = ph;
+    for (; r + 7 * 16 < rows; r += 8 * 16) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = part[(long long)(r + 16 * u) * cols + col];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) s += v[u];
+    }
+    for (; r < rows; r += 16) s += part[(long long)r * cols + col];
+  }
+  red[ph][cl] = s;
+  __syncthreads();
+  if (ph == 0 && col < cols) {
+    float t = 0.f;
+#pragma unroll
+    for (int p = 0; p < 16; ++p) t += red[p][cl];
+    y[col] = from_f32<DT>(t);
+  }
 }
 
 struct FwdPlan {
@@ -137,8 +159,8 @@ FwdPlan plan_fwd(int K, int N, int V) {
   const int cg_n = p.vec ? N / V : N;
   p.cgw = std::min(cg_n, 256);
   p.np = 256 / p.cgw;
-  // about 256 workgroups (fewer partial rows to sum), at most 512 rows each
-  const long long target = ((long long)K + 255) / 256;
+  // about 512 workgroups, at most 512 rows each
+  const long long target = ((long long)K + 511) / 512;
   long long u = std::max<long long>(1, (target + p.np - 1) / p.np);
   long long kc = std::min<long long>(u * p.np, 512);
   p.kc = (int)kc;
@@ -151,7 +173,6 @@ hipError_t fc_fwd_t(int M, int K, int N, const void *x, const void *w, void *y, 
   using T = typename Store<DT>::T;
   const FwdPlan pl = plan_fwd(K, N, Store<DT>::VEC);
   float *part = (float *)ws;
-  float *sum = part + (size_t)pl.blocks * MB * N;
   for (int m0 = 0; m0 < M; m0 += MB) {
     const int mcnt = std::min(MB, M - m0);
     if (pl.vec)
@@ -162,10 +183,8 @@ hipError_t fc_fwd_t(int M, int K, int N, const void *x, const void *w, void *y, 
                          part, m0, mcnt, K, N, pl.cgw, pl.np, pl.kc);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    e = launch_sum_rows(part, sum, pl.blocks, mcnt * N, st);
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((fc_store_kernel<DT>), dim3((mcnt * N + 255) / 256), dim3(256), 0, st, sum, (T *)y, m0, mcnt,
-                       N);
+    hipLaunchKernelGGL((fc_finalize_kernel<DT>), dim3((mcnt * N + 15) / 16), dim3(256), 0, st, part, pl.blocks,
+                       mcnt * N, (T *)y + (size_t)m0 * N);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -459,7 +478,7 @@ size_t fc_fwd_workspace(int M, int K, int N) {
   if (M <= 0 || K <= 0 || N <= 0) return 0;
   const FwdPlan a = plan_fwd(K, N, 8), b = plan_fwd(K, N, 4);
   const int blocks = std::max(a.blocks, b.blocks);
-  return ((size_t)blocks * MB * N + (size_t)MB * N) * sizeof(float);
+  return (size_t)blocks * MB * N * sizeof(float);
 }
 
 hipError_t launch_fc_fwd(int M, int K, int N, int dtype, const void *x, const void *w, void *y, void *ws,
