@@ -32,12 +32,16 @@ def _t(dtype):
 
 class ConvStack:
     def __init__(self, layers, size, batch, dtype="f32", alpha=0.01, device="cuda", skip_first_dgrad=True,
-                 fused=True, defer_reductions=True):
+                 fused=True, defer_reductions=True, overlap_wgrad=True):
         """fused: run a pooled layer through the fused entry points (forward
         epilogue writes pooled output + slope mask; backward rebuilds dz from
         them) wherever the library has fused kernels for the layer.
         defer_reductions: batch all gradient sums of a backward pass into one
-        cf_reduce_partials launch."""
+        cf_reduce_partials launch.
+        overlap_wgrad: in the backward pass of an unfused layer, run the weight
+        gradient on a second stream (default priority) concurrently with the
+        data gradient; both only read dz, and the small deep layers leave most
+        of the GPU idle when run one after the other."""
         self.fused = fused
         self.defer_reductions = defer_reductions
         self.reduce_bytes = 0
@@ -50,6 +54,8 @@ class ConvStack:
         self.skip_first_dgrad = skip_first_dgrad
         self.timer = None  # optional: {op name: [(start event, end event), ...]}
         self.timed_ops = None  # None = every op, else the set of op names to time
+        import torch as _torch
+        self.side = _torch.cuda.Stream(device=device) if overlap_wgrad else None
         self.L = []
         dhw = (size, size, size)
         for i, spec in enumerate(layers):
@@ -185,15 +191,17 @@ class ConvStack:
         l = self.L[-1]
         return l["p"] if l["spec"]["pool"] else l["z"]
 
-    def _call(self, name, fn, *args):
+    def _call(self, name, fn, *args, rec=None):
+        """fn(*args), bracketed by timing events on stream rec (None: the
+        current stream) when the op is timed."""
         if self.timer is None or (self.timed_ops is not None and name not in self.timed_ops):
             return fn(*args)
         import torch as _torch
         e0 = _torch.cuda.Event(enable_timing=True)
         e1 = _torch.cuda.Event(enable_timing=True)
-        e0.record()
+        e0.record(rec)
         r = fn(*args)
-        e1.record()
+        e1.record(rec)
         self.timer.setdefault(name, []).append((e0, e1))
         return r
 
@@ -234,6 +242,7 @@ class ConvStack:
         g = dout
         pend = []
         d = self.defer_reductions
+        side_used = False
         for i in range(len(self.L) - 1, -1, -1):
             l = self.L[i]
             s = l["spec"]
@@ -270,19 +279,36 @@ class ConvStack:
                 dy = l["dy"]
             else:
                 dy = g
+            # weight gradient on the side stream when a data gradient follows
+            ws_ = stream
+            if self.side is not None and l["dx"] is not None:
+                main = stream if stream is not None else torch.cuda.current_stream()
+                ev = torch.cuda.Event()
             if d:
                 pend += c(f"L{i+1}.bias_lrelu_bwd", B.cf_bias_lrelu_bwd_deferred, l["nvox"], s["cout"], self.dtype,
                           dy, l["z"], self.alpha, l["dz"], l["db"], l["ws_b"], None, stream)
-                pend += c(f"L{i+1}.conv_bwd_weight", B.cf_conv3d_bwd_weight_deferred, l["desc"],
-                          self.layer_input(i), l["dz"], l["dw"], l["ws_w"], None, stream)
             else:
                 c(f"L{i+1}.bias_lrelu_bwd", B.cf_bias_lrelu_bwd, l["nvox"], s["cout"], self.dtype, dy, l["z"],
                   self.alpha, l["dz"], l["db"], l["ws_b"], None, stream)
+            if self.side is not None and l["dx"] is not None:
+                ev.record(main)
+                self.side.wait_event(ev)
+                ws_ = self.side
+                side_used = True
+            if d:
+                pend += c(f"L{i+1}.conv_bwd_weight", B.cf_conv3d_bwd_weight_deferred, l["desc"],
+                          self.layer_input(i), l["dz"], l["dw"], l["ws_w"], None, ws_, rec=ws_)
+            else:
                 c(f"L{i+1}.conv_bwd_weight", B.cf_conv3d_bwd_weight, l["desc"], self.layer_input(i), l["dz"],
-                  l["dw"], l["ws_w"], None, stream)
+                  l["dw"], l["ws_w"], None, ws_, rec=ws_)
             if l["dx"] is not None:
                 c(f"L{i+1}.conv_bwd_data", B.cf_conv3d_bwd_data, l["desc"], l["dz"], l["w"], l["dx"], stream)
                 g = l["dx"]
+        if side_used:
+            # join: everything after the backward pass sees the weight gradients
+            ev = torch.cuda.Event()
+            ev.record(self.side)
+            (stream if stream is not None else torch.cuda.current_stream()).wait_event(ev)
         if pend:
             self.reduce_bytes = sum(j.rows * j.cols * 4 + j.cols * 4 for j in pend)
             self._call("L0.reduce_partials", B.cf_reduce_partials, pend, stream)
