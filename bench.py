@@ -222,8 +222,9 @@ def main():
                     help="only run 5 plain device copies of MIB MiB (calibrates the HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path (data-parallel sharding is "
-              "described in DESIGN.md, not implemented); run with --gpus 1", file=sys.stderr)
+        print("bench.py measures one GPU: the library has no multi-GPU path (the step would shard "
+              "data-parallel, with one allreduce of the weight and bias gradients per step, which is not "
+              "implemented); run with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np

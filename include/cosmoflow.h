@@ -164,7 +164,7 @@ cf_status cf_avgpool3d_bwd(int32_t n, int32_t d, int32_t h, int32_t w, int32_t c
 /* flags */
 #define CF_FUSE_POOL2 1u /* a 2^3 stride-2 average pool follows the activation */
 
-/* Bitmask of the fused entry points that accept (desc, flags) on this build:
+/* Bitmask of the fused entry points of this library that accept (desc, flags):
  * 1 = cf_conv3d_fwd_fused, 2 = cf_conv3d_bwd_weight_fused,
  * 4 = cf_conv3d_bwd_data_fused, 8 = cf_conv3d_bwd_weight_fused_dz.
  * Host-only; 0 on an invalid desc. */
