@@ -247,6 +247,11 @@ class ConvStack:
             l = self.L[i]
             s = l["spec"]
             c = self._call
+            if l["fused"] and side_used:
+                # the fused layers' kernels fill the GPU by themselves: they start
+                # after the side stream's weight gradients have finished
+                self._join_side(stream)
+                side_used = False
             if l["fused"] and l["dz_emit"]:
                 if d:
                     pend += c(f"L{i+1}.conv_bwd_weight_fused_dz", B.cf_conv3d_bwd_weight_fused_deferred, l["desc"],
@@ -306,12 +311,17 @@ class ConvStack:
                 g = l["dx"]
         if side_used:
             # join: everything after the backward pass sees the weight gradients
-            ev = torch.cuda.Event()
-            ev.record(self.side)
-            (stream if stream is not None else torch.cuda.current_stream()).wait_event(ev)
+            self._join_side(stream)
         if pend:
             self.reduce_bytes = sum(j.rows * j.cols * 4 + j.cols * 4 for j in pend)
             self._call("L0.reduce_partials", B.cf_reduce_partials, pend, stream)
+
+    def _join_side(self, stream):
+        """Work queued on `stream` (None: the current stream) after this call
+        waits for everything queued on the side stream so far."""
+        ev = torch.cuda.Event()
+        ev.record(self.side)
+        (stream if stream is not None else torch.cuda.current_stream()).wait_event(ev)
 
     def layer_input(self, i):
         if i == 0:
