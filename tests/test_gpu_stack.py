@@ -156,3 +156,29 @@ def test_full_size_sampled(name, fused):
             scale = np.abs(to_np(l["dx"])).max()
             assert np.abs(got - ref).max() <= TOL[dt] * scale, ("dgrad", i)
             g = l["dx"]
+
+
+@pytest.mark.parametrize("name", ["stack_128c_b8_bf16", "stack_64c_b1_f32"])
+def test_two_stream_backward_is_bitwise_identical(name):
+    """The deep layers' weight gradients on a second stream give the same bits
+    as the single-stream step (every kernel's result is independent of what
+    runs beside it), over two steps in a row."""
+    wl = inputs.WORKLOADS[name]
+    ws, bs = inputs.make_weights(name)
+    x = inputs.make_input(name)
+    outs = []
+    for overlap in (True, False):
+        st = ConvStack(wl["layers"], wl["size"], wl["batch"], wl["dtype"], inputs.ALPHA, "cuda", overlap_wgrad=overlap)
+        st.set_params(ws, bs)
+        st.set_input(x)
+        dout = torch.as_tensor(inputs.normal((wl["batch"],) + st.out_dhw + (wl["layers"][-1]["cout"],),
+                                             30000 + wl["cfg"]), device="cuda").to(st.tdt)
+        for _ in range(2):
+            st.forward()
+            st.backward(dout)
+        torch.cuda.synchronize()
+        outs.append([(l["dw"].clone(), l["db"].clone(), None if l["dx"] is None else l["dx"].clone()) for l in st.L])
+        del st
+    for (a_dw, a_db, a_dx), (b_dw, b_db, b_dx) in zip(*outs):
+        assert torch.equal(a_dw, b_dw) and torch.equal(a_db, b_db)
+        assert (a_dx is None and b_dx is None) or torch.equal(a_dx, b_dx)
