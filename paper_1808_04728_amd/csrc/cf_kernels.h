@@ -11,6 +11,13 @@
 
 namespace cf {
 
+// Compute units of a gfx950 device (MI350X / MI355X: 8 XCDs x 32 CUs).  The
+// library is built for gfx950 only, so persistent grids are sized from this
+// constant instead of a per-launch device query; on a partitioned device with
+// fewer CUs the same grid simply queues more workgroups per CU (same results:
+// no partition of work or summation order depends on it).
+constexpr int kNumCUs = 256;
+
 // Fully resolved geometry of one convolution layer.
 struct ConvShape {
   int n, d, h, w;        // input extent

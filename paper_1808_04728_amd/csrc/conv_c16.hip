@@ -61,7 +61,7 @@ __global__ __launch_bounds__(512, 1) void conv_c16_fwd_kernel(const uint16_t *__
                                                               uint16_t *__restrict__ out,
                                                               uint32_t *__restrict__ mask, C16Params p) {
   using G = C16<KE>;
-  extern __shared__ __attribute__((aligned(16))) uint4 smem[];
+  __shared__ __attribute__((aligned(16))) uint4 smem[(G::LDS_BYTES + 15) / 16];
   uint4 *halo = smem;                 // [HD][HH][2][HW] (+ padding to whole DMA chunks)
   uint4 *wp = smem + G::HALO_PAD;     // [TAPS][2][32]
 
@@ -308,19 +308,10 @@ template <int KE, int EPI, bool AMAX>
 hipError_t launch_t(const C16Params &p, const void *x, const void *w, const float *bias, float alpha, void *out,
                     uint32_t *mask, hipStream_t st) {
   using G = C16<KE>;
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void *)conv_c16_fwd_kernel<KE, EPI, AMAX>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, G::LDS_BYTES);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
-  int dev = 0, cus = 256;
-  if (hipGetDevice(&dev) == hipSuccess) hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   const long long tiles = (long long)p.n * ((p.od + TD - 1) / TD) * ((p.oh + TH - 1) / TH) * ((p.ow + TW - 1) / TW);
-  int blocks = (int)std::min<long long>(tiles, cus);
+  int blocks = (int)std::min<long long>(tiles, kNumCUs);
   blocks = std::max(8, (blocks + 7) / 8 * 8);
-  hipLaunchKernelGGL((conv_c16_fwd_kernel<KE, EPI, AMAX>), dim3(blocks), dim3(64 * NWAVE), G::LDS_BYTES, st,
+  hipLaunchKernelGGL((conv_c16_fwd_kernel<KE, EPI, AMAX>), dim3(blocks), dim3(64 * NWAVE), 0, st,
                      (const uint16_t *)x, (const uint16_t *)w, bias, alpha, (uint16_t *)out, mask, p);
   return hipGetLastError();
 }

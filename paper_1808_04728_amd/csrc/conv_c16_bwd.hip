@@ -90,7 +90,7 @@ __global__ __launch_bounds__(256, 2) void c16_dgrad_kernel(const uint16_t *__res
                                                            const uint16_t *__restrict__ w, float alpha,
                                                            uint16_t *__restrict__ dx, C16Params p) {
   using G = C16B<KE, FUSED>;
-  extern __shared__ __attribute__((aligned(16))) uint4 smem[];
+  __shared__ __attribute__((aligned(16))) uint4 smem[(G::LDS_BYTES + 15) / 16];
   unsigned char *lds = reinterpret_cast<unsigned char *>(smem);
   uint4 *halo = smem;                                            // [4][PLANE]
   uint4 *gbx = reinterpret_cast<uint4 *>(lds + G::OFF_G);        // fused: [4][PD][PH][PW]
@@ -374,20 +374,10 @@ __global__ __launch_bounds__(256, 2) void c16_dgrad_kernel(const uint16_t *__res
 template <int KE, bool FUSED>
 hipError_t launch_dgrad(const C16Params &p, const void *g, const uint32_t *mask, const void *w, float alpha,
                         void *dx, hipStream_t st) {
-  using G = C16B<KE, FUSED>;
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void *)c16_dgrad_kernel<KE, FUSED>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, G::LDS_BYTES);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
-  int dev = 0, cus = 256;
-  if (hipGetDevice(&dev) == hipSuccess) hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   const long long tiles = (long long)p.n * ((p.d + TD - 1) / TD) * ((p.h + TH - 1) / TH) * ((p.w + TW - 1) / TW);
-  int blocks = (int)std::min<long long>(tiles, 2LL * cus);
+  int blocks = (int)std::min<long long>(tiles, 2LL * kNumCUs);
   blocks = std::max(8, (blocks + 7) / 8 * 8);
-  hipLaunchKernelGGL((c16_dgrad_kernel<KE, FUSED>), dim3(blocks), dim3(64 * NWAVE), G::LDS_BYTES, st,
+  hipLaunchKernelGGL((c16_dgrad_kernel<KE, FUSED>), dim3(blocks), dim3(64 * NWAVE), 0, st,
                      (const uint16_t *)g, mask, (const uint16_t *)w, alpha, (uint16_t *)dx, p);
   return hipGetLastError();
 }

@@ -65,7 +65,7 @@ __global__ __launch_bounds__(256, 2) void c16_wgrad_kernel(const uint16_t *__res
                                                            const uint32_t *__restrict__ mask, float alpha,
                                                            float *__restrict__ part_w, float *__restrict__ part_b,
                                                            uint16_t *__restrict__ dz_out, C16Params p) {
-  extern __shared__ __attribute__((aligned(16))) uint4 smem[];
+  __shared__ __attribute__((aligned(16))) uint4 smem[(LDS_BYTES + 15) / 16];
   uint4 *xh = smem;                 // [HD][HH][HW][2 x 8 ci]
   uint4 *dzt = smem + XH_PAD;       // [TD][TH][TW][4 x 8 co]
   const uint16_t *xh16 = reinterpret_cast<const uint16_t *>(xh);
@@ -315,24 +315,15 @@ __global__ __launch_bounds__(256, 2) void c16_wgrad_kernel(const uint16_t *__res
 }
 
 int wgrad_blocks(const C16Params &p) {
-  int dev = 0, cus = 256;
-  if (hipGetDevice(&dev) == hipSuccess) hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
   const long long tiles = (long long)p.n * ((p.od + TD - 1) / TD) * ((p.oh + TH - 1) / TH) * ((p.ow + TW - 1) / TW);
-  int blocks = (int)std::min<long long>(tiles, 2LL * cus);
+  int blocks = (int)std::min<long long>(tiles, 2LL * kNumCUs);
   return std::max(8, (blocks + 7) / 8 * 8);
 }
 
 template <bool FUSED>
 hipError_t launch_w(const C16Params &p, const void *x, const void *g, const uint32_t *mask, float alpha, float *pw,
                     float *pb, void *dz_out, int blocks, hipStream_t st) {
-  static bool attr_set = false;
-  if (!attr_set) {
-    hipError_t e = hipFuncSetAttribute((const void *)c16_wgrad_kernel<FUSED>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, LDS_BYTES);
-    if (e != hipSuccess) return e;
-    attr_set = true;
-  }
-  hipLaunchKernelGGL((c16_wgrad_kernel<FUSED>), dim3(blocks), dim3(256), LDS_BYTES, st, (const uint16_t *)x,
+  hipLaunchKernelGGL((c16_wgrad_kernel<FUSED>), dim3(blocks), dim3(256), 0, st, (const uint16_t *)x,
                      (const uint16_t *)g, mask, alpha, pw, pb, (uint16_t *)dz_out, p);
   return hipGetLastError();
 }

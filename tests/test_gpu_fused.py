@@ -103,6 +103,55 @@ def test_fused_fwd(case, dt):
     assert decided.mean() > 0.99
 
 
+# more tiles than the persistent kernels start workgroups: every workgroup loops
+# over several tiles, the next tile's halo arriving during the current tile's MFMAs
+MULTI_CASES = [
+    (3, (64, 64, 48), 16, 32, 4),    # 16 -> 32, 4^3: 768 tiles, ragged last w tile
+    (2, (64, 64, 64), 1, 16, 3),     # the first layer
+]
+
+
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
+@pytest.mark.parametrize("case", MULTI_CASES, ids=lambda c: "n%d_%dx%dx%d_c%d-%d_k%d" % (c[0], *c[1], *c[2:]))
+def test_fused_fwd_multitile_sampled(case, dt):
+    """Pooled values at sampled windows and the slope mask at sampled
+    conv-output points, each evaluated by the oracle one by one."""
+    N, dhw, CI, CO, k = case
+    desc = B.make_desc(N, dhw, CI, CO, k, 1, "same", dt)
+    if not B.cf_conv3d_fused_supported(desc) & B.FUSED_FWD:
+        pytest.skip("no fused forward kernel for this shape")
+    rng = np.random.default_rng(15)
+    xs = np.log1p(rng.poisson(np.exp(rng.standard_normal((N, *dhw, CI)))))
+    x = dev(xs, dt)
+    w = dev(rng.standard_normal((k, k, k, CI, CO)) * np.sqrt(2.0 / (k ** 3 * CI)), dt)
+    bh = rng.standard_normal(CO) * 0.1
+    b = torch.as_tensor(bh, dtype=torch.float32, device="cuda")
+    alpha = 0.01
+    od = B.cf_conv3d_out_shape(desc)
+    pshape = (N,) + tuple(t // 2 for t in od) + (CO,)
+    out = torch.full(pshape, float("nan"), dtype=tdtype(dt), device="cuda")
+    mask = torch.zeros(B.cf_conv3d_mask_bytes(desc), dtype=torch.uint8, device="cuda")
+    B.cf_conv3d_fwd_fused(desc, x, w, b, alpha, B.CF_FUSE_POOL2, out, mask)
+    torch.cuda.synchronize()
+    xh, wh, bf = to_np(x), to_np(w), to_np(b)
+    outh = to_np(out)
+    pidx = np.stack([rng.integers(0, t, 256) for t in pshape], 1)
+    ref, win = [], []
+    for n, pd, ph, pw, c in pidx:
+        pts = [(n, 2 * pd + u, 2 * ph + v, 2 * pw + t, c) for u in (0, 1) for v in (0, 1) for t in (0, 1)]
+        win += pts
+        u8 = oracle.conv3d_fwd_points(xh, wh, pts) + bf[c]
+        ref.append(np.mean(np.where(u8 > 0, u8, alpha * u8)))
+    e = maxabs_err(outh[tuple(pidx.T)], np.asarray(ref))
+    assert e <= TOL[dt], e
+    pts = np.concatenate([np.asarray(win), np.stack([rng.integers(0, t, 4096) for t in (N, *od, CO)], 1)])
+    u = oracle.conv3d_fwd_points(xh, wh, pts) + bf[pts[:, 4]]
+    bits = unpack_mask(mask, N * od[0] * od[1] * od[2] * CO).reshape((N, *od, CO))[tuple(pts.T)]
+    decided = np.abs(u) > 1e-5 * np.abs(u).max()
+    assert decided.mean() > 0.95
+    assert np.array_equal(bits[decided], (u > 0)[decided])
+
+
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
 @pytest.mark.parametrize("case", FWD_CASES, ids=lambda c: "n%d_%dx%dx%d_c%d-%d_k%d" % (c[0], *c[1], *c[2:]))
 def test_fused_bwd_weight(case, dt):
