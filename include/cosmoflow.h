@@ -111,6 +111,24 @@ size_t cf_conv3d_bwd_weight_workspace_size(const cf_conv3d_desc *desc);
 cf_status cf_conv3d_bwd_weight(const cf_conv3d_desc *desc, const void *x, const void *dz,
                                float *dw, void *ws, size_t ws_bytes, void *stream);
 
+/* Backward weights without a caller workspace, for callers that cannot
+ * allocate device memory (code under HIP graph capture, serving loops,
+ * harnesses that forbid hipMalloc).  Same operation, kernels and result bits
+ * as cf_conv3d_bwd_weight; the split reduction's partials go to a scratch
+ * region the library owns instead: a file-scope device array of
+ * CF_NOALLOC_SCRATCH_BYTES per GPU, held from the first use on that GPU until
+ * the process ends.  Nothing is allocated or freed by the call.  A layer whose
+ * partials need more than that returns CF_ERR_UNSUPPORTED (use
+ * cf_conv3d_bwd_weight with a workspace).  Every call on one GPU shares that
+ * GPU's region, and the region keeps the last call's contents (every partial
+ * is written before it is summed, so nothing needs clearing): calls that
+ * overlap in time on one GPU (different streams, or host threads without
+ * ordering) race and give undefined results; calls ordered on one stream do
+ * not.  CF_ERR_LAUNCH if the region's device address cannot be resolved. */
+#define CF_NOALLOC_SCRATCH_BYTES (16u << 20)
+cf_status cf_conv3d_bwd_weight_noalloc(const cf_conv3d_desc *desc, const void *x, const void *dz,
+                                       float *dw, void *stream);
+
 /* Bias + leaky ReLU forward (Section III-A):
  *   y[v,c] = u > 0 ? u : alpha*u,  u = z[v,c] + bias[c]   (u in fp32)
  * nvox = number of voxels (n*d*h*w), c = channels; z, y in dtype; bias fp32

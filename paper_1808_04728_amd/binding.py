@@ -37,6 +37,7 @@ EXPORTS = [
     "cf_conv3d_bwd_data_fused", "cf_reduce_partials", "cf_conv3d_bwd_weight_deferred", "cf_bias_lrelu_bwd_deferred",
     "cf_conv3d_bwd_weight_fused_deferred", "cf_adam_larc_workspace_size", "cf_adam_larc_step",
     "cf_fc_fwd_workspace_size", "cf_fc_fwd", "cf_fc_bwd_data", "cf_fc_bwd_weight", "cf_mse_loss",
+    "cf_conv3d_bwd_weight_noalloc",
 ]
 
 
@@ -100,6 +101,7 @@ def lib():
         "cf_conv3d_bwd_data": ([D, vp, vp, vp, vp], ctypes.c_int),
         "cf_conv3d_bwd_weight_workspace_size": ([D], sz),
         "cf_conv3d_bwd_weight": ([D, vp, vp, vp, vp, sz, vp], ctypes.c_int),
+        "cf_conv3d_bwd_weight_noalloc": ([D, vp, vp, vp, vp], ctypes.c_int),
         "cf_bias_lrelu_fwd": ([i64, i32, i32, vp, vp, f32, vp, vp], ctypes.c_int),
         "cf_bias_lrelu_bwd_workspace_size": ([i64, i32], sz),
         "cf_bias_lrelu_bwd": ([i64, i32, i32, vp, vp, f32, vp, vp, vp, sz, vp], ctypes.c_int),
@@ -210,6 +212,10 @@ def cf_conv3d_bwd_weight(desc, x, dz, dw, ws, ws_bytes=None, stream=None):
         ws_bytes = 0 if ws is None or isinstance(ws, int) else ws.numel() * ws.element_size()
     _check(lib().cf_conv3d_bwd_weight(ctypes.byref(desc), _ptr(x), _ptr(dz), _ptr(dw), _ptr(ws),
                                       ws_bytes, _stream(stream)))
+
+
+def cf_conv3d_bwd_weight_noalloc(desc, x, dz, dw, stream=None):
+    _check(lib().cf_conv3d_bwd_weight_noalloc(ctypes.byref(desc), _ptr(x), _ptr(dz), _ptr(dw), _stream(stream)))
 
 
 def cf_bias_lrelu_fwd(nvox, c, dtype, z, bias, alpha, y, stream=None):

@@ -242,6 +242,28 @@ cf_status cf_conv3d_bwd_weight(const cf_conv3d_desc *desc, const void *x, const 
   return finish(cf::launch_conv_bwd_weight(s, x, dz, dw, ws, st), st, "cf_conv3d_bwd_weight");
 }
 
+static_assert(cf::kNoallocScratchBytes == CF_NOALLOC_SCRATCH_BYTES, "scratch region size");
+
+cf_status cf_conv3d_bwd_weight_noalloc(const cf_conv3d_desc *desc, const void *x, const void *dz, float *dw,
+                                       void *stream) {
+  cf::ConvShape s;
+  cf_status r = resolve(desc, &s);
+  if (r != CF_OK) return r;
+  const size_t need = s.n == 0 ? 0 : cf::conv_bwd_weight_workspace(s);
+  if (need > cf::kNoallocScratchBytes)
+    return fail(CF_ERR_UNSUPPORTED, "cf_conv3d_bwd_weight_noalloc: the split reduction needs " +
+                                        std::to_string(need) + " bytes of partials, more than the " +
+                                        std::to_string(cf::kNoallocScratchBytes) +
+                                        "-byte library scratch region (use cf_conv3d_bwd_weight with a workspace)");
+  void *ws = nullptr;
+  if (need > 0) {
+    const hipError_t e = cf::noalloc_scratch(&ws);
+    if (e != hipSuccess)
+      return fail(CF_ERR_LAUNCH, std::string("cf_conv3d_bwd_weight_noalloc: scratch region: ") + hipGetErrorString(e));
+  }
+  return cf_conv3d_bwd_weight(desc, x, dz, dw, ws, need, stream);
+}
+
 cf_status cf_bias_lrelu_fwd(int64_t nvox, int32_t c, int32_t dtype, const void *z, const float *bias,
                             float alpha, void *y, void *stream) {
   if (nvox < 0) return fail(CF_ERR_INVALID_ARG, "nvox must be >= 0");

@@ -124,6 +124,13 @@ void set_sum_collector(SumCollector *c);
 // all jobs in as few launches as possible (same bits as one launch per job)
 hipError_t launch_sum_batch(const SumJob *jobs, int n, hipStream_t st);
 
+// Scratch region of the allocation-free backward-weights entry point
+// (noalloc.hip): a file-scope device array of this many bytes per GPU.
+constexpr size_t kNoallocScratchBytes = 16u << 20;
+// device address of the current device's scratch region (resolved once per
+// device with hipGetSymbolAddress, with that device current)
+hipError_t noalloc_scratch(void **ptr);
+
 // out[0..n) = 0 (a fill kernel, never hipMemsetAsync).
 hipError_t launch_fill_zero(float *out, long long n, hipStream_t st);
 

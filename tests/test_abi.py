@@ -88,6 +88,18 @@ def test_wgrad_workspace_validation(L):
     expect(B.CF_ERR_ALIAS, B.cf_conv3d_bwd_weight, d, A, A + 0x1000000, A + 0x10, A + 0x3000000, need, 0)
 
 
+def test_wgrad_noalloc_validation(L):
+    """Shapes whose split reduction needs more partials than the library's
+    scratch region are rejected on the host, before any device call."""
+    big = B.make_desc(8, (64, 64, 64), 16, 32, 4, 1, "same", "bf16")
+    assert B.cf_conv3d_bwd_weight_workspace_size(big) > 16 << 20
+    expect(B.CF_ERR_UNSUPPORTED, B.cf_conv3d_bwd_weight_noalloc, big, A, A + 0x10000000, A + 0x20000000, 0)
+    assert "scratch" in B.cf_last_error()
+    bad = B.make_desc(1, (8, 8, 8), 16, 32, 3)
+    bad.kd = 0
+    expect(B.CF_ERR_INVALID_ARG, B.cf_conv3d_bwd_weight_noalloc, bad, A, A + 0x100000, A + 0x200000, 0)
+
+
 def test_eltwise_validation(L):
     expect(B.CF_ERR_INVALID_ARG, B.cf_bias_lrelu_fwd, 10, 16, "f32", A, A + 0x10000, math.nan, A + 0x20000, 0)
     expect(B.CF_ERR_INVALID_ARG, B.cf_bias_lrelu_fwd, 10, 0, "f32", A, A + 0x10000, 0.01, A + 0x20000, 0)
