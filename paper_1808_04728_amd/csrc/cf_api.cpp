@@ -378,7 +378,8 @@ static int32_t fused_mask(const cf::ConvShape &s, uint32_t flags) {
     if (cf::smallc_wgrad_fused_supported(s) || cf::c16_wgrad_supported(s)) m |= 2;
   }
   if (cf::c16_fwd_supported(s)) m |= 1;  // with or without the pool
-  if (flags == 0 && cf::direct_supported(s, true)) m |= 1;
+  if (flags == 0 && (cf::direct_supported(s, true) || cf::f32conv_supported(s, true))) m |= 1;
+  if (flags == CF_FUSE_POOL2 && cf::f32conv_pool_supported(s)) m |= 1;
   if (flags == CF_FUSE_POOL2 && cf::c16_bwd_supported(s)) m |= 4;
   if (flags == CF_FUSE_POOL2 && cf::c16_wgrad_supported(s) && !cf::smallc_wgrad_fused_supported(s)) m |= 8;
   return m;
@@ -445,6 +446,9 @@ cf_status cf_conv3d_fwd_fused(const cf_conv3d_desc *desc, const void *x, const v
   hipError_t e;
   if (pool && cf::smallc_supported(s, true))
     e = cf::launch_conv_fwd_smallc(s, x, w, bias, alpha, out, (uint16_t *)mask, true, st);
+  else if (cf::f32conv_supported(s, true) && !cf::c16_fwd_supported(s))
+    e = cf::launch_conv_fwd_f32(s, (const float *)x, (const float *)w, bias, alpha, (float *)out, (uint8_t *)mask,
+                                pool ? 2 : 1, st);
   else if (!pool && !cf::c16_fwd_supported(s))
     e = cf::launch_conv_fwd_direct(s, x, w, bias, alpha, out, mask, true, st);
   else

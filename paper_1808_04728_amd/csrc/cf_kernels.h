@@ -91,6 +91,16 @@ size_t direct_wgrad_workspace(const ConvShape &s);
 hipError_t launch_conv_bwd_weight_direct(const ConvShape &s, const void *x, const void *dz, float *dw, void *ws,
                                          hipStream_t st);
 
+// fp32 implicit GEMM on v_mfma_f32_16x16x4_f32 (conv_f32.hip): forward for
+// ci % 16 == 0 and co % 32 == 0, backward-data for co % 16 == 0 and ci % 16 == 0.
+// epi: 0 store z, 1 bias + lReLU (+ mask if non-null), 2 bias + lReLU + mask +
+// 2^3 pool (f32conv_pool_supported: stride 1, 32 output channels)
+bool f32conv_supported(const ConvShape &s, bool fwd);
+bool f32conv_pool_supported(const ConvShape &s);
+hipError_t launch_conv_fwd_f32(const ConvShape &s, const float *x, const float *w, const float *bias, float alpha,
+                               float *out, uint8_t *mask, int epi, hipStream_t st);
+hipError_t launch_conv_bwd_data_f32(const ConvShape &s, const float *dz, const float *w, float *dx, hipStream_t st);
+
 hipError_t launch_conv_fwd(const ConvShape &s, const void *x, const void *w, void *z,
                            hipStream_t st);
 hipError_t launch_conv_bwd_data(const ConvShape &s, const void *dz, const void *w, void *dx,

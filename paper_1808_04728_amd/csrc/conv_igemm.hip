@@ -570,6 +570,13 @@ hipError_t dispatch_wgrad(const WgradPlan &pl, const WgradParams &p, const void 
 
 }  // namespace
 
+// CF_CONV_KERNEL=igemm keeps forward and backward-data on the generic kernel
+// (tests compare it with the specialised fp32 kernel this way)
+static bool igemm_forced() {
+  const char *e = getenv("CF_CONV_KERNEL");
+  return e && !strcmp(e, "igemm");
+}
+
 hipError_t launch_conv_fwd(const ConvShape &s, const void *x, const void *w, void *z,
                            hipStream_t st) {
   // few input channels: the direct halo kernel (one im2col gather per MFMA tile)
@@ -579,6 +586,9 @@ hipError_t launch_conv_fwd(const ConvShape &s, const void *x, const void *w, voi
   if (c16_fwd_supported(s)) return launch_conv_fwd_c16(s, x, w, nullptr, 0.f, z, nullptr, 0, st);
   // many channels, bf16: waves split the taps, fragments gathered straight into registers
   if (direct_supported(s, true)) return launch_conv_fwd_direct(s, x, w, nullptr, 0.f, z, nullptr, false, st);
+  // fp32 with 16k input channels: register-streaming fp32 MFMA kernel
+  if (f32conv_supported(s, true) && !igemm_forced())
+    return launch_conv_fwd_f32(s, (const float *)x, (const float *)w, nullptr, 0.f, (float *)z, nullptr, 0, st);
   IgemmParams p{};
   p.nb = s.n;
   p.sd_ = s.d; p.sh_ = s.h; p.sw_ = s.w; p.sc = s.ci;
@@ -603,6 +613,8 @@ hipError_t launch_conv_bwd_data(const ConvShape &s, const void *dz, const void *
                                 hipStream_t st) {
   if (c16_bwd_supported(s)) return launch_conv_bwd_data_c16(s, dz, nullptr, w, 0.f, dx, false, st);
   if (direct_supported(s, false)) return launch_conv_bwd_data_direct(s, dz, w, dx, st);
+  if (f32conv_supported(s, false) && !igemm_forced())
+    return launch_conv_bwd_data_f32(s, (const float *)dz, (const float *)w, (float *)dx, st);
   // one launch per parity class (r_d, r_h, r_w) of input voxels
   for (int rd = 0; rd < s.sd; ++rd)
     for (int rh = 0; rh < s.sh; ++rh)
