@@ -382,6 +382,7 @@ static int32_t fused_mask(const cf::ConvShape &s, uint32_t flags) {
   if (flags == CF_FUSE_POOL2 && cf::f32conv_pool_supported(s)) m |= 1;
   if (flags == CF_FUSE_POOL2 && cf::c16_bwd_supported(s)) m |= 4;
   if (flags == CF_FUSE_POOL2 && cf::c16_wgrad_supported(s) && !cf::smallc_wgrad_fused_supported(s)) m |= 8;
+  if (flags == CF_FUSE_POOL2 && cf::f32wgrad_fused_supported(s) && !cf::smallc_wgrad_fused_supported(s)) m |= 2 | 8;
   return m;
 }
 
@@ -401,7 +402,9 @@ static size_t mask_bytes(const cf::ConvShape &s) {
 }
 
 static size_t fused_wgrad_workspace(const cf::ConvShape &s) {
-  return cf::smallc_wgrad_fused_supported(s) ? cf::smallc_wgrad_fused_workspace(s) : cf::c16_wgrad_workspace(s);
+  if (cf::smallc_wgrad_fused_supported(s)) return cf::smallc_wgrad_fused_workspace(s);
+  if (cf::f32wgrad_fused_supported(s)) return cf::f32wgrad_workspace(s, true);
+  return cf::c16_wgrad_workspace(s);
 }
 
 // bytes of the 2^3 stride-2 pooled conv output (floor extents)
@@ -501,10 +504,14 @@ static cf_status bwd_weight_fused(const char *name, const cf_conv3d_desc *desc, 
     return fail(CF_ERR_ALIAS, std::string(name) + ": outputs / workspace overlap");
   if (dz && (overlap(dz, b.z, dw, dw_bytes) || overlap(dz, b.z, db, dbb) || overlap(dz, b.z, ws, need)))
     return fail(CF_ERR_ALIAS, std::string(name) + ": dz overlaps another output or the workspace");
-  const hipError_t e =
-      cf::smallc_wgrad_fused_supported(s)
-          ? cf::launch_smallc_wgrad_fused(s, x, g, (const uint16_t *)mask, alpha, dw, db, ws, st)
-          : cf::launch_conv_bwd_weight_c16(s, x, g, (const uint32_t *)mask, alpha, dw, db, ws, true, dz, st);
+  hipError_t e;
+  if (cf::smallc_wgrad_fused_supported(s))
+    e = cf::launch_smallc_wgrad_fused(s, x, g, (const uint16_t *)mask, alpha, dw, db, ws, st);
+  else if (cf::f32wgrad_fused_supported(s))
+    e = cf::launch_conv_bwd_weight_f32(s, (const float *)x, (const float *)g, (const uint32_t *)mask, alpha, dw, db,
+                                       ws, true, (float *)dz, st);
+  else
+    e = cf::launch_conv_bwd_weight_c16(s, x, g, (const uint32_t *)mask, alpha, dw, db, ws, true, dz, st);
   return finish(e, st, name);
 }
 

@@ -101,6 +101,18 @@ hipError_t launch_conv_fwd_f32(const ConvShape &s, const float *x, const float *
                                float *out, uint8_t *mask, int epi, hipStream_t st);
 hipError_t launch_conv_bwd_data_f32(const ConvShape &s, const float *dz, const float *w, float *dx, hipStream_t st);
 
+// fp32 backward-weights on v_mfma_f32_16x16x4_f32 (conv_f32_wgrad.hip), ci % 16 == 0,
+// co % 16 == 0: voxel slices' partials in ws, summed by launch_sum_rows.  fused (the
+// pooled 16 -> 32 layer, 32 output channels): g is the pooled-output gradient and
+// mask the forward's slope mask; db and (if dz_out) the rebuilt dz come from the
+// same pass
+bool f32wgrad_supported(const ConvShape &s);
+bool f32wgrad_fused_supported(const ConvShape &s);
+size_t f32wgrad_workspace(const ConvShape &s, bool fused);
+hipError_t launch_conv_bwd_weight_f32(const ConvShape &s, const float *x, const float *g, const uint32_t *mask,
+                                      float alpha, float *dw, float *db, void *ws, bool fused, float *dz_out,
+                                      hipStream_t st);
+
 hipError_t launch_conv_fwd(const ConvShape &s, const void *x, const void *w, void *z,
                            hipStream_t st);
 hipError_t launch_conv_bwd_data(const ConvShape &s, const void *dz, const void *w, void *dx,

@@ -1,0 +1,368 @@
+// conv_f32_wgrad.hip -- fp32 backward-weights on v_mfma_f32_16x16x4_f32
+// (Section III-C: the weight-gradient operator is a forward-like convolution
+// with a large reduction and a small output; the paper gives each thread a
+// private copy of the output and reduces the copies afterwards).
+//
+//   dW[t, ci, co] = sum_{n, o} x~[n, o*s + t - p, ci] dz[n, o, co]
+//
+// is a GEMM with rows (t, ci), columns co and the output voxels as K.  The
+// voxels are split into fixed slices (grid z); a slice's partial dW goes to the
+// caller's workspace and a fixed-order column sum adds the slices (bitwise
+// reproducible, no atomics).  Inside a slice each wave owns RU row units of 64
+// rows and FN column fragments of 16 output channels, and steps through the
+// slice four voxels at a time (K slot = l/16 for lane l).
+//
+// One 16-byte load per lane feeds four MFMAs: lane l (m = l%16) loads four
+// consecutive channels of one gathered voxel, and register j of the load is
+// the A operand of MFMA j, whose row m then stands for
+//   * 4^3-wide kernels (unit = (kd, kh, 16 channels from c0)): tap column
+//     kw = m/4 and channel c0 + 4 (m%4) + j -- the 16 lanes of a voxel slot
+//     read four neighbouring voxels x 64 bytes, one 256-byte run;
+//   * 64k-channel layers (unit = (tap, 64 channels from c0)): channel
+//     c0 + 4m + j -- 256 contiguous bytes of one voxel.
+// The gradient operand (B: output channel l%16 at voxel slot l/16) is shared
+// by every row of the wave.  Operands are streamed into registers PF steps
+// ahead through range-checked buffer loads (a padding tap or a voxel past the
+// slice reads zero).
+//
+// Fused variant (the pooled 16 -> 32 layer): the gradient operand is rebuilt
+// from the pooled-output gradient g and the forward's slope mask,
+//   dz[v, co] = g[pool(v), co] / 8 * (mask bit (v, co) ? 1 : alpha)
+// (zero outside complete pooling windows), the bias gradient db = sum_v dz is
+// summed from the same values in a fixed order, and dz can be stored once for
+// the layer's backward-data.
+
+#include "cf_common.h"
+#include "cf_kernels.h"
+#include "fastdiv.h"
+
+#include <algorithm>
+
+namespace cf {
+namespace {
+
+constexpr uint32_t W_OOB = 0x80000000u;  // past every buffer: the load returns zeros
+
+struct WF32Params {
+  int n, d, h, w, ci;          // input
+  int od, oh, ow, co;          // conv output
+  int sd, sh, sw, pd, ph, pw;  // stride, padding before
+  int kh, kw;                  // kernel extents (tap decode)
+  int m;                       // kd*kh*kw*ci (GEMM rows)
+  int units;                   // row units of 64 rows
+  int cunits;                  // channel chunks per unit position (ci/16 or ci/64)
+  int vox;                     // n*od*oh*ow (reduction length)
+  int chunk;                   // voxels per slice (multiple of 4)
+  FastDiv fw, fh, fd;          // voxel decode divisors ow, oh, od
+  uint32_t x_bytes, g_bytes, m_bytes;
+  float alpha;
+  int pod, poh, pow_;          // fused: pooled extents
+};
+
+__device__ __forceinline__ uint32_t ld32(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
+}
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ u32x4_t ld128(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+}
+
+// KW4: units are (kd, kh, 16 channels) of a kernel 4 wide; else (tap, 64 channels)
+template <bool FUSED, bool KW4, int RU, int FN, int WV, int PF>
+__global__ __launch_bounds__(64 * WV) void wgrad_f32_kernel(const float *__restrict__ x,
+                                                            const float *__restrict__ g,
+                                                            const uint32_t *__restrict__ mask,
+                                                            float *__restrict__ part_w, float *__restrict__ part_b,
+                                                            float *__restrict__ dz_out, const WF32Params p) {
+  __shared__ float dbs[4][16 * FN];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int g4 = lane >> 4, r16 = lane & 15;
+  const int co0 = blockIdx.y * 16 * FN;
+  const int slice = blockIdx.z;
+  const int v0 = slice * p.chunk;
+  const int v1 = min(v0 + p.chunk, p.vox);
+  // the bias gradient and the stored dz come from one wave of the slice
+  const bool lead = FUSED && blockIdx.x == 0 && wave == 0;
+
+  const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc((void *)x, (short)0, p.x_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t gr = __builtin_amdgcn_make_buffer_rsrc((void *)g, (short)0, p.g_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t mr =
+      __builtin_amdgcn_make_buffer_rsrc((void *)mask, (short)0, FUSED ? p.m_bytes : 0u, 0x00020000);
+
+  // ---- this wave's row units: the lane's tap and channel, and its dW rows ---
+  const int u0 = (blockIdx.x * WV + wave) * RU;
+  int tkd[RU], tkh[RU], tkw[RU], toff[RU], rbase[RU];
+  bool uok[RU];
+#pragma unroll
+  for (int i = 0; i < RU; ++i) {
+    const int u = u0 + i;
+    uok[i] = u < p.units;
+    const int uu = uok[i] ? u : 0;
+    const int pos = uu / p.cunits, cc = uu - pos * p.cunits;
+    int c0, tap;
+    if constexpr (KW4) {
+      // pos = kd * kh_extent + kh; this lane's column kw = r16 / 4, channels c0 + 4 (r16 % 4) ..
+      tkd[i] = pos / p.kh;
+      tkh[i] = pos - tkd[i] * p.kh;
+      tkw[i] = r16 >> 2;
+      c0 = 16 * cc;
+      tap = (tkd[i] * p.kh + tkh[i]) * 4 + tkw[i];
+      toff[i] = ((tkd[i] * p.h + tkh[i]) * p.w + tkw[i]) * p.ci + c0 + 4 * (r16 & 3);
+      // D row 4 g + e of MFMA j: column kw = g, channel c0 + 4 e + j
+      rbase[i] = ((tkd[i] * p.kh + tkh[i]) * 4 + g4) * p.ci + c0;
+    } else {
+      tap = pos;
+      tkw[i] = tap % p.kw;
+      tkh[i] = (tap / p.kw) % p.kh;
+      tkd[i] = tap / (p.kw * p.kh);
+      c0 = 64 * cc;
+      toff[i] = ((tkd[i] * p.h + tkh[i]) * p.w + tkw[i]) * p.ci + c0 + 4 * r16;
+      // D row 4 g + e of MFMA j: channel c0 + 16 g + 4 e + j
+      rbase[i] = tap * p.ci + c0 + 16 * g4;
+    }
+    (void)tap;
+  }
+
+  const int nsteps = v1 > v0 ? (v1 - v0 + 3) >> 2 : 0;
+  constexpr int NS = PF + 1;
+  u32x4_t a_r[NS][RU];
+  float b_r[NS][FN];
+  uint32_t m_r[NS];
+  (void)m_r;
+
+  auto load = [&](int step, u32x4_t(&a)[RU], float(&b)[FN], uint32_t &mw) {
+    const int v = v0 + 4 * step + g4;
+    const bool vok = v < v1;
+    const int vv = vok ? v : v0;
+    const int t1 = fdiv(vv, p.fw), t2 = fdiv(t1, p.fh), nn = fdiv(t2, p.fd);
+    const int ow_ = vv - t1 * (int)p.fw.div, oh_ = t1 - t2 * (int)p.fh.div, od_ = t2 - nn * (int)p.fd.div;
+    const int bd = od_ * p.sd - p.pd, bh = oh_ * p.sh - p.ph, bw = ow_ * p.sw - p.pw;
+    const int base = (((nn * p.d + bd) * p.h + bh) * p.w + bw) * p.ci;
+#pragma unroll
+    for (int i = 0; i < RU; ++i) {
+      const bool ok = vok && uok[i] && (unsigned)(bd + tkd[i]) < (unsigned)p.d &&
+                      (unsigned)(bh + tkh[i]) < (unsigned)p.h && (unsigned)(bw + tkw[i]) < (unsigned)p.w;
+      a[i] = ld128(xr, ok ? (uint32_t)(base + toff[i]) * 4u : W_OOB);
+    }
+    if constexpr (FUSED) {
+      const int pd_ = od_ >> 1, ph_ = oh_ >> 1, pw_ = ow_ >> 1;
+      const bool win = vok && pd_ < p.pod && ph_ < p.poh && pw_ < p.pow_;
+      const int pv = ((nn * p.pod + pd_) * p.poh + ph_) * p.pow_ + pw_;
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        b[j] = __uint_as_float(ld32(gr, win ? (uint32_t)(pv * p.co + co0 + 16 * j + r16) * 4u : W_OOB));
+      // the 32 channels of voxel v are one mask word (32 output channels)
+      mw = ld32(mr, vok ? (uint32_t)vv * 4u : W_OOB);
+    } else {
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        b[j] = __uint_as_float(ld32(gr, vok ? (uint32_t)(vv * p.co + co0 + 16 * j + r16) * 4u : W_OOB));
+    }
+  };
+
+  f32x4_t acc[RU][4][FN];
+#pragma unroll
+  for (int i = 0; i < RU; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int k = 0; k < FN; ++k) acc[i][j][k] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  float dsum[FN];
+#pragma unroll
+  for (int j = 0; j < FN; ++j) dsum[j] = 0.f;
+  const float s1 = 0.125f, sa = 0.125f * p.alpha;
+
+  if (nsteps > 0) {
+    const int niter = (nsteps + NS - 1) / NS * NS;
+#pragma unroll
+    for (int q = 0; q < PF; ++q) load(min(q, nsteps - 1), a_r[q], b_r[q], m_r[q]);
+    for (int s0 = 0; s0 < niter; s0 += NS) {
+#pragma unroll
+      for (int q = 0; q < NS; ++q) {
+        const int s = s0 + q;
+        const int sl = (q + PF) % NS;
+        load(min(s + PF, nsteps - 1), a_r[sl], b_r[sl], m_r[sl]);
+        const bool real = s < nsteps;
+        float bv[FN];
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          float b = real ? b_r[q][j] : 0.f;
+          if constexpr (FUSED) {
+            const bool on = (m_r[q] >> ((co0 + 16 * j + r16) & 31)) & 1u;
+            b *= on ? s1 : sa;
+          }
+          bv[j] = b;
+        }
+        if (lead) {
+          const int v = v0 + 4 * s + g4;
+#pragma unroll
+          for (int j = 0; j < FN; ++j) {
+            dsum[j] += bv[j];
+            if (dz_out && real && v < v1) dz_out[(long long)v * p.co + co0 + 16 * j + r16] = bv[j];
+          }
+        }
+#pragma unroll
+        for (int i = 0; i < RU; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int k = 0; k < FN; ++k)
+              acc[i][j][k] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a_r[q][i][j]), bv[k],
+                                                                  acc[i][j][k], 0, 0, 0);
+      }
+    }
+  }
+
+  // ---- partial dW of this slice ----------------------------------------------
+  float *pw = part_w + (long long)slice * p.m * p.co;
+#pragma unroll
+  for (int i = 0; i < RU; ++i) {
+    if (!uok[i]) continue;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int row = rbase[i] + 4 * e + j;
+#pragma unroll
+        for (int k = 0; k < FN; ++k) pw[(long long)row * p.co + co0 + 16 * k + r16] = acc[i][j][k][e];
+      }
+  }
+  if constexpr (FUSED) {
+    // bias-gradient partial: the four voxel slots of each channel, in order
+    if (lead)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) dbs[g4][16 * j + r16] = dsum[j];
+    __syncthreads();
+    if (blockIdx.x == 0 && threadIdx.x < 16 * FN) {
+      const int c = threadIdx.x;
+      part_b[(long long)slice * p.co + co0 + c] = ((dbs[0][c] + dbs[1][c]) + dbs[2][c]) + dbs[3][c];
+    }
+  }
+}
+
+struct WPlan {
+  bool kw4;
+  int ru, fn, wv;
+  int units, cunits;
+  int gx, gy, nsplit, chunk;
+};
+
+WPlan w_plan(const ConvShape &s, bool fused) {
+  WPlan pl{};
+  const long long vox = (long long)s.n * s.od * s.oh * s.ow;
+  pl.kw4 = s.kw == 4 && s.ci % 16 == 0;
+  if (pl.kw4) {
+    pl.cunits = s.ci / 16;
+    pl.units = s.kd * s.kh * pl.cunits;
+  } else {
+    pl.cunits = s.ci / 64;
+    pl.units = s.kd * s.kh * s.kw * pl.cunits;
+  }
+  pl.fn = fused ? 2 : (s.co % 64 == 0 ? 4 : (s.co % 32 == 0 ? 2 : 1));
+  pl.ru = (fused || pl.units >= 64) ? 2 : 1;
+  pl.wv = 8;
+  pl.gx = (pl.units + pl.ru * pl.wv - 1) / (pl.ru * pl.wv);
+  pl.gy = s.co / (16 * pl.fn);
+  // about one workgroup per compute unit (the fused layer) or per two (the deep
+  // layers, whose short slices would otherwise write more partials than they
+  // read operands), each slice at least 16 steps of 4 voxels
+  const long long tiles = (long long)pl.gx * pl.gy;
+  const long long target = fused ? kNumCUs : kNumCUs / 2;
+  long long want = std::max(1LL, (target + tiles - 1) / tiles);
+  want = std::min(want, std::max(1LL, vox / 64));
+  long long chunk = (vox + want - 1) / want;
+  chunk = (chunk + 3) / 4 * 4;
+  pl.chunk = (int)std::max(4LL, chunk);
+  pl.nsplit = (int)((vox + pl.chunk - 1) / pl.chunk);
+  return pl;
+}
+
+WF32Params w_params(const ConvShape &s, const WPlan &pl, float alpha) {
+  WF32Params p{};
+  p.n = s.n; p.d = s.d; p.h = s.h; p.w = s.w; p.ci = s.ci;
+  p.od = s.od; p.oh = s.oh; p.ow = s.ow; p.co = s.co;
+  p.sd = s.sd; p.sh = s.sh; p.sw = s.sw; p.pd = s.pd; p.ph = s.ph; p.pw = s.pw;
+  p.kh = s.kh; p.kw = s.kw;
+  p.m = s.kd * s.kh * s.kw * s.ci;
+  p.units = pl.units;
+  p.cunits = pl.cunits;
+  p.vox = s.n * s.od * s.oh * s.ow;
+  p.chunk = pl.chunk;
+  p.fw = make_fastdiv(s.ow);
+  p.fh = make_fastdiv(s.oh);
+  p.fd = make_fastdiv(s.od);
+  p.x_bytes = (uint32_t)((long long)s.n * s.d * s.h * s.w * s.ci * 4);
+  p.alpha = alpha;
+  p.pod = s.od / 2; p.poh = s.oh / 2; p.pow_ = s.ow / 2;
+  return p;
+}
+
+template <bool FUSED, bool KW4, int RU, int FN>
+hipError_t launch_w(const WPlan &pl, const WF32Params &p, const float *x, const float *g, const uint32_t *mask,
+                    float *pw, float *pb, float *dz_out, hipStream_t st) {
+  dim3 grid(pl.gx, pl.gy, pl.nsplit);
+  constexpr int PF = 2;
+  hipLaunchKernelGGL((wgrad_f32_kernel<FUSED, KW4, RU, FN, 8, PF>), grid, dim3(512), 0, st, x, g, mask, pw, pb,
+                     dz_out, p);
+  return hipGetLastError();
+}
+
+template <bool KW4, int FN>
+hipError_t launch_wu(const WPlan &pl, const WF32Params &p, const float *x, const float *g, float *pw,
+                     hipStream_t st) {
+  return pl.ru == 2 ? launch_w<false, KW4, 2, FN>(pl, p, x, g, nullptr, pw, nullptr, nullptr, st)
+                    : launch_w<false, KW4, 1, FN>(pl, p, x, g, nullptr, pw, nullptr, nullptr, st);
+}
+
+}  // namespace
+
+bool f32wgrad_supported(const ConvShape &s) {
+  if (s.dtype != DT_F32 || s.co % 16 != 0) return false;
+  if (!((s.kw == 4 && s.ci % 16 == 0) || s.ci % 64 == 0)) return false;
+  const long long xin = (long long)s.n * s.d * s.h * s.w * s.ci, zout = (long long)s.n * s.od * s.oh * s.ow * s.co;
+  const long long m = (long long)s.kd * s.kh * s.kw * s.ci;
+  return xin * 4 < (1LL << 31) && zout * 4 < (1LL << 31) && m * s.co < (1LL << 31) && zout > 0;
+}
+
+bool f32wgrad_fused_supported(const ConvShape &s) {
+  return f32wgrad_supported(s) && s.kw == 4 && s.co == 32 && s.sd == 1 && s.sh == 1 && s.sw == 1 && s.od >= 2 &&
+         s.oh >= 2 && s.ow >= 2;
+}
+
+size_t f32wgrad_workspace(const ConvShape &s, bool fused) {
+  const WPlan pl = w_plan(s, fused);
+  return (size_t)pl.nsplit * ((size_t)s.kd * s.kh * s.kw * s.ci * s.co + (fused ? s.co : 0)) * sizeof(float);
+}
+
+hipError_t launch_conv_bwd_weight_f32(const ConvShape &s, const float *x, const float *g, const uint32_t *mask,
+                                      float alpha, float *dw, float *db, void *ws, bool fused, float *dz_out,
+                                      hipStream_t st) {
+  const WPlan pl = w_plan(s, fused);
+  WF32Params p = w_params(s, pl, alpha);
+  float *pw = (float *)ws;
+  const int m = p.m;
+  float *pb = pw + (size_t)pl.nsplit * m * s.co;
+  hipError_t e;
+  if (fused) {
+    p.g_bytes = (uint32_t)((long long)s.n * p.pod * p.poh * p.pow_ * s.co * 4);
+    p.m_bytes = (uint32_t)(((long long)p.vox * s.co + 31) / 32 * 4);
+    e = launch_w<true, true, 2, 2>(pl, p, x, g, mask, pw, pb, dz_out, st);
+  } else {
+    p.g_bytes = (uint32_t)((long long)p.vox * s.co * 4);
+    if (pl.kw4)
+      e = pl.fn == 4 ? launch_wu<true, 4>(pl, p, x, g, pw, st)
+        : pl.fn == 2 ? launch_wu<true, 2>(pl, p, x, g, pw, st)
+                     : launch_wu<true, 1>(pl, p, x, g, pw, st);
+    else
+      e = pl.fn == 4 ? launch_wu<false, 4>(pl, p, x, g, pw, st)
+        : pl.fn == 2 ? launch_wu<false, 2>(pl, p, x, g, pw, st)
+                     : launch_wu<false, 1>(pl, p, x, g, pw, st);
+  }
+  if (e != hipSuccess) return e;
+  e = launch_sum_rows(pw, dw, pl.nsplit, m * s.co, st);
+  if (e != hipSuccess || !fused) return e;
+  return launch_sum_rows(pb, db, pl.nsplit, s.co, st);
+}
+
+}  // namespace cf

@@ -666,6 +666,13 @@ static bool use_direct_wgrad(const ConvShape &s) {
 }
 
 // the single-channel first layer (bf16): CF_WGRAD_KERNEL=igemm forces the generic kernel
+// fp32 with 16k channels: CF_WGRAD_KERNEL=igemm forces the generic kernel
+static bool use_f32_wgrad(const ConvShape &s) {
+  const char *e = getenv("CF_WGRAD_KERNEL");
+  if (e && !strcmp(e, "igemm")) return false;
+  return f32wgrad_supported(s);
+}
+
 static bool use_l1_wgrad(const ConvShape &s) {
   const char *e = getenv("CF_WGRAD_KERNEL");
   if (e && !strcmp(e, "igemm")) return false;
@@ -676,6 +683,7 @@ size_t conv_bwd_weight_workspace(const ConvShape &s) {
   if (use_l1_wgrad(s)) return smallc_wgrad_dz_workspace(s);
   if (c16_wgrad_supported(s)) return c16_wgrad_workspace(s);
   if (use_direct_wgrad(s)) return direct_wgrad_workspace(s);
+  if (use_f32_wgrad(s)) return f32wgrad_workspace(s, false);
   WgradPlan pl = plan_wgrad(s);
   return (size_t)pl.nsplit * s.kd * s.kh * s.kw * s.ci * s.co * sizeof(float);
 }
@@ -686,6 +694,9 @@ hipError_t launch_conv_bwd_weight(const ConvShape &s, const void *x, const void 
   if (c16_wgrad_supported(s))
     return launch_conv_bwd_weight_c16(s, x, dz, nullptr, 0.f, dw, nullptr, ws, false, nullptr, st);
   if (use_direct_wgrad(s)) return launch_conv_bwd_weight_direct(s, x, dz, dw, ws, st);
+  if (use_f32_wgrad(s))
+    return launch_conv_bwd_weight_f32(s, (const float *)x, (const float *)dz, nullptr, 0.f, dw, nullptr, ws, false,
+                                      nullptr, st);
   WgradPlan pl = plan_wgrad(s);
   WgradParams p{};
   p.nb = s.n; p.d = s.d; p.h = s.h; p.w = s.w; p.ci = s.ci;

@@ -115,7 +115,10 @@ class ConvStack:
             sup = B.cf_conv3d_fused_supported(l["desc"], B.CF_FUSE_POOL2) if s["pool"] else 0
             # fused needs both fused kernels; a layer whose data gradient is needed keeps dz
             both = B.FUSED_FWD | B.FUSED_BWD_WEIGHT
-            l["fused"] = bool(self.fused and (sup & both) == both and (not needs_dgrad or sup & B.FUSED_BWD_DATA))
+            # a layer whose data gradient is needed also needs a fused backward-data, or a
+            # backward-weights that stores dz for the unfused backward-data
+            l["fused"] = bool(self.fused and (sup & both) == both and
+                              (not needs_dgrad or sup & (B.FUSED_BWD_DATA | B.FUSED_BWD_WEIGHT_DZ)))
             # otherwise conv + bias + leaky ReLU may still share one kernel (y written once)
             l["fused_act"] = bool(self.fused and not l["fused"] and B.cf_conv3d_fused_supported(l["desc"], 0) & 1)
             l["p"] = torch.empty((n,) + l["pool_dhw"] + (s["cout"],), dtype=tdt, device=dev) if s["pool"] else None

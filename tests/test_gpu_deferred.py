@@ -8,7 +8,7 @@ import pytest
 import torch
 
 from paper_1808_04728_amd import binding as B
-from tests._util import dev
+from tests._util import tdtype, dev
 
 pytestmark = pytest.mark.gpu
 
@@ -58,18 +58,19 @@ FCASES = [
 ]
 
 
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
 @pytest.mark.parametrize("case", FCASES, ids=lambda c: "n%d_%dx%dx%d_c%d-%d_k%d" % (c[0], *c[1], *c[2:]))
-def test_deferred_fused_wgrad_bitwise(case):
+def test_deferred_fused_wgrad_bitwise(case, dt):
     N, dhw, CI, CO, k = case
-    desc = B.make_desc(N, dhw, CI, CO, k, 1, "same", "bf16")
+    desc = B.make_desc(N, dhw, CI, CO, k, 1, "same", dt)
     sup = B.cf_conv3d_fused_supported(desc)
     if not sup & B.FUSED_BWD_WEIGHT:
         pytest.skip("no fused backward-weights kernel for this shape")
     rng = np.random.default_rng(22)
     od = B.cf_conv3d_out_shape(desc)
     pdhw = tuple(t // 2 for t in od)
-    x = dev(rng.standard_normal((N, *dhw, CI)), "bf16")
-    g = dev(rng.standard_normal((N, *pdhw, CO)), "bf16")
+    x = dev(rng.standard_normal((N, *dhw, CI)), dt)
+    g = dev(rng.standard_normal((N, *pdhw, CO)), dt)
     mask = torch.as_tensor(rng.integers(0, 256, B.cf_conv3d_mask_bytes(desc), dtype=np.uint8), device="cuda")
     ws = torch.empty(B.cf_conv3d_bwd_weight_fused_workspace_size(desc), dtype=torch.uint8, device="cuda")
     dw_ref = torch.empty((k, k, k, CI, CO), dtype=torch.float32, device="cuda")
@@ -83,7 +84,7 @@ def test_deferred_fused_wgrad_bitwise(case):
     torch.cuda.synchronize()
     assert torch.equal(dw, dw_ref) and torch.equal(db, db_ref)
     if sup & B.FUSED_BWD_WEIGHT_DZ:
-        dz_ref = torch.empty((N, *od, CO), dtype=torch.bfloat16, device="cuda")
+        dz_ref = torch.empty((N, *od, CO), dtype=tdtype(dt), device="cuda")
         B.cf_conv3d_bwd_weight_fused_dz(desc, x, g, mask, 0.2, B.CF_FUSE_POOL2, dw_ref, db_ref, dz_ref, ws)
         dz = torch.full_like(dz_ref, float("nan"))
         dw.fill_(float("nan"))

@@ -271,13 +271,13 @@ def test_fused_bwd_data(case, dt):
     assert e <= TOL[dt], e
 
 
-@pytest.mark.parametrize("dt", ["bf16"])
+@pytest.mark.parametrize("dt", ["f32", "bf16"])
 @pytest.mark.parametrize("case", FWD_CASES, ids=lambda c: "n%d_%dx%dx%d_c%d-%d_k%d" % (c[0], *c[1], *c[2:]))
 def test_fused_bwd_weight_dz(case, dt):
     """Backward-weights that also stores the rebuilt dz: dW, db bitwise equal to
     the plain fused call, every dz element written and equal to the oracle's
     dz within the path tolerance, and the unfused backward-data of that dz
-    bitwise equal to the fused backward-data."""
+    bitwise equal to the fused backward-data where the library has one."""
     N, dhw, CI, CO, k = case
     desc = B.make_desc(N, dhw, CI, CO, k, 1, "same", dt)
     if not B.cf_conv3d_fused_supported(desc) & B.FUSED_BWD_WEIGHT_DZ:
@@ -301,7 +301,9 @@ def test_fused_bwd_weight_dz(case, dt):
     B.cf_conv3d_bwd_weight_fused_dz(desc, x, g, mask, alpha, B.CF_FUSE_POOL2, dw2, db2, dz, ws)
     dx_f = torch.empty((N, *dhw, CI), dtype=tdtype(dt), device="cuda")
     dx_u = torch.full_like(dx_f, float("nan"))
-    B.cf_conv3d_bwd_data_fused(desc, g, mask, w, alpha, B.CF_FUSE_POOL2, dx_f)
+    has_fused_dgrad = bool(B.cf_conv3d_fused_supported(desc) & B.FUSED_BWD_DATA)
+    if has_fused_dgrad:
+        B.cf_conv3d_bwd_data_fused(desc, g, mask, w, alpha, B.CF_FUSE_POOL2, dx_f)
     B.cf_conv3d_bwd_data(desc, dz, w, dx_u)
     torch.cuda.synchronize()
     assert torch.equal(dw, dw2) and torch.equal(db, db2)
@@ -312,7 +314,8 @@ def test_fused_bwd_weight_dz(case, dt):
     assert np.isfinite(dz_np).all()
     e = maxabs_err(dz_np, dz_ref)
     assert e <= TOL[dt], e
-    assert torch.equal(dx_f, dx_u)
+    if has_fused_dgrad:
+        assert torch.equal(dx_f, dx_u)
     ref = oracle.conv3d_bwd_data(dz_ref, to_np(w), dhw)
     e = maxabs_err(to_np(dx_u), ref)
     assert e <= TOL[dt], e
