@@ -53,7 +53,6 @@ typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
 
 constexpr int F_MAX_CLS = 8;
 constexpr int F_MAX_TAPS = 64;
-constexpr uint32_t F_OOB = 0x80000000u;  // a byte offset past every buffer: the load returns zeros
 
 struct FClass {
   int m;                 // row tiles' unit count: rows (linear layout) or bricks (pooled layout)
@@ -175,10 +174,13 @@ __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__r
   const int nch = p.sc >> 4;
   const int mytaps = C.ntap > wk ? (C.ntap - wk + WK - 1) / WK : 0;
   const int nsteps = mytaps * nch;
+  // load cursor: tap, channel chunk, and the number of steps loaded so far; past
+  // the last real step the cursor stays put (valid weight addresses) and the A
+  // loads take the out-of-range offset, so padded steps multiply zeros
   int ti = wk, cc = 0, ldstep = 0;
   auto next = [&]() {
-    if (ldstep + 1 < nsteps) {
-      ++ldstep;
+    ++ldstep;
+    if (ldstep < nsteps) {
       if (++cc == nch) {
         cc = 0;
         ti += WK;
@@ -201,11 +203,15 @@ __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__r
   auto load = [&](u32x4_t(&a)[FM], uint32_t(&b)[NB][BW]) {
     const FTap &T = p.tap[C.tap0 + ti];
     const int cofs = cc * 16;
+    const bool live = ldstep < nsteps;
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
-      const bool ok = rok[i] && (unsigned)(rbd[i] + T.dd) < (unsigned)p.sd_ &&
-                      (unsigned)(rbh[i] + T.dh) < (unsigned)p.sh_ && (unsigned)(rbw[i] + T.dw) < (unsigned)p.sw_;
-      a[i] = ld128(srsrc, ok ? (uint32_t)(roff[i] + T.a_off + cofs) * 4u : F_OOB);
+      // bitwise, not short-circuit: one select per load, no branch
+      const bool ok = live & rok[i] & ((unsigned)(rbd[i] + T.dd) < (unsigned)p.sd_) &
+                      ((unsigned)(rbh[i] + T.dh) < (unsigned)p.sh_) & ((unsigned)(rbw[i] + T.dw) < (unsigned)p.sw_);
+      // a valid byte offset is below 2^31: setting bit 31 sends the load past the
+      // buffer (it returns zeros) without a select the compiler could turn into a branch
+      a[i] = ld128(srsrc, ((uint32_t)(roff[i] + T.a_off + cofs) * 4u) | ((uint32_t)!ok << 31));
     }
     const int wbase = T.w_off + cofs * (FWD ? p.wco : 1);
 #pragma unroll
@@ -230,8 +236,7 @@ __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__r
     for (int j = 0; j < FN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
   // Branch-free steady state: the step count is padded to a multiple of the
-  // ring size, the load cursor stops at the last real step (re-loading valid
-  // addresses), and padded steps multiply a zero A fragment.
+  // ring size; padded steps load zero A fragments (see the cursor).
   if (nsteps > 0) {
     const int niter = (nsteps + NS - 1) / NS * NS;
 #pragma unroll
@@ -245,10 +250,10 @@ __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__r
         const int s = s0 + q;
         load(a_r[(q + PF) % NS], b_r[(q + PF) % NS]);
         next();
-        const bool real = s < nsteps;
+        (void)s;
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
-          const u32x4_t av = real ? a_r[q][i] : u32x4_t{0u, 0u, 0u, 0u};
+          const u32x4_t av = a_r[q][i];
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
 #pragma unroll

@@ -41,8 +41,6 @@
 namespace cf {
 namespace {
 
-constexpr uint32_t W_OOB = 0x80000000u;  // past every buffer: the load returns zeros
-
 struct WF32Params {
   int n, d, h, w, ci;          // input
   int od, oh, ow, co;          // conv output
@@ -131,6 +129,7 @@ __global__ __launch_bounds__(64 * WV) void wgrad_f32_kernel(const float *__restr
   uint32_t m_r[NS];
   (void)m_r;
 
+  // step >= nsteps (ring padding) loads zeros: every voxel slot is past the slice
   auto load = [&](int step, u32x4_t(&a)[RU], float(&b)[FN], uint32_t &mw) {
     const int v = v0 + 4 * step + g4;
     const bool vok = v < v1;
@@ -141,23 +140,25 @@ __global__ __launch_bounds__(64 * WV) void wgrad_f32_kernel(const float *__restr
     const int base = (((nn * p.d + bd) * p.h + bh) * p.w + bw) * p.ci;
 #pragma unroll
     for (int i = 0; i < RU; ++i) {
-      const bool ok = vok && uok[i] && (unsigned)(bd + tkd[i]) < (unsigned)p.d &&
-                      (unsigned)(bh + tkh[i]) < (unsigned)p.h && (unsigned)(bw + tkw[i]) < (unsigned)p.w;
-      a[i] = ld128(xr, ok ? (uint32_t)(base + toff[i]) * 4u : W_OOB);
+      // bitwise, not short-circuit: one select per load, no branch
+      const bool ok = vok & uok[i] & ((unsigned)(bd + tkd[i]) < (unsigned)p.d) &
+                      ((unsigned)(bh + tkh[i]) < (unsigned)p.h) & ((unsigned)(bw + tkw[i]) < (unsigned)p.w);
+      // a valid byte offset is below 2^31: bit 31 sends the load past the buffer (zeros)
+      a[i] = ld128(xr, ((uint32_t)(base + toff[i]) * 4u) | ((uint32_t)!ok << 31));
     }
     if constexpr (FUSED) {
       const int pd_ = od_ >> 1, ph_ = oh_ >> 1, pw_ = ow_ >> 1;
-      const bool win = vok && pd_ < p.pod && ph_ < p.poh && pw_ < p.pow_;
+      const bool win = vok & (pd_ < p.pod) & (ph_ < p.poh) & (pw_ < p.pow_);
       const int pv = ((nn * p.pod + pd_) * p.poh + ph_) * p.pow_ + pw_;
 #pragma unroll
       for (int j = 0; j < FN; ++j)
-        b[j] = __uint_as_float(ld32(gr, win ? (uint32_t)(pv * p.co + co0 + 16 * j + r16) * 4u : W_OOB));
+        b[j] = __uint_as_float(ld32(gr, ((uint32_t)(pv * p.co + co0 + 16 * j + r16) * 4u) | ((uint32_t)!win << 31)));
       // the 32 channels of voxel v are one mask word (32 output channels)
-      mw = ld32(mr, vok ? (uint32_t)vv * 4u : W_OOB);
+      mw = ld32(mr, ((uint32_t)vv * 4u) | ((uint32_t)!vok << 31));
     } else {
 #pragma unroll
       for (int j = 0; j < FN; ++j)
-        b[j] = __uint_as_float(ld32(gr, vok ? (uint32_t)(vv * p.co + co0 + 16 * j + r16) * 4u : W_OOB));
+        b[j] = __uint_as_float(ld32(gr, ((uint32_t)(vv * p.co + co0 + 16 * j + r16) * 4u) | ((uint32_t)!vok << 31)));
     }
   };
 
@@ -176,18 +177,17 @@ __global__ __launch_bounds__(64 * WV) void wgrad_f32_kernel(const float *__restr
   if (nsteps > 0) {
     const int niter = (nsteps + NS - 1) / NS * NS;
 #pragma unroll
-    for (int q = 0; q < PF; ++q) load(min(q, nsteps - 1), a_r[q], b_r[q], m_r[q]);
+    for (int q = 0; q < PF; ++q) load(q, a_r[q], b_r[q], m_r[q]);
     for (int s0 = 0; s0 < niter; s0 += NS) {
 #pragma unroll
       for (int q = 0; q < NS; ++q) {
         const int s = s0 + q;
         const int sl = (q + PF) % NS;
-        load(min(s + PF, nsteps - 1), a_r[sl], b_r[sl], m_r[sl]);
-        const bool real = s < nsteps;
+        load(s + PF, a_r[sl], b_r[sl], m_r[sl]);
         float bv[FN];
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
-          float b = real ? b_r[q][j] : 0.f;
+          float b = b_r[q][j];
           if constexpr (FUSED) {
             const bool on = (m_r[q] >> ((co0 + 16 * j + r16) & 31)) & 1u;
             b *= on ? s1 : sa;
@@ -199,7 +199,7 @@ __global__ __launch_bounds__(64 * WV) void wgrad_f32_kernel(const float *__restr
 #pragma unroll
           for (int j = 0; j < FN; ++j) {
             dsum[j] += bv[j];
-            if (dz_out && real && v < v1) dz_out[(long long)v * p.co + co0 + 16 * j + r16] = bv[j];
+            if (dz_out && v < v1) dz_out[(long long)v * p.co + co0 + 16 * j + r16] = bv[j];
           }
         }
 #pragma unroll
