@@ -107,6 +107,12 @@ hipError_t launch_conv_bwd_data_f32(const ConvShape &s, const float *dz, const f
 // mask the forward's slope mask; db and (if dz_out) the rebuilt dz come from the
 // same pass
 bool f32wgrad_supported(const ConvShape &s);
+// the fused first layer in fp32 (one input channel, 16 outputs, 2^3 or 3^3): register-streamed
+// input windows, the bias gradient as an MFMA row of ones (conv_f32_wgrad.hip)
+bool l1f32_wgrad_supported(const ConvShape &s);
+size_t l1f32_wgrad_workspace(const ConvShape &s);
+hipError_t launch_l1_wgrad_f32(const ConvShape &s, const float *x, const float *dp, const uint16_t *mask,
+                               float alpha, float *dw, float *db, void *ws, hipStream_t st);
 bool f32wgrad_fused_supported(const ConvShape &s);
 size_t f32wgrad_workspace(const ConvShape &s, bool fused);
 hipError_t launch_conv_bwd_weight_f32(const ConvShape &s, const float *x, const float *g, const uint32_t *mask,

@@ -241,6 +241,147 @@ __global__ __launch_bounds__(64 * WV) void wgrad_f32_kernel(const float *__restr
   }
 }
 
+// ---------------------------------------------------------------------------
+// The single-input-channel first layer (fp32, 16 output channels, fused with
+// the pool and lReLU adjoints).  With one input channel every input voxel
+// feeds all k^3 taps, so a tap-per-row operand would load each voxel k^3
+// times.  Here lane l of fragment kw has row (kd, kh) = (l%16 / k, l%16 % k)
+// and K slot l/16 holding four consecutive voxels: the lane loads one window
+// of its (kd, kh) input row -- the aligned 16 bytes of its four voxels, the
+// voxel before and two after -- and takes the A operands of all k fragments
+// (kw = 0 .. k-1) from it by shifting.  Row k^2 of fragment 0 is a row of ones,
+// which makes the bias gradient db = sum_v dz a row of the same accumulators.
+// The gradient operand (B) is rebuilt per lane from the pooled gradient and
+// the mask (a lane's four voxels share two pooling windows along w).  A
+// wave walks 16-voxel segments of output rows; the eight waves of a
+// workgroup meet in LDS and write one partial row per workgroup.
+// ---------------------------------------------------------------------------
+
+struct L1F32Params {
+  int n, d, h, w;      // input
+  int od, oh, ow;      // conv output
+  int pd, ph;          // padding before (d, h)
+  int pod, poh, pow_;  // pooled extents
+  int total, per;      // 16-voxel row segments; per wave
+  FastDiv fs, fh, fd;  // segment decode: segments per row, oh, od
+  uint32_t x_bytes, g_bytes, m_bytes;
+  float alpha;
+};
+
+__device__ __forceinline__ float2 ld64f(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
+  const u32x2_t v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
+  return make_float2(__uint_as_float(v[0]), __uint_as_float(v[1]));
+}
+
+template <int KE, int PW, int WV, int PF>
+__global__ __launch_bounds__(64 * WV) void l1_wgrad_f32_kernel(const float *__restrict__ x,
+                                                               const float *__restrict__ dp,
+                                                               const uint16_t *__restrict__ mask16,
+                                                               float *__restrict__ part_w,
+                                                               float *__restrict__ part_b, const L1F32Params p) {
+  constexpr int R = KE * KE;  // (kd, kh) rows of a fragment
+  static_assert(R < 16 && PW <= 1 && KE - PW <= 3, "window of the voxel before and two after");
+  __shared__ float red[WV][KE][16][16];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int g4 = lane >> 4, r16 = lane & 15;
+  const bool rv = r16 < R;
+  const float ones = r16 == R ? 1.f : 0.f;
+  const int kd = rv ? r16 / KE : 0, kh = rv ? r16 % KE : 0;
+  const int gw = blockIdx.x * WV + wave;
+  const int s0 = gw * p.per, s1 = min(s0 + p.per, p.total);
+
+  const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc((void *)x, (short)0, p.x_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t gr = __builtin_amdgcn_make_buffer_rsrc((void *)dp, (short)0, p.g_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t mr = __builtin_amdgcn_make_buffer_rsrc((void *)mask16, (short)0, p.m_bytes, 0x00020000);
+
+  struct Ld {
+    u32x4_t cur;
+    float left;
+    float2 right;
+    float g0, g1;
+    float2 mk;  // the four voxels' 16-bit mask rows, as raw bits
+  };
+  constexpr int NS = PF + 1;
+  Ld ring[NS];
+  auto load = [&](int seg, Ld &L) {
+    const bool live = seg < s1;
+    const int sg = live ? seg : s0;
+    const int t1 = fdiv(sg, p.fs), t2 = fdiv(t1, p.fh), nn = fdiv(t2, p.fd);
+    const int ws = sg - t1 * (int)p.fs.div, oh_ = t1 - t2 * (int)p.fh.div, od_ = t2 - nn * (int)p.fd.div;
+    const int wv0 = ws * 16 + 4 * g4;  // this lane's first voxel along w
+    const int id = od_ + kd - p.pd, ih = oh_ + kh - p.ph;
+    const bool rowok = live & rv & ((unsigned)id < (unsigned)p.d) & ((unsigned)ih < (unsigned)p.h);
+    const uint32_t rb = (uint32_t)(((nn * p.d + id) * p.h + ih) * p.w + wv0) * 4u;
+    // a valid byte offset is below 2^31: bit 31 sends a masked lane past the buffer (zeros)
+    L.cur = ld128(xr, rb | ((uint32_t)!(rowok & (wv0 < p.w)) << 31));
+    L.left = __uint_as_float(ld32(xr, (rb - 4u) | ((uint32_t)!(rowok & (wv0 >= 1)) << 31)));
+    L.right = ld64f(xr, (rb + 16u) | ((uint32_t)!(rowok & (wv0 + 4 < p.w)) << 31));
+    const int pd_ = od_ >> 1, ph_ = oh_ >> 1, pw0 = wv0 >> 1;
+    const bool win = live & (pd_ < p.pod) & (ph_ < p.poh);
+    const uint32_t gb = (uint32_t)(((((nn * p.pod + pd_) * p.poh + ph_) * p.pow_ + pw0) * 16) + r16) * 4u;
+    L.g0 = __uint_as_float(ld32(gr, gb | ((uint32_t)!(win & (pw0 < p.pow_)) << 31)));
+    L.g1 = __uint_as_float(ld32(gr, (gb + 64u) | ((uint32_t)!(win & (pw0 + 1 < p.pow_)) << 31)));
+    const uint32_t mb = (uint32_t)(((nn * p.od + od_) * p.oh + oh_) * p.ow + wv0) * 2u;
+    L.mk = ld64f(mr, mb | ((uint32_t)!(live & (wv0 < p.ow)) << 31));
+  };
+
+  f32x4_t acc[KE];
+#pragma unroll
+  for (int k = 0; k < KE; ++k) acc[k] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  const float s1v = 0.125f, sav = 0.125f * p.alpha;
+  const int nsteps = s1 > s0 ? s1 - s0 : 0;
+  if (nsteps > 0) {
+    const int niter = (nsteps + NS - 1) / NS * NS;
+#pragma unroll
+    for (int q = 0; q < PF; ++q) load(s0 + q, ring[q]);
+    for (int b0 = 0; b0 < niter; b0 += NS) {
+#pragma unroll
+      for (int q = 0; q < NS; ++q) {
+        load(s0 + b0 + q + PF, ring[(q + PF) % NS]);
+        const Ld &L = ring[q];
+        // window E[k] = x[wv0 - 1 + k], k = 0 .. 6
+        const float E[7] = {L.left, __uint_as_float(L.cur[0]), __uint_as_float(L.cur[1]),
+                            __uint_as_float(L.cur[2]), __uint_as_float(L.cur[3]), L.right.x, L.right.y};
+        const uint32_t m01 = __float_as_uint(L.mk.x), m23 = __float_as_uint(L.mk.y);
+        const uint32_t mb[4] = {m01, m01 >> 16, m23, m23 >> 16};
+        float dz[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) dz[j] = (j < 2 ? L.g0 : L.g1) * (((mb[j] >> r16) & 1u) ? s1v : sav);
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int kw = 0; kw < KE; ++kw) {
+            const float a = rv ? E[kw - PW + 1 + j] : (kw == 0 ? ones : 0.f);
+            acc[kw] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, dz[j], acc[kw], 0, 0, 0);
+          }
+      }
+    }
+  }
+
+  // D row 4 (l/16) + e of fragment kw = (kd, kh) row, or the bias row R; column l%16
+#pragma unroll
+  for (int kw = 0; kw < KE; ++kw)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) red[wave][kw][4 * g4 + e][r16] = acc[kw][e];
+  __syncthreads();
+  constexpr int TAPS = KE * KE * KE;
+  for (int i = threadIdx.x; i < (TAPS + 1) * 16; i += 64 * WV) {
+    const int row = i >> 4, co = i & 15;
+    int kw = 0, rr = R;  // the bias row
+    if (row < TAPS) {
+      kw = row % KE;
+      rr = row / KE;  // (kd, kh) = (row / KE / KE, row / KE % KE): fragment row kd * KE + kh
+    }
+    float s = 0.f;
+#pragma unroll
+    for (int w = 0; w < WV; ++w) s += red[w][kw][rr][co];
+    if (row < TAPS) part_w[(long long)blockIdx.x * TAPS * 16 + i] = s;
+    else part_b[(long long)blockIdx.x * 16 + co] = s;
+  }
+}
+
 struct WPlan {
   bool kw4;
   int ru, fn, wv;
@@ -316,6 +457,59 @@ hipError_t launch_wu(const WPlan &pl, const WF32Params &p, const float *x, const
 }
 
 }  // namespace
+
+namespace {
+constexpr int kL1Blocks = kNumCUs;  // one workgroup of eight waves per compute unit
+
+L1F32Params l1_params(const ConvShape &s, float alpha) {
+  L1F32Params p{};
+  p.n = s.n; p.d = s.d; p.h = s.h; p.w = s.w;
+  p.od = s.od; p.oh = s.oh; p.ow = s.ow;
+  p.pd = s.pd; p.ph = s.ph;
+  p.pod = s.od / 2; p.poh = s.oh / 2; p.pow_ = s.ow / 2;
+  const int nseg = (s.ow + 15) / 16;
+  p.total = s.n * s.od * s.oh * nseg;
+  p.per = (p.total + kL1Blocks * 8 - 1) / (kL1Blocks * 8);
+  p.fs = make_fastdiv(nseg);
+  p.fh = make_fastdiv(s.oh);
+  p.fd = make_fastdiv(s.od);
+  p.x_bytes = (uint32_t)((long long)s.n * s.d * s.h * s.w * 4);
+  p.g_bytes = (uint32_t)((long long)s.n * p.pod * p.poh * p.pow_ * 16 * 4);
+  p.m_bytes = (uint32_t)((long long)s.n * s.od * s.oh * s.ow * 2);
+  p.alpha = alpha;
+  return p;
+}
+}  // namespace
+
+bool l1f32_wgrad_supported(const ConvShape &s) {
+  const long long xin = (long long)s.n * s.d * s.h * s.w, vout = (long long)s.n * s.od * s.oh * s.ow;
+  return s.dtype == DT_F32 && s.ci == 1 && s.co == 16 && s.sd == 1 && s.sh == 1 && s.sw == 1 && s.kd == s.kh &&
+         s.kd == s.kw && (s.kd == 2 || s.kd == 3) && s.pw <= 1 && s.kd - s.pw <= 3 && s.w % 4 == 0 &&
+         s.ow % 4 == 0 && s.od >= 2 && s.oh >= 2 && xin * 4 < (1LL << 31) && vout * 64 < (1LL << 31);
+}
+
+size_t l1f32_wgrad_workspace(const ConvShape &s) {
+  return (size_t)kL1Blocks * (s.kd * s.kh * s.kw + 1) * 16 * sizeof(float);
+}
+
+hipError_t launch_l1_wgrad_f32(const ConvShape &s, const float *x, const float *dp, const uint16_t *mask,
+                               float alpha, float *dw, float *db, void *ws, hipStream_t st) {
+  const L1F32Params p = l1_params(s, alpha);
+  const int taps = s.kd * s.kh * s.kw;
+  float *pw = (float *)ws;
+  float *pb = pw + (size_t)kL1Blocks * taps * 16;
+  if (s.kd == 2)
+    hipLaunchKernelGGL((l1_wgrad_f32_kernel<2, 0, 8, 2>), dim3(kL1Blocks), dim3(512), 0, st, x, dp, mask, pw, pb, p);
+  else if (s.pw == 0)
+    hipLaunchKernelGGL((l1_wgrad_f32_kernel<3, 0, 8, 2>), dim3(kL1Blocks), dim3(512), 0, st, x, dp, mask, pw, pb, p);
+  else
+    hipLaunchKernelGGL((l1_wgrad_f32_kernel<3, 1, 8, 2>), dim3(kL1Blocks), dim3(512), 0, st, x, dp, mask, pw, pb, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  e = launch_sum_rows(pw, dw, kL1Blocks, taps * 16, st);
+  if (e != hipSuccess) return e;
+  return launch_sum_rows(pb, db, kL1Blocks, 16, st);
+}
 
 bool f32wgrad_supported(const ConvShape &s) {
   if (s.dtype != DT_F32 || s.co % 16 != 0) return false;

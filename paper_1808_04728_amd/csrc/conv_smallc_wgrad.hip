@@ -725,6 +725,7 @@ bool smallc_wgrad_fused_supported(const ConvShape &s) {
 }
 
 size_t smallc_wgrad_fused_workspace(const ConvShape &s) {
+  if (l1f32_wgrad_supported(s)) return l1f32_wgrad_workspace(s);
   WPlan w = plan(s);
   const int M = s.kd * s.kh * s.kw * s.ci;
   return (size_t)w.blocks * (M + 1) * s.co * sizeof(float);
@@ -732,6 +733,8 @@ size_t smallc_wgrad_fused_workspace(const ConvShape &s) {
 
 hipError_t launch_smallc_wgrad_fused(const ConvShape &s, const void *x, const void *dp, const uint16_t *mask,
                                      float alpha, float *dw, float *db, void *ws, hipStream_t st) {
+  if (l1f32_wgrad_supported(s))
+    return launch_l1_wgrad_f32(s, (const float *)x, (const float *)dp, mask, alpha, dw, db, ws, st);
   WPlan w = plan(s);
   const SmallcParams p = params(s, w);
   const int M = s.kd * s.kh * s.kw * s.ci;

@@ -327,19 +327,22 @@ VALID_L1_CASES = [
     (2, (12, 10, 48), 3),    # out (10, 8, 46)
     (1, (9, 12, 128), 3),    # out (7, 10, 126): the paper's first-layer width
     (1, (10, 10, 40), 2),    # out (9, 9, 39): odd width
+    (2, (12, 10, 50), 3),    # out (10, 8, 48): the fp32 register-window kernel without padding
+    (1, (11, 10, 41), 2),    # out (10, 9, 40)
 ]
 
 
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
 @pytest.mark.parametrize("case", VALID_L1_CASES, ids=lambda c: "n%d_%dx%dx%d_k%d" % (c[0], *c[1], c[2]))
-def test_fused_bwd_weight_first_layer_valid(case):
+def test_fused_bwd_weight_first_layer_valid(case, dt):
     N, dhw, k = case
-    desc = B.make_desc(N, dhw, 1, 16, k, 1, "valid", "bf16")
+    desc = B.make_desc(N, dhw, 1, 16, k, 1, "valid", dt)
     assert B.cf_conv3d_fused_supported(desc) & B.FUSED_BWD_WEIGHT
     rng = np.random.default_rng(16)
     od = B.cf_conv3d_out_shape(desc)
     pdhw = tuple(t // 2 for t in od)
-    x = dev(rng.standard_normal((N, *dhw, 1)), "bf16")
-    g = dev(rng.standard_normal((N, *pdhw, 16)), "bf16")
+    x = dev(rng.standard_normal((N, *dhw, 1)), dt)
+    g = dev(rng.standard_normal((N, *pdhw, 16)), dt)
     nbits = N * od[0] * od[1] * od[2] * 16
     mbytes = B.cf_conv3d_mask_bytes(desc)
     mask_np = rng.integers(0, 256, mbytes, dtype=np.uint8)
@@ -352,6 +355,6 @@ def test_fused_bwd_weight_first_layer_valid(case):
     bits = np.unpackbits(mask_np, bitorder="little")[:nbits].astype(bool).reshape((N, *od, 16))
     dz = oracle.avgpool3d_bwd(to_np(g), od) * np.where(bits, 1.0, 0.2)
     e = maxabs_err(to_np(dw), oracle.conv3d_bwd_weight(to_np(x), dz, k, pad="valid"))
-    assert e <= TOL["bf16"], e
+    assert e <= TOL[dt], e
     e = maxabs_err(to_np(db), dz.reshape(-1, 16).sum(0))
     assert e <= TOL["f32"], e
