@@ -44,6 +44,7 @@
 
 #include <algorithm>
 #include <cstdlib>
+#include <type_traits>
 
 namespace cf {
 namespace {
@@ -93,9 +94,31 @@ __device__ __forceinline__ float f_of(uint32_t u) { return __uint_as_float(u); }
 
 __device__ __forceinline__ float lrelu(float u, float a) { return u > 0.f ? u : a * u; }
 
+// Shift mode: the operand of lane m (m = lane % 16) for kernel column uw is
+// that of voxel m + uw (forward) or m - uw (backward-data) of the same
+// 16-voxel fragment, a DPP row shift of the uw = 0 operand a; the lanes the
+// shift leaves without a source take the edge fragment e (the next 16 voxels
+// forward, the previous 16 backward) rotated into place.
+template <int UWI, bool FWD>
+__device__ __forceinline__ uint32_t shift_lane(uint32_t a, uint32_t e) {
+  if constexpr (UWI == 0) {
+    return a;
+  } else {
+    const int ed = __builtin_amdgcn_update_dpp(0, (int)e, FWD ? 0x120 + 16 - UWI : 0x120 + UWI, 0xf, 0xf, false);
+    return (uint32_t)__builtin_amdgcn_update_dpp(ed, (int)a, FWD ? 0x100 + UWI : 0x110 + UWI, 0xf, 0xf, false);
+  }
+}
+
 // EPI: 0 store the contraction, 1 bias + leaky ReLU (+ slope mask if mask != 0),
 // 2 bias + leaky ReLU + slope mask + 2^3 average pool (forward, brick rows).
-template <bool FWD, int FM, int FN, int WM, int WK, int PF, int EPI>
+// UW > 0 (shift mode, a stride-1 class whose UW taps along w are consecutive in
+// the tap table, destination w extent a multiple of 16): a k-step is one kernel
+// row (kd, kh) x 16 channels.  A fragment's 16 lanes are 16 consecutive voxels
+// along w, so the operand of tap column uw is the uw = 0 operand moved uw lanes
+// along the 16-lane row (DPP row shift), the lanes shifted in at the edge coming
+// from a second fragment 16 voxels further along (row rotate): two loads per
+// fragment and kernel row instead of UW.
+template <bool FWD, int FM, int FN, int WM, int WK, int PF, int EPI, int UW = 0>
 __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__restrict__ src,
                                                                 const float *__restrict__ wt,
                                                                 const float *__restrict__ bias,
@@ -170,63 +193,6 @@ __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__r
     roff[i] = (((n * p.sd_ + rbd[i]) * p.sh_ + rbh[i]) * p.sw_ + rbw[i]) * p.sc + 4 * g4;
   }
 
-  // ---- this wave's k-steps: taps wk, wk + WK, ... of the class, 16 channels each
-  const int nch = p.sc >> 4;
-  const int mytaps = C.ntap > wk ? (C.ntap - wk + WK - 1) / WK : 0;
-  const int nsteps = mytaps * nch;
-  // load cursor: tap, channel chunk, and the number of steps loaded so far; past
-  // the last real step the cursor stays put (valid weight addresses) and the A
-  // loads take the out-of-range offset, so padded steps multiply zeros
-  int ti = wk, cc = 0, ldstep = 0;
-  auto next = [&]() {
-    ++ldstep;
-    if (ldstep < nsteps) {
-      if (++cc == nch) {
-        cc = 0;
-        ti += WK;
-      }
-    }
-  };
-
-  // lane part of the weight element offsets
-  constexpr int NB = FWD ? 4 : FN;  // weight loads per k-step
-  int wl[NB];
-#pragma unroll
-  for (int v = 0; v < NB; ++v)
-    wl[v] = FWD ? (4 * g4 + v) * p.wco + n0 + FN * r16      // W[t][4g + v][n0 + FN r ..]
-                : (n0 + 16 * v + r16) * p.wco + 4 * g4;     // W[t][n0 + 16 v + r][4g ..]
-
-  constexpr int NS = PF + 1;
-  constexpr int BW = FWD ? FN : 4;  // floats per weight load
-  u32x4_t a_r[NS][FM];
-  uint32_t b_r[NS][NB][BW];
-  auto load = [&](u32x4_t(&a)[FM], uint32_t(&b)[NB][BW]) {
-    const FTap &T = p.tap[C.tap0 + ti];
-    const int cofs = cc * 16;
-    const bool live = ldstep < nsteps;
-#pragma unroll
-    for (int i = 0; i < FM; ++i) {
-      // bitwise, not short-circuit: one select per load, no branch
-      const bool ok = live & rok[i] & ((unsigned)(rbd[i] + T.dd) < (unsigned)p.sd_) &
-                      ((unsigned)(rbh[i] + T.dh) < (unsigned)p.sh_) & ((unsigned)(rbw[i] + T.dw) < (unsigned)p.sw_);
-      // a valid byte offset is below 2^31: setting bit 31 sends the load past the
-      // buffer (it returns zeros) without a select the compiler could turn into a branch
-      a[i] = ld128(srsrc, ((uint32_t)(roff[i] + T.a_off + cofs) * 4u) | ((uint32_t)!ok << 31));
-    }
-    const int wbase = T.w_off + cofs * (FWD ? p.wco : 1);
-#pragma unroll
-    for (int v = 0; v < NB; ++v) {
-      const uint32_t off = (uint32_t)(wl[v] + wbase) * 4u;
-      if constexpr (BW == 4) {
-        const u32x4_t q = ld128(wrsrc, off);
-        b[v][0] = q[0]; b[v][1] = q[1]; b[v][2] = q[2]; b[v][3] = q[3];
-      } else if constexpr (BW == 2) {
-        const u32x2_t q = ld64(wrsrc, off);
-        b[v][0] = q[0]; b[v][1] = q[1];
-      }
-    }
-  };
-
   // accumulators: forward acc[i][jj] holds columns co = n0 + FN*n + jj;
   // backward-data acc[i][v] holds columns n0 + 16 v + n
   f32x4_t acc[FM][FN];
@@ -235,36 +201,188 @@ __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__r
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  // Branch-free steady state: the step count is padded to a multiple of the
-  // ring size; padded steps load zero A fragments (see the cursor).
-  if (nsteps > 0) {
-    const int niter = (nsteps + NS - 1) / NS * NS;
+  if constexpr (UW > 0) {
+    // ---- shift mode: k-steps are kernel rows (UW taps) x 16 channels ---------
+    const int nch = p.sc >> 4;
+    const int nrows = C.ntap / UW;
+    const int myrows = nrows > wk ? (nrows - wk + WK - 1) / WK : 0;
+    const int nsteps = myrows * nch;
+    int ri = wk, cc = 0, ldstep = 0;
+    auto next = [&]() {
+      ++ldstep;
+      if (ldstep < nsteps) {
+        if (++cc == nch) {
+          cc = 0;
+          ri += WK;
+        }
+      }
+    };
+    constexpr int NB = FWD ? 4 : FN;
+    constexpr int BW = FWD ? FN : 4;
+    int wl[NB];
 #pragma unroll
-    for (int q = 0; q < PF; ++q) {
-      load(a_r[q], b_r[q]);
-      next();
-    }
-    for (int s0 = 0; s0 < niter; s0 += NS) {
+    for (int v = 0; v < NB; ++v)
+      wl[v] = FWD ? (4 * g4 + v) * p.wco + n0 + FN * r16 : (n0 + 16 * v + r16) * p.wco + 4 * g4;
+    constexpr int EDGE = FWD ? 16 : -16;  // voxels from a fragment to its edge fragment
+    constexpr int NS = PF + 1;
+    u32x4_t a_r[NS][FM], e_r[NS][FM];
+    uint32_t b_r[NS][UW][NB][BW];
+    auto load = [&](u32x4_t(&a)[FM], u32x4_t(&e)[FM], uint32_t(&b)[UW][NB][BW]) {
+      const FTap &T = p.tap[C.tap0 + ri * UW];
+      const int cofs = cc * 16;
+      const bool live = ldstep < nsteps;
 #pragma unroll
-      for (int q = 0; q < NS; ++q) {
-        const int s = s0 + q;
-        load(a_r[(q + PF) % NS], b_r[(q + PF) % NS]);
+      for (int i = 0; i < FM; ++i) {
+        const bool dh = live & rok[i] & ((unsigned)(rbd[i] + T.dd) < (unsigned)p.sd_) &
+                        ((unsigned)(rbh[i] + T.dh) < (unsigned)p.sh_);
+        const int w0 = rbw[i] + T.dw;
+        const bool oka = dh & ((unsigned)w0 < (unsigned)p.sw_);
+        const bool oke = dh & ((unsigned)(w0 + EDGE) < (unsigned)p.sw_);
+        const int o = roff[i] + T.a_off + cofs;
+        a[i] = ld128(srsrc, ((uint32_t)o * 4u) | ((uint32_t)!oka << 31));
+        e[i] = ld128(srsrc, ((uint32_t)(o + EDGE * p.sc) * 4u) | ((uint32_t)!oke << 31));
+      }
+#pragma unroll
+      for (int uw = 0; uw < UW; ++uw) {
+        const int wbase = p.tap[C.tap0 + ri * UW + uw].w_off + cofs * (FWD ? p.wco : 1);
+#pragma unroll
+        for (int v = 0; v < NB; ++v) {
+          const uint32_t off = (uint32_t)(wl[v] + wbase) * 4u;
+          if constexpr (BW == 4) {
+            const u32x4_t q = ld128(wrsrc, off);
+            b[uw][v][0] = q[0]; b[uw][v][1] = q[1]; b[uw][v][2] = q[2]; b[uw][v][3] = q[3];
+          } else {
+            const u32x2_t q = ld64(wrsrc, off);
+            b[uw][v][0] = q[0]; b[uw][v][1] = q[1];
+          }
+        }
+      }
+    };
+    if (nsteps > 0) {
+      const int niter = (nsteps + NS - 1) / NS * NS;
+#pragma unroll
+      for (int q = 0; q < PF; ++q) {
+        load(a_r[q], e_r[q], b_r[q]);
         next();
-        (void)s;
+      }
+      for (int s0 = 0; s0 < niter; s0 += NS) {
 #pragma unroll
-        for (int i = 0; i < FM; ++i) {
-          const u32x4_t av = a_r[q][i];
+        for (int q = 0; q < NS; ++q) {
+          load(a_r[(q + PF) % NS], e_r[(q + PF) % NS], b_r[(q + PF) % NS]);
+          next();
+          auto column = [&](auto uwc) {
+            constexpr int uw = decltype(uwc)::value;
 #pragma unroll
-          for (int j = 0; j < 4; ++j) {
+            for (int i = 0; i < FM; ++i) {
+              u32x4_t av;
 #pragma unroll
-            for (int v = 0; v < FN; ++v) {
-              const float bv = FWD ? f_of(b_r[q][j][v]) : f_of(b_r[q][v][j]);
-              acc[i][v] = __builtin_amdgcn_mfma_f32_16x16x4f32(f_of(av[j]), bv, acc[i][v], 0, 0, 0);
+              for (int j = 0; j < 4; ++j) av[j] = shift_lane<uw, FWD>(a_r[q][i][j], e_r[q][i][j]);
+#pragma unroll
+              for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int v = 0; v < FN; ++v) {
+                  const float bv = FWD ? f_of(b_r[q][uw][j][v]) : f_of(b_r[q][uw][v][j]);
+                  acc[i][v] = __builtin_amdgcn_mfma_f32_16x16x4f32(f_of(av[j]), bv, acc[i][v], 0, 0, 0);
+                }
+            }
+          };
+          column(std::integral_constant<int, 0>{});
+          if constexpr (UW > 1) column(std::integral_constant<int, 1>{});
+          if constexpr (UW > 2) column(std::integral_constant<int, 2>{});
+          if constexpr (UW > 3) column(std::integral_constant<int, 3>{});
+        }
+      }
+    }
+  } else {
+  // ---- this wave's k-steps: taps wk, wk + WK, ... of the class, 16 channels each
+    const int nch = p.sc >> 4;
+    const int mytaps = C.ntap > wk ? (C.ntap - wk + WK - 1) / WK : 0;
+    const int nsteps = mytaps * nch;
+    // load cursor: tap, channel chunk, and the number of steps loaded so far; past
+    // the last real step the cursor stays put (valid weight addresses) and the A
+    // loads take the out-of-range offset, so padded steps multiply zeros
+    int ti = wk, cc = 0, ldstep = 0;
+    auto next = [&]() {
+      ++ldstep;
+      if (ldstep < nsteps) {
+        if (++cc == nch) {
+          cc = 0;
+          ti += WK;
+        }
+      }
+    };
+  
+    // lane part of the weight element offsets
+    constexpr int NB = FWD ? 4 : FN;  // weight loads per k-step
+    int wl[NB];
+  #pragma unroll
+    for (int v = 0; v < NB; ++v)
+      wl[v] = FWD ? (4 * g4 + v) * p.wco + n0 + FN * r16      // W[t][4g + v][n0 + FN r ..]
+                  : (n0 + 16 * v + r16) * p.wco + 4 * g4;     // W[t][n0 + 16 v + r][4g ..]
+  
+    constexpr int NS = PF + 1;
+    constexpr int BW = FWD ? FN : 4;  // floats per weight load
+    u32x4_t a_r[NS][FM];
+    uint32_t b_r[NS][NB][BW];
+    auto load = [&](u32x4_t(&a)[FM], uint32_t(&b)[NB][BW]) {
+      const FTap &T = p.tap[C.tap0 + ti];
+      const int cofs = cc * 16;
+      const bool live = ldstep < nsteps;
+  #pragma unroll
+      for (int i = 0; i < FM; ++i) {
+        // bitwise, not short-circuit: one select per load, no branch
+        const bool ok = live & rok[i] & ((unsigned)(rbd[i] + T.dd) < (unsigned)p.sd_) &
+                        ((unsigned)(rbh[i] + T.dh) < (unsigned)p.sh_) & ((unsigned)(rbw[i] + T.dw) < (unsigned)p.sw_);
+        // a valid byte offset is below 2^31: setting bit 31 sends the load past the
+        // buffer (it returns zeros) without a select the compiler could turn into a branch
+        a[i] = ld128(srsrc, ((uint32_t)(roff[i] + T.a_off + cofs) * 4u) | ((uint32_t)!ok << 31));
+      }
+      const int wbase = T.w_off + cofs * (FWD ? p.wco : 1);
+  #pragma unroll
+      for (int v = 0; v < NB; ++v) {
+        const uint32_t off = (uint32_t)(wl[v] + wbase) * 4u;
+        if constexpr (BW == 4) {
+          const u32x4_t q = ld128(wrsrc, off);
+          b[v][0] = q[0]; b[v][1] = q[1]; b[v][2] = q[2]; b[v][3] = q[3];
+        } else if constexpr (BW == 2) {
+          const u32x2_t q = ld64(wrsrc, off);
+          b[v][0] = q[0]; b[v][1] = q[1];
+        }
+      }
+    };
+  
+    // Branch-free steady state: the step count is padded to a multiple of the
+    // ring size; padded steps load zero A fragments (see the cursor).
+    if (nsteps > 0) {
+      const int niter = (nsteps + NS - 1) / NS * NS;
+  #pragma unroll
+      for (int q = 0; q < PF; ++q) {
+        load(a_r[q], b_r[q]);
+        next();
+      }
+      for (int s0 = 0; s0 < niter; s0 += NS) {
+  #pragma unroll
+        for (int q = 0; q < NS; ++q) {
+          const int s = s0 + q;
+          load(a_r[(q + PF) % NS], b_r[(q + PF) % NS]);
+          next();
+          (void)s;
+  #pragma unroll
+          for (int i = 0; i < FM; ++i) {
+            const u32x4_t av = a_r[q][i];
+  #pragma unroll
+            for (int j = 0; j < 4; ++j) {
+  #pragma unroll
+              for (int v = 0; v < FN; ++v) {
+                const float bv = FWD ? f_of(b_r[q][j][v]) : f_of(b_r[q][v][j]);
+                acc[i][v] = __builtin_amdgcn_mfma_f32_16x16x4f32(f_of(av[j]), bv, acc[i][v], 0, 0, 0);
+              }
             }
           }
         }
       }
     }
+  
   }
 
   // ---- partial tiles meet in LDS -------------------------------------------
@@ -436,38 +554,68 @@ struct FCfg {
   int fm, wm, wk;
 };
 
-// the tile shapes instantiated for the linear layout
-constexpr FCfg kCand[] = {{4, 1, 1}, {4, 2, 1}, {2, 2, 1}, {4, 1, 4}, {2, 1, 4}, {1, 1, 4}, {1, 1, 8}};
+// the tile shapes instantiated for the linear layout (fm, wm, wk)
+constexpr FCfg kCand[] = {{4, 1, 1}, {4, 2, 1}, {2, 2, 1}, {4, 1, 4}, {2, 1, 4}, {1, 1, 4}, {1, 1, 8}, {2, 1, 8}};
+constexpr int kNCand = sizeof(kCand) / sizeof(kCand[0]);
 
-template <bool FWD, int FN, int EPI, int FM, int WM, int WK>
+template <bool FWD, int FN, int EPI, int FM, int WM, int WK, int UW = 0>
 hipError_t launch_f(const FParams &p, int tiles, const float *src, const float *w, const float *bias, float *dst,
                     uint8_t *mask, hipStream_t st) {
   dim3 grid((unsigned)tiles, p.dc / (16 * FN), 1);
   if (grid.x == 0 || grid.y == 0) return hipSuccess;
-  constexpr int PF = 2;
-  hipLaunchKernelGGL((conv_f32_kernel<FWD, FM, FN, WM, WK, PF, EPI>), grid, dim3(64 * WM * WK), 0, st, src, w,
+  // shift-mode k-steps hold UW taps: one step of prefetch covers the latency
+  constexpr int PF = UW > 0 ? 1 : 2;
+  hipLaunchKernelGGL((conv_f32_kernel<FWD, FM, FN, WM, WK, PF, EPI, UW>), grid, dim3(64 * WM * WK), 0, st, src, w,
                      bias, dst, mask, p);
   return hipGetLastError();
 }
 
+// shift mode applies to one stride-1 class (forward, or backward-data of a
+// stride-1 layer) with 4 taps along w, a destination w extent that is a
+// multiple of 16 (every fragment is 16 consecutive voxels of one row) and
+// source w stride 1.  CF_F32_SHIFT=0 turns it off, =1 uses it wherever it
+// applies, whatever the size (the tests cover both on small shapes).
+int f_shift_env() {
+  const char *e = getenv("CF_F32_SHIFT");
+  return e ? (e[0] == '0' ? 0 : 1) : -1;
+}
+bool f_shift_ok(const ConvShape &s, const FParams &p) {
+  if (f_shift_env() == 0) return false;
+  return p.ncls == 1 && s.sw == 1 && s.kw == 4 && p.dw % 16 == 0 && p.bstr_w == 1 && p.ostr_w == 1;
+}
+
+// Relative cost of a tile shape: a wave's MFMAs (k-steps x 4 x FM x FN) plus a
+// fixed per-wave overhead (prologue, reduction, epilogue; about 200 MFMAs,
+// fitted to the stack's layers), times the rounds of 2048 waves (two per SIMD)
+// the launch needs.  Ranks the shapes as measured on the 16 -> 32 layer and
+// the deep layers at batch 1.
+double f_cost(FParams &p, const FCfg &c, int fn) {
+  const long long ny = p.dc / (16 * fn);
+  const long long waves = (long long)f_assign(p, 16 * c.fm * c.wm) * ny * c.wm * c.wk;
+  int maxtap = 0;
+  for (int k = 0; k < p.ncls; ++k) maxtap = std::max(maxtap, p.cls[k].ntap);
+  const double steps = (double)((maxtap + c.wk - 1) / c.wk) * (p.sc / 16);
+  const double rounds = std::max(1.0, (double)waves / (8.0 * kNumCUs));
+  return rounds * (steps * 4.0 * c.fm * fn + 200.0);
+}
+
 template <bool FWD, int FN, int EPI>
-hipError_t launch_lin(FParams &p, const float *src, const float *w, const float *bias, float *dst, uint8_t *mask,
-                      hipStream_t st) {
-  // the largest row tile that still gives >= 2 workgroups per compute unit
-  // (one per CU with the K-split tiles), else the most K-split tile
-  const int ny = p.dc / (16 * FN);
-  int pick = 6;
-  // CF_F32_TILE=i forces candidate i (the tests cover every one this way)
-  const char *forced = getenv("CF_F32_TILE");
-  for (int i = forced ? 7 : 0; i < 7; ++i) {
-    const FCfg &c = kCand[i];
-    const long long wgs = (long long)f_assign(p, 16 * c.fm * c.wm) * ny;
-    if (wgs >= (c.wk > 1 ? 1 : 2) * (long long)kNumCUs) {
+hipError_t launch_lin(const ConvShape &s, FParams &p, const float *src, const float *w, const float *bias, float *dst,
+                      uint8_t *mask, hipStream_t st) {
+  if (f_shift_ok(s, p) && !getenv("CF_F32_TILE") &&
+      (f_shift_env() == 1 || f_assign(p, 64) * (p.dc / (16 * FN)) >= 4 * kNumCUs))
+    return launch_f<FWD, FN, EPI, 4, 1, 1, 4>(p, f_assign(p, 64), src, w, bias, dst, mask, st);
+  int pick = 0;
+  double best = 0.0;
+  for (int i = 0; i < kNCand; ++i) {
+    const double c = f_cost(p, kCand[i], FN);
+    if (i == 0 || c < best) {
+      best = c;
       pick = i;
-      break;
     }
   }
-  if (forced) pick = std::min(6, std::max(0, atoi(forced)));
+  // CF_F32_TILE=i forces candidate i (the tests cover every one this way)
+  if (const char *forced = getenv("CF_F32_TILE")) pick = std::min(kNCand - 1, std::max(0, atoi(forced)));
   const FCfg c = kCand[pick];
   const int tiles = f_assign(p, 16 * c.fm * c.wm);
 #define CF_F32_CASE(I, FM_, WM_, WK_) \
@@ -479,7 +627,8 @@ hipError_t launch_lin(FParams &p, const float *src, const float *w, const float 
     CF_F32_CASE(3, 4, 1, 4)
     CF_F32_CASE(4, 2, 1, 4)
     CF_F32_CASE(5, 1, 1, 4)
-    default: return launch_f<FWD, FN, EPI, 1, 1, 8>(p, tiles, src, w, bias, dst, mask, st);
+    CF_F32_CASE(6, 1, 1, 8)
+    default: return launch_f<FWD, FN, EPI, 2, 1, 8>(p, tiles, src, w, bias, dst, mask, st);
   }
 #undef CF_F32_CASE
 }
@@ -502,8 +651,8 @@ bool f32conv_supported(const ConvShape &s, bool fwd) {
 }
 
 bool f32conv_pool_supported(const ConvShape &s) {
-  return f32conv_supported(s, true) && s.sd == 1 && s.sh == 1 && s.sw == 1 && s.co == 32 && s.od >= 2 &&
-         s.oh >= 2 && s.ow >= 2;
+  // any stride: the bricks are laid over output voxels; 32 output channels per workgroup
+  return f32conv_supported(s, true) && s.co % 32 == 0 && s.od >= 2 && s.oh >= 2 && s.ow >= 2;
 }
 
 hipError_t launch_conv_fwd_f32(const ConvShape &s, const float *x, const float *w, const float *bias, float alpha,
@@ -522,23 +671,27 @@ hipError_t launch_conv_fwd_f32(const ConvShape &s, const float *x, const float *
     C.fd = make_fastdiv(bd);
     p.pod = s.od / 2; p.poh = s.oh / 2; p.pow_ = s.ow / 2;
     const int tiles = f_assign(p, 1);
+    // taps split eight ways when the bricks alone leave compute units idle
+    if ((long long)tiles * (s.co / 32) < 2LL * kNumCUs && f_shift_env() != 1)
+      return launch_f<true, 2, 2, 4, 1, 8>(p, tiles, x, w, bias, out, mask, st);
+    if (f_shift_ok(s, p)) return launch_f<true, 2, 2, 4, 1, 4, 4>(p, tiles, x, w, bias, out, mask, st);
     return launch_f<true, 2, 2, 4, 1, 4>(p, tiles, x, w, bias, out, mask, st);
   }
   const int fn = s.co % 64 == 0 ? 4 : 2;
   if (epi == 1)
-    return fn == 4 ? launch_lin<true, 4, 1>(p, x, w, bias, out, mask, st)
-                   : launch_lin<true, 2, 1>(p, x, w, bias, out, mask, st);
-  return fn == 4 ? launch_lin<true, 4, 0>(p, x, w, nullptr, out, nullptr, st)
-                 : launch_lin<true, 2, 0>(p, x, w, nullptr, out, nullptr, st);
+    return fn == 4 ? launch_lin<true, 4, 1>(s, p, x, w, bias, out, mask, st)
+                   : launch_lin<true, 2, 1>(s, p, x, w, bias, out, mask, st);
+  return fn == 4 ? launch_lin<true, 4, 0>(s, p, x, w, nullptr, out, nullptr, st)
+                 : launch_lin<true, 2, 0>(s, p, x, w, nullptr, out, nullptr, st);
 }
 
 hipError_t launch_conv_bwd_data_f32(const ConvShape &s, const float *dz, const float *w, float *dx, hipStream_t st) {
   FParams p{};
   f_tables(s, false, p);
   const int fn = s.ci % 64 == 0 ? 4 : (s.ci % 32 == 0 ? 2 : 1);
-  if (fn == 4) return launch_lin<false, 4, 0>(p, dz, w, nullptr, dx, nullptr, st);
-  if (fn == 2) return launch_lin<false, 2, 0>(p, dz, w, nullptr, dx, nullptr, st);
-  return launch_lin<false, 1, 0>(p, dz, w, nullptr, dx, nullptr, st);
+  if (fn == 4) return launch_lin<false, 4, 0>(s, p, dz, w, nullptr, dx, nullptr, st);
+  if (fn == 2) return launch_lin<false, 2, 0>(s, p, dz, w, nullptr, dx, nullptr, st);
+  return launch_lin<false, 1, 0>(s, p, dz, w, nullptr, dx, nullptr, st);
 }
 
 }  // namespace cf

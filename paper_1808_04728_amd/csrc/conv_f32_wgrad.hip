@@ -153,8 +153,8 @@ __global__ __launch_bounds__(64 * WV) void wgrad_f32_kernel(const float *__restr
 #pragma unroll
       for (int j = 0; j < FN; ++j)
         b[j] = __uint_as_float(ld32(gr, ((uint32_t)(pv * p.co + co0 + 16 * j + r16) * 4u) | ((uint32_t)!win << 31)));
-      // the 32 channels of voxel v are one mask word (32 output channels)
-      mw = ld32(mr, ((uint32_t)vv * 4u) | ((uint32_t)!vok << 31));
+      // the workgroup's 32 channels of voxel v are one mask word
+      mw = ld32(mr, ((uint32_t)(vv * (p.co >> 5) + (co0 >> 5)) * 4u) | ((uint32_t)!vok << 31));
     } else {
 #pragma unroll
       for (int j = 0; j < FN; ++j)
@@ -405,11 +405,11 @@ WPlan w_plan(const ConvShape &s, bool fused) {
   pl.wv = 8;
   pl.gx = (pl.units + pl.ru * pl.wv - 1) / (pl.ru * pl.wv);
   pl.gy = s.co / (16 * pl.fn);
-  // about one workgroup per compute unit (the fused layer) or per two (the deep
-  // layers, whose short slices would otherwise write more partials than they
-  // read operands), each slice at least 16 steps of 4 voxels
+  // about one workgroup per compute unit, or per two for short reductions
+  // (below 2^16 voxels, where more slices would write more partials than the
+  // slices read operands), each slice at least 16 steps of 4 voxels
   const long long tiles = (long long)pl.gx * pl.gy;
-  const long long target = fused ? kNumCUs : kNumCUs / 2;
+  const long long target = vox >= (1 << 16) ? kNumCUs : kNumCUs / 2;
   long long want = std::max(1LL, (target + tiles - 1) / tiles);
   want = std::min(want, std::max(1LL, vox / 64));
   long long chunk = (vox + want - 1) / want;
@@ -520,8 +520,8 @@ bool f32wgrad_supported(const ConvShape &s) {
 }
 
 bool f32wgrad_fused_supported(const ConvShape &s) {
-  return f32wgrad_supported(s) && s.kw == 4 && s.co == 32 && s.sd == 1 && s.sh == 1 && s.sw == 1 && s.od >= 2 &&
-         s.oh >= 2 && s.ow >= 2;
+  // 32 output channels per workgroup (one mask word per voxel and workgroup), any stride
+  return f32wgrad_supported(s) && s.co % 32 == 0 && s.od >= 2 && s.oh >= 2 && s.ow >= 2;
 }
 
 size_t f32wgrad_workspace(const ConvShape &s, bool fused) {
@@ -541,7 +541,8 @@ hipError_t launch_conv_bwd_weight_f32(const ConvShape &s, const float *x, const 
   if (fused) {
     p.g_bytes = (uint32_t)((long long)s.n * p.pod * p.poh * p.pow_ * s.co * 4);
     p.m_bytes = (uint32_t)(((long long)p.vox * s.co + 31) / 32 * 4);
-    e = launch_w<true, true, 2, 2>(pl, p, x, g, mask, pw, pb, dz_out, st);
+    e = pl.kw4 ? launch_w<true, true, 2, 2>(pl, p, x, g, mask, pw, pb, dz_out, st)
+               : launch_w<true, false, 2, 2>(pl, p, x, g, mask, pw, pb, dz_out, st);
   } else {
     p.g_bytes = (uint32_t)((long long)p.vox * s.co * 4);
     if (pl.kw4)

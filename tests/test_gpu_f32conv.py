@@ -22,7 +22,7 @@ CASES = [
     (1, (7, 8, 8), 128, 128, 2, 1, "valid"),
     (2, (5, 6, 7), 48, 96, 3, 2, "valid"),      # 48 = 3 k-steps of 16 channels, odd classes
 ]
-TILES = list(range(7))
+TILES = list(range(8))
 
 
 def ids(c):
@@ -59,3 +59,105 @@ def test_f32_fwd_and_bwd_data(case, tile, monkeypatch):
     assert np.array_equal(bits[decided], (u > 0)[decided])
     dxr = oracle.conv3d_bwd_data(to_np(dz), to_np(w), dhw, stride=s, pad=pad)
     assert maxabs_err(to_np(dx), dxr) <= TOL["f32"]
+
+
+# N, (D,H,W), CI, CO, k, stride: the pooled layers of the stack (16 -> 32 and the
+# stride-2 32 -> 64) at sizes with several bricks, ragged tails and odd extents
+POOLED = [
+    (1, (17, 9, 33), 16, 32, 4, 1),
+    (2, (12, 10, 14), 32, 64, 4, 2),
+    (1, (13, 11, 18), 32, 64, 4, 2),    # odd conv-output extents: floor pooling
+    (2, (7, 8, 9), 64, 64, 3, 1),       # 64-channel units of the weight gradient
+]
+
+
+@pytest.mark.parametrize("case", POOLED, ids=lambda c: "n%d_%dx%dx%d_c%d-%d_k%d_s%d" % (c[0], *c[1], *c[2:]))
+def test_f32_pooled_layer_fused(case):
+    """Fused forward (pooled output + slope mask) and fused backward-weights
+    (dW, db and the stored dz) of a pooled fp32 layer, any stride, against the
+    oracle; the unfused backward-data of the stored dz against the oracle."""
+    N, dhw, CI, CO, k, s = case
+    desc = B.make_desc(N, dhw, CI, CO, k, s, "same", "f32")
+    sup = B.cf_conv3d_fused_supported(desc, B.CF_FUSE_POOL2)
+    assert sup & B.FUSED_FWD and sup & B.FUSED_BWD_WEIGHT and sup & B.FUSED_BWD_WEIGHT_DZ
+    rng = np.random.default_rng(41)
+    od = B.cf_conv3d_out_shape(desc)
+    pdhw = tuple(t // 2 for t in od)
+    x = dev(np.log1p(rng.poisson(np.exp(rng.standard_normal((N, *dhw, CI))))), "f32")
+    w = dev(rng.standard_normal((k, k, k, CI, CO)) / np.sqrt(k ** 3 * CI), "f32")
+    bh = rng.standard_normal(CO) * 0.1
+    b = torch.as_tensor(bh, dtype=torch.float32, device="cuda")
+    out = torch.full((N, *pdhw, CO), float("nan"), device="cuda")
+    mask = torch.zeros(B.cf_conv3d_mask_bytes(desc), dtype=torch.uint8, device="cuda")
+    B.cf_conv3d_fwd_fused(desc, x, w, b, 0.01, B.CF_FUSE_POOL2, out, mask)
+    g = dev(rng.standard_normal((N, *pdhw, CO)), "f32")
+    mask_r = torch.as_tensor(rng.integers(0, 256, mask.numel(), dtype=np.uint8), device="cuda")
+    ws = torch.empty(B.cf_conv3d_bwd_weight_fused_workspace_size(desc, B.CF_FUSE_POOL2), dtype=torch.uint8,
+                     device="cuda")
+    dw = torch.full((k, k, k, CI, CO), float("nan"), device="cuda")
+    db = torch.full((CO,), float("nan"), device="cuda")
+    dz = torch.full((N, *od, CO), float("nan"), device="cuda")
+    B.cf_conv3d_bwd_weight_fused_dz(desc, x, g, mask_r, 0.2, B.CF_FUSE_POOL2, dw, db, dz, ws)
+    dx = torch.full((N, *dhw, CI), float("nan"), device="cuda")
+    B.cf_conv3d_bwd_data(desc, dz, w, dx)
+    torch.cuda.synchronize()
+    zr = oracle.conv3d_fwd(to_np(x), to_np(w), stride=s)
+    u = zr + bh
+    pr = oracle.avgpool3d_fwd(oracle.bias_lrelu_fwd(zr, bh, 0.01))
+    assert maxabs_err(to_np(out), pr) <= TOL["f32"]
+    nb = u.size
+    bits = np.unpackbits(mask.cpu().numpy(), bitorder="little")[:nb].astype(bool).reshape(u.shape)
+    decided = np.abs(u) > 1e-5 * np.abs(u).max()
+    assert np.array_equal(bits[decided], (u > 0)[decided])
+    rb = np.unpackbits(mask_r.cpu().numpy(), bitorder="little")[:nb].astype(bool).reshape(u.shape)
+    dzr = oracle.avgpool3d_bwd(to_np(g), od) * np.where(rb, 1.0, 0.2)
+    assert maxabs_err(to_np(dz), dzr) <= TOL["f32"]
+    assert maxabs_err(to_np(dw), oracle.conv3d_bwd_weight(to_np(x), dzr, k, stride=s)) <= TOL["f32"]
+    assert maxabs_err(to_np(db), dzr.reshape(-1, CO).sum(0)) <= TOL["f32"]
+    assert maxabs_err(to_np(dx), oracle.conv3d_bwd_data(dzr, to_np(w), dhw, stride=s)) <= TOL["f32"]
+
+
+# shift mode (stride-1 4-wide kernels, destination width a multiple of 16):
+# forward, forward + bias + lReLU + mask, pooled forward and backward-data, each
+# with the mode forced on and off, against the oracle
+SHIFT = [
+    (1, (9, 7, 32), 16, 32, 4),
+    (2, (5, 6, 48), 16, 32, 4),
+    (1, (6, 5, 32), 32, 64, 4),
+    (1, (8, 6, 16), 16, 32, 4),     # one fragment per row: both edges are padding
+]
+
+
+@pytest.mark.parametrize("mode", ["1", "0"])
+@pytest.mark.parametrize("case", SHIFT, ids=lambda c: "n%d_%dx%dx%d_c%d-%d_k%d" % (c[0], *c[1], *c[2:]))
+def test_f32_shift_mode(case, mode, monkeypatch):
+    N, dhw, CI, CO, k = case
+    monkeypatch.setenv("CF_F32_SHIFT", mode)
+    desc = B.make_desc(N, dhw, CI, CO, k, 1, "same", "f32")
+    rng = np.random.default_rng(51)
+    x = dev(rng.standard_normal((N, *dhw, CI)), "f32")
+    w = dev(rng.standard_normal((k, k, k, CI, CO)) / np.sqrt(k ** 3 * CI), "f32")
+    bh = rng.standard_normal(CO) * 0.1
+    b = torch.as_tensor(bh, dtype=torch.float32, device="cuda")
+    od = B.cf_conv3d_out_shape(desc)
+    z = torch.full((N, *od, CO), float("nan"), device="cuda")
+    y = torch.full_like(z, float("nan"))
+    B.cf_conv3d_fwd(desc, x, w, z)
+    B.cf_conv3d_fwd_fused(desc, x, w, b, 0.2, 0, y, None)
+    p = torch.full((N, *(t // 2 for t in od), CO), float("nan"), device="cuda")
+    mask = torch.zeros(B.cf_conv3d_mask_bytes(desc), dtype=torch.uint8, device="cuda")
+    B.cf_conv3d_fwd_fused(desc, x, w, b, 0.2, B.CF_FUSE_POOL2, p, mask)
+    dz = dev(rng.standard_normal((N, *od, CO)), "f32")
+    dx = torch.full((N, *dhw, CI), float("nan"), device="cuda")
+    B.cf_conv3d_bwd_data(desc, dz, w, dx)
+    torch.cuda.synchronize()
+    zr = oracle.conv3d_fwd(to_np(x), to_np(w))
+    assert maxabs_err(to_np(z), zr) <= TOL["f32"]
+    yr = oracle.bias_lrelu_fwd(zr, bh, 0.2)
+    assert maxabs_err(to_np(y), yr) <= TOL["f32"]
+    assert maxabs_err(to_np(p), oracle.avgpool3d_fwd(yr)) <= TOL["f32"]
+    u = zr + bh
+    bits = np.unpackbits(mask.cpu().numpy(), bitorder="little")[:u.size].astype(bool).reshape(u.shape)
+    decided = np.abs(u) > 1e-5 * np.abs(u).max()
+    assert np.array_equal(bits[decided], (u > 0)[decided])
+    assert maxabs_err(to_np(dx), oracle.conv3d_bwd_data(to_np(dz), to_np(w), dhw)) <= TOL["f32"]
