@@ -50,8 +50,9 @@ struct WF32Params {
   int units;                   // row units of 64 rows
   int cunits;                  // channel chunks per unit position (ci/16 or ci/64)
   int vox;                     // n*od*oh*ow (reduction length)
-  int chunk;                   // voxels per slice (multiple of 4)
-  FastDiv fw, fh, fd;          // voxel decode divisors ow, oh, od
+  int rows_per;                // output rows (n, od, oh) per slice
+  int nws;                     // steps of four voxels per output row
+  FastDiv fh, fd;              // row decode divisors oh, od
   uint32_t x_bytes, g_bytes, m_bytes;
   float alpha;
   int pod, poh, pow_;          // fused: pooled extents
@@ -78,8 +79,6 @@ __global__ __launch_bounds__(64 * WV) void wgrad_f32_kernel(const float *__restr
   const int g4 = lane >> 4, r16 = lane & 15;
   const int co0 = blockIdx.y * 16 * FN;
   const int slice = blockIdx.z;
-  const int v0 = slice * p.chunk;
-  const int v1 = min(v0 + p.chunk, p.vox);
   // the bias gradient and the stored dz come from one wave of the slice
   const bool lead = FUSED && blockIdx.x == 0 && wave == 0;
 
@@ -106,7 +105,7 @@ __global__ __launch_bounds__(64 * WV) void wgrad_f32_kernel(const float *__restr
       tkw[i] = r16 >> 2;
       c0 = 16 * cc;
       tap = (tkd[i] * p.kh + tkh[i]) * 4 + tkw[i];
-      toff[i] = ((tkd[i] * p.h + tkh[i]) * p.w + tkw[i]) * p.ci + c0 + 4 * (r16 & 3);
+      toff[i] = c0 + 4 * (r16 & 3);  // channel offset; the tap's voxel comes from the row base
       // D row 4 g + e of MFMA j: column kw = g, channel c0 + 4 e + j
       rbase[i] = ((tkd[i] * p.kh + tkh[i]) * 4 + g4) * p.ci + c0;
     } else {
@@ -115,50 +114,83 @@ __global__ __launch_bounds__(64 * WV) void wgrad_f32_kernel(const float *__restr
       tkh[i] = (tap / p.kw) % p.kh;
       tkd[i] = tap / (p.kw * p.kh);
       c0 = 64 * cc;
-      toff[i] = ((tkd[i] * p.h + tkh[i]) * p.w + tkw[i]) * p.ci + c0 + 4 * r16;
+      toff[i] = c0 + 4 * r16;
       // D row 4 g + e of MFMA j: channel c0 + 16 g + 4 e + j
       rbase[i] = tap * p.ci + c0 + 16 * g4;
     }
     (void)tap;
   }
 
-  const int nsteps = v1 > v0 ? (v1 - v0 + 3) >> 2 : 0;
+  // ---- the slice's output rows (n, od, oh), four voxels along w per step -----
+  // Row-dependent values are uniform and change once per row; a step only adds
+  // its w offset.  Steps past the slice (ring padding) load zeros.
+  const int nrow_all = p.n * p.od * p.oh;
+  const int r0 = slice * p.rows_per, r1 = min(r0 + p.rows_per, nrow_all);
+  const int nsteps = r1 > r0 ? (r1 - r0) * p.nws : 0;
+  int crow = r0, cws = 0, ldstep = 0;  // load cursor
+  int xrow[RU], rowvox = 0, prow = 0;
+  bool dok[RU], winrow = false;
+  auto setrow = [&](int row) {
+    const int t1 = fdiv(row, p.fh), nn = fdiv(t1, p.fd);
+    const int oh_ = row - t1 * (int)p.fh.div, od_ = t1 - nn * (int)p.fd.div;
+    const int bd = od_ * p.sd - p.pd, bh = oh_ * p.sh - p.ph;
+#pragma unroll
+    for (int i = 0; i < RU; ++i) {
+      dok[i] = uok[i] & ((unsigned)(bd + tkd[i]) < (unsigned)p.d) & ((unsigned)(bh + tkh[i]) < (unsigned)p.h);
+      xrow[i] = ((nn * p.d + bd + tkd[i]) * p.h + bh + tkh[i]) * p.w;
+    }
+    rowvox = row * p.ow;
+    if constexpr (FUSED) {
+      const int pd_ = od_ >> 1, ph_ = oh_ >> 1;
+      winrow = (pd_ < p.pod) & (ph_ < p.poh);
+      prow = ((nn * p.pod + pd_) * p.poh + ph_) * p.pow_;
+    }
+  };
+  if (nsteps > 0) setrow(r0);
+  auto next = [&]() {
+    ++ldstep;
+    if (ldstep < nsteps && ++cws == p.nws) {
+      cws = 0;
+      setrow(++crow);
+    }
+  };
+
   constexpr int NS = PF + 1;
   u32x4_t a_r[NS][RU];
   float b_r[NS][FN];
   uint32_t m_r[NS];
+  int v_r[NS];  // voxel of the lane's K slot (-1: none), for the stored dz
   (void)m_r;
+  (void)v_r;
 
-  // step >= nsteps (ring padding) loads zeros: every voxel slot is past the slice
-  auto load = [&](int step, u32x4_t(&a)[RU], float(&b)[FN], uint32_t &mw) {
-    const int v = v0 + 4 * step + g4;
-    const bool vok = v < v1;
-    const int vv = vok ? v : v0;
-    const int t1 = fdiv(vv, p.fw), t2 = fdiv(t1, p.fh), nn = fdiv(t2, p.fd);
-    const int ow_ = vv - t1 * (int)p.fw.div, oh_ = t1 - t2 * (int)p.fh.div, od_ = t2 - nn * (int)p.fd.div;
-    const int bd = od_ * p.sd - p.pd, bh = oh_ * p.sh - p.ph, bw = ow_ * p.sw - p.pw;
-    const int base = (((nn * p.d + bd) * p.h + bh) * p.w + bw) * p.ci;
+  auto load = [&](u32x4_t(&a)[RU], float(&b)[FN], uint32_t &mw, int &vx) {
+    const int w = 4 * cws + g4;
+    const bool wok = (ldstep < nsteps) & (w < p.ow);
+    const int bw = w * p.sw - p.pw;
 #pragma unroll
     for (int i = 0; i < RU; ++i) {
+      const int xw = bw + tkw[i];
       // bitwise, not short-circuit: one select per load, no branch
-      const bool ok = vok & uok[i] & ((unsigned)(bd + tkd[i]) < (unsigned)p.d) &
-                      ((unsigned)(bh + tkh[i]) < (unsigned)p.h) & ((unsigned)(bw + tkw[i]) < (unsigned)p.w);
+      const bool ok = dok[i] & wok & ((unsigned)xw < (unsigned)p.w);
       // a valid byte offset is below 2^31: bit 31 sends the load past the buffer (zeros)
-      a[i] = ld128(xr, ((uint32_t)(base + toff[i]) * 4u) | ((uint32_t)!ok << 31));
+      a[i] = ld128(xr, ((uint32_t)((xrow[i] + xw) * p.ci + toff[i]) * 4u) | ((uint32_t)!ok << 31));
     }
+    const int v = rowvox + w;
+    vx = wok ? v : -1;
     if constexpr (FUSED) {
-      const int pd_ = od_ >> 1, ph_ = oh_ >> 1, pw_ = ow_ >> 1;
-      const bool win = vok & (pd_ < p.pod) & (ph_ < p.poh) & (pw_ < p.pow_);
-      const int pv = ((nn * p.pod + pd_) * p.poh + ph_) * p.pow_ + pw_;
+      const int pw_ = w >> 1;
+      const bool win = winrow & wok & (pw_ < p.pow_);
+      const int gb = (prow + pw_) * p.co + co0 + r16;
 #pragma unroll
       for (int j = 0; j < FN; ++j)
-        b[j] = __uint_as_float(ld32(gr, ((uint32_t)(pv * p.co + co0 + 16 * j + r16) * 4u) | ((uint32_t)!win << 31)));
+        b[j] = __uint_as_float(ld32(gr, ((uint32_t)(gb + 16 * j) * 4u) | ((uint32_t)!win << 31)));
       // the workgroup's 32 channels of voxel v are one mask word
-      mw = ld32(mr, ((uint32_t)(vv * (p.co >> 5) + (co0 >> 5)) * 4u) | ((uint32_t)!vok << 31));
+      mw = ld32(mr, ((uint32_t)(v * (p.co >> 5) + (co0 >> 5)) * 4u) | ((uint32_t)!wok << 31));
     } else {
+      const int gb = v * p.co + co0 + r16;
 #pragma unroll
       for (int j = 0; j < FN; ++j)
-        b[j] = __uint_as_float(ld32(gr, ((uint32_t)(vv * p.co + co0 + 16 * j + r16) * 4u) | ((uint32_t)!vok << 31)));
+        b[j] = __uint_as_float(ld32(gr, ((uint32_t)(gb + 16 * j) * 4u) | ((uint32_t)!wok << 31)));
     }
   };
 
@@ -177,13 +209,16 @@ __global__ __launch_bounds__(64 * WV) void wgrad_f32_kernel(const float *__restr
   if (nsteps > 0) {
     const int niter = (nsteps + NS - 1) / NS * NS;
 #pragma unroll
-    for (int q = 0; q < PF; ++q) load(q, a_r[q], b_r[q], m_r[q]);
+    for (int q = 0; q < PF; ++q) {
+      load(a_r[q], b_r[q], m_r[q], v_r[q]);
+      next();
+    }
     for (int s0 = 0; s0 < niter; s0 += NS) {
 #pragma unroll
       for (int q = 0; q < NS; ++q) {
-        const int s = s0 + q;
         const int sl = (q + PF) % NS;
-        load(s + PF, a_r[sl], b_r[sl], m_r[sl]);
+        load(a_r[sl], b_r[sl], m_r[sl], v_r[sl]);
+        next();
         float bv[FN];
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
@@ -195,11 +230,10 @@ __global__ __launch_bounds__(64 * WV) void wgrad_f32_kernel(const float *__restr
           bv[j] = b;
         }
         if (lead) {
-          const int v = v0 + 4 * s + g4;
 #pragma unroll
           for (int j = 0; j < FN; ++j) {
             dsum[j] += bv[j];
-            if (dz_out && v < v1) dz_out[(long long)v * p.co + co0 + 16 * j + r16] = bv[j];
+            if (dz_out && v_r[q] >= 0) dz_out[(long long)v_r[q] * p.co + co0 + 16 * j + r16] = bv[j];
           }
         }
 #pragma unroll
@@ -386,7 +420,7 @@ struct WPlan {
   bool kw4;
   int ru, fn, wv;
   int units, cunits;
-  int gx, gy, nsplit, chunk;
+  int gx, gy, nsplit, rows_per;
 };
 
 WPlan w_plan(const ConvShape &s, bool fused) {
@@ -412,10 +446,13 @@ WPlan w_plan(const ConvShape &s, bool fused) {
   const long long target = vox >= (1 << 16) ? kNumCUs : kNumCUs / 2;
   long long want = std::max(1LL, (target + tiles - 1) / tiles);
   want = std::min(want, std::max(1LL, vox / 64));
-  long long chunk = (vox + want - 1) / want;
-  chunk = (chunk + 3) / 4 * 4;
-  pl.chunk = (int)std::max(4LL, chunk);
-  pl.nsplit = (int)((vox + pl.chunk - 1) / pl.chunk);
+  // slices of whole output rows, at least 16 steps of 4 voxels each
+  const long long rows = (long long)s.n * s.od * s.oh;
+  const long long nws = (s.ow + 3) / 4;
+  long long per = (rows + want - 1) / want;
+  per = std::max(per, (16 + nws - 1) / nws);
+  pl.rows_per = (int)std::max(1LL, per);
+  pl.nsplit = (int)((rows + pl.rows_per - 1) / pl.rows_per);
   return pl;
 }
 
@@ -429,8 +466,8 @@ WF32Params w_params(const ConvShape &s, const WPlan &pl, float alpha) {
   p.units = pl.units;
   p.cunits = pl.cunits;
   p.vox = s.n * s.od * s.oh * s.ow;
-  p.chunk = pl.chunk;
-  p.fw = make_fastdiv(s.ow);
+  p.rows_per = pl.rows_per;
+  p.nws = (s.ow + 3) / 4;
   p.fh = make_fastdiv(s.oh);
   p.fd = make_fastdiv(s.od);
   p.x_bytes = (uint32_t)((long long)s.n * s.d * s.h * s.w * s.ci * 4);
