@@ -1,6 +1,7 @@
 """Benchmark: one training step of the CosmoFlow conv hot path on one MI355X.
 
-    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--extra-workload NAME|none]
+                    [--no-cpu-baseline]
 
 A step is the whole hot path over one batch of synthetic cubes: forward
 (conv, bias + leaky ReLU, 2^3 average pool per layer) and backward (pool
@@ -9,9 +10,12 @@ the C ABI.  Inputs, weights and the upstream gradient are resident in HBM
 before timing starts.  Prints ONE JSON line.
 
 value = algorithmic conv FLOPs per step (fwd + wgrad + dgrad, padded taps
-included, layer-1 dgrad skipped) x steps / wall time of the timed steps.
-The roofline entry is for the op that takes the most time per step, timed
-with events on the launch stream over the same timed steps.
+included, layer-1 dgrad skipped) x steps / wall time of the timed steps, for
+the headline workload: the 128^3 stack at the paper's precision (fp32, batch
+1, as Table I times it).  The same measurement of the bf16 batch-8 128^3
+stack is reported under its own key.  The roofline entry is for the op that
+takes the most time per step, timed with events on the launch stream over
+the same timed steps.
 
 The parameter update that follows each step in training (Adam + LARC +
 linear decay, Section III-B) is timed on its own after the timed steps and
@@ -63,11 +67,16 @@ def cpu_baseline(name, seconds_hint=True):
     ws, bs = inputs.make_weights(name)
     layers = [dict(k=L["k"], stride=L["stride"], pool=L["pool"], pad=L.get("pad", "same")) for L in wl["layers"]]
     oracle.build(force=False)
-    t0 = time.perf_counter()
-    acts = oracle.stack_forward(x, layers, ws, bs, inputs.ALPHA)
-    dout = inputs.normal(acts[-1]["out"].shape, 30000 + wl["cfg"])
-    oracle.stack_backward(acts, layers, ws, dout, inputs.ALPHA, skip_first_dgrad=True)
-    dt = time.perf_counter() - t0
+    # one sample's step, repeated until about 10 s of CPU work
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        acts = oracle.stack_forward(x, layers, ws, bs, inputs.ALPHA)
+        dout = inputs.normal(acts[-1]["out"].shape, 30000 + wl["cfg"])
+        oracle.stack_backward(acts, layers, ws, dout, inputs.ALPHA, skip_first_dgrad=True)
+        reps += 1
+        if time.perf_counter() - t0 > 10.0 or reps >= 8:
+            break
+    dt = (time.perf_counter() - t0) / reps
     flops = 0
     size = wl["size"]
     for i, L in enumerate(wl["layers"]):
@@ -78,7 +87,7 @@ def cpu_baseline(name, seconds_hint=True):
     threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or os.cpu_count()
     return dict(value=flops / dt / 1e12, unit="TFLOP/s", cores=threads, kind="oracle",
                 sample=f"1 of {wl['batch']} samples (batch 1), full {wl['size']}^3 stack fwd+bwd in fp64, "
-                       f"{dt:.1f} s, {1.0 / dt:.4f} samples/s")
+                       f"{reps} repetitions, {dt:.2f} s each, {1.0 / dt:.4f} samples/s")
 
 
 def measured_traffic(workload, op):
@@ -204,43 +213,19 @@ def hbm_passes(B, np, torch, wl):
     return dict(shape=[n, s, s, s, c], dtype=dt, unit="GB/s", peak=HBM_PEAK_GBS, passes=out)
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="stack_128c_b8_bf16")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--op-breakdown", action="store_true", help="print per-op times to stderr")
-    ap.add_argument("--with-update", action="store_true",
-                    help="apply the Adam + LARC parameter update inside every timed step")
-    ap.add_argument("--with-head", action="store_true",
-                    help="run the FC head + loss inside every step (its input gradient drives the backward pass)")
-    ap.add_argument("--unfused", action="store_true",
-                    help="run every layer through the unfused entry points (conv, bias + lReLU, pool separately)")
-    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
-                    help="only run 5 plain device copies of MIB MiB (calibrates the HBM byte counters)")
-    args = ap.parse_args()
-    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py measures one GPU: the library has no multi-GPU path (the step would shard "
-              "data-parallel, with one allreduce of the weight and bias gradients per step, which is not "
-              "implemented); run with --gpus 1", file=sys.stderr)
-        sys.exit(2)
-
+def run_stack(name, args, steps, warmup, extras):
+    """Warm up, find the dominant op (events around every call over 3 steps),
+    then time `steps` steps with events around the dominant op only.  extras:
+    also time the FC head and the parameter update on their own (after the
+    timed steps)."""
     import numpy as np
     import torch
-
-    if args.copy_probe:
-        copy_probe(args.copy_probe)
-        return
 
     from paper_1808_04728_amd import binding as B
     from paper_1808_04728_amd import inputs
     from paper_1808_04728_amd.stack import ConvStack
 
-    name = args.workload
     wl = inputs.WORKLOADS[name]
-    torch.cuda.set_device(0)
     st = ConvStack(wl["layers"], wl["size"], wl["batch"], wl["dtype"], inputs.ALPHA, "cuda:0", fused=not args.unfused)
     ws, bs = inputs.make_weights(name)
     st.set_params(ws, bs)
@@ -267,7 +252,7 @@ def main():
         if args.with_update:
             st.update(hp)
 
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         step()
     torch.cuda.synchronize()
 
@@ -279,6 +264,7 @@ def main():
     op_ms = {k: float(np.mean([a.elapsed_time(b) for a, b in v])) for k, v in st.timer.items()}
     dominant = max(op_ms, key=op_ms.get)
     if args.op_breakdown:
+        print(f"{name}:", file=sys.stderr)
         for k, v in sorted(op_ms.items(), key=lambda kv: -kv[1]):
             fl = st.op_flops(k)
             extra = f"{fl / v / 1e9:8.1f} TFLOP/s" if fl else f"{st.op_bytes(k) / v / 1e6:8.1f} GB/s"
@@ -289,12 +275,34 @@ def main():
     st.timed_ops = {dominant}
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
+    for _ in range(steps):
         step()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     dom_ms = float(np.mean([a.elapsed_time(b) for a, b in st.timer[dominant]]))
     st.timer = None
+
+    ms = wall * 1e3 / steps
+    flops = st.conv_flops()
+    tflops = flops / (ms * 1e-3) / 1e12
+    peak = PEAK[wl["dtype"]]
+    dom_flops = st.op_flops(dominant)
+    if dom_flops:
+        ach = dom_flops / (dom_ms * 1e-3) / 1e12
+        roof = dict(bound="mfma", achieved=round(ach, 2), peak=peak, unit="TFLOP/s", frac=round(ach / peak, 4),
+                    traffic=measured_traffic(name, dominant), kernel=dominant, launch_ms=round(dom_ms, 4),
+                    per_launch=f"{dom_flops / 1e9:.2f} GFLOP", algorithmic_bytes=st.op_bytes(dominant))
+    else:
+        gbs = st.op_bytes(dominant) / (dom_ms * 1e-3) / 1e9
+        roof = dict(bound="hbm", achieved=round(gbs, 1), peak=HBM_PEAK_GBS, unit="GB/s",
+                    frac=round(gbs / HBM_PEAK_GBS, 4), traffic=measured_traffic(name, dominant), kernel=dominant,
+                    launch_ms=round(dom_ms, 4), per_launch=f"{st.op_bytes(dominant) / 2**20:.1f} MiB",
+                    algorithmic_bytes=st.op_bytes(dominant))
+    out = dict(wl=wl, ms=ms, tflops=tflops, flops=flops, peak=peak, roofline=roof,
+               op_ms={k: round(v, 4) for k, v in sorted(op_ms.items(), key=lambda kv: -kv[1])},
+               samples_per_s=round(wl["batch"] / (ms * 1e-3), 2))
+    if not extras:
+        return out
 
     # the FC head + loss alone (before any parameter update): forward and
     # backward twice, queued behind a step so that the device never waits for
@@ -313,10 +321,10 @@ def main():
     head_ms = float(np.mean([a.elapsed_time(b) for a, b in hts])) / 2
     head_bytes = head.weight_bytes()
     head_gbs = head_bytes / (head_ms * 1e-3) / 1e9
-    head_res = dict(widths=[feats, *inputs.HEAD_WIDTHS], ms=round(head_ms, 4),
-                    algorithmic_bytes=head_bytes, achieved=round(head_gbs, 1), unit="GB/s", peak=HBM_PEAK_GBS,
-                    frac=round(head_gbs / HBM_PEAK_GBS, 4), in_step=args.with_head,
-                    loss=round(float(head.loss[0].item()), 6))
+    out["head"] = dict(widths=[feats, *inputs.HEAD_WIDTHS], ms=round(head_ms, 4),
+                       algorithmic_bytes=head_bytes, achieved=round(head_gbs, 1), unit="GB/s", peak=HBM_PEAK_GBS,
+                       frac=round(head_gbs / HBM_PEAK_GBS, 4), in_step=args.with_head,
+                       loss=round(float(head.loss[0].item()), 6))
 
     # the parameter update alone, after the timed steps (it changes the weights):
     # K updates queued behind a step, so that the device never waits for the host
@@ -338,51 +346,90 @@ def main():
                   launch_ms=round(upd_ms, 4), algorithmic_bytes=upd_bytes, achieved=round(upd_gbs, 1),
                   unit="GB/s", peak=HBM_PEAK_GBS, frac=round(upd_gbs / HBM_PEAK_GBS, 4), in_step=args.with_update)
     update["paper_network_size"] = update_at_paper_size(step, B, np, torch, wl["dtype"] == "bf16")
+    out["update"] = update
+    return out
 
-    passes = hbm_passes(B, np, torch, wl)
 
-    ms = wall * 1e3 / args.steps
-    flops = st.conv_flops()
-    tflops = flops / (ms * 1e-3) / 1e12
-    peak = PEAK[wl["dtype"]]
-    dom_flops = st.op_flops(dominant)
-    if dom_flops:
-        ach = dom_flops / (dom_ms * 1e-3) / 1e12
-        roof = dict(bound="mfma", achieved=round(ach, 2), peak=peak, unit="TFLOP/s", frac=round(ach / peak, 4),
-                    traffic=measured_traffic(name, dominant), kernel=dominant, launch_ms=round(dom_ms, 4),
-                    per_launch=f"{dom_flops / 1e9:.2f} GFLOP", algorithmic_bytes=st.op_bytes(dominant))
-    else:
-        gbs = st.op_bytes(dominant) / (dom_ms * 1e-3) / 1e9
-        roof = dict(bound="hbm", achieved=round(gbs, 1), peak=HBM_PEAK_GBS, unit="GB/s",
-                    frac=round(gbs / HBM_PEAK_GBS, 4), traffic=measured_traffic(name, dominant), kernel=dominant,
-                    launch_ms=round(dom_ms, 4), per_launch=f"{st.op_bytes(dominant) / 2**20:.1f} MiB",
-                    algorithmic_bytes=st.op_bytes(dominant))
+def config_of(name, wl, flops, args):
+    return {"workload": describe(name, wl) + (", unfused entry points" if args.unfused else "")
+            + (", Adam + LARC update in every step" if args.with_update else "")
+            + (", FC head + loss in every step" if args.with_head else ""),
+            "name": name, "edge": wl["size"], "batch": wl["batch"],
+            "input_channels": wl["c0"], "conv_gflop_per_step": round(flops / 1e9, 3)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="stack_128c_b1_f32",
+                    help="headline workload (default: the 128^3 stack at the paper's fp32, batch 1)")
+    ap.add_argument("--extra-workload", default="stack_128c_b8_bf16",
+                    help="second workload reported under its own key ('none' to skip)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--op-breakdown", action="store_true", help="print per-op times to stderr")
+    ap.add_argument("--with-update", action="store_true",
+                    help="apply the Adam + LARC parameter update inside every timed step")
+    ap.add_argument("--with-head", action="store_true",
+                    help="run the FC head + loss inside every step (its input gradient drives the backward pass)")
+    ap.add_argument("--unfused", action="store_true",
+                    help="run every layer through the unfused entry points (conv, bias + lReLU, pool separately)")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="only run 5 plain device copies of MIB MiB (calibrates the HBM byte counters)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU: the library has no multi-GPU path (the step would shard "
+              "data-parallel, with one allreduce of the weight and bias gradients per step, which is not "
+              "implemented); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    if args.copy_probe:
+        copy_probe(args.copy_probe)
+        return
+
+    from paper_1808_04728_amd import binding as B
+    from paper_1808_04728_amd import inputs
+
+    torch.cuda.set_device(0)
+    name = args.workload
+    r = run_stack(name, args, args.steps, args.warmup, extras=True)
+    wl = r["wl"]
     res = {
         "metric": METRIC,
-        "value": round(tflops, 3),
+        "value": round(r["tflops"], 3),
         "unit": "TFLOP/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms, 4),
+        "ms_per_step": round(r["ms"], 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": wl["dtype"],
         "data": "synthetic",
-        "config": {"workload": describe(name, wl) + (", unfused entry points" if args.unfused else "")
-                   + (", Adam + LARC update in every step" if args.with_update else "")
-                   + (", FC head + loss in every step" if args.with_head else ""),
-                   "name": name, "edge": wl["size"], "batch": wl["batch"],
-                   "input_channels": wl["c0"], "conv_gflop_per_step": round(flops / 1e9, 3)},
-        "samples_per_s": round(wl["batch"] / (ms * 1e-3), 2),
-        "mfma_peak_frac": round(tflops / peak, 4),
-        "roofline": roof,
-        "op_ms": {k: round(v, 4) for k, v in sorted(op_ms.items(), key=lambda kv: -kv[1])},
-        "update": update,
-        "head": head_res,
-        "hbm_passes": passes,
+        "config": config_of(name, wl, r["flops"], args),
+        "samples_per_s": r["samples_per_s"],
+        "mfma_peak_frac": round(r["tflops"] / r["peak"], 4),
+        "roofline": r["roofline"],
+        "op_ms": r["op_ms"],
+        "update": r["update"],
+        "head": r["head"],
     }
+    if args.extra_workload != "none" and args.extra_workload != name:
+        x = run_stack(args.extra_workload, args, args.steps, args.warmup, extras=False)
+        xw = x["wl"]
+        res[args.extra_workload] = dict(
+            value=round(x["tflops"], 3), unit="TFLOP/s", ms_per_step=round(x["ms"], 4), dtype=xw["dtype"],
+            samples_per_s=x["samples_per_s"], mfma_peak_frac=round(x["tflops"] / x["peak"], 4),
+            config=config_of(args.extra_workload, xw, x["flops"], args), roofline=x["roofline"], op_ms=x["op_ms"])
+    # the unfused elementwise and pool passes at the largest first-layer activation
+    # of the two workloads (the bf16 batch-8 one: 512 MiB, beyond the last-level cache)
+    pw = inputs.WORKLOADS[args.extra_workload] if args.extra_workload in inputs.WORKLOADS else wl
+    res["hbm_passes"] = hbm_passes(B, np, torch, pw)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(name)
     print(json.dumps(res), flush=True)
