@@ -208,14 +208,12 @@ __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__r
     const int myrows = nrows > wk ? (nrows - wk + WK - 1) / WK : 0;
     const int nsteps = myrows * nch;
     int ri = wk, cc = 0, ldstep = 0;
-    auto next = [&]() {
+    auto next = [&]() {  // branch-free: see the linear cursor below
       ++ldstep;
-      if (ldstep < nsteps) {
-        if (++cc == nch) {
-          cc = 0;
-          ri += WK;
-        }
-      }
+      const int c1 = cc + (ldstep < nsteps ? 1 : 0);
+      const bool wrap = c1 == nch;
+      cc = wrap ? 0 : c1;
+      ri += wrap ? WK : 0;
     };
     constexpr int NB = FWD ? 4 : FN;
     constexpr int BW = FWD ? FN : 4;
@@ -270,6 +268,7 @@ __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__r
         for (int q = 0; q < NS; ++q) {
           load(a_r[(q + PF) % NS], e_r[(q + PF) % NS], b_r[(q + PF) % NS]);
           next();
+          __builtin_amdgcn_sched_barrier(0);  // prefetch loads stay ahead of the MFMAs
           auto column = [&](auto uwc) {
             constexpr int uw = decltype(uwc)::value;
 #pragma unroll
@@ -302,14 +301,14 @@ __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__r
     // the last real step the cursor stays put (valid weight addresses) and the A
     // loads take the out-of-range offset, so padded steps multiply zeros
     int ti = wk, cc = 0, ldstep = 0;
+    // branch-free (scalar selects): control flow between the ring's steps lets
+    // the compiler sink the prefetch loads and wait for all of them at once
     auto next = [&]() {
       ++ldstep;
-      if (ldstep < nsteps) {
-        if (++cc == nch) {
-          cc = 0;
-          ti += WK;
-        }
-      }
+      const int c1 = cc + (ldstep < nsteps ? 1 : 0);
+      const bool wrap = c1 == nch;
+      cc = wrap ? 0 : c1;
+      ti += wrap ? WK : 0;
     };
   
     // lane part of the weight element offsets
@@ -366,6 +365,9 @@ __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__r
           const int s = s0 + q;
           load(a_r[(q + PF) % NS], b_r[(q + PF) % NS]);
           next();
+          // keep the prefetch loads ahead of this step's MFMAs: sunk below them,
+          // the wait before the next step would cover every load in flight
+          __builtin_amdgcn_sched_barrier(0);
           (void)s;
   #pragma unroll
           for (int i = 0; i < FM; ++i) {

@@ -37,6 +37,7 @@
 #include "fastdiv.h"
 
 #include <algorithm>
+#include <cstdlib>
 
 namespace cf {
 namespace {
@@ -147,12 +148,17 @@ __global__ __launch_bounds__(64 * WV) void wgrad_f32_kernel(const float *__restr
     }
   };
   if (nsteps > 0) setrow(r0);
+  // branch-free (scalar selects): control flow between the ring's steps would
+  // let the compiler sink every prefetch load to the end of the ring and wait
+  // for all of them before the first step's MFMAs
   auto next = [&]() {
     ++ldstep;
-    if (ldstep < nsteps && ++cws == p.nws) {
-      cws = 0;
-      setrow(++crow);
-    }
+    const int adv = ldstep < nsteps ? 1 : 0;
+    const int c1 = cws + adv;
+    const bool wrap = c1 == p.nws;
+    cws = wrap ? 0 : c1;
+    crow += wrap ? 1 : 0;
+    setrow(min(crow, nrow_all - 1));
   };
 
   constexpr int NS = PF + 1;
@@ -219,6 +225,10 @@ __global__ __launch_bounds__(64 * WV) void wgrad_f32_kernel(const float *__restr
         const int sl = (q + PF) % NS;
         load(a_r[sl], b_r[sl], m_r[sl], v_r[sl]);
         next();
+        // keep this step's prefetch loads ahead of its MFMAs: the scheduler would
+        // otherwise sink them, and the wait before the next step's MFMAs would
+        // then cover every load in flight
+        __builtin_amdgcn_sched_barrier(0);
         float bv[FN];
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
@@ -374,6 +384,10 @@ __global__ __launch_bounds__(64 * WV) void l1_wgrad_f32_kernel(const float *__re
 #pragma unroll
       for (int q = 0; q < NS; ++q) {
         load(s0 + b0 + q + PF, ring[(q + PF) % NS]);
+        // keep this step's prefetch loads ahead of its MFMAs: the scheduler would
+        // otherwise sink them, and the wait before the next step's MFMAs would
+        // then cover every load in flight
+        __builtin_amdgcn_sched_barrier(0);
         const Ld &L = ring[q];
         // window E[k] = x[wv0 - 1 + k], k = 0 .. 6
         const float E[7] = {L.left, __uint_as_float(L.cur[0]), __uint_as_float(L.cur[1]),
@@ -441,16 +455,22 @@ WPlan w_plan(const ConvShape &s, bool fused) {
   pl.gy = s.co / (16 * pl.fn);
   // about one workgroup per compute unit, or per two for short reductions
   // (below 2^16 voxels, where more slices would write more partials than the
-  // slices read operands), each slice at least 16 steps of 4 voxels
+  // slices read operands)
   const long long tiles = (long long)pl.gx * pl.gy;
-  const long long target = vox >= (1 << 16) ? kNumCUs : kNumCUs / 2;
+  long long target = vox >= (1 << 16) ? kNumCUs : kNumCUs / 2;
+  // CF_F32W_TARGET overrides the workgroup target (measurement sweeps)
+  if (const char *e = getenv("CF_F32W_TARGET")) target = std::max(1, atoi(e));
   long long want = std::max(1LL, (target + tiles - 1) / tiles);
-  want = std::min(want, std::max(1LL, vox / 64));
+  // CF_F32W_MINSTEPS overrides the shortest slice (measurement sweeps; 8 steps of
+  // 4 voxels measured best on the stack's deep layers)
+  const char *ms = getenv("CF_F32W_MINSTEPS");
+  const long long minsteps = ms ? std::max(1, atoi(ms)) : 8;
+  want = std::min(want, std::max(1LL, vox / (4 * minsteps)));
   // slices of whole output rows, at least 16 steps of 4 voxels each
   const long long rows = (long long)s.n * s.od * s.oh;
   const long long nws = (s.ow + 3) / 4;
   long long per = (rows + want - 1) / want;
-  per = std::max(per, (16 + nws - 1) / nws);
+  per = std::max(per, (minsteps + nws - 1) / nws);
   pl.rows_per = (int)std::max(1LL, per);
   pl.nsplit = (int)((rows + pl.rows_per - 1) / pl.rows_per);
   return pl;
