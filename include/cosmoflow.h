@@ -181,10 +181,14 @@ cf_status cf_avgpool3d_bwd(int32_t n, int32_t d, int32_t h, int32_t w, int32_t c
 
 /* flags */
 #define CF_FUSE_POOL2 1u /* a 2^3 stride-2 average pool follows the activation */
+#define CF_FUSE_MASK 2u  /* forward: also write the slope mask (implied by CF_FUSE_POOL2) */
 
 /* Bitmask of the fused entry points of this library that accept (desc, flags):
  * 1 = cf_conv3d_fwd_fused, 2 = cf_conv3d_bwd_weight_fused,
  * 4 = cf_conv3d_bwd_data_fused, 8 = cf_conv3d_bwd_weight_fused_dz.
+ * The backward calls take (g, mask) = (pooled-output gradient, slope mask)
+ * with CF_FUSE_POOL2, and (dy, y) -- the gradient of the activation and the
+ * activation the fused forward wrote -- with flags == 0 (fp32 layers).
  * Host-only; 0 on an invalid desc. */
 int32_t cf_conv3d_fused_supported(const cf_conv3d_desc *desc, uint32_t flags);
 
@@ -197,7 +201,8 @@ size_t cf_conv3d_mask_bytes(const cf_conv3d_desc *desc);
  * With CF_FUSE_POOL2: out = avgpool 2^3 stride 2 of y, [n,od/2,oh/2,ow/2,c_out]
  * (floor), summed in fp32 and rounded once; mask (required, see
  * cf_conv3d_mask_bytes) records u > 0 for every conv-output element.
- * Without it: out = y [n,od,oh,ow,c_out] in dtype, and mask may be NULL.
+ * Without it: out = y [n,od,oh,ow,c_out] in dtype, and mask may be NULL
+ * (required with CF_FUSE_MASK).
  * alpha must be finite and >= 0 (then u > 0 <=> y > 0, the slope rule of
  * cf_bias_lrelu_bwd).  Unsupported shapes return CF_ERR_UNSUPPORTED (see
  * cf_conv3d_fused_supported); the unfused calls cover every shape. */
@@ -211,6 +216,10 @@ size_t cf_conv3d_bwd_weight_fused_workspace_size(const cf_conv3d_desc *desc, uin
 /* Fused backward-weights.  With CF_FUSE_POOL2, g is the gradient of the
  * pooled output [n,od/2,oh/2,ow/2,c_out] and mask the forward's slope mask:
  *   dz[v,c] = g[pool(v),c] / 8 * (mask(v,c) ? 1 : alpha)  (0 where no window covers v)
+ * With flags == 0 (unpooled layer, the "dy + y" form), g is the gradient dy of
+ * the activation and mask points to the activation y [n,od,oh,ow,c_out] the
+ * fused forward wrote (both in dtype):
+ *   dz[v,c] = dy[v,c] * (y[v,c] > 0 ? 1 : alpha)   (the slope rule of cf_bias_lrelu_bwd)
  *   dW[t,ci,co] = sum_{n,o} x[n, o*s + t - pad_before, ci] * dz[n,o,co]   (fp32)
  *   db[c] = sum_v dz[v,c]                                                  (fp32)
  * dz is formed in fp32 (bf16 path: rounded to bf16 before the product, as
@@ -222,7 +231,7 @@ cf_status cf_conv3d_bwd_weight_fused(const cf_conv3d_desc *desc, const void *x, 
                                      float *db, void *ws, size_t ws_bytes, void *stream);
 
 /* Fused backward-weights that also stores the rebuilt dz (bit 8 of
- * cf_conv3d_fused_supported; CF_FUSE_POOL2 required).  dW, db and ws exactly
+ * cf_conv3d_fused_supported; either form of the inputs).  dW, db and ws exactly
  * as cf_conv3d_bwd_weight_fused (bitwise the same results); in addition dz
  * [n,od,oh,ow,c_out] in dtype receives every element of the rebuilt
  * gradient, rounded as described there -- the input a following
@@ -235,9 +244,9 @@ cf_status cf_conv3d_bwd_weight_fused_dz(const cf_conv3d_desc *desc, const void *
                                         float *db, void *dz, void *ws, size_t ws_bytes,
                                         void *stream);
 
-/* Fused backward-data (CF_FUSE_POOL2 required): dz is rebuilt from the
- * pooled-output gradient g and the slope mask exactly as in
- * cf_conv3d_bwd_weight_fused (rounded to the path dtype), then
+/* Fused backward-data: dz is rebuilt from (g, mask) -- the pooled-output
+ * gradient and the slope mask with CF_FUSE_POOL2, (dy, y) with flags == 0 --
+ * exactly as in cf_conv3d_bwd_weight_fused (rounded to the path dtype), then
  *   dx[n,i,ci] = sum over (o,t) with o*s + t - pad_before = i of sum_co dz[n,o,co] * W[t,ci,co].
  * dx [n,d,h,w,c_in] in dtype; every element is written. */
 cf_status cf_conv3d_bwd_data_fused(const cf_conv3d_desc *desc, const void *g, const void *mask,

@@ -22,6 +22,7 @@ CF_OK, CF_ERR_INVALID_ARG, CF_ERR_UNSUPPORTED, CF_ERR_ALIGNMENT, CF_ERR_ALIAS, \
 CF_F32, CF_BF16 = 0, 1
 CF_PAD_SAME_TF, CF_PAD_VALID = 0, 1
 CF_FUSE_POOL2 = 1
+CF_FUSE_MASK = 2
 FUSED_FWD, FUSED_BWD_WEIGHT, FUSED_BWD_DATA, FUSED_BWD_WEIGHT_DZ = 1, 2, 4, 8
 
 STATUS_NAMES = {0: "CF_OK", 1: "CF_ERR_INVALID_ARG", 2: "CF_ERR_UNSUPPORTED", 3: "CF_ERR_ALIGNMENT",

@@ -373,12 +373,19 @@ cf_status cf_avgpool3d_bwd(int32_t n, int32_t d, int32_t h, int32_t w, int32_t c
 
 static int32_t fused_mask(const cf::ConvShape &s, uint32_t flags) {
   int32_t m = 0;
+  if (flags & ~(CF_FUSE_POOL2 | CF_FUSE_MASK)) return 0;
+  // the mask flag only asks the forward for the mask; with the pool it is implied
+  const bool ymode = flags == 0;  // unpooled backward from (dy, y)
+  if (flags & CF_FUSE_POOL2) flags = CF_FUSE_POOL2;
   if (flags == CF_FUSE_POOL2) {
     if (cf::smallc_supported(s, true)) m |= 1;
     if (cf::smallc_wgrad_fused_supported(s) || cf::c16_wgrad_supported(s)) m |= 2;
   }
   if (cf::c16_fwd_supported(s)) m |= 1;  // with or without the pool
-  if (flags == 0 && (cf::direct_supported(s, true) || cf::f32conv_supported(s, true))) m |= 1;
+  if ((flags == 0 || flags == CF_FUSE_MASK) && (cf::direct_supported(s, true) || cf::f32conv_supported(s, true)))
+    m |= 1;
+  if (ymode && cf::f32wgrad_supported(s)) m |= 2 | 8;
+  if (ymode && cf::f32conv_supported(s, false)) m |= 4;
   if (flags == CF_FUSE_POOL2 && cf::f32conv_pool_supported(s)) m |= 1;
   if (flags == CF_FUSE_POOL2 && cf::c16_bwd_supported(s)) m |= 4;
   if (flags == CF_FUSE_POOL2 && cf::c16_wgrad_supported(s) && !cf::smallc_wgrad_fused_supported(s)) m |= 8;
@@ -401,9 +408,10 @@ static size_t mask_bytes(const cf::ConvShape &s) {
   return (bits + 31) / 32 * 4;
 }
 
-static size_t fused_wgrad_workspace(const cf::ConvShape &s) {
+static size_t fused_wgrad_workspace(const cf::ConvShape &s, uint32_t flags) {
+  if (!(flags & CF_FUSE_POOL2)) return cf::f32wgrad_workspace(s, 3);  // (dy, y)
   if (cf::smallc_wgrad_fused_supported(s)) return cf::smallc_wgrad_fused_workspace(s);
-  if (cf::f32wgrad_fused_supported(s)) return cf::f32wgrad_workspace(s, true);
+  if (cf::f32wgrad_fused_supported(s)) return cf::f32wgrad_workspace(s, 1);
   return cf::c16_wgrad_workspace(s);
 }
 
@@ -429,13 +437,14 @@ cf_status cf_conv3d_fwd_fused(const cf_conv3d_desc *desc, const void *x, const v
   cf_status r = resolve(desc, &s);
   if (r != CF_OK) return r;
   if (!std::isfinite(alpha) || alpha < 0.f) return fail(CF_ERR_INVALID_ARG, "alpha must be finite and >= 0");
-  if (flags & ~CF_FUSE_POOL2) return fail(CF_ERR_INVALID_ARG, "unknown flags");
+  if (flags & ~(CF_FUSE_POOL2 | CF_FUSE_MASK)) return fail(CF_ERR_INVALID_ARG, "unknown flags");
   if (!(fused_mask(s, flags) & 1))
     return fail(CF_ERR_UNSUPPORTED, "conv3d_fwd_fused: no fused kernel for this layer shape / flags");
   if (s.n == 0) return ok();
   const bool pool = (flags & CF_FUSE_POOL2) != 0;
   if ((r = check_ptrs({x, w, out})) != CF_OK) return r;
   if (pool && !mask) return fail(CF_ERR_INVALID_ARG, "conv3d_fwd_fused: the pooled variant needs the mask");
+  if ((flags & CF_FUSE_MASK) && !mask) return fail(CF_ERR_INVALID_ARG, "conv3d_fwd_fused: CF_FUSE_MASK needs the mask");
   if (mask && !aligned16(mask)) return fail(CF_ERR_ALIGNMENT, "mask not 16-byte aligned");
   if (!bias) return fail(CF_ERR_INVALID_ARG, "bias is NULL");
   Sizes b = conv_bytes(s);
@@ -466,7 +475,7 @@ size_t cf_conv3d_bwd_weight_fused_workspace_size(const cf_conv3d_desc *desc, uin
     g_last_error = keep;
     return 0;
   }
-  return fused_wgrad_workspace(s);
+  return fused_wgrad_workspace(s, flags);
 }
 
 static cf_status bwd_weight_fused(const char *name, const cf_conv3d_desc *desc, const void *x, const void *g,
@@ -476,9 +485,10 @@ static cf_status bwd_weight_fused(const char *name, const cf_conv3d_desc *desc, 
   cf_status r = resolve(desc, &s);
   if (r != CF_OK) return r;
   if (!std::isfinite(alpha) || alpha < 0.f) return fail(CF_ERR_INVALID_ARG, "alpha must be finite and >= 0");
-  if (flags & ~CF_FUSE_POOL2) return fail(CF_ERR_INVALID_ARG, "unknown flags");
+  if (flags & ~(CF_FUSE_POOL2 | CF_FUSE_MASK)) return fail(CF_ERR_INVALID_ARG, "unknown flags");
   if (!(fused_mask(s, flags) & (dz ? 8 : 2)))
     return fail(CF_ERR_UNSUPPORTED, std::string(name) + ": no fused kernel for this layer shape / flags");
+  const bool pool = (flags & CF_FUSE_POOL2) != 0;
   hipStream_t st = (hipStream_t)stream;
   const size_t dw_bytes = (size_t)s.kd * s.kh * s.kw * s.ci * s.co * sizeof(float);
   if (s.n == 0) {
@@ -489,11 +499,12 @@ static cf_status bwd_weight_fused(const char *name, const cf_conv3d_desc *desc, 
   }
   if ((r = check_ptrs({x, g, mask, dw, db})) != CF_OK) return r;
   if (dz && (r = check_ptrs({dz})) != CF_OK) return r;
-  const size_t need = fused_wgrad_workspace(s);
+  const size_t need = fused_wgrad_workspace(s, flags);
   if (!ws || ws_bytes < need) return fail(CF_ERR_WORKSPACE, std::string(name) + ": workspace smaller than the size query");
   if (!aligned16(ws)) return fail(CF_ERR_ALIGNMENT, "workspace not 16-byte aligned");
   Sizes b = conv_bytes(s);
-  const size_t gb = pooled_bytes(s), mb = mask_bytes(s), dbb = (size_t)s.co * 4;
+  // pooled: g = pooled-output gradient, mask = slope mask; else g = dy, mask = y
+  const size_t gb = pool ? pooled_bytes(s) : b.z, mb = pool ? mask_bytes(s) : b.z, dbb = (size_t)s.co * 4;
   const void *ins[3] = {x, g, mask};
   const size_t insz[3] = {b.x, gb, mb};
   for (int i = 0; i < 3; ++i)
@@ -505,11 +516,14 @@ static cf_status bwd_weight_fused(const char *name, const cf_conv3d_desc *desc, 
   if (dz && (overlap(dz, b.z, dw, dw_bytes) || overlap(dz, b.z, db, dbb) || overlap(dz, b.z, ws, need)))
     return fail(CF_ERR_ALIAS, std::string(name) + ": dz overlaps another output or the workspace");
   hipError_t e;
-  if (cf::smallc_wgrad_fused_supported(s))
+  if (!pool)
+    e = cf::launch_conv_bwd_weight_f32(s, (const float *)x, (const float *)g, mask, alpha, dw, db, ws, 3, (float *)dz,
+                                       st);
+  else if (cf::smallc_wgrad_fused_supported(s))
     e = cf::launch_smallc_wgrad_fused(s, x, g, (const uint16_t *)mask, alpha, dw, db, ws, st);
   else if (cf::f32wgrad_fused_supported(s))
-    e = cf::launch_conv_bwd_weight_f32(s, (const float *)x, (const float *)g, (const uint32_t *)mask, alpha, dw, db,
-                                       ws, true, (float *)dz, st);
+    e = cf::launch_conv_bwd_weight_f32(s, (const float *)x, (const float *)g, mask, alpha, dw, db, ws, 1, (float *)dz,
+                                       st);
   else
     e = cf::launch_conv_bwd_weight_c16(s, x, g, (const uint32_t *)mask, alpha, dw, db, ws, true, dz, st);
   return finish(e, st, name);
@@ -536,17 +550,22 @@ cf_status cf_conv3d_bwd_data_fused(const cf_conv3d_desc *desc, const void *g, co
   cf_status r = resolve(desc, &s);
   if (r != CF_OK) return r;
   if (!std::isfinite(alpha) || alpha < 0.f) return fail(CF_ERR_INVALID_ARG, "alpha must be finite and >= 0");
-  if (flags & ~CF_FUSE_POOL2) return fail(CF_ERR_INVALID_ARG, "unknown flags");
+  if (flags & ~(CF_FUSE_POOL2 | CF_FUSE_MASK)) return fail(CF_ERR_INVALID_ARG, "unknown flags");
   if (!(fused_mask(s, flags) & 4))
     return fail(CF_ERR_UNSUPPORTED, "conv3d_bwd_data_fused: no fused kernel for this layer shape / flags");
   if (s.n == 0) return ok();
   if ((r = check_ptrs({g, mask, w, dx})) != CF_OK) return r;
   Sizes b = conv_bytes(s);
-  if (overlap(dx, b.x, g, pooled_bytes(s)) || overlap(dx, b.x, mask, mask_bytes(s)) || overlap(dx, b.x, w, b.w))
+  const bool pool = (flags & CF_FUSE_POOL2) != 0;
+  const size_t gb = pool ? pooled_bytes(s) : b.z, mb = pool ? mask_bytes(s) : b.z;
+  if (overlap(dx, b.x, g, gb) || overlap(dx, b.x, mask, mb) || overlap(dx, b.x, w, b.w))
     return fail(CF_ERR_ALIAS, "conv3d_bwd_data_fused: dx overlaps an input");
   hipStream_t st = (hipStream_t)stream;
-  return finish(cf::launch_conv_bwd_data_c16(s, g, (const uint32_t *)mask, w, alpha, dx, true, st), st,
-                "cf_conv3d_bwd_data_fused");
+  const hipError_t e =
+      pool ? cf::launch_conv_bwd_data_c16(s, g, (const uint32_t *)mask, w, alpha, dx, true, st)
+           : cf::launch_conv_bwd_data_f32(s, (const float *)g, (const float *)w, (float *)dx, st, (const float *)mask,
+                                          alpha);
+  return finish(e, st, "cf_conv3d_bwd_data_fused");
 }
 
 // ---------------------------------------------------------------------------

@@ -99,7 +99,9 @@ bool f32conv_supported(const ConvShape &s, bool fwd);
 bool f32conv_pool_supported(const ConvShape &s);
 hipError_t launch_conv_fwd_f32(const ConvShape &s, const float *x, const float *w, const float *bias, float alpha,
                                float *out, uint8_t *mask, int epi, hipStream_t st);
-hipError_t launch_conv_bwd_data_f32(const ConvShape &s, const float *dz, const float *w, float *dx, hipStream_t st);
+// y non-null: the A operand is dz = dy * (y > 0 ? 1 : alpha) from dy (the dz argument) and y
+hipError_t launch_conv_bwd_data_f32(const ConvShape &s, const float *dz, const float *w, float *dx, hipStream_t st,
+                                    const float *y = nullptr, float alpha = 0.f);
 
 // fp32 backward-weights on v_mfma_f32_16x16x4_f32 (conv_f32_wgrad.hip), ci % 16 == 0,
 // co % 16 == 0: voxel slices' partials in ws, summed by launch_sum_rows.  fused (the
@@ -114,9 +116,10 @@ size_t l1f32_wgrad_workspace(const ConvShape &s);
 hipError_t launch_l1_wgrad_f32(const ConvShape &s, const float *x, const float *dp, const uint16_t *mask,
                                float alpha, float *dw, float *db, void *ws, hipStream_t st);
 bool f32wgrad_fused_supported(const ConvShape &s);
-size_t f32wgrad_workspace(const ConvShape &s, bool fused);
-hipError_t launch_conv_bwd_weight_f32(const ConvShape &s, const float *x, const float *g, const uint32_t *mask,
-                                      float alpha, float *dw, float *db, void *ws, bool fused, float *dz_out,
+// gm: 0 g = dz; 1 g = pooled gradient, aux = slope mask; 3 g = dy, aux = the activation y
+size_t f32wgrad_workspace(const ConvShape &s, int gm);
+hipError_t launch_conv_bwd_weight_f32(const ConvShape &s, const float *x, const float *g, const void *aux,
+                                      float alpha, float *dw, float *db, void *ws, int gm, float *dz_out,
                                       hipStream_t st);
 
 hipError_t launch_conv_fwd(const ConvShape &s, const void *x, const void *w, void *z,

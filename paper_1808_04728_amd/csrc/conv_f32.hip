@@ -118,8 +118,13 @@ __device__ __forceinline__ uint32_t shift_lane(uint32_t a, uint32_t e) {
 // along the 16-lane row (DPP row shift), the lanes shifted in at the edge coming
 // from a second fragment 16 voxels further along (row rotate): two loads per
 // fragment and kernel row instead of UW.
-template <bool FWD, int FM, int FN, int WM, int WK, int PF, int EPI, int UW = 0>
+//
+// DYY (backward-data of an unpooled fused layer): the gathered operand is
+// dz = dy * (y > 0 ? 1 : alpha), formed from dy (src) and the layer's saved
+// activation y (ysrc, the same layout) after both loads arrive.
+template <bool FWD, int FM, int FN, int WM, int WK, int PF, int EPI, int UW = 0, bool DYY = false>
 __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__restrict__ src,
+                                                                const float *__restrict__ ysrc,
                                                                 const float *__restrict__ wt,
                                                                 const float *__restrict__ bias,
                                                                 float *__restrict__ dst, uint8_t *__restrict__ mask,
@@ -160,7 +165,18 @@ __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__r
   const int m0 = tile * BM;
 
   const __amdgpu_buffer_rsrc_t srsrc = __builtin_amdgcn_make_buffer_rsrc((void *)src, (short)0, p.src_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t yrsrc =
+      __builtin_amdgcn_make_buffer_rsrc((void *)ysrc, (short)0, DYY ? p.src_bytes : 0u, 0x00020000);
   const __amdgpu_buffer_rsrc_t wrsrc = __builtin_amdgcn_make_buffer_rsrc((void *)wt, (short)0, p.w_bytes, 0x00020000);
+  // dz from dy and y, four channels at a time (DYY)
+  auto slope4 = [&](u32x4_t d, u32x4_t y) {
+    u32x4_t r;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) r[j] = __float_as_uint(f_of(d[j]) * (f_of(y[j]) > 0.f ? 1.f : p.alpha));
+    return r;
+  };
+  (void)yrsrc;
+  (void)slope4;
 
   // ---- source base of this lane's row in each of its fragments -------------
   int rbd[FM], rbh[FM], rbw[FM], roff[FM];
@@ -224,8 +240,10 @@ __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__r
     constexpr int EDGE = FWD ? 16 : -16;  // voxels from a fragment to its edge fragment
     constexpr int NS = PF + 1;
     u32x4_t a_r[NS][FM], e_r[NS][FM];
+    u32x4_t ya_r[DYY ? NS : 1][FM], ye_r[DYY ? NS : 1][FM];
     uint32_t b_r[NS][UW][NB][BW];
-    auto load = [&](u32x4_t(&a)[FM], u32x4_t(&e)[FM], uint32_t(&b)[UW][NB][BW]) {
+    auto load = [&](u32x4_t(&a)[FM], u32x4_t(&e)[FM], u32x4_t(&ya)[FM], u32x4_t(&ye)[FM],
+                    uint32_t(&b)[UW][NB][BW]) {
       const FTap &T = p.tap[C.tap0 + ri * UW];
       const int cofs = cc * 16;
       const bool live = ldstep < nsteps;
@@ -239,6 +257,10 @@ __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__r
         const int o = roff[i] + T.a_off + cofs;
         a[i] = ld128(srsrc, ((uint32_t)o * 4u) | ((uint32_t)!oka << 31));
         e[i] = ld128(srsrc, ((uint32_t)(o + EDGE * p.sc) * 4u) | ((uint32_t)!oke << 31));
+        if constexpr (DYY) {
+          ya[i] = ld128(yrsrc, ((uint32_t)o * 4u) | ((uint32_t)!oka << 31));
+          ye[i] = ld128(yrsrc, ((uint32_t)(o + EDGE * p.sc) * 4u) | ((uint32_t)!oke << 31));
+        }
       }
 #pragma unroll
       for (int uw = 0; uw < UW; ++uw) {
@@ -260,13 +282,21 @@ __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__r
       const int niter = (nsteps + NS - 1) / NS * NS;
 #pragma unroll
       for (int q = 0; q < PF; ++q) {
-        load(a_r[q], e_r[q], b_r[q]);
+        load(a_r[q], e_r[q], ya_r[DYY ? q : 0], ye_r[DYY ? q : 0], b_r[q]);
         next();
       }
       for (int s0 = 0; s0 < niter; s0 += NS) {
 #pragma unroll
         for (int q = 0; q < NS; ++q) {
-          load(a_r[(q + PF) % NS], e_r[(q + PF) % NS], b_r[(q + PF) % NS]);
+          load(a_r[(q + PF) % NS], e_r[(q + PF) % NS], ya_r[DYY ? (q + PF) % NS : 0], ye_r[DYY ? (q + PF) % NS : 0],
+               b_r[(q + PF) % NS]);
+          if constexpr (DYY) {
+#pragma unroll
+            for (int i = 0; i < FM; ++i) {
+              a_r[q][i] = slope4(a_r[q][i], ya_r[q][i]);
+              e_r[q][i] = slope4(e_r[q][i], ye_r[q][i]);
+            }
+          }
           next();
           __builtin_amdgcn_sched_barrier(0);  // prefetch loads stay ahead of the MFMAs
           auto column = [&](auto uwc) {
@@ -322,8 +352,9 @@ __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__r
     constexpr int NS = PF + 1;
     constexpr int BW = FWD ? FN : 4;  // floats per weight load
     u32x4_t a_r[NS][FM];
+    u32x4_t ya_r[DYY ? NS : 1][FM];
     uint32_t b_r[NS][NB][BW];
-    auto load = [&](u32x4_t(&a)[FM], uint32_t(&b)[NB][BW]) {
+    auto load = [&](u32x4_t(&a)[FM], u32x4_t(&ya)[FM], uint32_t(&b)[NB][BW]) {
       const FTap &T = p.tap[C.tap0 + ti];
       const int cofs = cc * 16;
       const bool live = ldstep < nsteps;
@@ -335,6 +366,7 @@ __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__r
         // a valid byte offset is below 2^31: setting bit 31 sends the load past the
         // buffer (it returns zeros) without a select the compiler could turn into a branch
         a[i] = ld128(srsrc, ((uint32_t)(roff[i] + T.a_off + cofs) * 4u) | ((uint32_t)!ok << 31));
+        if constexpr (DYY) ya[i] = ld128(yrsrc, ((uint32_t)(roff[i] + T.a_off + cofs) * 4u) | ((uint32_t)!ok << 31));
       }
       const int wbase = T.w_off + cofs * (FWD ? p.wco : 1);
   #pragma unroll
@@ -356,14 +388,14 @@ __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__r
       const int niter = (nsteps + NS - 1) / NS * NS;
   #pragma unroll
       for (int q = 0; q < PF; ++q) {
-        load(a_r[q], b_r[q]);
+        load(a_r[q], ya_r[DYY ? q : 0], b_r[q]);
         next();
       }
       for (int s0 = 0; s0 < niter; s0 += NS) {
   #pragma unroll
         for (int q = 0; q < NS; ++q) {
           const int s = s0 + q;
-          load(a_r[(q + PF) % NS], b_r[(q + PF) % NS]);
+          load(a_r[(q + PF) % NS], ya_r[DYY ? (q + PF) % NS : 0], b_r[(q + PF) % NS]);
           next();
           // keep the prefetch loads ahead of this step's MFMAs: sunk below them,
           // the wait before the next step would cover every load in flight
@@ -371,7 +403,8 @@ __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__r
           (void)s;
   #pragma unroll
           for (int i = 0; i < FM; ++i) {
-            const u32x4_t av = a_r[q][i];
+            u32x4_t av = a_r[q][i];
+            if constexpr (DYY) av = slope4(av, ya_r[q][i]);
   #pragma unroll
             for (int j = 0; j < 4; ++j) {
   #pragma unroll
@@ -560,15 +593,15 @@ struct FCfg {
 constexpr FCfg kCand[] = {{4, 1, 1}, {4, 2, 1}, {2, 2, 1}, {4, 1, 4}, {2, 1, 4}, {1, 1, 4}, {1, 1, 8}, {2, 1, 8}};
 constexpr int kNCand = sizeof(kCand) / sizeof(kCand[0]);
 
-template <bool FWD, int FN, int EPI, int FM, int WM, int WK, int UW = 0>
+template <bool FWD, int FN, int EPI, int FM, int WM, int WK, int UW = 0, bool DYY = false>
 hipError_t launch_f(const FParams &p, int tiles, const float *src, const float *w, const float *bias, float *dst,
-                    uint8_t *mask, hipStream_t st) {
+                    uint8_t *mask, hipStream_t st, const float *ysrc = nullptr) {
   dim3 grid((unsigned)tiles, p.dc / (16 * FN), 1);
   if (grid.x == 0 || grid.y == 0) return hipSuccess;
   // shift-mode k-steps hold UW taps: one step of prefetch covers the latency
   constexpr int PF = UW > 0 ? 1 : 2;
-  hipLaunchKernelGGL((conv_f32_kernel<FWD, FM, FN, WM, WK, PF, EPI, UW>), grid, dim3(64 * WM * WK), 0, st, src, w,
-                     bias, dst, mask, p);
+  hipLaunchKernelGGL((conv_f32_kernel<FWD, FM, FN, WM, WK, PF, EPI, UW, DYY>), grid, dim3(64 * WM * WK), 0, st, src,
+                     ysrc, w, bias, dst, mask, p);
   return hipGetLastError();
 }
 
@@ -601,12 +634,12 @@ double f_cost(FParams &p, const FCfg &c, int fn) {
   return rounds * (steps * 4.0 * c.fm * fn + 200.0);
 }
 
-template <bool FWD, int FN, int EPI>
+template <bool FWD, int FN, int EPI, bool DYY = false>
 hipError_t launch_lin(const ConvShape &s, FParams &p, const float *src, const float *w, const float *bias, float *dst,
-                      uint8_t *mask, hipStream_t st) {
+                      uint8_t *mask, hipStream_t st, const float *ysrc = nullptr) {
   if (f_shift_ok(s, p) && !getenv("CF_F32_TILE") &&
       (f_shift_env() == 1 || f_assign(p, 64) * (p.dc / (16 * FN)) >= 4 * kNumCUs))
-    return launch_f<FWD, FN, EPI, 4, 1, 1, 4>(p, f_assign(p, 64), src, w, bias, dst, mask, st);
+    return launch_f<FWD, FN, EPI, 4, 1, 1, 4, DYY>(p, f_assign(p, 64), src, w, bias, dst, mask, st, ysrc);
   int pick = 0;
   double best = 0.0;
   for (int i = 0; i < kNCand; ++i) {
@@ -621,7 +654,7 @@ hipError_t launch_lin(const ConvShape &s, FParams &p, const float *src, const fl
   const FCfg c = kCand[pick];
   const int tiles = f_assign(p, 16 * c.fm * c.wm);
 #define CF_F32_CASE(I, FM_, WM_, WK_) \
-  case I: return launch_f<FWD, FN, EPI, FM_, WM_, WK_>(p, tiles, src, w, bias, dst, mask, st);
+  case I: return launch_f<FWD, FN, EPI, FM_, WM_, WK_, 0, DYY>(p, tiles, src, w, bias, dst, mask, st, ysrc);
   switch (pick) {
     CF_F32_CASE(0, 4, 1, 1)
     CF_F32_CASE(1, 4, 2, 1)
@@ -630,7 +663,7 @@ hipError_t launch_lin(const ConvShape &s, FParams &p, const float *src, const fl
     CF_F32_CASE(4, 2, 1, 4)
     CF_F32_CASE(5, 1, 1, 4)
     CF_F32_CASE(6, 1, 1, 8)
-    default: return launch_f<FWD, FN, EPI, 2, 1, 8>(p, tiles, src, w, bias, dst, mask, st);
+    default: return launch_f<FWD, FN, EPI, 2, 1, 8, 0, DYY>(p, tiles, src, w, bias, dst, mask, st, ysrc);
   }
 #undef CF_F32_CASE
 }
@@ -687,10 +720,17 @@ hipError_t launch_conv_fwd_f32(const ConvShape &s, const float *x, const float *
                  : launch_lin<true, 2, 0>(s, p, x, w, nullptr, out, nullptr, st);
 }
 
-hipError_t launch_conv_bwd_data_f32(const ConvShape &s, const float *dz, const float *w, float *dx, hipStream_t st) {
+hipError_t launch_conv_bwd_data_f32(const ConvShape &s, const float *dz, const float *w, float *dx, hipStream_t st,
+                                    const float *y, float alpha) {
   FParams p{};
   f_tables(s, false, p);
+  p.alpha = alpha;
   const int fn = s.ci % 64 == 0 ? 4 : (s.ci % 32 == 0 ? 2 : 1);
+  if (y) {
+    if (fn == 4) return launch_lin<false, 4, 0, true>(s, p, dz, w, nullptr, dx, nullptr, st, y);
+    if (fn == 2) return launch_lin<false, 2, 0, true>(s, p, dz, w, nullptr, dx, nullptr, st, y);
+    return launch_lin<false, 1, 0, true>(s, p, dz, w, nullptr, dx, nullptr, st, y);
+  }
   if (fn == 4) return launch_lin<false, 4, 0>(s, p, dz, w, nullptr, dx, nullptr, st);
   if (fn == 2) return launch_lin<false, 2, 0>(s, p, dz, w, nullptr, dx, nullptr, st);
   return launch_lin<false, 1, 0>(s, p, dz, w, nullptr, dx, nullptr, st);

@@ -25,12 +25,15 @@
 // ahead through range-checked buffer loads (a padding tap or a voxel past the
 // slice reads zero).
 //
-// Fused variant (the pooled 16 -> 32 layer): the gradient operand is rebuilt
-// from the pooled-output gradient g and the forward's slope mask,
+// Fused variants: the gradient operand is rebuilt from the layer's output
+// gradient -- pooled layers: from the pooled-output gradient g and the
+// forward's slope mask,
 //   dz[v, co] = g[pool(v), co] / 8 * (mask bit (v, co) ? 1 : alpha)
-// (zero outside complete pooling windows), the bias gradient db = sum_v dz is
-// summed from the same values in a fixed order, and dz can be stored once for
-// the layer's backward-data.
+// (zero outside complete pooling windows); unpooled layers: from the gradient
+// dy of the activation y and y itself,
+//   dz[v, co] = dy[v, co] * (y[v, co] > 0 ? 1 : alpha)
+// -- the bias gradient db = sum_v dz is summed from the same values in a fixed
+// order, and dz can be stored once for the layer's backward-data.
 
 #include "cf_common.h"
 #include "cf_kernels.h"
@@ -67,11 +70,16 @@ __device__ __forceinline__ u32x4_t ld128(__amdgpu_buffer_rsrc_t r, uint32_t off)
   return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
 }
 
-// KW4: units are (kd, kh, 16 channels) of a kernel 4 wide; else (tap, 64 channels)
-template <bool FUSED, bool KW4, int RU, int FN, int WV, int PF>
+// gradient operand of the weight-gradient kernel
+enum : int { GM_DZ = 0, GM_POOL_MASK = 1, GM_DY_Y = 3 };
+
+// KW4: units are (kd, kh, 16 channels) of a kernel 4 wide; else (tap, 64 channels).
+// GM_DZ: g is dz; GM_POOL_MASK: g is the pooled gradient, aux the slope mask;
+// GM_DY_Y: g is dy, aux the activation y.
+template <int GM, bool KW4, int RU, int FN, int WV, int PF>
 __global__ __launch_bounds__(64 * WV) void wgrad_f32_kernel(const float *__restrict__ x,
                                                             const float *__restrict__ g,
-                                                            const uint32_t *__restrict__ mask,
+                                                            const void *__restrict__ aux,
                                                             float *__restrict__ part_w, float *__restrict__ part_b,
                                                             float *__restrict__ dz_out, const WF32Params p) {
   __shared__ float dbs[4][16 * FN];
@@ -81,12 +89,13 @@ __global__ __launch_bounds__(64 * WV) void wgrad_f32_kernel(const float *__restr
   const int co0 = blockIdx.y * 16 * FN;
   const int slice = blockIdx.z;
   // the bias gradient and the stored dz come from one wave of the slice
+  constexpr bool FUSED = GM != GM_DZ;
   const bool lead = FUSED && blockIdx.x == 0 && wave == 0;
 
   const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc((void *)x, (short)0, p.x_bytes, 0x00020000);
   const __amdgpu_buffer_rsrc_t gr = __builtin_amdgcn_make_buffer_rsrc((void *)g, (short)0, p.g_bytes, 0x00020000);
   const __amdgpu_buffer_rsrc_t mr =
-      __builtin_amdgcn_make_buffer_rsrc((void *)mask, (short)0, FUSED ? p.m_bytes : 0u, 0x00020000);
+      __builtin_amdgcn_make_buffer_rsrc((void *)aux, (short)0, FUSED ? p.m_bytes : 0u, 0x00020000);
 
   // ---- this wave's row units: the lane's tap and channel, and its dW rows ---
   const int u0 = (blockIdx.x * WV + wave) * RU;
@@ -141,7 +150,7 @@ __global__ __launch_bounds__(64 * WV) void wgrad_f32_kernel(const float *__restr
       xrow[i] = ((nn * p.d + bd + tkd[i]) * p.h + bh + tkh[i]) * p.w;
     }
     rowvox = row * p.ow;
-    if constexpr (FUSED) {
+    if constexpr (GM == GM_POOL_MASK) {
       const int pd_ = od_ >> 1, ph_ = oh_ >> 1;
       winrow = (pd_ < p.pod) & (ph_ < p.poh);
       prow = ((nn * p.pod + pd_) * p.poh + ph_) * p.pow_;
@@ -165,11 +174,13 @@ __global__ __launch_bounds__(64 * WV) void wgrad_f32_kernel(const float *__restr
   u32x4_t a_r[NS][RU];
   float b_r[NS][FN];
   uint32_t m_r[NS];
+  float y_r[NS][FN];
   int v_r[NS];  // voxel of the lane's K slot (-1: none), for the stored dz
   (void)m_r;
+  (void)y_r;
   (void)v_r;
 
-  auto load = [&](u32x4_t(&a)[RU], float(&b)[FN], uint32_t &mw, int &vx) {
+  auto load = [&](u32x4_t(&a)[RU], float(&b)[FN], uint32_t &mw, float(&yv)[FN], int &vx) {
     const int w = 4 * cws + g4;
     const bool wok = (ldstep < nsteps) & (w < p.ow);
     const int bw = w * p.sw - p.pw;
@@ -183,7 +194,7 @@ __global__ __launch_bounds__(64 * WV) void wgrad_f32_kernel(const float *__restr
     }
     const int v = rowvox + w;
     vx = wok ? v : -1;
-    if constexpr (FUSED) {
+    if constexpr (GM == GM_POOL_MASK) {
       const int pw_ = w >> 1;
       const bool win = winrow & wok & (pw_ < p.pow_);
       const int gb = (prow + pw_) * p.co + co0 + r16;
@@ -195,8 +206,11 @@ __global__ __launch_bounds__(64 * WV) void wgrad_f32_kernel(const float *__restr
     } else {
       const int gb = v * p.co + co0 + r16;
 #pragma unroll
-      for (int j = 0; j < FN; ++j)
-        b[j] = __uint_as_float(ld32(gr, ((uint32_t)(gb + 16 * j) * 4u) | ((uint32_t)!wok << 31)));
+      for (int j = 0; j < FN; ++j) {
+        const uint32_t off = ((uint32_t)(gb + 16 * j) * 4u) | ((uint32_t)!wok << 31);
+        b[j] = __uint_as_float(ld32(gr, off));
+        if constexpr (GM == GM_DY_Y) yv[j] = __uint_as_float(ld32(mr, off));  // y: the layout of dy
+      }
     }
   };
 
@@ -216,14 +230,14 @@ __global__ __launch_bounds__(64 * WV) void wgrad_f32_kernel(const float *__restr
     const int niter = (nsteps + NS - 1) / NS * NS;
 #pragma unroll
     for (int q = 0; q < PF; ++q) {
-      load(a_r[q], b_r[q], m_r[q], v_r[q]);
+      load(a_r[q], b_r[q], m_r[q], y_r[q], v_r[q]);
       next();
     }
     for (int s0 = 0; s0 < niter; s0 += NS) {
 #pragma unroll
       for (int q = 0; q < NS; ++q) {
         const int sl = (q + PF) % NS;
-        load(a_r[sl], b_r[sl], m_r[sl], v_r[sl]);
+        load(a_r[sl], b_r[sl], m_r[sl], y_r[sl], v_r[sl]);
         next();
         // keep this step's prefetch loads ahead of its MFMAs: the scheduler would
         // otherwise sink them, and the wait before the next step's MFMAs would
@@ -233,9 +247,11 @@ __global__ __launch_bounds__(64 * WV) void wgrad_f32_kernel(const float *__restr
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
           float b = b_r[q][j];
-          if constexpr (FUSED) {
+          if constexpr (GM == GM_POOL_MASK) {
             const bool on = (m_r[q] >> ((co0 + 16 * j + r16) & 31)) & 1u;
             b *= on ? s1 : sa;
+          } else if constexpr (GM == GM_DY_Y) {
+            b *= y_r[q][j] > 0.f ? 1.f : p.alpha;
           }
           bv[j] = b;
         }
@@ -437,7 +453,8 @@ struct WPlan {
   int gx, gy, nsplit, rows_per;
 };
 
-WPlan w_plan(const ConvShape &s, bool fused) {
+WPlan w_plan(const ConvShape &s, int gm) {
+  const bool fused = gm == GM_POOL_MASK;  // 32 channels per workgroup (one mask word)
   WPlan pl{};
   const long long vox = (long long)s.n * s.od * s.oh * s.ow;
   pl.kw4 = s.kw == 4 && s.ci % 16 == 0;
@@ -466,7 +483,7 @@ WPlan w_plan(const ConvShape &s, bool fused) {
   const char *ms = getenv("CF_F32W_MINSTEPS");
   const long long minsteps = ms ? std::max(1, atoi(ms)) : 8;
   want = std::min(want, std::max(1LL, vox / (4 * minsteps)));
-  // slices of whole output rows, at least 16 steps of 4 voxels each
+  // slices of whole output rows, at least minsteps steps of 4 voxels each
   const long long rows = (long long)s.n * s.od * s.oh;
   const long long nws = (s.ow + 3) / 4;
   long long per = (rows + want - 1) / want;
@@ -496,21 +513,33 @@ WF32Params w_params(const ConvShape &s, const WPlan &pl, float alpha) {
   return p;
 }
 
-template <bool FUSED, bool KW4, int RU, int FN>
-hipError_t launch_w(const WPlan &pl, const WF32Params &p, const float *x, const float *g, const uint32_t *mask,
+template <int GM, bool KW4, int RU, int FN>
+hipError_t launch_w(const WPlan &pl, const WF32Params &p, const float *x, const float *g, const void *aux,
                     float *pw, float *pb, float *dz_out, hipStream_t st) {
   dim3 grid(pl.gx, pl.gy, pl.nsplit);
   constexpr int PF = 2;
-  hipLaunchKernelGGL((wgrad_f32_kernel<FUSED, KW4, RU, FN, 8, PF>), grid, dim3(512), 0, st, x, g, mask, pw, pb,
+  hipLaunchKernelGGL((wgrad_f32_kernel<GM, KW4, RU, FN, 8, PF>), grid, dim3(512), 0, st, x, g, aux, pw, pb,
                      dz_out, p);
   return hipGetLastError();
 }
 
-template <bool KW4, int FN>
-hipError_t launch_wu(const WPlan &pl, const WF32Params &p, const float *x, const float *g, float *pw,
-                     hipStream_t st) {
-  return pl.ru == 2 ? launch_w<false, KW4, 2, FN>(pl, p, x, g, nullptr, pw, nullptr, nullptr, st)
-                    : launch_w<false, KW4, 1, FN>(pl, p, x, g, nullptr, pw, nullptr, nullptr, st);
+template <int GM, bool KW4, int FN>
+hipError_t launch_wu(const WPlan &pl, const WF32Params &p, const float *x, const float *g, const void *aux,
+                     float *pw, float *pb, float *dz_out, hipStream_t st) {
+  return pl.ru == 2 ? launch_w<GM, KW4, 2, FN>(pl, p, x, g, aux, pw, pb, dz_out, st)
+                    : launch_w<GM, KW4, 1, FN>(pl, p, x, g, aux, pw, pb, dz_out, st);
+}
+
+template <int GM>
+hipError_t launch_wfn(const WPlan &pl, const WF32Params &p, const float *x, const float *g, const void *aux,
+                      float *pw, float *pb, float *dz_out, hipStream_t st) {
+  if (pl.kw4)
+    return pl.fn == 4 ? launch_wu<GM, true, 4>(pl, p, x, g, aux, pw, pb, dz_out, st)
+         : pl.fn == 2 ? launch_wu<GM, true, 2>(pl, p, x, g, aux, pw, pb, dz_out, st)
+                      : launch_wu<GM, true, 1>(pl, p, x, g, aux, pw, pb, dz_out, st);
+  return pl.fn == 4 ? launch_wu<GM, false, 4>(pl, p, x, g, aux, pw, pb, dz_out, st)
+       : pl.fn == 2 ? launch_wu<GM, false, 2>(pl, p, x, g, aux, pw, pb, dz_out, st)
+                    : launch_wu<GM, false, 1>(pl, p, x, g, aux, pw, pb, dz_out, st);
 }
 
 }  // namespace
@@ -581,39 +610,35 @@ bool f32wgrad_fused_supported(const ConvShape &s) {
   return f32wgrad_supported(s) && s.co % 32 == 0 && s.od >= 2 && s.oh >= 2 && s.ow >= 2;
 }
 
-size_t f32wgrad_workspace(const ConvShape &s, bool fused) {
-  const WPlan pl = w_plan(s, fused);
-  return (size_t)pl.nsplit * ((size_t)s.kd * s.kh * s.kw * s.ci * s.co + (fused ? s.co : 0)) * sizeof(float);
+size_t f32wgrad_workspace(const ConvShape &s, int gm) {
+  const WPlan pl = w_plan(s, gm);
+  return (size_t)pl.nsplit * ((size_t)s.kd * s.kh * s.kw * s.ci * s.co + (gm != GM_DZ ? s.co : 0)) * sizeof(float);
 }
 
-hipError_t launch_conv_bwd_weight_f32(const ConvShape &s, const float *x, const float *g, const uint32_t *mask,
-                                      float alpha, float *dw, float *db, void *ws, bool fused, float *dz_out,
+hipError_t launch_conv_bwd_weight_f32(const ConvShape &s, const float *x, const float *g, const void *aux,
+                                      float alpha, float *dw, float *db, void *ws, int gm, float *dz_out,
                                       hipStream_t st) {
-  const WPlan pl = w_plan(s, fused);
+  const WPlan pl = w_plan(s, gm);
   WF32Params p = w_params(s, pl, alpha);
   float *pw = (float *)ws;
   const int m = p.m;
   float *pb = pw + (size_t)pl.nsplit * m * s.co;
   hipError_t e;
-  if (fused) {
+  if (gm == GM_POOL_MASK) {
     p.g_bytes = (uint32_t)((long long)s.n * p.pod * p.poh * p.pow_ * s.co * 4);
     p.m_bytes = (uint32_t)(((long long)p.vox * s.co + 31) / 32 * 4);
-    e = pl.kw4 ? launch_w<true, true, 2, 2>(pl, p, x, g, mask, pw, pb, dz_out, st)
-               : launch_w<true, false, 2, 2>(pl, p, x, g, mask, pw, pb, dz_out, st);
+    e = pl.kw4 ? launch_w<GM_POOL_MASK, true, 2, 2>(pl, p, x, g, aux, pw, pb, dz_out, st)
+               : launch_w<GM_POOL_MASK, false, 2, 2>(pl, p, x, g, aux, pw, pb, dz_out, st);
+  } else if (gm == GM_DY_Y) {
+    p.g_bytes = p.m_bytes = (uint32_t)((long long)p.vox * s.co * 4);
+    e = launch_wfn<GM_DY_Y>(pl, p, x, g, aux, pw, pb, dz_out, st);
   } else {
     p.g_bytes = (uint32_t)((long long)p.vox * s.co * 4);
-    if (pl.kw4)
-      e = pl.fn == 4 ? launch_wu<true, 4>(pl, p, x, g, pw, st)
-        : pl.fn == 2 ? launch_wu<true, 2>(pl, p, x, g, pw, st)
-                     : launch_wu<true, 1>(pl, p, x, g, pw, st);
-    else
-      e = pl.fn == 4 ? launch_wu<false, 4>(pl, p, x, g, pw, st)
-        : pl.fn == 2 ? launch_wu<false, 2>(pl, p, x, g, pw, st)
-                     : launch_wu<false, 1>(pl, p, x, g, pw, st);
+    e = launch_wfn<GM_DZ>(pl, p, x, g, nullptr, pw, nullptr, nullptr, st);
   }
   if (e != hipSuccess) return e;
   e = launch_sum_rows(pw, dw, pl.nsplit, m * s.co, st);
-  if (e != hipSuccess || !fused) return e;
+  if (e != hipSuccess || gm == GM_DZ) return e;
   return launch_sum_rows(pb, db, pl.nsplit, s.co, st);
 }
 

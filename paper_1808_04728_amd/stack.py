@@ -120,7 +120,12 @@ class ConvStack:
             l["fused"] = bool(self.fused and (sup & both) == both and
                               (not needs_dgrad or sup & (B.FUSED_BWD_DATA | B.FUSED_BWD_WEIGHT_DZ)))
             # otherwise conv + bias + leaky ReLU may still share one kernel (y written once)
-            l["fused_act"] = bool(self.fused and not l["fused"] and B.cf_conv3d_fused_supported(l["desc"], 0) & 1)
+            sup0 = B.cf_conv3d_fused_supported(l["desc"], 0) if not s["pool"] else 0
+            l["fused_act"] = bool(self.fused and not l["fused"] and sup0 & B.FUSED_FWD)
+            # and its backward may take (dy, y) straight into the weight and data
+            # gradients (dz formed inside both, no separate leaky-ReLU backward)
+            l["fused_y"] = bool(l["fused_act"] and sup0 & B.FUSED_BWD_WEIGHT and
+                                (not needs_dgrad or sup0 & B.FUSED_BWD_DATA))
             l["p"] = torch.empty((n,) + l["pool_dhw"] + (s["cout"],), dtype=tdt, device=dev) if s["pool"] else None
             l["gout"] = torch.empty((n,) + l["pool_dhw"] + (s["cout"],), dtype=tdt, device=dev)
             l["dx"] = None
@@ -138,6 +143,12 @@ class ConvStack:
                 continue
             l["z"] = torch.empty((n,) + l["out_dhw"] + (s["cout"],), dtype=tdt, device=dev)  # z, then y in place
             l["dy"] = torch.empty_like(l["z"]) if s["pool"] else None
+            if l["fused_y"]:
+                l["dz"] = None
+                wsf = B.cf_conv3d_bwd_weight_fused_workspace_size(l["desc"], 0)
+                l["ws_w"] = torch.empty(max(wsf, 16), dtype=torch.uint8, device=dev)
+                l["ws_b"] = None
+                continue
             l["dz"] = torch.empty_like(l["z"])
             wsw = B.cf_conv3d_bwd_weight_workspace_size(l["desc"])
             wsb = B.cf_bias_lrelu_bwd_workspace_size(l["nvox"], s["cout"])
@@ -280,6 +291,29 @@ class ConvStack:
                       self.alpha, B.CF_FUSE_POOL2, l["dx"], stream)
                     g = l["dx"]
                 continue
+            if l["fused_y"]:
+                # (dy, y): the weight gradient (and db) on the side stream, the data
+                # gradient on the main stream, both forming dz from dy and y
+                ws_ = stream
+                if self.side is not None and l["dx"] is not None:
+                    main = stream if stream is not None else torch.cuda.current_stream()
+                    ev = torch.cuda.Event()
+                    ev.record(main)
+                    self.side.wait_event(ev)
+                    ws_ = self.side
+                    side_used = True
+                if d:
+                    pend += c(f"L{i+1}.conv_bwd_weight_fused", B.cf_conv3d_bwd_weight_fused_deferred, l["desc"],
+                              self.layer_input(i), g, l["z"], self.alpha, 0, l["dw"], l["db"], None, l["ws_w"],
+                              None, ws_, rec=ws_)
+                else:
+                    c(f"L{i+1}.conv_bwd_weight_fused", B.cf_conv3d_bwd_weight_fused, l["desc"], self.layer_input(i),
+                      g, l["z"], self.alpha, 0, l["dw"], l["db"], l["ws_w"], None, ws_, rec=ws_)
+                if l["dx"] is not None:
+                    c(f"L{i+1}.conv_bwd_data_fused", B.cf_conv3d_bwd_data_fused, l["desc"], g, l["z"], l["w"],
+                      self.alpha, 0, l["dx"], stream)
+                    g = l["dx"]
+                continue
             if s["pool"]:
                 d, hh, w = l["out_dhw"]
                 c(f"L{i+1}.avgpool_bwd", B.cf_avgpool3d_bwd, self.batch, d, hh, w, s["cout"], 2, 2, self.dtype,
@@ -363,6 +397,9 @@ class ConvStack:
         pb = zb // 8
         op = name.split(".")[1]
         mb = l["nvox"] * s["cout"] // 8
+        if op in ("conv_bwd_weight_fused", "conv_bwd_data_fused") and not s["pool"]:
+            # the (dy, y) form reads dy and y in place of the pooled gradient and mask
+            pb = mb = zb
         return {"conv_fwd_fused": xb + wb + pb + mb, "conv_bwd_weight_fused": xb + pb + mb + wb // es * 4,
                 "conv_bwd_weight_fused_dz": xb + pb + mb + wb // es * 4 + zb,
                 "conv_bwd_data_fused": pb + mb + wb + xb,

@@ -100,6 +100,24 @@ def test_wgrad_noalloc_validation(L):
     expect(B.CF_ERR_INVALID_ARG, B.cf_conv3d_bwd_weight_noalloc, bad, A, A + 0x100000, A + 0x200000, 0)
 
 
+def test_fused_flags(L):
+    """Support bits of the fused entry points: the pooled form on the pooled
+    layers, the (dy, y) form on unpooled fp32 layers, none for unknown flags."""
+    deep = B.make_desc(1, (8, 8, 8), 64, 64, 3, 1, "same", "f32")
+    assert B.cf_conv3d_fused_supported(deep, 0) == (B.FUSED_FWD | B.FUSED_BWD_WEIGHT | B.FUSED_BWD_DATA |
+                                                    B.FUSED_BWD_WEIGHT_DZ)
+    assert B.cf_conv3d_fused_supported(deep, B.CF_FUSE_MASK) == B.FUSED_FWD
+    assert B.cf_conv3d_fused_supported(deep, 4) == 0
+    assert B.cf_conv3d_bwd_weight_fused_workspace_size(deep, 0) > 0
+    l2 = B.make_desc(1, (64, 64, 64), 16, 32, 4, 1, "same", "f32")
+    assert B.cf_conv3d_fused_supported(l2, B.CF_FUSE_POOL2 | B.CF_FUSE_MASK) == \
+        B.cf_conv3d_fused_supported(l2, B.CF_FUSE_POOL2)
+    expect(B.CF_ERR_INVALID_ARG, B.cf_conv3d_fwd_fused, deep, A, A + 0x100000, A + 0x200000, 0.01,
+           B.CF_FUSE_MASK, A + 0x300000, None, 0)
+    expect(B.CF_ERR_INVALID_ARG, B.cf_conv3d_fwd_fused, deep, A, A + 0x100000, A + 0x200000, 0.01, 4,
+           A + 0x300000, A + 0x400000, 0)
+
+
 def test_eltwise_validation(L):
     expect(B.CF_ERR_INVALID_ARG, B.cf_bias_lrelu_fwd, 10, 16, "f32", A, A + 0x10000, math.nan, A + 0x20000, 0)
     expect(B.CF_ERR_INVALID_ARG, B.cf_bias_lrelu_fwd, 10, 0, "f32", A, A + 0x10000, 0.01, A + 0x20000, 0)

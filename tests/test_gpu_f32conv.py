@@ -161,3 +161,49 @@ def test_f32_shift_mode(case, mode, monkeypatch):
     decided = np.abs(u) > 1e-5 * np.abs(u).max()
     assert np.array_equal(bits[decided], (u > 0)[decided])
     assert maxabs_err(to_np(dx), oracle.conv3d_bwd_data(to_np(dz), to_np(w), dhw)) <= TOL["f32"]
+
+
+# unpooled fp32 layers, backward from (dy, y): N, (D,H,W), CI, CO, k, stride
+DYY = [
+    (1, (8, 8, 8), 64, 64, 3, 1),
+    (2, (5, 6, 7), 64, 128, 2, 1),
+    (1, (9, 7, 8), 128, 128, 2, 1),
+    (2, (12, 10, 14), 32, 64, 4, 2),    # stride 2: every backward-data class
+    (1, (6, 5, 32), 16, 32, 4, 1),      # shift-mode backward-data
+]
+
+
+@pytest.mark.parametrize("case", DYY, ids=lambda c: "n%d_%dx%dx%d_c%d-%d_k%d_s%d" % (c[0], *c[1], *c[2:]))
+def test_f32_unpooled_fused_backward(case):
+    """dW, db (and the stored dz) from (dy, y) and dx from (dy, y), with
+    dz = dy * (y > 0 ? 1 : alpha): the activation y comes from the fused
+    forward of the same layer (exact zeros included where the bias cancels)."""
+    N, dhw, CI, CO, k, s = case
+    desc = B.make_desc(N, dhw, CI, CO, k, s, "same", "f32")
+    sup = B.cf_conv3d_fused_supported(desc, 0)
+    assert sup & B.FUSED_FWD and sup & B.FUSED_BWD_WEIGHT and sup & B.FUSED_BWD_DATA and sup & B.FUSED_BWD_WEIGHT_DZ
+    rng = np.random.default_rng(61)
+    od = B.cf_conv3d_out_shape(desc)
+    x = dev(rng.standard_normal((N, *dhw, CI)), "f32")
+    w = dev(rng.standard_normal((k, k, k, CI, CO)) / np.sqrt(k ** 3 * CI), "f32")
+    b = torch.as_tensor(rng.standard_normal(CO) * 0.1, dtype=torch.float32, device="cuda")
+    y = torch.full((N, *od, CO), float("nan"), device="cuda")
+    B.cf_conv3d_fwd_fused(desc, x, w, b, 0.2, 0, y, None)
+    y[..., 0] = 0.0  # exact zeros: the slope there is alpha
+    dy = dev(rng.standard_normal((N, *od, CO)), "f32")
+    ws = torch.empty(B.cf_conv3d_bwd_weight_fused_workspace_size(desc, 0), dtype=torch.uint8, device="cuda")
+    dw = torch.full((k, k, k, CI, CO), float("nan"), device="cuda")
+    db = torch.full((CO,), float("nan"), device="cuda")
+    B.cf_conv3d_bwd_weight_fused(desc, x, dy, y, 0.2, 0, dw, db, ws)
+    dw2, db2 = torch.full_like(dw, float("nan")), torch.full_like(db, float("nan"))
+    dz = torch.full((N, *od, CO), float("nan"), device="cuda")
+    B.cf_conv3d_bwd_weight_fused_dz(desc, x, dy, y, 0.2, 0, dw2, db2, dz, ws)
+    dx = torch.full((N, *dhw, CI), float("nan"), device="cuda")
+    B.cf_conv3d_bwd_data_fused(desc, dy, y, w, 0.2, 0, dx)
+    torch.cuda.synchronize()
+    assert torch.equal(dw, dw2) and torch.equal(db, db2)
+    dzr, dbr = oracle.bias_lrelu_bwd(to_np(dy), to_np(y), 0.2)
+    assert maxabs_err(to_np(dz), dzr) <= TOL["f32"]
+    assert maxabs_err(to_np(db), dbr) <= TOL["f32"]
+    assert maxabs_err(to_np(dw), oracle.conv3d_bwd_weight(to_np(x), dzr, k, stride=s)) <= TOL["f32"]
+    assert maxabs_err(to_np(dx), oracle.conv3d_bwd_data(dzr, to_np(w), dhw, stride=s)) <= TOL["f32"]

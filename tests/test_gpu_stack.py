@@ -71,6 +71,9 @@ def test_stack_64_f32_chain(fused, name):
         if l["fused"]:
             dz = fused_dz(l, g, a)
             dbr = dz.reshape(-1, s["cout"]).sum(0)
+        elif l["fused_y"]:
+            # weight and data gradients formed dz from (dy, y) themselves
+            dz, dbr = oracle.bias_lrelu_bwd(to_np(g), to_np(l["z"]), a)
         else:
             dy = oracle.avgpool3d_bwd(to_np(g), l["out_dhw"]) if s["pool"] else to_np(g)
             if s["pool"]:
@@ -184,7 +187,12 @@ def test_full_size_sampled(name, fused, rand_bias):
         s = l["spec"]
         pad = s.get("pad", "same")
         xin = to_np(st.layer_input(i))
-        dz = fused_dz(l, g, a) if l["fused"] else to_np(l["dz"])
+        if l["fused"]:
+            dz = fused_dz(l, g, a)
+        elif l["fused_y"]:
+            dz = oracle.bias_lrelu_bwd(to_np(g), to_np(l["z"]), a)[0]
+        else:
+            dz = to_np(l["dz"])
         dwg = to_np(l["dw"])
         widx = with_argmax(sample_idx(rng, l["dw"].shape, 64), dwg)
         ref = oracle.conv3d_bwd_weight_points(xin, dz, s["k"], widx, stride=s["stride"], pad=pad)
