@@ -136,7 +136,7 @@ __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__r
   constexpr bool BRICK = EPI == 2;
   constexpr int TWB = BM / 4;                // brick: w extent of a tile (2 x 2 x TWB voxels)
   static_assert(!BRICK || (BM % 64 == 0 && FWD), "pooled tiles hold whole 16-row w segments");
-  static_assert(FWD ? (FN == 2 || FN == 4) : (FN >= 1 && FN <= 4), "column groups");
+  static_assert(FN == 1 || FN == 2 || FN == 4, "column groups");
   __shared__ __attribute__((aligned(16))) float red[WK * BM * RED_LD];
 
   const int lane = threadIdx.x & 63;
@@ -271,9 +271,11 @@ __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__r
           if constexpr (BW == 4) {
             const u32x4_t q = ld128(wrsrc, off);
             b[uw][v][0] = q[0]; b[uw][v][1] = q[1]; b[uw][v][2] = q[2]; b[uw][v][3] = q[3];
-          } else {
+          } else if constexpr (BW == 2) {
             const u32x2_t q = ld64(wrsrc, off);
             b[uw][v][0] = q[0]; b[uw][v][1] = q[1];
+          } else {
+            b[uw][v][0] = __builtin_amdgcn_raw_buffer_load_b32(wrsrc, off, 0, 0);
           }
         }
       }
@@ -378,6 +380,8 @@ __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__r
         } else if constexpr (BW == 2) {
           const u32x2_t q = ld64(wrsrc, off);
           b[v][0] = q[0]; b[v][1] = q[1];
+        } else {
+          b[v][0] = __builtin_amdgcn_raw_buffer_load_b32(wrsrc, off, 0, 0);
         }
       }
     };
@@ -706,9 +710,10 @@ hipError_t launch_conv_fwd_f32(const ConvShape &s, const float *x, const float *
     C.fd = make_fastdiv(bd);
     p.pod = s.od / 2; p.poh = s.oh / 2; p.pow_ = s.ow / 2;
     const int tiles = f_assign(p, 1);
-    // taps split eight ways when the bricks alone leave compute units idle
+    // taps split eight ways and 16-channel column groups when the bricks alone
+    // leave compute units idle (the stride-2 layer at batch 1)
     if ((long long)tiles * (s.co / 32) < 2LL * kNumCUs && f_shift_env() != 1)
-      return launch_f<true, 2, 2, 4, 1, 8>(p, tiles, x, w, bias, out, mask, st);
+      return launch_f<true, 1, 2, 4, 1, 8>(p, tiles, x, w, bias, out, mask, st);
     if (f_shift_ok(s, p)) return launch_f<true, 2, 2, 4, 1, 4, 4>(p, tiles, x, w, bias, out, mask, st);
     return launch_f<true, 2, 2, 4, 1, 4>(p, tiles, x, w, bias, out, mask, st);
   }
