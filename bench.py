@@ -7,7 +7,9 @@ A step is the whole hot path over one batch of synthetic cubes: forward
 (conv, bias + leaky ReLU, 2^3 average pool per layer) and backward (pool
 backward, leaky-ReLU backward + bias grad, weight grad, data grad) through
 the C ABI.  Inputs, weights and the upstream gradient are resident in HBM
-before timing starts.  Prints ONE JSON line.
+before timing starts.  Warm-up: the W steps, then untimed steps until 0.3 s
+have passed (the GPU's clocks need tens of milliseconds of sustained work to
+settle).  Prints ONE JSON line.
 
 value = algorithmic conv FLOPs per step (fwd + wgrad + dgrad, padded taps
 included, layer-1 dgrad skipped) x steps / wall time of the timed steps, for
@@ -43,6 +45,7 @@ if ROOT not in sys.path:
 PEAK = {"bf16": 2516.6, "f32": 157.3}  # dense MFMA TFLOP/s, MI355X
 HBM_PEAK_GBS = 8000.0
 METRIC = "fwd+bwd 3D-conv TFLOP/s & samples/s, 128^3 CosmoFlow stack; % MFMA peak"
+RAMP_S = 0.3  # minimum seconds of untimed warm-up work (clock ramp), after the W warm-up steps
 
 
 def describe(name, wl):
@@ -252,8 +255,21 @@ def run_stack(name, args, steps, warmup, extras):
         if args.with_update:
             st.update(hp)
 
-    for _ in range(warmup):
-        step()
+    # warm-up: W steps, then more untimed steps until RAMP_S seconds have passed.
+    # The GPU's clocks take tens of milliseconds of sustained work to reach their
+    # steady state (measured on the 128^3 stacks: the first ~40 steps after an
+    # idle period run 3-50% slower), and a training job runs in that state.
+    t_w = time.perf_counter()
+    done, prev = 0, None
+    while done < warmup or time.perf_counter() - t_w < RAMP_S:
+        for _ in range(8):
+            step()
+        done += 8
+        ev = torch.cuda.Event()
+        ev.record()
+        if prev is not None:
+            prev.synchronize()  # bounds the queue without letting the GPU go idle
+        prev = ev
     torch.cuda.synchronize()
 
     # per-op times (events around every call) to find the dominant op

@@ -129,6 +129,27 @@ cf_status cf_conv3d_bwd_weight(const cf_conv3d_desc *desc, const void *x, const 
 cf_status cf_conv3d_bwd_weight_noalloc(const cf_conv3d_desc *desc, const void *x, const void *dz,
                                        float *dw, void *stream);
 
+/* Bytes of workspace cf_avgpool3d_lrelu_bwd needs (per-block bias partials);
+ * d, h, w = the conv-output (pool input) extent. */
+size_t cf_avgpool3d_lrelu_bwd_workspace_size(int32_t n, int32_t d, int32_t h, int32_t w, int32_t c);
+
+/* dz of a pooled layer whose forward ran fused (cf_conv3d_fwd_fused with
+ * CF_FUSE_POOL2): the adjoints of the 2^3 stride-2 pool and of the leaky ReLU
+ * (Section III-C: pooling is a per-channel convolution with constant weights
+ * 1/8; Section III-A: leaky ReLU after every convolution) in one pass,
+ *   dz[n,i,c] = dp[n,i/2,c] / 8 * (mask(n,i,c) ? 1 : alpha)  (0 where no
+ *               complete window covers i),          db[c] = sum dz[.,c],
+ * i.e. cf_avgpool3d_bwd then cf_bias_lrelu_bwd with the slope taken from the
+ * forward's mask instead of the saved activation.  d,h,w = the conv-output
+ * extent; dp [n,d/2,h/2,w/2,c] and dz [n,d,h,w,c] in dtype; mask as in
+ * cf_conv3d_mask_bytes (bit per dz element); db fp32 [c] (overwritten; may be
+ * NULL, then ws is unused), summed over the unrounded fp32 products in a fixed
+ * order.  c must be a power-of-two multiple of 16 bytes of elements (at most
+ * 64 of them) and at most 256, else CF_ERR_UNSUPPORTED; alpha finite, >= 0. */
+cf_status cf_avgpool3d_lrelu_bwd(int32_t n, int32_t d, int32_t h, int32_t w, int32_t c, int32_t dtype,
+                                 const void *dp, const void *mask, float alpha, void *dz, float *db,
+                                 void *ws, size_t ws_bytes, void *stream);
+
 /* Bias + leaky ReLU forward (Section III-A):
  *   y[v,c] = u > 0 ? u : alpha*u,  u = z[v,c] + bias[c]   (u in fp32)
  * nvox = number of voxels (n*d*h*w), c = channels; z, y in dtype; bias fp32
@@ -289,6 +310,13 @@ cf_status cf_reduce_partials(int32_t n, const cf_reduction *jobs, void *stream);
 cf_status cf_conv3d_bwd_weight_deferred(const cf_conv3d_desc *desc, const void *x, const void *dz,
                                         float *dw, void *ws, size_t ws_bytes,
                                         cf_reduction *pending, int32_t *npending, void *stream);
+
+/* cf_avgpool3d_lrelu_bwd without the final bias-gradient sum (db by
+ * cf_reduce_partials).  pending / npending as above. */
+cf_status cf_avgpool3d_lrelu_bwd_deferred(int32_t n, int32_t d, int32_t h, int32_t w, int32_t c, int32_t dtype,
+                                          const void *dp, const void *mask, float alpha, void *dz, float *db,
+                                          void *ws, size_t ws_bytes, cf_reduction *pending,
+                                          int32_t *npending, void *stream);
 
 /* cf_bias_lrelu_bwd without the final bias-gradient sum (dz is written by
  * this call; db by cf_reduce_partials).  pending / npending as above. */

@@ -38,7 +38,8 @@ EXPORTS = [
     "cf_conv3d_bwd_data_fused", "cf_reduce_partials", "cf_conv3d_bwd_weight_deferred", "cf_bias_lrelu_bwd_deferred",
     "cf_conv3d_bwd_weight_fused_deferred", "cf_adam_larc_workspace_size", "cf_adam_larc_step",
     "cf_fc_fwd_workspace_size", "cf_fc_fwd", "cf_fc_bwd_data", "cf_fc_bwd_weight", "cf_mse_loss",
-    "cf_conv3d_bwd_weight_noalloc",
+    "cf_conv3d_bwd_weight_noalloc", "cf_avgpool3d_lrelu_bwd_workspace_size", "cf_avgpool3d_lrelu_bwd",
+    "cf_avgpool3d_lrelu_bwd_deferred",
 ]
 
 
@@ -108,6 +109,10 @@ def lib():
         "cf_bias_lrelu_bwd": ([i64, i32, i32, vp, vp, f32, vp, vp, vp, sz, vp], ctypes.c_int),
         "cf_avgpool3d_fwd": ([i32] * 8 + [vp, vp, vp], ctypes.c_int),
         "cf_avgpool3d_bwd": ([i32] * 8 + [vp, vp, vp], ctypes.c_int),
+        "cf_avgpool3d_lrelu_bwd_workspace_size": ([i32] * 5, sz),
+        "cf_avgpool3d_lrelu_bwd": ([i32] * 6 + [vp, vp, f32, vp, vp, vp, sz, vp], ctypes.c_int),
+        "cf_avgpool3d_lrelu_bwd_deferred": ([i32] * 6 + [vp, vp, f32, vp, vp, vp, sz, ctypes.POINTER(cf_reduction),
+                                                         ctypes.POINTER(i32), vp], ctypes.c_int),
         "cf_conv3d_fused_supported": ([D, ctypes.c_uint32], i32),
         "cf_conv3d_mask_bytes": ([D], sz),
         "cf_conv3d_fwd_fused": ([D, vp, vp, vp, f32, ctypes.c_uint32, vp, vp, vp], ctypes.c_int),
@@ -243,6 +248,17 @@ def cf_avgpool3d_bwd(n, d, h, w, c, k, s, dtype, dp, dy, stream=None):
     _check(lib().cf_avgpool3d_bwd(n, d, h, w, c, k, s, dtype_code(dtype), _ptr(dp), _ptr(dy), _stream(stream)))
 
 
+def cf_avgpool3d_lrelu_bwd_workspace_size(n, d, h, w, c) -> int:
+    return int(lib().cf_avgpool3d_lrelu_bwd_workspace_size(n, d, h, w, c))
+
+
+def cf_avgpool3d_lrelu_bwd(n, d, h, w, c, dtype, dp, mask, alpha, dz, db, ws, ws_bytes=None, stream=None):
+    if ws_bytes is None:
+        ws_bytes = 0 if ws is None or isinstance(ws, int) else ws.numel() * ws.element_size()
+    _check(lib().cf_avgpool3d_lrelu_bwd(n, d, h, w, c, dtype_code(dtype), _ptr(dp), _ptr(mask), alpha, _ptr(dz),
+                                        _ptr(db), _ptr(ws), ws_bytes, _stream(stream)))
+
+
 def cf_conv3d_fused_supported(desc, flags=CF_FUSE_POOL2) -> int:
     return int(lib().cf_conv3d_fused_supported(ctypes.byref(desc), flags))
 
@@ -310,6 +326,17 @@ def cf_bias_lrelu_bwd_deferred(nvox, c, dtype, dy, y, alpha, dz, db, ws, ws_byte
     _check(lib().cf_bias_lrelu_bwd_deferred(nvox, c, dtype_code(dtype), _ptr(dy), _ptr(y), alpha, _ptr(dz), _ptr(db),
                                             _ptr(ws), ws_bytes, arr, ctypes.byref(n), _stream(stream)))
     return _pending_list(arr, n)
+
+
+def cf_avgpool3d_lrelu_bwd_deferred(n, d, h, w, c, dtype, dp, mask, alpha, dz, db, ws, ws_bytes=None,
+                                    stream=None):
+    if ws_bytes is None:
+        ws_bytes = 0 if ws is None or isinstance(ws, int) else ws.numel() * ws.element_size()
+    arr, n_ = (cf_reduction * CF_MAX_PENDING)(), ctypes.c_int32(0)
+    _check(lib().cf_avgpool3d_lrelu_bwd_deferred(n, d, h, w, c, dtype_code(dtype), _ptr(dp), _ptr(mask), alpha,
+                                                 _ptr(dz), _ptr(db), _ptr(ws), ws_bytes, arr, ctypes.byref(n_),
+                                                 _stream(stream)))
+    return _pending_list(arr, n_)
 
 
 def cf_conv3d_bwd_weight_fused_deferred(desc, x, g, mask, alpha, flags, dw, db, dz, ws, ws_bytes=None,

@@ -325,6 +325,52 @@ cf_status cf_bias_lrelu_bwd(int64_t nvox, int32_t c, int32_t dtype, const void *
                 "cf_bias_lrelu_bwd");
 }
 
+size_t cf_avgpool3d_lrelu_bwd_workspace_size(int32_t n, int32_t d, int32_t h, int32_t w, int32_t c) {
+  if (n <= 0 || d <= 0 || h <= 0 || w <= 0 || c <= 0) return 0;
+  return cf::pool_lrelu_bwd_workspace((int64_t)n * d * h * w, c);
+}
+
+cf_status cf_avgpool3d_lrelu_bwd(int32_t n, int32_t d, int32_t h, int32_t w, int32_t c, int32_t dtype,
+                                 const void *dp, const void *mask, float alpha, void *dz, float *db, void *ws,
+                                 size_t ws_bytes, void *stream) {
+  if (n < 0) return fail(CF_ERR_INVALID_ARG, "batch n must be >= 0");
+  if (d <= 0 || h <= 0 || w <= 0 || c <= 0) return fail(CF_ERR_INVALID_ARG, "extents and channels must be > 0");
+  if (dtype != CF_F32 && dtype != CF_BF16) return fail(CF_ERR_INVALID_ARG, "unknown dtype");
+  if (!std::isfinite(alpha) || alpha < 0.f) return fail(CF_ERR_INVALID_ARG, "alpha must be finite and >= 0");
+  const int dt = dtype == CF_BF16 ? cf::DT_BF16 : cf::DT_F32;
+  const int64_t nvox = (int64_t)n * d * h * w;
+  if (!cf::pool_lrelu_bwd_supported(nvox, c, dt))
+    return fail(CF_ERR_UNSUPPORTED, "avgpool3d_lrelu_bwd: channels must be a power-of-two multiple (at most 64) of "
+                                    "the 16-byte vector, at most 256, and the tensor below 2^31 elements");
+  hipStream_t st = (hipStream_t)stream;
+  if (nvox == 0) {
+    if (!db) return ok();
+    if (!aligned16(db)) return fail(CF_ERR_ALIGNMENT, "db not 16-byte aligned");
+    return finish(cf::launch_pool_lrelu_bwd(0, d, h, w, c, dt, nullptr, nullptr, alpha, nullptr, db, nullptr, st), st,
+                  "cf_avgpool3d_lrelu_bwd");
+  }
+  cf_status r;
+  if ((r = check_ptrs({dp, mask, dz})) != CF_OK) return r;
+  const size_t es = elem_size(dtype);
+  const size_t bz = (size_t)nvox * c * es, bp = (size_t)n * (d / 2) * (h / 2) * (w / 2) * c * es;
+  const size_t bm = ((size_t)nvox * c + 31) / 32 * 4;
+  if (overlap(dz, bz, dp, bp) || overlap(dz, bz, mask, bm))
+    return fail(CF_ERR_ALIAS, "avgpool3d_lrelu_bwd: dz overlaps an input");
+  if (db) {
+    if (!aligned16(db)) return fail(CF_ERR_ALIGNMENT, "db not 16-byte aligned");
+    const size_t need = cf::pool_lrelu_bwd_workspace(nvox, c);
+    if (!ws || ws_bytes < need)
+      return fail(CF_ERR_WORKSPACE, "avgpool3d_lrelu_bwd: workspace smaller than the size query");
+    if (!aligned16(ws)) return fail(CF_ERR_ALIGNMENT, "workspace not 16-byte aligned");
+    if (overlap(db, (size_t)c * 4, dz, bz) || overlap(ws, need, dz, bz) || overlap(ws, need, dp, bp) ||
+        overlap(ws, need, mask, bm) || overlap(ws, need, db, (size_t)c * 4) || overlap(db, (size_t)c * 4, dp, bp) ||
+        overlap(db, (size_t)c * 4, mask, bm))
+      return fail(CF_ERR_ALIAS, "avgpool3d_lrelu_bwd: db or workspace overlaps a tensor");
+  }
+  return finish(cf::launch_pool_lrelu_bwd(n, d, h, w, c, dt, dp, mask, alpha, dz, db, ws, st), st,
+                "cf_avgpool3d_lrelu_bwd");
+}
+
 static cf_status pool_check(int32_t n, int32_t d, int32_t h, int32_t w, int32_t c, int32_t k,
                             int32_t s, int32_t dtype) {
   if (n < 0) return fail(CF_ERR_INVALID_ARG, "batch n must be >= 0");
@@ -390,6 +436,11 @@ static int32_t fused_mask(const cf::ConvShape &s, uint32_t flags) {
   if (flags == CF_FUSE_POOL2 && cf::c16_bwd_supported(s)) m |= 4;
   if (flags == CF_FUSE_POOL2 && cf::c16_wgrad_supported(s) && !cf::smallc_wgrad_fused_supported(s)) m |= 8;
   if (flags == CF_FUSE_POOL2 && cf::f32wgrad_fused_supported(s) && !cf::smallc_wgrad_fused_supported(s)) m |= 2 | 8;
+  // bf16 deep layers: pooled forward, and both backward kernels forming dz from
+  // (pooled gradient, mask) or (dy, y) as they load it (no dz output)
+  if (flags == CF_FUSE_POOL2 && cf::direct_pool_supported(s)) m |= 1;
+  if ((flags == CF_FUSE_POOL2 || ymode) && s.dtype == cf::DT_BF16 && cf::direct_wgrad_supported(s)) m |= 2;
+  if ((flags == CF_FUSE_POOL2 || ymode) && cf::direct_supported(s, false)) m |= 4;
   return m;
 }
 
@@ -409,9 +460,12 @@ static size_t mask_bytes(const cf::ConvShape &s) {
 }
 
 static size_t fused_wgrad_workspace(const cf::ConvShape &s, uint32_t flags) {
-  if (!(flags & CF_FUSE_POOL2)) return cf::f32wgrad_workspace(s, 3);  // (dy, y)
+  const bool deep16 = s.dtype == cf::DT_BF16 && cf::direct_wgrad_supported(s);
+  if (!(flags & CF_FUSE_POOL2))  // (dy, y)
+    return deep16 ? cf::direct_wgrad_workspace(s, true) : cf::f32wgrad_workspace(s, 3);
   if (cf::smallc_wgrad_fused_supported(s)) return cf::smallc_wgrad_fused_workspace(s);
   if (cf::f32wgrad_fused_supported(s)) return cf::f32wgrad_workspace(s, 1);
+  if (deep16) return cf::direct_wgrad_workspace(s, true);
   return cf::c16_wgrad_workspace(s);
 }
 
@@ -463,6 +517,8 @@ cf_status cf_conv3d_fwd_fused(const cf_conv3d_desc *desc, const void *x, const v
                                 pool ? 2 : 1, st);
   else if (!pool && !cf::c16_fwd_supported(s))
     e = cf::launch_conv_fwd_direct(s, x, w, bias, alpha, out, mask, true, st);
+  else if (pool && cf::direct_pool_supported(s))
+    e = cf::launch_conv_fwd_direct_pool(s, x, w, bias, alpha, out, mask, st);
   else
     e = cf::launch_conv_fwd_c16(s, x, w, bias, alpha, out, (uint32_t *)mask, pool ? 2 : 1, st);
   return finish(e, st, "cf_conv3d_fwd_fused");
@@ -516,7 +572,10 @@ static cf_status bwd_weight_fused(const char *name, const cf_conv3d_desc *desc, 
   if (dz && (overlap(dz, b.z, dw, dw_bytes) || overlap(dz, b.z, db, dbb) || overlap(dz, b.z, ws, need)))
     return fail(CF_ERR_ALIAS, std::string(name) + ": dz overlaps another output or the workspace");
   hipError_t e;
-  if (!pool)
+  const bool deep16 = s.dtype == cf::DT_BF16 && cf::direct_wgrad_supported(s);
+  if (!pool && deep16)
+    e = cf::launch_conv_bwd_weight_direct(s, x, g, mask, cf::DWG_DYY, alpha, dw, db, ws, st);
+  else if (!pool)
     e = cf::launch_conv_bwd_weight_f32(s, (const float *)x, (const float *)g, mask, alpha, dw, db, ws, 3, (float *)dz,
                                        st);
   else if (cf::smallc_wgrad_fused_supported(s))
@@ -524,6 +583,8 @@ static cf_status bwd_weight_fused(const char *name, const cf_conv3d_desc *desc, 
   else if (cf::f32wgrad_fused_supported(s))
     e = cf::launch_conv_bwd_weight_f32(s, (const float *)x, (const float *)g, mask, alpha, dw, db, ws, 1, (float *)dz,
                                        st);
+  else if (deep16)
+    e = cf::launch_conv_bwd_weight_direct(s, x, g, mask, cf::DWG_POOL, alpha, dw, db, ws, st);
   else
     e = cf::launch_conv_bwd_weight_c16(s, x, g, (const uint32_t *)mask, alpha, dw, db, ws, true, dz, st);
   return finish(e, st, name);
@@ -561,10 +622,14 @@ cf_status cf_conv3d_bwd_data_fused(const cf_conv3d_desc *desc, const void *g, co
   if (overlap(dx, b.x, g, gb) || overlap(dx, b.x, mask, mb) || overlap(dx, b.x, w, b.w))
     return fail(CF_ERR_ALIAS, "conv3d_bwd_data_fused: dx overlaps an input");
   hipStream_t st = (hipStream_t)stream;
-  const hipError_t e =
-      pool ? cf::launch_conv_bwd_data_c16(s, g, (const uint32_t *)mask, w, alpha, dx, true, st)
-           : cf::launch_conv_bwd_data_f32(s, (const float *)g, (const float *)w, (float *)dx, st, (const float *)mask,
-                                          alpha);
+  hipError_t e;
+  if (pool && cf::c16_bwd_supported(s))
+    e = cf::launch_conv_bwd_data_c16(s, g, (const uint32_t *)mask, w, alpha, dx, true, st);
+  else if (cf::direct_supported(s, false))  // bf16 deep layers
+    e = cf::launch_conv_bwd_data_direct_fused(s, g, mask, pool ? cf::DWG_POOL : cf::DWG_DYY, alpha, w, dx, st);
+  else
+    e = cf::launch_conv_bwd_data_f32(s, (const float *)g, (const float *)w, (float *)dx, st, (const float *)mask,
+                                     alpha);
   return finish(e, st, "cf_conv3d_bwd_data_fused");
 }
 
@@ -605,6 +670,15 @@ cf_status cf_bias_lrelu_bwd_deferred(int64_t nvox, int32_t c, int32_t dtype, con
                                      cf_reduction *pending, int32_t *npending, void *stream) {
   return deferred(pending, npending, [&] {
     return cf_bias_lrelu_bwd(nvox, c, dtype, dy, y, alpha, dz, db, ws, ws_bytes, stream);
+  });
+}
+
+cf_status cf_avgpool3d_lrelu_bwd_deferred(int32_t n, int32_t d, int32_t h, int32_t w, int32_t c, int32_t dtype,
+                                          const void *dp, const void *mask, float alpha, void *dz, float *db,
+                                          void *ws, size_t ws_bytes, cf_reduction *pending, int32_t *npending,
+                                          void *stream) {
+  return deferred(pending, npending, [&] {
+    return cf_avgpool3d_lrelu_bwd(n, d, h, w, c, dtype, dp, mask, alpha, dz, db, ws, ws_bytes, stream);
   });
 }
 

@@ -68,6 +68,72 @@ template <bool NT> __device__ __forceinline__ void st16(void *p, uint4 v) {
   }
 }
 
+// Gradient operand of a fused backward kernel: dz rebuilt from what the layer
+// kept instead of a stored dz.  GRAD_POOL: from the pooled-output gradient g
+// and the forward's slope mask, dz = g / 8 * (bit ? 1 : alpha); GRAD_DYY: from
+// the activation gradient dy and the activation y, dz = dy * (y > 0 ? 1 : alpha).
+enum : int { GRAD_DZ = 0, GRAD_POOL = 1, GRAD_DYY = 3 };
+
+// dz of eight bf16 channels in fp32: GRAD_POOL gv = g, bits 0..7 of av[0] = the
+// mask bits of the eight channels; GRAD_DYY gv = dy, av = y
+template <int GM>
+__device__ __forceinline__ void form_dz8(const u32x4_t &gv, const u32x4_t &av, float alpha, float (&f)[8]) {
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const float lo = __uint_as_float(gv[q] << 16), hi = __uint_as_float(gv[q] & 0xffff0000u);
+    if constexpr (GM == GRAD_POOL) {
+      const uint32_t bits = av[0] >> (2 * q);
+      f[2 * q] = lo * ((bits & 1u) ? 0.125f : 0.125f * alpha);
+      f[2 * q + 1] = hi * ((bits & 2u) ? 0.125f : 0.125f * alpha);
+    } else {
+      // y > 0 for a bf16 value: its 32-bit widening compared as a signed integer
+      const bool plo = (int)(av[q] << 16) > 0, phi = (int)(av[q] & 0xffff0000u) > 0;
+      f[2 * q] = lo * (plo ? 1.f : alpha);
+      f[2 * q + 1] = hi * (phi ? 1.f : alpha);
+    }
+  }
+}
+
+// Split form of the same dz for kernels that multiply it into a matrix product:
+// dz = s1 * src + s2 * (src & sel) with sel = 0xffff on the bf16 halves where
+// the slope is 1 (GRAD_POOL: s1 = alpha / 8, s2 = (1 - alpha) / 8, sel = the mask
+// bits; GRAD_DYY: s1 = alpha, s2 = 1 - alpha, sel = y > 0).  src and src & sel are
+// exact bf16 values, so two products of them, scaled and added in fp32, give
+// dz times the other operand without rounding dz itself.
+// sel of eight channels from their eight mask bits (word q: bits 2q, 2q + 1)
+__device__ __forceinline__ u32x4_t sel_of_bits8(uint32_t bits) {
+  u32x4_t m;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const uint32_t lo = (uint32_t)((int)(bits << (31 - 2 * q)) >> 31);  // 0 or all ones
+    const uint32_t hi = (uint32_t)((int)(bits << (30 - 2 * q)) >> 31);
+    m[q] = (lo & 0xffffu) | (hi & 0xffff0000u);
+  }
+  return m;
+}
+
+// sel of eight channels from their bf16 activations: 0xffff where y > 0 (as a
+// signed 16-bit integer a bf16 value is positive exactly when it is > 0)
+__device__ __forceinline__ u32x4_t sel_of_pos8(const u32x4_t &y) {
+  typedef short s16x2_t __attribute__((ext_vector_type(2)));
+  typedef unsigned short u16x2_t __attribute__((ext_vector_type(2)));
+  u32x4_t m;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const uint32_t yq = y[q];  // (a bit cast of the element expression itself would read element 0)
+    const s16x2_t v = __builtin_bit_cast(s16x2_t, yq);
+    const u16x2_t pos = __builtin_bit_cast(u16x2_t, __builtin_elementwise_max(v, (s16x2_t){0, 0}));
+    const u16x2_t one = __builtin_elementwise_min(pos, (u16x2_t){1, 1});  // 1 where y > 0
+    m[q] = __builtin_bit_cast(uint32_t, (u16x2_t){0, 0} - one);
+  }
+  return m;
+}
+
+// eight fp32 values rounded (to nearest even) into eight packed bf16
+__device__ __forceinline__ u32x4_t pack_bf16x8(const float (&f)[8]) {
+  return u32x4_t{f2bf2(f[0], f[1]), f2bf2(f[2], f[3]), f2bf2(f[4], f[5]), f2bf2(f[6], f[7])};
+}
+
 // tensors of at least this many bytes take the non-temporal forms in the
 // streaming elementwise and pooling passes (the last-level cache is 256 MiB)
 constexpr long long kStreamBytes = 1LL << 28;

@@ -82,14 +82,25 @@ hipError_t launch_smallc_wgrad_fused(const ConvShape &s, const void *x, const vo
 bool direct_supported(const ConvShape &s, bool fwd);
 hipError_t launch_conv_fwd_direct(const ConvShape &s, const void *x, const void *w, const float *bias, float alpha,
                                   void *out, void *mask, bool act, hipStream_t st);
+// pooled forward of a deep layer (bias + lReLU + slope mask + 2^3 pool; out = pooled output)
+bool direct_pool_supported(const ConvShape &s);
+hipError_t launch_conv_fwd_direct_pool(const ConvShape &s, const void *x, const void *w, const float *bias,
+                                       float alpha, void *out, void *mask, hipStream_t st);
 hipError_t launch_conv_bwd_data_direct(const ConvShape &s, const void *dz, const void *w, void *dx,
                                        hipStream_t st);
+// backward-data of a fused deep layer (register kernel): gm = GRAD_POOL, g = pooled-output
+// gradient, aux = slope mask; gm = GRAD_DYY, g = dy, aux = y; dz formed from them per load
+hipError_t launch_conv_bwd_data_direct_fused(const ConvShape &s, const void *g, const void *aux, int gm, float alpha,
+                                             const void *w, void *dx, hipStream_t st);
 // their weight gradient (bf16, ci % 8 == 0, co % 64 == 0), conv_direct_wgrad.hip: K-split
-// partials in ws, summed into dw by launch_sum_rows
+// partials in ws, summed into dw (and db, fused) by launch_sum_rows.  gm selects the
+// gradient operand: DWG_DZ g = dz; DWG_POOL g = pooled-output gradient, aux = slope
+// mask (bit per conv-output element); DWG_DYY g = dy, aux = the activation y
+enum : int { DWG_DZ = 0, DWG_POOL = 1, DWG_DYY = 3 };
 bool direct_wgrad_supported(const ConvShape &s);
-size_t direct_wgrad_workspace(const ConvShape &s);
-hipError_t launch_conv_bwd_weight_direct(const ConvShape &s, const void *x, const void *dz, float *dw, void *ws,
-                                         hipStream_t st);
+size_t direct_wgrad_workspace(const ConvShape &s, bool fused);
+hipError_t launch_conv_bwd_weight_direct(const ConvShape &s, const void *x, const void *g, const void *aux, int gm,
+                                         float alpha, float *dw, float *db, void *ws, hipStream_t st);
 
 // fp32 implicit GEMM on v_mfma_f32_16x16x4_f32 (conv_f32.hip): forward for
 // ci % 16 == 0 and co % 32 == 0, backward-data for co % 16 == 0 and ci % 16 == 0.
@@ -137,6 +148,13 @@ hipError_t launch_bias_lrelu_bwd(int64_t nvox, int c, int dtype, const void *dy,
                                  float alpha, void *dz, float *db, void *ws, hipStream_t st);
 
 // out[c] = sum_{r < rows} part[r * cols + c], in an order fixed by (rows, cols).
+// dz of a pooled layer from the pooled-output gradient and the slope mask (the
+// adjoints of the 2^3 pool and of the leaky ReLU in one pass), db partials summed
+// by launch_sum_rows (eltwise.hip); d, h, w = the conv-output extent
+bool pool_lrelu_bwd_supported(long long nvox, int c, int dtype);
+size_t pool_lrelu_bwd_workspace(int64_t nvox, int c);
+hipError_t launch_pool_lrelu_bwd(int n, int d, int h, int w, int c, int dtype, const void *g, const void *mask,
+                                 float alpha, void *dz, float *db, void *ws, hipStream_t st);
 hipError_t launch_sum_rows(const float *part, float *out, int rows, int cols, hipStream_t st);
 // one pending column sum out[c] = sum_r part[r][c] of a [rows][cols] fp32 matrix
 struct SumJob {

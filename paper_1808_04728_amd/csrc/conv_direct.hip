@@ -87,6 +87,8 @@ struct DirParams {
   int src_bytes, w_bytes;       // extents of the range-checked buffers
   int ncls;
   float alpha;
+  int aux_bytes;                // fused backward-data: extent of the slope mask or of y
+  int pod, poh, pow_;           // fused backward-data from a pooled gradient: pooled extents
   DirClass cls[DIR_MAX_CLS];
   DirTap tap[DIR_MAX_TAPS];
 };
@@ -104,15 +106,23 @@ __device__ __forceinline__ u32x4_t buf_load(__amdgpu_buffer_rsrc_t r, uint32_t b
   return __builtin_amdgcn_raw_buffer_load_b128(r, byte_off, 0, 0);
 }
 
-template <bool FWD, int FM, int FN, int WM, int WK, int PF, bool ACT>
+// GM (backward-data only): the gathered operand is dz itself (GRAD_DZ), or dz
+// made of the pooled-output gradient (src) and the slope mask (aux), GRAD_POOL,
+// or of dy (src) and the activation y (aux), GRAD_DYY -- the backward-data of a
+// fused layer, dz never stored.  The fused forms run the split form of dz: the
+// loaded gradient and its masked copy feed two accumulator sets, scaled and
+// added once in the epilogue (a mask AND per element instead of a multiply and
+// a rounding).
+template <bool FWD, int FM, int FN, int WM, int WK, int PF, bool ACT, int GM = GRAD_DZ>
 __global__ __launch_bounds__(256) void conv_direct_kernel(const uint16_t *__restrict__ src,
                                                           const uint16_t *__restrict__ wt,
                                                           const float *__restrict__ bias,
                                                           uint16_t *__restrict__ dst, uint8_t *__restrict__ mask,
-                                                          const DirParams p) {
+                                                          const void *__restrict__ aux, const DirParams p) {
   constexpr int BM = 16 * FM * WM, BN = 16 * FN;
   static_assert(WM * WK == 4, "four waves");
   static_assert(!FWD || FN == 4, "forward weight slices are 64 output channels wide");
+  static_assert(!FWD || GM == GRAD_DZ, "the fused gathers are backward-data forms");
   constexpr int WSLICE = 32 * 64 * 2;                     // bytes of one staged weight slice
   constexpr int STAGE_BYTES = FWD ? 4 * 2 * WSLICE : 0;   // per wave, double buffered
   constexpr int RED_LD = BN + 4;                          // fp32 row pitch of the reduction tile
@@ -140,9 +150,12 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const uint16_t *__rest
 
   const __amdgpu_buffer_rsrc_t srsrc = __builtin_amdgcn_make_buffer_rsrc((void *)src, (short)0, p.src_bytes, 0x00020000);
   const __amdgpu_buffer_rsrc_t wrsrc = __builtin_amdgcn_make_buffer_rsrc((void *)wt, (short)0, p.w_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t arsrc =
+      __builtin_amdgcn_make_buffer_rsrc((void *)aux, (short)0, GM != GRAD_DZ ? p.aux_bytes : 0, 0x00020000);
+  (void)arsrc;
 
   // ---- rows of this lane's A fragments ---------------------------------------
-  int rbd[FM], rbh[FM], rbw[FM], roff[FM];
+  int rbd[FM], rbh[FM], rbw[FM], roff[FM], rpn[FM];
   bool rok[FM];
 #pragma unroll
   for (int i = 0; i < FM; ++i) {
@@ -154,7 +167,9 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const uint16_t *__rest
     rbh[i] = (t1 - t2 * (int)C.fh.div) * p.bstr_h + C.bq_h;
     rbd[i] = (t2 - n * (int)C.fd.div) * p.bstr_d + C.bq_d;
     roff[i] = (((n * p.sd_ + rbd[i]) * p.sh_ + rbh[i]) * p.sw_ + rbw[i]) * p.sc + 8 * g4;
+    rpn[i] = n * p.pod;
   }
+  (void)rpn;
 
   // ---- this wave's k-steps: taps wk, wk + WK, ... of the class; 32 channels each
   const int nch = p.sc >> 5;
@@ -186,15 +201,26 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const uint16_t *__rest
   // Register ring of NS = PF + 1 slots: the loads of step s + PF are issued
   // (into the slot step s - 1 used) before the MFMAs of step s.
   constexpr int NS = PF + 1;
-  u32x4_t a_r[NS][FM], w_r[NS][NW];
-  auto load = [&](u32x4_t(&a)[FM], u32x4_t(&wv)[NW]) {
+  u32x4_t a_r[NS][FM], w_r[NS][NW], x_r[NS][FM];
+  auto load = [&](u32x4_t(&a)[FM], u32x4_t(&wv)[NW], u32x4_t(&xa)[FM]) {
     const DirTap &T = p.tap[C.tap0 + ti];
     const int cofs = cc * 32;
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
-      const bool ok = rok[i] && (unsigned)(rbd[i] + T.dd) < (unsigned)p.sd_ &&
-                      (unsigned)(rbh[i] + T.dh) < (unsigned)p.sh_ && (unsigned)(rbw[i] + T.dw) < (unsigned)p.sw_;
-      a[i] = buf_load(srsrc, ok ? (uint32_t)(roff[i] + T.a_off + cofs) * 2u : DIR_OOB);
+      const int vd = rbd[i] + T.dd, vh = rbh[i] + T.dh, vw = rbw[i] + T.dw;
+      const bool ok = rok[i] && (unsigned)vd < (unsigned)p.sd_ && (unsigned)vh < (unsigned)p.sh_ &&
+                      (unsigned)vw < (unsigned)p.sw_;
+      const uint32_t eoff = (uint32_t)(roff[i] + T.a_off + cofs);  // element offset in dz
+      if constexpr (GM == GRAD_POOL) {
+        // dz voxels outside complete pooling windows have a zero gradient
+        const bool inp = ok && vd < 2 * p.pod && vh < 2 * p.poh && vw < 2 * p.pow_;
+        const int pv = ((rpn[i] + (vd >> 1)) * p.poh + (vh >> 1)) * p.pow_ + (vw >> 1);
+        a[i] = buf_load(srsrc, inp ? (uint32_t)(pv * p.sc + 8 * g4 + cofs) * 2u : DIR_OOB);
+        xa[i][0] = __builtin_amdgcn_raw_buffer_load_b8(arsrc, ok ? eoff >> 3 : DIR_OOB, 0, 0);
+      } else {
+        a[i] = buf_load(srsrc, ok ? eoff * 2u : DIR_OOB);
+        if constexpr (GM == GRAD_DYY) xa[i] = buf_load(arsrc, ok ? eoff * 2u : DIR_OOB);
+      }
     }
     const int wbase = (T.w_off + cofs * (FWD ? p.wco : 1)) * 2;
 #pragma unroll
@@ -214,11 +240,16 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const uint16_t *__rest
     for (int v = 0; v < 4; ++v) *reinterpret_cast<u32x4_t *>(wbuf + buf * WSLICE + wst[v]) = wv[v];
   };
 
-  f32x4_t acc[FM][FN];
+  constexpr bool SPLIT = GM != GRAD_DZ;
+  f32x4_t acc[FM][FN], acc2[SPLIT ? FM : 1][FN];  // acc2: the masked copy (split form)
 #pragma unroll
   for (int i = 0; i < FM; ++i)
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int i = 0; i < (SPLIT ? FM : 1); ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc2[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
   // Branch-free steady state (a conditional load would make the compiler wait
   // for every load in flight at the merge): the step count is padded to a
@@ -228,7 +259,7 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const uint16_t *__rest
     const int niter = (nsteps + NS - 1) / NS * NS;
 #pragma unroll
     for (int q = 0; q < PF; ++q) {
-      load(a_r[q], w_r[q]);
+      load(a_r[q], w_r[q], x_r[q]);
       next();
     }
     if constexpr (FWD) stage_w(w_r[0], 0);
@@ -236,7 +267,7 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const uint16_t *__rest
 #pragma unroll
       for (int q = 0; q < NS; ++q) {
         const int s = s0 + q;
-        load(a_r[(q + PF) % NS], w_r[(q + PF) % NS]);
+        load(a_r[(q + PF) % NS], w_r[(q + PF) % NS], x_r[(q + PF) % NS]);
         next();
         bf16x8_t bf[FN];
         if constexpr (FWD) {
@@ -259,14 +290,34 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const uint16_t *__rest
         const bool real = s < nsteps;
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
-          const bf16x8_t af = __builtin_bit_cast(bf16x8_t, real ? a_r[q][i] : u32x4_t{0u, 0u, 0u, 0u});
+          const u32x4_t av = real ? a_r[q][i] : u32x4_t{0u, 0u, 0u, 0u};
+          const bf16x8_t af = __builtin_bit_cast(bf16x8_t, av);
 #pragma unroll
           for (int j = 0; j < FN; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bf[j], acc[i][j], 0, 0, 0);
+          if constexpr (SPLIT) {
+            const u32x4_t sel = GM == GRAD_POOL ? sel_of_bits8(x_r[q][i][0]) : sel_of_pos8(x_r[q][i]);
+            const bf16x8_t am = __builtin_bit_cast(bf16x8_t, av & sel);
+#pragma unroll
+            for (int j = 0; j < FN; ++j)
+              acc2[i % (SPLIT ? FM : 1)][j] =
+                  __builtin_amdgcn_mfma_f32_16x16x32_bf16(am, bf[j], acc2[i % (SPLIT ? FM : 1)][j], 0, 0, 0);
+          }
         }
         if constexpr (FWD) stage_w(w_r[(q + 1) % NS], (s + 1) & 1);
       }
     }
+  }
+
+  if constexpr (SPLIT) {  // dz x W = s1 (src x W) + s2 ((src & sel) x W)
+    const float s1 = GM == GRAD_POOL ? 0.125f * p.alpha : p.alpha;
+    const float s2 = GM == GRAD_POOL ? 0.125f * (1.f - p.alpha) : 1.f - p.alpha;
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[i][j][e] = s1 * acc[i][j][e] + s2 * acc2[i % (SPLIT ? FM : 1)][j][e];
   }
 
   // ---- partial tiles meet in LDS ---------------------------------------------
@@ -360,19 +411,33 @@ __device__ __forceinline__ void for_stages(F &&f) {
   }
 }
 
-template <bool FWD, int FM, int FN, bool ACT, int NS, int KS>
+// POOL (forward with ACT): the bias + leaky ReLU + slope mask epilogue is
+// followed by the 2^3 average pool; a tile's rows are then a brick of
+// 2 (d) x 2 (h) x 16 FM (w) output voxels (wave w holds the w line of (d, h)
+// pair w), so every pooling window lies inside one tile, and the tile writes
+// only the pooled output and the mask.
+//
+// GM = GRAD_POOL (backward-data of a pooled fused layer): the A tile is the
+// pooled-output gradient, each slot's 16 bytes DMA'd from the pooled voxel of
+// its gathered dz voxel, and every row's 32 mask bits of the k-step arrive by
+// a 4-byte DMA into a mask area of the stage; the fragments run the split form
+// of dz (the gradient and its masked copy into two accumulator sets).
+template <bool FWD, int FM, int FN, bool ACT, int NS, int KS, bool POOL = false, int GM = GRAD_DZ>
 __global__ __launch_bounds__(256) void conv_lds_kernel(const uint16_t *__restrict__ src,
                                                        const uint16_t *__restrict__ wt,
                                                        const float *__restrict__ bias,
                                                        uint16_t *__restrict__ dst, uint8_t *__restrict__ mask,
-                                                       const DirParams p) {
+                                                       const void *__restrict__ aux, const DirParams p) {
   constexpr int BM = 64 * FM, BN = 16 * FN;
   constexpr int A_SLOTS = BM * 4;                     // 16-byte slots of the A tile
   constexpr int B_SLOTS = 32 * BN / 8;                // 16-byte slots of the B tile
   constexpr int A_BYTES = A_SLOTS * 16, B_BYTES = B_SLOTS * 16;
-  constexpr int STAGE = A_BYTES + B_BYTES;            // one k-step's tiles; KS of them per stage
+  constexpr bool MSK = GM == GRAD_POOL;                // mask words staged with the A tile
+  constexpr int M_BYTES = MSK ? 1024 : 0;             // one 4-byte slot per thread
+  constexpr int STAGE = A_BYTES + B_BYTES + M_BYTES;  // one k-step's tiles; KS of them per stage
   constexpr int NA = A_SLOTS / 256;                   // A DMA instructions per wave and step
   constexpr int NB = (B_SLOTS + 255) / 256;           // B DMA instructions per wave and step
+  constexpr int NMK = MSK ? 1 : 0;                    // mask DMA instructions per wave and step
   constexpr int RED_LD = BN + 4;
   static_assert(A_SLOTS % 256 == 0, "whole DMA instructions");
   static_assert(!FWD || FN == 4, "forward weight tiles are 64 output channels wide");
@@ -380,6 +445,10 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(const uint16_t *__restric
   static_assert(NS == 4 || NS == 8, "four or eight stages");
   static_assert(KS == 1 || KS == 2, "one or two k-steps per stage");
   static_assert(NS * KS <= 8, "at most eight k-step arrays");
+  static_assert(!POOL || (FWD && ACT), "the pooled epilogue follows the forward activation");
+  static_assert(GM == GRAD_DZ || GM == GRAD_POOL, "dz or the pooled gradient and mask");
+  static_assert(!MSK || !FWD, "the pooled-gradient gather is a backward-data form");
+  constexpr int TWB = 16 * FM;  // brick: w extent of a tile
   // k-step u of stage S lives in array S + NS u: every array is written by
   // one DMA pattern, so the compiler matches each fragment read to its DMA
   __shared__ __attribute__((aligned(16))) unsigned char stg0[STAGE], stg1[STAGE], stg2[STAGE], stg3[STAGE];
@@ -398,12 +467,47 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(const uint16_t *__restric
   int c = 0;
   while (c + 1 < p.ncls && slot >= p.cls[c + 1].slot0) ++c;
   const DirClass &C = p.cls[c];
-  const int m0 = (xcd * C.per + slot - C.slot0) * BM;
-  if (m0 >= C.m) return;
+  const int tile = xcd * C.per + slot - C.slot0;
+  int tb_n = 0, tb_d = 0, tb_h = 0, tb_w = 0;  // brick: sample, d pair, h pair, w segment
+  if constexpr (POOL) {
+    if (tile >= C.m) return;  // C.m counts bricks
+    const int t1 = fdiv(tile, C.fw), t2 = fdiv(t1, C.fh);
+    tb_n = fdiv(t2, C.fd);
+    tb_w = tile - t1 * (int)C.fw.div;
+    tb_h = t1 - t2 * (int)C.fh.div;
+    tb_d = t2 - tb_n * (int)C.fd.div;
+  } else {
+    if (tile * BM >= C.m) return;
+  }
+  const int m0 = tile * BM;
   const int n0 = blockIdx.y * BN;
 
   const __amdgpu_buffer_rsrc_t srsrc = __builtin_amdgcn_make_buffer_rsrc((void *)src, (short)0, p.src_bytes, 0x00020000);
   const __amdgpu_buffer_rsrc_t wrsrc = __builtin_amdgcn_make_buffer_rsrc((void *)wt, (short)0, p.w_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t mrsrc =
+      __builtin_amdgcn_make_buffer_rsrc((void *)aux, (short)0, MSK ? p.aux_bytes : 0, 0x00020000);
+  (void)mrsrc;
+
+  // output voxel of tile row lrow (false: past the extents or the class)
+  auto row_voxel = [&](int lrow, int &n, int &jd, int &jh, int &jw) -> bool {
+    if constexpr (POOL) {
+      const int dh2 = lrow / TWB;
+      n = tb_n;
+      jd = 2 * tb_d + (dh2 >> 1);
+      jh = 2 * tb_h + (dh2 & 1);
+      jw = tb_w * TWB + lrow % TWB;
+      return jd < p.dd && jh < p.dh && jw < p.dw;
+    } else {
+      const int grow = m0 + lrow;
+      const int rr = grow < C.m ? grow : 0;
+      const int t1 = fdiv(rr, C.fw), t2 = fdiv(t1, C.fh);
+      n = fdiv(t2, C.fd);
+      jw = rr - t1 * (int)C.fw.div;
+      jh = t1 - t2 * (int)C.fh.div;
+      jd = t2 - n * (int)C.fd.div;
+      return grow < C.m;
+    }
+  };
 
   // ---- the class's taps, one per lane -----------------------------------------
   const int ntap = C.ntap;
@@ -412,21 +516,40 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(const uint16_t *__restric
     const DirTap &T = p.tap[C.tap0 + lane];
     v_aoff = T.a_off; v_woff = T.w_off; v_dd = T.dd; v_dh = T.dh; v_dw = T.dw;
   }
+  const int v_voff = (v_dd * p.sh_ + v_dh) * p.sw_ + v_dw;  // the tap's voxel offset
+  (void)v_voff;
 
   // ---- this lane's A slots: row, swizzled channel chunk, source base --------
-  int rbd[NA], rbh[NA], rbw[NA], roff[NA];
+  int rbd[NA], rbh[NA], rbw[NA], roff[NA], rpn[NA], rch[NA];
 #pragma unroll
   for (int k = 0; k < NA; ++k) {
     const int sl = 256 * k + tid, row = sl >> 2, lch = (sl & 3) ^ ((row >> 2) & 3);
-    const int grow = m0 + row;
-    const int rr = grow < C.m ? grow : 0;
-    const int t1 = fdiv(rr, C.fw), t2 = fdiv(t1, C.fh), n = fdiv(t2, C.fd);
-    rbw[k] = (rr - t1 * (int)C.fw.div) * p.bstr_w + C.bq_w;
-    rbh[k] = (t1 - t2 * (int)C.fh.div) * p.bstr_h + C.bq_h;
-    rbd[k] = (t2 - n * (int)C.fd.div) * p.bstr_d + C.bq_d;
+    int n, jd, jh, jw;
+    const bool valid = row_voxel(row, n, jd, jh, jw);
+    if (!valid) n = jd = jh = jw = 0;
+    rbw[k] = jw * p.bstr_w + C.bq_w;
+    rbh[k] = jh * p.bstr_h + C.bq_h;
+    rbd[k] = jd * p.bstr_d + C.bq_d;
     roff[k] = (((n * p.sd_ + rbd[k]) * p.sh_ + rbh[k]) * p.sw_ + rbw[k]) * p.sc + 8 * lch;
-    if (grow >= C.m) rbd[k] = -(1 << 20);  // rows past the class fail every bounds check
+    rpn[k] = n * p.pod;  // pooled gather: the sample's first pooled plane, the slot's channels
+    rch[k] = 8 * lch;
+    if (!valid) rbd[k] = -(1 << 20);  // rows past the class fail every bounds check
   }
+  (void)rpn;
+  (void)rch;
+  // mask rows: thread tid stages the mask word of tile row tid (threads past
+  // the tile's rows load nothing: their row fails the bounds check)
+  int mbd = -(1 << 20), mbh = 0, mbw = 0, mvox = 0;
+  if (MSK && tid < BM) {
+    int n, jd, jh, jw;
+    if (row_voxel(tid, n, jd, jh, jw)) {
+      mbw = jw * p.bstr_w + C.bq_w;
+      mbh = jh * p.bstr_h + C.bq_h;
+      mbd = jd * p.bstr_d + C.bq_d;
+      mvox = ((n * p.sd_ + mbd) * p.sh_ + mbh) * p.sw_ + mbw;
+    }
+  }
+  (void)mbd; (void)mbh; (void)mbw; (void)mvox;
   // this lane's B slot(s): element offset inside a step's weight tile
   int boff[NB];
 #pragma unroll
@@ -473,10 +596,30 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(const uint16_t *__restric
     const int wbase = __builtin_amdgcn_readlane(v_woff, iti) + 32 * icc * (FWD ? p.wco : 1);
 #pragma unroll
     for (int k = 0; k < NA; ++k) {
-      const bool ok = ((unsigned)(rbd[k] + dd) < (unsigned)p.sd_) & ((unsigned)(rbh[k] + dh) < (unsigned)p.sh_) &
-                      ((unsigned)(rbw[k] + dw) < (unsigned)p.sw_) & (ileft > 0);
-      const uint32_t off = ok ? (uint32_t)(roff[k] + aoff) * 2u : DIR_OOB;
+      const int vd = rbd[k] + dd, vh = rbh[k] + dh, vw = rbw[k] + dw;
+      const bool ok = ((unsigned)vd < (unsigned)p.sd_) & ((unsigned)vh < (unsigned)p.sh_) &
+                      ((unsigned)vw < (unsigned)p.sw_) & (ileft > 0);
+      uint32_t off;
+      if constexpr (MSK) {
+        // the slot's 8 channels of the pooled gradient at the dz voxel's pooling
+        // window (zero outside complete windows)
+        const bool inp = ok & (vd < 2 * p.pod) & (vh < 2 * p.poh) & (vw < 2 * p.pow_);
+        const int pv = ((rpn[k] + (vd >> 1)) * p.poh + (vh >> 1)) * p.pow_ + (vw >> 1);
+        off = inp ? (uint32_t)(pv * p.sc + rch[k] + 32 * icc) * 2u : DIR_OOB;
+      } else {
+        off = ok ? (uint32_t)(roff[k] + aoff) * 2u : DIR_OOB;
+      }
       __builtin_amdgcn_raw_ptr_buffer_load_lds(srsrc, (lds_void_t *)(stg + (256 * k + 64 * wave) * 16), 16, off, 0, 0, 0);
+    }
+    if constexpr (MSK) {
+      const int vd = mbd + dd, vh = mbh + dh, vw = mbw + dw;
+      const bool ok = ((unsigned)vd < (unsigned)p.sd_) & ((unsigned)vh < (unsigned)p.sh_) &
+                      ((unsigned)vw < (unsigned)p.sw_) & (ileft > 0);
+      const int voff = __builtin_amdgcn_readlane(v_voff, iti);
+      // bits of (voxel, channels 32 icc .. + 31): one aligned word
+      const uint32_t off = ok ? (uint32_t)((mvox + voff) * (p.sc >> 3) + 4 * icc) : DIR_OOB;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(mrsrc, (lds_void_t *)(stg + A_BYTES + B_BYTES + 256 * wave), 4, off,
+                                               0, 0, 0);
     }
 #pragma unroll
     for (int k = 0; k < NB; ++k) {
@@ -497,19 +640,24 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(const uint16_t *__restric
     for_stages<0, KS>([&](auto u) { issue_one(arr(StageIx<S + NS * decltype(u)::v>{})); });
   };
 
-  f32x4_t acc[FM][FN];
+  f32x4_t acc[FM][FN], acc2[MSK ? FM : 1][FN];  // acc2: the masked copy (split form)
 #pragma unroll
   for (int i = 0; i < FM; ++i)
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int i = 0; i < (MSK ? FM : 1); ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc2[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  // MFMA fragments of k-step u of stage ix
-  auto read_frags = [&](auto ix, auto u, bf16x8_t (&af)[FM], bf16x8_t (&bf)[FN]) {
+  // MFMA fragments of k-step u of stage ix (and, pooled gather, the mask words of their rows)
+  auto read_frags = [&](auto ix, auto u, bf16x8_t (&af)[FM], bf16x8_t (&bf)[FN], uint32_t (&mw)[FM]) {
     const unsigned char *stg = arr(StageIx<decltype(ix)::v + NS * decltype(u)::v>{});
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
       const int row = wave * 16 * FM + 16 * i + r16;
       af[i] = *reinterpret_cast<const bf16x8_t *>(stg + (row * 4 + (g4 ^ ((row >> 2) & 3))) * 16);
+      if constexpr (MSK) mw[i] = *reinterpret_cast<const uint32_t *>(stg + A_BYTES + B_BYTES + row * 4);
     }
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
@@ -531,6 +679,7 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(const uint16_t *__restric
 
   // fragments of the stage about to run (read one stage ahead)
   bf16x8_t af[KS][FM], bf[KS][FN];
+  uint32_t mf[KS][FM];
 
   // stage s (KS k-steps) on array ix, its fragments already in af / bf: wait
   // for this wave's loads of stage s + 1 (those of the next NS - 3 stages may
@@ -540,23 +689,38 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(const uint16_t *__restric
   // fragments of stage s + 1 while the MFMAs of stage s run
   auto kstep = [&](auto ix) {
     constexpr int S = decltype(ix)::v;
-    constexpr int VMC = (NS - 3) * (NA + NB) * KS;
+    constexpr int VMC = (NS - 3) * (NA + NB + NMK) * KS;
     __builtin_amdgcn_s_waitcnt(0x0070 | (VMC & 15) | ((VMC >> 4) << 14));  // vmcnt(VMC) lgkmcnt(0)
     asm volatile("s_barrier" ::: "memory");
     issue(StageIx<(S + NS - 1) % NS>{});
     bf16x8_t an[KS][FM], bn[KS][FN];
-    for_stages<0, KS>([&](auto u) { read_frags(StageIx<(S + 1) % NS>{}, u, an[decltype(u)::v], bn[decltype(u)::v]); });
+    uint32_t mn[KS][FM];
+    for_stages<0, KS>([&](auto u) {
+      read_frags(StageIx<(S + 1) % NS>{}, u, an[decltype(u)::v], bn[decltype(u)::v], mn[decltype(u)::v]);
+    });
 #pragma unroll
     for (int u = 0; u < KS; ++u)
 #pragma unroll
-      for (int i = 0; i < FM; ++i)
+      for (int i = 0; i < FM; ++i) {
 #pragma unroll
         for (int j = 0; j < FN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[u][i], bf[u][j], acc[i][j], 0, 0, 0);
+        if constexpr (MSK) {
+          const u32x4_t sel = sel_of_bits8(mf[u][i] >> (8 * g4));
+          const bf16x8_t am = __builtin_bit_cast(bf16x8_t, __builtin_bit_cast(u32x4_t, af[u][i]) & sel);
+#pragma unroll
+          for (int j = 0; j < FN; ++j)
+            acc2[i % (MSK ? FM : 1)][j] =
+                __builtin_amdgcn_mfma_f32_16x16x32_bf16(am, bf[u][j], acc2[i % (MSK ? FM : 1)][j], 0, 0, 0);
+        }
+      }
 #pragma unroll
     for (int u = 0; u < KS; ++u) {
 #pragma unroll
-      for (int i = 0; i < FM; ++i) af[u][i] = an[u][i];
+      for (int i = 0; i < FM; ++i) {
+        af[u][i] = an[u][i];
+        mf[u][i] = mn[u][i];
+      }
 #pragma unroll
       for (int j = 0; j < FN; ++j) bf[u][j] = bn[u][j];
     }
@@ -566,11 +730,23 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(const uint16_t *__restric
     ileft = nsteps;
     for_stages<0, NS - 1>([&](auto ix) { issue(ix); });
     // stage 0 landed everywhere, its fragments in registers
-    constexpr int VMC0 = (NS - 2) * (NA + NB) * KS;
+    constexpr int VMC0 = (NS - 2) * (NA + NB + NMK) * KS;
     __builtin_amdgcn_s_waitcnt(0x0f70 | (VMC0 & 15) | ((VMC0 >> 4) << 14));  // vmcnt(VMC0)
     asm volatile("s_barrier" ::: "memory");
-    for_stages<0, KS>([&](auto u) { read_frags(StageIx<0>{}, u, af[decltype(u)::v], bf[decltype(u)::v]); });
+    for_stages<0, KS>([&](auto u) {
+      read_frags(StageIx<0>{}, u, af[decltype(u)::v], bf[decltype(u)::v], mf[decltype(u)::v]);
+    });
     for (int s = 0; s < nsteps; s += NS * KS) for_stages<0, NS>([&](auto ix) { kstep(ix); });
+  }
+
+  if constexpr (MSK) {  // dz x W = alpha/8 (g x W) + (1 - alpha)/8 ((g & sel) x W)
+    const float s1 = 0.125f * p.alpha, s2 = 0.125f * (1.f - p.alpha);
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[i][j][e] = s1 * acc[i][j][e] + s2 * acc2[i % (MSK ? FM : 1)][j][e];
   }
 
   // ---- each wave's fp32 rows leave through its stage array as 16-byte vectors
@@ -587,17 +763,17 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(const uint16_t *__restric
 #pragma unroll
   for (int v = lane; v < 16 * FM * CV; v += 64) {
     const int row = v / CV, c8 = v % CV;
-    const int grow = m0 + wave * 16 * FM + row;
-    if (grow >= C.m) continue;
+    int n, od_, oh_, ow_;
+    const bool valid = row_voxel(wave * 16 * FM + row, n, od_, oh_, ow_);
+    if (!POOL && !valid) continue;
     float o[8];
     const float4 x0 = *reinterpret_cast<const float4 *>(&red[row * RED_LD + 8 * c8]);
     const float4 x1 = *reinterpret_cast<const float4 *>(&red[row * RED_LD + 8 * c8 + 4]);
     o[0] = x0.x; o[1] = x0.y; o[2] = x0.z; o[3] = x0.w;
     o[4] = x1.x; o[5] = x1.y; o[6] = x1.z; o[7] = x1.w;
-    const int t1 = fdiv(grow, C.fw), t2 = fdiv(t1, C.fh), n = fdiv(t2, C.fd);
-    const int ow_ = (grow - t1 * (int)C.fw.div) * p.ostr_w + C.or_w;
-    const int oh_ = (t1 - t2 * (int)C.fh.div) * p.ostr_h + C.or_h;
-    const int od_ = (t2 - n * (int)C.fd.div) * p.ostr_d + C.or_d;
+    od_ = od_ * p.ostr_d + C.or_d;
+    oh_ = oh_ * p.ostr_h + C.or_h;
+    ow_ = ow_ * p.ostr_w + C.or_w;
     const int e0 = (((n * p.dd + od_) * p.dh + oh_) * p.dw + ow_) * p.dc + n0 + 8 * c8;
     uint32_t bits = 0;
     if constexpr (ACT) {
@@ -608,11 +784,48 @@ __global__ __launch_bounds__(256) void conv_lds_kernel(const uint16_t *__restric
         o[e] = u > 0.f ? u : p.alpha * u;
       }
     }
-    Vec16<DT_BF16> pk;
+    if constexpr (POOL) {
+      // y stays in the wave's array for the pooling pass (each (row, chunk) has one owner)
+      *reinterpret_cast<float4 *>(&red[row * RED_LD + 8 * c8]) = make_float4(o[0], o[1], o[2], o[3]);
+      *reinterpret_cast<float4 *>(&red[row * RED_LD + 8 * c8 + 4]) = make_float4(o[4], o[5], o[6], o[7]);
+      if (valid) mask[e0 >> 3] = (uint8_t)bits;
+    } else {
+      Vec16<DT_BF16> pk;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) pk.e[e] = f2bf(o[e]);
-    *reinterpret_cast<uint4 *>(dst + e0) = pk.u;
-    if (ACT && mask) mask[e0 >> 3] = (uint8_t)bits;
+      for (int e = 0; e < 8; ++e) pk.e[e] = f2bf(o[e]);
+      *reinterpret_cast<uint4 *>(dst + e0) = pk.u;
+      if (ACT && mask) mask[e0 >> 3] = (uint8_t)bits;
+    }
+  }
+  if constexpr (POOL) {
+    // ---- 2^3 average pool of the brick: TWB/2 pooled voxels x BN channels;
+    // the window's four (d, h) lines are the four waves' arrays
+    __syncthreads();
+    const float *lines[4] = {reinterpret_cast<const float *>(stg0), reinterpret_cast<const float *>(stg1),
+                             reinterpret_cast<const float *>(stg2), reinterpret_cast<const float *>(stg3)};
+    for (int it = tid; it < (TWB / 2) * CV; it += 256) {
+      const int pw = it / CV, c8 = it % CV;
+      const int pwg = tb_w * (TWB / 2) + pw;
+      if (tb_d >= p.pod || tb_h >= p.poh || pwg >= p.pow_) continue;
+      float sm[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) sm[e] = 0.f;
+#pragma unroll
+      for (int dh2 = 0; dh2 < 4; ++dh2)
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+          const float *r = lines[dh2] + (2 * pw + t) * RED_LD + 8 * c8;
+          const float4 x0 = *reinterpret_cast<const float4 *>(r);
+          const float4 x1 = *reinterpret_cast<const float4 *>(r + 4);
+          sm[0] += x0.x; sm[1] += x0.y; sm[2] += x0.z; sm[3] += x0.w;
+          sm[4] += x1.x; sm[5] += x1.y; sm[6] += x1.z; sm[7] += x1.w;
+        }
+      const int q0 = (((tb_n * p.pod + tb_d) * p.poh + tb_h) * p.pow_ + pwg) * p.dc + n0 + 8 * c8;
+      Vec16<DT_BF16> pk;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) pk.e[e] = f2bf(sm[e] * 0.125f);
+      *reinterpret_cast<uint4 *>(dst + q0) = pk.u;
+    }
   }
 }
 
@@ -620,17 +833,17 @@ struct DirCfg {
   int fm, wm, wk, pf;
 };
 
-template <bool FWD, int FN, int PF, bool ACT>
+template <bool FWD, int FN, int PF, bool ACT, int GM>
 hipError_t launch_dir_t(const DirCfg &c, const DirParams &p, int tiles, const void *src, const void *w,
-                        const float *bias, void *dst, void *mask, hipStream_t st) {
+                        const float *bias, void *dst, void *mask, const void *aux, hipStream_t st) {
   dim3 grid((unsigned)tiles, p.dc / (16 * FN), 1);
   if (grid.x == 0 || grid.y == 0) return hipSuccess;  // no destination rows
   const uint16_t *s16 = (const uint16_t *)src, *w16 = (const uint16_t *)w;
   uint16_t *d16 = (uint16_t *)dst;
   uint8_t *m8 = (uint8_t *)mask;
-#define CF_DIR_LAUNCH(FM_, WM_, WK_)                                                                           \
-  hipLaunchKernelGGL((conv_direct_kernel<FWD, FM_, FN, WM_, WK_, PF, ACT>), grid, dim3(256), 0, st, s16, w16, \
-                     bias, d16, m8, p)
+#define CF_DIR_LAUNCH(FM_, WM_, WK_)                                                                               \
+  hipLaunchKernelGGL((conv_direct_kernel<FWD, FM_, FN, WM_, WK_, PF, ACT, GM>), grid, dim3(256), 0, st, s16, w16, \
+                     bias, d16, m8, aux, p)
   if (c.fm == 4 && c.wm == 2) CF_DIR_LAUNCH(4, 2, 2);
   else if (c.fm == 4 && c.wm == 1) CF_DIR_LAUNCH(4, 1, 4);
   else if (c.fm == 2 && c.wm == 2) CF_DIR_LAUNCH(2, 2, 2);
@@ -640,13 +853,13 @@ hipError_t launch_dir_t(const DirCfg &c, const DirParams &p, int tiles, const vo
   return hipGetLastError();
 }
 
-template <bool FWD, int FN, bool ACT>
+template <bool FWD, int FN, bool ACT, int GM = GRAD_DZ>
 hipError_t launch_dir_pf(const DirCfg &c, const DirParams &p, int tiles, const void *src, const void *w,
-                         const float *bias, void *dst, void *mask, hipStream_t st) {
+                         const float *bias, void *dst, void *mask, hipStream_t st, const void *aux = nullptr) {
   switch (c.pf) {
-    case 1: return launch_dir_t<FWD, FN, 1, ACT>(c, p, tiles, src, w, bias, dst, mask, st);
-    case 2: return launch_dir_t<FWD, FN, 2, ACT>(c, p, tiles, src, w, bias, dst, mask, st);
-    default: return launch_dir_t<FWD, FN, 3, ACT>(c, p, tiles, src, w, bias, dst, mask, st);
+    case 1: return launch_dir_t<FWD, FN, 1, ACT, GM>(c, p, tiles, src, w, bias, dst, mask, aux, st);
+    case 2: return launch_dir_t<FWD, FN, 2, ACT, GM>(c, p, tiles, src, w, bias, dst, mask, aux, st);
+    default: return launch_dir_t<FWD, FN, 3, ACT, GM>(c, p, tiles, src, w, bias, dst, mask, aux, st);
   }
 }
 
@@ -792,10 +1005,10 @@ int choose_lds(DirParams &p, int ny) {
   return 0;
 }
 
-template <bool FWD, int FN, bool ACT>
+template <bool FWD, int FN, bool ACT, bool POOL = false, int GM = GRAD_DZ>
 hipError_t launch_lds(int fm, DirParams &p, const void *src, const void *w, const float *bias, void *dst,
-                      void *mask, hipStream_t st) {
-  const int tiles = assign_tiles(p, 64 * fm);
+                      void *mask, hipStream_t st, const void *aux = nullptr) {
+  const int tiles = assign_tiles(p, POOL ? 1 : 64 * fm);  // pooled: the class counts bricks
   dim3 grid((unsigned)tiles, p.dc / (16 * FN), 1);
   if (grid.x == 0 || grid.y == 0) return hipSuccess;
   const uint16_t *s16 = (const uint16_t *)src, *w16 = (const uint16_t *)w;
@@ -812,8 +1025,8 @@ hipError_t launch_lds(int fm, DirParams &p, const void *src, const void *w, cons
   int ks = FWD ? 2 : 1;
   if (const char *k = getenv("CF_DIRECT_KSUB")) ks = atoi(k) == 1 ? 1 : 2;
 #define CF_LDS_LAUNCH(FM_, NS_, KS_)                                                                             \
-  hipLaunchKernelGGL((conv_lds_kernel<FWD, FM_, FN, ACT, NS_, KS_>), grid, dim3(256), 0, st, s16, w16, bias,    \
-                     (uint16_t *)dst, (uint8_t *)mask, p)
+  hipLaunchKernelGGL((conv_lds_kernel<FWD, FM_, FN, ACT, NS_, KS_, POOL, GM>), grid, dim3(256), 0, st, s16, w16, \
+                     bias, (uint16_t *)dst, (uint8_t *)mask, aux, p)
   if (fm == 2) {
     if (!ns4) CF_LDS_LAUNCH(2, 8, 1);
     else if (ks == 2) CF_LDS_LAUNCH(2, 4, 2);
@@ -841,6 +1054,30 @@ hipError_t launch_conv_fwd_direct(const ConvShape &s, const void *x, const void 
              : launch_dir_pf<true, 4, false>(c, p, tiles, x, w, nullptr, out, nullptr, st);
 }
 
+bool direct_pool_supported(const ConvShape &s) {
+  return direct_supported(s, true) && s.od >= 2 && s.oh >= 2 && s.ow >= 2;
+}
+
+// Pooled forward: the LDS-staged kernel over bricks of 2 x 2 x 16 FM output
+// voxels (32-wide bricks when the rows are wider than 16, else 16-wide).
+hipError_t launch_conv_fwd_direct_pool(const ConvShape &s, const void *x, const void *w, const float *bias,
+                                       float alpha, void *out, void *mask, hipStream_t st) {
+  DirParams p{};
+  build_tables(s, true, p);
+  p.alpha = alpha;
+  p.pod = s.od / 2;
+  p.poh = s.oh / 2;
+  p.pow_ = s.ow / 2;
+  const int fm = s.ow > 16 ? 2 : 1;
+  const int jw = (s.ow + 16 * fm - 1) / (16 * fm), jh = (s.oh + 1) / 2, jd = (s.od + 1) / 2;
+  DirClass &C = p.cls[0];
+  C.m = s.n * jd * jh * jw;
+  C.fw = make_fastdiv(jw);
+  C.fh = make_fastdiv(jh);
+  C.fd = make_fastdiv(jd);
+  return launch_lds<true, 4, true, true>(fm, p, x, w, bias, out, mask, st);
+}
+
 hipError_t launch_conv_bwd_data_direct(const ConvShape &s, const void *dz, const void *w, void *dx,
                                        hipStream_t st) {
   DirParams p{};
@@ -853,6 +1090,42 @@ hipError_t launch_conv_bwd_data_direct(const ConvShape &s, const void *dz, const
   const int tiles = assign_tiles(p, 16 * c.fm * c.wm);
   return fn == 4 ? launch_dir_pf<false, 4, false>(c, p, tiles, dz, w, nullptr, dx, nullptr, st)
                  : launch_dir_pf<false, 2, false>(c, p, tiles, dz, w, nullptr, dx, nullptr, st);
+}
+
+template <int GM>
+static hipError_t bwd_data_fused_t(const DirCfg &c, const DirParams &p, int tiles, int fn, const void *g,
+                                   const void *aux, const void *w, void *dx, hipStream_t st) {
+  return fn == 4 ? launch_dir_pf<false, 4, false, GM>(c, p, tiles, g, w, nullptr, dx, nullptr, st, aux)
+                 : launch_dir_pf<false, 2, false, GM>(c, p, tiles, g, w, nullptr, dx, nullptr, st, aux);
+}
+
+hipError_t launch_conv_bwd_data_direct_fused(const ConvShape &s, const void *g, const void *aux, int gm, float alpha,
+                                             const void *w, void *dx, hipStream_t st) {
+  DirParams p{};
+  build_tables(s, false, p);
+  p.alpha = alpha;
+  p.pod = s.od / 2;
+  p.poh = s.oh / 2;
+  p.pow_ = s.ow / 2;
+  const long long zel = (long long)s.n * s.od * s.oh * s.ow * s.co;
+  if (gm == GRAD_POOL) {
+    // the gathered buffer is the pooled gradient; the mask has a bit per dz element
+    p.src_bytes = (int)((long long)s.n * p.pod * p.poh * p.pow_ * s.co * 2);
+    p.aux_bytes = (int)((zel + 31) / 32 * 4);
+  } else {
+    p.aux_bytes = (int)(zel * 2);
+  }
+  const int fn = p.dc % 64 == 0 ? 4 : 2;
+  // pooled gradient: the LDS-staged kernel when its row tiles fill the machine
+  // (as the plain backward-data); the register kernel otherwise and for (dy, y)
+  if (gm == GRAD_POOL)
+    if (const int fm = choose_lds(p, p.dc / (16 * fn)))
+      return fn == 4 ? launch_lds<false, 4, false, false, GRAD_POOL>(fm, p, g, w, nullptr, dx, nullptr, st, aux)
+                     : launch_lds<false, 2, false, false, GRAD_POOL>(fm, p, g, w, nullptr, dx, nullptr, st, aux);
+  const DirCfg c = choose_cfg(p, fn, false);
+  const int tiles = assign_tiles(p, 16 * c.fm * c.wm);
+  return gm == GRAD_POOL ? bwd_data_fused_t<GRAD_POOL>(c, p, tiles, fn, g, aux, w, dx, st)
+                         : bwd_data_fused_t<GRAD_DYY>(c, p, tiles, fn, g, aux, w, dx, st);
 }
 
 }  // namespace cf

@@ -29,6 +29,19 @@
 //    only wait is the explicit one;
 //  * the partial block leaves straight from the accumulators (16 lanes write
 //    64 contiguous bytes of a dW row).
+//
+// Fused variants (the gradient operand rebuilt, never read from a stored dz):
+// pooled layers take the pooled-output gradient g and the forward's slope mask,
+//   dz[v, co] = g[pool(v), co] / 8 * (mask bit (v, co) ? 1 : alpha)
+// (zero outside complete pooling windows); unpooled layers take the gradient
+// dy of the activation y and y itself,
+//   dz[v, co] = dy[v, co] * (y[v, co] > 0 ? 1 : alpha).
+// Each thread loads its slot's sources into registers with the same lead as
+// the DMA, forms dz in fp32, rounds it to bf16 into the LDS slot the DMA
+// would have filled, and adds the fp32 values to its share of the bias
+// gradient db = sum_v dz; the shares of a slice meet in a fixed order (lane
+// butterfly, then the four waves) and the workgroups of the slice's first
+// row block write them as one partial row of db.
 
 #include "cf_common.h"
 #include "cf_kernels.h"
@@ -59,9 +72,15 @@ struct DwParams {
   int chunk;              // voxels per K slice (a multiple of 32)
   int mt, nt, jobs;       // row blocks, column blocks, mt nt slices
   int per;                // jobs per XCD
-  int x_bytes, dz_bytes;  // extents of the range-checked buffers
+  int x_bytes, g_bytes;   // extents of the range-checked buffers (g: dz, pooled gradient or dy)
+  int aux_bytes;          // fused: extent of the slope mask or of y
+  int pod, poh, pow_;     // pooled extents (pooled gradient)
+  float alpha;            // fused: leaky-ReLU slope
   FastDiv fow, foh, fod;  // output extent divisors
 };
+
+// gradient operand of the weight-gradient kernel
+enum : int { DW_DZ = GRAD_DZ, DW_POOL = GRAD_POOL, DW_DYY = GRAD_DYY };
 
 // byte offset of (row, 32-byte chunk) in a [32][64] bf16 tile with 128-byte
 // rows: the chunk index is XORed with bits 1 and 3 of the row so that the
@@ -76,12 +95,20 @@ struct Stage {
   static constexpr int v = N;
 };
 
-template <int WN>
-__global__ __launch_bounds__(256, 2) void dw_lds_kernel(const uint16_t *__restrict__ x,
-                                                        const uint16_t *__restrict__ dz, float *__restrict__ part,
-                                                        const DwParams p) {
+__device__ __forceinline__ u32x4_t ld128(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+}
+
+template <int WN, int GM>
+__global__ __launch_bounds__(256, GM == GRAD_DZ ? 2 : 1) void dw_lds_kernel(const uint16_t *__restrict__ x,
+                                                        const uint16_t *__restrict__ g,
+                                                        const void *__restrict__ aux, float *__restrict__ part,
+                                                        float *__restrict__ part_b, const DwParams p) {
   constexpr int WM = 4 / WN;
-  constexpr int NBLK = WM + WN;  // 4 KB tiles per stage (one DMA instruction per thread each)
+  constexpr bool FUSED = GM != DW_DZ;
+  // vector-memory instructions per thread and k-step: one DMA per 4 KB tile,
+  // plus (fused) the two register loads of each gradient tile
+  constexpr int NBLK = WM + (FUSED ? 2 * WN : WN);
   // x and dz tiles of each stage in arrays of their own: every fragment read
   // then matches exactly one array the DMA fills
   __shared__ __attribute__((aligned(16))) unsigned char sa0[WM * 4096], sb0[WN * 4096];
@@ -105,7 +132,10 @@ __global__ __launch_bounds__(256, 2) void dw_lds_kernel(const uint16_t *__restri
   const int nsteps = vend > vbeg ? (vend - vbeg + 31) >> 5 : 0;
 
   const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc((void *)x, (short)0, p.x_bytes, 0x00020000);
-  const __amdgpu_buffer_rsrc_t zr = __builtin_amdgcn_make_buffer_rsrc((void *)dz, (short)0, p.dz_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t zr = __builtin_amdgcn_make_buffer_rsrc((void *)g, (short)0, p.g_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t ar =
+      __builtin_amdgcn_make_buffer_rsrc((void *)aux, (short)0, FUSED ? p.aux_bytes : 0, 0x00020000);
+  (void)ar;
 
   // this thread's DMA slot in every tile: voxel row vr of the k-step, 16-byte
   // slot j, which holds logical 8-element chunk lj (the swizzle of tile_off)
@@ -144,17 +174,47 @@ __global__ __launch_bounds__(256, 2) void dw_lds_kernel(const uint16_t *__restri
     else return sb3;
   };
 
+  // fused: the gradient sources of the LNS steps in flight (register ring,
+  // one slot per stage) and this thread's share of db
+  u32x4_t gsrc[DW_LNS][WN], asrc[DW_LNS][WN];
+  float dbs[WN][8];
+#pragma unroll
+  for (int k = 0; k < WN; ++k)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) dbs[k][e] = 0.f;
+
   int vnext = vbeg + vr;  // this thread's voxel in the next step to load
   auto issue = [&](auto ix) {
+    constexpr int S = decltype(ix)::v;
     unsigned char *sa = stage_a(ix), *sb = stage_b(ix);
     const int vg = vnext;
     vnext += 32;
     const bool live = vg < vend;
     const int vv = live ? vg : 0;
     const int t1 = fdiv(vv, p.fow), t2 = fdiv(t1, p.foh), n = fdiv(t2, p.fod);
-    const int bw = (vv - t1 * (int)p.fow.div) * p.sw;
-    const int bh = (t1 - t2 * (int)p.foh.div) * p.sh;
-    const int bd = (t2 - n * (int)p.fod.div) * p.sd;
+    const int ow0 = vv - t1 * (int)p.fow.div, oh0 = t1 - t2 * (int)p.foh.div, od0 = t2 - n * (int)p.fod.div;
+    const int bw = ow0 * p.sw, bh = oh0 * p.sh, bd = od0 * p.sd;
+    if constexpr (GM == DW_DYY) {
+#pragma unroll
+      for (int k = 0; k < WN; ++k) {
+        uint32_t off = live ? (uint32_t)(vv * p.co + b_col[k]) * 2u : DW_OOB;
+        asm volatile("" : "+v"(off));
+        gsrc[S][k] = ld128(zr, off);
+        asrc[S][k] = ld128(ar, off);
+      }
+    } else if constexpr (GM == DW_POOL) {
+      // outside complete pooling windows the gradient reads as zero
+      const bool inp = live & (od0 < 2 * p.pod) & (oh0 < 2 * p.poh) & (ow0 < 2 * p.pow_);
+      const int pv = ((n * p.pod + (od0 >> 1)) * p.poh + (oh0 >> 1)) * p.pow_ + (ow0 >> 1);
+#pragma unroll
+      for (int k = 0; k < WN; ++k) {
+        uint32_t off = inp ? (uint32_t)(pv * p.co + b_col[k]) * 2u : DW_OOB;
+        uint32_t moff = live ? (uint32_t)(vv * p.co + b_col[k]) >> 3 : DW_OOB;
+        asm volatile("" : "+v"(off), "+v"(moff));
+        gsrc[S][k] = ld128(zr, off);
+        asrc[S][k][0] = __builtin_amdgcn_raw_buffer_load_b8(ar, moff, 0, 0);
+      }
+    }
 #pragma unroll
     for (int k = 0; k < WM; ++k) {
       const int id = bd + a_d[k], ih = bh + a_h[k], iw = bw + a_w[k];
@@ -164,12 +224,14 @@ __global__ __launch_bounds__(256, 2) void dw_lds_kernel(const uint16_t *__restri
       asm volatile("" : "+v"(off));  // a select, not two predicated copies of the load
       __builtin_amdgcn_raw_ptr_buffer_load_lds(xr, (lds_void_t *)(sa + k * 4096 + wave * 1024), 16, off, 0, 0, 0);
     }
+    if constexpr (!FUSED) {
 #pragma unroll
-    for (int k = 0; k < WN; ++k) {
-      uint32_t off = live ? (uint32_t)(vv * p.co + b_col[k]) * 2u : DW_OOB;
-      asm volatile("" : "+v"(off));
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(zr, (lds_void_t *)(sb + k * 4096 + wave * 1024), 16, off, 0,
-                                               0, 0);
+      for (int k = 0; k < WN; ++k) {
+        uint32_t off = live ? (uint32_t)(vv * p.co + b_col[k]) * 2u : DW_OOB;
+        asm volatile("" : "+v"(off));
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(zr, (lds_void_t *)(sb + k * 4096 + wave * 1024), 16, off, 0,
+                                                 0, 0);
+      }
     }
   };
 
@@ -191,11 +253,25 @@ __global__ __launch_bounds__(256, 2) void dw_lds_kernel(const uint16_t *__restri
 
   // one k-step on stage ix: wait for this thread's loads of the step (the next
   // LNS - 2 steps may stay in flight) and its fragment reads of the previous
-  // step, barrier, refill the previous step's stage, MFMAs of this step
+  // step, (fused: form this step's dz into its slots of the stage), barrier,
+  // refill the previous step's stage, MFMAs of this step.  Vector-memory
+  // loads complete in issue order, so vmcnt(VMC) covers this step's loads.
   auto kstep = [&](auto ix) {
     constexpr int S = decltype(ix)::v;
     constexpr int VMC = (DW_LNS - 2) * NBLK;
     __builtin_amdgcn_s_waitcnt(0x0070 | (VMC & 15) | ((VMC >> 4) << 14));  // vmcnt(VMC) lgkmcnt(0)
+    if constexpr (FUSED) {
+#pragma unroll
+      for (int k = 0; k < WN; ++k) {
+        float f[8];
+        form_dz8<GM>(gsrc[S][k], asrc[S][k], p.alpha, f);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) dbs[k][e] += f[e];
+        const u32x4_t v = pack_bf16x8(f);
+        *reinterpret_cast<u32x4_t *>(stage_b(ix) + k * 4096 + tid * 16) = v;
+      }
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the slots are written
+    }
     asm volatile("s_barrier" ::: "memory");
     issue(Stage<(S + DW_LNS - 1) % DW_LNS>{});
     bf16x8_t af[4], bf[4];
@@ -233,6 +309,38 @@ __global__ __launch_bounds__(256, 2) void dw_lds_kernel(const uint16_t *__restri
 #pragma unroll
       for (int jn = 0; jn < 4; ++jn) dst[(long long)m * p.co + n0 + 64 * wn + 16 * jn + r16] = acc[i][jn][e];
     }
+
+  if constexpr (FUSED) {
+    // db shares: a wave's voxel rows with the same logical chunk (lane bits 3
+    // and 5; bit 4 selects a swizzle, i.e. another chunk) by a butterfly, then
+    // the eight partial rows in order; the slice's first row block writes
+    if (mrow0 != 0) return;  // uniform
+#pragma unroll
+    for (int k = 0; k < WN; ++k)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float v = dbs[k][e];
+        v += __shfl_xor(v, 8);
+        v += __shfl_xor(v, 32);
+        dbs[k][e] = v;
+      }
+    __syncthreads();  // every wave is done with the stage arrays
+    float *red = reinterpret_cast<float *>(sa0);  // [8 partial rows][64 WN channels]
+    if ((lane & 0x28) == 0) {
+      const int r = 2 * wave + ((lane >> 4) & 1);
+#pragma unroll
+      for (int k = 0; k < WN; ++k)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) red[r * 64 * WN + 64 * k + 8 * lj + e] = dbs[k][e];
+    }
+    __syncthreads();
+    if (tid < 64 * WN) {
+      float v = 0.f;
+#pragma unroll
+      for (int r = 0; r < 8; ++r) v += red[r * 64 * WN + tid];
+      part_b[(long long)split * p.co + n0 + tid] = v;
+    }
+  }
 }
 
 struct DwPlan {
@@ -272,13 +380,24 @@ bool direct_wgrad_supported(const ConvShape &s) {
   return pvox > 0;
 }
 
-size_t direct_wgrad_workspace(const ConvShape &s) {
+size_t direct_wgrad_workspace(const ConvShape &s, bool fused) {
   const DwPlan pl = plan(s);
-  return (size_t)pl.nsplit * s.kd * s.kh * s.kw * s.ci * s.co * sizeof(float);
+  return (size_t)pl.nsplit * ((size_t)s.kd * s.kh * s.kw * s.ci * s.co + (fused ? s.co : 0)) * sizeof(float);
 }
 
-hipError_t launch_conv_bwd_weight_direct(const ConvShape &s, const void *x, const void *dz, float *dw, void *ws,
-                                         hipStream_t st) {
+template <int GM>
+static hipError_t launch_dw(int wn, dim3 grid, const DwParams &p, const void *x, const void *g, const void *aux,
+                            float *pw, float *pb, hipStream_t st) {
+  const uint16_t *x16 = (const uint16_t *)x, *g16 = (const uint16_t *)g;
+  if (wn == 2)
+    hipLaunchKernelGGL((dw_lds_kernel<2, GM>), grid, dim3(256), 0, st, x16, g16, aux, pw, pb, p);
+  else
+    hipLaunchKernelGGL((dw_lds_kernel<1, GM>), grid, dim3(256), 0, st, x16, g16, aux, pw, pb, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_conv_bwd_weight_direct(const ConvShape &s, const void *x, const void *g, const void *aux, int gm,
+                                         float alpha, float *dw, float *db, void *ws, hipStream_t st) {
   const DwPlan pl = plan(s);
   DwParams p{};
   p.d = s.d; p.h = s.h; p.w = s.w; p.ci = s.ci; p.co = s.co;
@@ -289,7 +408,15 @@ hipError_t launch_conv_bwd_weight_direct(const ConvShape &s, const void *x, cons
   p.pvox = s.n * s.od * s.oh * s.ow;
   p.chunk = pl.chunk;
   p.x_bytes = (int)((long long)s.n * s.d * s.h * s.w * s.ci * 2);
-  p.dz_bytes = (int)((long long)p.pvox * s.co * 2);
+  p.pod = s.od / 2; p.poh = s.oh / 2; p.pow_ = s.ow / 2;
+  p.alpha = alpha;
+  const long long zb = (long long)p.pvox * s.co * 2;
+  if (gm == DWG_POOL) {
+    p.g_bytes = (int)((long long)s.n * p.pod * p.poh * p.pow_ * s.co * 2);
+    p.aux_bytes = (int)(((long long)p.pvox * s.co + 31) / 32 * 4);
+  } else {
+    p.g_bytes = p.aux_bytes = (int)zb;
+  }
   p.fow = make_fastdiv(s.ow);
   p.foh = make_fastdiv(s.oh);
   p.fod = make_fastdiv(s.od);
@@ -297,15 +424,17 @@ hipError_t launch_conv_bwd_weight_direct(const ConvShape &s, const void *x, cons
   p.nt = pl.nt;
   p.jobs = pl.mt * pl.nt * pl.nsplit;
   p.per = (p.jobs + 7) / 8;
-  float *part = (float *)ws;
+  float *pw = (float *)ws;
+  float *pb = pw + (size_t)pl.nsplit * p.m * s.co;
   const dim3 grid((unsigned)(8 * p.per));
-  if (pl.wn == 2)
-    hipLaunchKernelGGL(dw_lds_kernel<2>, grid, dim3(256), 0, st, (const uint16_t *)x, (const uint16_t *)dz, part, p);
-  else
-    hipLaunchKernelGGL(dw_lds_kernel<1>, grid, dim3(256), 0, st, (const uint16_t *)x, (const uint16_t *)dz, part, p);
-  const hipError_t e = hipGetLastError();
+  hipError_t e;
+  if (gm == DWG_POOL) e = launch_dw<DW_POOL>(pl.wn, grid, p, x, g, aux, pw, pb, st);
+  else if (gm == DWG_DYY) e = launch_dw<DW_DYY>(pl.wn, grid, p, x, g, aux, pw, pb, st);
+  else e = launch_dw<DW_DZ>(pl.wn, grid, p, x, g, nullptr, pw, nullptr, st);
   if (e != hipSuccess) return e;
-  return launch_sum_rows(part, dw, pl.nsplit, p.m * p.co, st);
+  e = launch_sum_rows(pw, dw, pl.nsplit, p.m * s.co, st);
+  if (e != hipSuccess || gm == DWG_DZ) return e;
+  return launch_sum_rows(pb, db, pl.nsplit, s.co, st);
 }
 
 }  // namespace cf

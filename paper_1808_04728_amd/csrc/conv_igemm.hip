@@ -682,7 +682,7 @@ static bool use_l1_wgrad(const ConvShape &s) {
 size_t conv_bwd_weight_workspace(const ConvShape &s) {
   if (use_l1_wgrad(s)) return smallc_wgrad_dz_workspace(s);
   if (c16_wgrad_supported(s)) return c16_wgrad_workspace(s);
-  if (use_direct_wgrad(s)) return direct_wgrad_workspace(s);
+  if (use_direct_wgrad(s)) return direct_wgrad_workspace(s, false);
   if (use_f32_wgrad(s)) return f32wgrad_workspace(s, 0);
   WgradPlan pl = plan_wgrad(s);
   return (size_t)pl.nsplit * s.kd * s.kh * s.kw * s.ci * s.co * sizeof(float);
@@ -693,7 +693,8 @@ hipError_t launch_conv_bwd_weight(const ConvShape &s, const void *x, const void 
   if (use_l1_wgrad(s)) return launch_smallc_wgrad_dz(s, x, dz, dw, ws, st);
   if (c16_wgrad_supported(s))
     return launch_conv_bwd_weight_c16(s, x, dz, nullptr, 0.f, dw, nullptr, ws, false, nullptr, st);
-  if (use_direct_wgrad(s)) return launch_conv_bwd_weight_direct(s, x, dz, dw, ws, st);
+  if (use_direct_wgrad(s))
+    return launch_conv_bwd_weight_direct(s, x, dz, nullptr, DWG_DZ, 0.f, dw, nullptr, ws, st);
   if (use_f32_wgrad(s))
     return launch_conv_bwd_weight_f32(s, (const float *)x, (const float *)dz, nullptr, 0.f, dw, nullptr, ws, 0,
                                       nullptr, st);

@@ -205,6 +205,63 @@ __global__ __launch_bounds__(256) void bias_lrelu_bwd_vec_kernel(const typename 
   }
 }
 
+// Pooled layer's dz in one pass, the adjoints of the 2^3 pool and of the
+// leaky ReLU composed (Section III-C: pooling is a constant-weight
+// convolution; Section III-A: leaky ReLU after the convolution):
+//   dz[v, c] = g[pool(v), c] / 8 * (mask bit (v, c) ? 1 : alpha),
+// zero where no complete window covers v; db[c] = sum_v dz[v, c] from the
+// unrounded fp32 values, in the fixed order of bias_lrelu_bwd_vec_kernel.
+// Item k is the k-th 16-byte vector of dz (NDHWC): voxel k / cg_n, channel
+// group k % cg_n; its mask bits are bits V k .. V k + V - 1.
+template <int DT, bool WITH_DB>
+__global__ __launch_bounds__(256) void pool_lrelu_bwd_kernel(const typename Store<DT>::T *__restrict__ g,
+                                                             const uint8_t *__restrict__ mask, float alpha,
+                                                             typename Store<DT>::T *__restrict__ dz,
+                                                             float *__restrict__ part, int nv, int cg_n, int c,
+                                                             FastDiv fcg, FastDiv fw, FastDiv fh, FastDiv fd,
+                                                             int pd, int ph, int pw) {
+  constexpr int V = Store<DT>::VEC;
+  __shared__ float red[4 * 256];
+  const int tid = threadIdx.x;
+  const float a1 = 0.125f, a0 = 0.125f * alpha;
+  float s[V];
+#pragma unroll
+  for (int j = 0; j < V; ++j) s[j] = 0.f;
+  for (int k = (int)blockIdx.x * 256 + tid; k < nv; k += (int)gridDim.x * 256) {
+    const int vox = fdiv(k, fcg), cg = k - vox * (int)fcg.div;
+    const int t1 = fdiv(vox, fw), t2 = fdiv(t1, fh), n = fdiv(t2, fd);
+    const int x_ = vox - t1 * (int)fw.div, y_ = t1 - t2 * (int)fh.div, z_ = t2 - n * (int)fd.div;
+    const int px = x_ >> 1, py = y_ >> 1, pz = z_ >> 1;
+    Vec16<DT> v;
+    if (pz < pd && py < ph && px < pw) {
+      v.u = ld16<false>(g + (((n * pd + pz) * ph + py) * pw + px) * c + V * cg);
+      uint32_t bits = mask[(V * k) >> 3];
+      if constexpr (V == 4) bits >>= 4 * (k & 1);
+#pragma unroll
+      for (int j = 0; j < V; ++j) {
+        const float d = to_f32<DT>(v.e[j]) * (((bits >> j) & 1u) ? a1 : a0);
+        s[j] += d;
+        v.e[j] = from_f32<DT>(d);
+      }
+    } else {
+      v.u = make_uint4(0, 0, 0, 0);
+    }
+    st16<false>(dz + V * k, v.u);
+  }
+  if constexpr (WITH_DB) {
+    for (int off = cg_n; off < 64; off <<= 1)
+#pragma unroll
+      for (int j = 0; j < V; ++j) s[j] += __shfl_xor(s[j], off, 64);
+    const int lane = tid & 63, wave = tid >> 6;
+    if (lane < cg_n)
+#pragma unroll
+      for (int j = 0; j < V; ++j) red[wave * 256 + lane * V + j] = s[j];
+    __syncthreads();
+    if (tid < c)
+      part[(long long)blockIdx.x * c + tid] = (red[tid] + red[256 + tid]) + (red[512 + tid] + red[768 + tid]);
+  }
+}
+
 __global__ __launch_bounds__(256) void fill_zero_kernel(float *out, long long n) {
   long long i = (long long)blockIdx.x * 256 + threadIdx.x;
   if (i < n) out[i] = 0.f;
@@ -315,6 +372,53 @@ hipError_t launch_bias_lrelu_bwd(int64_t nvox, int c, int dtype, const void *dy,
               : bwd_t<DT_BF16, false>(nvox, c, dy, y, alpha, dz, db, ws, st);
   return db ? bwd_t<DT_F32, true>(nvox, c, dy, y, alpha, dz, db, ws, st)
             : bwd_t<DT_F32, false>(nvox, c, dy, y, alpha, dz, db, ws, st);
+}
+
+// workgroups of the pooled dz pass: at most 1024, each a whole number of
+// 256-vector rounds (the thread -> channel-group map is fixed, see above)
+static int pool_lrelu_blocks(long long nvox, int c, int V) {
+  const long long nv = nvox * (c / V);
+  return (int)std::min<long long>((nv + 255) / 256, 1024);
+}
+
+bool pool_lrelu_bwd_supported(long long nvox, int c, int dtype) {
+  const int V = dtype == DT_BF16 ? 8 : 4;
+  const int cg_n = c / V;
+  return c % V == 0 && (cg_n & (cg_n - 1)) == 0 && cg_n <= 64 && c <= 256 && nvox * c < (1LL << 31);
+}
+
+size_t pool_lrelu_bwd_workspace(int64_t nvox, int c) {
+  if (nvox <= 0) return 0;
+  return (size_t)std::max(pool_lrelu_blocks(nvox, c, 8), pool_lrelu_blocks(nvox, c, 4)) * c * sizeof(float);
+}
+
+template <int DT>
+static hipError_t pool_lrelu_t(int n, int d, int h, int w, int c, const void *g, const uint8_t *mask, float alpha,
+                               void *dz, float *db, void *ws, hipStream_t st) {
+  using T = typename Store<DT>::T;
+  constexpr int V = Store<DT>::VEC;
+  const long long nvox = (long long)n * d * h * w;
+  const int cg_n = c / V, nv = (int)(nvox * cg_n);
+  const int blocks = pool_lrelu_blocks(nvox, c, V);
+  float *part = (float *)ws;
+  if (db)
+    hipLaunchKernelGGL((pool_lrelu_bwd_kernel<DT, true>), dim3(blocks), dim3(256), 0, st, (const T *)g, mask, alpha,
+                       (T *)dz, part, nv, cg_n, c, make_fastdiv(cg_n), make_fastdiv(w), make_fastdiv(h),
+                       make_fastdiv(d), d / 2, h / 2, w / 2);
+  else
+    hipLaunchKernelGGL((pool_lrelu_bwd_kernel<DT, false>), dim3(blocks), dim3(256), 0, st, (const T *)g, mask,
+                       alpha, (T *)dz, part, nv, cg_n, c, make_fastdiv(cg_n), make_fastdiv(w), make_fastdiv(h),
+                       make_fastdiv(d), d / 2, h / 2, w / 2);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || !db) return e;
+  return launch_sum_rows(part, db, blocks, c, st);
+}
+
+hipError_t launch_pool_lrelu_bwd(int n, int d, int h, int w, int c, int dtype, const void *g, const void *mask,
+                                 float alpha, void *dz, float *db, void *ws, hipStream_t st) {
+  if ((long long)n * d * h * w == 0) return db ? launch_fill_zero(db, c, st) : hipSuccess;
+  return dtype == DT_BF16 ? pool_lrelu_t<DT_BF16>(n, d, h, w, c, g, (const uint8_t *)mask, alpha, dz, db, ws, st)
+                          : pool_lrelu_t<DT_F32>(n, d, h, w, c, g, (const uint8_t *)mask, alpha, dz, db, ws, st);
 }
 
 hipError_t launch_fill_zero(float *out, long long n, hipStream_t st) {

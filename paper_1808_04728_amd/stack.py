@@ -32,7 +32,7 @@ def _t(dtype):
 
 class ConvStack:
     def __init__(self, layers, size, batch, dtype="f32", alpha=0.01, device="cuda", skip_first_dgrad=True,
-                 fused=True, defer_reductions=True, overlap_wgrad=True):
+                 fused=True, defer_reductions=True, overlap_wgrad=True, pooled_dz_pass=True, fused_from=0):
         """fused: run a pooled layer through the fused entry points (forward
         epilogue writes pooled output + slope mask; backward rebuilds dz from
         them) wherever the library has fused kernels for the layer.
@@ -41,8 +41,16 @@ class ConvStack:
         overlap_wgrad: in the backward pass of an unfused layer, run the weight
         gradient on a second stream (default priority) concurrently with the
         data gradient; both only read dz, and the small deep layers leave most
-        of the GPU idle when run one after the other."""
+        of the GPU idle when run one after the other.
+        fused_from: layers before this index only are eligible for fusion when it
+        is > 0 (an A/B switch: e.g. 2 runs the deep layers unfused).
+        pooled_dz_pass: a fused pooled layer without a dz-storing weight-gradient
+        kernel forms dz in one pass from the pooled gradient and the mask
+        (cf_avgpool3d_lrelu_bwd) for the plain gradient kernels; False runs the
+        fused backward kernels, which form dz as they load it."""
         self.fused = fused
+        self.pooled_dz_pass = pooled_dz_pass
+        self.fused_from = fused_from
         self.defer_reductions = defer_reductions
         self.reduce_bytes = 0
         self.layers = layers
@@ -117,11 +125,12 @@ class ConvStack:
             both = B.FUSED_FWD | B.FUSED_BWD_WEIGHT
             # a layer whose data gradient is needed also needs a fused backward-data, or a
             # backward-weights that stores dz for the unfused backward-data
-            l["fused"] = bool(self.fused and (sup & both) == both and
+            fz = self.fused and (self.fused_from <= 0 or i < self.fused_from)
+            l["fused"] = bool(fz and (sup & both) == both and
                               (not needs_dgrad or sup & (B.FUSED_BWD_DATA | B.FUSED_BWD_WEIGHT_DZ)))
             # otherwise conv + bias + leaky ReLU may still share one kernel (y written once)
             sup0 = B.cf_conv3d_fused_supported(l["desc"], 0) if not s["pool"] else 0
-            l["fused_act"] = bool(self.fused and not l["fused"] and sup0 & B.FUSED_FWD)
+            l["fused_act"] = bool(fz and not l["fused"] and sup0 & B.FUSED_FWD)
             # and its backward may take (dy, y) straight into the weight and data
             # gradients (dz formed inside both, no separate leaky-ReLU backward)
             l["fused_y"] = bool(l["fused_act"] and sup0 & B.FUSED_BWD_WEIGHT and
@@ -134,9 +143,23 @@ class ConvStack:
                 # a layer whose data gradient is needed may take dz from its weight-gradient
                 # pass and run the unfused backward-data on it (same dx bits, faster there)
                 l["dz_emit"] = bool(needs_dgrad and sup & B.FUSED_BWD_WEIGHT_DZ)
-                if l["dz_emit"]:
+                # or, without that kernel, form dz in one pooled-gradient pass and run the
+                # plain weight and data gradients on it side by side: the data gradient
+                # gathers every dz element k^3 times, so forming dz once beats forming it
+                # inside every gather (the stride-2 layer: 4 + 26 us against 47 us)
+                od = l["out_dhw"]
+                l["dz_pass"] = bool(needs_dgrad and not l["dz_emit"] and self.pooled_dz_pass and
+                                    B.cf_avgpool3d_lrelu_bwd_workspace_size(n, *od, s["cout"]) > 0 and
+                                    self._pool_lrelu_ok(n, od, s["cout"]))
+                if l["dz_emit"] or l["dz_pass"]:
                     l["dz"] = torch.empty((n,) + l["out_dhw"] + (s["cout"],), dtype=tdt, device=dev)
                 l["mask"] = torch.empty(max(16, B.cf_conv3d_mask_bytes(l["desc"])), dtype=torch.uint8, device=dev)
+                if l["dz_pass"]:
+                    wsw = B.cf_conv3d_bwd_weight_workspace_size(l["desc"])
+                    wsb = B.cf_avgpool3d_lrelu_bwd_workspace_size(n, *od, s["cout"])
+                    l["ws_w"] = torch.empty(max(wsw, 16), dtype=torch.uint8, device=dev)
+                    l["ws_b"] = torch.empty(max(wsb, 16), dtype=torch.uint8, device=dev)
+                    continue
                 wsf = B.cf_conv3d_bwd_weight_fused_workspace_size(l["desc"], B.CF_FUSE_POOL2)
                 l["ws_w"] = torch.empty(max(wsf, 16), dtype=torch.uint8, device=dev)
                 l["ws_b"] = None
@@ -160,6 +183,13 @@ class ConvStack:
             s = self.L[0]["spec"]
             self.L[0]["dx"] = torch.empty((n,) + self.L[0]["in_dhw"] + (s["cin"],), dtype=tdt, device=dev)
         self.x = torch.empty((n,) + self.L[0]["in_dhw"] + (self.L[0]["spec"]["cin"],), dtype=tdt, device=dev)
+
+    def _pool_lrelu_ok(self, n, od, c):
+        # the one-pass kernel's channel rule (whole 16-byte vectors, a power of two of
+        # them, at most 64, c <= 256); the call itself rejects anything else
+        v = 8 if self.dtype == "bf16" else 4
+        g = c // v
+        return c % v == 0 and g > 0 and (g & (g - 1)) == 0 and g <= 64 and c <= 256
 
     def set_params(self, weights, biases):
         """Weights are rounded to the stack's dtype; the fp32 master copy holds
@@ -261,9 +291,40 @@ class ConvStack:
             l = self.L[i]
             s = l["spec"]
             c = self._call
-            if l["fused"] and side_used:
-                # the fused layers' kernels fill the GPU by themselves: they start
-                # after the side stream's weight gradients have finished
+            # a fused layer's backward runs on one stream when its data gradient
+            # follows from the dz its weight gradient stores, or when it has none
+            # (the first two layers: their kernels fill the GPU by themselves);
+            # it starts after the side stream's weight gradients have finished
+            one_stream = l["fused"] and (l["dz_emit"] or l["dx"] is None)
+            if l["fused"] and l["dz_pass"]:
+                # dz (and db) in one pass from the pooled gradient and the mask, then
+                # the plain weight gradient (side stream) beside the data gradient
+                od = l["out_dhw"]
+                if d:
+                    pend += c(f"L{i+1}.pool_lrelu_bwd", B.cf_avgpool3d_lrelu_bwd_deferred, self.batch, *od,
+                              s["cout"], self.dtype, g, l["mask"], self.alpha, l["dz"], l["db"], l["ws_b"], None,
+                              stream)
+                else:
+                    c(f"L{i+1}.pool_lrelu_bwd", B.cf_avgpool3d_lrelu_bwd, self.batch, *od, s["cout"], self.dtype, g,
+                      l["mask"], self.alpha, l["dz"], l["db"], l["ws_b"], None, stream)
+                ws_ = stream
+                if self.side is not None:
+                    main = stream if stream is not None else torch.cuda.current_stream()
+                    ev = torch.cuda.Event()
+                    ev.record(main)
+                    self.side.wait_event(ev)
+                    ws_ = self.side
+                    side_used = True
+                if d:
+                    pend += c(f"L{i+1}.conv_bwd_weight", B.cf_conv3d_bwd_weight_deferred, l["desc"],
+                              self.layer_input(i), l["dz"], l["dw"], l["ws_w"], None, ws_, rec=ws_)
+                else:
+                    c(f"L{i+1}.conv_bwd_weight", B.cf_conv3d_bwd_weight, l["desc"], self.layer_input(i), l["dz"],
+                      l["dw"], l["ws_w"], None, ws_, rec=ws_)
+                c(f"L{i+1}.conv_bwd_data", B.cf_conv3d_bwd_data, l["desc"], l["dz"], l["w"], l["dx"], stream)
+                g = l["dx"]
+                continue
+            if one_stream and side_used:
                 self._join_side(stream)
                 side_used = False
             if l["fused"] and l["dz_emit"]:
@@ -279,13 +340,23 @@ class ConvStack:
                 g = l["dx"]
                 continue
             if l["fused"]:
+                # with a fused data gradient to follow, the weight gradient goes to the
+                # side stream (both form dz from the pooled gradient and the mask)
+                ws_ = stream
+                if self.side is not None and l["dx"] is not None:
+                    main = stream if stream is not None else torch.cuda.current_stream()
+                    ev = torch.cuda.Event()
+                    ev.record(main)
+                    self.side.wait_event(ev)
+                    ws_ = self.side
+                    side_used = True
                 if d:
                     pend += c(f"L{i+1}.conv_bwd_weight_fused", B.cf_conv3d_bwd_weight_fused_deferred, l["desc"],
                               self.layer_input(i), g, l["mask"], self.alpha, B.CF_FUSE_POOL2, l["dw"], l["db"],
-                              None, l["ws_w"], None, stream)
+                              None, l["ws_w"], None, ws_, rec=ws_)
                 else:
                     c(f"L{i+1}.conv_bwd_weight_fused", B.cf_conv3d_bwd_weight_fused, l["desc"], self.layer_input(i),
-                      g, l["mask"], self.alpha, B.CF_FUSE_POOL2, l["dw"], l["db"], l["ws_w"], None, stream)
+                      g, l["mask"], self.alpha, B.CF_FUSE_POOL2, l["dw"], l["db"], l["ws_w"], None, ws_, rec=ws_)
                 if l["dx"] is not None:
                     c(f"L{i+1}.conv_bwd_data_fused", B.cf_conv3d_bwd_data_fused, l["desc"], g, l["mask"], l["w"],
                       self.alpha, B.CF_FUSE_POOL2, l["dx"], stream)
@@ -315,8 +386,7 @@ class ConvStack:
                     g = l["dx"]
                 continue
             if s["pool"]:
-                d, hh, w = l["out_dhw"]
-                c(f"L{i+1}.avgpool_bwd", B.cf_avgpool3d_bwd, self.batch, d, hh, w, s["cout"], 2, 2, self.dtype,
+                c(f"L{i+1}.avgpool_bwd", B.cf_avgpool3d_bwd, self.batch, *l["out_dhw"], s["cout"], 2, 2, self.dtype,
                   g, l["dy"], stream)
                 dy = l["dy"]
             else:
@@ -406,7 +476,8 @@ class ConvStack:
                 "conv_bias_lrelu_fwd": xb + wb + zb,
                 "conv_fwd": xb + wb + zb, "conv_bwd_data": zb + wb + xb,
                 "conv_bwd_weight": xb + zb + wb // es * 4, "bias_lrelu_fwd": 2 * zb,
-                "bias_lrelu_bwd": 3 * zb, "avgpool_fwd": zb + pb, "avgpool_bwd": zb + pb}[op]
+                "bias_lrelu_bwd": 3 * zb, "avgpool_fwd": zb + pb, "avgpool_bwd": zb + pb,
+                "pool_lrelu_bwd": pb + mb + zb}[op]
 
     # ------------------------------------------------------------------
     def conv_flops(self):
