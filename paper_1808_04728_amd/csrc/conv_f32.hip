@@ -638,12 +638,15 @@ double f_cost(FParams &p, const FCfg &c, int fn) {
   return rounds * (steps * 4.0 * c.fm * fn + 200.0);
 }
 
-template <bool FWD, int FN, int EPI, bool DYY = false>
-hipError_t launch_lin(const ConvShape &s, FParams &p, const float *src, const float *w, const float *bias, float *dst,
-                      uint8_t *mask, hipStream_t st, const float *ysrc = nullptr) {
+// The tile of a linear-layout launch: shift mode (pick -1) for the large
+// stride-1 4-wide layers, else the candidate of least cost.
+template <int FN>
+int f_pick(const ConvShape &s, FParams &p, double *cost) {
   if (f_shift_ok(s, p) && !getenv("CF_F32_TILE") &&
-      (f_shift_env() == 1 || f_assign(p, 64) * (p.dc / (16 * FN)) >= 4 * kNumCUs))
-    return launch_f<FWD, FN, EPI, 4, 1, 1, 4, DYY>(p, f_assign(p, 64), src, w, bias, dst, mask, st, ysrc);
+      (f_shift_env() == 1 || f_assign(p, 64) * (p.dc / (16 * FN)) >= 4 * kNumCUs)) {
+    *cost = 0.0;
+    return -1;
+  }
   int pick = 0;
   double best = 0.0;
   for (int i = 0; i < kNCand; ++i) {
@@ -655,6 +658,17 @@ hipError_t launch_lin(const ConvShape &s, FParams &p, const float *src, const fl
   }
   // CF_F32_TILE=i forces candidate i (the tests cover every one this way)
   if (const char *forced = getenv("CF_F32_TILE")) pick = std::min(kNCand - 1, std::max(0, atoi(forced)));
+  *cost = best;
+  return pick;
+}
+
+template <bool FWD, int FN, int EPI, bool DYY = false>
+hipError_t launch_lin(const ConvShape &s, FParams &p, const float *src, const float *w, const float *bias, float *dst,
+                      uint8_t *mask, hipStream_t st, const float *ysrc = nullptr) {
+  double cost;
+  const int pick = f_pick<FN>(s, p, &cost);
+  if (pick < 0)
+    return launch_f<FWD, FN, EPI, 4, 1, 1, 4, DYY>(p, f_assign(p, 64), src, w, bias, dst, mask, st, ysrc);
   const FCfg c = kCand[pick];
   const int tiles = f_assign(p, 16 * c.fm * c.wm);
 #define CF_F32_CASE(I, FM_, WM_, WK_) \
@@ -670,6 +684,31 @@ hipError_t launch_lin(const ConvShape &s, FParams &p, const float *src, const fl
     default: return launch_f<FWD, FN, EPI, 2, 1, 8, 0, DYY>(p, tiles, src, w, bias, dst, mask, st, ysrc);
   }
 #undef CF_F32_CASE
+}
+
+// Column groups per workgroup (FN x 16 output columns): the widest that
+// divides the columns unless a narrower one costs less -- narrow groups give
+// the small deep layers (a few hundred rows at batch 1) several times more
+// workgroups, each with a share of the columns, instead of a few dozen that
+// leave most compute units idle.  CF_F32_FN=1|2|4 forces a width.
+int f_pick_fn(const ConvShape &s, FParams &p, int fnmax) {
+  if (const char *e = getenv("CF_F32_FN")) {
+    const int f = atoi(e);
+    if ((f == 1 || f == 2 || f == 4) && f <= fnmax && p.dc % (16 * f) == 0) return f;
+  }
+  int best_fn = fnmax;
+  double best = 0.0;
+  for (int f = fnmax; f >= 1; f >>= 1) {
+    if (p.dc % (16 * f) != 0) continue;
+    double c;
+    const int pick = f == 4 ? f_pick<4>(s, p, &c) : f == 2 ? f_pick<2>(s, p, &c) : f_pick<1>(s, p, &c);
+    if (pick < 0) return fnmax;  // shift mode: the large layers keep the widest groups
+    if (f == fnmax || c < best) {
+      best = c;
+      best_fn = f;
+    }
+  }
+  return best_fn;
 }
 
 }  // namespace
@@ -714,15 +753,20 @@ hipError_t launch_conv_fwd_f32(const ConvShape &s, const float *x, const float *
     // leave compute units idle (the stride-2 layer at batch 1)
     if ((long long)tiles * (s.co / 32) < 2LL * kNumCUs && f_shift_env() != 1)
       return launch_f<true, 1, 2, 4, 1, 8>(p, tiles, x, w, bias, out, mask, st);
-    if (f_shift_ok(s, p)) return launch_f<true, 2, 2, 4, 1, 4, 4>(p, tiles, x, w, bias, out, mask, st);
+    // shift mode: one wave per brick with every tap (measured on the 16 -> 32 layer at
+    // 128^3: 177 -> 168 us against four waves with a quarter of the taps each)
+    if (f_shift_ok(s, p)) return launch_f<true, 2, 2, 4, 1, 1, 4>(p, tiles, x, w, bias, out, mask, st);
     return launch_f<true, 2, 2, 4, 1, 4>(p, tiles, x, w, bias, out, mask, st);
   }
-  const int fn = s.co % 64 == 0 ? 4 : 2;
-  if (epi == 1)
-    return fn == 4 ? launch_lin<true, 4, 1>(s, p, x, w, bias, out, mask, st)
-                   : launch_lin<true, 2, 1>(s, p, x, w, bias, out, mask, st);
-  return fn == 4 ? launch_lin<true, 4, 0>(s, p, x, w, nullptr, out, nullptr, st)
-                 : launch_lin<true, 2, 0>(s, p, x, w, nullptr, out, nullptr, st);
+  const int fn = f_pick_fn(s, p, s.co % 64 == 0 ? 4 : 2);
+  if (epi == 1) {
+    if (fn == 4) return launch_lin<true, 4, 1>(s, p, x, w, bias, out, mask, st);
+    if (fn == 2) return launch_lin<true, 2, 1>(s, p, x, w, bias, out, mask, st);
+    return launch_lin<true, 1, 1>(s, p, x, w, bias, out, mask, st);
+  }
+  if (fn == 4) return launch_lin<true, 4, 0>(s, p, x, w, nullptr, out, nullptr, st);
+  if (fn == 2) return launch_lin<true, 2, 0>(s, p, x, w, nullptr, out, nullptr, st);
+  return launch_lin<true, 1, 0>(s, p, x, w, nullptr, out, nullptr, st);
 }
 
 hipError_t launch_conv_bwd_data_f32(const ConvShape &s, const float *dz, const float *w, float *dx, hipStream_t st,
@@ -730,7 +774,7 @@ hipError_t launch_conv_bwd_data_f32(const ConvShape &s, const float *dz, const f
   FParams p{};
   f_tables(s, false, p);
   p.alpha = alpha;
-  const int fn = s.ci % 64 == 0 ? 4 : (s.ci % 32 == 0 ? 2 : 1);
+  const int fn = f_pick_fn(s, p, s.ci % 64 == 0 ? 4 : (s.ci % 32 == 0 ? 2 : 1));
   if (y) {
     if (fn == 4) return launch_lin<false, 4, 0, true>(s, p, dz, w, nullptr, dx, nullptr, st, y);
     if (fn == 2) return launch_lin<false, 2, 0, true>(s, p, dz, w, nullptr, dx, nullptr, st, y);

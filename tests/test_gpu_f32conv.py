@@ -29,12 +29,20 @@ def ids(c):
     return "n%d_%dx%dx%d_c%d-%d_k%d_s%d_%s" % (c[0], *c[1], *c[2:])
 
 
+@pytest.mark.parametrize("fn", ["auto", "1", "2", "4"])
 @pytest.mark.parametrize("tile", TILES)
 @pytest.mark.parametrize("case", CASES, ids=ids)
-def test_f32_fwd_and_bwd_data(case, tile, monkeypatch):
+def test_f32_fwd_and_bwd_data(case, tile, fn, monkeypatch):
+    """Every tile shape, with the column-group width forced to 1, 2 or 4
+    groups of 16 (CF_F32_FN; ignored where it does not divide the columns) or
+    left to the cost model."""
+    if fn != "auto" and tile not in (0, 3, 6):
+        pytest.skip("column-group widths are covered on three tile shapes")
     N, dhw, CI, CO, k, s, pad = case
     desc = B.make_desc(N, dhw, CI, CO, k, s, pad, "f32")
     monkeypatch.setenv("CF_F32_TILE", str(tile))
+    if fn != "auto":
+        monkeypatch.setenv("CF_F32_FN", fn)
     rng = np.random.default_rng(31 + tile)
     x = dev(rng.standard_normal((N, *dhw, CI)), "f32")
     w = dev(rng.standard_normal((k, k, k, CI, CO)) / np.sqrt(k ** 3 * CI), "f32")
