@@ -265,12 +265,13 @@ __global__ __launch_bounds__(256) void conv_smallc_fwd_kernel(
           if constexpr (NF == 1) {
             // the eight ballots of the pair go to LDS as they are (one lane writes);
             // the row's mask words are interleaved from them after the last pair
-            // one 64-bit move per ballot (uniform values, every lane gets a copy)
+            // (moves the compiler places: it tracks the wait states between a
+            // compare writing an SGPR pair and a vector instruction reading it)
             uint64_t bv[2][4];
 #pragma unroll
             for (int dd = 0; dd < 2; ++dd)
 #pragma unroll
-              for (int j = 0; j < 4; ++j) asm volatile("v_mov_b64 %0, %1" : "=v"(bv[dd][j]) : "s"(bal[dd][j]));
+              for (int j = 0; j < 4; ++j) bv[dd][j] = bal[dd][j];
             if (lane == 0) {
 #pragma unroll
               for (int dd = 0; dd < 2; ++dd)
