@@ -280,11 +280,14 @@ def run_stack(name, args, steps, warmup, extras):
     op_ms = {k: float(np.mean([a.elapsed_time(b) for a, b in v])) for k, v in st.timer.items()}
     dominant = max(op_ms, key=op_ms.get)
     if args.op_breakdown:
+        # in call order (the order of the ops' launches within a step), with each
+        # op's FLOPs and algorithmic bytes
         print(f"{name}:", file=sys.stderr)
-        for k, v in sorted(op_ms.items(), key=lambda kv: -kv[1]):
-            fl = st.op_flops(k)
-            extra = f"{fl / v / 1e9:8.1f} TFLOP/s" if fl else f"{st.op_bytes(k) / v / 1e6:8.1f} GB/s"
-            print(f"  {k:24s} {v * 1e3:9.1f} us  {extra}", file=sys.stderr)
+        for k, v in op_ms.items():
+            fl, nb = st.op_flops(k), st.op_bytes(k)
+            extra = f"{fl / v / 1e9:8.1f} TFLOP/s" if fl else f"{nb / v / 1e6:8.1f} GB/s"
+            print(f"  op {k:30s} {v * 1e3:9.1f} us {fl / 1e9:10.4f} GFLOP {nb / 1e6:10.4f} MB  {extra}",
+                  file=sys.stderr)
 
     # timed region: events bracket only the dominant op
     st.timer = {}
