@@ -466,15 +466,27 @@ WPlan w_plan(const ConvShape &s, int gm) {
     pl.units = s.kd * s.kh * s.kw * pl.cunits;
   }
   pl.fn = fused ? 2 : (s.co % 64 == 0 ? 4 : (s.co % 32 == 0 ? 2 : 1));
-  pl.ru = (fused || pl.units >= 64) ? 2 : 1;
+  // Row units per wave and workgroups per launch (measured on the 128^3 stack at
+  // batch 1, sums included):
+  //  * about one workgroup per compute unit, or per two for short reductions
+  //    (below 2^16 voxels, where more slices would write more partials than the
+  //    slices read operands);
+  //  * pooled layers with short reductions (the stride-2 layer) take one row
+  //    unit per wave and one workgroup per compute unit: twice the workgroups
+  //    over the same slices (40 -> 31 us);
+  //  * pooled layers with long reductions (2^18 voxels and more: the 16 -> 32
+  //    layer) take two workgroups per compute unit, four waves per SIMD, whose
+  //    address work and load waits hide behind each other's MFMAs (218 -> 200
+  //    us, although the partials double).
+  const bool shortk = vox < (1 << 16);
+  pl.ru = (fused ? !shortk : pl.units >= 64) ? 2 : 1;
+  // CF_F32W_RU=1|2 overrides the row units per wave (measurement sweeps)
+  if (const char *e = getenv("CF_F32W_RU")) pl.ru = atoi(e) == 1 ? 1 : 2;
   pl.wv = 8;
   pl.gx = (pl.units + pl.ru * pl.wv - 1) / (pl.ru * pl.wv);
   pl.gy = s.co / (16 * pl.fn);
-  // about one workgroup per compute unit, or per two for short reductions
-  // (below 2^16 voxels, where more slices would write more partials than the
-  // slices read operands)
   const long long tiles = (long long)pl.gx * pl.gy;
-  long long target = vox >= (1 << 16) ? kNumCUs : kNumCUs / 2;
+  long long target = shortk ? (fused ? kNumCUs : kNumCUs / 2) : (fused && vox >= (1 << 18) ? 2 * kNumCUs : kNumCUs);
   // CF_F32W_TARGET overrides the workgroup target (measurement sweeps)
   if (const char *e = getenv("CF_F32W_TARGET")) target = std::max(1, atoi(e));
   long long want = std::max(1LL, (target + tiles - 1) / tiles);
@@ -545,7 +557,13 @@ hipError_t launch_wfn(const WPlan &pl, const WF32Params &p, const float *x, cons
 }  // namespace
 
 namespace {
-constexpr int kL1Blocks = kNumCUs;  // one workgroup of eight waves per compute unit
+// two workgroups of eight waves per compute unit (four waves per SIMD; 62 -> 58
+// us against one at 128^3); CF_L1F32_BLOCKS overrides the count (measurement
+// sweeps)
+int l1_blocks() {
+  const char *e = getenv("CF_L1F32_BLOCKS");
+  return e ? std::max(1, std::min(8 * kNumCUs, atoi(e))) : 2 * kNumCUs;
+}
 
 L1F32Params l1_params(const ConvShape &s, float alpha) {
   L1F32Params p{};
@@ -555,7 +573,7 @@ L1F32Params l1_params(const ConvShape &s, float alpha) {
   p.pod = s.od / 2; p.poh = s.oh / 2; p.pow_ = s.ow / 2;
   const int nseg = (s.ow + 15) / 16;
   p.total = s.n * s.od * s.oh * nseg;
-  p.per = (p.total + kL1Blocks * 8 - 1) / (kL1Blocks * 8);
+  p.per = (p.total + l1_blocks() * 8 - 1) / (l1_blocks() * 8);
   p.fs = make_fastdiv(nseg);
   p.fh = make_fastdiv(s.oh);
   p.fd = make_fastdiv(s.od);
@@ -575,26 +593,27 @@ bool l1f32_wgrad_supported(const ConvShape &s) {
 }
 
 size_t l1f32_wgrad_workspace(const ConvShape &s) {
-  return (size_t)kL1Blocks * (s.kd * s.kh * s.kw + 1) * 16 * sizeof(float);
+  return (size_t)l1_blocks() * (s.kd * s.kh * s.kw + 1) * 16 * sizeof(float);
 }
 
 hipError_t launch_l1_wgrad_f32(const ConvShape &s, const float *x, const float *dp, const uint16_t *mask,
                                float alpha, float *dw, float *db, void *ws, hipStream_t st) {
   const L1F32Params p = l1_params(s, alpha);
+  const int nb = l1_blocks();
   const int taps = s.kd * s.kh * s.kw;
   float *pw = (float *)ws;
-  float *pb = pw + (size_t)kL1Blocks * taps * 16;
+  float *pb = pw + (size_t)nb * taps * 16;
   if (s.kd == 2)
-    hipLaunchKernelGGL((l1_wgrad_f32_kernel<2, 0, 8, 2>), dim3(kL1Blocks), dim3(512), 0, st, x, dp, mask, pw, pb, p);
+    hipLaunchKernelGGL((l1_wgrad_f32_kernel<2, 0, 8, 2>), dim3(nb), dim3(512), 0, st, x, dp, mask, pw, pb, p);
   else if (s.pw == 0)
-    hipLaunchKernelGGL((l1_wgrad_f32_kernel<3, 0, 8, 2>), dim3(kL1Blocks), dim3(512), 0, st, x, dp, mask, pw, pb, p);
+    hipLaunchKernelGGL((l1_wgrad_f32_kernel<3, 0, 8, 2>), dim3(nb), dim3(512), 0, st, x, dp, mask, pw, pb, p);
   else
-    hipLaunchKernelGGL((l1_wgrad_f32_kernel<3, 1, 8, 2>), dim3(kL1Blocks), dim3(512), 0, st, x, dp, mask, pw, pb, p);
+    hipLaunchKernelGGL((l1_wgrad_f32_kernel<3, 1, 8, 2>), dim3(nb), dim3(512), 0, st, x, dp, mask, pw, pb, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  e = launch_sum_rows(pw, dw, kL1Blocks, taps * 16, st);
+  e = launch_sum_rows(pw, dw, nb, taps * 16, st);
   if (e != hipSuccess) return e;
-  return launch_sum_rows(pb, db, kL1Blocks, 16, st);
+  return launch_sum_rows(pb, db, nb, 16, st);
 }
 
 bool f32wgrad_supported(const ConvShape &s) {
@@ -627,8 +646,8 @@ hipError_t launch_conv_bwd_weight_f32(const ConvShape &s, const float *x, const 
   if (gm == GM_POOL_MASK) {
     p.g_bytes = (uint32_t)((long long)s.n * p.pod * p.poh * p.pow_ * s.co * 4);
     p.m_bytes = (uint32_t)(((long long)p.vox * s.co + 31) / 32 * 4);
-    e = pl.kw4 ? launch_w<GM_POOL_MASK, true, 2, 2>(pl, p, x, g, aux, pw, pb, dz_out, st)
-               : launch_w<GM_POOL_MASK, false, 2, 2>(pl, p, x, g, aux, pw, pb, dz_out, st);
+    e = pl.kw4 ? launch_wu<GM_POOL_MASK, true, 2>(pl, p, x, g, aux, pw, pb, dz_out, st)
+               : launch_wu<GM_POOL_MASK, false, 2>(pl, p, x, g, aux, pw, pb, dz_out, st);
   } else if (gm == GM_DY_Y) {
     p.g_bytes = p.m_bytes = (uint32_t)((long long)p.vox * s.co * 4);
     e = launch_wfn<GM_DY_Y>(pl, p, x, g, aux, pw, pb, dz_out, st);

@@ -79,11 +79,15 @@ POOLED = [
 ]
 
 
+@pytest.mark.parametrize("ru", ["auto", "1", "2"])
 @pytest.mark.parametrize("case", POOLED, ids=lambda c: "n%d_%dx%dx%d_c%d-%d_k%d_s%d" % (c[0], *c[1], *c[2:]))
-def test_f32_pooled_layer_fused(case):
+def test_f32_pooled_layer_fused(case, ru, monkeypatch):
     """Fused forward (pooled output + slope mask) and fused backward-weights
     (dW, db and the stored dz) of a pooled fp32 layer, any stride, against the
-    oracle; the unfused backward-data of the stored dz against the oracle."""
+    oracle; the unfused backward-data of the stored dz against the oracle.
+    CF_F32W_RU forces one or two row units per wave in the weight gradient."""
+    if ru != "auto":
+        monkeypatch.setenv("CF_F32W_RU", ru)
     N, dhw, CI, CO, k, s = case
     desc = B.make_desc(N, dhw, CI, CO, k, s, "same", "f32")
     sup = B.cf_conv3d_fused_supported(desc, B.CF_FUSE_POOL2)
