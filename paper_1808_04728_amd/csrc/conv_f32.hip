@@ -122,7 +122,16 @@ __device__ __forceinline__ uint32_t shift_lane(uint32_t a, uint32_t e) {
 // DYY (backward-data of an unpooled fused layer): the gathered operand is
 // dz = dy * (y > 0 ? 1 : alpha), formed from dy (src) and the layer's saved
 // activation y (ysrc, the same layout) after both loads arrive.
-template <bool FWD, int FM, int FN, int WM, int WK, int PF, int EPI, int UW = 0, bool DYY = false>
+//
+// TK (taps in K, a stride-1 class whose 4 taps along w are consecutive in the
+// tap table): a k-step is one kernel row (kd, kh) x 8 channels.  K slot g of an
+// MFMA is tap column g of the row and register j of a lane's 16-byte load is
+// channel c0 + j: lane (m, g) loads channels c0 .. c0 + 3 of its own source
+// voxel, the one tap column g reads (m + g forward, m - g backward-data, along
+// w), with its own range check.  Four loads per fragment and kernel row (two per
+// k-step) instead of shift mode's two plus 24 lane moves, and no alignment of
+// the fragments along w.  The launches use it for the forward.
+template <bool FWD, int FM, int FN, int WM, int WK, int PF, int EPI, int UW = 0, bool DYY = false, bool TK = false>
 __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__restrict__ src,
                                                                 const float *__restrict__ ysrc,
                                                                 const float *__restrict__ wt,
@@ -217,7 +226,102 @@ __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__r
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  if constexpr (UW > 0) {
+  if constexpr (TK) {
+    // ---- taps in K: k-steps are kernel rows (4 taps) x 8 channels ------------
+    static_assert(!DYY && UW == 0, "taps-in-K mode reads a plain source");
+    constexpr int SG = FWD ? 1 : -1;            // source voxel of tap column g: m + SG g along w
+    const int nch = p.sc >> 3;
+    const int nrows = C.ntap >> 2;
+    const int myrows = nrows > wk ? (nrows - wk + WK - 1) / WK : 0;
+    const int nsteps = myrows * nch;
+    int ri = wk, cc = 0, ldstep = 0;
+    auto next = [&]() {  // branch-free: see the linear cursor below
+      ++ldstep;
+      const int c1 = cc + (ldstep < nsteps ? 1 : 0);
+      const bool wrap = c1 == nch;
+      cc = wrap ? 0 : c1;
+      ri += wrap ? WK : 0;
+    };
+    // this lane's K slot is tap column g4: its source voxel and w range check
+    // (tap column 0 of every row has dw = 0), and the weights of its tap
+    int aoff[FM];
+    bool wok[FM];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      aoff[i] = roff[i] - 4 * g4 + SG * g4 * p.sc;
+      wok[i] = rok[i] & ((unsigned)(rbw[i] + SG * g4) < (unsigned)p.sw_);
+    }
+    const int tstr = p.wco * (FWD ? p.sc : p.dc);  // elements from one tap's weights to the next
+    constexpr int NB = FWD ? 4 : FN;              // weight loads per channel quad
+    constexpr int BW = FWD ? FN : 4;              // floats per weight load
+    int wl[NB];
+#pragma unroll
+    for (int v = 0; v < NB; ++v)
+      wl[v] = g4 * tstr + (FWD ? v * p.wco + n0 + FN * r16      // W[t_g][c0 + v][n0 + FN r ..]
+                               : (n0 + 16 * v + r16) * p.wco);  // W[t_g][n0 + 16 v + r][c0 ..]
+    constexpr int NS = PF + 1;
+    u32x4_t a_r[NS][2][FM];
+    uint32_t b_r[NS][2][NB][BW];
+    auto load = [&](u32x4_t(&a)[2][FM], uint32_t(&b)[2][NB][BW]) {
+      const FTap &T = p.tap[C.tap0 + ri * 4];
+      const int cofs = cc * 8;
+      const bool live = ldstep < nsteps;
+#pragma unroll
+      for (int i = 0; i < FM; ++i) {
+        const bool ok = live & wok[i] & ((unsigned)(rbd[i] + T.dd) < (unsigned)p.sd_) &
+                        ((unsigned)(rbh[i] + T.dh) < (unsigned)p.sh_);
+        // a masked lane reads from 2^31, past the buffer (zeros) for both loads: OR-ing
+        // bit 31 into a negative offset could wrap back into range at + 16
+        const uint32_t o = ok ? (uint32_t)(aoff[i] + T.a_off + cofs) * 4u : 0x80000000u;
+        a[0][i] = ld128(srsrc, o);
+        a[1][i] = ld128(srsrc, o + 16u);
+      }
+#pragma unroll
+      for (int c = 0; c < 2; ++c) {
+        const int wbase = T.w_off + (cofs + 4 * c) * (FWD ? p.wco : 1);
+#pragma unroll
+        for (int v = 0; v < NB; ++v) {
+          const uint32_t off = (uint32_t)(wl[v] + wbase) * 4u;
+          if constexpr (BW == 4) {
+            const u32x4_t q = ld128(wrsrc, off);
+            b[c][v][0] = q[0]; b[c][v][1] = q[1]; b[c][v][2] = q[2]; b[c][v][3] = q[3];
+          } else if constexpr (BW == 2) {
+            const u32x2_t q = ld64(wrsrc, off);
+            b[c][v][0] = q[0]; b[c][v][1] = q[1];
+          } else {
+            b[c][v][0] = __builtin_amdgcn_raw_buffer_load_b32(wrsrc, off, 0, 0);
+          }
+        }
+      }
+    };
+    if (nsteps > 0) {
+      const int niter = (nsteps + NS - 1) / NS * NS;
+#pragma unroll
+      for (int q = 0; q < PF; ++q) {
+        load(a_r[q], b_r[q]);
+        next();
+      }
+      for (int s0 = 0; s0 < niter; s0 += NS) {
+#pragma unroll
+        for (int q = 0; q < NS; ++q) {
+          load(a_r[(q + PF) % NS], b_r[(q + PF) % NS]);
+          next();
+          __builtin_amdgcn_sched_barrier(0);  // prefetch loads stay ahead of the MFMAs
+#pragma unroll
+          for (int c = 0; c < 2; ++c)
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+              for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int v = 0; v < FN; ++v) {
+                  const float bv = FWD ? f_of(b_r[q][c][j][v]) : f_of(b_r[q][c][v][j]);
+                  acc[i][v] = __builtin_amdgcn_mfma_f32_16x16x4f32(f_of(a_r[q][c][i][j]), bv, acc[i][v], 0, 0, 0);
+                }
+        }
+      }
+    }
+  } else if constexpr (UW > 0) {
     // ---- shift mode: k-steps are kernel rows (UW taps) x 16 channels ---------
     const int nch = p.sc >> 4;
     const int nrows = C.ntap / UW;
@@ -597,15 +701,16 @@ struct FCfg {
 constexpr FCfg kCand[] = {{4, 1, 1}, {4, 2, 1}, {2, 2, 1}, {4, 1, 4}, {2, 1, 4}, {1, 1, 4}, {1, 1, 8}, {2, 1, 8}};
 constexpr int kNCand = sizeof(kCand) / sizeof(kCand[0]);
 
-template <bool FWD, int FN, int EPI, int FM, int WM, int WK, int UW = 0, bool DYY = false>
+template <bool FWD, int FN, int EPI, int FM, int WM, int WK, int UW = 0, bool DYY = false, bool TK = false>
 hipError_t launch_f(const FParams &p, int tiles, const float *src, const float *w, const float *bias, float *dst,
                     uint8_t *mask, hipStream_t st, const float *ysrc = nullptr) {
   dim3 grid((unsigned)tiles, p.dc / (16 * FN), 1);
   if (grid.x == 0 || grid.y == 0) return hipSuccess;
-  // shift-mode k-steps hold UW taps: one step of prefetch covers the latency
-  constexpr int PF = UW > 0 ? 1 : 2;
-  hipLaunchKernelGGL((conv_f32_kernel<FWD, FM, FN, WM, WK, PF, EPI, UW, DYY>), grid, dim3(64 * WM * WK), 0, st, src,
-                     ysrc, w, bias, dst, mask, p);
+  // shift-mode and taps-in-K k-steps hold four taps: one step of prefetch covers
+  // the latency
+  constexpr int PF = UW > 0 || TK ? 1 : 2;
+  hipLaunchKernelGGL((conv_f32_kernel<FWD, FM, FN, WM, WK, PF, EPI, UW, DYY, TK>), grid, dim3(64 * WM * WK), 0, st,
+                     src, ysrc, w, bias, dst, mask, p);
   return hipGetLastError();
 }
 
@@ -617,6 +722,15 @@ hipError_t launch_f(const FParams &p, int tiles, const float *src, const float *
 int f_shift_env() {
   const char *e = getenv("CF_F32_SHIFT");
   return e ? (e[0] == '0' ? 0 : 1) : -1;
+}
+// Taps in K replaces shift mode in the forward (the 16 -> 32 layer's pooled
+// forward at 128^3: 169 -> 155 us).  Backward-data keeps shift mode: its source
+// holds 32 channels, 128 bytes per voxel, so each 16-byte lane load touches its
+// own cache line, and taps in K issues twice the loads (measured 195 -> 281 us).
+// CF_F32_TK=0 keeps shift mode everywhere.
+bool f_tk() {
+  const char *e = getenv("CF_F32_TK");
+  return !(e && e[0] == '0');
 }
 bool f_shift_ok(const ConvShape &s, const FParams &p) {
   if (f_shift_env() == 0) return false;
@@ -667,8 +781,12 @@ hipError_t launch_lin(const ConvShape &s, FParams &p, const float *src, const fl
                       uint8_t *mask, hipStream_t st, const float *ysrc = nullptr) {
   double cost;
   const int pick = f_pick<FN>(s, p, &cost);
-  if (pick < 0)
+  if (pick < 0) {
+    if constexpr (FWD && !DYY) {
+      if (f_tk()) return launch_f<FWD, FN, EPI, 4, 1, 1, 0, false, true>(p, f_assign(p, 64), src, w, bias, dst, mask, st);
+    }
     return launch_f<FWD, FN, EPI, 4, 1, 1, 4, DYY>(p, f_assign(p, 64), src, w, bias, dst, mask, st, ysrc);
+  }
   const FCfg c = kCand[pick];
   const int tiles = f_assign(p, 16 * c.fm * c.wm);
 #define CF_F32_CASE(I, FM_, WM_, WK_) \
@@ -755,7 +873,10 @@ hipError_t launch_conv_fwd_f32(const ConvShape &s, const float *x, const float *
       return launch_f<true, 1, 2, 4, 1, 8>(p, tiles, x, w, bias, out, mask, st);
     // shift mode: one wave per brick with every tap (measured on the 16 -> 32 layer at
     // 128^3: 177 -> 168 us against four waves with a quarter of the taps each)
-    if (f_shift_ok(s, p)) return launch_f<true, 2, 2, 4, 1, 1, 4>(p, tiles, x, w, bias, out, mask, st);
+    if (f_shift_ok(s, p)) {
+      if (f_tk()) return launch_f<true, 2, 2, 4, 1, 1, 0, false, true>(p, tiles, x, w, bias, out, mask, st);
+      return launch_f<true, 2, 2, 4, 1, 1, 4>(p, tiles, x, w, bias, out, mask, st);
+    }
     return launch_f<true, 2, 2, 4, 1, 4>(p, tiles, x, w, bias, out, mask, st);
   }
   const int fn = f_pick_fn(s, p, s.co % 64 == 0 ? 4 : 2);

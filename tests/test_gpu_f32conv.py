@@ -129,9 +129,10 @@ def test_f32_pooled_layer_fused(case, ru, monkeypatch):
     assert maxabs_err(to_np(dx), oracle.conv3d_bwd_data(dzr, to_np(w), dhw, stride=s)) <= TOL["f32"]
 
 
-# shift mode (stride-1 4-wide kernels, destination width a multiple of 16):
-# forward, forward + bias + lReLU + mask, pooled forward and backward-data, each
-# with the mode forced on and off, against the oracle
+# the four-tap modes (stride-1 4-wide kernels, destination width a multiple of
+# 16): forward, forward + bias + lReLU + mask, pooled forward and backward-data,
+# each with taps in K ("tk"), with DPP lane shifts ("dpp") and with neither
+# ("off": one tap per k-step), against the oracle
 SHIFT = [
     (1, (9, 7, 32), 16, 32, 4),
     (2, (5, 6, 48), 16, 32, 4),
@@ -140,11 +141,12 @@ SHIFT = [
 ]
 
 
-@pytest.mark.parametrize("mode", ["1", "0"])
+@pytest.mark.parametrize("mode", ["tk", "dpp", "off"])
 @pytest.mark.parametrize("case", SHIFT, ids=lambda c: "n%d_%dx%dx%d_c%d-%d_k%d" % (c[0], *c[1], *c[2:]))
 def test_f32_shift_mode(case, mode, monkeypatch):
     N, dhw, CI, CO, k = case
-    monkeypatch.setenv("CF_F32_SHIFT", mode)
+    monkeypatch.setenv("CF_F32_SHIFT", "0" if mode == "off" else "1")
+    monkeypatch.setenv("CF_F32_TK", "0" if mode == "dpp" else "1")
     desc = B.make_desc(N, dhw, CI, CO, k, 1, "same", "f32")
     rng = np.random.default_rng(51)
     x = dev(rng.standard_normal((N, *dhw, CI)), "f32")
