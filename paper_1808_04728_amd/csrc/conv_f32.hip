@@ -104,7 +104,8 @@ __device__ __forceinline__ uint32_t shift_lane(uint32_t a, uint32_t e) {
   if constexpr (UWI == 0) {
     return a;
   } else {
-    const int ed = __builtin_amdgcn_update_dpp(0, (int)e, FWD ? 0x120 + 16 - UWI : 0x120 + UWI, 0xf, 0xf, false);
+    // a row rotate writes every lane: no old value to keep
+    const int ed = __builtin_amdgcn_mov_dpp((int)e, FWD ? 0x120 + 16 - UWI : 0x120 + UWI, 0xf, 0xf, false);
     return (uint32_t)__builtin_amdgcn_update_dpp(ed, (int)a, FWD ? 0x100 + UWI : 0x110 + UWI, 0xf, 0xf, false);
   }
 }
@@ -131,7 +132,14 @@ __device__ __forceinline__ uint32_t shift_lane(uint32_t a, uint32_t e) {
 // w), with its own range check.  Four loads per fragment and kernel row (two per
 // k-step) instead of shift mode's two plus 24 lane moves, and no alignment of
 // the fragments along w.  The launches use it for the forward.
-template <bool FWD, int FM, int FN, int WM, int WK, int PF, int EPI, int UW = 0, bool DYY = false, bool TK = false>
+//
+// OS (output shift; backward-data of a stride-1 layer with 4 taps along w,
+// tiles of whole destination w rows): one accumulator set per tap column uw
+// holds P_uw[p] = sum over kernel rows and channels of dz[p] W[uw] for the
+// source voxels p of the tile's own rows, unshifted; the epilogue adds
+// P_uw[w + pw - uw] into dx[w].  One load per fragment and k-step, no lane moves.
+template <bool FWD, int FM, int FN, int WM, int WK, int PF, int EPI, int UW = 0, bool DYY = false, bool TK = false,
+          bool OS = false>
 __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__restrict__ src,
                                                                 const float *__restrict__ ysrc,
                                                                 const float *__restrict__ wt,
@@ -226,7 +234,87 @@ __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__r
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-  if constexpr (TK) {
+  f32x4_t acco[OS ? 4 : 1][OS ? FM : 1][OS ? FN : 1];  // output shift: one set per tap column
+  if constexpr (OS) {
+    static_assert(!FWD && !DYY && UW == 0 && !TK && WM == 1 && WK == 1 && EPI == 0, "output shift: backward-data");
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int v = 0; v < FN; ++v) acco[u][i][v] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    const int nch = p.sc >> 4;
+    const int nsteps = (C.ntap >> 2) * nch;  // kernel rows x 16-channel chunks
+    int ri = 0, cc = 0, ldstep = 0;
+    auto next = [&]() {  // branch-free: see the linear cursor below
+      ++ldstep;
+      const int c1 = cc + (ldstep < nsteps ? 1 : 0);
+      const bool wrap = c1 == nch;
+      cc = wrap ? 0 : c1;
+      ri += wrap ? 1 : 0;
+    };
+    // a row's source voxel along w is its own w (the tile's rows are whole w rows)
+    int soff[FM];
+    bool swok[FM];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      soff[i] = roff[i] - C.bq_w * p.sc;
+      swok[i] = rok[i] & ((unsigned)(rbw[i] - C.bq_w) < (unsigned)p.sw_);
+    }
+    int wl[FN];
+#pragma unroll
+    for (int v = 0; v < FN; ++v) wl[v] = (n0 + 16 * v + r16) * p.wco + 4 * g4;  // W[t][n0 + 16 v + r][4g ..]
+    constexpr int NS = PF + 1;
+    u32x4_t a_r[NS][FM];
+    uint32_t b_r[NS][4][FN][4];
+    auto load = [&](u32x4_t(&a)[FM], uint32_t(&b)[4][FN][4]) {
+      const FTap &T = p.tap[C.tap0 + ri * 4];
+      const int cofs = cc * 16;
+      const bool live = ldstep < nsteps;
+#pragma unroll
+      for (int i = 0; i < FM; ++i) {
+        const bool ok = live & swok[i] & ((unsigned)(rbd[i] + T.dd) < (unsigned)p.sd_) &
+                        ((unsigned)(rbh[i] + T.dh) < (unsigned)p.sh_);
+        // a valid byte offset is below 2^31: bit 31 sends the load past the buffer (zeros)
+        a[i] = ld128(srsrc, ((uint32_t)(soff[i] + T.a_off + cofs) * 4u) | ((uint32_t)!ok << 31));
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int wbase = p.tap[C.tap0 + ri * 4 + u].w_off + cofs;
+#pragma unroll
+        for (int v = 0; v < FN; ++v) {
+          const u32x4_t q = ld128(wrsrc, (uint32_t)(wl[v] + wbase) * 4u);
+          b[u][v][0] = q[0]; b[u][v][1] = q[1]; b[u][v][2] = q[2]; b[u][v][3] = q[3];
+        }
+      }
+    };
+    if (nsteps > 0) {
+      const int niter = (nsteps + NS - 1) / NS * NS;
+#pragma unroll
+      for (int q = 0; q < PF; ++q) {
+        load(a_r[q], b_r[q]);
+        next();
+      }
+      for (int s0 = 0; s0 < niter; s0 += NS) {
+#pragma unroll
+        for (int q = 0; q < NS; ++q) {
+          load(a_r[(q + PF) % NS], b_r[(q + PF) % NS]);
+          next();
+          __builtin_amdgcn_sched_barrier(0);  // prefetch loads stay ahead of the MFMAs
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+#pragma unroll
+              for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int v = 0; v < FN; ++v)
+                  acco[u][i][v] = __builtin_amdgcn_mfma_f32_16x16x4f32(f_of(a_r[q][i][j]), f_of(b_r[q][u][v][j]),
+                                                                       acco[u][i][v], 0, 0, 0);
+        }
+      }
+    }
+  } else if constexpr (TK) {
     // ---- taps in K: k-steps are kernel rows (4 taps) x 8 channels ------------
     static_assert(!DYY && UW == 0, "taps-in-K mode reads a plain source");
     constexpr int SG = FWD ? 1 : -1;            // source voxel of tap column g: m + SG g along w
@@ -405,21 +493,25 @@ __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__r
           }
           next();
           __builtin_amdgcn_sched_barrier(0);  // prefetch loads stay ahead of the MFMAs
+          // a column's shifted operands of every fragment first, then its MFMAs:
+          // interleaved one operand at a time, the moves and the MFMA reading
+          // their result stall on each other
           auto column = [&](auto uwc) {
             constexpr int uw = decltype(uwc)::value;
+            uint32_t av[FM][4];
 #pragma unroll
-            for (int i = 0; i < FM; ++i) {
-              u32x4_t av;
+            for (int i = 0; i < FM; ++i)
 #pragma unroll
-              for (int j = 0; j < 4; ++j) av[j] = shift_lane<uw, FWD>(a_r[q][i][j], e_r[q][i][j]);
+              for (int j = 0; j < 4; ++j) av[i][j] = shift_lane<uw, FWD>(a_r[q][i][j], e_r[q][i][j]);
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
 #pragma unroll
               for (int j = 0; j < 4; ++j)
 #pragma unroll
                 for (int v = 0; v < FN; ++v) {
                   const float bv = FWD ? f_of(b_r[q][uw][j][v]) : f_of(b_r[q][uw][v][j]);
-                  acc[i][v] = __builtin_amdgcn_mfma_f32_16x16x4f32(f_of(av[j]), bv, acc[i][v], 0, 0, 0);
+                  acc[i][v] = __builtin_amdgcn_mfma_f32_16x16x4f32(f_of(av[i][j]), bv, acc[i][v], 0, 0, 0);
                 }
-            }
           };
           column(std::integral_constant<int, 0>{});
           if constexpr (UW > 1) column(std::integral_constant<int, 1>{});
@@ -526,6 +618,33 @@ __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__r
       }
     }
   
+  }
+
+  if constexpr (OS) {
+    // ---- output shift: dx[w] = sum over tap columns k of P_k[w + pw - k] (zero
+    // past the ends of the w row), one tap column at a time through the LDS tile
+    const int jwn = (int)C.fw.div;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int v = 0; v < FN; ++v)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) red[(16 * i + 4 * g4 + e) * RED_LD + 16 * v + r16] = acco[k][i][v][e];
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int row = 16 * i + 4 * g4 + e, jw = row % jwn, sw = jw + C.bq_w - k;
+          if ((unsigned)sw < (unsigned)jwn) {
+#pragma unroll
+            for (int v = 0; v < FN; ++v) acc[i][v][e] += red[(row - jw + sw) * RED_LD + 16 * v + r16];
+          }
+        }
+      __syncthreads();
+    }
   }
 
   // ---- partial tiles meet in LDS -------------------------------------------
@@ -701,15 +820,16 @@ struct FCfg {
 constexpr FCfg kCand[] = {{4, 1, 1}, {4, 2, 1}, {2, 2, 1}, {4, 1, 4}, {2, 1, 4}, {1, 1, 4}, {1, 1, 8}, {2, 1, 8}};
 constexpr int kNCand = sizeof(kCand) / sizeof(kCand[0]);
 
-template <bool FWD, int FN, int EPI, int FM, int WM, int WK, int UW = 0, bool DYY = false, bool TK = false>
+template <bool FWD, int FN, int EPI, int FM, int WM, int WK, int UW = 0, bool DYY = false, bool TK = false,
+          bool OS = false>
 hipError_t launch_f(const FParams &p, int tiles, const float *src, const float *w, const float *bias, float *dst,
                     uint8_t *mask, hipStream_t st, const float *ysrc = nullptr) {
   dim3 grid((unsigned)tiles, p.dc / (16 * FN), 1);
   if (grid.x == 0 || grid.y == 0) return hipSuccess;
   // shift-mode and taps-in-K k-steps hold four taps: one step of prefetch covers
   // the latency
-  constexpr int PF = UW > 0 || TK ? 1 : 2;
-  hipLaunchKernelGGL((conv_f32_kernel<FWD, FM, FN, WM, WK, PF, EPI, UW, DYY, TK>), grid, dim3(64 * WM * WK), 0, st,
+  constexpr int PF = UW > 0 || TK || OS ? 1 : 2;
+  hipLaunchKernelGGL((conv_f32_kernel<FWD, FM, FN, WM, WK, PF, EPI, UW, DYY, TK, OS>), grid, dim3(64 * WM * WK), 0, st,
                      src, ysrc, w, bias, dst, mask, p);
   return hipGetLastError();
 }
@@ -731,6 +851,15 @@ int f_shift_env() {
 bool f_tk() {
   const char *e = getenv("CF_F32_TK");
   return !(e && e[0] == '0');
+}
+// Output shift replaces shift mode in backward-data where the destination w rows
+// tile the 64-row tiles exactly (w extent 16, 32 or 64).  CF_F32_OS=0 keeps
+// shift mode.
+bool f_os_ok(const FParams &p) {
+  const char *e = getenv("CF_F32_OS");
+  if (e && e[0] == '0') return false;
+  const int jw = (int)p.cls[0].fw.div;
+  return p.ncls == 1 && (jw == 16 || jw == 32 || jw == 64);
 }
 bool f_shift_ok(const ConvShape &s, const FParams &p) {
   if (f_shift_env() == 0) return false;
@@ -784,6 +913,10 @@ hipError_t launch_lin(const ConvShape &s, FParams &p, const float *src, const fl
   if (pick < 0) {
     if constexpr (FWD && !DYY) {
       if (f_tk()) return launch_f<FWD, FN, EPI, 4, 1, 1, 0, false, true>(p, f_assign(p, 64), src, w, bias, dst, mask, st);
+    }
+    if constexpr (!FWD && !DYY && FN == 1 && EPI == 0) {
+      if (f_os_ok(p))
+        return launch_f<FWD, FN, EPI, 4, 1, 1, 0, false, false, true>(p, f_assign(p, 64), src, w, bias, dst, mask, st);
     }
     return launch_f<FWD, FN, EPI, 4, 1, 1, 4, DYY>(p, f_assign(p, 64), src, w, bias, dst, mask, st, ysrc);
   }

@@ -131,13 +131,15 @@ def test_f32_pooled_layer_fused(case, ru, monkeypatch):
 
 # the four-tap modes (stride-1 4-wide kernels, destination width a multiple of
 # 16): forward, forward + bias + lReLU + mask, pooled forward and backward-data,
-# each with taps in K ("tk"), with DPP lane shifts ("dpp") and with neither
-# ("off": one tap per k-step), against the oracle
+# each with the default modes ("tk": taps in K forward, output shift backward
+# where the w rows tile), with DPP lane shifts ("dpp") and with neither ("off":
+# one tap per k-step), against the oracle
 SHIFT = [
     (1, (9, 7, 32), 16, 32, 4),
     (2, (5, 6, 48), 16, 32, 4),
     (1, (6, 5, 32), 32, 64, 4),
     (1, (8, 6, 16), 16, 32, 4),     # one fragment per row: both edges are padding
+    (2, (3, 5, 64), 16, 32, 4),     # whole 64-voxel w rows per tile (output shift)
 ]
 
 
@@ -147,6 +149,7 @@ def test_f32_shift_mode(case, mode, monkeypatch):
     N, dhw, CI, CO, k = case
     monkeypatch.setenv("CF_F32_SHIFT", "0" if mode == "off" else "1")
     monkeypatch.setenv("CF_F32_TK", "0" if mode == "dpp" else "1")
+    monkeypatch.setenv("CF_F32_OS", "0" if mode == "dpp" else "1")
     desc = B.make_desc(N, dhw, CI, CO, k, 1, "same", "f32")
     rng = np.random.default_rng(51)
     x = dev(rng.standard_normal((N, *dhw, CI)), "f32")
