@@ -157,9 +157,10 @@ __global__ __launch_bounds__(64 * WV) void wgrad_f32_kernel(const float *__restr
     }
   };
   if (nsteps > 0) setrow(r0);
-  // branch-free (scalar selects): control flow between the ring's steps would
-  // let the compiler sink every prefetch load to the end of the ring and wait
-  // for all of them before the first step's MFMAs
+  // The row values change once per row: they are recomputed under a uniform
+  // branch when the cursor wraps (every step, as scalar selects, their ~60
+  // scalar instructions per step cost the 16 -> 32 layer's launch at two waves
+  // per SIMD 219 -> 195 us with its sums)
   auto next = [&]() {
     ++ldstep;
     const int adv = ldstep < nsteps ? 1 : 0;
@@ -167,7 +168,7 @@ __global__ __launch_bounds__(64 * WV) void wgrad_f32_kernel(const float *__restr
     const bool wrap = c1 == p.nws;
     cws = wrap ? 0 : c1;
     crow += wrap ? 1 : 0;
-    setrow(min(crow, nrow_all - 1));
+    if (wrap) setrow(min(crow, nrow_all - 1));
   };
 
   constexpr int NS = PF + 1;
@@ -474,10 +475,9 @@ WPlan w_plan(const ConvShape &s, int gm) {
   //  * pooled layers with short reductions (the stride-2 layer) take one row
   //    unit per wave and one workgroup per compute unit: twice the workgroups
   //    over the same slices (40 -> 31 us);
-  //  * pooled layers with long reductions (2^18 voxels and more: the 16 -> 32
-  //    layer) take two workgroups per compute unit, four waves per SIMD, whose
-  //    address work and load waits hide behind each other's MFMAs (218 -> 200
-  //    us, although the partials double).
+  //  (with a scalar-heavy step, two workgroups per compute unit measured faster
+  //  on the 16 -> 32 layer, 218 -> 200 us; with the row values computed once per
+  //  row, one is: 195 against 201 us, and half the partials).
   const bool shortk = vox < (1 << 16);
   pl.ru = (fused ? !shortk : pl.units >= 64) ? 2 : 1;
   // CF_F32W_RU=1|2 overrides the row units per wave (measurement sweeps)
@@ -486,7 +486,7 @@ WPlan w_plan(const ConvShape &s, int gm) {
   pl.gx = (pl.units + pl.ru * pl.wv - 1) / (pl.ru * pl.wv);
   pl.gy = s.co / (16 * pl.fn);
   const long long tiles = (long long)pl.gx * pl.gy;
-  long long target = shortk ? (fused ? kNumCUs : kNumCUs / 2) : (fused && vox >= (1 << 18) ? 2 * kNumCUs : kNumCUs);
+  long long target = shortk ? (fused ? kNumCUs : kNumCUs / 2) : kNumCUs;
   // CF_F32W_TARGET overrides the workgroup target (measurement sweeps)
   if (const char *e = getenv("CF_F32W_TARGET")) target = std::max(1, atoi(e));
   long long want = std::max(1LL, (target + tiles - 1) / tiles);
