@@ -844,7 +844,9 @@ int f_shift_env() {
   return e ? (e[0] == '0' ? 0 : 1) : -1;
 }
 // Taps in K replaces shift mode in the forward (the 16 -> 32 layer's pooled
-// forward at 128^3: 169 -> 155 us).  Backward-data keeps shift mode: its source
+// forward at 128^3: 169 -> 155 us) and, needing no 16-voxel alignment, the
+// linear tiles of 4-wide forwards whose w extent is not a multiple of 16 (the
+// paper's 63^3 -> 60^3 layer at batch 1: 160 -> 146 us).  Backward-data keeps shift mode: its source
 // holds 32 channels, 128 bytes per voxel, so each 16-byte lane load touches its
 // own cache line, and taps in K issues twice the loads (measured 195 -> 281 us).
 // CF_F32_TK=0 keeps shift mode everywhere.
@@ -860,6 +862,13 @@ bool f_os_ok(const FParams &p) {
   if (e && e[0] == '0') return false;
   const int jw = (int)p.cls[0].fw.div;
   return p.ncls == 1 && (jw == 16 || jw == 32 || jw == 64);
+}
+// taps in K needs 4 taps along w in one class (any stride, any w extent), and
+// is used on 16-channel sources: with 32 channels, 128 bytes per voxel, every
+// lane's 16-byte load touches its own cache line (the paper's 30^3 -> 27^3
+// layer inside its step: 83 -> 139 us)
+bool f_tk_ok(const ConvShape &s, const FParams &p) {
+  return f_shift_env() != 0 && p.ncls == 1 && s.kw == 4 && p.sc == 16;
 }
 bool f_shift_ok(const ConvShape &s, const FParams &p) {
   if (f_shift_env() == 0) return false;
@@ -884,8 +893,9 @@ double f_cost(FParams &p, const FCfg &c, int fn) {
 // The tile of a linear-layout launch: shift mode (pick -1) for the large
 // stride-1 4-wide layers, else the candidate of least cost.
 template <int FN>
-int f_pick(const ConvShape &s, FParams &p, double *cost) {
-  if (f_shift_ok(s, p) && !getenv("CF_F32_TILE") &&
+int f_pick(const ConvShape &s, FParams &p, double *cost, bool fwd) {
+  const bool four = fwd && f_tk() ? f_tk_ok(s, p) : f_shift_ok(s, p);
+  if (four && !getenv("CF_F32_TILE") &&
       (f_shift_env() == 1 || f_assign(p, 64) * (p.dc / (16 * FN)) >= 4 * kNumCUs)) {
     *cost = 0.0;
     return -1;
@@ -909,7 +919,7 @@ template <bool FWD, int FN, int EPI, bool DYY = false>
 hipError_t launch_lin(const ConvShape &s, FParams &p, const float *src, const float *w, const float *bias, float *dst,
                       uint8_t *mask, hipStream_t st, const float *ysrc = nullptr) {
   double cost;
-  const int pick = f_pick<FN>(s, p, &cost);
+  const int pick = f_pick<FN>(s, p, &cost, FWD);
   if (pick < 0) {
     if constexpr (FWD && !DYY) {
       if (f_tk()) return launch_f<FWD, FN, EPI, 4, 1, 1, 0, false, true>(p, f_assign(p, 64), src, w, bias, dst, mask, st);
@@ -942,7 +952,7 @@ hipError_t launch_lin(const ConvShape &s, FParams &p, const float *src, const fl
 // the small deep layers (a few hundred rows at batch 1) several times more
 // workgroups, each with a share of the columns, instead of a few dozen that
 // leave most compute units idle.  CF_F32_FN=1|2|4 forces a width.
-int f_pick_fn(const ConvShape &s, FParams &p, int fnmax) {
+int f_pick_fn(const ConvShape &s, FParams &p, int fnmax, bool fwd) {
   if (const char *e = getenv("CF_F32_FN")) {
     const int f = atoi(e);
     if ((f == 1 || f == 2 || f == 4) && f <= fnmax && p.dc % (16 * f) == 0) return f;
@@ -952,7 +962,7 @@ int f_pick_fn(const ConvShape &s, FParams &p, int fnmax) {
   for (int f = fnmax; f >= 1; f >>= 1) {
     if (p.dc % (16 * f) != 0) continue;
     double c;
-    const int pick = f == 4 ? f_pick<4>(s, p, &c) : f == 2 ? f_pick<2>(s, p, &c) : f_pick<1>(s, p, &c);
+    const int pick = f == 4 ? f_pick<4>(s, p, &c, fwd) : f == 2 ? f_pick<2>(s, p, &c, fwd) : f_pick<1>(s, p, &c, fwd);
     if (pick < 0) return fnmax;  // shift mode: the large layers keep the widest groups
     if (f == fnmax || c < best) {
       best = c;
@@ -1000,19 +1010,21 @@ hipError_t launch_conv_fwd_f32(const ConvShape &s, const float *x, const float *
     C.fd = make_fastdiv(bd);
     p.pod = s.od / 2; p.poh = s.oh / 2; p.pow_ = s.ow / 2;
     const int tiles = f_assign(p, 1);
-    // taps split eight ways and 16-channel column groups when the bricks alone
-    // leave compute units idle (the stride-2 layer at batch 1)
-    if ((long long)tiles * (s.co / 32) < 2LL * kNumCUs && f_shift_env() != 1)
+    // taps (kernel rows in taps-in-K mode) split eight ways and 16-channel column
+    // groups when the bricks alone leave compute units idle (the stride-2 layer
+    // at batch 1)
+    if ((long long)tiles * (s.co / 32) < 2LL * kNumCUs && f_shift_env() != 1) {
+      if (f_tk() && f_tk_ok(s, p)) return launch_f<true, 1, 2, 4, 1, 8, 0, false, true>(p, tiles, x, w, bias, out, mask, st);
       return launch_f<true, 1, 2, 4, 1, 8>(p, tiles, x, w, bias, out, mask, st);
-    // shift mode: one wave per brick with every tap (measured on the 16 -> 32 layer at
-    // 128^3: 177 -> 168 us against four waves with a quarter of the taps each)
-    if (f_shift_ok(s, p)) {
-      if (f_tk()) return launch_f<true, 2, 2, 4, 1, 1, 0, false, true>(p, tiles, x, w, bias, out, mask, st);
-      return launch_f<true, 2, 2, 4, 1, 1, 4>(p, tiles, x, w, bias, out, mask, st);
     }
+    // taps in K (or shift mode): one wave per brick with every tap (measured on the
+    // 16 -> 32 layer at 128^3, shift mode: 177 -> 168 us against four waves with a
+    // quarter of the taps each)
+    if (f_tk() && f_tk_ok(s, p)) return launch_f<true, 2, 2, 4, 1, 1, 0, false, true>(p, tiles, x, w, bias, out, mask, st);
+    if (f_shift_ok(s, p)) return launch_f<true, 2, 2, 4, 1, 1, 4>(p, tiles, x, w, bias, out, mask, st);
     return launch_f<true, 2, 2, 4, 1, 4>(p, tiles, x, w, bias, out, mask, st);
   }
-  const int fn = f_pick_fn(s, p, s.co % 64 == 0 ? 4 : 2);
+  const int fn = f_pick_fn(s, p, s.co % 64 == 0 ? 4 : 2, true);
   if (epi == 1) {
     if (fn == 4) return launch_lin<true, 4, 1>(s, p, x, w, bias, out, mask, st);
     if (fn == 2) return launch_lin<true, 2, 1>(s, p, x, w, bias, out, mask, st);
@@ -1028,7 +1040,7 @@ hipError_t launch_conv_bwd_data_f32(const ConvShape &s, const float *dz, const f
   FParams p{};
   f_tables(s, false, p);
   p.alpha = alpha;
-  const int fn = f_pick_fn(s, p, s.ci % 64 == 0 ? 4 : (s.ci % 32 == 0 ? 2 : 1));
+  const int fn = f_pick_fn(s, p, s.ci % 64 == 0 ? 4 : (s.ci % 32 == 0 ? 2 : 1), false);
   if (y) {
     if (fn == 4) return launch_lin<false, 4, 0, true>(s, p, dz, w, nullptr, dx, nullptr, st, y);
     if (fn == 2) return launch_lin<false, 2, 0, true>(s, p, dz, w, nullptr, dx, nullptr, st, y);
