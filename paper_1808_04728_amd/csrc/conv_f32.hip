@@ -80,6 +80,7 @@ struct FParams {
   int ncls;
   float alpha;
   int pod, poh, pow_;          // pooled extents (pooled epilogue)
+  int rowtile;                 // output shift: a tile is one destination w row (C.m counts rows of w)
   FClass cls[F_MAX_CLS];
   FTap tap[F_MAX_TAPS];
 };
@@ -177,7 +178,7 @@ __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__r
     tb_h = t1 - t2 * (int)C.fh.div;
     tb_d = t2 - tb_n * (int)C.fd.div;
   } else {
-    if (tile * BM >= C.m) return;
+    if (p.rowtile ? tile >= C.m : tile * BM >= C.m) return;
   }
   const int m0 = tile * BM;
 
@@ -209,6 +210,13 @@ __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__r
       jh = 2 * tb_h + (dh2 & 1);
       jw = tb_w * TWB + seg * 16 + (lrow & 15);
       rok[i] = jd < p.dd && jh < p.dh && jw < p.dw;
+    } else if (p.rowtile) {
+      const int t2 = fdiv(tile, C.fh);
+      n = fdiv(t2, C.fd);
+      jw = lrow;
+      jh = tile - t2 * (int)C.fh.div;
+      jd = t2 - n * (int)C.fd.div;
+      rok[i] = jw < (int)C.fw.div;
     } else {
       const int row = m0 + lrow;
       rok[i] = row < C.m;
@@ -637,7 +645,8 @@ __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__r
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const int row = 16 * i + 4 * g4 + e, jw = row % jwn, sw = jw + C.bq_w - k;
+          const int row = 16 * i + 4 * g4 + e, jw = p.rowtile ? row : row % jwn;
+          const int sw = jw + C.bq_w - k;
           if ((unsigned)sw < (unsigned)jwn) {
 #pragma unroll
             for (int v = 0; v < FN; ++v) acc[i][v][e] += red[(row - jw + sw) * RED_LD + 16 * v + r16];
@@ -683,6 +692,13 @@ __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__r
       oh_ = 2 * tb_h + (dh2 & 1);
       ow_ = tb_w * TWB + seg * 16 + (row & 15);
       valid = od_ < p.dd && oh_ < p.dh && ow_ < p.dw;
+    } else if (p.rowtile) {
+      const int t2 = fdiv(tile, C.fh);
+      n = fdiv(t2, C.fd);
+      valid = row < (int)C.fw.div;
+      ow_ = row * p.ostr_w + C.or_w;
+      oh_ = (tile - t2 * (int)C.fh.div) * p.ostr_h + C.or_h;
+      od_ = (t2 - n * (int)C.fd.div) * p.ostr_d + C.or_d;
     } else {
       const int grow = m0 + row;
       valid = grow < C.m;
@@ -854,14 +870,16 @@ bool f_tk() {
   const char *e = getenv("CF_F32_TK");
   return !(e && e[0] == '0');
 }
-// Output shift replaces shift mode in backward-data where the destination w rows
-// tile the 64-row tiles exactly (w extent 16, 32 or 64).  CF_F32_OS=0 keeps
-// shift mode.
-bool f_os_ok(const FParams &p) {
+// Output shift replaces shift mode in backward-data (16 destination channels)
+// where the destination w rows tile the 64-row tiles exactly (w extent 16, 32
+// or 64), or fill one tile each (other w extents from 33 to 63: a tile per w
+// row, the rows past the extent idle; the paper's 60^3 -> 63^3 backward-data),
+// the source no wider along w.  CF_F32_OS=0 keeps shift mode.
+bool f_os_ok(const ConvShape &s, const FParams &p) {
   const char *e = getenv("CF_F32_OS");
   if (e && e[0] == '0') return false;
   const int jw = (int)p.cls[0].fw.div;
-  return p.ncls == 1 && (jw == 16 || jw == 32 || jw == 64);
+  return f_shift_env() != 0 && p.ncls == 1 && s.kw == 4 && (jw == 16 || (jw >= 32 && jw <= 64)) && p.sw_ <= jw;
 }
 // taps in K needs 4 taps along w in one class (any stride, any w extent), and
 // is used on 16-channel sources: with 32 channels, 128 bytes per voxel, every
@@ -894,7 +912,7 @@ double f_cost(FParams &p, const FCfg &c, int fn) {
 // stride-1 4-wide layers, else the candidate of least cost.
 template <int FN>
 int f_pick(const ConvShape &s, FParams &p, double *cost, bool fwd) {
-  const bool four = fwd && f_tk() ? f_tk_ok(s, p) : f_shift_ok(s, p);
+  const bool four = fwd && f_tk() ? f_tk_ok(s, p) : (!fwd && FN == 1 && f_os_ok(s, p)) || f_shift_ok(s, p);
   if (four && !getenv("CF_F32_TILE") &&
       (f_shift_env() == 1 || f_assign(p, 64) * (p.dc / (16 * FN)) >= 4 * kNumCUs)) {
     *cost = 0.0;
@@ -925,8 +943,15 @@ hipError_t launch_lin(const ConvShape &s, FParams &p, const float *src, const fl
       if (f_tk()) return launch_f<FWD, FN, EPI, 4, 1, 1, 0, false, true>(p, f_assign(p, 64), src, w, bias, dst, mask, st);
     }
     if constexpr (!FWD && !DYY && FN == 1 && EPI == 0) {
-      if (f_os_ok(p))
+      if (f_os_ok(s, p)) {
+        const int jw = (int)p.cls[0].fw.div;
+        if (64 % jw != 0) {  // a tile per destination w row
+          p.rowtile = 1;
+          p.cls[0].m /= (int)p.cls[0].fw.div;
+          return launch_f<FWD, FN, EPI, 4, 1, 1, 0, false, false, true>(p, f_assign(p, 1), src, w, bias, dst, mask, st);
+        }
         return launch_f<FWD, FN, EPI, 4, 1, 1, 0, false, false, true>(p, f_assign(p, 64), src, w, bias, dst, mask, st);
+      }
     }
     return launch_f<FWD, FN, EPI, 4, 1, 1, 4, DYY>(p, f_assign(p, 64), src, w, bias, dst, mask, st, ysrc);
   }

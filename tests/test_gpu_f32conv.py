@@ -129,8 +129,8 @@ def test_f32_pooled_layer_fused(case, ru, monkeypatch):
     assert maxabs_err(to_np(dx), oracle.conv3d_bwd_data(dzr, to_np(w), dhw, stride=s)) <= TOL["f32"]
 
 
-# the four-tap modes (stride-1 4-wide kernels, destination width a multiple of
-# 16): forward, forward + bias + lReLU + mask, pooled forward and backward-data,
+# the four-tap modes (stride-1 4-wide kernels): forward, forward + bias + lReLU
+# + mask, pooled forward and backward-data,
 # each with the default modes ("tk": taps in K forward, output shift backward
 # where the w rows tile), with DPP lane shifts ("dpp") and with neither ("off":
 # one tap per k-step), against the oracle
@@ -140,17 +140,20 @@ SHIFT = [
     (1, (6, 5, 32), 32, 64, 4),
     (1, (8, 6, 16), 16, 32, 4),     # one fragment per row: both edges are padding
     (2, (3, 5, 64), 16, 32, 4),     # whole 64-voxel w rows per tile (output shift)
+    (2, (4, 5, 45), 16, 32, 4),     # a 64-row tile per 45-voxel w row (output shift)
+    (1, (6, 5, 63), 16, 32, 4, "valid"),  # the paper's padding: 60 -> 63 backward-data
 ]
 
 
 @pytest.mark.parametrize("mode", ["tk", "dpp", "off"])
-@pytest.mark.parametrize("case", SHIFT, ids=lambda c: "n%d_%dx%dx%d_c%d-%d_k%d" % (c[0], *c[1], *c[2:]))
+@pytest.mark.parametrize("case", SHIFT, ids=lambda c: "n%d_%dx%dx%d_c%d-%d_k%d" % (c[0], *c[1], *c[2:5]) + "".join(c[5:]))
 def test_f32_shift_mode(case, mode, monkeypatch):
-    N, dhw, CI, CO, k = case
+    N, dhw, CI, CO, k = case[:5]
+    pad = case[5] if len(case) > 5 else "same"
     monkeypatch.setenv("CF_F32_SHIFT", "0" if mode == "off" else "1")
     monkeypatch.setenv("CF_F32_TK", "0" if mode == "dpp" else "1")
     monkeypatch.setenv("CF_F32_OS", "0" if mode == "dpp" else "1")
-    desc = B.make_desc(N, dhw, CI, CO, k, 1, "same", "f32")
+    desc = B.make_desc(N, dhw, CI, CO, k, 1, pad, "f32")
     rng = np.random.default_rng(51)
     x = dev(rng.standard_normal((N, *dhw, CI)), "f32")
     w = dev(rng.standard_normal((k, k, k, CI, CO)) / np.sqrt(k ** 3 * CI), "f32")
@@ -168,7 +171,7 @@ def test_f32_shift_mode(case, mode, monkeypatch):
     dx = torch.full((N, *dhw, CI), float("nan"), device="cuda")
     B.cf_conv3d_bwd_data(desc, dz, w, dx)
     torch.cuda.synchronize()
-    zr = oracle.conv3d_fwd(to_np(x), to_np(w))
+    zr = oracle.conv3d_fwd(to_np(x), to_np(w), pad=pad)
     assert maxabs_err(to_np(z), zr) <= TOL["f32"]
     yr = oracle.bias_lrelu_fwd(zr, bh, 0.2)
     assert maxabs_err(to_np(y), yr) <= TOL["f32"]
@@ -177,7 +180,7 @@ def test_f32_shift_mode(case, mode, monkeypatch):
     bits = np.unpackbits(mask.cpu().numpy(), bitorder="little")[:u.size].astype(bool).reshape(u.shape)
     decided = np.abs(u) > 1e-5 * np.abs(u).max()
     assert np.array_equal(bits[decided], (u > 0)[decided])
-    assert maxabs_err(to_np(dx), oracle.conv3d_bwd_data(to_np(dz), to_np(w), dhw)) <= TOL["f32"]
+    assert maxabs_err(to_np(dx), oracle.conv3d_bwd_data(to_np(dz), to_np(w), dhw, pad=pad)) <= TOL["f32"]
 
 
 # unpooled fp32 layers, backward from (dy, y): N, (D,H,W), CI, CO, k, stride
