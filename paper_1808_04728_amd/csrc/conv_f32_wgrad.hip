@@ -168,7 +168,7 @@ __global__ __launch_bounds__(64 * WV) void wgrad_f32_kernel(const float *__restr
     const bool wrap = c1 == p.nws;
     cws = wrap ? 0 : c1;
     crow += wrap ? 1 : 0;
-    if (wrap) setrow(min(crow, nrow_all - 1));
+    if (__builtin_expect(wrap, 0)) setrow(min(crow, nrow_all - 1));
   };
 
   constexpr int NS = PF + 1;
@@ -385,7 +385,10 @@ __global__ __launch_bounds__(64 * WV) void l1_wgrad_f32_kernel(const float *__re
     L.g0 = __uint_as_float(ld32(gr, gb | ((uint32_t)!(win & (pw0 < p.pow_)) << 31)));
     L.g1 = __uint_as_float(ld32(gr, (gb + 64u) | ((uint32_t)!(win & (pw0 + 1 < p.pow_)) << 31)));
     const uint32_t mb = (uint32_t)(((nn * p.od + od_) * p.oh + oh_) * p.ow + wv0) * 2u;
-    L.mk = ld64f(mr, mb | ((uint32_t)!(live & (wv0 < p.ow)) << 31));
+    // two 4-byte loads: with an output w extent of 2 mod 4 the four voxels' rows
+    // are 4-byte but not 8-byte aligned
+    const uint32_t mbad = (uint32_t)!(live & (wv0 < p.ow)) << 31;
+    L.mk = make_float2(__uint_as_float(ld32(mr, mb | mbad)), __uint_as_float(ld32(mr, (mb + 4u) | mbad)));
   };
 
   f32x4_t acc[KE];
@@ -589,7 +592,7 @@ bool l1f32_wgrad_supported(const ConvShape &s) {
   const long long xin = (long long)s.n * s.d * s.h * s.w, vout = (long long)s.n * s.od * s.oh * s.ow;
   return s.dtype == DT_F32 && s.ci == 1 && s.co == 16 && s.sd == 1 && s.sh == 1 && s.sw == 1 && s.kd == s.kh &&
          s.kd == s.kw && (s.kd == 2 || s.kd == 3) && s.pw <= 1 && s.kd - s.pw <= 3 && s.w % 4 == 0 &&
-         s.ow % 4 == 0 && s.od >= 2 && s.oh >= 2 && xin * 4 < (1LL << 31) && vout * 64 < (1LL << 31);
+         s.ow % 2 == 0 && s.od >= 2 && s.oh >= 2 && xin * 4 < (1LL << 31) && vout * 64 < (1LL << 31);
 }
 
 size_t l1f32_wgrad_workspace(const ConvShape &s) {
