@@ -132,42 +132,71 @@ __global__ __launch_bounds__(64 * WV) void wgrad_f32_kernel(const float *__restr
   }
 
   // ---- the slice's output rows (n, od, oh), four voxels along w per step -----
-  // Row-dependent values are uniform and change once per row; a step only adds
-  // its w offset.  Steps past the slice (ring padding) load zeros.
+  // The load cursor is kept per lane: the output w of the lane's K slot, per
+  // unit the w and element offset of its x value, the gradient's offset (and,
+  // pooled, its pooled w and the mask word).  It is set at the start of every
+  // output row, under a uniform branch marked unlikely, and advanced by
+  // additions between: computed per step, the offsets cost about 35 vector
+  // instructions (four of them quarter-rate multiplies) per 16 MFMAs, and the
+  // vector ALU does not run beside the MFMAs.  Steps past the slice (ring
+  // padding) load zeros.
   const int nrow_all = p.n * p.od * p.oh;
   const int r0 = slice * p.rows_per, r1 = min(r0 + p.rows_per, nrow_all);
   const int nsteps = r1 > r0 ? (r1 - r0) * p.nws : 0;
-  int crow = r0, cws = 0, ldstep = 0;  // load cursor
-  int xrow[RU], rowvox = 0, prow = 0;
+  int crow = r0, cws = 0, ldstep = 0;  // load cursor (uniform)
+  int cw = 0, cv = 0, cg = 0, cm = 0, cpw = 0;
+  int cxw[RU], cxo[RU];
   bool dok[RU], winrow = false;
-  auto setrow = [&](int row) {
+  (void)cm;
+  (void)cpw;
+  // always inlined: called at two sites, an outlined copy would keep the
+  // captured per-lane arrays in scratch memory
+  auto setrow = [&](int row) __attribute__((always_inline)) {
     const int t1 = fdiv(row, p.fh), nn = fdiv(t1, p.fd);
     const int oh_ = row - t1 * (int)p.fh.div, od_ = t1 - nn * (int)p.fd.div;
     const int bd = od_ * p.sd - p.pd, bh = oh_ * p.sh - p.ph;
+    cw = g4;
+    const int bw = g4 * p.sw - p.pw;
 #pragma unroll
     for (int i = 0; i < RU; ++i) {
       dok[i] = uok[i] & ((unsigned)(bd + tkd[i]) < (unsigned)p.d) & ((unsigned)(bh + tkh[i]) < (unsigned)p.h);
-      xrow[i] = ((nn * p.d + bd + tkd[i]) * p.h + bh + tkh[i]) * p.w;
+      cxw[i] = bw + tkw[i];
+      cxo[i] = (((nn * p.d + bd + tkd[i]) * p.h + bh + tkh[i]) * p.w + cxw[i]) * p.ci + toff[i];
     }
-    rowvox = row * p.ow;
+    cv = row * p.ow + g4;
     if constexpr (GM == GM_POOL_MASK) {
       const int pd_ = od_ >> 1, ph_ = oh_ >> 1;
       winrow = (pd_ < p.pod) & (ph_ < p.poh);
-      prow = ((nn * p.pod + pd_) * p.poh + ph_) * p.pow_;
+      cpw = g4 >> 1;
+      cg = (((nn * p.pod + pd_) * p.poh + ph_) * p.pow_ + cpw) * p.co + co0 + r16;
+      cm = cv * (p.co >> 5) + (co0 >> 5);
+    } else {
+      cg = cv * p.co + co0 + r16;
     }
   };
   if (nsteps > 0) setrow(r0);
-  // The row values change once per row: they are recomputed under a uniform
-  // branch when the cursor wraps (every step, as scalar selects, their ~60
-  // scalar instructions per step cost the 16 -> 32 layer's launch at two waves
-  // per SIMD 219 -> 195 us with its sums)
+  // per-step advances: 4 output voxels along w
+  const int dxw = 4 * p.sw, dxo = 4 * p.sw * p.ci;
+  const int dg = (GM == GM_POOL_MASK ? 2 : 4) * p.co, dm = 4 * (p.co >> 5);
   auto next = [&]() {
     ++ldstep;
-    const int adv = ldstep < nsteps ? 1 : 0;
-    const int c1 = cws + adv;
+    const bool adv = ldstep < nsteps;
+    const int c1 = cws + (adv ? 1 : 0);
     const bool wrap = c1 == p.nws;
     cws = wrap ? 0 : c1;
     crow += wrap ? 1 : 0;
+    cw += adv ? 4 : 0;
+    cv += adv ? 4 : 0;
+#pragma unroll
+    for (int i = 0; i < RU; ++i) {
+      cxw[i] += adv ? dxw : 0;
+      cxo[i] += adv ? dxo : 0;
+    }
+    cg += adv ? dg : 0;
+    if constexpr (GM == GM_POOL_MASK) {
+      cpw += adv ? 2 : 0;
+      cm += adv ? dm : 0;
+    }
     if (__builtin_expect(wrap, 0)) setrow(min(crow, nrow_all - 1));
   };
 
@@ -182,33 +211,26 @@ __global__ __launch_bounds__(64 * WV) void wgrad_f32_kernel(const float *__restr
   (void)v_r;
 
   auto load = [&](u32x4_t(&a)[RU], float(&b)[FN], uint32_t &mw, float(&yv)[FN], int &vx) {
-    const int w = 4 * cws + g4;
-    const bool wok = (ldstep < nsteps) & (w < p.ow);
-    const int bw = w * p.sw - p.pw;
+    const bool wok = (ldstep < nsteps) & (cw < p.ow);
 #pragma unroll
     for (int i = 0; i < RU; ++i) {
-      const int xw = bw + tkw[i];
       // bitwise, not short-circuit: one select per load, no branch
-      const bool ok = dok[i] & wok & ((unsigned)xw < (unsigned)p.w);
+      const bool ok = dok[i] & wok & ((unsigned)cxw[i] < (unsigned)p.w);
       // a valid byte offset is below 2^31: bit 31 sends the load past the buffer (zeros)
-      a[i] = ld128(xr, ((uint32_t)((xrow[i] + xw) * p.ci + toff[i]) * 4u) | ((uint32_t)!ok << 31));
+      a[i] = ld128(xr, ((uint32_t)cxo[i] * 4u) | ((uint32_t)!ok << 31));
     }
-    const int v = rowvox + w;
-    vx = wok ? v : -1;
+    vx = wok ? cv : -1;
     if constexpr (GM == GM_POOL_MASK) {
-      const int pw_ = w >> 1;
-      const bool win = winrow & wok & (pw_ < p.pow_);
-      const int gb = (prow + pw_) * p.co + co0 + r16;
+      const bool win = winrow & wok & (cpw < p.pow_);
 #pragma unroll
       for (int j = 0; j < FN; ++j)
-        b[j] = __uint_as_float(ld32(gr, ((uint32_t)(gb + 16 * j) * 4u) | ((uint32_t)!win << 31)));
+        b[j] = __uint_as_float(ld32(gr, ((uint32_t)(cg + 16 * j) * 4u) | ((uint32_t)!win << 31)));
       // the workgroup's 32 channels of voxel v are one mask word
-      mw = ld32(mr, ((uint32_t)(v * (p.co >> 5) + (co0 >> 5)) * 4u) | ((uint32_t)!wok << 31));
+      mw = ld32(mr, ((uint32_t)cm * 4u) | ((uint32_t)!wok << 31));
     } else {
-      const int gb = v * p.co + co0 + r16;
 #pragma unroll
       for (int j = 0; j < FN; ++j) {
-        const uint32_t off = ((uint32_t)(gb + 16 * j) * 4u) | ((uint32_t)!wok << 31);
+        const uint32_t off = ((uint32_t)(cg + 16 * j) * 4u) | ((uint32_t)!wok << 31);
         b[j] = __uint_as_float(ld32(gr, off));
         if constexpr (GM == GM_DY_Y) yv[j] = __uint_as_float(ld32(mr, off));  // y: the layout of dy
       }
