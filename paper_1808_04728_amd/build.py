@@ -34,6 +34,7 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
 # 120 accvgpr moves in the 16 -> 32 forward's loop, none in VGPR form).
 EXTRA = {
     "conv_smallc.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+    "conv_smallc_pair.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
     "conv_f32.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
     "conv_f32_wgrad.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
 }

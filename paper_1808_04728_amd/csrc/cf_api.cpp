@@ -510,7 +510,9 @@ cf_status cf_conv3d_fwd_fused(const cf_conv3d_desc *desc, const void *x, const v
     return fail(CF_ERR_ALIAS, "conv3d_fwd_fused: an output overlaps an input");
   hipStream_t st = (hipStream_t)stream;
   hipError_t e;
-  if (pool && cf::smallc_supported(s, true))
+  if (pool && cf::l1pair_supported(s))
+    e = cf::launch_l1pair_fwd(s, x, w, bias, alpha, out, (uint16_t *)mask, st);
+  else if (pool && cf::smallc_supported(s, true))
     e = cf::launch_conv_fwd_smallc(s, x, w, bias, alpha, out, (uint16_t *)mask, true, st);
   else if (cf::f32conv_supported(s, true) && !cf::c16_fwd_supported(s))
     e = cf::launch_conv_fwd_f32(s, (const float *)x, (const float *)w, bias, alpha, (float *)out, (uint8_t *)mask,

@@ -67,6 +67,11 @@ hipError_t launch_conv_fwd_c16(const ConvShape &s, const void *x, const void *w,
 bool smallc_supported(const ConvShape &s, bool fused);
 hipError_t launch_conv_fwd_smallc(const ConvShape &s, const void *x, const void *w, const float *bias,
                                   float alpha, void *out, uint16_t *mask, bool fused, hipStream_t st);
+// bf16 first layer (1 -> 16 channels, 3^3, stride 1) with the pooled epilogue,
+// even output extents: voxel-pair windows, conv_smallc_pair.hip.
+bool l1pair_supported(const ConvShape &s);
+hipError_t launch_l1pair_fwd(const ConvShape &s, const void *x, const void *w, const float *bias, float alpha,
+                             void *out, uint16_t *mask, hipStream_t st);
 bool smallc_wgrad_fused_supported(const ConvShape &s);
 size_t smallc_wgrad_fused_workspace(const ConvShape &s);
 // the same layer unfused (dz given), bf16, one input channel, 16 outputs: partials in ws

@@ -103,6 +103,45 @@ def test_fused_fwd(case, dt):
     assert decided.mean() > 0.99
 
 
+# bf16 first layer with even output extents runs on the voxel-pair kernel:
+# SAME and VALID leading pads, widths that end inside a 16-voxel segment, two
+# 128-wide w tiles, partial d and h tiles, and alpha 0.2
+PAIR_CASES = [
+    (1, (8, 8, 128), "valid", 0.01),    # out (6, 6, 126): the paper's first-layer width
+    (1, (6, 10, 136), "same", 0.2),     # out (6, 10, 136): a second w tile 8 voxels wide
+    (2, (12, 6, 24), "valid", 0.01),    # out (10, 4, 22)
+    (1, (4, 4, 8), "same", 0.01),       # one 8-voxel segment
+    (1, (10, 18, 64), "same", 0.01),    # h tiles 8 + 8 + 2, d tiles 4 + 4 + 2
+]
+
+
+@pytest.mark.parametrize("case", PAIR_CASES, ids=lambda c: "n%d_%dx%dx%d_%s_a%g" % (c[0], *c[1], c[2], c[3]))
+def test_fused_fwd_first_layer_pairs(case):
+    N, dhw, pad, alpha = case
+    dt = "bf16"
+    desc = B.make_desc(N, dhw, 1, 16, 3, 1, pad, dt)
+    assert B.cf_conv3d_fused_supported(desc) & B.FUSED_FWD
+    rng = np.random.default_rng(17)
+    x = dev(np.log1p(rng.poisson(np.exp(rng.standard_normal((N, *dhw, 1))))), dt)  # many exact zeros
+    w = dev(rng.standard_normal((3, 3, 3, 1, 16)) * np.sqrt(2.0 / 27), dt)
+    b = torch.as_tensor(rng.standard_normal(16) * 0.1, dtype=torch.float32, device="cuda")
+    od = B.cf_conv3d_out_shape(desc)
+    assert all(t % 2 == 0 for t in od)
+    out = torch.full((N,) + tuple(t // 2 for t in od) + (16,), float("nan"), dtype=tdtype(dt), device="cuda")
+    mask = torch.zeros(B.cf_conv3d_mask_bytes(desc), dtype=torch.uint8, device="cuda")
+    B.cf_conv3d_fwd_fused(desc, x, w, b, alpha, B.CF_FUSE_POOL2, out, mask)
+    torch.cuda.synchronize()
+    z = oracle.conv3d_fwd(to_np(x), to_np(w), pad=pad)
+    u = z + to_np(b)
+    p = oracle.avgpool3d_fwd(oracle.bias_lrelu_fwd(z, to_np(b), alpha))
+    e = maxabs_err(to_np(out), p)
+    assert e <= TOL[dt], e
+    bits = unpack_mask(mask, u.size).reshape(u.shape)
+    decided = np.abs(u) > 1e-5 * np.abs(u).max()
+    assert np.array_equal(bits[decided], (u > 0)[decided])
+    assert decided.mean() > 0.99
+
+
 # more tiles than the persistent kernels start workgroups: every workgroup loops
 # over several tiles, the next tile's halo arriving during the current tile's MFMAs
 MULTI_CASES = [
