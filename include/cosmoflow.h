@@ -274,6 +274,21 @@ cf_status cf_conv3d_bwd_data_fused(const cf_conv3d_desc *desc, const void *g, co
                                    const void *w, float alpha, uint32_t flags, void *dx,
                                    void *stream);
 
+/* Fused backward of a layer in one call (Section III-A: leaky ReLU follows
+ * every convolution; Section III-C: the weight- and data-gradient operators of
+ * the same layer read the same dz): dW and db exactly as
+ * cf_conv3d_bwd_weight_fused and dx exactly as cf_conv3d_bwd_data_fused, with
+ * the same arguments (bitwise the same results).  Where both products are
+ * small (the stack's unpooled deep layers in fp32) one launch runs them side
+ * by side; otherwise the two calls run in sequence.  ws: the
+ * cf_conv3d_bwd_weight_fused_workspace_size bytes; dx must not overlap dW, db
+ * or ws (CF_ERR_ALIAS).  Supported wherever both fused calls are (bits 2 and 4
+ * of cf_conv3d_fused_supported). */
+cf_status cf_conv3d_bwd_fused(const cf_conv3d_desc *desc, const void *x, const void *g,
+                              const void *mask, const void *w, float alpha, uint32_t flags,
+                              float *dw, float *db, void *dx, void *ws, size_t ws_bytes,
+                              void *stream);
+
 /* ------------------------------------------------------------------------
  * Deferred gradient sums.  Every weight- and bias-gradient entry point ends
  * with fixed-order column sums of per-workgroup fp32 partials held in its
@@ -333,6 +348,14 @@ cf_status cf_conv3d_bwd_weight_fused_deferred(const cf_conv3d_desc *desc, const 
                                               uint32_t flags, float *dw, float *db, void *dz,
                                               void *ws, size_t ws_bytes, cf_reduction *pending,
                                               int32_t *npending, void *stream);
+
+/* cf_conv3d_bwd_fused without the final sums of dW and db (dx is written by
+ * this call).  pending / npending as above. */
+cf_status cf_conv3d_bwd_fused_deferred(const cf_conv3d_desc *desc, const void *x, const void *g,
+                                       const void *mask, const void *w, float alpha,
+                                       uint32_t flags, float *dw, float *db, void *dx, void *ws,
+                                       size_t ws_bytes, cf_reduction *pending, int32_t *npending,
+                                       void *stream);
 
 /* ------------------------------------------------------------------------
  * Parameter update (Section III-B, "SGD Optimizer").  Per parameter group l

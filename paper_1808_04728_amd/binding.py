@@ -39,7 +39,7 @@ EXPORTS = [
     "cf_conv3d_bwd_weight_fused_deferred", "cf_adam_larc_workspace_size", "cf_adam_larc_step",
     "cf_fc_fwd_workspace_size", "cf_fc_fwd", "cf_fc_bwd_data", "cf_fc_bwd_weight", "cf_mse_loss",
     "cf_conv3d_bwd_weight_noalloc", "cf_avgpool3d_lrelu_bwd_workspace_size", "cf_avgpool3d_lrelu_bwd",
-    "cf_avgpool3d_lrelu_bwd_deferred",
+    "cf_avgpool3d_lrelu_bwd_deferred", "cf_conv3d_bwd_fused", "cf_conv3d_bwd_fused_deferred",
 ]
 
 
@@ -121,6 +121,9 @@ def lib():
         "cf_conv3d_bwd_weight_fused_dz": ([D, vp, vp, vp, f32, ctypes.c_uint32, vp, vp, vp, vp, sz, vp],
                                           ctypes.c_int),
         "cf_conv3d_bwd_data_fused": ([D, vp, vp, vp, f32, ctypes.c_uint32, vp, vp], ctypes.c_int),
+        "cf_conv3d_bwd_fused": ([D, vp, vp, vp, vp, f32, ctypes.c_uint32, vp, vp, vp, vp, sz, vp], ctypes.c_int),
+        "cf_conv3d_bwd_fused_deferred": ([D, vp, vp, vp, vp, f32, ctypes.c_uint32, vp, vp, vp, vp, sz,
+                                          ctypes.POINTER(cf_reduction), ctypes.POINTER(i32), vp], ctypes.c_int),
         "cf_reduce_partials": ([i32, ctypes.POINTER(cf_reduction), vp], ctypes.c_int),
         "cf_conv3d_bwd_weight_deferred": ([D, vp, vp, vp, vp, sz, ctypes.POINTER(cf_reduction),
                                            ctypes.POINTER(i32), vp], ctypes.c_int),
@@ -295,6 +298,13 @@ def cf_conv3d_bwd_data_fused(desc, g, mask, w, alpha, flags, dx, stream=None):
                                           _stream(stream)))
 
 
+def cf_conv3d_bwd_fused(desc, x, g, mask, w, alpha, flags, dw, db, dx, ws, ws_bytes=None, stream=None):
+    if ws_bytes is None:
+        ws_bytes = 0 if ws is None or isinstance(ws, int) else ws.numel() * ws.element_size()
+    _check(lib().cf_conv3d_bwd_fused(ctypes.byref(desc), _ptr(x), _ptr(g), _ptr(mask), _ptr(w), alpha, flags,
+                                     _ptr(dw), _ptr(db), _ptr(dx), _ptr(ws), ws_bytes, _stream(stream)))
+
+
 # ---- deferred gradient sums --------------------------------------------------
 # The _deferred calls return a list of pending cf_reduction jobs (host
 # structures holding device pointers); cf_reduce_partials runs any collection
@@ -347,6 +357,16 @@ def cf_conv3d_bwd_weight_fused_deferred(desc, x, g, mask, alpha, flags, dw, db, 
     _check(lib().cf_conv3d_bwd_weight_fused_deferred(ctypes.byref(desc), _ptr(x), _ptr(g), _ptr(mask), alpha, flags,
                                                      _ptr(dw), _ptr(db), _ptr(dz), _ptr(ws), ws_bytes, arr,
                                                      ctypes.byref(n), _stream(stream)))
+    return _pending_list(arr, n)
+
+
+def cf_conv3d_bwd_fused_deferred(desc, x, g, mask, w, alpha, flags, dw, db, dx, ws, ws_bytes=None, stream=None):
+    if ws_bytes is None:
+        ws_bytes = 0 if ws is None or isinstance(ws, int) else ws.numel() * ws.element_size()
+    arr, n = (cf_reduction * CF_MAX_PENDING)(), ctypes.c_int32(0)
+    _check(lib().cf_conv3d_bwd_fused_deferred(ctypes.byref(desc), _ptr(x), _ptr(g), _ptr(mask), _ptr(w), alpha,
+                                              flags, _ptr(dw), _ptr(db), _ptr(dx), _ptr(ws), ws_bytes, arr,
+                                              ctypes.byref(n), _stream(stream)))
     return _pending_list(arr, n)
 
 

@@ -536,9 +536,10 @@ size_t cf_conv3d_bwd_weight_fused_workspace_size(const cf_conv3d_desc *desc, uin
   return fused_wgrad_workspace(s, flags);
 }
 
+// check_only: validate every argument and return without launching
 static cf_status bwd_weight_fused(const char *name, const cf_conv3d_desc *desc, const void *x, const void *g,
                                   const void *mask, float alpha, uint32_t flags, float *dw, float *db, void *dz,
-                                  void *ws, size_t ws_bytes, void *stream) {
+                                  void *ws, size_t ws_bytes, void *stream, bool check_only = false) {
   cf::ConvShape s;
   cf_status r = resolve(desc, &s);
   if (r != CF_OK) return r;
@@ -551,6 +552,7 @@ static cf_status bwd_weight_fused(const char *name, const cf_conv3d_desc *desc, 
   const size_t dw_bytes = (size_t)s.kd * s.kh * s.kw * s.ci * s.co * sizeof(float);
   if (s.n == 0) {
     if ((r = check_ptrs({dw, db})) != CF_OK) return r;
+    if (check_only) return CF_OK;
     hipError_t e = cf::launch_fill_zero(dw, (long long)(dw_bytes / 4), st);
     if (e == hipSuccess) e = cf::launch_fill_zero(db, s.co, st);
     return finish(e, st, name);
@@ -573,6 +575,7 @@ static cf_status bwd_weight_fused(const char *name, const cf_conv3d_desc *desc, 
     return fail(CF_ERR_ALIAS, std::string(name) + ": outputs / workspace overlap");
   if (dz && (overlap(dz, b.z, dw, dw_bytes) || overlap(dz, b.z, db, dbb) || overlap(dz, b.z, ws, need)))
     return fail(CF_ERR_ALIAS, std::string(name) + ": dz overlaps another output or the workspace");
+  if (check_only) return CF_OK;
   hipError_t e;
   const bool deep16 = s.dtype == cf::DT_BF16 && cf::direct_wgrad_supported(s);
   if (!pool && deep16)
@@ -607,8 +610,8 @@ cf_status cf_conv3d_bwd_weight_fused_dz(const cf_conv3d_desc *desc, const void *
                           ws_bytes, stream);
 }
 
-cf_status cf_conv3d_bwd_data_fused(const cf_conv3d_desc *desc, const void *g, const void *mask, const void *w,
-                                   float alpha, uint32_t flags, void *dx, void *stream) {
+static cf_status bwd_data_fused(const cf_conv3d_desc *desc, const void *g, const void *mask, const void *w,
+                                float alpha, uint32_t flags, void *dx, void *stream, bool check_only) {
   cf::ConvShape s;
   cf_status r = resolve(desc, &s);
   if (r != CF_OK) return r;
@@ -623,6 +626,7 @@ cf_status cf_conv3d_bwd_data_fused(const cf_conv3d_desc *desc, const void *g, co
   const size_t gb = pool ? pooled_bytes(s) : b.z, mb = pool ? mask_bytes(s) : b.z;
   if (overlap(dx, b.x, g, gb) || overlap(dx, b.x, mask, mb) || overlap(dx, b.x, w, b.w))
     return fail(CF_ERR_ALIAS, "conv3d_bwd_data_fused: dx overlaps an input");
+  if (check_only) return CF_OK;
   hipStream_t st = (hipStream_t)stream;
   hipError_t e;
   if (pool && cf::c16_bwd_supported(s))
@@ -633,6 +637,39 @@ cf_status cf_conv3d_bwd_data_fused(const cf_conv3d_desc *desc, const void *g, co
     e = cf::launch_conv_bwd_data_f32(s, (const float *)g, (const float *)w, (float *)dx, st, (const float *)mask,
                                      alpha);
   return finish(e, st, "cf_conv3d_bwd_data_fused");
+}
+
+cf_status cf_conv3d_bwd_data_fused(const cf_conv3d_desc *desc, const void *g, const void *mask, const void *w,
+                                   float alpha, uint32_t flags, void *dx, void *stream) {
+  return bwd_data_fused(desc, g, mask, w, alpha, flags, dx, stream, false);
+}
+
+cf_status cf_conv3d_bwd_fused(const cf_conv3d_desc *desc, const void *x, const void *g, const void *mask,
+                              const void *w, float alpha, uint32_t flags, float *dw, float *db, void *dx, void *ws,
+                              size_t ws_bytes, void *stream) {
+  const char *name = "cf_conv3d_bwd_fused";
+  cf_status r = bwd_weight_fused(name, desc, x, g, mask, alpha, flags, dw, db, nullptr, ws, ws_bytes, stream, true);
+  if (r != CF_OK) return r;
+  if ((r = bwd_data_fused(desc, g, mask, w, alpha, flags, dx, stream, true)) != CF_OK) return r;
+  cf::ConvShape s;
+  resolve(desc, &s);
+  if (s.n > 0) {
+    const size_t dxb = conv_bytes(s).x, dwb = (size_t)s.kd * s.kh * s.kw * s.ci * s.co * sizeof(float);
+    if (overlap(dx, dxb, dw, dwb) || overlap(dx, dxb, db, (size_t)s.co * 4) ||
+        overlap(dx, dxb, ws, fused_wgrad_workspace(s, flags)))
+      return fail(CF_ERR_ALIAS, "cf_conv3d_bwd_fused: dx overlaps dW, db or the workspace");
+  }
+  // fp32 unpooled layers: both products from (dy, y) in one launch where the
+  // kernels allow; everything else is the two calls in sequence
+  if (s.n > 0 && s.dtype == cf::DT_F32 && !(flags & CF_FUSE_POOL2)) {
+    hipStream_t st = (hipStream_t)stream;
+    return finish(cf::launch_conv_bwd_fused_f32(s, (const float *)x, (const float *)g, (const float *)mask,
+                                                (const float *)w, alpha, dw, db, (float *)dx, ws, st),
+                  st, name);
+  }
+  if ((r = bwd_weight_fused(name, desc, x, g, mask, alpha, flags, dw, db, nullptr, ws, ws_bytes, stream)) != CF_OK)
+    return r;
+  return bwd_data_fused(desc, g, mask, w, alpha, flags, dx, stream, false);
 }
 
 // ---------------------------------------------------------------------------
@@ -691,6 +728,15 @@ cf_status cf_conv3d_bwd_weight_fused_deferred(const cf_conv3d_desc *desc, const 
   return deferred(pending, npending, [&] {
     return bwd_weight_fused(dz ? "cf_conv3d_bwd_weight_fused_dz" : "cf_conv3d_bwd_weight_fused", desc, x, g, mask,
                             alpha, flags, dw, db, dz, ws, ws_bytes, stream);
+  });
+}
+
+cf_status cf_conv3d_bwd_fused_deferred(const cf_conv3d_desc *desc, const void *x, const void *g, const void *mask,
+                                       const void *w, float alpha, uint32_t flags, float *dw, float *db, void *dx,
+                                       void *ws, size_t ws_bytes, cf_reduction *pending, int32_t *npending,
+                                       void *stream) {
+  return deferred(pending, npending, [&] {
+    return cf_conv3d_bwd_fused(desc, x, g, mask, w, alpha, flags, dw, db, dx, ws, ws_bytes, stream);
   });
 }
 

@@ -134,6 +134,12 @@ hipError_t launch_l1_wgrad_f32(const ConvShape &s, const float *x, const float *
 bool f32wgrad_fused_supported(const ConvShape &s);
 // gm: 0 g = dz; 1 g = pooled gradient, aux = slope mask; 3 g = dy, aux = the activation y
 size_t f32wgrad_workspace(const ConvShape &s, int gm);
+// fp32 backward of an unpooled fused layer (dz = dy * slope(y)): dW, db and dx
+// in one launch where the planners pick the instantiated tile shapes, else the
+// two launches in sequence; workspace as the (dy, y) weight gradient's.
+hipError_t launch_conv_bwd_fused_f32(const ConvShape &s, const float *x, const float *dy, const float *y,
+                                     const float *w, float alpha, float *dw, float *db, float *dx, void *ws,
+                                     hipStream_t st);
 hipError_t launch_conv_bwd_weight_f32(const ConvShape &s, const float *x, const float *g, const void *aux,
                                       float alpha, float *dw, float *db, void *ws, int gm, float *dz_out,
                                       hipStream_t st);

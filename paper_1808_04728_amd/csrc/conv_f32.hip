@@ -40,6 +40,7 @@
 
 #include "cf_common.h"
 #include "cf_kernels.h"
+#include "conv_f32_wgrad_kernel.h"
 #include "fastdiv.h"
 
 #include <algorithm>
@@ -139,14 +140,15 @@ __device__ __forceinline__ uint32_t shift_lane(uint32_t a, uint32_t e) {
 // holds P_uw[p] = sum over kernel rows and channels of dz[p] W[uw] for the
 // source voxels p of the tile's own rows, unshifted; the epilogue adds
 // P_uw[w + pw - uw] into dx[w].  One load per fragment and k-step, no lane moves.
+//
+// The kernel body runs as the workgroup of grid position (bx, by): the
+// launch's own grid, or a share of the combined backward launch below.
 template <bool FWD, int FM, int FN, int WM, int WK, int PF, int EPI, int UW = 0, bool DYY = false, bool TK = false,
           bool OS = false>
-__global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__restrict__ src,
-                                                                const float *__restrict__ ysrc,
-                                                                const float *__restrict__ wt,
-                                                                const float *__restrict__ bias,
-                                                                float *__restrict__ dst, uint8_t *__restrict__ mask,
-                                                                const FParams p) {
+__device__ __forceinline__ void conv_f32_body(const float *__restrict__ src, const float *__restrict__ ysrc,
+                                              const float *__restrict__ wt, const float *__restrict__ bias,
+                                              float *__restrict__ dst, uint8_t *__restrict__ mask, const FParams p,
+                                              int bx, int by) {
   constexpr int BM = 16 * FM * WM;           // rows of a tile
   constexpr int BN = 16 * FN;                // columns of a tile
   constexpr int RED_LD = BN + 4;             // fp32 row pitch of the reduction tile
@@ -163,12 +165,12 @@ __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__r
   const int g4 = lane >> 4, r16 = lane & 15;
 
   // ---- class and tile of this workgroup (uniform), XCD-major --------------
-  const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+  const int xcd = bx & 7, slot = bx >> 3;
   int c = 0;
   while (c + 1 < p.ncls && slot >= p.cls[c + 1].slot0) ++c;
   const FClass &C = p.cls[c];
   const int tile = xcd * C.per + slot - C.slot0;
-  const int n0 = blockIdx.y * BN;
+  const int n0 = by * BN;
   int tb_n = 0, tb_d = 0, tb_h = 0, tb_w = 0;  // brick: sample, d pair, h pair, w tile
   if constexpr (BRICK) {
     if (tile >= C.m) return;
@@ -762,6 +764,18 @@ __global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__r
   }
 }
 
+template <bool FWD, int FM, int FN, int WM, int WK, int PF, int EPI, int UW = 0, bool DYY = false, bool TK = false,
+          bool OS = false>
+__global__ __launch_bounds__(64 * WM * WK) void conv_f32_kernel(const float *__restrict__ src,
+                                                                const float *__restrict__ ysrc,
+                                                                const float *__restrict__ wt,
+                                                                const float *__restrict__ bias,
+                                                                float *__restrict__ dst, uint8_t *__restrict__ mask,
+                                                                const FParams p) {
+  conv_f32_body<FWD, FM, FN, WM, WK, PF, EPI, UW, DYY, TK, OS>(src, ysrc, wt, bias, dst, mask, p, blockIdx.x,
+                                                               blockIdx.y);
+}
+
 // Class and tap tables (forward: one class; backward-data: s^3 parity classes).
 void f_tables(const ConvShape &s, bool fwd, FParams &p) {
   const int S[3] = {s.sd, s.sh, s.sw}, P[3] = {s.pd, s.ph, s.pw}, K[3] = {s.kd, s.kh, s.kw};
@@ -1058,6 +1072,90 @@ hipError_t launch_conv_fwd_f32(const ConvShape &s, const float *x, const float *
   if (fn == 4) return launch_lin<true, 4, 0>(s, p, x, w, nullptr, out, nullptr, st);
   if (fn == 2) return launch_lin<true, 2, 0>(s, p, x, w, nullptr, out, nullptr, st);
   return launch_lin<true, 1, 0>(s, p, x, w, nullptr, out, nullptr, st);
+}
+
+namespace {
+
+// ---------------------------------------------------------------------------
+// Backward of an unpooled fused layer in one launch, dz = dy * slope(y) formed
+// inside both products: the weight-gradient workgroups (its grid gx x gy x
+// nsplit, flattened, first) and the backward-data workgroups (tiles x column
+// groups, from an offset rounded up to a multiple of 8 so that their XCD-major
+// tile order keeps its XCDs) share one grid.  The stack's deep layers run
+// both kernels with a few hundred latency-bound workgroups each; side by side
+// they share the machine that either leaves mostly idle, with no second queue
+// to synchronise.  One tile shape per side is instantiated: the one the
+// launch planners pick for the deep layers (backward-data 16-row tiles, one
+// 16-column group, K split over 8 waves; weight gradient one 64-channel row
+// unit per wave), the weight gradient with two column groups.
+// ---------------------------------------------------------------------------
+constexpr int PAIR_PICK = 6;  // kCand[6] = {fm 1, wm 1, wk 8}
+static_assert(kCand[PAIR_PICK].fm == 1 && kCand[PAIR_PICK].wm == 1 && kCand[PAIR_PICK].wk == 8, "pair tile");
+
+__global__ __launch_bounds__(512, 4) void bwd_pair_f32_kernel(const float *__restrict__ x, const float *__restrict__ dy,
+                                                           const float *__restrict__ y, const float *__restrict__ w,
+                                                           float *__restrict__ dx, float *__restrict__ part_w,
+                                                           float *__restrict__ part_b, const FParams fp,
+                                                           const WF32Params wp, int wgx, int wgy, int nw, int dbase,
+                                                           int dtiles) {
+  const int b = blockIdx.x;
+  if (b < nw) {
+    const int t = b / wgx;
+    wgrad_f32_body<GM_DY_Y, false, 1, 2, 8, 2>(x, dy, y, part_w, part_b, nullptr, wp, b - t * wgx, t % wgy, t / wgy);
+  } else if (b >= dbase) {
+    const int j = b - dbase;
+    conv_f32_body<false, 1, 1, 1, 8, 2, 0, 0, true>(dy, y, w, nullptr, dx, nullptr, fp, j % dtiles, j / dtiles);
+  }
+}
+
+// CF_F32_PAIR=0 runs the two products as separate launches
+bool pair_env() {
+  const char *e = getenv("CF_F32_PAIR");
+  return !(e && e[0] == '0');
+}
+
+}  // namespace
+
+hipError_t launch_conv_bwd_fused_f32(const ConvShape &s, const float *x, const float *dy, const float *y,
+                                     const float *w, float alpha, float *dw, float *db, float *dx, void *ws,
+                                     hipStream_t st) {
+  // the backward-data plan, as launch_conv_bwd_data_f32 makes it
+  FParams fp{};
+  f_tables(s, false, fp);
+  fp.alpha = alpha;
+  const int fn = f_pick_fn(s, fp, s.ci % 64 == 0 ? 4 : (s.ci % 32 == 0 ? 2 : 1), false);
+  double cost = 0.0;
+  const int pick = fn == 1 ? f_pick<1>(s, fp, &cost, false) : -1;
+  const WPlan wpl = f32w_plan(s, GM_DY_Y);
+  // the weight gradient runs with two column groups per workgroup (its slices
+  // as planned: every partial is the one the plain launch writes, bit for bit)
+  // so that the combined kernel stays within 128 registers, two workgroups per
+  // compute unit
+  if (!(pick == PAIR_PICK && !wpl.kw4 && (wpl.fn == 4 || wpl.fn == 2) && wpl.ru == 1 && wpl.wv == 8 &&
+        s.co % 32 == 0 && pair_env())) {
+    hipError_t e = launch_conv_bwd_weight_f32(s, x, dy, y, alpha, dw, db, ws, GM_DY_Y, nullptr, st);
+    if (e != hipSuccess) return e;
+    return launch_conv_bwd_data_f32(s, dy, w, dx, st, y, alpha);
+  }
+  const int dtiles = f_assign(fp, 16);
+  const int dcols = fp.dc / 16;
+  WF32Params wp = f32w_params(s, wpl, alpha);
+  wp.g_bytes = wp.m_bytes = (uint32_t)((long long)wp.vox * s.co * 4);
+  const int wgy = s.co / 32;
+  const int nw = wpl.gx * wgy * wpl.nsplit;
+  const int dbase = (nw + 7) / 8 * 8;
+  const long long blocks = (long long)dbase + (long long)dtiles * dcols;
+  if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
+  float *pw = (float *)ws;
+  float *pb = pw + (size_t)wpl.nsplit * wp.m * s.co;
+  if (blocks > 0)
+    hipLaunchKernelGGL(bwd_pair_f32_kernel, dim3((unsigned)blocks), dim3(512), 0, st, x, dy, y, w, dx, pw, pb, fp, wp,
+                       wpl.gx, wgy, nw, dbase, dtiles);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  e = launch_sum_rows(pw, dw, wpl.nsplit, wp.m * s.co, st);
+  if (e != hipSuccess) return e;
+  return launch_sum_rows(pb, db, wpl.nsplit, s.co, st);
 }
 
 hipError_t launch_conv_bwd_data_f32(const ConvShape &s, const float *dz, const float *w, float *dx, hipStream_t st,

@@ -368,6 +368,17 @@ class ConvStack:
                       self.alpha, B.CF_FUSE_POOL2, l["dx"], stream)
                     g = l["dx"]
                 continue
+            if l["fused_y"] and self.side is None and l["dx"] is not None:
+                # (dy, y): dW, db and dx in one call (one launch where the kernels allow)
+                if d:
+                    pend += c(f"L{i+1}.conv_bwd_fused", B.cf_conv3d_bwd_fused_deferred, l["desc"],
+                              self.layer_input(i), g, l["z"], l["w"], self.alpha, 0, l["dw"], l["db"], l["dx"],
+                              l["ws_w"], None, stream)
+                else:
+                    c(f"L{i+1}.conv_bwd_fused", B.cf_conv3d_bwd_fused, l["desc"], self.layer_input(i), g, l["z"],
+                      l["w"], self.alpha, 0, l["dw"], l["db"], l["dx"], l["ws_w"], None, stream)
+                g = l["dx"]
+                continue
             if l["fused_y"]:
                 # (dy, y): the weight gradient (and db) on the side stream, the data
                 # gradient on the main stream, both forming dz from dy and y
@@ -454,7 +465,8 @@ class ConvStack:
         i = int(name[1:name.index(".")]) - 1
         l = self.L[i]
         s = l["spec"]
-        return 2 * l["nvox"] * s["cout"] * s["k"] ** 3 * s["cin"]
+        f = 2 * l["nvox"] * s["cout"] * s["k"] ** 3 * s["cin"]
+        return 2 * f if name.endswith(".conv_bwd_fused") else f  # weight and data gradients
 
     def op_bytes(self, name):
         """Algorithmic HBM bytes of one call (every tensor read once, written once)."""
@@ -473,12 +485,13 @@ class ConvStack:
         pb = zb // 8
         op = name.split(".")[1]
         mb = l["nvox"] * s["cout"] // 8
-        if op in ("conv_bwd_weight_fused", "conv_bwd_data_fused") and not s["pool"]:
+        if op in ("conv_bwd_weight_fused", "conv_bwd_data_fused", "conv_bwd_fused") and not s["pool"]:
             # the (dy, y) form reads dy and y in place of the pooled gradient and mask
             pb = mb = zb
         return {"conv_fwd_fused": xb + wb + pb + mb, "conv_bwd_weight_fused": xb + pb + mb + wb // es * 4,
                 "conv_bwd_weight_fused_dz": xb + pb + mb + wb // es * 4 + zb,
                 "conv_bwd_data_fused": pb + mb + wb + xb,
+                "conv_bwd_fused": xb + pb + mb + wb // es * 4 + wb + xb,
                 "conv_bias_lrelu_fwd": xb + wb + zb,
                 "conv_fwd": xb + wb + zb, "conv_bwd_data": zb + wb + xb,
                 "conv_bwd_weight": xb + zb + wb // es * 4, "bias_lrelu_fwd": 2 * zb,

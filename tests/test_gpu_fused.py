@@ -310,6 +310,76 @@ def test_fused_bwd_data(case, dt):
     assert e <= TOL[dt], e
 
 
+# the one-call fused backward: N, (D,H,W), CI, CO, k, flags, dtype.  The
+# stack's fp32 deep layers at 128^3 batch 1 take the combined launch; the rest
+# run the two calls in sequence
+BWD1_CASES = [
+    (1, (8, 8, 8), 64, 64, 3, 0, "f32"),
+    (1, (8, 8, 8), 64, 128, 2, 0, "f32"),
+    (1, (8, 8, 8), 128, 128, 2, 0, "f32"),
+    (2, (6, 5, 7), 64, 64, 3, 0, "f32"),     # ragged extents
+    (1, (16, 16, 16), 64, 64, 3, 0, "f32"),  # more rows: other tile shapes
+    (2, (8, 8, 8), 64, 64, 3, 0, "bf16"),
+    (1, (16, 12, 64), 16, 32, 4, 1, "bf16"),  # pooled form (CF_FUSE_POOL2)
+]
+
+
+@pytest.mark.parametrize("case", BWD1_CASES, ids=lambda c: "n%d_%dx%dx%d_c%d-%d_k%d_f%d_%s" % (c[0], *c[1], *c[2:]))
+def test_fused_bwd_one_call(case, monkeypatch):
+    """cf_conv3d_bwd_fused (and its deferred form) return the bits of
+    cf_conv3d_bwd_weight_fused + cf_conv3d_bwd_data_fused, with the combined
+    launch on and off; the results also match the oracle."""
+    N, dhw, CI, CO, k, flags, dt = case
+    desc = B.make_desc(N, dhw, CI, CO, k, 1, "same", dt)
+    sup = B.cf_conv3d_fused_supported(desc, flags)
+    if not (sup & B.FUSED_BWD_WEIGHT and sup & B.FUSED_BWD_DATA):
+        pytest.skip("no fused backward pair for this shape")
+    rng = np.random.default_rng(21)
+    od = B.cf_conv3d_out_shape(desc)
+    alpha = 0.01
+    x = dev(rng.standard_normal((N, *dhw, CI)), dt)
+    w = dev(rng.standard_normal((k, k, k, CI, CO)) * np.sqrt(2.0 / (k ** 3 * CI)), dt)
+    if flags:
+        g = dev(rng.standard_normal((N,) + tuple(t // 2 for t in od) + (CO,)), dt)
+        aux = torch.as_tensor(rng.integers(0, 256, B.cf_conv3d_mask_bytes(desc), dtype=np.uint8), device="cuda")
+    else:
+        g = dev(rng.standard_normal((N, *od, CO)), dt)
+        yv = rng.standard_normal((N, *od, CO))
+        yv[rng.random(yv.shape) < 0.05] = 0.0  # exact zeros take the alpha slope
+        aux = dev(yv, dt)
+    ws = torch.empty(B.cf_conv3d_bwd_weight_fused_workspace_size(desc, flags), dtype=torch.uint8, device="cuda")
+
+    def outs():
+        return (torch.full((k, k, k, CI, CO), float("nan"), device="cuda"), torch.full((CO,), float("nan"), device="cuda"),
+                torch.full((N, *dhw, CI), float("nan"), dtype=tdtype(dt), device="cuda"))
+
+    dw0, db0, dx0 = outs()
+    B.cf_conv3d_bwd_weight_fused(desc, x, g, aux, alpha, flags, dw0, db0, ws)
+    B.cf_conv3d_bwd_data_fused(desc, g, aux, w, alpha, flags, dx0)
+    got = []
+    for pair in ("1", "0"):
+        monkeypatch.setenv("CF_F32_PAIR", pair)
+        dw1, db1, dx1 = outs()
+        B.cf_conv3d_bwd_fused(desc, x, g, aux, w, alpha, flags, dw1, db1, dx1, ws)
+        dw2, db2, dx2 = outs()
+        jobs = B.cf_conv3d_bwd_fused_deferred(desc, x, g, aux, w, alpha, flags, dw2, db2, dx2, ws)
+        B.cf_reduce_partials(jobs)
+        got += [(dw1, db1, dx1), (dw2, db2, dx2)]
+    torch.cuda.synchronize()
+    for i, (dw1, db1, dx1) in enumerate(got):
+        what = ("one launch allowed", "one launch allowed, deferred", "two launches", "two launches, deferred")[i]
+        assert torch.equal(dw1, dw0), (what, "dW", (dw1 - dw0).abs().max().item())
+        assert torch.equal(db1, db0), (what, "db", (db1 - db0).abs().max().item())
+        assert torch.equal(dx1, dx0), (what, "dx", (dx1.float() - dx0.float()).abs().max().item())
+    if flags == 0:
+        dz = to_np(g) * np.where(to_np(aux) > 0, 1.0, alpha)
+        if dt == "bf16":
+            dz = to_np(dev(dz, dt))  # the bf16 path rounds dz before the products
+        assert maxabs_err(to_np(dw0), oracle.conv3d_bwd_weight(to_np(x), dz, (k, k, k))) <= TOL[dt]
+        assert maxabs_err(to_np(dx0), oracle.conv3d_bwd_data(dz, to_np(w), dhw)) <= TOL[dt]
+        assert maxabs_err(to_np(db0), dz.sum(axis=(0, 1, 2, 3))) <= TOL[dt]
+
+
 @pytest.mark.parametrize("dt", ["f32", "bf16"])
 @pytest.mark.parametrize("case", FWD_CASES, ids=lambda c: "n%d_%dx%dx%d_c%d-%d_k%d" % (c[0], *c[1], *c[2:]))
 def test_fused_bwd_weight_dz(case, dt):
