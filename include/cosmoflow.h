@@ -189,6 +189,16 @@ cf_status cf_avgpool3d_bwd(int32_t n, int32_t d, int32_t h, int32_t w, int32_t c
                            int32_t k, int32_t s, int32_t dtype, const void *dp, void *dy,
                            void *stream);
 
+/* Both backward products of a layer from one dz (Section III-C: the data
+ * and weight gradients read the same dz): dW exactly as cf_conv3d_bwd_weight
+ * and dx exactly as cf_conv3d_bwd_data, with their arguments (bitwise the same
+ * results).  Where both products run on the fp32 register-streamed kernels
+ * one launch holds them side by side; otherwise the two calls run in
+ * sequence.  ws: cf_conv3d_bwd_weight_workspace_size bytes; dx must not
+ * overlap x, dW or ws (CF_ERR_ALIAS). */
+cf_status cf_conv3d_bwd(const cf_conv3d_desc *desc, const void *x, const void *dz, const void *w,
+                        float *dw, void *dx, void *ws, size_t ws_bytes, void *stream);
+
 /* ------------------------------------------------------------------------
  * Fused layer variants.  Same mathematics as the unfused composition
  *   conv -> bias + leaky ReLU -> 2^3 stride-2 average pool     (forward)
@@ -348,6 +358,12 @@ cf_status cf_conv3d_bwd_weight_fused_deferred(const cf_conv3d_desc *desc, const 
                                               uint32_t flags, float *dw, float *db, void *dz,
                                               void *ws, size_t ws_bytes, cf_reduction *pending,
                                               int32_t *npending, void *stream);
+
+/* cf_conv3d_bwd without the final sums of dW (dx is written by this call).
+ * pending / npending as above. */
+cf_status cf_conv3d_bwd_deferred(const cf_conv3d_desc *desc, const void *x, const void *dz,
+                                 const void *w, float *dw, void *dx, void *ws, size_t ws_bytes,
+                                 cf_reduction *pending, int32_t *npending, void *stream);
 
 /* cf_conv3d_bwd_fused without the final sums of dW and db (dx is written by
  * this call).  pending / npending as above. */

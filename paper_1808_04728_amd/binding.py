@@ -40,6 +40,7 @@ EXPORTS = [
     "cf_fc_fwd_workspace_size", "cf_fc_fwd", "cf_fc_bwd_data", "cf_fc_bwd_weight", "cf_mse_loss",
     "cf_conv3d_bwd_weight_noalloc", "cf_avgpool3d_lrelu_bwd_workspace_size", "cf_avgpool3d_lrelu_bwd",
     "cf_avgpool3d_lrelu_bwd_deferred", "cf_conv3d_bwd_fused", "cf_conv3d_bwd_fused_deferred",
+    "cf_conv3d_bwd", "cf_conv3d_bwd_deferred",
 ]
 
 
@@ -121,6 +122,9 @@ def lib():
         "cf_conv3d_bwd_weight_fused_dz": ([D, vp, vp, vp, f32, ctypes.c_uint32, vp, vp, vp, vp, sz, vp],
                                           ctypes.c_int),
         "cf_conv3d_bwd_data_fused": ([D, vp, vp, vp, f32, ctypes.c_uint32, vp, vp], ctypes.c_int),
+        "cf_conv3d_bwd": ([D, vp, vp, vp, vp, vp, vp, sz, vp], ctypes.c_int),
+        "cf_conv3d_bwd_deferred": ([D, vp, vp, vp, vp, vp, vp, sz, ctypes.POINTER(cf_reduction),
+                                    ctypes.POINTER(i32), vp], ctypes.c_int),
         "cf_conv3d_bwd_fused": ([D, vp, vp, vp, vp, f32, ctypes.c_uint32, vp, vp, vp, vp, sz, vp], ctypes.c_int),
         "cf_conv3d_bwd_fused_deferred": ([D, vp, vp, vp, vp, f32, ctypes.c_uint32, vp, vp, vp, vp, sz,
                                           ctypes.POINTER(cf_reduction), ctypes.POINTER(i32), vp], ctypes.c_int),
@@ -298,6 +302,13 @@ def cf_conv3d_bwd_data_fused(desc, g, mask, w, alpha, flags, dx, stream=None):
                                           _stream(stream)))
 
 
+def cf_conv3d_bwd(desc, x, dz, w, dw, dx, ws, ws_bytes=None, stream=None):
+    if ws_bytes is None:
+        ws_bytes = 0 if ws is None or isinstance(ws, int) else ws.numel() * ws.element_size()
+    _check(lib().cf_conv3d_bwd(ctypes.byref(desc), _ptr(x), _ptr(dz), _ptr(w), _ptr(dw), _ptr(dx), _ptr(ws),
+                               ws_bytes, _stream(stream)))
+
+
 def cf_conv3d_bwd_fused(desc, x, g, mask, w, alpha, flags, dw, db, dx, ws, ws_bytes=None, stream=None):
     if ws_bytes is None:
         ws_bytes = 0 if ws is None or isinstance(ws, int) else ws.numel() * ws.element_size()
@@ -357,6 +368,15 @@ def cf_conv3d_bwd_weight_fused_deferred(desc, x, g, mask, alpha, flags, dw, db, 
     _check(lib().cf_conv3d_bwd_weight_fused_deferred(ctypes.byref(desc), _ptr(x), _ptr(g), _ptr(mask), alpha, flags,
                                                      _ptr(dw), _ptr(db), _ptr(dz), _ptr(ws), ws_bytes, arr,
                                                      ctypes.byref(n), _stream(stream)))
+    return _pending_list(arr, n)
+
+
+def cf_conv3d_bwd_deferred(desc, x, dz, w, dw, dx, ws, ws_bytes=None, stream=None):
+    if ws_bytes is None:
+        ws_bytes = 0 if ws is None or isinstance(ws, int) else ws.numel() * ws.element_size()
+    arr, n = (cf_reduction * CF_MAX_PENDING)(), ctypes.c_int32(0)
+    _check(lib().cf_conv3d_bwd_deferred(ctypes.byref(desc), _ptr(x), _ptr(dz), _ptr(w), _ptr(dw), _ptr(dx), _ptr(ws),
+                                        ws_bytes, arr, ctypes.byref(n), _stream(stream)))
     return _pending_list(arr, n)
 
 

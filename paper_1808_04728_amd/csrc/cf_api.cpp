@@ -191,8 +191,9 @@ cf_status cf_conv3d_fwd(const cf_conv3d_desc *desc, const void *x, const void *w
   return finish(cf::launch_conv_fwd(s, x, w, z, st), st, "cf_conv3d_fwd");
 }
 
-cf_status cf_conv3d_bwd_data(const cf_conv3d_desc *desc, const void *dz, const void *w, void *dx,
-                             void *stream) {
+// check_only: validate every argument and return without launching
+static cf_status bwd_data(const cf_conv3d_desc *desc, const void *dz, const void *w, void *dx, void *stream,
+                          bool check_only) {
   cf::ConvShape s;
   cf_status r = resolve(desc, &s);
   if (r != CF_OK) return r;
@@ -201,8 +202,14 @@ cf_status cf_conv3d_bwd_data(const cf_conv3d_desc *desc, const void *dz, const v
   Sizes b = conv_bytes(s);
   if (overlap(dx, b.x, dz, b.z) || overlap(dx, b.x, w, b.w))
     return fail(CF_ERR_ALIAS, "conv3d_bwd_data: dx overlaps dz or W");
+  if (check_only) return CF_OK;
   hipStream_t st = (hipStream_t)stream;
   return finish(cf::launch_conv_bwd_data(s, dz, w, dx, st), st, "cf_conv3d_bwd_data");
+}
+
+cf_status cf_conv3d_bwd_data(const cf_conv3d_desc *desc, const void *dz, const void *w, void *dx,
+                             void *stream) {
+  return bwd_data(desc, dz, w, dx, stream, false);
 }
 
 size_t cf_conv3d_bwd_weight_workspace_size(const cf_conv3d_desc *desc) {
@@ -216,8 +223,8 @@ size_t cf_conv3d_bwd_weight_workspace_size(const cf_conv3d_desc *desc) {
   return cf::conv_bwd_weight_workspace(s);
 }
 
-cf_status cf_conv3d_bwd_weight(const cf_conv3d_desc *desc, const void *x, const void *dz, float *dw,
-                               void *ws, size_t ws_bytes, void *stream) {
+static cf_status bwd_weight(const cf_conv3d_desc *desc, const void *x, const void *dz, float *dw, void *ws,
+                            size_t ws_bytes, void *stream, bool check_only) {
   cf::ConvShape s;
   cf_status r = resolve(desc, &s);
   if (r != CF_OK) return r;
@@ -226,6 +233,7 @@ cf_status cf_conv3d_bwd_weight(const cf_conv3d_desc *desc, const void *x, const 
   const size_t dw_bytes = (size_t)s.kd * s.kh * s.kw * s.ci * s.co * sizeof(float);
   if (s.n == 0) {
     if ((r = check_ptrs({dw})) != CF_OK) return r;
+    if (check_only) return CF_OK;
     // the sum over an empty batch is zero
     return finish(cf::launch_fill_zero(dw, (long long)(dw_bytes / sizeof(float)), st), st,
                   "cf_conv3d_bwd_weight");
@@ -239,7 +247,29 @@ cf_status cf_conv3d_bwd_weight(const cf_conv3d_desc *desc, const void *x, const 
     return fail(CF_ERR_ALIAS, "conv3d_bwd_weight: dW overlaps x or dz");
   if (overlap(ws, need, x, b.x) || overlap(ws, need, dz, b.z) || overlap(ws, need, dw, dw_bytes))
     return fail(CF_ERR_ALIAS, "conv3d_bwd_weight: workspace overlaps a tensor");
+  if (check_only) return CF_OK;
   return finish(cf::launch_conv_bwd_weight(s, x, dz, dw, ws, st), st, "cf_conv3d_bwd_weight");
+}
+
+cf_status cf_conv3d_bwd_weight(const cf_conv3d_desc *desc, const void *x, const void *dz, float *dw,
+                               void *ws, size_t ws_bytes, void *stream) {
+  return bwd_weight(desc, x, dz, dw, ws, ws_bytes, stream, false);
+}
+
+cf_status cf_conv3d_bwd(const cf_conv3d_desc *desc, const void *x, const void *dz, const void *w, float *dw,
+                        void *dx, void *ws, size_t ws_bytes, void *stream) {
+  cf_status r = bwd_weight(desc, x, dz, dw, ws, ws_bytes, stream, true);
+  if (r != CF_OK) return r;
+  if ((r = bwd_data(desc, dz, w, dx, stream, true)) != CF_OK) return r;
+  cf::ConvShape s;
+  resolve(desc, &s);
+  if (s.n == 0) return bwd_weight(desc, x, dz, dw, ws, ws_bytes, stream, false);  // dW = 0, dx empty
+  const size_t dxb = conv_bytes(s).x, dwb = (size_t)s.kd * s.kh * s.kw * s.ci * s.co * sizeof(float);
+  if (overlap(dx, dxb, dw, dwb) || overlap(dx, dxb, x, conv_bytes(s).x) ||
+      overlap(dx, dxb, ws, cf::conv_bwd_weight_workspace(s)))
+    return fail(CF_ERR_ALIAS, "cf_conv3d_bwd: dx overlaps x, dW or the workspace");
+  hipStream_t st = (hipStream_t)stream;
+  return finish(cf::launch_conv_bwd(s, x, dz, w, dw, dx, ws, st), st, "cf_conv3d_bwd");
 }
 
 static_assert(cf::kNoallocScratchBytes == CF_NOALLOC_SCRATCH_BYTES, "scratch region size");
@@ -729,6 +759,12 @@ cf_status cf_conv3d_bwd_weight_fused_deferred(const cf_conv3d_desc *desc, const 
     return bwd_weight_fused(dz ? "cf_conv3d_bwd_weight_fused_dz" : "cf_conv3d_bwd_weight_fused", desc, x, g, mask,
                             alpha, flags, dw, db, dz, ws, ws_bytes, stream);
   });
+}
+
+cf_status cf_conv3d_bwd_deferred(const cf_conv3d_desc *desc, const void *x, const void *dz, const void *w,
+                                 float *dw, void *dx, void *ws, size_t ws_bytes, cf_reduction *pending,
+                                 int32_t *npending, void *stream) {
+  return deferred(pending, npending, [&] { return cf_conv3d_bwd(desc, x, dz, w, dw, dx, ws, ws_bytes, stream); });
 }
 
 cf_status cf_conv3d_bwd_fused_deferred(const cf_conv3d_desc *desc, const void *x, const void *g, const void *mask,

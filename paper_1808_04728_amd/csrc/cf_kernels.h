@@ -140,6 +140,14 @@ size_t f32wgrad_workspace(const ConvShape &s, int gm);
 hipError_t launch_conv_bwd_fused_f32(const ConvShape &s, const float *x, const float *dy, const float *y,
                                      const float *w, float alpha, float *dw, float *db, float *dx, void *ws,
                                      hipStream_t st);
+// fp32 weight and data gradients of a layer from a stored dz: one launch where
+// the planners pick the instantiated tile shapes, else the two launches in
+// sequence; workspace as cf_conv3d_bwd_weight's.
+hipError_t launch_conv_bwd_f32(const ConvShape &s, const float *x, const float *dz, const float *w, float *dw,
+                               float *dx, void *ws, hipStream_t st);
+// both backward products of a layer from a stored dz (conv_igemm.hip's dispatch)
+hipError_t launch_conv_bwd(const ConvShape &s, const void *x, const void *dz, const void *w, float *dw, void *dx,
+                           void *ws, hipStream_t st);
 hipError_t launch_conv_bwd_weight_f32(const ConvShape &s, const float *x, const float *g, const void *aux,
                                       float alpha, float *dw, float *db, void *ws, int gm, float *dz_out,
                                       hipStream_t st);

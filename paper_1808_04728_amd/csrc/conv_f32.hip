@@ -1089,22 +1089,33 @@ namespace {
 // 16-column group, K split over 8 waves; weight gradient one 64-channel row
 // unit per wave), the weight gradient with two column groups.
 // ---------------------------------------------------------------------------
-constexpr int PAIR_PICK = 6;  // kCand[6] = {fm 1, wm 1, wk 8}
-static_assert(kCand[PAIR_PICK].fm == 1 && kCand[PAIR_PICK].wm == 1 && kCand[PAIR_PICK].wk == 8, "pair tile");
+// The tile shapes instantiated: the deep layers' (dy, y) form (backward-data
+// kCand[6] = 16-row tiles, one 16-column group, K split over 8 waves; weight
+// gradient one 64-channel row unit per wave, two column groups instead of the
+// planned four, so that the kernel stays within 128 registers and two
+// 8-wave workgroups fit per compute unit) and the stride-2 layer's plain form
+// on a stored dz (backward-data kCand[3] = 64-row tiles, two column groups, K
+// over 4 waves, 142 registers alone; weight gradient 16-channel row units on
+// 4 waves, four column groups: three 4-wave workgroups per compute unit).
+// A launch keeps the weight gradient's planned slices, so every partial is
+// the one its plain launch writes, bit for bit.
+static_assert(kCand[6].fm == 1 && kCand[6].wm == 1 && kCand[6].wk == 8, "deep-layer pair tile");
+static_assert(kCand[3].fm == 4 && kCand[3].wm == 1 && kCand[3].wk == 4, "stride-2 pair tile");
 
-__global__ __launch_bounds__(512, 4) void bwd_pair_f32_kernel(const float *__restrict__ x, const float *__restrict__ dy,
-                                                           const float *__restrict__ y, const float *__restrict__ w,
-                                                           float *__restrict__ dx, float *__restrict__ part_w,
-                                                           float *__restrict__ part_b, const FParams fp,
-                                                           const WF32Params wp, int wgx, int wgy, int nw, int dbase,
-                                                           int dtiles) {
+template <int GM, bool WKW4, int WV, int WFN, int DFN, int DFM, int DWM, int DWK, bool DYY, int MINW>
+__global__ __launch_bounds__(64 * WV, MINW) void bwd_pair_f32_kernel(
+    const float *__restrict__ x, const float *__restrict__ dy, const float *__restrict__ y,
+    const float *__restrict__ w, float *__restrict__ dx, float *__restrict__ part_w, float *__restrict__ part_b,
+    const FParams fp, const WF32Params wp, int wgx, int wgy, int nw, int dbase, int dtiles) {
+  static_assert(WV == DWM * DWK, "one block size for both products");
   const int b = blockIdx.x;
   if (b < nw) {
     const int t = b / wgx;
-    wgrad_f32_body<GM_DY_Y, false, 1, 2, 8, 2>(x, dy, y, part_w, part_b, nullptr, wp, b - t * wgx, t % wgy, t / wgy);
+    wgrad_f32_body<GM, WKW4, 1, WFN, WV, 2>(x, dy, y, part_w, part_b, nullptr, wp, b - t * wgx, t % wgy, t / wgy);
   } else if (b >= dbase) {
     const int j = b - dbase;
-    conv_f32_body<false, 1, 1, 1, 8, 2, 0, 0, true>(dy, y, w, nullptr, dx, nullptr, fp, j % dtiles, j / dtiles);
+    conv_f32_body<false, DFM, DFN, DWM, DWK, 2, 0, 0, DYY>(dy, y, w, nullptr, dx, nullptr, fp, j % dtiles,
+                                                            j / dtiles);
   }
 }
 
@@ -1116,46 +1127,74 @@ bool pair_env() {
 
 }  // namespace
 
-hipError_t launch_conv_bwd_fused_f32(const ConvShape &s, const float *x, const float *dy, const float *y,
-                                     const float *w, float alpha, float *dw, float *db, float *dx, void *ws,
-                                     hipStream_t st) {
-  // the backward-data plan, as launch_conv_bwd_data_f32 makes it
-  FParams fp{};
-  f_tables(s, false, fp);
-  fp.alpha = alpha;
-  const int fn = f_pick_fn(s, fp, s.ci % 64 == 0 ? 4 : (s.ci % 32 == 0 ? 2 : 1), false);
-  double cost = 0.0;
-  const int pick = fn == 1 ? f_pick<1>(s, fp, &cost, false) : -1;
-  const WPlan wpl = f32w_plan(s, GM_DY_Y);
-  // the weight gradient runs with two column groups per workgroup (its slices
-  // as planned: every partial is the one the plain launch writes, bit for bit)
-  // so that the combined kernel stays within 128 registers, two workgroups per
-  // compute unit
-  if (!(pick == PAIR_PICK && !wpl.kw4 && (wpl.fn == 4 || wpl.fn == 2) && wpl.ru == 1 && wpl.wv == 8 &&
-        s.co % 32 == 0 && pair_env())) {
-    hipError_t e = launch_conv_bwd_weight_f32(s, x, dy, y, alpha, dw, db, ws, GM_DY_Y, nullptr, st);
-    if (e != hipSuccess) return e;
-    return launch_conv_bwd_data_f32(s, dy, w, dx, st, y, alpha);
-  }
-  const int dtiles = f_assign(fp, 16);
-  const int dcols = fp.dc / 16;
+namespace {
+// one grid for both products: the weight-gradient workgroups of plan wpl (with
+// WV waves and two column groups), then, from an offset rounded up to a multiple
+// of 8, the backward-data tiles of plan fp
+template <int GM, bool WKW4, int WV, int WFN, int DFN, int DFM, int DWM, int DWK, bool DYY, int MINW>
+hipError_t launch_pair(const ConvShape &s, const WPlan &wpl, FParams &fp, const float *x, const float *g,
+                       const float *y, const float *w, float alpha, float *dw, float *db, float *dx, void *ws,
+                       hipStream_t st) {
+  const int dtiles = f_assign(fp, 16 * DFM * DWM);
+  const int dcols = fp.dc / (16 * DFN);
   WF32Params wp = f32w_params(s, wpl, alpha);
-  wp.g_bytes = wp.m_bytes = (uint32_t)((long long)wp.vox * s.co * 4);
-  const int wgy = s.co / 32;
-  const int nw = wpl.gx * wgy * wpl.nsplit;
+  wp.g_bytes = (uint32_t)((long long)wp.vox * s.co * 4);
+  if (GM == GM_DY_Y) wp.m_bytes = wp.g_bytes;
+  const int wgx = (wpl.units + WV - 1) / WV;  // one row unit per wave
+  const int wgy = s.co / (16 * WFN);
+  const int nw = wgx * wgy * wpl.nsplit;
   const int dbase = (nw + 7) / 8 * 8;
   const long long blocks = (long long)dbase + (long long)dtiles * dcols;
   if (blocks > 0x7fffffffLL) return hipErrorInvalidValue;
   float *pw = (float *)ws;
-  float *pb = pw + (size_t)wpl.nsplit * wp.m * s.co;
-  if (blocks > 0)
-    hipLaunchKernelGGL(bwd_pair_f32_kernel, dim3((unsigned)blocks), dim3(512), 0, st, x, dy, y, w, dx, pw, pb, fp, wp,
-                       wpl.gx, wgy, nw, dbase, dtiles);
+  float *pb = GM == GM_DZ ? nullptr : pw + (size_t)wpl.nsplit * wp.m * s.co;
+  hipLaunchKernelGGL((bwd_pair_f32_kernel<GM, WKW4, WV, WFN, DFN, DFM, DWM, DWK, DYY, MINW>), dim3((unsigned)blocks),
+                     dim3(64 * WV), 0, st, x, g, y, w, dx, pw, pb, fp, wp, wgx, wgy, nw, dbase, dtiles);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   e = launch_sum_rows(pw, dw, wpl.nsplit, wp.m * s.co, st);
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || GM == GM_DZ) return e;
   return launch_sum_rows(pb, db, wpl.nsplit, s.co, st);
+}
+
+// the backward-data plan, as launch_conv_bwd_data_f32 makes it: column groups
+// and the kCand tile (-1 for the shift / output-shift modes)
+int dgrad_plan(const ConvShape &s, FParams &fp, float alpha, int *fn) {
+  f_tables(s, false, fp);
+  fp.alpha = alpha;
+  *fn = f_pick_fn(s, fp, s.ci % 64 == 0 ? 4 : (s.ci % 32 == 0 ? 2 : 1), false);
+  double cost = 0.0;
+  return *fn == 1 ? f_pick<1>(s, fp, &cost, false) : *fn == 2 ? f_pick<2>(s, fp, &cost, false)
+                                                              : f_pick<4>(s, fp, &cost, false);
+}
+}  // namespace
+
+hipError_t launch_conv_bwd_fused_f32(const ConvShape &s, const float *x, const float *dy, const float *y,
+                                     const float *w, float alpha, float *dw, float *db, float *dx, void *ws,
+                                     hipStream_t st) {
+  FParams fp{};
+  int fn = 0;
+  const int pick = dgrad_plan(s, fp, alpha, &fn);
+  const WPlan wpl = f32w_plan(s, GM_DY_Y);
+  if (fn == 1 && pick == 6 && !wpl.kw4 && wpl.ru == 1 && wpl.fn >= 2 && s.co % 32 == 0 && pair_env())
+    return launch_pair<GM_DY_Y, false, 8, 2, 1, 1, 1, 8, true, 4>(s, wpl, fp, x, dy, y, w, alpha, dw, db, dx, ws, st);
+  hipError_t e = launch_conv_bwd_weight_f32(s, x, dy, y, alpha, dw, db, ws, GM_DY_Y, nullptr, st);
+  if (e != hipSuccess) return e;
+  return launch_conv_bwd_data_f32(s, dy, w, dx, st, y, alpha);
+}
+
+hipError_t launch_conv_bwd_f32(const ConvShape &s, const float *x, const float *dz, const float *w, float *dw,
+                               float *dx, void *ws, hipStream_t st) {
+  FParams fp{};
+  int fn = 0;
+  const int pick = dgrad_plan(s, fp, 0.f, &fn);
+  const WPlan wpl = f32w_plan(s, GM_DZ);
+  if (fn == 2 && pick == 3 && wpl.kw4 && wpl.ru == 1 && wpl.fn == 4 && pair_env())
+    return launch_pair<GM_DZ, true, 4, 4, 2, 4, 1, 4, false, 3>(s, wpl, fp, x, dz, nullptr, w, 0.f, dw, nullptr, dx, ws,
+                                                                st);
+  hipError_t e = launch_conv_bwd_weight_f32(s, x, dz, nullptr, 0.f, dw, nullptr, ws, GM_DZ, nullptr, st);
+  if (e != hipSuccess) return e;
+  return launch_conv_bwd_data_f32(s, dz, w, dx, st, nullptr, 0.f);
 }
 
 hipError_t launch_conv_bwd_data_f32(const ConvShape &s, const float *dz, const float *w, float *dx, hipStream_t st,

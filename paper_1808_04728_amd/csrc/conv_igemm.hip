@@ -714,4 +714,19 @@ hipError_t launch_conv_bwd_weight(const ConvShape &s, const void *x, const void 
   return launch_sum_rows(part, dw, pl.nsplit, p.m * p.co, st);
 }
 
+// weight and data gradients from one stored dz: the fp32 register-streamed
+// kernels share one launch (launch_conv_bwd_f32); every other path runs the
+// two dispatchers above in sequence
+hipError_t launch_conv_bwd(const ConvShape &s, const void *x, const void *dz, const void *w, float *dw, void *dx,
+                           void *ws, hipStream_t st) {
+  const bool wf32 = !use_l1_wgrad(s) && !c16_wgrad_supported(s) && !use_direct_wgrad(s) && use_f32_wgrad(s);
+  const bool df32 = !c16_bwd_supported(s) && !direct_supported(s, false) && f32conv_supported(s, false) &&
+                    !igemm_forced();
+  if (wf32 && df32)
+    return launch_conv_bwd_f32(s, (const float *)x, (const float *)dz, (const float *)w, dw, (float *)dx, ws, st);
+  hipError_t e = launch_conv_bwd_weight(s, x, dz, dw, ws, st);
+  if (e != hipSuccess) return e;
+  return launch_conv_bwd_data(s, dz, w, dx, st);
+}
+
 }  // namespace cf

@@ -148,7 +148,10 @@ class ConvStack:
                 l["z"] = l["dy"] = l["dz"] = None
                 # a layer whose data gradient is needed may take dz from its weight-gradient
                 # pass and run the unfused backward-data on it (same dx bits, faster there)
-                l["dz_emit"] = bool(needs_dgrad and sup & B.FUSED_BWD_WEIGHT_DZ)
+                # (in fp32 the stride-2 layer takes the one-pass dz below instead: its
+                # two plain products then share one launch)
+                pair_pass = self.dtype == "f32" and s["stride"] > 1 and self.pooled_dz_pass
+                l["dz_emit"] = bool(needs_dgrad and sup & B.FUSED_BWD_WEIGHT_DZ and not pair_pass)
                 # or, without that kernel, form dz in one pooled-gradient pass and run the
                 # plain weight and data gradients on it side by side: the data gradient
                 # gathers every dz element k^3 times, so forming dz once beats forming it
@@ -313,14 +316,22 @@ class ConvStack:
                 else:
                     c(f"L{i+1}.pool_lrelu_bwd", B.cf_avgpool3d_lrelu_bwd, self.batch, *od, s["cout"], self.dtype, g,
                       l["mask"], self.alpha, l["dz"], l["db"], l["ws_b"], None, stream)
-                ws_ = stream
-                if self.side is not None:
-                    main = stream if stream is not None else torch.cuda.current_stream()
-                    ev = torch.cuda.Event()
-                    ev.record(main)
-                    self.side.wait_event(ev)
-                    ws_ = self.side
-                    side_used = True
+                if self.side is None:
+                    # both plain products from dz in one call (one launch where the kernels allow)
+                    if d:
+                        pend += c(f"L{i+1}.conv_bwd", B.cf_conv3d_bwd_deferred, l["desc"], self.layer_input(i),
+                                  l["dz"], l["w"], l["dw"], l["dx"], l["ws_w"], None, stream)
+                    else:
+                        c(f"L{i+1}.conv_bwd", B.cf_conv3d_bwd, l["desc"], self.layer_input(i), l["dz"], l["w"],
+                          l["dw"], l["dx"], l["ws_w"], None, stream)
+                    g = l["dx"]
+                    continue
+                main = stream if stream is not None else torch.cuda.current_stream()
+                ev = torch.cuda.Event()
+                ev.record(main)
+                self.side.wait_event(ev)
+                ws_ = self.side
+                side_used = True
                 if d:
                     pend += c(f"L{i+1}.conv_bwd_weight", B.cf_conv3d_bwd_weight_deferred, l["desc"],
                               self.layer_input(i), l["dz"], l["dw"], l["ws_w"], None, ws_, rec=ws_)
@@ -466,7 +477,7 @@ class ConvStack:
         l = self.L[i]
         s = l["spec"]
         f = 2 * l["nvox"] * s["cout"] * s["k"] ** 3 * s["cin"]
-        return 2 * f if name.endswith(".conv_bwd_fused") else f  # weight and data gradients
+        return 2 * f if name.endswith((".conv_bwd_fused", ".conv_bwd")) else f  # weight and data gradients
 
     def op_bytes(self, name):
         """Algorithmic HBM bytes of one call (every tensor read once, written once)."""
@@ -492,6 +503,7 @@ class ConvStack:
                 "conv_bwd_weight_fused_dz": xb + pb + mb + wb // es * 4 + zb,
                 "conv_bwd_data_fused": pb + mb + wb + xb,
                 "conv_bwd_fused": xb + pb + mb + wb // es * 4 + wb + xb,
+                "conv_bwd": xb + zb + wb // es * 4 + wb + xb,
                 "conv_bias_lrelu_fwd": xb + wb + zb,
                 "conv_fwd": xb + wb + zb, "conv_bwd_data": zb + wb + xb,
                 "conv_bwd_weight": xb + zb + wb // es * 4, "bias_lrelu_fwd": 2 * zb,

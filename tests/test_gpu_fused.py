@@ -310,6 +310,54 @@ def test_fused_bwd_data(case, dt):
     assert e <= TOL[dt], e
 
 
+# the one-call plain backward from a stored dz: N, (D,H,W), CI, CO, k, stride, dtype.
+# The fp32 stride-2 layer of the 128^3 stack takes the combined launch
+BWDP_CASES = [
+    (1, (32, 32, 32), 32, 64, 4, 2, "f32"),
+    (2, (14, 12, 18), 32, 64, 4, 2, "f32"),  # ragged, other tile plans
+    (1, (16, 16, 16), 16, 32, 4, 1, "f32"),
+    (2, (16, 16, 16), 32, 64, 4, 2, "bf16"),
+]
+
+
+@pytest.mark.parametrize("case", BWDP_CASES, ids=lambda c: "n%d_%dx%dx%d_c%d-%d_k%d_s%d_%s" % (c[0], *c[1], *c[2:]))
+def test_bwd_one_call(case, monkeypatch):
+    """cf_conv3d_bwd (and its deferred form) return the bits of
+    cf_conv3d_bwd_weight + cf_conv3d_bwd_data, with the combined launch on and
+    off, and match the oracle."""
+    N, dhw, CI, CO, k, st, dt = case
+    desc = B.make_desc(N, dhw, CI, CO, k, st, "same", dt)
+    rng = np.random.default_rng(23)
+    od = B.cf_conv3d_out_shape(desc)
+    x = dev(rng.standard_normal((N, *dhw, CI)), dt)
+    w = dev(rng.standard_normal((k, k, k, CI, CO)) * np.sqrt(2.0 / (k ** 3 * CI)), dt)
+    dz = dev(rng.standard_normal((N, *od, CO)), dt)
+    ws = torch.empty(max(16, B.cf_conv3d_bwd_weight_workspace_size(desc)), dtype=torch.uint8, device="cuda")
+
+    def outs():
+        return (torch.full((k, k, k, CI, CO), float("nan"), device="cuda"),
+                torch.full((N, *dhw, CI), float("nan"), dtype=tdtype(dt), device="cuda"))
+
+    dw0, dx0 = outs()
+    B.cf_conv3d_bwd_weight(desc, x, dz, dw0, ws)
+    B.cf_conv3d_bwd_data(desc, dz, w, dx0)
+    got = []
+    for pair in ("1", "0"):
+        monkeypatch.setenv("CF_F32_PAIR", pair)
+        dw1, dx1 = outs()
+        B.cf_conv3d_bwd(desc, x, dz, w, dw1, dx1, ws)
+        dw2, dx2 = outs()
+        B.cf_reduce_partials(B.cf_conv3d_bwd_deferred(desc, x, dz, w, dw2, dx2, ws))
+        got += [(dw1, dx1), (dw2, dx2)]
+    torch.cuda.synchronize()
+    for i, (dw1, dx1) in enumerate(got):
+        what = ("one launch allowed", "one launch allowed, deferred", "two launches", "two launches, deferred")[i]
+        assert torch.equal(dw1, dw0), (what, "dW", (dw1 - dw0).abs().max().item())
+        assert torch.equal(dx1, dx0), (what, "dx", (dx1.float() - dx0.float()).abs().max().item())
+    assert maxabs_err(to_np(dw0), oracle.conv3d_bwd_weight(to_np(x), to_np(dz), (k, k, k), stride=st)) <= TOL[dt]
+    assert maxabs_err(to_np(dx0), oracle.conv3d_bwd_data(to_np(dz), to_np(w), dhw, stride=st)) <= TOL[dt]
+
+
 # the one-call fused backward: N, (D,H,W), CI, CO, k, flags, dtype.  The
 # stack's fp32 deep layers at 128^3 batch 1 take the combined launch; the rest
 # run the two calls in sequence
