@@ -32,7 +32,8 @@ def _t(dtype):
 
 class ConvStack:
     def __init__(self, layers, size, batch, dtype="f32", alpha=0.01, device="cuda", skip_first_dgrad=True,
-                 fused=True, defer_reductions=True, overlap_wgrad=None, pooled_dz_pass=True, fused_from=0):
+                 fused=True, defer_reductions=True, overlap_wgrad=None, pooled_dz_pass=True, fused_from=0,
+                 dz_pass_layers=None):
         """fused: run a pooled layer through the fused entry points (forward
         epilogue writes pooled output + slope mask; backward rebuilds dz from
         them) wherever the library has fused kernels for the layer.
@@ -51,9 +52,13 @@ class ConvStack:
         pooled_dz_pass: a fused pooled layer without a dz-storing weight-gradient
         kernel forms dz in one pass from the pooled gradient and the mask
         (cf_avgpool3d_lrelu_bwd) for the plain gradient kernels; False runs the
-        fused backward kernels, which form dz as they load it."""
+        fused backward kernels, which form dz as they load it.
+        dz_pass_layers: indices of fused pooled layers that form dz in that one
+        pass even where a dz-storing weight-gradient kernel exists (None: the
+        fp32 stride-2 layers, whose two plain products then share one launch)."""
         self.fused = fused
         self.pooled_dz_pass = pooled_dz_pass
+        self.dz_pass_layers = dz_pass_layers
         self.fused_from = fused_from
         self.defer_reductions = defer_reductions
         self.reduce_bytes = 0
@@ -150,7 +155,10 @@ class ConvStack:
                 # pass and run the unfused backward-data on it (same dx bits, faster there)
                 # (in fp32 the stride-2 layer takes the one-pass dz below instead: its
                 # two plain products then share one launch)
-                pair_pass = self.dtype == "f32" and s["stride"] > 1 and self.pooled_dz_pass
+                if self.dz_pass_layers is None:
+                    pair_pass = self.dtype == "f32" and s["stride"] > 1 and self.pooled_dz_pass
+                else:
+                    pair_pass = i in self.dz_pass_layers and self.pooled_dz_pass
                 l["dz_emit"] = bool(needs_dgrad and sup & B.FUSED_BWD_WEIGHT_DZ and not pair_pass)
                 # or, without that kernel, form dz in one pooled-gradient pass and run the
                 # plain weight and data gradients on it side by side: the data gradient
