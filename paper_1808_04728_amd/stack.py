@@ -54,8 +54,8 @@ class ConvStack:
         (cf_avgpool3d_lrelu_bwd) for the plain gradient kernels; False runs the
         fused backward kernels, which form dz as they load it.
         dz_pass_layers: indices of fused pooled layers that form dz in that one
-        pass even where a dz-storing weight-gradient kernel exists (None: the
-        fp32 stride-2 layers, whose two plain products then share one launch)."""
+        pass even where a dz-storing weight-gradient kernel exists (None: every
+        such layer of an fp32 stack)."""
         self.fused = fused
         self.pooled_dz_pass = pooled_dz_pass
         self.dz_pass_layers = dz_pass_layers
@@ -156,7 +156,10 @@ class ConvStack:
                 # (in fp32 the stride-2 layer takes the one-pass dz below instead: its
                 # two plain products then share one launch)
                 if self.dz_pass_layers is None:
-                    pair_pass = self.dtype == "f32" and s["stride"] > 1 and self.pooled_dz_pass
+                    # fp32: the plain weight gradient on a stored dz beats the one that
+                    # rebuilds it per load (the 16 -> 32 layer: 189 -> 171 us, with an
+                    # 12 us dz pass), and the stride-2 layer's two products share a launch
+                    pair_pass = self.dtype == "f32" and self.pooled_dz_pass
                 else:
                     pair_pass = i in self.dz_pass_layers and self.pooled_dz_pass
                 l["dz_emit"] = bool(needs_dgrad and sup & B.FUSED_BWD_WEIGHT_DZ and not pair_pass)
@@ -324,8 +327,9 @@ class ConvStack:
                 else:
                     c(f"L{i+1}.pool_lrelu_bwd", B.cf_avgpool3d_lrelu_bwd, self.batch, *od, s["cout"], self.dtype, g,
                       l["mask"], self.alpha, l["dz"], l["db"], l["ws_b"], None, stream)
-                if self.side is None:
-                    # both plain products from dz in one call (one launch where the kernels allow)
+                if self.side is None and s["stride"] > 1:
+                    # both plain products from dz in one call (the stride-2 layer's share
+                    # one launch)
                     if d:
                         pend += c(f"L{i+1}.conv_bwd", B.cf_conv3d_bwd_deferred, l["desc"], self.layer_input(i),
                                   l["dz"], l["w"], l["dw"], l["dx"], l["ws_w"], None, stream)
@@ -334,12 +338,14 @@ class ConvStack:
                           l["dw"], l["dx"], l["ws_w"], None, stream)
                     g = l["dx"]
                     continue
-                main = stream if stream is not None else torch.cuda.current_stream()
-                ev = torch.cuda.Event()
-                ev.record(main)
-                self.side.wait_event(ev)
-                ws_ = self.side
-                side_used = True
+                ws_ = stream
+                if self.side is not None:
+                    main = stream if stream is not None else torch.cuda.current_stream()
+                    ev = torch.cuda.Event()
+                    ev.record(main)
+                    self.side.wait_event(ev)
+                    ws_ = self.side
+                    side_used = True
                 if d:
                     pend += c(f"L{i+1}.conv_bwd_weight", B.cf_conv3d_bwd_weight_deferred, l["desc"],
                               self.layer_input(i), l["dz"], l["dw"], l["ws_w"], None, ws_, rec=ws_)
