@@ -100,6 +100,37 @@ def test_wgrad_noalloc_validation(L):
     expect(B.CF_ERR_INVALID_ARG, B.cf_conv3d_bwd_weight_noalloc, bad, A, A + 0x100000, A + 0x200000, 0)
 
 
+def test_one_call_backward_validation(L):
+    """cf_conv3d_bwd and cf_conv3d_bwd_fused validate everything the two
+    calls they stand for validate, and reject a dx that overlaps the weight
+    gradient's outputs or workspace, before any device work."""
+    d = B.make_desc(1, (32, 32, 32), 32, 64, 4, 2, "same", "f32")
+    need = B.cf_conv3d_bwd_weight_workspace_size(d)
+    x, dz, w, dw, dx, ws = A, A + 0x1000000, A + 0x2000000, A + 0x3000000, A + 0x4000000, A + 0x5000000
+    expect(B.CF_ERR_WORKSPACE, B.cf_conv3d_bwd, d, x, dz, w, dw, dx, ws, need - 16, 0)
+    expect(B.CF_ERR_INVALID_ARG, B.cf_conv3d_bwd, d, x, dz, None, dw, dx, ws, need, 0)
+    expect(B.CF_ERR_ALIAS, B.cf_conv3d_bwd, d, x, dz, w, dw, dw + 0x40, ws, need, 0)   # dx over dW
+    expect(B.CF_ERR_ALIAS, B.cf_conv3d_bwd, d, x, dz, w, dw, ws + 0x40, ws, need, 0)   # dx over ws
+    expect(B.CF_ERR_ALIAS, B.cf_conv3d_bwd, d, x, dz, w, dw, x + 0x40, ws, need, 0)    # dx over x
+    deep = B.make_desc(1, (8, 8, 8), 64, 64, 3, 1, "same", "f32")
+    nf = B.cf_conv3d_bwd_weight_fused_workspace_size(deep, 0)
+    db = A + 0x6000000
+    expect(B.CF_ERR_WORKSPACE, B.cf_conv3d_bwd_fused, deep, x, dz, A + 0x7000000, w, 0.01, 0, dw, db, dx, ws,
+           nf - 16, 0)
+    expect(B.CF_ERR_INVALID_ARG, B.cf_conv3d_bwd_fused, deep, x, dz, A + 0x7000000, w, float("nan"), 0, dw, db,
+           dx, ws, nf, 0)
+    expect(B.CF_ERR_INVALID_ARG, B.cf_conv3d_bwd_fused, deep, x, dz, A + 0x7000000, w, 0.01, 4, dw, db, dx, ws,
+           nf, 0)
+    expect(B.CF_ERR_ALIAS, B.cf_conv3d_bwd_fused, deep, x, dz, A + 0x7000000, w, 0.01, 0, dw, db, db, ws, nf, 0)
+    expect(B.CF_ERR_ALIAS, B.cf_conv3d_bwd_fused, deep, x, dz, A + 0x7000000, w, 0.01, 0, dw, db, ws, ws, nf, 0)
+    # the pooled form where no fused backward-data exists (fp32 16 -> 32): unsupported
+    l2 = B.make_desc(1, (64, 64, 64), 16, 32, 4, 1, "same", "f32")
+    n2 = B.cf_conv3d_bwd_weight_fused_workspace_size(l2, B.CF_FUSE_POOL2)
+    P = [A + k * 0x10000000 for k in range(8)]  # 256 MiB apart: no overlap at this size
+    expect(B.CF_ERR_UNSUPPORTED, B.cf_conv3d_bwd_fused, l2, P[0], P[1], P[2], P[3], 0.01, B.CF_FUSE_POOL2, P[4],
+           P[5], P[6], P[7], n2, 0)
+
+
 def test_fused_flags(L):
     """Support bits of the fused entry points: the pooled form on the pooled
     layers, the (dy, y) form on unpooled fp32 layers, none for unknown flags."""
