@@ -57,13 +57,30 @@ __device__ __forceinline__ u32x4_t ld128(__amdgpu_buffer_rsrc_t r, uint32_t off)
 }
 
 
+// xcd_major: workgroup b (on XCD b % 8 by round-robin dispatch) takes grid
+// position xcd * per + b / 8 of the (x fastest, then y, z) order, so an XCD
+// runs a contiguous run of slices with all their row units and column groups,
+// and the input and gradient rows those share meet in that XCD's L2 (the
+// grid's size is a multiple of 8 when it is set)
 template <int GM, bool KW4, int RU, int FN, int WV, int PF>
 __global__ __launch_bounds__(64 * WV) void wgrad_f32_kernel(const float *__restrict__ x,
                                                             const float *__restrict__ g,
                                                             const void *__restrict__ aux,
                                                             float *__restrict__ part_w, float *__restrict__ part_b,
-                                                            float *__restrict__ dz_out, const WF32Params p) {
-  wgrad_f32_body<GM, KW4, RU, FN, WV, PF>(x, g, aux, part_w, part_b, dz_out, p, blockIdx.x, blockIdx.y, blockIdx.z);
+                                                            float *__restrict__ dz_out, const WF32Params p,
+                                                            int xcd_major) {
+  int bx = blockIdx.x, by = blockIdx.y, bz = blockIdx.z;
+  if (xcd_major) {
+    const int gx = gridDim.x, gy = gridDim.y;
+    const int b = bx + gx * (by + gy * bz);
+    const int per = gx * gy * (int)gridDim.z / 8;
+    const int j = (b & 7) * per + (b >> 3);
+    bx = j % gx;
+    const int t = j / gx;
+    by = t % gy;
+    bz = t / gy;
+  }
+  wgrad_f32_body<GM, KW4, RU, FN, WV, PF>(x, g, aux, part_w, part_b, dz_out, p, bx, by, bz);
 }
 
 // ---------------------------------------------------------------------------
@@ -291,13 +308,20 @@ WF32Params w_params(const ConvShape &s, const WPlan &pl, float alpha) {
   return p;
 }
 
+// CF_F32W_XCD=0 keeps the plain grid order of the weight-gradient workgroups
+bool xcd_env() {
+  const char *e = getenv("CF_F32W_XCD");
+  return !(e && e[0] == '0');
+}
+
 template <int GM, bool KW4, int RU, int FN>
 hipError_t launch_w(const WPlan &pl, const WF32Params &p, const float *x, const float *g, const void *aux,
                     float *pw, float *pb, float *dz_out, hipStream_t st) {
   dim3 grid(pl.gx, pl.gy, pl.nsplit);
   constexpr int PF = 2;
+  const int xm = ((long long)pl.gx * pl.gy * pl.nsplit) % 8 == 0 && xcd_env();
   hipLaunchKernelGGL((wgrad_f32_kernel<GM, KW4, RU, FN, 8, PF>), grid, dim3(512), 0, st, x, g, aux, pw, pb,
-                     dz_out, p);
+                     dz_out, p, xm);
   return hipGetLastError();
 }
 
