@@ -262,7 +262,10 @@ WPlan w_plan(const ConvShape &s, int gm) {
   //  on the 16 -> 32 layer, 218 -> 200 us; with the row values computed once per
   //  row, one is: 195 against 201 us, and half the partials).
   const bool shortk = vox < (1 << 16);
-  pl.ru = (fused ? !shortk : pl.units >= 64) ? 2 : 1;
+  // two row units per wave wherever the reduction is long: the A fragment's
+  // loads and the gradient operand then feed twice the MFMAs (the 16 -> 32
+  // layer's plain weight gradient on a stored dz: 171.5 -> 159.1 us)
+  pl.ru = (fused ? !shortk : (!shortk || pl.units >= 64)) ? 2 : 1;
   // CF_F32W_RU=1|2 overrides the row units per wave (measurement sweeps)
   if (const char *e = getenv("CF_F32W_RU")) pl.ru = atoi(e) == 1 ? 1 : 2;
   pl.wv = 8;
