@@ -272,7 +272,12 @@ WPlan w_plan(const ConvShape &s, int gm) {
   pl.gx = (pl.units + pl.ru * pl.wv - 1) / (pl.ru * pl.wv);
   pl.gy = s.co / (16 * pl.fn);
   const long long tiles = (long long)pl.gx * pl.gy;
-  long long target = shortk ? (fused ? kNumCUs : kNumCUs / 2) : kNumCUs;
+  // plain reductions of 2^18 voxels and more: two workgroups per compute unit
+  // (four waves per SIMD; the 16 -> 32 layer at 128^3 on a stored dz: step
+  // -4.5 us with twice the partials; at the paper's 60^3, 2^17.7 voxels, the
+  // doubled partials cost more than the waves gain: +3 us)
+  const bool longk = vox >= (1 << 18);
+  long long target = shortk ? (fused ? kNumCUs : kNumCUs / 2) : (!fused && longk ? 2 * kNumCUs : kNumCUs);
   // CF_F32W_TARGET overrides the workgroup target (measurement sweeps)
   if (const char *e = getenv("CF_F32W_TARGET")) target = std::max(1, atoi(e));
   long long want = std::max(1LL, (target + tiles - 1) / tiles);
