@@ -441,37 +441,44 @@ __global__ __launch_bounds__(256) void l1_wgrad_kernel(const uint16_t *__restric
     have = tile_origin(it + 1, nn, nd0, nh0, nw0);
     if (have) load_tile(nn, nd0, nh0, nw0);
 
-    // ---- MFMA over this wave's eight w-rows of 32 voxels ------------------
+    // ---- MFMA over this wave's eight w-rows of 32 voxels: the four w-rows
+    // (2a + i, 2b + j) of pooled rows (a, b) = wave and wave + 4, so that the
+    // pooled-gradient operand of a pooled row is formed once for its four rows
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const int row = wave + 4 * k;
-      const int ld = row / TH, lh = row % TH;
-      const unsigned char *dpb = reinterpret_cast<const unsigned char *>(dps) + ((ld >> 1) * 4 + (lh >> 1)) * 512;
+    for (int pp = 0; pp < 2; ++pp) {
+      const int prow = wave + 4 * pp;  // pooled row (a, b) = (prow / 4, prow % 4)
+      const unsigned char *dpb = reinterpret_cast<const unsigned char *>(dps) + prow * 512;
       const v4i16_t g = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t *)(dpb + dpoff));
       const uint32_t p0 = (uint32_t)(uint16_t)g[0] | ((uint32_t)(uint16_t)g[1] << 16);
       const uint32_t p1 = (uint32_t)(uint16_t)g[2] | ((uint32_t)(uint16_t)g[3] << 16);
-      uint32_t bu[4], bm[4];
+      uint32_t bu[4];
       bu[0] = __builtin_amdgcn_perm(p0, p0, 0x01000100u);
       bu[1] = __builtin_amdgcn_perm(p0, p0, 0x03020302u);
       bu[2] = __builtin_amdgcn_perm(p1, p1, 0x01000100u);
       bu[3] = __builtin_amdgcn_perm(p1, p1, 0x03020302u);
-      const uint4 mq = mks[row * 4 + q];
-      const uint32_t mk[4] = {mq.x, mq.y, mq.z, mq.w};
-      // mask dword d holds channel bits of voxels 2d (bits 0..15) and 2d+1 (16..31):
-      // move bit r and bit 16+r to the two sign positions, spread each over its half
-      typedef short v2i16_t __attribute__((ext_vector_type(2)));
-#pragma unroll
-      for (int d = 0; d < 4; ++d) {
-        const v2i16_t sg = __builtin_bit_cast(v2i16_t, mk[d] << (15 - r)) >> (v2i16_t){15, 15};
-        bm[d] = bu[d] & __builtin_bit_cast(uint32_t, sg);
-      }
       const bf16x8_t Bu = __builtin_bit_cast(bf16x8_t, make_uint4(bu[0], bu[1], bu[2], bu[3]));
-      const bf16x8_t Bm = __builtin_bit_cast(bf16x8_t, make_uint4(bm[0], bm[1], bm[2], bm[3]));
 #pragma unroll
-      for (int mf = 0; mf < MF; ++mf) {
-        const bf16x8_t a = __builtin_bit_cast(bf16x8_t, xs[(arow[mf] + ld * HH + lh) * XP + q]);
-        acc_u[mf] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, Bu, acc_u[mf], 0, 0, 0);
-        acc_m[mf] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, Bm, acc_m[mf], 0, 0, 0);
+      for (int k = 0; k < 4; ++k) {
+        const int ld = 2 * (prow >> 2) + (k >> 1), lh = 2 * (prow & 3) + (k & 1);
+        const int row = ld * TH + lh;
+        uint32_t bm[4];
+        const uint4 mq = mks[row * 4 + q];
+        const uint32_t mk[4] = {mq.x, mq.y, mq.z, mq.w};
+        // mask dword d holds channel bits of voxels 2d (bits 0..15) and 2d+1 (16..31):
+        // move bit r and bit 16+r to the two sign positions, spread each over its half
+        typedef short v2i16_t __attribute__((ext_vector_type(2)));
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+          const v2i16_t sg = __builtin_bit_cast(v2i16_t, mk[d] << (15 - r)) >> (v2i16_t){15, 15};
+          bm[d] = bu[d] & __builtin_bit_cast(uint32_t, sg);
+        }
+        const bf16x8_t Bm = __builtin_bit_cast(bf16x8_t, make_uint4(bm[0], bm[1], bm[2], bm[3]));
+#pragma unroll
+        for (int mf = 0; mf < MF; ++mf) {
+          const bf16x8_t a = __builtin_bit_cast(bf16x8_t, xs[(arow[mf] + ld * HH + lh) * XP + q]);
+          acc_u[mf] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, Bu, acc_u[mf], 0, 0, 0);
+          acc_m[mf] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, Bm, acc_m[mf], 0, 0, 0);
+        }
       }
     }
     __syncthreads();
