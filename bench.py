@@ -247,8 +247,7 @@ def run_stack(name, args, steps, warmup, extras):
     def step():
         st.forward()
         if args.with_head:
-            head.forward(st.output())
-            head.backward()
+            head.step(st.output())
             st.backward(head_dout)
         else:
             st.backward(dout)
@@ -325,24 +324,33 @@ def run_stack(name, args, steps, warmup, extras):
 
     # the FC head + loss alone (before any parameter update): forward and
     # backward twice, queued behind a step so that the device never waits for
-    # the host to submit its ~25 short launches
-    hts = []
-    for _ in range(5):
-        step()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(2):
-            head.forward(st.output())
-            head.backward()
-        e1.record()
-        hts.append((e0, e1))
-    torch.cuda.synchronize()
-    head_ms = float(np.mean([a.elapsed_time(b) for a, b in hts])) / 2
+    # the host to submit the launches; the one-call head (four launches) and,
+    # for reference, the per-layer calls (22 launches)
+    def head_time(fn):
+        hts = []
+        for _ in range(5):
+            step()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(2):
+                fn()
+            e1.record()
+            hts.append((e0, e1))
+        torch.cuda.synchronize()
+        return float(np.mean([a.elapsed_time(b) for a, b in hts])) / 2
+
+    def per_layer():
+        head.forward(st.output())
+        head.backward()
+
+    per_layer_ms = head_time(per_layer)
+    head_ms = head_time(lambda: head.step(st.output()))
     head_bytes = head.weight_bytes()
     head_gbs = head_bytes / (head_ms * 1e-3) / 1e9
     out["head"] = dict(widths=[feats, *inputs.HEAD_WIDTHS], ms=round(head_ms, 4),
                        algorithmic_bytes=head_bytes, achieved=round(head_gbs, 1), unit="GB/s", peak=HBM_PEAK_GBS,
-                       frac=round(head_gbs / HBM_PEAK_GBS, 4), in_step=args.with_head,
+                       frac=round(head_gbs / HBM_PEAK_GBS, 4), in_step=args.with_head, one_call=head.fused,
+                       per_layer_ms=round(per_layer_ms, 4),
                        loss=round(float(head.loss[0].item()), 6))
 
     # the parameter update alone, after the timed steps (it changes the weights):

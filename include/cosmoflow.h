@@ -476,6 +476,41 @@ cf_status cf_fc_bwd_weight(int32_t m, int32_t k, int32_t n, int32_t dtype, const
 cf_status cf_mse_loss(int32_t m, int32_t n, int32_t dtype, const void *p, const float *t,
                       float *loss, void *dp, void *stream);
 
+/* The whole head in one call (Section III-A: fully-connected layers with
+ * leaky ReLU after the convolutions; the loss as cf_mse_loss reads it):
+ * forward, loss and backward of nlayers layers of widths dims[0] -> dims[1]
+ * -> ... -> dims[nlayers], in four kernel launches -- the first layer's
+ * split-K forward, its column sums with bias and leaky ReLU, one workgroup
+ * for the rest of the forward, the loss and the later layers' backward
+ * (their weights and activations held in LDS), and one pass over the first
+ * layer's W for its dW and dx.  The results are
+ * those of the per-layer calls (cf_fc_fwd, cf_bias_lrelu_fwd, cf_mse_loss,
+ * cf_bias_lrelu_bwd, cf_fc_bwd_weight, cf_fc_bwd_data) with the same rounding
+ * points; the first layer's y, dW and dx are bitwise those calls' results
+ * (given the same dz), the later layers' sums take their own fixed order.
+ * Deterministic.
+ *   x [m][dims[0]] (dtype), w[i] [dims[i]][dims[i+1]] (dtype), b[i] fp32
+ *   [dims[i+1]], target fp32 [m][dims[nlayers]];
+ *   outputs: y[i] [m][dims[i+1]] = lrelu(z + b) (dtype); loss (one fp32);
+ *   dz[i] [m][dims[i+1]] (dtype) = dL/dy[i] * slope (dL/dy of the last layer
+ *   is the loss gradient rounded to dtype); db[i] fp32 [dims[i+1]]; dw[i] fp32
+ *   [dims[i]][dims[i+1]]; dx[i] [m][dims[i]] (dtype) the gradient of layer
+ *   i's input (dx[0]: of x).
+ * Limits (else CF_ERR_UNSUPPORTED, nothing launched): 2 <= nlayers <= 4,
+ * 1 <= m <= 8; dims[0] a multiple of 8 below 2^31; dims[1] / V a power of
+ * two from 8 to 64 (V = 8 for bf16, 4 for fp32); every later width <= 512,
+ * m * (dims[1] + ... + dims[nlayers]) <= 8192 and the sum over the later
+ * layers of dims[i] * (dims[i+1] + 1) <= 16384.  Every pointer (the arrays
+ * are host arrays of nlayers device pointers) non-NULL and 16-byte aligned;
+ * no output may overlap an input or another output (CF_ERR_ALIAS).
+ * ws: cf_fc_head_workspace_size() bytes (the first layer's partial sums),
+ * no initialisation needed. */
+size_t cf_fc_head_workspace_size(int32_t m, int32_t nlayers, const int32_t *dims);
+cf_status cf_fc_head(int32_t m, int32_t nlayers, const int32_t *dims, int32_t dtype, const void *x,
+                     const void *const *w, const float *const *b, float alpha, const float *target, void *const *y,
+                     void *const *dz, void *const *dx, float *const *dw, float *const *db, float *loss, void *ws,
+                     size_t ws_bytes, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -38,6 +38,7 @@ EXPORTS = [
     "cf_conv3d_bwd_data_fused", "cf_reduce_partials", "cf_conv3d_bwd_weight_deferred", "cf_bias_lrelu_bwd_deferred",
     "cf_conv3d_bwd_weight_fused_deferred", "cf_adam_larc_workspace_size", "cf_adam_larc_step",
     "cf_fc_fwd_workspace_size", "cf_fc_fwd", "cf_fc_bwd_data", "cf_fc_bwd_weight", "cf_mse_loss",
+    "cf_fc_head_workspace_size", "cf_fc_head",
     "cf_conv3d_bwd_weight_noalloc", "cf_avgpool3d_lrelu_bwd_workspace_size", "cf_avgpool3d_lrelu_bwd",
     "cf_avgpool3d_lrelu_bwd_deferred", "cf_conv3d_bwd_fused", "cf_conv3d_bwd_fused_deferred",
     "cf_conv3d_bwd", "cf_conv3d_bwd_deferred",
@@ -144,6 +145,10 @@ def lib():
         "cf_fc_bwd_data": ([i32, i32, i32, i32, vp, vp, vp, vp], ctypes.c_int),
         "cf_fc_bwd_weight": ([i32, i32, i32, i32, vp, vp, vp, vp], ctypes.c_int),
         "cf_mse_loss": ([i32, i32, i32, vp, vp, vp, vp, vp], ctypes.c_int),
+        "cf_fc_head_workspace_size": ([i32, i32, ctypes.POINTER(i32)], sz),
+        "cf_fc_head": ([i32, i32, ctypes.POINTER(i32), i32, vp, ctypes.POINTER(vp), ctypes.POINTER(vp), f32, vp,
+                        ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp), ctypes.POINTER(vp),
+                        ctypes.POINTER(vp), vp, vp, sz, vp], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         f = getattr(L, name)
@@ -436,6 +441,28 @@ def cf_fc_bwd_data(m, k, n, dtype, dz, w, dx, stream=None):
 
 def cf_fc_bwd_weight(m, k, n, dtype, x, dz, dw, stream=None):
     _check(lib().cf_fc_bwd_weight(m, k, n, dtype_code(dtype), _ptr(x), _ptr(dz), _ptr(dw), _stream(stream)))
+
+
+def _i32s(v):
+    return (ctypes.c_int32 * len(v))(*[int(a) for a in v])
+
+
+def _ptrs(ts):
+    """Host array of the device pointers of a list of tensors."""
+    return (ctypes.c_void_p * max(len(ts), 1))(*[_ptr(t) for t in ts])
+
+
+def cf_fc_head_workspace_size(m, dims) -> int:
+    return int(lib().cf_fc_head_workspace_size(m, len(dims) - 1, _i32s(dims)))
+
+
+def cf_fc_head(m, dims, dtype, x, w, b, alpha, target, y, dz, dx, dw, db, loss, ws, ws_bytes=None, stream=None):
+    """Forward, loss and backward of the whole head (lists of per-layer tensors)."""
+    if ws_bytes is None:
+        ws_bytes = 0 if ws is None or isinstance(ws, int) else ws.numel() * ws.element_size()
+    _check(lib().cf_fc_head(m, len(dims) - 1, _i32s(dims), dtype_code(dtype), _ptr(x), _ptrs(w), _ptrs(b),
+                            float(alpha), _ptr(target), _ptrs(y), _ptrs(dz), _ptrs(dx), _ptrs(dw), _ptrs(db),
+                            _ptr(loss), _ptr(ws), ws_bytes, _stream(stream)))
 
 
 def cf_mse_loss(m, n, dtype, p, t, loss, dp, stream=None):

@@ -894,6 +894,67 @@ cf_status cf_fc_bwd_weight(int32_t m, int32_t k, int32_t n, int32_t dtype, const
   return finish(cf::launch_fc_bwd_weight(m, k, n, kdt(dtype), x, dz, dw, st), st, "cf_fc_bwd_weight");
 }
 
+size_t cf_fc_head_workspace_size(int32_t m, int32_t nlayers, const int32_t *dims) {
+  if (!dims || nlayers < 2 || nlayers > 4 || m < 1) return 0;
+  int d[5];
+  for (int i = 0; i <= nlayers; ++i) {
+    if (dims[i] < 1) return 0;
+    d[i] = dims[i];
+  }
+  return cf::fc_head_workspace(m, nlayers, d);
+}
+
+cf_status cf_fc_head(int32_t m, int32_t nlayers, const int32_t *dims, int32_t dtype, const void *x,
+                     const void *const *w, const float *const *b, float alpha, const float *target, void *const *y,
+                     void *const *dz, void *const *dx, float *const *dw, float *const *db, float *loss, void *ws,
+                     size_t ws_bytes, void *stream) {
+  if (dtype != CF_F32 && dtype != CF_BF16) return fail(CF_ERR_INVALID_ARG, "unknown dtype");
+  if (!dims || !w || !b || !y || !dz || !dx || !dw || !db)
+    return fail(CF_ERR_INVALID_ARG, "fc_head: NULL dims or pointer array");
+  if (nlayers < 2 || nlayers > 4) return fail(CF_ERR_UNSUPPORTED, "fc_head: 2 to 4 layers");
+  if (m < 1 || m > 8) return fail(CF_ERR_UNSUPPORTED, "fc_head: 1 to 8 batch rows");
+  int d[5];
+  for (int i = 0; i <= nlayers; ++i) {
+    if (dims[i] < 1) return fail(CF_ERR_INVALID_ARG, "fc_head: every width must be > 0");
+    d[i] = dims[i];
+  }
+  if (!cf::fc_head_supported(m, nlayers, d, kdt(dtype)))
+    return fail(CF_ERR_UNSUPPORTED, "fc_head: widths outside the fused head's limits (see cf_fc_head)");
+  cf_status r;
+  if ((r = check_ptrs({x, target, loss, ws})) != CF_OK) return r;
+  const size_t es = elem_size(dtype);
+  // (pointer, bytes) of every input and every output
+  std::vector<std::pair<const void *, size_t>> in, out;
+  in.push_back({x, (size_t)m * d[0] * es});
+  in.push_back({target, (size_t)m * d[nlayers] * 4});
+  for (int i = 0; i < nlayers; ++i) {
+    if ((r = check_ptrs({w[i], b[i], y[i], dz[i], dx[i], dw[i], db[i]})) != CF_OK) return r;
+    const size_t kn = (size_t)d[i] * d[i + 1];
+    in.push_back({w[i], kn * es});
+    in.push_back({b[i], (size_t)d[i + 1] * 4});
+    out.push_back({y[i], (size_t)m * d[i + 1] * es});
+    out.push_back({dz[i], (size_t)m * d[i + 1] * es});
+    out.push_back({dx[i], (size_t)m * d[i] * es});
+    out.push_back({dw[i], kn * 4});
+    out.push_back({db[i], (size_t)d[i + 1] * 4});
+  }
+  out.push_back({loss, 4});
+  const size_t need = cf::fc_head_workspace(m, nlayers, d);
+  if (ws_bytes < need) return fail(CF_ERR_WORKSPACE, "fc_head: workspace smaller than cf_fc_head_workspace_size()");
+  out.push_back({ws, need});
+  for (size_t i = 0; i < out.size(); ++i) {
+    for (const auto &t : in)
+      if (overlap(out[i].first, out[i].second, t.first, t.second))
+        return fail(CF_ERR_ALIAS, "fc_head: an output or the workspace overlaps an input");
+    for (size_t j = i + 1; j < out.size(); ++j)
+      if (overlap(out[i].first, out[i].second, out[j].first, out[j].second))
+        return fail(CF_ERR_ALIAS, "fc_head: two outputs overlap");
+  }
+  hipStream_t st = (hipStream_t)stream;
+  return finish(cf::launch_fc_head(m, nlayers, d, kdt(dtype), x, w, b, alpha, target, y, dz, dx, dw, db, loss, ws, st),
+                st, "cf_fc_head");
+}
+
 cf_status cf_mse_loss(int32_t m, int32_t n, int32_t dtype, const void *p, const float *t, float *loss, void *dp,
                       void *stream) {
   if (m <= 0 || n <= 0) return fail(CF_ERR_INVALID_ARG, "mse_loss: m and n must be > 0");

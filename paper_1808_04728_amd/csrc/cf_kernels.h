@@ -236,6 +236,15 @@ hipError_t launch_fc_bwd_data(int M, int K, int N, int dtype, const void *dz, co
 hipError_t launch_fc_bwd_weight(int M, int K, int N, int dtype, const void *x, const void *dz, float *dw,
                                 hipStream_t st);
 // mean squared error over n predictions; inv = 1 / n; dp may be null
+// The whole head (fc.hip): first layer split-K forward and its column sums
+// with bias and leaky ReLU, one workgroup for the rest of the forward, the
+// loss and the later layers' backward, one pass for the first layer's dW and dx.
+bool fc_head_supported(int M, int L, const int *dims, int dtype);
+size_t fc_head_workspace(int M, int L, const int *dims);
+hipError_t launch_fc_head(int M, int L, const int *dims, int dtype, const void *x, const void *const *w,
+                          const float *const *b, float alpha, const float *target, void *const *y, void *const *dz,
+                          void *const *dx, float *const *dw, float *const *db, float *loss, void *ws,
+                          hipStream_t st);
 hipError_t launch_mse_loss(long long n, int dtype, const void *p, const float *t, float *loss, void *dp,
                            float inv, hipStream_t st);
 

@@ -120,9 +120,12 @@ __global__ __launch_bounds__(256) void fc_fwd_kernel(const typename Store<DT>::T
 // y[m0 + i] = RNE(sum over the rows of the partial matrix [rows][cols]):
 // 16 columns per workgroup, 16 row phases per column (phase p sums rows p,
 // p + 16, ... in order, eight loads in flight), phases combined in order.
-template <int DT>
+// BIAS_ACT: then y = lrelu(y + bias[col % n]) rounded again, as the per-layer
+// bias + leaky ReLU call does on the stored z.
+template <int DT, bool BIAS_ACT = false>
 __global__ __launch_bounds__(256) void fc_finalize_kernel(const float *__restrict__ part, int rows, int cols,
-                                                          typename Store<DT>::T *y) {
+                                                          typename Store<DT>::T *y, const float *__restrict__ bias = nullptr,
+                                                          int n = 1, float alpha = 0.f) {
   __shared__ float red[16][16];
   const int tid = threadIdx.x, cl = tid & 15, ph = tid >> 4;
   const int col = (int)blockIdx.x * 16 + cl;
@@ -144,7 +147,12 @@ __global__ __launch_bounds__(256) void fc_finalize_kernel(const float *__restric
     float t = 0.f;
 #pragma unroll
     for (int p = 0; p < 16; ++p) t += red[p][cl];
-    y[col] = from_f32<DT>(t);
+    if constexpr (BIAS_ACT) {
+      const float u = to_f32<DT>(from_f32<DT>(t)) + bias[col % n];
+      y[col] = from_f32<DT>(u > 0.f ? u : alpha * u);
+    } else {
+      y[col] = from_f32<DT>(t);
+    }
   }
 }
 
@@ -472,6 +480,260 @@ __global__ __launch_bounds__(256) void mse_loss_kernel(const typename Store<DT>:
   if (tid == 0) loss[0] = red[0] * inv;
 }
 
+// ---- the whole head in four launches ----------------------------------------
+// (1) fc_fwd_kernel: the first layer's split-K partial rows (as cf_fc_fwd);
+// (2) fc_finalize_kernel<BIAS_ACT>: their column sums with bias and leaky ReLU;
+// (3) fc_head_tail_kernel, one workgroup: every later layer forward from LDS,
+//     the loss, every later layer backward, and the first layer's leaky-ReLU
+//     backward (dz1, db1);
+// (4) fc_head_bwd1_kernel: the first layer's dW and dx in one pass over W.
+// The layers after the first are a few thousand weights (the network's 128 ->
+// 64 -> 3): their weights and activations live in LDS.  Rounding points are
+// those of the per-layer calls (z and y rounded to the dtype, dz rounded, db
+// summing the unrounded products), and the first layer's y, dW and dx are the
+// per-layer kernels' sums in the same order.
+
+constexpr int HEAD_MAX_L = 4;    // layers
+constexpr int HEAD_MAX_W = 512;  // width of every layer's output
+constexpr int HEAD_ACT = 8192;   // batch rows x (sum of the output widths), fp32 in LDS
+constexpr int HEAD_WT = 16384;   // weights after the first layer, rows padded by one (fp32 in LDS)
+
+struct HeadParams {
+  int m, L;  // batch rows, layers
+  int dims[HEAD_MAX_L + 1];
+  float alpha, inv;  // inv = 1 / (m * dims[L])
+  const void *w[HEAD_MAX_L];
+  const float *b[HEAD_MAX_L];
+  const float *target;
+  void *y[HEAD_MAX_L];
+  void *dz[HEAD_MAX_L];
+  void *dx[HEAD_MAX_L];
+  float *dw[HEAD_MAX_L];
+  float *db[HEAD_MAX_L];
+  float *loss;
+};
+
+template <int DT>
+__global__ __launch_bounds__(1024) void fc_head_tail_kernel(const HeadParams p) {
+  using T = typename Store<DT>::T;
+  __shared__ float wl[HEAD_WT];         // layer i >= 1: [K][N + 1]
+  __shared__ float ys[HEAD_ACT];        // layer i: y [m][N] (fp32 values of the stored dtype)
+  __shared__ float gb[8 * HEAD_MAX_W];  // gradient of the current layer's output
+  __shared__ float zb[8 * HEAD_MAX_W];  // dz of the current layer (rounded)
+  __shared__ float red[1024];
+  __shared__ float bl[HEAD_MAX_L * HEAD_MAX_W];  // biases of layers 1 .. L-1
+  const int tid = threadIdx.x, m = p.m, L = p.L;
+  const float alpha = p.alpha;
+
+  // Everything the workgroup reads from global memory, in one round: the
+  // weights of layers 1 .. L-1 (16-byte loads), their biases, the target (in
+  // zb until the loss) and layer 0's y (written by the finalize kernel).
+  {
+    constexpr int EV = 16 / sizeof(T);
+    int off = 0;
+    for (int i = 1; i < L; ++i) {
+      const int K = p.dims[i], N = p.dims[i + 1], KN = K * N, nv = KN / EV;
+      const T *w = (const T *)p.w[i];
+      for (int v = tid; v < nv; v += 1024) {
+        Vec16<DT> u;
+        u.u = ld16<false>(w + (long long)v * EV);
+#pragma unroll
+        for (int e = 0; e < EV; ++e) {
+          const int q = v * EV + e, k = q / N, j = q - k * N;
+          wl[off + k * (N + 1) + j] = to_f32<DT>(u.e[e]);
+        }
+      }
+      for (int q = nv * EV + tid; q < KN; q += 1024) {
+        const int k = q / N, j = q - k * N;
+        wl[off + k * (N + 1) + j] = to_f32<DT>(w[q]);
+      }
+      for (int j = tid; j < N; j += 1024) bl[(i - 1) * HEAD_MAX_W + j] = p.b[i][j];
+      off += K * (N + 1);
+    }
+    for (int o = tid; o < m * p.dims[L]; o += 1024) zb[o] = p.target[o];
+    for (int o = tid; o < m * p.dims[1]; o += 1024) ys[o] = to_f32<DT>(((const T *)p.y[0])[o]);
+  }
+  __syncthreads();
+  // layers 1 .. L-1 forward: z = y_prev W (k ascending), rounded; y = lrelu(z + b)
+  int yo = 0, wo = 0;
+  for (int i = 1; i < L; ++i) {
+    const int K = p.dims[i], N = p.dims[i + 1];
+    const int yin = yo, yout = yo + m * K;
+    for (int o = tid; o < m * N; o += 1024) {
+      const int mm = o / N, j = o - mm * N;
+      float acc = 0.f;
+#pragma unroll 16
+      for (int k = 0; k < K; ++k) acc = fmaf(ys[yin + mm * K + k], wl[wo + k * (N + 1) + j], acc);
+      const T z = from_f32<DT>(acc);
+      const float u = to_f32<DT>(z) + bl[(i - 1) * HEAD_MAX_W + j];
+      const T y = from_f32<DT>(u > 0.f ? u : alpha * u);
+      ((T *)p.y[i])[o] = y;
+      ys[yout + o] = to_f32<DT>(y);
+    }
+    yo = yout;
+    wo += K * (N + 1);
+    __syncthreads();
+  }
+  // loss = sum e^2 / (m n), dL/dy = 2 e / (m n) rounded to the dtype
+  {
+    const int n = m * p.dims[L];
+    float s = 0.f;
+    for (int o = tid; o < n; o += 1024) {
+      const float e = ys[yo + o] - zb[o];
+      s = fmaf(e, e, s);
+      gb[o] = to_f32<DT>(from_f32<DT>(2.f * e * p.inv));
+    }
+    red[tid] = s;
+    __syncthreads();  // also: the target in zb is read
+    for (int h = 512; h > 0; h >>= 1) {
+      if (tid < h) red[tid] += red[tid + h];
+      __syncthreads();
+    }
+    if (tid == 0) p.loss[0] = red[0] * p.inv;
+  }
+  // backward, layer L-1 down to 0
+  for (int i = L - 1; i >= 0; --i) {
+    const int N = p.dims[i + 1];
+    // dz = g * slope(y), rounded; db = sum over the batch rows of the unrounded products
+    for (int o = tid; o < m * N; o += 1024) {
+      const float d = gb[o] * (ys[yo + o] > 0.f ? 1.f : alpha);
+      const T dzv = from_f32<DT>(d);
+      ((T *)p.dz[i])[o] = dzv;
+      zb[o] = to_f32<DT>(dzv);
+    }
+    for (int j = tid; j < N; j += 1024) {
+      float s = 0.f;
+#pragma unroll 8
+      for (int mm = 0; mm < m; ++mm) s += gb[mm * N + j] * (ys[yo + mm * N + j] > 0.f ? 1.f : alpha);
+      p.db[i][j] = s;
+    }
+    __syncthreads();
+    if (i == 0) break;
+    const int K = p.dims[i];
+    const int yin = yo - m * K;
+    wo -= K * (N + 1);
+    // dW[k][j] = sum over the batch rows (ascending) of y_prev[mm][k] dz[mm][j]
+    for (int e = tid; e < K * N; e += 1024) {
+      const int k = e / N, j = e - k * N;
+      float acc = 0.f;
+#pragma unroll 8
+      for (int mm = 0; mm < m; ++mm) acc = fmaf(ys[yin + mm * K + k], zb[mm * N + j], acc);
+      p.dw[i][e] = acc;
+    }
+    // dx[mm][k] = sum over j (ascending) of dz[mm][j] W[k][j], rounded: the next g
+    for (int o = tid; o < m * K; o += 1024) {
+      const int mm = o / K, k = o - mm * K;
+      float acc = 0.f;
+#pragma unroll 16
+      for (int j = 0; j < N; ++j) acc = fmaf(zb[mm * N + j], wl[wo + k * (N + 1) + j], acc);
+      const T v = from_f32<DT>(acc);
+      ((T *)p.dx[i])[o] = v;
+      gb[o] = to_f32<DT>(v);
+    }
+    yo = yin;
+    __syncthreads();
+  }
+}
+
+// First layer backward: lane gl of a G-lane group owns columns [V gl, V gl + V)
+// of dz (resident in registers for all batch rows); a group walks blocks of
+// eight rows k of W.  dx[mm][k]: the lane's V products in column order, then
+// an xor butterfly over the group (the order of fc_bwd_data_kernel); dW[k][c]:
+// the batch rows in ascending order (that of fc_bwd_weight_blk_kernel).
+template <int DT, int G>
+__global__ __launch_bounds__(256) void fc_head_bwd1_kernel(const typename Store<DT>::T *__restrict__ x,
+                                                           const typename Store<DT>::T *__restrict__ dz,
+                                                           const typename Store<DT>::T *__restrict__ w,
+                                                           float *__restrict__ dw, typename Store<DT>::T *__restrict__ dx,
+                                                           int M, int K, int N) {
+  using T = typename Store<DT>::T;
+  constexpr int V = Store<DT>::VEC;
+  constexpr int XV = 16 / sizeof(T);  // elements of a 16-byte load
+  const int tid = threadIdx.x, gl = tid & (G - 1);
+  constexpr int GROUPS = 256 / G;
+  float dzr[MB][V];
+#pragma unroll
+  for (int mm = 0; mm < MB; ++mm) {
+    if (mm < M) {
+      Vec16<DT> g;
+      g.u = ld16<false>(dz + (long long)mm * N + gl * V);
+#pragma unroll
+      for (int j = 0; j < V; ++j) dzr[mm][j] = to_f32<DT>(g.e[j]);
+    } else {
+#pragma unroll
+      for (int j = 0; j < V; ++j) dzr[mm][j] = 0.f;
+    }
+  }
+  const int nblk = K / 8;
+  for (int kb = (int)blockIdx.x * GROUPS + tid / G; kb < nblk; kb += (int)gridDim.x * GROUPS) {
+    const long long k0 = (long long)kb * 8;
+    // x[mm][k0 .. k0 + 7] for every batch row
+    float xv[MB][8];
+#pragma unroll
+    for (int mm = 0; mm < MB; ++mm) {
+      if (mm < M) {
+#pragma unroll
+        for (int h = 0; h < 8 / XV; ++h) {
+          Vec16<DT> v;
+          v.u = ld16<false>(x + (long long)mm * K + k0 + h * XV);
+#pragma unroll
+          for (int e = 0; e < XV; ++e) xv[mm][h * XV + e] = to_f32<DT>(v.e[e]);
+        }
+      } else {
+#pragma unroll
+        for (int r = 0; r < 8; ++r) xv[mm][r] = 0.f;
+      }
+    }
+    float dxo[8];  // lane mm < M: dx[mm][k0 + r]
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      const long long k = k0 + r;
+      Vec16<DT> wv;
+      wv.u = ld16<false>(w + k * N + gl * V);
+      float wf[V];
+#pragma unroll
+      for (int j = 0; j < V; ++j) wf[j] = to_f32<DT>(wv.e[j]);
+      // dW row k, this lane's columns
+      float a[V];
+#pragma unroll
+      for (int j = 0; j < V; ++j) a[j] = 0.f;
+#pragma unroll
+      for (int mm = 0; mm < MB; ++mm)
+        if (mm < M)
+#pragma unroll
+          for (int j = 0; j < V; ++j) a[j] = fmaf(xv[mm][r], dzr[mm][j], a[j]);
+#pragma unroll
+      for (int j = 0; j < V; j += 4)
+        *reinterpret_cast<float4 *>(dw + k * N + gl * V + j) = make_float4(a[j], a[j + 1], a[j + 2], a[j + 3]);
+      // dx column k
+      float acc[MB];
+#pragma unroll
+      for (int mm = 0; mm < MB; ++mm) {
+        acc[mm] = 0.f;
+#pragma unroll
+        for (int j = 0; j < V; ++j) acc[mm] = fmaf(dzr[mm][j], wf[j], acc[mm]);
+      }
+#pragma unroll
+      for (int off = G >> 1; off > 0; off >>= 1)
+#pragma unroll
+        for (int mm = 0; mm < MB; ++mm) acc[mm] += __shfl_xor(acc[mm], off, 64);
+      dxo[r] = acc[0];
+#pragma unroll
+      for (int mm = 1; mm < MB; ++mm)
+        if (gl == mm) dxo[r] = acc[mm];
+    }
+    if (gl < M) {
+      Vec16<DT> o;
+#pragma unroll
+      for (int h = 0; h < 8 / XV; ++h) {
+#pragma unroll
+        for (int e = 0; e < XV; ++e) o.e[e] = from_f32<DT>(dxo[h * XV + e]);
+        *reinterpret_cast<uint4 *>(dx + (long long)gl * K + k0 + h * XV) = o.u;
+      }
+    }
+  }
+}
+
 }  // namespace
 
 size_t fc_fwd_workspace(int M, int K, int N) {
@@ -497,6 +759,73 @@ hipError_t launch_fc_bwd_weight(int M, int K, int N, int dtype, const void *x, c
                                 hipStream_t st) {
   return dtype == DT_BF16 ? fc_bwd_weight_t<DT_BF16>(M, K, N, x, dz, dw, st)
                           : fc_bwd_weight_t<DT_F32>(M, K, N, x, dz, dw, st);
+}
+
+bool fc_head_supported(int M, int L, const int *dims, int dtype) {
+  if (L < 2 || L > HEAD_MAX_L || M < 1 || M > MB) return false;
+  const int V = dtype == DT_BF16 ? Store<DT_BF16>::VEC : Store<DT_F32>::VEC;
+  const long long K0 = dims[0], N1 = dims[1];
+  if (K0 < 8 || K0 % 8 != 0 || K0 >= (1LL << 31) || N1 % V != 0) return false;
+  const long long g = N1 / V;  // lanes per row of the first layer's backward: a power of two, 8 .. 64
+  if (g < 8 || g > 64 || (g & (g - 1)) != 0 || K0 * N1 >= (1LL << 40)) return false;
+  long long act = 0, wts = 0;
+  for (int i = 1; i <= L; ++i) {
+    if (dims[i] < 1 || dims[i] > HEAD_MAX_W) return false;
+    act += (long long)M * dims[i];
+    if (i < L) wts += (long long)dims[i] * (dims[i + 1] + 1);
+  }
+  return act <= HEAD_ACT && wts <= HEAD_WT;
+}
+
+size_t fc_head_workspace(int M, int L, const int *dims) { return fc_fwd_workspace(M, dims[0], dims[1]); }
+
+hipError_t launch_fc_head(int M, int L, const int *dims, int dtype, const void *x, const void *const *w,
+                          const float *const *b, float alpha, const float *target, void *const *y, void *const *dz,
+                          void *const *dx, float *const *dw, float *const *db, float *loss, void *ws,
+                          hipStream_t st) {
+  const int K0 = dims[0], N1 = dims[1];
+  const int V = dtype == DT_BF16 ? Store<DT_BF16>::VEC : Store<DT_F32>::VEC;
+  const FwdPlan pl = plan_fwd(K0, N1, V);
+  float *part = (float *)ws;
+  HeadParams hp{};
+  hp.m = M; hp.L = L;
+  for (int i = 0; i <= L; ++i) hp.dims[i] = dims[i];
+  hp.alpha = alpha;
+  hp.inv = (float)(1.0 / ((double)M * dims[L]));
+  for (int i = 0; i < L; ++i) {
+    hp.w[i] = w[i]; hp.b[i] = b[i]; hp.y[i] = y[i]; hp.dz[i] = dz[i]; hp.dx[i] = dx[i];
+    hp.dw[i] = dw[i]; hp.db[i] = db[i];
+  }
+  hp.target = target;
+  hp.loss = loss;
+  const int G = N1 / V;
+  const int blocks = std::min((K0 / 8 + 256 / G - 1) / (256 / G), 2 * kNumCUs);
+#define CF_HEAD_LAUNCH(DTV, TT)                                                                                    \
+  {                                                                                                                \
+    hipLaunchKernelGGL((fc_fwd_kernel<DTV, true>), dim3(pl.blocks), dim3(256), 0, st, (const TT *)x,              \
+                       (const TT *)w[0], part, 0, M, K0, N1, pl.cgw, pl.np, pl.kc);                                \
+    hipError_t e = hipGetLastError();                                                                              \
+    if (e != hipSuccess) return e;                                                                                 \
+    hipLaunchKernelGGL((fc_finalize_kernel<DTV, true>), dim3((M * N1 + 15) / 16), dim3(256), 0, st, part,          \
+                       pl.blocks, M * N1, (TT *)y[0], b[0], N1, alpha);                                            \
+    if ((e = hipGetLastError()) != hipSuccess) return e;                                                           \
+    hipLaunchKernelGGL((fc_head_tail_kernel<DTV>), dim3(1), dim3(1024), 0, st, hp);                               \
+    if ((e = hipGetLastError()) != hipSuccess) return e;                                                           \
+    switch (G) {                                                                                                   \
+      case 8: hipLaunchKernelGGL((fc_head_bwd1_kernel<DTV, 8>), dim3(blocks), dim3(256), 0, st, (const TT *)x,     \
+                                 (const TT *)dz[0], (const TT *)w[0], dw[0], (TT *)dx[0], M, K0, N1); break;       \
+      case 16: hipLaunchKernelGGL((fc_head_bwd1_kernel<DTV, 16>), dim3(blocks), dim3(256), 0, st, (const TT *)x,   \
+                                  (const TT *)dz[0], (const TT *)w[0], dw[0], (TT *)dx[0], M, K0, N1); break;      \
+      case 32: hipLaunchKernelGGL((fc_head_bwd1_kernel<DTV, 32>), dim3(blocks), dim3(256), 0, st, (const TT *)x,   \
+                                  (const TT *)dz[0], (const TT *)w[0], dw[0], (TT *)dx[0], M, K0, N1); break;      \
+      default: hipLaunchKernelGGL((fc_head_bwd1_kernel<DTV, 64>), dim3(blocks), dim3(256), 0, st, (const TT *)x,   \
+                                  (const TT *)dz[0], (const TT *)w[0], dw[0], (TT *)dx[0], M, K0, N1); break;      \
+    }                                                                                                              \
+    return hipGetLastError();                                                                                      \
+  }
+  if (dtype == DT_BF16) CF_HEAD_LAUNCH(DT_BF16, uint16_t)
+  CF_HEAD_LAUNCH(DT_F32, float)
+#undef CF_HEAD_LAUNCH
 }
 
 hipError_t launch_mse_loss(long long n, int dtype, const void *p, const float *t, float *loss, void *dp,

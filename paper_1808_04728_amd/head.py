@@ -12,7 +12,9 @@ error of the three outputs over the batch.
             of the convolution stack's output)
 
 Every step is one ``binding`` call (a HIP kernel); PyTorch allocates the
-buffers once and supplies the stream.
+buffers once and supplies the stream.  ``step`` runs forward, loss and
+backward through one cf_fc_head call (four launches) where the widths allow
+it, with the same outputs.
 """
 from __future__ import annotations
 
@@ -45,6 +47,9 @@ class FCHead:
         self.loss = torch.zeros(4, dtype=torch.float32, device=dev)
         ws = max(B.cf_fc_fwd_workspace_size(batch, self.dims[i], self.dims[i + 1]) for i in range(L))
         ws = max(ws, max(B.cf_bias_lrelu_bwd_workspace_size(batch, self.dims[i + 1]) for i in range(L)))
+        self.fused = B.cf_fc_head_workspace_size(batch, self.dims) > 0 and self._fused_fits()
+        if self.fused:
+            ws = max(ws, B.cf_fc_head_workspace_size(batch, self.dims))
         self.ws = torch.empty(max(ws, 16), dtype=torch.uint8, device=dev)
         self.x = None
 
@@ -80,6 +85,30 @@ class FCHead:
             B.cf_fc_bwd_weight(self.m, k, n, self.dtype, xin, self.dz[i], self.dw[i], stream=stream)
             B.cf_fc_bwd_data(self.m, k, n, self.dtype, self.dz[i], self.w[i], self.dx[i], stream=stream)
             g = self.dx[i]
+        return self.dx[0]
+
+    def _fused_fits(self):
+        """The limits of cf_fc_head (checked again by the library)."""
+        d, m = self.dims, self.m
+        v = 8 if self.dtype == "bf16" else 4
+        g = d[1] // v
+        return (2 <= len(d) - 1 <= 4 and 1 <= m <= 8 and d[0] % 8 == 0 and d[1] % v == 0 and g in (8, 16, 32, 64)
+                and all(1 <= n <= 512 for n in d[1:]) and m * sum(d[1:]) <= 8192
+                and sum(d[i] * (d[i + 1] + 1) for i in range(1, len(d) - 1)) <= 16384)
+
+    def step(self, x, stream=None):
+        """Forward, loss and backward in one cf_fc_head call: fills y, dz, dx,
+        dw, db of every layer and the loss (dz of the last layer holds dL/dz,
+        not the loss gradient); returns the gradient of the head's input.
+        Falls back to forward() + backward() when the widths are outside the
+        fused call's limits."""
+        if not self.fused:
+            self.forward(x, stream)
+            return self.backward(stream)
+        assert x.is_contiguous() and x.numel() == self.m * self.dims[0] and x.dtype == self.w[0].dtype
+        self.x = x
+        B.cf_fc_head(self.m, self.dims, self.dtype, x, self.w, self.b, self.alpha, self.target, self.y, self.dz,
+                     self.dx, self.dw, self.db, self.loss, self.ws, stream=stream)
         return self.dx[0]
 
     def weight_bytes(self):

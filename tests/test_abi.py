@@ -255,3 +255,41 @@ def test_fc_and_loss_validation(L):
     expect(B.CF_ERR_ALIGNMENT, B.cf_mse_loss, 8, 3, "f32", x, z, ws, w + 8, 0)
     expect(B.CF_ERR_ALIAS, B.cf_mse_loss, 8, 3, "f32", x, z, x + 16, None, 0)
     expect(B.CF_ERR_ALIAS, B.cf_mse_loss, 8, 3, "f32", x, z, ws, z, 0)
+
+
+def test_fc_head_validation(L):
+    """cf_fc_head: the fused head's limits and argument checks reject before any launch."""
+    dims = [65536, 128, 64, 3]
+    need = B.cf_fc_head_workspace_size(8, dims)
+    assert need == B.cf_fc_fwd_workspace_size(8, 65536, 128) and need > 0
+    assert B.cf_fc_head_workspace_size(8, [65536]) == 0
+    assert B.cf_fc_head_workspace_size(8, [65536, 0, 3]) == 0
+    P = [A + k * 0x10000000 for k in range(32)]  # 256 MiB apart: no overlap
+    x, tgt, loss, ws = P[0], P[1], P[2], P[3]
+    w, b, y, dz, dx, dw, db = ([P[4 + 7 * i + j] for i in range(3)] for j in range(7))
+
+    def call(m=8, d=dims, dt="bf16", **kw):
+        a = dict(x=x, w=w, b=b, target=tgt, y=y, dz=dz, dx=dx, dw=dw, db=db, loss=loss, ws=ws)
+        a.update(kw)
+        B.cf_fc_head(m, d, dt, a["x"], a["w"], a["b"], 0.01, a["target"], a["y"], a["dz"], a["dx"], a["dw"],
+                     a["db"], a["loss"], a["ws"], need, 0)
+
+    expect(B.CF_ERR_UNSUPPORTED, lambda: call(m=9))
+    expect(B.CF_ERR_UNSUPPORTED, lambda: call(m=0))
+    expect(B.CF_ERR_UNSUPPORTED, lambda: call(d=[65536, 128]))  # one layer
+    expect(B.CF_ERR_UNSUPPORTED, lambda: call(d=[65536, 128, 64, 3, 3, 3]))  # five layers
+    expect(B.CF_ERR_UNSUPPORTED, lambda: call(d=[65532, 128, 64, 3]))  # first width not a multiple of 8
+    expect(B.CF_ERR_UNSUPPORTED, lambda: call(d=[65536, 96, 64, 3]))  # 96 / 8 bf16 lanes: not a power of two
+    expect(B.CF_ERR_UNSUPPORTED, lambda: call(d=[65536, 32, 64, 3]))  # four lanes per row: below eight
+    expect(B.CF_ERR_UNSUPPORTED, lambda: call(d=[65536, 128, 600, 3]))  # a later width above 512
+    expect(B.CF_ERR_UNSUPPORTED, lambda: call(d=[65536, 512, 512, 3]))  # later weights beyond LDS
+    expect(B.CF_ERR_INVALID_ARG, lambda: call(d=[65536, 128, 0, 3]))
+    expect(B.CF_ERR_INVALID_ARG, lambda: call(target=None))
+    expect(B.CF_ERR_INVALID_ARG, lambda: call(w=[w[0], None, w[2]]))
+    expect(B.CF_ERR_ALIGNMENT, lambda: call(x=x + 8))
+    expect(B.CF_ERR_ALIAS, lambda: call(y=[x + 1024, y[1], y[2]]))  # an output inside x
+    expect(B.CF_ERR_ALIAS, lambda: call(db=[db[0], dw[1] + 64, db[2]]))  # two outputs overlap
+    expect(B.CF_ERR_ALIAS, lambda: call(ws=w[0]))  # the workspace over an input
+    with pytest.raises(B.CfError) as e:
+        B.cf_fc_head(8, dims, "bf16", x, w, b, 0.01, tgt, y, dz, dx, dw, db, loss, ws, need - 16, 0)
+    assert e.value.status == B.CF_ERR_WORKSPACE

@@ -144,3 +144,94 @@ def test_head_chain(dt):
         assert maxabs_err(to_np(h.dx[i]), oracle.fc_bwd_data(to_np(h.dz[i]), wn[i])) <= TOL[dt], ("dx", i)
         g = to_np(h.dx[i])
     assert dfeat.data_ptr() == h.dx[0].data_ptr()
+
+
+def _head_setup(dt, m, dims, seed):
+    rng = np.random.default_rng(seed)
+    feat = dev(rng.standard_normal((m, dims[0]), dtype=np.float32), dt)
+    ws = [rng.standard_normal((dims[i], dims[i + 1])) * np.sqrt(2.0 / dims[i]) for i in range(len(dims) - 1)]
+    bs = [rng.normal(0, 0.1, dims[i + 1]) for i in range(len(dims) - 1)]
+    tgt = rng.uniform(0.2, 1.0, (m, dims[-1]))
+    h = FCHead(m, dims[0], dims[1:], dtype=dt, alpha=0.01)
+    h.set_params(ws, bs, tgt)
+    return h, feat, bs
+
+
+def _grad_of_loss(h, dt):
+    """dL/dy of the last layer as the one-call head forms it: 2 (y - t) / (m n)
+    in fp32, rounded once to the dtype."""
+    y = h.y[-1].float().cpu()
+    inv = np.float32(1.0 / (h.m * h.dims[-1]))
+    dp = (torch.tensor(2.0, dtype=torch.float32) * (y - h.target.cpu())) * torch.tensor(inv)
+    return to_np(dp.to(tdtype(dt)))
+
+
+HEAD_CASES = [(8, [65536, 128, 64, 3]), (1, [65536, 128, 64, 3]), (5, [4000, 64, 48, 16, 3]), (3, [1024, 256, 7])]
+
+
+@pytest.mark.parametrize("dt", DTYPES)
+@pytest.mark.parametrize("m,dims", HEAD_CASES)
+def test_head_one_call(dt, m, dims):
+    """cf_fc_head (four launches) against the oracle, teacher-forced per op
+    from the GPU's own intermediate tensors, as the per-layer chain test."""
+    h, feat, bs = _head_setup(dt, m, dims, 33 + m)
+    assert h.fused
+    dfeat = h.step(feat)
+    torch.cuda.synchronize()
+    L = len(dims) - 1
+    wn = [to_np(w) for w in h.w]
+    tn = h.target.cpu().double().numpy()
+    lref, _, acts = oracle.head_forward(to_np(feat), wn, bs, 0.01, tn)
+    for i in range(L):
+        assert maxabs_err(to_np(h.y[i]), acts[i]["y"]) <= TOL[dt], ("fwd", i)
+    assert abs(h.loss[0].item() - lref) <= TOL[dt] * abs(lref)
+    # the loss gradient: against the oracle's, and as rounded by the kernel for the teacher-forced steps
+    dp = _grad_of_loss(h, dt)
+    assert maxabs_err(dp, oracle.mse_loss(to_np(h.y[-1]), tn)[1]) <= TOL[dt]
+    g = dp
+    for i in range(L - 1, -1, -1):
+        dz, db = oracle.bias_lrelu_bwd(g, to_np(h.y[i]), 0.01)
+        assert maxabs_err(to_np(h.dz[i]), dz) <= TOL[dt], ("dz", i)
+        assert maxabs_err(to_np(h.db[i]), db) <= 1e-5, ("db", i)
+        xin = to_np(feat) if i == 0 else to_np(h.y[i - 1])
+        assert maxabs_err(to_np(h.dw[i]), oracle.fc_bwd_weight(xin, to_np(h.dz[i]))) <= 1e-5, ("dw", i)
+        assert maxabs_err(to_np(h.dx[i]), oracle.fc_bwd_data(to_np(h.dz[i]), wn[i])) <= TOL[dt], ("dx", i)
+        g = to_np(h.dx[i])
+    assert dfeat.data_ptr() == h.dx[0].data_ptr()
+
+
+@pytest.mark.parametrize("dt", DTYPES)
+def test_head_one_call_matches_per_layer_calls(dt):
+    """The first layer's y is bitwise the per-layer calls' (same split-K sums,
+    bias and leaky ReLU); its dW and dx are bitwise cf_fc_bwd_weight and
+    cf_fc_bwd_data on the one-call dz; the rest agrees to the dtype's
+    tolerance; two calls give the same bits."""
+    m, dims = 8, [65536, 128, 64, 3]
+    h, feat, _ = _head_setup(dt, m, dims, 7)
+    h.forward(feat)
+    h.backward()
+    torch.cuda.synchronize()
+    ref = {k: [t.clone() for t in getattr(h, k)] for k in ("y", "dz", "dx", "dw", "db")}
+    ref_loss = h.loss[0].item()
+    h.step(feat)
+    torch.cuda.synchronize()
+    one = {k: [t.clone() for t in getattr(h, k)] for k in ("y", "dz", "dx", "dw", "db")}
+    assert torch.equal(one["y"][0], ref["y"][0])
+    dw0 = torch.empty_like(h.dw[0])
+    dx0 = torch.empty_like(h.dx[0])
+    B.cf_fc_bwd_weight(m, dims[0], dims[1], dt, feat, one["dz"][0], dw0)
+    B.cf_fc_bwd_data(m, dims[0], dims[1], dt, one["dz"][0], h.w[0], dx0)
+    torch.cuda.synchronize()
+    assert torch.equal(one["dw"][0], dw0) and torch.equal(one["dx"][0], dx0)
+    for k in ("y", "dz", "dx"):
+        for i in range(3):
+            assert maxabs_err(to_np(one[k][i]), to_np(ref[k][i])) <= 2 * TOL[dt], (k, i)
+    for k in ("dw", "db"):
+        for i in range(3):
+            assert maxabs_err(to_np(one[k][i]), to_np(ref[k][i])) <= 2 * TOL[dt], (k, i)
+    assert abs(h.loss[0].item() - ref_loss) <= TOL[dt] * abs(ref_loss)
+    h.step(feat)
+    torch.cuda.synchronize()
+    for k in ("y", "dz", "dx", "dw", "db"):
+        for a, b in zip(one[k], getattr(h, k)):
+            assert torch.equal(a, b), k
