@@ -235,3 +235,19 @@ def test_head_one_call_matches_per_layer_calls(dt):
     for k in ("y", "dz", "dx", "dw", "db"):
         for a, b in zip(one[k], getattr(h, k)):
             assert torch.equal(a, b), k
+
+
+@pytest.mark.parametrize("dt", DTYPES)
+def test_head_step_outside_limits_runs_per_layer(dt):
+    """Widths outside cf_fc_head's limits (40 first-layer outputs: not a power
+    of two of vector lanes) make FCHead.step run the per-layer calls, with the
+    same results as forward() + backward()."""
+    m, dims = 3, [1000, 40, 3]
+    h, feat, _ = _head_setup(dt, m, dims, 5)
+    assert not h.fused
+    d1 = h.step(feat).clone()
+    l1 = h.loss[0].item()
+    h.forward(feat)
+    d2 = h.backward()
+    torch.cuda.synchronize()
+    assert torch.equal(d1, d2) and h.loss[0].item() == l1
